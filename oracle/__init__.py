@@ -1,0 +1,193 @@
+"""ctypes binding of the fp64 CPU oracle (``oracle/spc_oracle.c``).
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, the smoke check and the
+benchmark's CPU-baseline leg, never by the GPU library.  Arrays are numpy;
+logits may be float32, float64, or uint16 (raw bfloat16 bits).
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from .build import LIB, build
+
+_lib = None
+
+F32, BF16, F64 = 0, 1, 2
+CHOW, DIFF, OPT, ALWAYS, NEVER = 0, 1, 2, 3, 4
+FLAG_DRAFT_OUT_OF_RANGE, FLAG_EMPTY_RESIDUAL = 1, 2
+
+_P = ctypes.c_void_p
+_I32, _I64, _D = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+
+
+class RowStats(ctypes.Structure):
+    _fields_ = [("m", ctypes.c_double), ("lse", ctypes.c_double),
+                ("maxprob", ctypes.c_double), ("argmax", ctypes.c_int32)]
+
+
+def lib():
+    """Load the oracle library, compiling it first if it is not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            build()
+        L = ctypes.CDLL(LIB)
+        L.orc_softmax_row.argtypes = [_P, ctypes.c_int, _I64, _D, _P, ctypes.POINTER(RowStats)]
+        L.orc_softmax_row.restype = None
+        L.orc_tv.argtypes = [_P, _P, _I64]
+        L.orc_tv.restype = _D
+        L.orc_defer.argtypes = [ctypes.c_int, _D, _D, _D, _D, ctypes.POINTER(_D)]
+        L.orc_defer.restype = ctypes.c_int
+        L.orc_target.argtypes = [ctypes.c_int, _P, _P, _I64, _P]
+        L.orc_target.restype = None
+        L.orc_accept.argtypes = [_D, _D, _D, ctypes.POINTER(_D)]
+        L.orc_accept.restype = ctypes.c_int
+        L.orc_residual.argtypes = [_P, _P, _I64, _P]
+        L.orc_residual.restype = _D
+        L.orc_sample.argtypes = [_P, _I64, _D, ctypes.POINTER(_D)]
+        L.orc_sample.restype = _I32
+        L.orc_verify.argtypes = [_P, _P, ctypes.c_int, _P, _P, _I32, _I32, _I64, _P, _P, _P,
+                                 _P, _P, _P, _P, _P, _P, _P, _P, _P]
+        L.orc_verify.restype = ctypes.c_int
+        L.orc_greedy_verify.argtypes = [_P, _P, ctypes.c_int, _P, _I32, _I32, _I64, _P, _P,
+                                        _P, _P, _P, _P, _P, _P, _P]
+        L.orc_greedy_verify.restype = ctypes.c_int
+        L.orc_num_threads.argtypes = []
+        L.orc_num_threads.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _logits(a):
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.float32:
+        return a, F32
+    if a.dtype == np.float64:
+        return a, F64
+    if a.dtype in (np.uint16, np.int16):
+        return a.view(np.uint16), BF16
+    raise TypeError(f"unsupported logit dtype {a.dtype}")
+
+
+def _per_seq(x, B, dtype):
+    a = np.asarray(x, dtype=dtype)
+    if a.ndim == 0:
+        a = np.full(B, a, dtype=dtype)
+    assert a.shape == (B,)
+    return np.ascontiguousarray(a)
+
+
+def num_threads():
+    return lib().orc_num_threads()
+
+
+def softmax_row(z, T=1.0):
+    """(prob, m, lse, maxprob, argmax) of softmax(z / T) for one row."""
+    z, dt = _logits(z)
+    V = z.shape[-1]
+    prob = np.empty(V, np.float64)
+    st = RowStats()
+    lib().orc_softmax_row(_ptr(z), dt, V, float(T), _ptr(prob), ctypes.byref(st))
+    return prob, st.m, st.lse, st.maxprob, st.argmax
+
+
+def tv(p, q):
+    p = np.ascontiguousarray(p, np.float64)
+    q = np.ascontiguousarray(q, np.float64)
+    return lib().orc_tv(_ptr(p), _ptr(q), p.size)
+
+
+def defer(rule, alpha, maxq, maxp, tv_=0.0):
+    mg = _D()
+    d = lib().orc_defer(rule, float(alpha), float(maxq), float(maxp), float(tv_), ctypes.byref(mg))
+    return d, mg.value
+
+
+def target(delta, q, p):
+    q = np.ascontiguousarray(q, np.float64)
+    p = np.ascontiguousarray(p, np.float64)
+    pi = np.empty_like(q)
+    lib().orc_target(int(delta), _ptr(q), _ptr(p), q.size, _ptr(pi))
+    return pi
+
+
+def accept(pi_x, q_x, u):
+    mg = _D()
+    a = lib().orc_accept(float(pi_x), float(q_x), float(u), ctypes.byref(mg))
+    return a, mg.value
+
+
+def residual(pi, q):
+    pi = np.ascontiguousarray(pi, np.float64)
+    q = np.ascontiguousarray(q, np.float64)
+    w = np.empty_like(q)
+    W = lib().orc_residual(_ptr(pi), _ptr(q), q.size, _ptr(w))
+    return w, W
+
+
+def sample(w, u):
+    w = np.ascontiguousarray(w, np.float64)
+    mg = _D()
+    k = lib().orc_sample(_ptr(w), w.size, float(u), ctypes.byref(mg))
+    return k, mg.value
+
+
+def verify(q, p, draft, uniforms, rule, alpha, temperature):
+    """One verify step for B sequences.  q, p: [B, gamma+1, V]; draft: [B, gamma];
+    uniforms: [B, gamma+1]; rule/alpha/temperature: scalars or [B]."""
+    q, dt = _logits(q)
+    p, dt2 = _logits(p)
+    assert dt == dt2 and q.shape == p.shape and q.ndim == 3
+    B, G, V = q.shape
+    gamma = G - 1
+    draft = np.ascontiguousarray(draft, np.int32)
+    uniforms = np.ascontiguousarray(uniforms, np.float32)
+    assert draft.shape == (B, gamma) and uniforms.shape == (B, G)
+    rule = _per_seq(rule, B, np.int32)
+    alpha = _per_seq(alpha, B, np.float32)
+    temperature = _per_seq(temperature, B, np.float32)
+    out = dict(
+        accept_len=np.empty(B, np.int32), next_token=np.empty(B, np.int32),
+        defer=np.empty((B, G), np.uint8), row_stats=np.empty((B, G, 8), np.float64),
+        defer_margin=np.empty((B, G)), accept_margin=np.empty((B, gamma)),
+        sample_margin=np.empty(B), sample_norm=np.empty(B), flags=np.empty(B, np.int32))
+    rc = lib().orc_verify(
+        _ptr(q), _ptr(p), dt, _ptr(draft), _ptr(uniforms), B, gamma, V, _ptr(rule),
+        _ptr(alpha), _ptr(temperature), _ptr(out["accept_len"]), _ptr(out["next_token"]),
+        _ptr(out["defer"]), _ptr(out["row_stats"]), _ptr(out["defer_margin"]),
+        _ptr(out["accept_margin"]), _ptr(out["sample_margin"]), _ptr(out["sample_norm"]),
+        _ptr(out["flags"]))
+    if rc != 0:
+        raise ValueError("orc_verify rejected its arguments")
+    return out
+
+
+def greedy_verify(q, p, draft, rule, alpha):
+    """The temperature-0 step (Lemma 6) for B sequences."""
+    q, dt = _logits(q)
+    p, dt2 = _logits(p)
+    assert dt == dt2 and q.shape == p.shape and q.ndim == 3
+    B, G, V = q.shape
+    gamma = G - 1
+    draft = np.ascontiguousarray(draft, np.int32)
+    assert draft.shape == (B, gamma)
+    rule = _per_seq(rule, B, np.int32)
+    alpha = _per_seq(alpha, B, np.float32)
+    out = dict(
+        accept_len=np.empty(B, np.int32), next_token=np.empty(B, np.int32),
+        defer=np.empty((B, G), np.uint8), row_stats=np.empty((B, G, 8), np.float64),
+        argmax=np.empty((B, G, 2), np.int32), defer_margin=np.empty((B, G)),
+        flags=np.empty(B, np.int32))
+    rc = lib().orc_greedy_verify(
+        _ptr(q), _ptr(p), dt, _ptr(draft), B, gamma, V, _ptr(rule), _ptr(alpha),
+        _ptr(out["accept_len"]), _ptr(out["next_token"]), _ptr(out["defer"]),
+        _ptr(out["row_stats"]), _ptr(out["argmax"]), _ptr(out["defer_margin"]),
+        _ptr(out["flags"]))
+    if rc != 0:
+        raise ValueError("orc_greedy_verify rejected its arguments")
+    return out

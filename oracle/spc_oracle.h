@@ -1,0 +1,121 @@
+/*
+ * spc_oracle.h -- plain fp64 CPU oracle of one speculative-cascade verify step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This library exists so that tests, the smoke
+ * check and the benchmark's CPU-baseline leg can check the GPU library
+ * against an independent, slow, obviously correct implementation of the
+ * paper "Faster Cascades via Speculative Decoding" (Narasimhan et al.,
+ * arXiv 2405.19261).  No product code may link or call it, and it shares no
+ * code, header or constant with the GPU library.
+ *
+ * Everything is computed in IEEE double precision with sequential loops in
+ * vocabulary-index order.  Inputs of type float32 or bfloat16 widen to double
+ * exactly, so the oracle sees exactly the values the GPU reads.
+ *
+ * Layouts (row-major, host memory, caller-owned):
+ *   logits   [B][gamma+1][V]  dtype ORC_F32, ORC_BF16 (raw uint16 bits) or ORC_F64
+ *   draft    [B][gamma]       int32
+ *   uniforms [B][gamma+1]     float32 in [0,1): u[b][j<gamma] drive the
+ *                             accept draws, u[b][gamma] the one replacement or
+ *                             bonus sample
+ *   rule/alpha/temperature    one value per sequence, [B]
+ */
+#ifndef SPC_ORACLE_H
+#define SPC_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { ORC_F32 = 0, ORC_BF16 = 1, ORC_F64 = 2 };
+
+/* Largest block size gamma the oracle accepts. */
+#define ORC_MAX_GAMMA 64
+
+/* Deferral rules of Table 1 (Section 4.2 and eq. (2), (5), (11)), plus the two
+ * constant rules: ALWAYS (delta = 1: standard speculative decoding, Alg. 1)
+ * and NEVER (delta = 0: the drafter alone). */
+enum { ORC_CHOW = 0, ORC_DIFF = 1, ORC_OPT = 2, ORC_ALWAYS = 3, ORC_NEVER = 4 };
+
+/* Per-sequence flags reported by orc_verify / orc_greedy_verify. */
+enum {
+  ORC_FLAG_DRAFT_OUT_OF_RANGE = 1, /* a draft token outside [0,V) was rejected */
+  ORC_FLAG_EMPTY_RESIDUAL = 2      /* rejection with zero residual mass: sampled p instead */
+};
+
+/* Statistics of one tempered softmax row (Section 2 notation; temperature
+ * read as q = softmax(z / T)). */
+typedef struct {
+  double m;       /* max_v z_v / T                                */
+  double lse;     /* log sum_v exp(z_v / T)                       */
+  double maxprob; /* max_v softmax(z/T)_v                         */
+  int32_t argmax; /* smallest v with z_v == max z (raw logits)    */
+} orc_row_stats;
+
+/* softmax(z / T) of one row of V logits; prob may be NULL.  T > 0. */
+void orc_softmax_row(const void* z, int dtype, int64_t V, double T, double* prob,
+                     orc_row_stats* st);
+
+/* D_TV(p, q) = sum_v max(0, p_v - q_v)  (Lemma 3). */
+double orc_tv(const double* p, const double* q, int64_t V);
+
+/* delta(q, p) of Table 1 for one position; *margin = |lhs - rhs| of the
+ * defining inequality (infinity for ALWAYS / NEVER). Returns 0 or 1, or -1 for
+ * an unknown rule. */
+int orc_defer(int rule, double alpha, double maxq, double maxp, double tv, double* margin);
+
+/* pi = (1 - delta) q + delta p   (eq. (6)). */
+void orc_target(int delta, const double* q, const double* p, int64_t V, double* pi);
+
+/* Accept draw of Alg. 4: a = 1(u < min(1, pi_x / q_x)); a token with
+ * q_x <= pi_x is always kept (Section 4.1).  *margin = |u - min(1, ratio)|. */
+int orc_accept(double pi_x, double q_x, double u, double* margin);
+
+/* Unnormalised residual w = max(0, pi - q) (Alg. 4); returns sum_v w_v. */
+double orc_residual(const double* pi, const double* q, int64_t V, double* w);
+
+/* Inverse-CDF draw from norm(w): the smallest k with C_k / W > u, where
+ * C_k = sum_{v<=k} w_v in index order and W = C_{V-1}.  Returns -1 when W is
+ * not positive.  *margin = min(C_k/W - u, u - C_{k-1}/W). */
+int32_t orc_sample(const double* w, int64_t V, double u, double* margin);
+
+/* One GenSpecSample (Alg. 4) with the target T_delta (Alg. 5) for each of B
+ * sequences.  rule/alpha/temperature are per sequence.  Outputs:
+ *   accept_len [B]            j* in [0, gamma]
+ *   next_token [B]            the token emitted at position j*
+ *   defer      [B][gamma+1]   delta at every position
+ * Optional outputs (may be NULL):
+ *   row_stats     [B][gamma+1][8] = {m_q, lse_q, maxprob_q, m_p, lse_p, maxprob_p, tv, 0}
+ *   defer_margin  [B][gamma+1]
+ *   accept_margin [B][gamma]      (infinity where the draw is exact)
+ *   sample_margin [B]
+ *   sample_norm   [B]             W = mass of the distribution sampled at j*
+ *   flags         [B]             ORC_FLAG_*
+ * Returns 0, or -1 on an argument error.  Sequences run in parallel (OpenMP). */
+int orc_verify(const void* q_logits, const void* p_logits, int dtype, const int32_t* draft,
+               const float* uniforms, int32_t B, int32_t gamma, int64_t V,
+               const int32_t* rule, const float* alpha, const float* temperature,
+               int32_t* accept_len, int32_t* next_token, uint8_t* defer, double* row_stats,
+               double* defer_margin, double* accept_margin, double* sample_margin,
+               double* sample_norm, int32_t* flags);
+
+/* The greedy (temperature 0) step of Lemma 6: one-hot q~ and p~ at the
+ * argmaxes of the raw logits, max-probabilities from the temperature-1
+ * softmax, D_TV(p~, q~) = 1(argmax q != argmax p).  No uniforms.  row_stats
+ * holds the temperature-1 statistics and the one-hot TV. */
+int orc_greedy_verify(const void* q_logits, const void* p_logits, int dtype,
+                      const int32_t* draft, int32_t B, int32_t gamma, int64_t V,
+                      const int32_t* rule, const float* alpha, int32_t* accept_len,
+                      int32_t* next_token, uint8_t* defer, double* row_stats,
+                      int32_t* argmax_qp, double* defer_margin, int32_t* flags);
+
+/* Number of OpenMP threads orc_verify uses. */
+int orc_num_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif
