@@ -1,0 +1,189 @@
+/*
+ * speccascade.h -- C interface of libspeccascade, the verify/defer step of
+ * speculative cascades on AMD Instinct MI355X (gfx950).
+ *
+ * One call performs, for a block of gamma drafted positions in each of B
+ * sequences, the verification half of GenSpecSample (Alg. 4) with the
+ * cascade target T_delta (eq. (6), Alg. 5) of "Faster Cascades via
+ * Speculative Decoding" (Narasimhan et al., arXiv 2405.19261):
+ *
+ *   q_{t+j} = softmax(z^q_{t+j} / T),  p_{t+j} = softmax(z^p_{t+j} / T)   (j = 0..gamma)
+ *   delta_j  by the deferral rule of Table 1 (Chow eq. (2), Diff eq. (5),
+ *            OPT eq. (11) with D_TV of Lemma 3)
+ *   pi_j     = (1 - delta_j) q_j + delta_j p_j                            (eq. (6))
+ *   a_j      = 1(u_j < min(1, pi_j(x_j) / q_j(x_j))), j < gamma; a_gamma = 0
+ *   j*       = min{ j : a_j = 0 }
+ *   token    ~ norm(max(0, pi_{j*} - q_{j*}))  if j* < gamma,  else ~ pi_gamma
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers are DEVICE pointers on the current HIP device, allocated and
+ *   owned by the caller.  The library reads inputs, writes outputs, and keeps
+ *   no reference to either after the call returns.
+ * - Work is enqueued on `stream` (NULL = the default stream) and is
+ *   asynchronous: outputs are valid once the caller synchronises the stream.
+ *   No call synchronises the host with the device.
+ * - Logit tensors are row-major [B][gamma+1][V] (row stride V elements), in
+ *   float32 or bfloat16.  Row gamma of the drafter tensor is the drafter's
+ *   distribution at the bonus position t+gamma, which the extra-token target
+ *   pi_{t+gamma} of Alg. 4 needs.
+ * - Every argument is checked before any HIP call; a failed check returns
+ *   its status and enqueues nothing.  spc_last_error() then describes it.
+ * - Preconditions that are NOT checked: logits are finite or -inf, with at
+ *   least one finite entry per row; uniforms lie in [0, 1).
+ * - Defined behaviour: a draft token outside [0, V) rejects its position
+ *   (no out-of-bounds read).  out_defer_mask is filled for all gamma+1
+ *   positions, including those past j*.  Sequence b emits
+ *   draft_tokens[b][0 .. accept_len[b]-1] followed by next_token[b].
+ * - The internal workspace (used when no caller workspace is passed) is one
+ *   buffer per device: calls that use it must not overlap in time on one
+ *   device (issue them on one stream).  Calls with distinct caller
+ *   workspaces may run concurrently.
+ */
+#ifndef SPECCASCADE_H
+#define SPECCASCADE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { SPC_F32 = 0, SPC_BF16 = 1 } spc_dtype;
+
+/* Deferral rules of Table 1 plus two constant rules. */
+typedef enum {
+  SPC_RULE_CHOW = 0,   /* delta = 1(max_v q(v) < 1 - alpha)                 eq. (2)  */
+  SPC_RULE_DIFF = 1,   /* delta = 1(max_v q(v) < max_v p(v) - alpha)        eq. (5)  */
+  SPC_RULE_OPT = 2,    /* delta = 1(max_v q(v) < max_v p(v) - alpha D_TV)   eq. (11) */
+  SPC_RULE_ALWAYS = 3, /* delta = 1: standard speculative decoding (Alg. 1)          */
+  SPC_RULE_NEVER = 4   /* delta = 0: the drafter's own distribution                  */
+} spc_rule;
+
+typedef enum {
+  SPC_OK = 0,
+  SPC_E_NULL = -1,      /* a required pointer is NULL                                 */
+  SPC_E_SHAPE = -2,     /* B < 1, gamma < 1, gamma > SPC_MAX_GAMMA, V < 2, or
+                           B*(gamma+1)*V does not fit the index range                 */
+  SPC_E_RULE = -3,      /* a rule id outside spc_rule                                 */
+  SPC_E_PARAM = -4,     /* alpha not finite, temperature not > 0 and finite,
+                           or an unknown dtype                                        */
+  SPC_E_ALIGN = -5,     /* a logit base pointer not 16-byte aligned                   */
+  SPC_E_WORKSPACE = -6, /* caller workspace too small or misaligned                   */
+  SPC_E_HIP = -7        /* a HIP call failed; spc_last_error() holds its message      */
+} spc_status;
+
+/* Largest block size: the first-rejection search runs in one 64-lane wavefront. */
+#define SPC_MAX_GAMMA 63
+
+/*
+ * spc_verify -- one verify step at temperature `temperature` > 0 with the same
+ * rule, alpha and temperature for all B sequences.
+ *
+ *   q_logits, p_logits  [B][gamma+1][V] drafter / verifier logits, `dtype`
+ *   draft_tokens        [B][gamma] int32: x_t .. x_{t+gamma-1}
+ *   uniforms            [B][gamma+1] float32 in [0,1): u[b][j], j < gamma, is
+ *                       the draw of a_j (Alg. 4); u[b][gamma] drives the one
+ *                       replacement or extra-token sample (inverse CDF in
+ *                       vocabulary order: the smallest k whose cumulative mass
+ *                       exceeds u times the total)
+ *   rule, alpha         deferral rule (spc_rule) and its parameter
+ *   out_accept_len      [B] int32: j* in [0, gamma]
+ *   out_next_token      [B] int32: the token emitted at position t + j*
+ *   out_defer_mask      [B][gamma+1] uint8: delta_j at every position
+ */
+spc_status spc_verify(const void* q_logits, const void* p_logits, spc_dtype dtype,
+                      const int32_t* draft_tokens, const float* uniforms, int32_t B,
+                      int32_t gamma, int32_t V, int32_t rule, float alpha, float temperature,
+                      int32_t* out_accept_len, int32_t* out_next_token,
+                      uint8_t* out_defer_mask, hipStream_t stream);
+
+/*
+ * spc_greedy_verify -- the temperature-0 step (Lemma 6, greedy case).
+ * q~ and p~ are one-hot at the argmax of the raw logits (lowest index on a
+ * tie); the rule's max-probabilities come from the temperature-1 softmax and
+ * D_TV(p~, q~) = 1(argmax q != argmax p).  A draft is kept exactly when it
+ * equals the argmax of pi~_j = (1 - delta_j) q~_j + delta_j p~_j, and the
+ * emitted token is that argmax at position j*.  No uniforms are used; the
+ * result is a deterministic function of the inputs.
+ */
+spc_status spc_greedy_verify(const void* q_logits, const void* p_logits, spc_dtype dtype,
+                             const int32_t* draft_tokens, int32_t B, int32_t gamma, int32_t V,
+                             int32_t rule, float alpha, int32_t* out_accept_len,
+                             int32_t* out_next_token, uint8_t* out_defer_mask,
+                             hipStream_t stream);
+
+/*
+ * Extended arguments.  Every field may be NULL / 0.
+ *   rule_per_seq, alpha_per_seq, temp_per_seq  [B] device arrays overriding
+ *       the scalar rule / alpha / temperature per sequence.  A per-sequence
+ *       temperature of 0 selects the greedy step for that sequence.  Values
+ *       are checked by the kernels: an invalid one makes that sequence emit
+ *       accept_len = -1 and next_token = -1.
+ *   out_row_stats  [B][gamma+1][8] float32: {m_q, lse_q, maxprob_q, m_p,
+ *       lse_p, maxprob_p, tv, 0} with m = max_v z_v / T and lse = log sum_v
+ *       exp(z_v / T); greedy rows hold the temperature-1 values and the
+ *       one-hot TV.  tv is computed for OPT rows only (0 elsewhere).
+ *   out_argmax     [B][gamma+1][2] int32: argmax of raw q and p logits
+ *       (filled for greedy rows; -1 elsewhere).
+ *   out_sample_norm [B] float32: the total mass W of the distribution
+ *       sampled at j* (for a replacement, sum_v max(0, p - q) = D_TV).
+ *   workspace, workspace_bytes  caller-owned device buffer of at least
+ *       spc_workspace_bytes(B, gamma, V, dtype) bytes, 256-byte aligned,
+ *       whose first spc_workspace_zero_bytes(B, gamma, V, dtype) bytes are
+ *       zero before its first use (the kernels leave them zero again).
+ *       NULL selects the internal per-device workspace, allocated on first
+ *       use and grown as needed.
+ *   ev_hot_begin, ev_hot_end  optional HIP events recorded on `stream`
+ *       immediately before and after the vocabulary-streaming statistics
+ *       kernel, for timing it alone.
+ */
+typedef struct {
+  const int32_t* rule_per_seq;
+  const float* alpha_per_seq;
+  const float* temp_per_seq;
+  float* out_row_stats;
+  int32_t* out_argmax;
+  float* out_sample_norm;
+  void* workspace;
+  size_t workspace_bytes;
+  hipEvent_t ev_hot_begin;
+  hipEvent_t ev_hot_end;
+} spc_verify_ex_args;
+
+/* spc_verify with extended arguments; `ex` may be NULL.  `temperature`
+ * applies where temp_per_seq is NULL and must then be > 0 (use
+ * spc_greedy_verify for a batch-wide temperature 0). */
+spc_status spc_verify_ex(const void* q_logits, const void* p_logits, spc_dtype dtype,
+                         const int32_t* draft_tokens, const float* uniforms, int32_t B,
+                         int32_t gamma, int32_t V, int32_t rule, float alpha, float temperature,
+                         int32_t* out_accept_len, int32_t* out_next_token,
+                         uint8_t* out_defer_mask, const spc_verify_ex_args* ex,
+                         hipStream_t stream);
+
+/* Bytes of device workspace one call of this shape needs. */
+size_t spc_workspace_bytes(int32_t B, int32_t gamma, int32_t V, spc_dtype dtype);
+
+/* Leading bytes of a workspace that must be zero before its first use
+ * (completion counters at fixed offsets: the same for every shape, so one
+ * zeroed workspace serves calls of any shape it is large enough for). */
+size_t spc_workspace_zero_bytes(int32_t B, int32_t gamma, int32_t V, spc_dtype dtype);
+
+/* Thread-local description of the last non-OK status ("" if none). */
+const char* spc_last_error(void);
+
+/* Frees the internal workspace of every device.  Not safe while a call that
+ * uses it may still be running: synchronise first. */
+void spc_release(void);
+
+/* Library version string. */
+const char* spc_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPECCASCADE_H */

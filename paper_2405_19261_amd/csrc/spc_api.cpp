@@ -1,0 +1,256 @@
+// spc_api.cpp -- the C interface of libspeccascade (declared in
+// include/speccascade.h): argument checks, workspace, kernel dispatch.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <map>
+#include <mutex>
+#include <string>
+
+#include "spc_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+spc_status fail(spc_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct DevWorkspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+std::mutex g_ws_mu;
+std::map<int, DevWorkspace> g_ws;
+
+// Rows (gridDim.y of the statistics kernels) are capped by the launch limit.
+constexpr int64_t kMaxRows = 65535;
+
+bool vec_path(int dtype, int64_t V) {
+  const int64_t eb = dtype == SPC_BF16 ? 2 : 4;
+  return (V * eb) % 16 == 0;  // every row starts on a 16-byte boundary
+}
+
+}  // namespace
+
+namespace spc {
+
+WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
+  // The completion counters sit at fixed offsets sized for the largest shape
+  // the interface accepts, so a workspace reused across shapes never has one
+  // call's data overlap another call's counters; they stay zero between calls.
+  const int64_t R = B * (gamma + 1);
+  const int64_t K = (V + tile_elems(dtype, vec) - 1) / tile_elems(dtype, vec);
+  const size_t cap = 4 * (size_t)(kMaxRows + 1);
+  WsLayout L;
+  L.row_cnt = 0;
+  L.seq_cnt = cap;
+  L.tv_row_cnt = 2 * cap;
+  L.tv_seq_cnt = 3 * cap;
+  L.samp_cnt = 4 * cap;
+  size_t o = align_up(5 * cap, 256);
+  L.zero_end = o;
+  L.tiles = o; o = align_up(o + sizeof(TilePart) * R * K, 256);
+  L.tvpart = o; o = align_up(o + sizeof(double) * R * K, 256);
+  L.masses = o; o = align_up(o + sizeof(double) * B * K, 256);
+  L.rows = o; o = align_up(o + sizeof(RowStat) * R, 256);
+  L.seqs = o; o = align_up(o + sizeof(SeqState) * B, 256);
+  L.total = o;
+  return L;
+}
+
+}  // namespace spc
+
+namespace {
+
+spc_status check_shape(int32_t B, int32_t gamma, int32_t V) {
+  if (B < 1 || gamma < 1 || gamma > SPC_MAX_GAMMA || V < 2)
+    return fail(SPC_E_SHAPE, "bad shape B=%d gamma=%d V=%d (need B>=1, 1<=gamma<=%d, V>=2)", B,
+                gamma, V, SPC_MAX_GAMMA);
+  const int64_t R = (int64_t)B * (gamma + 1);
+  if (R > kMaxRows)
+    return fail(SPC_E_SHAPE, "B*(gamma+1)=%lld exceeds %lld rows", (long long)R,
+                (long long)kMaxRows);
+  return SPC_OK;
+}
+
+spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int32_t* draft,
+                       const float* uniforms, int32_t B, int32_t gamma, int32_t V, int32_t rule,
+                       float alpha, float temperature, bool force_greedy, int32_t* out_accept,
+                       int32_t* out_token, uint8_t* out_defer, const spc_verify_ex_args* ex,
+                       hipStream_t stream) {
+  g_err.clear();
+  if (!q || !p || !draft || !out_accept || !out_token || !out_defer)
+    return fail(SPC_E_NULL, "a required pointer is NULL");
+  if (!force_greedy && !uniforms) return fail(SPC_E_NULL, "uniforms is NULL");
+  spc_status st = check_shape(B, gamma, V);
+  if (st != SPC_OK) return st;
+  if (dtype != SPC_F32 && dtype != SPC_BF16) return fail(SPC_E_PARAM, "unknown dtype %d", dtype);
+  const bool per_rule = ex && ex->rule_per_seq;
+  const bool per_alpha = ex && ex->alpha_per_seq;
+  const bool per_temp = ex && ex->temp_per_seq;
+  if (!per_rule && (rule < SPC_RULE_CHOW || rule > SPC_RULE_NEVER))
+    return fail(SPC_E_RULE, "unknown rule %d", rule);
+  if (!per_alpha && !isfinite(alpha)) return fail(SPC_E_PARAM, "alpha is not finite");
+  if (!force_greedy && !per_temp && !(isfinite(temperature) && temperature >= 1e-20f))
+    return fail(SPC_E_PARAM, "temperature must be finite and >= 1e-20 (got %g)",
+                (double)temperature);
+  if (((uintptr_t)q | (uintptr_t)p) % 16 != 0)
+    return fail(SPC_E_ALIGN, "logit base pointers must be 16-byte aligned");
+
+  const bool vec = vec_path(dtype, V);
+  const spc::WsLayout L = spc::ws_layout(B, gamma, V, dtype, vec);
+  char* ws = nullptr;
+  if (ex && ex->workspace) {
+    if (ex->workspace_bytes < L.total || ((uintptr_t)ex->workspace % 256) != 0)
+      return fail(SPC_E_WORKSPACE, "workspace of %zu bytes (need %zu, 256-byte aligned)",
+                  ex->workspace_bytes, L.total);
+    ws = static_cast<char*>(ex->workspace);
+  } else {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(SPC_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    DevWorkspace& w = g_ws[dev];
+    if (w.bytes < L.total) {
+      // growing: the old buffer may still be in use by work on `stream`
+      if (w.ptr) {
+        e = hipStreamSynchronize(stream);
+        if (e == hipSuccess) e = hipFree(w.ptr);
+        w.ptr = nullptr;
+        w.bytes = 0;
+        if (e != hipSuccess) return fail(SPC_E_HIP, "workspace release: %s", hipGetErrorString(e));
+      }
+      const size_t want = L.total + L.total / 4;  // headroom for nearby shapes
+      e = hipMalloc(&w.ptr, want);
+      if (e != hipSuccess) {
+        w.ptr = nullptr;
+        return fail(SPC_E_HIP, "hipMalloc(%zu): %s", want, hipGetErrorString(e));
+      }
+      // zero counters, ordered before this call's kernels on the same stream;
+      // the kernels leave them zero
+      e = hipMemsetAsync(w.ptr, 0, L.zero_end, stream);
+      if (e != hipSuccess) {
+        (void)hipFree(w.ptr);
+        w.ptr = nullptr;
+        return fail(SPC_E_HIP, "hipMemsetAsync: %s", hipGetErrorString(e));
+      }
+      w.bytes = want;
+    }
+    ws = static_cast<char*>(w.ptr);
+  }
+
+  spc::Params P{};
+  P.q = q;
+  P.p = p;
+  P.draft = draft;
+  P.uniforms = uniforms;
+  P.B = B;
+  P.gamma = gamma;
+  P.V = V;
+  P.K = (int32_t)((V + spc::tile_elems(dtype, vec) - 1) / spc::tile_elems(dtype, vec));
+  P.rule = rule;
+  P.alpha = alpha;
+  P.temp = force_greedy ? 0.0f : temperature;
+  P.force_greedy = force_greedy ? 1 : 0;
+  P.rule_ps = per_rule ? ex->rule_per_seq : nullptr;
+  P.alpha_ps = per_alpha ? ex->alpha_per_seq : nullptr;
+  P.temp_ps = (per_temp && !force_greedy) ? ex->temp_per_seq : nullptr;
+  P.out_accept = out_accept;
+  P.out_token = out_token;
+  P.out_defer = out_defer;
+  P.out_stats = ex ? ex->out_row_stats : nullptr;
+  P.out_argmax = ex ? ex->out_argmax : nullptr;
+  P.out_norm = ex ? ex->out_sample_norm : nullptr;
+  P.row_cnt = reinterpret_cast<uint32_t*>(ws + L.row_cnt);
+  P.seq_cnt = reinterpret_cast<uint32_t*>(ws + L.seq_cnt);
+  P.tv_row_cnt = reinterpret_cast<uint32_t*>(ws + L.tv_row_cnt);
+  P.tv_seq_cnt = reinterpret_cast<uint32_t*>(ws + L.tv_seq_cnt);
+  P.samp_cnt = reinterpret_cast<uint32_t*>(ws + L.samp_cnt);
+  P.tiles = reinterpret_cast<spc::TilePart*>(ws + L.tiles);
+  P.tvpart = reinterpret_cast<double*>(ws + L.tvpart);
+  P.masses = reinterpret_cast<double*>(ws + L.masses);
+  P.rows = reinterpret_cast<spc::RowStat*>(ws + L.rows);
+  P.seqs = reinterpret_cast<spc::SeqState*>(ws + L.seqs);
+
+  // sequences at temperature > 0 may exist unless the whole batch is greedy;
+  // OPT at temperature > 0 needs the TV pass
+  const bool need_sample = !force_greedy && (per_temp || temperature > 0.0f);
+  const bool need_tv = need_sample && (per_rule || rule == SPC_RULE_OPT);
+  hipError_t e = spc::launch_verify(P, dtype, vec, need_tv, need_sample,
+                                    ex ? ex->ev_hot_begin : nullptr,
+                                    ex ? ex->ev_hot_end : nullptr, stream);
+  if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
+  return SPC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+spc_status spc_verify(const void* q_logits, const void* p_logits, spc_dtype dtype,
+                      const int32_t* draft_tokens, const float* uniforms, int32_t B,
+                      int32_t gamma, int32_t V, int32_t rule, float alpha, float temperature,
+                      int32_t* out_accept_len, int32_t* out_next_token,
+                      uint8_t* out_defer_mask, hipStream_t stream) {
+  return verify_impl(q_logits, p_logits, dtype, draft_tokens, uniforms, B, gamma, V, rule, alpha,
+                     temperature, false, out_accept_len, out_next_token, out_defer_mask,
+                     nullptr, stream);
+}
+
+spc_status spc_greedy_verify(const void* q_logits, const void* p_logits, spc_dtype dtype,
+                             const int32_t* draft_tokens, int32_t B, int32_t gamma, int32_t V,
+                             int32_t rule, float alpha, int32_t* out_accept_len,
+                             int32_t* out_next_token, uint8_t* out_defer_mask,
+                             hipStream_t stream) {
+  return verify_impl(q_logits, p_logits, dtype, draft_tokens, nullptr, B, gamma, V, rule, alpha,
+                     0.0f, true, out_accept_len, out_next_token, out_defer_mask, nullptr, stream);
+}
+
+spc_status spc_verify_ex(const void* q_logits, const void* p_logits, spc_dtype dtype,
+                         const int32_t* draft_tokens, const float* uniforms, int32_t B,
+                         int32_t gamma, int32_t V, int32_t rule, float alpha, float temperature,
+                         int32_t* out_accept_len, int32_t* out_next_token,
+                         uint8_t* out_defer_mask, const spc_verify_ex_args* ex,
+                         hipStream_t stream) {
+  return verify_impl(q_logits, p_logits, dtype, draft_tokens, uniforms, B, gamma, V, rule, alpha,
+                     temperature, false, out_accept_len, out_next_token, out_defer_mask, ex,
+                     stream);
+}
+
+size_t spc_workspace_bytes(int32_t B, int32_t gamma, int32_t V, spc_dtype dtype) {
+  if (check_shape(B, gamma, V) != SPC_OK || (dtype != SPC_F32 && dtype != SPC_BF16)) return 0;
+  return spc::ws_layout(B, gamma, V, dtype, vec_path(dtype, V)).total;
+}
+
+size_t spc_workspace_zero_bytes(int32_t B, int32_t gamma, int32_t V, spc_dtype dtype) {
+  if (check_shape(B, gamma, V) != SPC_OK || (dtype != SPC_F32 && dtype != SPC_BF16)) return 0;
+  return spc::ws_layout(B, gamma, V, dtype, vec_path(dtype, V)).zero_end;
+}
+
+const char* spc_last_error(void) { return g_err.c_str(); }
+
+void spc_release(void) {
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  int cur = 0;
+  if (hipGetDevice(&cur) != hipSuccess) cur = 0;
+  for (auto& kv : g_ws) {
+    if (kv.second.ptr && hipSetDevice(kv.first) == hipSuccess) (void)hipFree(kv.second.ptr);
+  }
+  g_ws.clear();
+  (void)hipSetDevice(cur);
+}
+
+const char* spc_version(void) { return "libspeccascade 0.1 (gfx950)"; }
+
+}  // extern "C"

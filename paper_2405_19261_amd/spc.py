@@ -1,0 +1,196 @@
+"""Python binding of libspeccascade (the C interface in include/speccascade.h).
+
+Argument marshalling only: every step of the verify path runs in the gfx950
+kernels of ``libspeccascade.so``.  Functions carry the C names; tensors are
+torch tensors on the current HIP device (PyTorch supplies device memory and
+streams, nothing else).  A missing or unloadable library raises -- there is no
+fallback implementation.
+"""
+import ctypes
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspeccascade.so")
+
+SPC_F32, SPC_BF16 = 0, 1
+SPC_RULE_CHOW, SPC_RULE_DIFF, SPC_RULE_OPT, SPC_RULE_ALWAYS, SPC_RULE_NEVER = range(5)
+SPC_MAX_GAMMA = 63
+STATUS = {0: "SPC_OK", -1: "SPC_E_NULL", -2: "SPC_E_SHAPE", -3: "SPC_E_RULE",
+          -4: "SPC_E_PARAM", -5: "SPC_E_ALIGN", -6: "SPC_E_WORKSPACE", -7: "SPC_E_HIP"}
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+
+
+class ExArgs(ctypes.Structure):
+    """spc_verify_ex_args."""
+    _fields_ = [("rule_per_seq", _P), ("alpha_per_seq", _P), ("temp_per_seq", _P),
+                ("out_row_stats", _P), ("out_argmax", _P), ("out_sample_norm", _P),
+                ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
+                ("ev_hot_begin", _P), ("ev_hot_end", _P)]
+
+
+class SpcError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """The loaded shared library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run `python -m "
+                               "paper_2405_19261_amd.build` (or __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        common = [_P, _P, ctypes.c_int]
+        L.spc_verify.argtypes = common + [_P, _P, _I32, _I32, _I32, _I32, ctypes.c_float,
+                                          ctypes.c_float, _P, _P, _P, _P]
+        L.spc_verify.restype = ctypes.c_int
+        L.spc_greedy_verify.argtypes = common + [_P, _I32, _I32, _I32, _I32, ctypes.c_float,
+                                                 _P, _P, _P, _P]
+        L.spc_greedy_verify.restype = ctypes.c_int
+        L.spc_verify_ex.argtypes = common + [_P, _P, _I32, _I32, _I32, _I32, ctypes.c_float,
+                                             ctypes.c_float, _P, _P, _P,
+                                             ctypes.POINTER(ExArgs), _P]
+        L.spc_verify_ex.restype = ctypes.c_int
+        L.spc_workspace_bytes.argtypes = [_I32, _I32, _I32, ctypes.c_int]
+        L.spc_workspace_bytes.restype = ctypes.c_size_t
+        L.spc_workspace_zero_bytes.argtypes = [_I32, _I32, _I32, ctypes.c_int]
+        L.spc_workspace_zero_bytes.restype = ctypes.c_size_t
+        L.spc_last_error.argtypes = []
+        L.spc_last_error.restype = ctypes.c_char_p
+        L.spc_release.argtypes = []
+        L.spc_release.restype = None
+        L.spc_version.argtypes = []
+        L.spc_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _dtype_code(t):
+    if t.dtype == torch.float32:
+        return SPC_F32
+    if t.dtype == torch.bfloat16:
+        return SPC_BF16
+    raise TypeError(f"logits must be float32 or bfloat16, not {t.dtype}")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _event(ev):
+    """A raw hipEvent_t: an int handle, or an object with a ``handle`` or
+    ``cuda_event`` attribute."""
+    if ev is None:
+        return None
+    for attr in ("handle", "cuda_event"):
+        if hasattr(ev, attr):
+            ev = getattr(ev, attr)
+            break
+    if not ev:
+        raise ValueError("event is not created")
+    return ctypes.c_void_p(int(ev))
+
+
+def _check(status):
+    if status != 0:
+        raise SpcError(status, lib().spc_last_error().decode())
+
+
+def _outputs(q, B, gamma, out):
+    if out is not None:
+        return out
+    dev = q.device
+    return (torch.empty(B, dtype=torch.int32, device=dev),
+            torch.empty(B, dtype=torch.int32, device=dev),
+            torch.empty((B, gamma + 1), dtype=torch.uint8, device=dev))
+
+
+def _shape(q, p, draft):
+    if q.dim() != 3 or q.shape != p.shape or q.dtype != p.dtype:
+        raise ValueError("q and p must both be [B, gamma+1, V] of one dtype")
+    if not (q.is_contiguous() and p.is_contiguous() and draft.is_contiguous()):
+        raise ValueError("inputs must be contiguous")
+    B, g1, V = q.shape
+    return B, g1 - 1, V
+
+
+def spc_verify(q, p, draft, uniforms, rule, alpha, temperature, out=None, stream=None):
+    """One verify step; returns (accept_len [B], next_token [B], defer_mask [B, gamma+1])."""
+    B, gamma, V = _shape(q, p, draft)
+    acc, tok, dm = _outputs(q, B, gamma, out)
+    _check(lib().spc_verify(_ptr(q), _ptr(p), _dtype_code(q), _ptr(draft), _ptr(uniforms), B,
+                            gamma, V, int(rule), float(alpha), float(temperature), _ptr(acc),
+                            _ptr(tok), _ptr(dm), _stream(stream)))
+    return acc, tok, dm
+
+
+def spc_greedy_verify(q, p, draft, rule, alpha, out=None, stream=None):
+    """The temperature-0 step; returns (accept_len, next_token, defer_mask)."""
+    B, gamma, V = _shape(q, p, draft)
+    acc, tok, dm = _outputs(q, B, gamma, out)
+    _check(lib().spc_greedy_verify(_ptr(q), _ptr(p), _dtype_code(q), _ptr(draft), B, gamma, V,
+                                   int(rule), float(alpha), _ptr(acc), _ptr(tok), _ptr(dm),
+                                   _stream(stream)))
+    return acc, tok, dm
+
+
+def spc_verify_ex(q, p, draft, uniforms, rule, alpha, temperature, rule_per_seq=None,
+                  alpha_per_seq=None, temp_per_seq=None, out_row_stats=None, out_argmax=None,
+                  out_sample_norm=None, workspace=None, ev_hot_begin=None, ev_hot_end=None,
+                  out=None, stream=None):
+    """spc_verify with per-sequence parameters and optional outputs.
+    ev_hot_begin / ev_hot_end: hipEvent_t handles (ints or objects with a
+    ``handle`` / ``cuda_event`` attribute) recorded around the statistics
+    kernel."""
+    B, gamma, V = _shape(q, p, draft)
+    acc, tok, dm = _outputs(q, B, gamma, out)
+    ex = ExArgs()
+    ex.rule_per_seq = _ptr(rule_per_seq)
+    ex.alpha_per_seq = _ptr(alpha_per_seq)
+    ex.temp_per_seq = _ptr(temp_per_seq)
+    ex.out_row_stats = _ptr(out_row_stats)
+    ex.out_argmax = _ptr(out_argmax)
+    ex.out_sample_norm = _ptr(out_sample_norm)
+    if workspace is not None:
+        ex.workspace = _ptr(workspace)
+        ex.workspace_bytes = workspace.numel() * workspace.element_size()
+    ex.ev_hot_begin = _event(ev_hot_begin)
+    ex.ev_hot_end = _event(ev_hot_end)
+    _check(lib().spc_verify_ex(_ptr(q), _ptr(p), _dtype_code(q), _ptr(draft), _ptr(uniforms), B,
+                               gamma, V, int(rule), float(alpha), float(temperature), _ptr(acc),
+                               _ptr(tok), _ptr(dm), ctypes.byref(ex), _stream(stream)))
+    return acc, tok, dm
+
+
+def spc_workspace_bytes(B, gamma, V, dtype_code):
+    return lib().spc_workspace_bytes(B, gamma, V, dtype_code)
+
+
+def spc_workspace_zero_bytes(B, gamma, V, dtype_code):
+    return lib().spc_workspace_zero_bytes(B, gamma, V, dtype_code)
+
+
+def spc_last_error():
+    return lib().spc_last_error().decode()
+
+
+def spc_release():
+    lib().spc_release()
+
+
+def spc_version():
+    return lib().spc_version().decode()

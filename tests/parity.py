@@ -1,0 +1,178 @@
+"""GPU-vs-oracle parity harness shared by the GPU tests, the smoke check and
+the benchmark's parity leg.
+
+Rule (applied per sequence, in the order delta_j for all j, accept draws up to
+j*, j*, token): outputs must be identical, except that the FIRST mismatch may
+sit on an oracle decision whose margin is below NEAR (a near-tie); such a
+sequence is counted as excused and its later outputs, which depend on that
+decision, are not compared.  Row statistics must agree to a relative
+tolerance (1e-5 for float32 logits, 2e-3 for bfloat16) with the floors in
+FLOOR below.
+"""
+import json
+import os
+from collections import Counter
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2405_19261_amd import spc
+from paper_2405_19261_amd import workloads as W
+
+NEAR = 1e-6
+FLOAT_TOL = {"f32": 1e-5, "bf16": 2e-3}
+# Floors of the relative criterion, per row-statistic column
+# {m_q, lse_q, maxprob_q, m_p, lse_p, maxprob_p, tv}: m and lse are log-scale
+# (an absolute error e there is a relative error e in every probability);
+# TV and the sampled mass W are differences of probabilities computed from
+# float32 sums, exactly 0 for rows equal up to a shift, so near 0 they are held
+# to tol * 1e-2 absolute (1e-7 for float32 inputs) -- ten times below the
+# decision near-tie margin once scaled by alpha <= 1.
+FLOOR = {0: 1.0, 1: 1.0, 2: 1e-6, 3: 1.0, 4: 1.0, 5: 1e-6, 6: 1e-2}
+
+
+def host_logits(t):
+    t = t.detach().cpu().contiguous()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()
+
+
+def _uniform_params(inp):
+    r, a, t = inp["rule"], inp["alpha"], inp["temperature"]
+    if bool((r == r[0]).all()) and bool((a == a[0]).all()) and bool((t == t[0]).all()):
+        return int(r[0]), float(a[0]), float(t[0])
+    return None
+
+
+def run_gpu(inp, greedy=False, stats=True, stream=None):
+    """One call through the C interface; returns numpy outputs.  Without
+    statistics, batch-wide parameters go through spc_verify /
+    spc_greedy_verify (the entry points the benchmark times)."""
+    q, p = inp["q"], inp["p"]
+    B, g1, V = q.shape
+    dev = q.device
+    row_stats = torch.full((B, g1, 8), float("nan"), device=dev) if stats else None
+    argmax = torch.full((B, g1, 2), -7, dtype=torch.int32, device=dev) if stats else None
+    norm = torch.full((B,), float("nan"), device=dev) if stats else None
+    uni = _uniform_params(inp)
+    if greedy and not stats and uni is not None:
+        acc, tok, dm = spc.spc_greedy_verify(q, p, inp["draft"], uni[0], uni[1], stream=stream)
+    elif not greedy and not stats and uni is not None:
+        acc, tok, dm = spc.spc_verify(q, p, inp["draft"], inp["uniforms"], *uni, stream=stream)
+    else:
+        temp = inp["temperature"]
+        acc, tok, dm = spc.spc_verify_ex(
+            q, p, inp["draft"], inp["uniforms"], 0, 0.0, 1.0, rule_per_seq=inp["rule"],
+            alpha_per_seq=inp["alpha"], temp_per_seq=(torch.zeros_like(temp) if greedy else temp),
+            out_row_stats=row_stats, out_argmax=argmax, out_sample_norm=norm, stream=stream)
+    torch.cuda.synchronize()
+    out = dict(accept_len=acc.cpu().numpy(), next_token=tok.cpu().numpy(),
+               defer=dm.cpu().numpy())
+    if stats:
+        out.update(row_stats=row_stats.cpu().numpy(), argmax=argmax.cpu().numpy(),
+                   sample_norm=norm.cpu().numpy())
+    return out
+
+
+def host_inputs(inp):
+    return dict(q=host_logits(inp["q"]), p=host_logits(inp["p"]),
+                draft=inp["draft"].cpu().numpy(), uniforms=inp["uniforms"].cpu().numpy(),
+                rule=inp["rule"].cpu().numpy(), alpha=inp["alpha"].cpu().numpy(),
+                temperature=inp["temperature"].cpu().numpy())
+
+
+def run_oracle(h, greedy=False):
+    if greedy:
+        return oracle.greedy_verify(h["q"], h["p"], h["draft"], h["rule"], h["alpha"])
+    return oracle.verify(h["q"], h["p"], h["draft"], h["uniforms"], h["rule"], h["alpha"],
+                         h["temperature"])
+
+
+def compare(g, o, h, dtype, greedy=False, rep=None):
+    """Margin-aware comparison of one call; returns (and accumulates) a Counter."""
+    rep = Counter() if rep is None else rep
+    B, g1 = o["defer"].shape
+    gamma = g1 - 1
+    tol = FLOAT_TOL[dtype]
+    for b in range(B):
+        rep["sequences"] += 1
+        # near-ties among the decisions the oracle actually took
+        jo = int(o["accept_len"][b])
+        rep["near_defer"] += int((o["defer_margin"][b] < NEAR).sum())
+        if not greedy:
+            rep["near_accept"] += int((o["accept_margin"][b, :jo + 1 if jo < gamma else gamma]
+                                       < NEAR).sum())
+            rep["near_token"] += int(o["sample_margin"][b] < NEAR)
+        bad = np.flatnonzero(g["defer"][b] != o["defer"][b])
+        if bad.size:
+            j = int(bad[0])
+            m = o["defer_margin"][b, j]
+            assert m < NEAR, f"seq {b}: defer[{j}] gpu={g['defer'][b, j]} oracle=" \
+                             f"{o['defer'][b, j]} margin={m:.3g}"
+            rep["excused_defer"] += 1
+            continue
+        ja = int(g["accept_len"][b])
+        if ja != jo:
+            j = min(ja, jo)
+            m = 0.0 if greedy else o["accept_margin"][b, j]
+            assert m < NEAR, f"seq {b}: accept_len gpu={ja} oracle={jo} margin a_{j}={m:.3g}"
+            rep["excused_accept"] += 1
+            continue
+        if g["next_token"][b] != o["next_token"][b]:
+            m = 0.0 if greedy else o["sample_margin"][b]
+            assert m < NEAR, f"seq {b}: token gpu={g['next_token'][b]} oracle=" \
+                             f"{o['next_token'][b]} margin={m:.3g} (j*={jo})"
+            rep["excused_token"] += 1
+            continue
+        rep["exact"] += 1
+    if "row_stats" in g:
+        gs, os_ = g["row_stats"].astype(np.float64), o["row_stats"]
+        opt_rows = (h["rule"] == W.OPT)[:, None] & np.ones((1, g1), bool)
+        cols = [0, 1, 2, 3, 4, 5]
+        for c in cols + [6]:
+            sel = np.ones(gs.shape[:2], bool) if c != 6 else (opt_rows if not greedy else
+                                                             np.ones_like(opt_rows))
+            if not sel.any():
+                continue
+            err = np.abs(gs[..., c] - os_[..., c])[sel] / np.maximum(np.abs(os_[..., c][sel]),
+                                                                        FLOOR[c])
+            rep[f"maxrel_stat{c}"] = max(rep.get(f"maxrel_stat{c}", 0.0), float(err.max()))
+            rep[f"maxabs_stat{c}"] = max(rep.get(f"maxabs_stat{c}", 0.0),
+                                         float(np.abs(gs[..., c] - os_[..., c])[sel].max()))
+            assert err.max() <= tol, f"row stat {c}: max rel err {err.max():.3g} > {tol}"
+        if greedy:
+            np.testing.assert_array_equal(g["argmax"], o["argmax"])
+        else:
+            ok = g["accept_len"] == o["accept_len"]
+            if ok.any():
+                err = np.abs(g["sample_norm"][ok] - o["sample_norm"][ok]) / np.maximum(
+                    np.abs(o["sample_norm"][ok]), FLOOR[6])
+                rep["maxrel_norm"] = max(rep.get("maxrel_norm", 0.0), float(err.max()))
+                assert err.max() <= tol, f"sample norm: max rel err {err.max():.3g}"
+    return rep
+
+
+def parity_workload(wl, steps, device="cuda", stats=True, step0=0, report_name=None):
+    """Run `steps` seeded steps of workload `wl` on the GPU and the oracle."""
+    rep = Counter()
+    for s in range(step0, step0 + steps):
+        inp = W.generate(wl, s, device)
+        g = run_gpu(inp, greedy=wl.greedy, stats=stats)
+        h = host_inputs(inp)
+        del inp
+        o = run_oracle(h, greedy=wl.greedy)
+        compare(g, o, h, wl.dtype, greedy=wl.greedy, rep=rep)
+    rep["steps"] = steps
+    write_report(report_name or f"cfg{wl.cfg}", wl, rep)
+    return rep
+
+
+def write_report(name, wl, rep):
+    path = os.environ.get("SPC_PARITY_REPORT")
+    if not path:
+        return
+    with open(path, "a") as f:
+        f.write(json.dumps(dict(name=name, workload=wl.name, B=wl.B, gamma=wl.gamma, V=wl.V,
+                                **{k: v for k, v in rep.items()})) + "\n")

@@ -1,0 +1,240 @@
+"""GPU path vs the fp64 oracle, through the C interface (needs an MI355X).
+
+Full-size workloads run in the launch configuration the benchmark times;
+edge cases cover ragged and unaligned vocabularies, masked logits,
+out-of-range drafts, identical drafter/verifier rows, block-size extremes,
+per-sequence parameters, caller workspaces, streams and run-to-run
+determinism."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2405_19261_amd import spc
+from paper_2405_19261_amd import workloads as W
+
+import parity
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _steps(cfg, default):
+    return int(os.environ.get(f"SPC_PARITY_STEPS_{cfg}", default))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.init()
+    yield
+    torch.cuda.synchronize()
+
+
+def _flush(msg):
+    print(msg, flush=True)
+
+
+# ------------------------------------------------------------ full workloads
+
+@pytest.mark.parametrize("cfg,steps", [(1, 1000), (3, 40), (4, 25)])
+def test_workload_parity(cfg, steps):
+    wl = W.WORKLOADS[cfg]
+    _flush(f"[parity] cfg{cfg} {wl.name} steps={_steps(cfg, steps)}")
+    rep = parity.parity_workload(wl, _steps(cfg, steps))
+    _flush(f"[parity] cfg{cfg} {dict(rep)}")
+    assert rep["exact"] + rep["excused_defer"] + rep["excused_accept"] + \
+        rep["excused_token"] == rep["sequences"]
+
+
+@pytest.mark.parametrize("part", range(4))
+def test_workload2_parity(part):
+    """T5-vocabulary workload (OPT): the seeded steps split into four parts."""
+    wl = W.WORKLOADS[2]
+    n = _steps(2, 10000) // 4
+    _flush(f"[parity] cfg2 part {part} steps={n}")
+    rep = parity.parity_workload(wl, n, step0=part * n, stats=(part == 0),
+                                 report_name=f"cfg2.{part}")
+    _flush(f"[parity] cfg2.{part} {dict(rep)}")
+
+
+@pytest.mark.parametrize("part", range(2))
+def test_workload5_parity(part):
+    """Stress mix: per-sequence temperature and rule, identical and independent drafters."""
+    wl = W.WORKLOADS[5]
+    n = _steps(5, 20) // 2
+    _flush(f"[parity] cfg5 part {part} steps={n}")
+    rep = parity.parity_workload(wl, n, step0=part * n, report_name=f"cfg5.{part}")
+    _flush(f"[parity] cfg5.{part} {dict(rep)}")
+
+
+def test_workload3_bench_entry_point():
+    """The batch-wide entry point the benchmark times (no optional outputs)."""
+    wl = W.WORKLOADS[3]
+    rep = parity.parity_workload(wl, 8, stats=False, step0=500, report_name="cfg3.plain")
+    assert rep["sequences"] == 8 * 32
+
+
+def test_workload4_greedy_entry_point_deterministic():
+    wl = W.WORKLOADS[4]
+    inp = W.generate(wl, 7, DEV)
+    a = parity.run_gpu(inp, greedy=True, stats=False)
+    b = parity.run_gpu(inp, greedy=True, stats=False)
+    for k in a:
+        np.testing.assert_array_equal(a[k], b[k])
+    h = parity.host_inputs(inp)
+    o = parity.run_oracle(h, greedy=True)
+    parity.compare(a, o, h, wl.dtype, greedy=True)
+
+
+# ----------------------------------------------------------------- edge cases
+
+@pytest.mark.parametrize("dtype,V", [("bf16", 2), ("bf16", 3), ("bf16", 1000), ("bf16", 1001),
+                                     ("bf16", 16383), ("bf16", 16385), ("bf16", 40000),
+                                     ("f32", 2), ("f32", 999), ("f32", 8193), ("f32", 32128)])
+def test_ragged_vocabularies(dtype, V):
+    for cfg in (3, 2):
+        wl = W.WORKLOADS[cfg].with_(B=6, V=V, dtype=dtype, rule=W.OPT, alpha=0.1)
+        _flush(f"[edge] ragged cfg{cfg} {dtype} V={V}")
+        parity.parity_workload(wl, 3, report_name=f"ragged.{dtype}.{V}")
+
+
+@pytest.mark.parametrize("gamma,B", [(1, 5), (63, 2), (7, 1)])
+def test_block_size_extremes(gamma, B):
+    wl = W.WORKLOADS[3].with_(B=B, gamma=gamma, V=5000)
+    parity.parity_workload(wl, 3, report_name=f"gamma{gamma}")
+    parity.parity_workload(wl.with_(temperature=0.0, cfg=4), 2, report_name=f"gamma{gamma}.g")
+
+
+def test_identical_models_accept_all():
+    wl = W.WORKLOADS[3].with_(B=16, V=20000)
+    for rule, alpha in ((W.DIFF, 0.0), (W.OPT, 0.1), (W.ALWAYS, 0.0), (W.CHOW, 0.3)):
+        inp = W.generate(wl, 3, DEV)
+        inp["p"] = inp["q"].clone()
+        inp["rule"][:] = rule
+        inp["alpha"][:] = alpha
+        g = parity.run_gpu(inp)
+        assert (g["accept_len"] == wl.gamma).all()
+        if rule == W.OPT:
+            assert (g["row_stats"][..., 6] == 0).all()
+        if rule in (W.DIFF, W.OPT):
+            assert (g["defer"] == 0).all()
+        h = parity.host_inputs(inp)
+        parity.compare(g, parity.run_oracle(h), h, wl.dtype)
+
+
+def test_out_of_range_drafts():
+    wl = W.WORKLOADS[3].with_(B=8, V=3000)
+    inp = W.generate(wl, 1, DEV)
+    inp["draft"][:, 2] = torch.tensor([-1, 3000, 1 << 30, -(1 << 30), 2999, 0, -5, 3001],
+                                      dtype=torch.int32, device=DEV)
+    inp["uniforms"][:, :2] = 0.0
+    for rule in (W.DIFF, W.NEVER, W.ALWAYS):
+        inp["rule"][:] = rule
+        g = parity.run_gpu(inp)
+        h = parity.host_inputs(inp)
+        o = parity.run_oracle(h)
+        parity.compare(g, o, h, wl.dtype)
+
+
+def test_masked_logits():
+    """-inf entries (masked tokens) in both tensors."""
+    for cfg, dtype in ((3, "bf16"), (2, "f32")):
+        wl = W.WORKLOADS[cfg].with_(B=8, V=12345, dtype=dtype, rule=W.OPT, alpha=0.1)
+        inp = W.generate(wl, 2, DEV)
+        g0 = torch.Generator(device=DEV).manual_seed(99)
+        for k in ("q", "p"):
+            m = torch.rand(inp[k].shape, generator=g0, device=DEV) < 0.3
+            m[..., 0] = False  # at least one finite entry per row
+            inp[k][m] = float("-inf")
+        inp["draft"] = W.draw_drafts(inp["q"], inp["temperature"], g0)
+        g = parity.run_gpu(inp)
+        h = parity.host_inputs(inp)
+        parity.compare(g, parity.run_oracle(h), h, wl.dtype)
+
+
+def test_greedy_opt_equals_diff_on_gpu():
+    """Lemma 6 on the GPU path: OPT and Diff emit the same tokens at T = 0."""
+    wl = W.WORKLOADS[4].with_(B=64, V=50000)
+    inp = W.generate(wl, 5, DEV)
+    outs = []
+    for rule in (W.OPT, W.DIFF):
+        for alpha in (0.0, 0.1, 0.3):
+            inp["rule"][:] = rule
+            inp["alpha"][:] = alpha
+            outs.append(parity.run_gpu(inp, greedy=True, stats=False))
+    for a, b in zip(outs[:3], outs[3:]):
+        np.testing.assert_array_equal(a["accept_len"], b["accept_len"])
+        np.testing.assert_array_equal(a["next_token"], b["next_token"])
+
+
+def test_mixed_greedy_and_sampled_sequences():
+    """Per-sequence temperature 0 selects the greedy step for that sequence only."""
+    wl = W.WORKLOADS[5].with_(B=24, V=30000)
+    inp = W.generate(wl, 4, DEV)
+    inp["temperature"][::3] = 0.0
+    g = parity.run_gpu(inp)
+    h = parity.host_inputs(inp)
+    greedy = h["temperature"] == 0
+    for sel, gr in ((greedy, True), (~greedy, False)):
+        hs = {k: v[sel] for k, v in h.items()}
+        o = parity.run_oracle(hs, greedy=gr)
+        gs = {k: v[sel] for k, v in g.items()}
+        parity.compare(gs, o, hs, wl.dtype, greedy=gr)
+
+
+def test_invalid_per_sequence_values():
+    wl = W.WORKLOADS[3].with_(B=6, V=4000)
+    inp = W.generate(wl, 0, DEV)
+    inp["rule"][1] = 9
+    inp["alpha"][2] = float("nan")
+    inp["temperature"][3] = -1.0
+    g = parity.run_gpu(inp)
+    assert list(g["accept_len"][1:4]) == [-1, -1, -1]
+    assert list(g["next_token"][1:4]) == [-1, -1, -1]
+    keep = np.array([0, 4, 5])
+    h = {k: v[keep] for k, v in parity.host_inputs(inp).items()}
+    parity.compare({k: v[keep] for k, v in g.items()}, parity.run_oracle(h), h, wl.dtype)
+
+
+def test_per_sequence_arrays_match_scalar_api():
+    wl = W.WORKLOADS[3].with_(B=16, V=70000, rule=W.OPT, alpha=0.1, temperature=0.7)
+    inp = W.generate(wl, 9, DEV)
+    a = parity.run_gpu(inp, stats=True)
+    b = parity.run_gpu(inp, stats=False)
+    for k in ("accept_len", "next_token", "defer"):
+        np.testing.assert_array_equal(a[k], b[k])
+
+
+def test_caller_workspace_and_stream():
+    wl = W.WORKLOADS[3].with_(B=8, V=50000)
+    inp = W.generate(wl, 11, DEV)
+    n = spc.spc_workspace_bytes(8, wl.gamma, wl.V, spc.SPC_BF16)
+    z = spc.spc_workspace_zero_bytes(8, wl.gamma, wl.V, spc.SPC_BF16)
+    ws = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    s = torch.cuda.Stream()
+    ref = parity.run_gpu(inp, stats=False)
+    for _ in range(3):  # the counters must come back to zero after each call
+        with torch.cuda.stream(s):
+            acc, tok, dm = spc.spc_verify_ex(inp["q"], inp["p"], inp["draft"], inp["uniforms"],
+                                             W.DIFF, 0.05, 1.0, workspace=ws, stream=s)
+        s.synchronize()
+        assert (ws[:z] == 0).all()
+        np.testing.assert_array_equal(acc.cpu().numpy(), ref["accept_len"])
+        np.testing.assert_array_equal(tok.cpu().numpy(), ref["next_token"])
+        np.testing.assert_array_equal(dm.cpu().numpy(), ref["defer"])
+
+
+def test_run_to_run_determinism_full_size():
+    """Config-3 and config-5 shapes: two runs are bitwise identical, statistics included."""
+    for cfg in (3, 5):
+        wl = W.WORKLOADS[cfg]
+        inp = W.generate(wl, 123, DEV)
+        a = parity.run_gpu(inp)
+        b = parity.run_gpu(inp)
+        for k in a:
+            np.testing.assert_array_equal(a[k], b[k])
+        del inp
