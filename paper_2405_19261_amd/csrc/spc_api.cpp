@@ -46,25 +46,19 @@ bool vec_path(int dtype, int64_t V) {
 namespace spc {
 
 WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
-  // The completion counters sit at fixed offsets sized for the largest shape
+  // The completion counters sit at a fixed offset sized for the largest batch
   // the interface accepts, so a workspace reused across shapes never has one
   // call's data overlap another call's counters; they stay zero between calls.
   const int64_t R = B * (gamma + 1);
-  const int64_t K = (V + tile_elems(dtype, vec) - 1) / tile_elems(dtype, vec);
-  const size_t cap = 4 * (size_t)(kMaxRows + 1);
+  const int64_t nt = (V + stat_tile_elems(dtype, vec) - 1) / stat_tile_elems(dtype, vec);
+  const int64_t K = (V + samp_tile_elems(dtype, vec) - 1) / samp_tile_elems(dtype, vec);
   WsLayout L;
-  L.row_cnt = 0;
-  L.seq_cnt = cap;
-  L.tv_row_cnt = 2 * cap;
-  L.tv_seq_cnt = 3 * cap;
-  L.samp_cnt = 4 * cap;
-  size_t o = align_up(5 * cap, 256);
+  L.samp_cnt = 0;
+  size_t o = align_up(4 * (size_t)(kMaxRows + 1), 256);
   L.zero_end = o;
-  L.tiles = o; o = align_up(o + sizeof(TilePart) * R * K, 256);
-  L.tvpart = o; o = align_up(o + sizeof(double) * R * K, 256);
+  L.tiles = o; o = align_up(o + sizeof(TilePart) * R * nt, 256);
+  L.tvpart = o; o = align_up(o + sizeof(double) * R * nt, 256);
   L.masses = o; o = align_up(o + sizeof(double) * B * K, 256);
-  L.rows = o; o = align_up(o + sizeof(RowStat) * R, 256);
-  L.seqs = o; o = align_up(o + sizeof(SeqState) * B, 256);
   L.total = o;
   return L;
 }
@@ -158,7 +152,8 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   P.B = B;
   P.gamma = gamma;
   P.V = V;
-  P.K = (int32_t)((V + spc::tile_elems(dtype, vec) - 1) / spc::tile_elems(dtype, vec));
+  P.nt = (int32_t)((V + spc::stat_tile_elems(dtype, vec) - 1) / spc::stat_tile_elems(dtype, vec));
+  P.K = (int32_t)((V + spc::samp_tile_elems(dtype, vec) - 1) / spc::samp_tile_elems(dtype, vec));
   P.rule = rule;
   P.alpha = alpha;
   P.temp = force_greedy ? 0.0f : temperature;
@@ -172,22 +167,17 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   P.out_stats = ex ? ex->out_row_stats : nullptr;
   P.out_argmax = ex ? ex->out_argmax : nullptr;
   P.out_norm = ex ? ex->out_sample_norm : nullptr;
-  P.row_cnt = reinterpret_cast<uint32_t*>(ws + L.row_cnt);
-  P.seq_cnt = reinterpret_cast<uint32_t*>(ws + L.seq_cnt);
-  P.tv_row_cnt = reinterpret_cast<uint32_t*>(ws + L.tv_row_cnt);
-  P.tv_seq_cnt = reinterpret_cast<uint32_t*>(ws + L.tv_seq_cnt);
   P.samp_cnt = reinterpret_cast<uint32_t*>(ws + L.samp_cnt);
   P.tiles = reinterpret_cast<spc::TilePart*>(ws + L.tiles);
   P.tvpart = reinterpret_cast<double*>(ws + L.tvpart);
   P.masses = reinterpret_cast<double*>(ws + L.masses);
-  P.rows = reinterpret_cast<spc::RowStat*>(ws + L.rows);
-  P.seqs = reinterpret_cast<spc::SeqState*>(ws + L.seqs);
 
   // sequences at temperature > 0 may exist unless the whole batch is greedy;
   // OPT at temperature > 0 needs the TV pass
   const bool need_sample = !force_greedy && (per_temp || temperature > 0.0f);
   const bool need_tv = need_sample && (per_rule || rule == SPC_RULE_OPT);
-  hipError_t e = spc::launch_verify(P, dtype, vec, need_tv, need_sample,
+  const bool need_argmax = force_greedy || per_temp;
+  hipError_t e = spc::launch_verify(P, dtype, vec, need_tv, need_sample, need_argmax,
                                     ex ? ex->ev_hot_begin : nullptr,
                                     ex ? ex->ev_hot_end : nullptr, stream);
   if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));

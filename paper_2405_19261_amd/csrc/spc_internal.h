@@ -16,14 +16,14 @@ constexpr int kThreads = 256;  // four 64-lane wavefronts per workgroup
 // extra-token target pi_{t+gamma}, which is q or p.
 enum SampleKind : int32_t { kNone = -1, kResidual = 0, kQ = 1, kP = 2 };
 
-// Partial statistics of one (row, chunk) tile, both tensors.  With c the
-// per-sequence log2(e)/T:  s = sum over the tile of 2^(z*c - r),  r a
-// reference near the tile's largest z*c (-inf for an all -inf tile).
+// Partial statistics of one (row, stats tile), both tensors.  With c the
+// per-sequence log2(e)/T:  s = sum over the tile of 2^(z*c - r),  r the
+// reference zmax * c_hi of the tile (-inf for an all -inf tile).
 struct TilePart {
   double s_q, s_p;
   float r_q, r_p;
   float zmax_q, zmax_p;   // largest raw logit of the tile
-  int32_t amax_q, amax_p; // lowest row index attaining it (greedy rows), else -1
+  int32_t amax_q, amax_p; // lowest row index attaining it (greedy batches), else -1
 };
 
 // Per-row statistics after merging the tiles of a row.
@@ -34,9 +34,9 @@ struct RowStat {
   int32_t amax_q, amax_p;
 };
 
-// Per-sequence state handed from the decision step to the sampler.
+// Per-sequence decision, as the sampler needs it.
 struct SeqState {
-  int32_t row;   // row index b*(gamma+1) + j*
+  int32_t row;   // j*
   int32_t kind;  // SampleKind
   float u;       // the sample's uniform u[b][gamma]
   int32_t pad;
@@ -47,7 +47,9 @@ struct Params {
   const void* p;
   const int32_t* draft;
   const float* uniforms;
-  int32_t B, gamma, V, K;  // K = tiles per row
+  int32_t B, gamma, V;
+  int32_t nt;              // statistics tiles per row
+  int32_t K;               // sampling tiles per row
   int32_t rule;
   float alpha, temp;
   int32_t force_greedy;    // spc_greedy_verify: every sequence at temperature 0
@@ -61,32 +63,29 @@ struct Params {
   int32_t* out_argmax;
   float* out_norm;
   // workspace
-  uint32_t* row_cnt;      // [R]   tiles of a row done (statistics pass)
-  uint32_t* seq_cnt;      // [B]   rows of a sequence done (statistics pass)
-  uint32_t* tv_row_cnt;   // [R]
-  uint32_t* tv_seq_cnt;   // [B]
-  uint32_t* samp_cnt;     // [B]
-  TilePart* tiles;        // [R][K]
-  double* tvpart;         // [R][K]
-  double* masses;         // [B][K]
-  RowStat* rows;          // [R]
-  SeqState* seqs;         // [B]
+  uint32_t* samp_cnt;     // [B]   sampling tiles of a sequence done
+  TilePart* tiles;        // [R][nt] statistics partials
+  double* tvpart;         // [R][nt] TV partials
+  double* masses;         // [B][K]  sampling-tile masses
 };
 
-// Tile geometry: elements per tile for a dtype and load path.
-int tile_elems(int dtype, bool vec);
+// Entries per statistics tile / per sampling tile for a dtype and load path.
+int stat_tile_elems(int dtype, bool vec);
+int samp_tile_elems(int dtype, bool vec);
 
 // Workspace layout for a shape; offsets in bytes from the base.
 struct WsLayout {
-  size_t row_cnt, seq_cnt, tv_row_cnt, tv_seq_cnt, samp_cnt, zero_end;
-  size_t tiles, tvpart, masses, rows, seqs, total;
+  size_t samp_cnt, zero_end;
+  size_t tiles, tvpart, masses, total;
 };
 WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec);
 
 // Enqueue the kernels of one verify call.  need_tv: the batch may hold OPT
 // sequences at temperature > 0; need_sample: it may hold sequences at
-// temperature > 0.  Returns the first launch error.
+// temperature > 0; need_argmax: it may hold greedy (temperature 0)
+// sequences.  Returns the first launch error.
 hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
-                         hipEvent_t ev_begin, hipEvent_t ev_end, hipStream_t stream);
+                         bool need_argmax, hipEvent_t ev_begin, hipEvent_t ev_end,
+                         hipStream_t stream);
 
 }  // namespace spc

@@ -1,27 +1,30 @@
 // spc_kernels.hip -- gfx950 kernels of the speculative-cascade verify step.
 //
 // The step (GenSpecSample, Alg. 4, with the cascade target T_delta of eq. (6)
-// and the deferral rules of Table 1) runs as up to three vocabulary-streaming
-// kernels.  A row is one position (b, j) of one tensor pair (q, p); a tile is
-// one chunk of TILE consecutive vocabulary entries of a row.
+// and the deferral rules of Table 1) runs as two or three kernels.  A row is
+// one position (b, j) of the logit pair (q, p); rows are cut into tiles of
+// consecutive vocabulary entries.
 //
-//   k_stats   grid (tiles per row, rows).  Reads every logit of q and p once
-//             and reduces each tile to {max z, sum 2^(z c - r)} (c = log2 e / T).
-//             The last tile of a row to finish merges the row; the last row of
-//             a sequence to finish runs the per-sequence decision (deferral
-//             delta_j, accept draws a_j, first rejection j*), and, when the
-//             sample is the extra token from q or p, the sample itself.
-//   k_tv      only for OPT sequences: D_TV(p, q) = sum_v max(0, p_v - q_v)
-//             (Lemma 3) needs both normalisers, so it is a second pass over
-//             those rows; its last finisher per sequence runs the decision.
-//   k_resid   for sequences rejected at j* < gamma: the mass of the residual
-//             max(0, p - q) on each tile of row j*; the last finisher picks the
-//             tile and scans it (inverse CDF in vocabulary order).
+//   k_stats   grid (stats tiles per row, rows), one small tile per workgroup.
+//             Reads every logit of q and p once and reduces the tile to
+//             {max z, sum 2^(z c - r)} for both tensors (c = log2(e) / T);
+//             the tile partial goes to the workspace with plain stores.
+//   k_tv      OPT sequences at temperature > 0 only: D_TV(p, q) of Lemma 3
+//             needs both normalisers, so it is a second pass over those rows,
+//             one partial per tile.
+//   k_sample  grid (sample tiles per row, sequences).  Every workgroup of
+//             sequence b merges that sequence's row partials and takes the
+//             per-sequence decision (deferral delta_j, accept draws a_j, first
+//             rejection j*) -- a small, fixed-order computation, so every
+//             workgroup reaches the same result -- then computes the mass of
+//             its tile of row j* under the sampled distribution (residual
+//             max(0, p - q), or the extra-token target q or p).  The last tile
+//             to finish picks the token: inverse CDF in vocabulary order.
 //
-// Completion counters implement "last workgroup to arrive does the next step"
-// with device-scope fences; each counter is reset to zero by its last
-// arriver, so the zeroed workspace is zero again after every call.  Merges
-// run in a fixed order, so results do not depend on scheduling.
+// Kernel boundaries order the passes; within k_sample one completion counter
+// per sequence ("last workgroup to arrive draws") is reset by its last
+// arriver, so the zeroed workspace is zero again after every call.  All
+// merges run in a fixed order: results do not depend on scheduling.
 #include <math.h>
 
 #include "spc_internal.h"
@@ -36,15 +39,23 @@ constexpr double kLn2 = 0.69314718055994530942;   // ln(2)
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // ------------------------------------------------------------------ geometry
-template <int DT, bool VEC>
-struct Geo {
+// A lane load is one 16-byte vector (8 bf16 or 4 f32 entries) on the vector
+// path, one entry on the scalar path (rows not 16-byte aligned).  A tile is U
+// lane loads per thread, U * kThreads * VW entries.
+template <int DT, bool VEC, int U_>
+struct Tile {
   static constexpr int EB = (DT == 1) ? 2 : 4;  // element bytes (1 = bf16, 0 = f32)
-  static constexpr int VW = VEC ? 16 / EB : 1;  // elements per lane load
+  static constexpr int VW = VEC ? 16 / EB : 1;  // entries per lane load
   static constexpr int NW = VEC ? 4 : 1;        // 32-bit words per lane load
-  static constexpr int U = VEC ? 8 : 16;        // lane loads per tensor per tile
-  static constexpr int SLOTS = kThreads * U;    // lane loads per tensor per tile
-  static constexpr int TILE = SLOTS * VW;       // vocabulary entries per tile
+  static constexpr int U = U_;                  // lane loads per thread
+  static constexpr int N = kThreads * U * VW;   // entries per tile
 };
+// statistics / TV tiles: small, so that many workgroups are resident
+template <int DT, bool VEC>
+using StatTile = Tile<DT, VEC, VEC ? 2 : 8>;
+// sampling tiles
+template <int DT, bool VEC>
+using SampTile = Tile<DT, VEC, VEC ? 8 : 16>;
 
 // bfloat16 -> float32 is exact: the bf16 bits are the top half of the float.
 template <int DT, bool VEC>
@@ -61,28 +72,47 @@ __device__ __forceinline__ float elem(const uint32_t* w, int e) {
   }
 }
 
-// One lane load: VW entries starting at entry `slot * VW` of a row; entries
-// at or past V read as -inf (they add nothing to any sum or max).
-template <int DT, bool VEC, bool NT>
-__device__ __forceinline__ void load_slot(const char* row, int64_t slot, int V, uint32_t* w) {
-  using G = Geo<DT, VEC>;
-  const int64_t e0 = slot * G::VW;
-  if (e0 < V) {
-    if constexpr (VEC) {
-      const u32x4* src = reinterpret_cast<const u32x4*>(row + e0 * G::EB);
-      u32x4 v;
-      if constexpr (NT) v = __builtin_nontemporal_load(src);
-      else v = *src;
-      w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
-    } else if constexpr (DT == 1) {
-      w[0] = *reinterpret_cast<const uint16_t*>(row + e0 * 2);
-    } else {
-      w[0] = *reinterpret_cast<const uint32_t*>(row + e0 * 4);
-    }
-  } else {
+// Lane loads of one tile of one row into w[U][NW].  Thread t's lane load i
+// covers entries e = t0 + (OWN ? t*U + i : i*kThreads + t) * VW .. + VW - 1:
+// interleaved (coalesced) when OWN is false, thread-contiguous when true.
+// Entries at or past `end` read as -inf; a lane past the end re-reads a valid
+// address and discards the value, so the loads are branch-free.
+template <int DT, bool VEC, int U, bool OWN, bool NT>
+__device__ __forceinline__ void load_tile(const char* row, int64_t t0, int64_t end,
+                                          uint32_t (&w)[U][Tile<DT, VEC, U>::NW]) {
+  using T = Tile<DT, VEC, U>;
+  constexpr uint32_t kPad = (DT == 1) ? 0xff80ff80u : 0xff800000u;
+  const bool full = t0 + T::N <= end;
 #pragma unroll
-    for (int i = 0; i < G::NW; ++i) w[i] = (DT == 1) ? 0xff80ff80u : 0xff800000u;
+  for (int i = 0; i < U; ++i) {
+    const int64_t slot = OWN ? (int64_t)threadIdx.x * U + i : (int64_t)i * kThreads + threadIdx.x;
+    const int64_t e = t0 + slot * T::VW;
+    const bool ok = full || e < end;
+    const int64_t ec = ok ? e : t0;  // a valid address; the value is discarded
+    const char* a = row + ec * T::EB;
+    if constexpr (VEC) {
+      const u32x4* src = reinterpret_cast<const u32x4*>(a);
+      const u32x4 v = NT ? __builtin_nontemporal_load(src) : *src;
+      w[i][0] = ok ? v.x : kPad;
+      w[i][1] = ok ? v.y : kPad;
+      w[i][2] = ok ? v.z : kPad;
+      w[i][3] = ok ? v.w : kPad;
+    } else if constexpr (DT == 1) {
+      const uint32_t v = *reinterpret_cast<const uint16_t*>(a);
+      w[i][0] = ok ? v : kPad;
+    } else {
+      const uint32_t v = *reinterpret_cast<const uint32_t*>(a);
+      w[i][0] = ok ? v : kPad;
+    }
   }
+}
+
+// Entry index of lane load i, element e of this thread (layout as load_tile).
+template <int DT, bool VEC, int U, bool OWN>
+__device__ __forceinline__ int64_t entry_of(int64_t t0, int i, int e) {
+  using T = Tile<DT, VEC, U>;
+  const int64_t slot = OWN ? (int64_t)threadIdx.x * U + i : (int64_t)i * kThreads + threadIdx.x;
+  return t0 + slot * T::VW + e;
 }
 
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -94,33 +124,10 @@ __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2
 // agent-scope relaxed atomics (write-through / read-through the L2), and the
 // order "data, then counter" is enforced by waiting for the stores to
 // complete before the counter update (and the counter read before the data
-// reads).
-template <typename T>
-__device__ __forceinline__ void st_dev(T* dst, const T& v) {
-  static_assert(sizeof(T) % 8 == 0, "8-byte words");
-  uint64_t w[sizeof(T) / 8];
-  __builtin_memcpy(w, &v, sizeof(T));
-  uint64_t* d = reinterpret_cast<uint64_t*>(dst);
-#pragma unroll
-  for (unsigned i = 0; i < sizeof(T) / 8; ++i)
-    __hip_atomic_store(d + i, w[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-template <typename T>
-__device__ __forceinline__ T ld_dev(const T* src) {
-  static_assert(sizeof(T) % 8 == 0, "8-byte words");
-  uint64_t w[sizeof(T) / 8];
-  uint64_t* s = reinterpret_cast<uint64_t*>(const_cast<T*>(src));
-#pragma unroll
-  for (unsigned i = 0; i < sizeof(T) / 8; ++i)
-    w[i] = __hip_atomic_load(s + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  T v;
-  __builtin_memcpy(&v, w, sizeof(T));
-  return v;
-}
-
+// reads).  Data from an earlier kernel needs nothing: the kernel boundary
+// orders it.
 __device__ __forceinline__ void st_dev_f64(double* dst, double v) {
-  __hip_atomic_store(reinterpret_cast<uint64_t*>(dst), __double_as_longlong(v),
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(dst), (uint64_t)__double_as_longlong(v),
                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ double ld_dev_f64(const double* src) {
@@ -150,9 +157,14 @@ __device__ __forceinline__ int wave_min(int v) {
   for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
   return v;
 }
-__device__ __forceinline__ int wave_maxi(int v) {
+// Inclusive prefix sum over a wavefront's lanes (fp64, fixed order).
+__device__ __forceinline__ double wave_incl_scan(double v) {
+  const int lane = threadIdx.x & 63;
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+  for (int o = 1; o < 64; o <<= 1) {
+    const double n = __shfl_up(v, o, 64);
+    if (lane >= o) v += n;
+  }
   return v;
 }
 
@@ -162,14 +174,22 @@ struct PickState {
   double rem;   // target mass remaining at the start of that tile
 };
 
+constexpr int kPickLds = 256;  // tile masses kept in LDS by the sampler
+
 struct Shared {
   float m[4][2];
   double d[4][2];
   int i[4][2];
   double scan[4];
   int flag;
+};
+
+// Per-sequence state built by every sampling workgroup.
+struct SeqShared {
+  RowStat rows[SPC_MAX_GAMMA + 1];
   SeqState seq;
   PickState pk;
+  double mass[kPickLds];
 };
 
 // All threads receive the block-wide max of (a, b).
@@ -177,6 +197,7 @@ __device__ __forceinline__ void block_max2(float& a, float& b, Shared& sh) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   a = wave_max(a);
   b = wave_max(b);
+  __syncthreads();  // sh.m may still be read by an earlier step
   if (lane == 0) { sh.m[wv][0] = a; sh.m[wv][1] = b; }
   __syncthreads();
   a = fmaxf(fmaxf(sh.m[0][0], sh.m[1][0]), fmaxf(sh.m[2][0], sh.m[3][0]));
@@ -188,7 +209,7 @@ __device__ __forceinline__ void block_sum2(double& a, double& b, Shared& sh) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   a = wave_sum(a);
   b = wave_sum(b);
-  __syncthreads();  // sh.d may still be read by an earlier step
+  __syncthreads();
   if (lane == 0) { sh.d[wv][0] = a; sh.d[wv][1] = b; }
   __syncthreads();
   a = ((sh.d[0][0] + sh.d[1][0]) + sh.d[2][0]) + sh.d[3][0];
@@ -210,11 +231,7 @@ __device__ __forceinline__ void block_min2(int& a, int& b, Shared& sh) {
 // last thread's value equals *total bit for bit.
 __device__ __forceinline__ double block_incl_scan(double v, Shared& sh, double* total) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const double n = __shfl_up(v, o, 64);
-    if (lane >= o) v += n;
-  }
+  v = wave_incl_scan(v);
   __syncthreads();
   if (lane == 63) sh.scan[wv] = v;
   __syncthreads();
@@ -222,6 +239,29 @@ __device__ __forceinline__ double block_incl_scan(double v, Shared& sh, double* 
   for (int w = 0; w < wv; ++w) off += sh.scan[w];
   *total = ((sh.scan[0] + sh.scan[1]) + sh.scan[2]) + sh.scan[3];
   return off + v;
+}
+
+// "Am I the last of `n` arrivals?" for the whole block.  Thread 0 wrote the
+// data it shares with st_dev_* before the call; on true, the counter is reset
+// and the block reads the other arrivals' data with ld_dev_*.
+__device__ __forceinline__ bool arrive_last(uint32_t* cnt, uint32_t n, Shared& sh) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    vmem_drain();  // this thread's shared stores are complete
+    const uint32_t prev =
+        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const bool last = (prev == n - 1);
+    if (last) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    sh.flag = last;
+  }
+  __syncthreads();
+  const bool last = sh.flag;
+  if (last) {
+    vmem_drain();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  }
+  return last;
 }
 
 // ------------------------------------------------------ per-sequence params
@@ -234,7 +274,7 @@ struct SeqParam {
   bool valid;
 };
 
-__device__ SeqParam seq_param(const Params& P, int b) {
+__device__ __forceinline__ SeqParam seq_param(const Params& P, int b) {
   SeqParam s;
   s.rule = P.rule_ps ? P.rule_ps[b] : P.rule;
   const float alpha = P.alpha_ps ? P.alpha_ps[b] : P.alpha;
@@ -303,11 +343,11 @@ __device__ __forceinline__ float residual_weight(float zq, float zp, const ProbS
   return prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo) * exp2m1_pos(d);
 }
 
-// Weight of one entry under the distribution sampled at j*.
-__device__ __forceinline__ float sample_weight(int kind, float zq, float zp, const ProbScale& s) {
-  if (kind == kQ) return prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
-  if (kind == kP) return prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
-  return residual_weight(zq, zp, s);
+template <int KIND>
+__device__ __forceinline__ float weight_of(float zq, float zp, const ProbScale& s) {
+  if constexpr (KIND == kQ) return prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
+  else if constexpr (KIND == kP) return prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
+  else return residual_weight(zq, zp, s);
 }
 
 template <int DT>
@@ -332,70 +372,81 @@ __device__ __forceinline__ int defer_rule(int rule, double alpha, double maxq, d
   }
 }
 
-// --------------------------------------------------------------- row merge
-// Wave 0 merges the K tile partials of row r into its RowStat (lane 0 writes).
-__device__ void row_merge(const Params& P, int r, bool greedy) {
-  const int lane = threadIdx.x;
-  const int K = P.K;
-  const TilePart* t = P.tiles + (int64_t)r * K;
-  float rq = kNegInf, rp = kNegInf, zq = kNegInf, zp = kNegInf;
-  for (int k = lane; k < K; k += 64) {
-    const TilePart tk = ld_dev(t + k);
-    rq = fmaxf(rq, tk.r_q);
-    rp = fmaxf(rp, tk.r_p);
-    zq = fmaxf(zq, tk.zmax_q);
-    zp = fmaxf(zp, tk.zmax_p);
+// ------------------------------------------------------------- row merge
+// One wavefront merges the nt tile partials of row r (fixed order: lanes take
+// tiles lane, lane+64, ...; a butterfly combines the lanes), adding the TV
+// partials when `tv`.  Every lane returns the same RowStat.
+__device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy, bool tv) {
+  const int lane = threadIdx.x & 63;
+  const int nt = P.nt;
+  const TilePart* t = P.tiles + (int64_t)r * nt;
+  float zq = kNegInf, zp = kNegInf, rq = kNegInf, rp = kNegInf;
+  for (int k = lane; k < nt; k += 64) {
+    zq = fmaxf(zq, t[k].zmax_q);
+    zp = fmaxf(zp, t[k].zmax_p);
+    rq = fmaxf(rq, t[k].r_q);
+    rp = fmaxf(rp, t[k].r_p);
   }
-  rq = wave_max(rq); rp = wave_max(rp); zq = wave_max(zq); zp = wave_max(zp);
-  double sq = 0.0, sp = 0.0;
+  zq = wave_max(zq);
+  zp = wave_max(zp);
+  rq = wave_max(rq);
+  rp = wave_max(rp);
+  double sq = 0.0, sp = 0.0, tvs = 0.0;
   int aq = 0x7fffffff, ap = 0x7fffffff;
-  for (int k = lane; k < K; k += 64) {
-    const TilePart tk = ld_dev(t + k);
+  for (int k = lane; k < nt; k += 64) {
+    const TilePart tk = t[k];
     if (tk.r_q != kNegInf) sq += tk.s_q * exp2((double)tk.r_q - (double)rq);
     if (tk.r_p != kNegInf) sp += tk.s_p * exp2((double)tk.r_p - (double)rp);
     if (greedy) {
       if (tk.zmax_q == zq) aq = min(aq, tk.amax_q);
       if (tk.zmax_p == zp) ap = min(ap, tk.amax_p);
     }
+    if (tv) tvs += P.tvpart[(int64_t)r * nt + k];
   }
-  sq = wave_sum(sq); sp = wave_sum(sp);
-  aq = wave_min(aq); ap = wave_min(ap);
-  if (lane == 0) {
-    RowStat rs;
-    rs.lz_q = (double)rq + log2(sq);
-    rs.lz_p = (double)rp + log2(sp);
-    rs.tv = 0.0;
-    rs.zmax_q = zq;
-    rs.zmax_p = zp;
-    rs.amax_q = greedy ? aq : -1;
-    rs.amax_p = greedy ? ap : -1;
-    st_dev(P.rows + r, rs);
-  }
+  sq = wave_sum(sq);
+  sp = wave_sum(sp);
+  tvs = wave_sum(tvs);
+  aq = wave_min(aq);
+  ap = wave_min(ap);
+  RowStat rs;
+  rs.lz_q = (double)rq + log2(sq);
+  rs.lz_p = (double)rp + log2(sp);
+  rs.tv = tvs;
+  rs.zmax_q = zq;
+  rs.zmax_p = zp;
+  rs.amax_q = greedy ? aq : -1;
+  rs.amax_p = greedy ? ap : -1;
+  return rs;
 }
 
 // ------------------------------------------------------------- decision
-// Wave 0: delta_j and the accept draws of one sequence, j*, and the outputs
-// that follow from them (Alg. 4, first-rejection search by one ballot).
+// Wave 0: delta_j and the accept draws of one sequence from its merged rows,
+// j* (first-rejection search by one ballot), and the sampling state.  With
+// `write`, also the outputs that follow (every sampling workgroup of the
+// sequence computes the same decision; one writes it).
 template <int DT>
-__device__ void decide(const Params& P, int b, const SeqParam& sp, Shared& sh) {
+__device__ __forceinline__ void decide(const Params& P, int b, const SeqParam& sp,
+                                       SeqShared& ss, bool write) {
   const int lane = threadIdx.x;
   const int gamma = P.gamma, g1 = gamma + 1;
   const bool on = lane < g1;
   const int64_t row = (int64_t)b * g1 + lane;
   if (!sp.valid) {
-    if (on) P.out_defer[row] = 0;
-    if (lane == 0) {
-      P.out_accept[b] = -1;
-      P.out_token[b] = -1;
-      if (P.out_norm) P.out_norm[b] = 0.0f;
-      sh.seq = SeqState{-1, kNone, 0.0f, 0};
+    if (write) {
+      if (on) P.out_defer[row] = 0;
+      if (lane == 0) {
+        P.out_accept[b] = -1;
+        P.out_token[b] = -1;
+        if (P.out_norm) P.out_norm[b] = 0.0f;
+      }
     }
+    if (lane == 0) ss.seq = SeqState{-1, kNone, 0.0f, 0};
     return;
   }
   int delta = 0, keep = 1;
   RowStat rs{};
   if (on) {
-    rs = ld_dev(P.rows + row);
+    rs = ss.rows[lane];
     const double maxq = exp2((double)rs.zmax_q * sp.c - rs.lz_q);
     const double maxp = exp2((double)rs.zmax_p * sp.c - rs.lz_p);
     // greedy: one-hot q~, p~ give D_TV = 1(argmax q != argmax p)  (Lemma 6)
@@ -416,22 +467,24 @@ __device__ void decide(const Params& P, int b, const SeqParam& sp, Shared& sh) {
     } else {
       keep = 0;  // a_gamma = 0
     }
-    P.out_defer[row] = (uint8_t)delta;
-    if (P.out_stats) {
-      const double T = sp.greedy ? 1.0 : kLog2e / sp.c;
-      float* o = P.out_stats + row * 8;
-      o[0] = (float)((double)rs.zmax_q / T);
-      o[1] = (float)(rs.lz_q * kLn2);
-      o[2] = (float)maxq;
-      o[3] = (float)((double)rs.zmax_p / T);
-      o[4] = (float)(rs.lz_p * kLn2);
-      o[5] = (float)maxp;
-      o[6] = (float)tv;
-      o[7] = 0.0f;
-    }
-    if (P.out_argmax) {
-      P.out_argmax[row * 2 + 0] = rs.amax_q;
-      P.out_argmax[row * 2 + 1] = rs.amax_p;
+    if (write) {
+      P.out_defer[row] = (uint8_t)delta;
+      if (P.out_stats) {
+        const double T = sp.greedy ? 1.0 : kLog2e / sp.c;
+        float* o = P.out_stats + row * 8;
+        o[0] = (float)((double)rs.zmax_q / T);
+        o[1] = (float)(rs.lz_q * kLn2);
+        o[2] = (float)maxq;
+        o[3] = (float)((double)rs.zmax_p / T);
+        o[4] = (float)(rs.lz_p * kLn2);
+        o[5] = (float)maxp;
+        o[6] = (float)tv;
+        o[7] = 0.0f;
+      }
+      if (P.out_argmax) {
+        P.out_argmax[row * 2 + 0] = rs.amax_q;
+        P.out_argmax[row * 2 + 1] = rs.amax_p;
+      }
     }
   }
   const unsigned long long rej = __ballot(on && !keep);
@@ -440,376 +493,429 @@ __device__ void decide(const Params& P, int b, const SeqParam& sp, Shared& sh) {
   const int aq = __shfl(rs.amax_q, jstar, 64);
   const int ap = __shfl(rs.amax_p, jstar, 64);
   if (lane == 0) {
-    P.out_accept[b] = jstar;
-    SeqState s{b * g1 + jstar, kNone, 0.0f, 0};
+    SeqState s{jstar, kNone, 0.0f, 0};
     if (sp.greedy) {
-      P.out_token[b] = dstar ? ap : aq;
-      if (P.out_norm) P.out_norm[b] = 1.0f;
+      if (write) {
+        P.out_token[b] = dstar ? ap : aq;
+        if (P.out_norm) P.out_norm[b] = 1.0f;
+      }
     } else {
       // a rejection with delta = 0 only happens for an out-of-range draft;
       // its residual max(0, q - q) is empty, so p is sampled instead
       s.kind = (jstar < gamma) ? (dstar ? kResidual : kP) : (dstar ? kP : kQ);
       s.u = P.uniforms[(int64_t)b * g1 + gamma];
     }
-    sh.seq = s;
+    if (write) P.out_accept[b] = jstar;
+    ss.seq = s;
   }
 }
 
-// Mass of tile k under `kind` (Q/P from the statistics pass, residual from
-// the residual pass).
-__device__ __forceinline__ double tile_mass(const Params& P, int b, int row, int k, int kind,
-                                            const RowStat& rs) {
-  if (kind == kResidual) return ld_dev_f64(P.masses + (int64_t)b * P.K + k);
-  const TilePart t = ld_dev(P.tiles + (int64_t)row * P.K + k);
-  const float r = (kind == kQ) ? t.r_q : t.r_p;
-  if (r == kNegInf) return 0.0;
-  const double s = (kind == kQ) ? t.s_q : t.s_p;
-  return s * exp2((double)r - ((kind == kQ) ? rs.lz_q : rs.lz_p));
+// Whole block: merge the rows of sequence b into ss.rows and decide it.
+template <int DT>
+__device__ __forceinline__ void merge_and_decide(const Params& P, int b, const SeqParam& sp,
+                                                 SeqShared& ss, bool write) {
+  const int wv = threadIdx.x >> 6, g1 = P.gamma + 1;
+  const bool tv = needs_tv(sp);
+  if (sp.valid) {
+    for (int j = wv; j < g1; j += kThreads / 64) {
+      const RowStat rs = merge_row(P, b * g1 + j, sp.greedy, tv);
+      if ((threadIdx.x & 63) == 0) ss.rows[j] = rs;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < 64) decide<DT>(P, b, sp, ss, write);
+  __syncthreads();
 }
 
-// Whole block: inverse-CDF draw at row s.row.  The smallest entry k with
-// C_k > u * W (C the running mass in vocabulary order): tile masses -> tile,
-// then block-wide inclusive scans over the tile's lane loads -> lane, then a
-// sequential search inside the lane's entries.
-template <int DT, bool VEC>
-__device__ void pick(const Params& P, int b, const SeqState& s, const SeqParam& sp,
-                     Shared& sh) {
-  using G = Geo<DT, VEC>;
+// ------------------------------------------------------------- sampling
+// Whole block: the mass of sampling tile k of a row under the sampled
+// distribution (valid in every thread).
+template <int DT, bool VEC, int KIND>
+__device__ __forceinline__ double block_tile_mass(const char* qrow, const char* prow, int V,
+                                                  int k, const ProbScale& ps, Shared& sh) {
+  using T = SampTile<DT, VEC>;
+  const int64_t t0 = (int64_t)k * T::N;
+  uint32_t wq[T::U][T::NW] = {}, wp[T::U][T::NW] = {};
+  if (KIND != kP) load_tile<DT, VEC, T::U, false, false>(qrow, t0, V, wq);
+  if (KIND != kQ) load_tile<DT, VEC, T::U, false, false>(prow, t0, V, wp);
+  double acc = 0.0;
+#pragma unroll
+  for (int i = 0; i < T::U; ++i) {
+    float t = 0.0f;
+#pragma unroll
+    for (int e = 0; e < T::VW; ++e)
+      t += weight_of<KIND>(elem<DT, VEC>(wq[i], e), elem<DT, VEC>(wp[i], e), ps);
+    acc += (double)t;
+  }
+  double unused = 0.0;
+  block_sum2(acc, unused, sh);
+  return acc;
+}
+
+// The in-tile part of the draw: each thread takes U consecutive lane loads of
+// tile pk.k, one block-wide scan of the per-thread masses finds the thread,
+// and that thread walks its entries.
+template <int DT, bool VEC, int KIND>
+__device__ __forceinline__ void pick_in_tile(const Params& P, int b, int row, const PickState& pk,
+                                             const ProbScale& ps, Shared& sh) {
+  using T = SampTile<DT, VEC>;
   const int tid = threadIdx.x;
-  const int K = P.K;
-  const RowStat rs = ld_dev(P.rows + s.row);
-  if (tid == 0) {
-    int kind = s.kind;
-    double W = 0.0;
-    for (int k = 0; k < K; ++k) W += tile_mass(P, b, s.row, k, kind, rs);
-    if (kind == kResidual && !(W > 0.0)) {  // empty residual (rounding): sample p
-      kind = kP;
-      W = 0.0;
-      for (int k = 0; k < K; ++k) W += tile_mass(P, b, s.row, k, kind, rs);
+  const int V = P.V;
+  const char* qrow = (const char*)P.q + (int64_t)row * V * T::EB;
+  const char* prow = (const char*)P.p + (int64_t)row * V * T::EB;
+  const int64_t t0 = (int64_t)pk.k * T::N;
+  uint32_t wq[T::U][T::NW] = {}, wp[T::U][T::NW] = {};
+  if (KIND != kP) load_tile<DT, VEC, T::U, true, false>(qrow, t0, V, wq);
+  if (KIND != kQ) load_tile<DT, VEC, T::U, true, false>(prow, t0, V, wp);
+  // per lane-load masses, in entry order
+  double slot_mass[T::U];
+  double tsum = 0.0;
+  int last_pos = -1;
+#pragma unroll
+  for (int i = 0; i < T::U; ++i) {
+    double m = 0.0;
+#pragma unroll
+    for (int e = 0; e < T::VW; ++e) {
+      const float w = weight_of<KIND>(elem<DT, VEC>(wq[i], e), elem<DT, VEC>(wp[i], e), ps);
+      m += (double)w;
+      if (w > 0.0f) last_pos = (int)entry_of<DT, VEC, T::U, true>(t0, i, e);
     }
-    const double target = (double)s.u * W;
-    double C = 0.0, rem = 0.0;
-    int ks = -1, klast = -1;
-    for (int k = 0; k < K; ++k) {
-      const double m = tile_mass(P, b, s.row, k, kind, rs);
-      if (m > 0.0) klast = k;
-      if (ks < 0 && C + m > target) {
-        ks = k;
-        rem = target - C;
+    slot_mass[i] = m;
+    tsum += m;
+  }
+  double total;
+  const double incl = block_incl_scan(tsum, sh, &total);
+  if (total > pk.rem) {  // block-uniform
+    int cand = (incl > pk.rem) ? tid : 0x7fffffff, unused = 0;
+    block_min2(cand, unused, sh);
+    if (tid == cand) {
+      // the lane load where the running mass crosses, then its entries
+      double run = incl - tsum, before = 0.0;
+      int islot = -1;
+#pragma unroll
+      for (int i = 0; i < T::U; ++i) {
+        if (islot < 0 && run + slot_mass[i] > pk.rem) {
+          islot = i;
+          before = run;
+        }
+        run += slot_mass[i];
       }
-      C += m;
+      int hit = -1;
+      if (islot >= 0) {
+        uint32_t sq[T::NW] = {}, sp_[T::NW] = {};
+#pragma unroll
+        for (int i = 0; i < T::U; ++i)
+          if (i == islot)
+#pragma unroll
+            for (int j = 0; j < T::NW; ++j) {
+              sq[j] = wq[i][j];
+              sp_[j] = wp[i][j];
+            }
+        run = before;
+        int lastw = -1;
+        const int64_t base = entry_of<DT, VEC, T::U, true>(t0, islot, 0);
+#pragma unroll
+        for (int e = 0; e < T::VW; ++e) {
+          const float w = weight_of<KIND>(elem<DT, VEC>(sq, e), elem<DT, VEC>(sp_, e), ps);
+          run += (double)w;
+          if (w > 0.0f) lastw = (int)(base + e);
+          if (hit < 0 && run > pk.rem && w > 0.0f) hit = (int)(base + e);
+        }
+        if (hit < 0) hit = lastw;  // rounding inside the lane load
+      }
+      // rounding inside the thread: its last entry with mass
+      P.out_token[b] = hit >= 0 ? hit : last_pos;
+    }
+    return;
+  }
+  // rounding: no thread reached u*W; take the last entry of the tile with mass
+  int lp = -last_pos, unused = 0;
+  block_min2(lp, unused, sh);
+  if (tid == 0) P.out_token[b] = -lp;
+}
+
+// Wave 0 gathers the K tile masses of sequence b (into LDS when they fit);
+// returns their total W to the whole block.
+__device__ __forceinline__ double gather_masses(const Params& P, int b, SeqShared& ss,
+                                                Shared& sh) {
+  const int lane = threadIdx.x & 63, K = P.K;
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    double W = 0.0;
+    for (int k0 = 0; k0 < K; k0 += 64) {
+      const int k = k0 + lane;
+      const double m = (k < K) ? ld_dev_f64(P.masses + (int64_t)b * K + k) : 0.0;
+      if (k < K && k < kPickLds) ss.mass[k] = m;
+      W += wave_sum(m);
+    }
+    if (lane == 0) sh.d[0][0] = W;
+  }
+  __syncthreads();
+  return sh.d[0][0];
+}
+
+// Whole block: inverse-CDF draw at row j* of sequence b -- the smallest entry
+// k with C_k > u * W, C the running mass in vocabulary order and W the total.
+// Wave 0 scans the tile masses (64 at a time) to find the tile, then
+// pick_in_tile finds the entry.
+template <int DT, bool VEC>
+__device__ __forceinline__ void pick(const Params& P, int b, const SeqParam& sp, SeqShared& ss,
+                                     Shared& sh) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int K = P.K;
+  const SeqState s = ss.seq;
+  const int row = b * (P.gamma + 1) + s.row;
+  const ProbScale ps = prob_scale(sp, ss.rows[s.row]);
+  int kind = s.kind;
+  double W = gather_masses(P, b, ss, sh);
+  if (kind == kResidual && !(W > 0.0)) {
+    // empty residual (possible only through rounding): sample p instead
+    kind = kP;
+    const int V = P.V;
+    const char* qrow = (const char*)P.q + (int64_t)row * V * SampTile<DT, VEC>::EB;
+    const char* prow = (const char*)P.p + (int64_t)row * V * SampTile<DT, VEC>::EB;
+    for (int k = 0; k < K; ++k) {
+      const double m = block_tile_mass<DT, VEC, kP>(qrow, prow, V, k, ps, sh);
+      if (tid == 0) st_dev_f64(P.masses + (int64_t)b * K + k, m);
+    }
+    if (tid == 0) vmem_drain();
+    W = gather_masses(P, b, ss, sh);
+  }
+  if (tid < 64) {
+    const double target = (double)s.u * W;
+    double carry = 0.0, rem = 0.0;
+    int ks = -1, klast = -1;
+    for (int k0 = 0; k0 < K; k0 += 64) {
+      const int k = k0 + lane;
+      const double m = (k >= K) ? 0.0
+                       : (k < kPickLds) ? ss.mass[k] : ld_dev_f64(P.masses + (int64_t)b * K + k);
+      const double incl = carry + wave_incl_scan(m);
+      const unsigned long long pos = __ballot(m > 0.0);
+      const unsigned long long hit = __ballot(m > 0.0 && incl > target);
+      if (pos) klast = k0 + 63 - __clzll(pos);
+      if (ks < 0 && hit) {
+        const int l = __ffsll(hit) - 1;
+        ks = k0 + l;
+        rem = target - (__shfl(incl, l, 64) - __shfl(m, l, 64));
+      }
+      carry = __shfl(incl, 63, 64);
     }
     if (ks < 0) {  // rounding left u*W at or past the end: last entry with mass
       ks = klast;
       rem = __builtin_huge_val();
     }
-    sh.pk = PickState{ks, kind, rem};
-    if (P.out_norm) P.out_norm[b] = (float)W;
+    if (lane == 0) {
+      ss.pk = PickState{ks, kind, rem};
+      if (P.out_norm) P.out_norm[b] = (float)W;
+    }
   }
   __syncthreads();
-  const PickState pk = sh.pk;
+  const PickState pk = ss.pk;
   if (pk.k < 0) {
     if (tid == 0) P.out_token[b] = -1;
     return;
   }
-  const ProbScale ps = prob_scale(sp, rs);
-  const int V = P.V;
-  const char* qrow = (const char*)P.q + (int64_t)s.row * V * G::EB;
-  const char* prow = (const char*)P.p + (int64_t)s.row * V * G::EB;
-  const int64_t slot0 = (int64_t)pk.k * G::SLOTS;
-  double rem = pk.rem;
-  int token = 0x7fffffff, last_pos = -1;
-  for (int i = 0; i < G::U; ++i) {
-    const int64_t slot = slot0 + (int64_t)i * kThreads + tid;
-    uint32_t wq[G::NW], wp[G::NW];
-    load_slot<DT, VEC, false>(qrow, slot, V, wq);
-    load_slot<DT, VEC, false>(prow, slot, V, wp);
-    float w[G::VW];
-    double tsum = 0.0;
-#pragma unroll
-    for (int e = 0; e < G::VW; ++e) {
-      w[e] = sample_weight(pk.kind, elem<DT, VEC>(wq, e), elem<DT, VEC>(wp, e), ps);
-      tsum += (double)w[e];
-      if (w[e] > 0.0f) last_pos = (int)(slot * G::VW + e);
-    }
-    double total;
-    const double incl = block_incl_scan(tsum, sh, &total);
-    if (total > rem) {  // block-uniform: the draw falls in this block of entries
-      int cand = (incl > rem) ? tid : 0x7fffffff, unused = 0;
-      block_min2(cand, unused, sh);
-      if (tid == cand) {
-        double run = incl - tsum;
-        int hit = -1, lastw = -1;
-#pragma unroll
-        for (int e = 0; e < G::VW; ++e) {
-          run += (double)w[e];
-          if (w[e] > 0.0f) lastw = e;
-          if (hit < 0 && run > rem) hit = e;
-        }
-        if (hit < 0) hit = lastw;  // rounding inside the lane: its last entry with mass
-        P.out_token[b] = (int)(slot * G::VW + hit);
-      }
-      return;
-    }
-    rem -= total;
-  }
-  // rounding: no block reached u*W; take the last entry of the tile with mass
-  int lp = last_pos, unused = 0;
-  lp = -lp;
-  block_min2(lp, unused, sh);
-  if (tid == 0) P.out_token[b] = -lp;
-  (void)token;
-}
-
-// After the decision: sample now (extra token from q or p) or leave the
-// sequence to the residual pass.
-template <int DT, bool VEC>
-__device__ void decide_and_sample(const Params& P, int b, const SeqParam& sp, Shared& sh) {
-  if (threadIdx.x < 64) decide<DT>(P, b, sp, sh);
-  __syncthreads();
-  const SeqState s = sh.seq;
-  if (threadIdx.x == 0) st_dev(P.seqs + b, s);
-  if (s.kind == kQ || s.kind == kP) pick<DT, VEC>(P, b, s, sp, sh);
-}
-
-// "Am I the last of `n` arrivals?" for the whole block.  Data this block
-// shares was written with st_dev by thread 0 before the call; on true, the
-// counter is reset and the caller reads the other arrivals' data with ld_dev.
-__device__ __forceinline__ bool arrive_last(uint32_t* cnt, uint32_t n, Shared& sh) {
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    vmem_drain();  // this thread's shared stores are complete
-    const uint32_t prev =
-        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const bool last = (prev == n - 1);
-    if (last) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    sh.flag = last;
-  }
-  __syncthreads();
-  const bool last = sh.flag;
-  if (last) {
-    vmem_drain();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-  }
-  return last;
+  if (pk.kind == kQ) pick_in_tile<DT, VEC, kQ>(P, b, row, pk, ps, sh);
+  else if (pk.kind == kP) pick_in_tile<DT, VEC, kP>(P, b, row, pk, ps, sh);
+  else pick_in_tile<DT, VEC, kResidual>(P, b, row, pk, ps, sh);
 }
 
 // ================================================================ kernels
 
-template <int DT, bool VEC>
+// Statistics pass.  grid (nt, R): stats tile k of row r.  Each thread takes
+// the exact max of its entries and the sum of 2^(z c - r_t), r_t = max * c_hi
+// (a reference near its largest z c); the block combines the threads against
+// the tile max.  With ARGMAX (batches that may hold greedy rows) the lowest
+// entry attaining the max is found as well.
+template <int DT, bool VEC, bool ARGMAX>
 __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
-  using G = Geo<DT, VEC>;
+  using T = StatTile<DT, VEC>;
   __shared__ Shared sh;
-  const int k = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
-  const int g1 = P.gamma + 1, b = r / g1;
-  const SeqParam sp = seq_param(P, b);
+  const int k = blockIdx.x, r = blockIdx.y;
+  const SeqParam sp = seq_param(P, r / (P.gamma + 1));
   const int V = P.V;
-  const char* qrow = (const char*)P.q + (int64_t)r * V * G::EB;
-  const char* prow = (const char*)P.p + (int64_t)r * V * G::EB;
-  const int64_t slot0 = (int64_t)k * G::SLOTS;
+  const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
+  const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
+  const int64_t t0 = (int64_t)k * T::N;
+  uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
+  load_tile<DT, VEC, T::U, false, true>(qrow, t0, V, wq);
+  load_tile<DT, VEC, T::U, false, true>(prow, t0, V, wp);
 
-  uint32_t wq[G::U][G::NW], wp[G::U][G::NW];
-#pragma unroll
-  for (int i = 0; i < G::U; ++i) {
-    load_slot<DT, VEC, true>(qrow, slot0 + i * kThreads + tid, V, wq[i]);
-    load_slot<DT, VEC, true>(prow, slot0 + i * kThreads + tid, V, wp[i]);
-  }
   float mq = kNegInf, mp = kNegInf;
 #pragma unroll
-  for (int i = 0; i < G::U; ++i)
+  for (int i = 0; i < T::U; ++i)
 #pragma unroll
-    for (int e = 0; e < G::VW; ++e) {
+    for (int e = 0; e < T::VW; ++e) {
       mq = fmaxf(mq, elem<DT, VEC>(wq[i], e));
       mp = fmaxf(mp, elem<DT, VEC>(wp[i], e));
     }
-  float Mq = mq, Mp = mp;
-  block_max2(Mq, Mp, sh);
-
-  int aq = -1, ap = -1;
-  if (sp.greedy) {  // lowest entry attaining the tile max (only lanes holding it search)
-    int cq = 0x7fffffff, cp = 0x7fffffff;
-    if (mq == Mq && Mq != kNegInf) {
-      for (int i = 0; i < G::U && cq == 0x7fffffff; ++i)
-        for (int e = 0; e < G::VW; ++e)
-          if (elem<DT, VEC>(wq[i], e) == Mq) {
-            cq = (int)((slot0 + i * kThreads + tid) * G::VW + e);
-            break;
-          }
-    }
-    if (mp == Mp && Mp != kNegInf) {
-      for (int i = 0; i < G::U && cp == 0x7fffffff; ++i)
-        for (int e = 0; e < G::VW; ++e)
-          if (elem<DT, VEC>(wp[i], e) == Mp) {
-            cp = (int)((slot0 + i * kThreads + tid) * G::VW + e);
-            break;
-          }
-    }
-    block_min2(cq, cp, sh);
-    aq = cq;
-    ap = cp;
+  int iq = 0x7fffffff, ip = 0x7fffffff;
+  if constexpr (ARGMAX) {
+    // entries are visited in increasing index order: the first match wins
+#pragma unroll
+    for (int i = 0; i < T::U; ++i)
+#pragma unroll
+      for (int e = 0; e < T::VW; ++e) {
+        const int idx = (int)entry_of<DT, VEC, T::U, false>(t0, i, e);
+        if (iq == 0x7fffffff && elem<DT, VEC>(wq[i], e) == mq) iq = idx;
+        if (ip == 0x7fffffff && elem<DT, VEC>(wp[i], e) == mp) ip = idx;
+      }
   }
-
-  // sum over the tile of 2^(z c - r), r = Mq * c_hi rounded (a reference, not
-  // an exact product: the partial is exact with respect to its own r)
-  const float rq = (Mq == kNegInf) ? 0.0f : Mq * sp.c_hi;
-  const float rp = (Mp == kNegInf) ? 0.0f : Mp * sp.c_hi;
+  const float rq = (mq == kNegInf) ? 0.0f : mq * sp.c_hi;
+  const float rp = (mp == kNegInf) ? 0.0f : mp * sp.c_hi;
   float sq = 0.0f, spp = 0.0f;
 #pragma unroll
-  for (int i = 0; i < G::U; ++i) {
-    float tq[G::VW], tp[G::VW];
+  for (int i = 0; i < T::U; ++i) {
+    float tq[T::VW], tp[T::VW];
 #pragma unroll
-    for (int e = 0; e < G::VW; ++e) {
+    for (int e = 0; e < T::VW; ++e) {
       const float zq = elem<DT, VEC>(wq[i], e), zp = elem<DT, VEC>(wp[i], e);
       tq[e] = exp2_hw(fmaf(zq, sp.c_lo, fmaf(zq, sp.c_hi, -rq)));
       tp[e] = exp2_hw(fmaf(zp, sp.c_lo, fmaf(zp, sp.c_hi, -rp)));
     }
 #pragma unroll
-    for (int w = 1; w < G::VW; w <<= 1)
+    for (int h = 1; h < T::VW; h <<= 1)
 #pragma unroll
-      for (int e = 0; e + w < G::VW; e += 2 * w) {
-        tq[e] += tq[e + w];
-        tp[e] += tp[e + w];
+      for (int e = 0; e + h < T::VW; e += 2 * h) {
+        tq[e] += tq[e + h];
+        tp[e] += tp[e + h];
       }
     sq += tq[0];
     spp += tp[0];
   }
-  double Sq = sq, Sp = spp;
-  block_sum2(Sq, Sp, sh);
-  if (tid == 0) {
+  float Mq = mq, Mp = mp;
+  block_max2(Mq, Mp, sh);
+  const float Rq = Mq * sp.c_hi, Rp = Mp * sp.c_hi;
+  double dq = (mq == kNegInf) ? 0.0 : (double)sq * (double)exp2_hw(rq - Rq);
+  double dp = (mp == kNegInf) ? 0.0 : (double)spp * (double)exp2_hw(rp - Rp);
+  block_sum2(dq, dp, sh);
+  if constexpr (ARGMAX) {
+    iq = (mq == Mq) ? iq : 0x7fffffff;
+    ip = (mp == Mp) ? ip : 0x7fffffff;
+    block_min2(iq, ip, sh);
+  }
+  if (threadIdx.x == 0) {
     TilePart t;
-    t.s_q = Sq;
-    t.s_p = Sp;
-    t.r_q = (Mq == kNegInf) ? kNegInf : rq;
-    t.r_p = (Mp == kNegInf) ? kNegInf : rp;
+    t.s_q = dq;
+    t.s_p = dp;
+    t.r_q = (Mq == kNegInf) ? kNegInf : Rq;
+    t.r_p = (Mp == kNegInf) ? kNegInf : Rp;
     t.zmax_q = Mq;
     t.zmax_p = Mp;
-    t.amax_q = aq;
-    t.amax_p = ap;
-    st_dev(P.tiles + (int64_t)r * P.K + k, t);
+    t.amax_q = ARGMAX ? iq : -1;
+    t.amax_p = ARGMAX ? ip : -1;
+    P.tiles[(int64_t)r * P.nt + k] = t;
   }
-  if (!arrive_last(P.row_cnt + r, (uint32_t)P.K, sh)) return;
-  if (tid < 64) row_merge(P, r, sp.greedy);
-  if (!arrive_last(P.seq_cnt + b, (uint32_t)g1, sh)) return;
-  if (needs_tv(sp)) return;  // the TV pass decides OPT sequences
-  decide_and_sample<DT, VEC>(P, b, sp, sh);
 }
 
+// TV pass (OPT rows at temperature > 0): D_TV(p, q) of Lemma 3, which needs
+// both normalisers.  grid (nt, R): stats tile k of row r; wave 0 merges the
+// row's statistics first (a fixed-order computation every tile of the row
+// repeats identically).
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kThreads) void k_tv(Params P) {
-  using G = Geo<DT, VEC>;
+  using T = StatTile<DT, VEC>;
   __shared__ Shared sh;
-  const int k = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
-  const int g1 = P.gamma + 1, b = r / g1;
-  const SeqParam sp = seq_param(P, b);
+  __shared__ RowStat srow;
+  const int k = blockIdx.x, r = blockIdx.y;
+  const SeqParam sp = seq_param(P, r / (P.gamma + 1));
   if (!needs_tv(sp)) return;  // block-uniform
-  const RowStat rs = ld_dev(P.rows + r);
-  const ProbScale ps = prob_scale(sp, rs);
   const int V = P.V;
-  const char* qrow = (const char*)P.q + (int64_t)r * V * G::EB;
-  const char* prow = (const char*)P.p + (int64_t)r * V * G::EB;
-  const int64_t slot0 = (int64_t)k * G::SLOTS;
-  uint32_t wq[G::U][G::NW], wp[G::U][G::NW];
-#pragma unroll
-  for (int i = 0; i < G::U; ++i) {
-    load_slot<DT, VEC, true>(qrow, slot0 + i * kThreads + tid, V, wq[i]);
-    load_slot<DT, VEC, true>(prow, slot0 + i * kThreads + tid, V, wp[i]);
+  const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
+  const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
+  const int64_t t0 = (int64_t)k * T::N;
+  uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
+  load_tile<DT, VEC, T::U, false, true>(qrow, t0, V, wq);
+  load_tile<DT, VEC, T::U, false, true>(prow, t0, V, wp);
+  if (threadIdx.x < 64) {
+    const RowStat rs = merge_row(P, r, false, false);
+    if (threadIdx.x == 0) srow = rs;
   }
-  float acc = 0.0f;
-#pragma unroll
-  for (int i = 0; i < G::U; ++i) {
-    float t[G::VW];
-#pragma unroll
-    for (int e = 0; e < G::VW; ++e)
-      t[e] = sample_weight(kResidual, elem<DT, VEC>(wq[i], e), elem<DT, VEC>(wp[i], e), ps);
-#pragma unroll
-    for (int w = 1; w < G::VW; w <<= 1)
-#pragma unroll
-      for (int e = 0; e + w < G::VW; e += 2 * w) t[e] += t[e + w];
-    acc += t[0];
-  }
-  double tv = acc, unused = 0.0;
-  block_sum2(tv, unused, sh);
-  if (tid == 0) st_dev_f64(P.tvpart + (int64_t)r * P.K + k, tv);
-  if (!arrive_last(P.tv_row_cnt + r, (uint32_t)P.K, sh)) return;
-  if (tid == 0) {
-    double s = 0.0;
-    for (int j = 0; j < P.K; ++j) s += ld_dev_f64(P.tvpart + (int64_t)r * P.K + j);
-    st_dev_f64(&P.rows[r].tv, s);
-  }
-  if (!arrive_last(P.tv_seq_cnt + b, (uint32_t)g1, sh)) return;
-  decide_and_sample<DT, VEC>(P, b, sp, sh);
-}
-
-template <int DT, bool VEC>
-__global__ __launch_bounds__(kThreads) void k_resid(Params P) {
-  using G = Geo<DT, VEC>;
-  __shared__ Shared sh;
-  const int k = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
-  const SeqState s = ld_dev(P.seqs + b);
-  if (s.kind != kResidual) return;  // block-uniform
-  const SeqParam sp = seq_param(P, b);
-  const RowStat rs = ld_dev(P.rows + s.row);
-  const ProbScale ps = prob_scale(sp, rs);
-  const int V = P.V;
-  const char* qrow = (const char*)P.q + (int64_t)s.row * V * G::EB;
-  const char* prow = (const char*)P.p + (int64_t)s.row * V * G::EB;
-  const int64_t slot0 = (int64_t)k * G::SLOTS;
-  uint32_t wq[G::U][G::NW], wp[G::U][G::NW];
-#pragma unroll
-  for (int i = 0; i < G::U; ++i) {
-    load_slot<DT, VEC, false>(qrow, slot0 + i * kThreads + tid, V, wq[i]);
-    load_slot<DT, VEC, false>(prow, slot0 + i * kThreads + tid, V, wp[i]);
-  }
+  __syncthreads();
+  const ProbScale ps = prob_scale(sp, srow);
   double acc = 0.0;
 #pragma unroll
-  for (int i = 0; i < G::U; ++i)
+  for (int i = 0; i < T::U; ++i) {
+    float t = 0.0f;
 #pragma unroll
-    for (int e = 0; e < G::VW; ++e)
-      acc += (double)sample_weight(kResidual, elem<DT, VEC>(wq[i], e),
-                                   elem<DT, VEC>(wp[i], e), ps);
+    for (int e = 0; e < T::VW; ++e)
+      t += residual_weight(elem<DT, VEC>(wq[i], e), elem<DT, VEC>(wp[i], e), ps);
+    acc += (double)t;
+  }
   double unused = 0.0;
   block_sum2(acc, unused, sh);
-  if (tid == 0) st_dev_f64(P.masses + (int64_t)b * P.K + k, acc);
+  if (threadIdx.x == 0) P.tvpart[(int64_t)r * P.nt + k] = acc;
+}
+
+// Sampling pass.  grid (K, B): every workgroup of sequence b merges the
+// sequence's rows and decides it (workgroup 0 writes the outputs); sampling
+// tile k of row j* then computes its mass and the last tile to finish draws.
+template <int DT, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_sample(Params P) {
+  __shared__ Shared sh;
+  __shared__ SeqShared ss;
+  const int k = blockIdx.x, b = blockIdx.y;
+  const SeqParam sp = seq_param(P, b);
+  merge_and_decide<DT>(P, b, sp, ss, k == 0);
+  const SeqState s = ss.seq;
+  if (s.kind == kNone) return;  // block-uniform
+  const int row = b * (P.gamma + 1) + s.row;
+  const ProbScale ps = prob_scale(sp, ss.rows[s.row]);
+  const int V = P.V;
+  constexpr int EB = SampTile<DT, VEC>::EB;
+  const char* qrow = (const char*)P.q + (int64_t)row * V * EB;
+  const char* prow = (const char*)P.p + (int64_t)row * V * EB;
+  double m;
+  if (s.kind == kQ) m = block_tile_mass<DT, VEC, kQ>(qrow, prow, V, k, ps, sh);
+  else if (s.kind == kP) m = block_tile_mass<DT, VEC, kP>(qrow, prow, V, k, ps, sh);
+  else m = block_tile_mass<DT, VEC, kResidual>(qrow, prow, V, k, ps, sh);
+  if (threadIdx.x == 0) st_dev_f64(P.masses + (int64_t)b * P.K + k, m);
   if (!arrive_last(P.samp_cnt + b, (uint32_t)P.K, sh)) return;
-  pick<DT, VEC>(P, b, s, sp, sh);
+  pick<DT, VEC>(P, b, sp, ss, sh);
 }
 
 template <int DT, bool VEC>
-hipError_t launch_t(const Params& P, bool need_tv, bool need_sample, hipEvent_t e0,
-                    hipEvent_t e1, hipStream_t st) {
+hipError_t launch_t(const Params& P, bool need_tv, bool need_sample, bool need_argmax,
+                    hipEvent_t e0, hipEvent_t e1, hipStream_t st) {
   const unsigned R = (unsigned)(P.B * (P.gamma + 1));
   hipError_t err;
   if (e0 && (err = hipEventRecord(e0, st)) != hipSuccess) return err;
-  hipLaunchKernelGGL((k_stats<DT, VEC>), dim3(P.K, R), dim3(kThreads), 0, st, P);
+  if (need_argmax)
+    hipLaunchKernelGGL((k_stats<DT, VEC, true>), dim3(P.nt, R), dim3(kThreads), 0, st, P);
+  else
+    hipLaunchKernelGGL((k_stats<DT, VEC, false>), dim3(P.nt, R), dim3(kThreads), 0, st, P);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (e1 && (err = hipEventRecord(e1, st)) != hipSuccess) return err;
   if (need_tv) {
-    hipLaunchKernelGGL((k_tv<DT, VEC>), dim3(P.K, R), dim3(kThreads), 0, st, P);
+    hipLaunchKernelGGL((k_tv<DT, VEC>), dim3(P.nt, R), dim3(kThreads), 0, st, P);
     if ((err = hipGetLastError()) != hipSuccess) return err;
   }
-  if (need_sample) {
-    hipLaunchKernelGGL((k_resid<DT, VEC>), dim3(P.K, P.B), dim3(kThreads), 0, st, P);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
-  }
-  return hipSuccess;
+  // a batch with no sequence at temperature > 0 only needs the decisions
+  hipLaunchKernelGGL((k_sample<DT, VEC>), dim3(need_sample ? P.K : 1, P.B), dim3(kThreads), 0,
+                     st, P);
+  return hipGetLastError();
 }
 
 }  // namespace
 
-int tile_elems(int dtype, bool vec) {
-  if (dtype == 1) return vec ? Geo<1, true>::TILE : Geo<1, false>::TILE;
-  return vec ? Geo<0, true>::TILE : Geo<0, false>::TILE;
+int stat_tile_elems(int dtype, bool vec) {
+  if (dtype == 1) return vec ? StatTile<1, true>::N : StatTile<1, false>::N;
+  return vec ? StatTile<0, true>::N : StatTile<0, false>::N;
+}
+
+int samp_tile_elems(int dtype, bool vec) {
+  if (dtype == 1) return vec ? SampTile<1, true>::N : SampTile<1, false>::N;
+  return vec ? SampTile<0, true>::N : SampTile<0, false>::N;
 }
 
 hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
-                         hipEvent_t e0, hipEvent_t e1, hipStream_t st) {
+                         bool need_argmax, hipEvent_t e0, hipEvent_t e1, hipStream_t st) {
   if (dtype == 1) {
-    return vec ? launch_t<1, true>(P, need_tv, need_sample, e0, e1, st)
-               : launch_t<1, false>(P, need_tv, need_sample, e0, e1, st);
+    return vec ? launch_t<1, true>(P, need_tv, need_sample, need_argmax, e0, e1, st)
+               : launch_t<1, false>(P, need_tv, need_sample, need_argmax, e0, e1, st);
   }
-  return vec ? launch_t<0, true>(P, need_tv, need_sample, e0, e1, st)
-             : launch_t<0, false>(P, need_tv, need_sample, e0, e1, st);
+  return vec ? launch_t<0, true>(P, need_tv, need_sample, need_argmax, e0, e1, st)
+             : launch_t<0, false>(P, need_tv, need_sample, need_argmax, e0, e1, st);
 }
 
 }  // namespace spc
