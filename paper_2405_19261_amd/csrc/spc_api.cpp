@@ -51,14 +51,13 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
   // call's data overlap another call's counters; they stay zero between calls.
   const int64_t R = B * (gamma + 1);
   const int64_t nt = (V + stat_tile_elems(dtype, vec) - 1) / stat_tile_elems(dtype, vec);
-  const int64_t K = (V + samp_tile_elems(dtype, vec) - 1) / samp_tile_elems(dtype, vec);
   WsLayout L;
   L.samp_cnt = 0;
   size_t o = align_up(4 * (size_t)(kMaxRows + 1), 256);
   L.zero_end = o;
   L.tiles = o; o = align_up(o + sizeof(TilePart) * R * nt, 256);
   L.tvpart = o; o = align_up(o + sizeof(double) * R * nt, 256);
-  L.masses = o; o = align_up(o + sizeof(double) * B * K, 256);
+  L.masses = o; o = align_up(o + sizeof(double) * B * nt * kChunksPerTile, 256);
   L.total = o;
   return L;
 }
@@ -153,7 +152,7 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   P.gamma = gamma;
   P.V = V;
   P.nt = (int32_t)((V + spc::stat_tile_elems(dtype, vec) - 1) / spc::stat_tile_elems(dtype, vec));
-  P.K = (int32_t)((V + spc::samp_tile_elems(dtype, vec) - 1) / spc::samp_tile_elems(dtype, vec));
+  P.K = spc::samp_groups(P.nt);
   P.rule = rule;
   P.alpha = alpha;
   P.temp = force_greedy ? 0.0f : temperature;

@@ -11,6 +11,8 @@
 namespace spc {
 
 constexpr int kThreads = 256;  // four 64-lane wavefronts per workgroup
+// A tile is read as kChunksPerTile wave-contiguous chunks by the sampler.
+constexpr int kChunksPerTile = kThreads / 64;
 
 // Sampling distribution at j* (Alg. 4): the residual max(0, p - q), or the
 // extra-token target pi_{t+gamma}, which is q or p.
@@ -49,7 +51,7 @@ struct Params {
   const float* uniforms;
   int32_t B, gamma, V;
   int32_t nt;              // statistics tiles per row
-  int32_t K;               // sampling tiles per row
+  int32_t K;               // sampling workgroups per sequence
   int32_t rule;
   float alpha, temp;
   int32_t force_greedy;    // spc_greedy_verify: every sequence at temperature 0
@@ -63,15 +65,16 @@ struct Params {
   int32_t* out_argmax;
   float* out_norm;
   // workspace
-  uint32_t* samp_cnt;     // [B]   sampling tiles of a sequence done
+  uint32_t* samp_cnt;     // [B]   sampling workgroups of a sequence done
   TilePart* tiles;        // [R][nt] statistics partials
   double* tvpart;         // [R][nt] TV partials
-  double* masses;         // [B][K]  sampling-tile masses
+  double* masses;         // [B][nt][4] residual chunk masses of row j*
 };
 
-// Entries per statistics tile / per sampling tile for a dtype and load path.
+// Entries per statistics tile for a dtype and load path, and sampling
+// workgroups per sequence for a row of nt such tiles.
 int stat_tile_elems(int dtype, bool vec);
-int samp_tile_elems(int dtype, bool vec);
+int samp_groups(int64_t nt);
 
 // Workspace layout for a shape; offsets in bytes from the base.
 struct WsLayout {

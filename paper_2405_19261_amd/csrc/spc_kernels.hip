@@ -38,6 +38,12 @@ constexpr double kLn2 = 0.69314718055994530942;   // ln(2)
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+constexpr int kWaves = kThreads / 64;
+// The sampling pass runs 1024-thread workgroups: a wavefront per row while
+// deciding, a 256-thread group per tile while summing residual masses.
+constexpr int kSampThreads = 1024;
+constexpr int kSampWaves = kSampThreads / 64;
+
 // ------------------------------------------------------------------ geometry
 // A lane load is one 16-byte vector (8 bf16 or 4 f32 entries) on the vector
 // path, one entry on the scalar path (rows not 16-byte aligned).  A tile is U
@@ -53,9 +59,10 @@ struct Tile {
 // statistics / TV tiles: small, so that many workgroups are resident
 template <int DT, bool VEC>
 using StatTile = Tile<DT, VEC, VEC ? 2 : 8>;
-// sampling tiles
-template <int DT, bool VEC>
-using SampTile = Tile<DT, VEC, VEC ? 8 : 16>;
+// The sampling pass works on the same tiles (so a draw can use the statistics
+// partials as tile masses); a sampling workgroup sums the residual masses of
+// kSampBatch tiles per batch, and takes two batches.
+constexpr int kSampBatch = kSampThreads / kThreads;
 
 // bfloat16 -> float32 is exact: the bf16 bits are the top half of the float.
 template <int DT, bool VEC>
@@ -72,20 +79,21 @@ __device__ __forceinline__ float elem(const uint32_t* w, int e) {
   }
 }
 
-// Lane loads of one tile of one row into w[U][NW].  Thread t's lane load i
-// covers entries e = t0 + (OWN ? t*U + i : i*kThreads + t) * VW .. + VW - 1:
-// interleaved (coalesced) when OWN is false, thread-contiguous when true.
+// Lane loads of one tile of one row into w[U][NW] by the GT threads of a
+// group, tid the thread's index in it.  Thread t's lane load i covers entries
+// e = t0 + (OWN ? t*U + i : i*GT + t) * VW .. + VW - 1: interleaved
+// (coalesced) when OWN is false, thread-contiguous when true.
 // Entries at or past `end` read as -inf; a lane past the end re-reads a valid
 // address and discards the value, so the loads are branch-free.
-template <int DT, bool VEC, int U, bool OWN, bool NT>
+template <int DT, bool VEC, int U, bool OWN, bool NT, int GT = kThreads>
 __device__ __forceinline__ void load_tile(const char* row, int64_t t0, int64_t end,
-                                          uint32_t (&w)[U][Tile<DT, VEC, U>::NW]) {
+                                          uint32_t (&w)[U][Tile<DT, VEC, U>::NW], int tid) {
   using T = Tile<DT, VEC, U>;
   constexpr uint32_t kPad = (DT == 1) ? 0xff80ff80u : 0xff800000u;
-  const bool full = t0 + T::N <= end;
+  const bool full = t0 + (int64_t)GT * U * T::VW <= end;
 #pragma unroll
   for (int i = 0; i < U; ++i) {
-    const int64_t slot = OWN ? (int64_t)threadIdx.x * U + i : (int64_t)i * kThreads + threadIdx.x;
+    const int64_t slot = OWN ? (int64_t)tid * U + i : (int64_t)i * GT + tid;
     const int64_t e = t0 + slot * T::VW;
     const bool ok = full || e < end;
     const int64_t ec = ok ? e : t0;  // a valid address; the value is discarded
@@ -108,14 +116,39 @@ __device__ __forceinline__ void load_tile(const char* row, int64_t t0, int64_t e
 }
 
 // Entry index of lane load i, element e of this thread (layout as load_tile).
-template <int DT, bool VEC, int U, bool OWN>
-__device__ __forceinline__ int64_t entry_of(int64_t t0, int i, int e) {
+template <int DT, bool VEC, int U, bool OWN, int GT = kThreads>
+__device__ __forceinline__ int64_t entry_of(int64_t t0, int i, int e, int tid) {
   using T = Tile<DT, VEC, U>;
-  const int64_t slot = OWN ? (int64_t)threadIdx.x * U + i : (int64_t)i * kThreads + threadIdx.x;
+  const int64_t slot = OWN ? (int64_t)tid * U + i : (int64_t)i * GT + tid;
   return t0 + slot * T::VW + e;
 }
 
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float log2_hw(float x) { return __builtin_amdgcn_logf(x); }
+
+// 2^d in fp64 by exact argument reduction, d = n + f with n = floor(d) and
+// f in [0, 1), and the hardware 2^f: relative error about one float32 ulp.
+// Arguments below -1022 give 0.
+__device__ __forceinline__ double exp2_acc(double d) {
+  if (d < -1022.0) return 0.0;
+  const double n = floor(d);
+  return ldexp((double)exp2_hw((float)(d - n)), (int)n);
+}
+
+// log2 of a positive finite fp64 value: S = m 2^e with m in [1/sqrt(2),
+// sqrt(2)), m = head + tail with a float32 head, log2(m) = log2(head) +
+// tail / (head ln 2): absolute error about one float32 ulp of |log2 m| <= 1/2.
+__device__ __forceinline__ double log2_acc(double S) {
+  int e;
+  double m = frexp(S, &e);
+  if (m < 0.70710678118654752) {
+    m *= 2.0;
+    --e;
+  }
+  const float mh = (float)m;
+  const double tail = m - (double)mh;
+  return (double)e + (double)log2_hw(mh) + tail * (double)__builtin_amdgcn_rcpf(mh) * kLog2e;
+}
 
 // ------------------------------------------- cross-workgroup communication
 // Agent-scope fences on gfx950 write back and invalidate the whole L2, which
@@ -142,94 +175,163 @@ __device__ __forceinline__ void vmem_drain() {
 }
 
 // ------------------------------------------------------- wavefront reductions
+// DPP row operations combine the lanes of each 16-lane row without going
+// through LDS; readlane then brings the four row results to every lane in a
+// fixed order, so every lane (and every run) gets the same value.  All 64
+// lanes must be active.
+constexpr int kDppXor1 = 0xb1;         // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4e;         // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141;  // row_half_mirror
+constexpr int kDppMirror = 0x140;      // row_mirror
+constexpr int kDppShr = 0x110;         // row_shr:n is kDppShr + n
+
+// Lanes with no source lane (row_shr at the start of a row) read 0.
+template <int CTRL>
+__device__ __forceinline__ int dpp_i32(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xf, 0xf, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(dpp_i32<CTRL>(__float_as_int(v)));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const int lo = dpp_i32<CTRL>(__double2loint(v));
+  const int hi = dpp_i32<CTRL>(__double2hiint(v));
+  return __hiloint2double(hi, lo);
+}
+
+// Value of lane l (l uniform across the wave).
+__device__ __forceinline__ int lane_i32(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ float lane_f32(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+__device__ __forceinline__ double lane_f64(double v, int l) {
+  return __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(v), l),
+                          __builtin_amdgcn_readlane(__double2loint(v), l));
+}
+
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  v = fmaxf(v, dpp_f32<kDppXor1>(v));
+  v = fmaxf(v, dpp_f32<kDppXor2>(v));
+  v = fmaxf(v, dpp_f32<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f32<kDppMirror>(v));
+  return fmaxf(fmaxf(lane_f32(v, 0), lane_f32(v, 16)), fmaxf(lane_f32(v, 32), lane_f32(v, 48)));
 }
 __device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v += dpp_f64<kDppXor1>(v);
+  v += dpp_f64<kDppXor2>(v);
+  v += dpp_f64<kDppHalfMirror>(v);
+  v += dpp_f64<kDppMirror>(v);
+  return (lane_f64(v, 0) + lane_f64(v, 16)) + (lane_f64(v, 32) + lane_f64(v, 48));
 }
 __device__ __forceinline__ int wave_min(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
-  return v;
+  v = min(v, dpp_i32<kDppXor1>(v));
+  v = min(v, dpp_i32<kDppXor2>(v));
+  v = min(v, dpp_i32<kDppHalfMirror>(v));
+  v = min(v, dpp_i32<kDppMirror>(v));
+  return min(min(lane_i32(v, 0), lane_i32(v, 16)), min(lane_i32(v, 32), lane_i32(v, 48)));
 }
-// Inclusive prefix sum over a wavefront's lanes (fp64, fixed order).
+// Inclusive prefix sum over a wavefront's lanes (fp64, fixed order): a
+// Hillis-Steele scan inside each row, then the earlier rows' totals.
 __device__ __forceinline__ double wave_incl_scan(double v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const double n = __shfl_up(v, o, 64);
-    if (lane >= o) v += n;
-  }
-  return v;
+  v += dpp_f64<kDppShr + 1>(v);
+  v += dpp_f64<kDppShr + 2>(v);
+  v += dpp_f64<kDppShr + 4>(v);
+  v += dpp_f64<kDppShr + 8>(v);
+  const double t0 = lane_f64(v, 15), t1 = lane_f64(v, 31), t2 = lane_f64(v, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  const double off = row == 0 ? 0.0 : row == 1 ? t0 : row == 2 ? t0 + t1 : (t0 + t1) + t2;
+  return off + v;
 }
 
-struct PickState {
-  int k;        // tile holding the sample
-  int kind;     // SampleKind actually sampled
-  double rem;   // target mass remaining at the start of that tile
-};
-
-constexpr int kPickLds = 256;  // tile masses kept in LDS by the sampler
-
-struct Shared {
-  float m[4][2];
-  double d[4][2];
-  int i[4][2];
-  double scan[4];
+// Block-wide scratch of a workgroup of NWV wavefronts.
+template <int NWV>
+struct SharedT {
+  static constexpr int kNW = NWV;
+  float m[NWV][2];
+  double d[NWV][2];
+  double dv[NWV];
+  int i[NWV][2];
+  double scan[NWV];
   int flag;
+};
+using Shared = SharedT<kWaves>;
+using SampShared = SharedT<kSampWaves>;
+
+// Merged statistics and decision of one row of a sequence.
+struct RowDecision {
+  RowStat rs;
+  float maxq, maxp, tv;  // inputs of the deferral rule
+  float u;               // the row's uniform
+  int delta, keep;       // delta_j and a_j
 };
 
 // Per-sequence state built by every sampling workgroup.
 struct SeqShared {
-  RowStat rows[SPC_MAX_GAMMA + 1];
+  RowDecision rows[SPC_MAX_GAMMA + 1];
   SeqState seq;
-  PickState pk;
-  double mass[kPickLds];
 };
 
+// Block reductions: per-wave results combined in wave order (a fixed order,
+// so every thread and every run gets the same value).
 // All threads receive the block-wide max of (a, b).
-__device__ __forceinline__ void block_max2(float& a, float& b, Shared& sh) {
+template <int NWV>
+__device__ __forceinline__ void block_max2(float& a, float& b, SharedT<NWV>& sh) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   a = wave_max(a);
   b = wave_max(b);
   __syncthreads();  // sh.m may still be read by an earlier step
   if (lane == 0) { sh.m[wv][0] = a; sh.m[wv][1] = b; }
   __syncthreads();
-  a = fmaxf(fmaxf(sh.m[0][0], sh.m[1][0]), fmaxf(sh.m[2][0], sh.m[3][0]));
-  b = fmaxf(fmaxf(sh.m[0][1], sh.m[1][1]), fmaxf(sh.m[2][1], sh.m[3][1]));
+  a = sh.m[0][0];
+  b = sh.m[0][1];
+#pragma unroll
+  for (int w = 1; w < NWV; ++w) {
+    a = fmaxf(a, sh.m[w][0]);
+    b = fmaxf(b, sh.m[w][1]);
+  }
 }
 
-// Block sums in a fixed order; valid in every thread.
-__device__ __forceinline__ void block_sum2(double& a, double& b, Shared& sh) {
+// Block sums; valid in every thread.
+template <int NWV>
+__device__ __forceinline__ void block_sum2(double& a, double& b, SharedT<NWV>& sh) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   a = wave_sum(a);
   b = wave_sum(b);
   __syncthreads();
   if (lane == 0) { sh.d[wv][0] = a; sh.d[wv][1] = b; }
   __syncthreads();
-  a = ((sh.d[0][0] + sh.d[1][0]) + sh.d[2][0]) + sh.d[3][0];
-  b = ((sh.d[0][1] + sh.d[1][1]) + sh.d[2][1]) + sh.d[3][1];
+  a = sh.d[0][0];
+  b = sh.d[0][1];
+#pragma unroll
+  for (int w = 1; w < NWV; ++w) {
+    a += sh.d[w][0];
+    b += sh.d[w][1];
+  }
 }
 
-__device__ __forceinline__ void block_min2(int& a, int& b, Shared& sh) {
+template <int NWV>
+__device__ __forceinline__ void block_min2(int& a, int& b, SharedT<NWV>& sh) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   a = wave_min(a);
   b = wave_min(b);
   __syncthreads();
   if (lane == 0) { sh.i[wv][0] = a; sh.i[wv][1] = b; }
   __syncthreads();
-  a = min(min(sh.i[0][0], sh.i[1][0]), min(sh.i[2][0], sh.i[3][0]));
-  b = min(min(sh.i[0][1], sh.i[1][1]), min(sh.i[2][1], sh.i[3][1]));
+  a = sh.i[0][0];
+  b = sh.i[0][1];
+#pragma unroll
+  for (int w = 1; w < NWV; ++w) {
+    a = min(a, sh.i[w][0]);
+    b = min(b, sh.i[w][1]);
+  }
 }
 
 // Inclusive prefix sum over the block's threads in thread order (fp64); the
 // last thread's value equals *total bit for bit.
-__device__ __forceinline__ double block_incl_scan(double v, Shared& sh, double* total) {
+template <int NWV>
+__device__ __forceinline__ double block_incl_scan(double v, SharedT<NWV>& sh, double* total) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   v = wave_incl_scan(v);
   __syncthreads();
@@ -237,14 +339,18 @@ __device__ __forceinline__ double block_incl_scan(double v, Shared& sh, double* 
   __syncthreads();
   double off = 0.0;
   for (int w = 0; w < wv; ++w) off += sh.scan[w];
-  *total = ((sh.scan[0] + sh.scan[1]) + sh.scan[2]) + sh.scan[3];
+  double tot = 0.0;
+#pragma unroll
+  for (int w = 0; w < NWV; ++w) tot += sh.scan[w];
+  *total = tot;
   return off + v;
 }
 
 // "Am I the last of `n` arrivals?" for the whole block.  Thread 0 wrote the
 // data it shares with st_dev_* before the call; on true, the counter is reset
 // and the block reads the other arrivals' data with ld_dev_*.
-__device__ __forceinline__ bool arrive_last(uint32_t* cnt, uint32_t n, Shared& sh) {
+template <int NWV>
+__device__ __forceinline__ bool arrive_last(uint32_t* cnt, uint32_t n, SharedT<NWV>& sh) {
   __syncthreads();
   if (threadIdx.x == 0) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
@@ -322,25 +428,21 @@ __device__ __forceinline__ float prob(float z, float c_hi, float c_lo, float l_h
   return exp2_hw(fmaf(z, c_hi, -l_hi) + fmaf(z, c_lo, -l_lo));
 }
 
-// 2^d - 1 for d > 0 with a relative error of a few float32 ulps: a Taylor
-// series of expm1(x), x = d ln 2, below d = 1/4 (where 2^d - 1 would cancel),
-// the hardware 2^d above.
-__device__ __forceinline__ float exp2m1_pos(float d) {
-  const float x = d * 0.693147180559945309f;
-  const float series =
-      x * (1.0f + x * (0.5f + x * (1.0f / 6 + x * (1.0f / 24 + x * (1.0f / 120 + x * (1.0f / 720))))));
-  return d < 0.25f ? series : exp2_hw(d) - 1.0f;
-}
-
-// Residual weight max(0, p_v - q_v) = q_v * max(0, 2^d - 1), d = log2(p_v / q_v)
-// evaluated in fp64 so that p ~ q does not cancel.
+// Residual weight max(0, p_v - q_v), branch-free.  d = log2(p_v / q_v) is
+// formed in fp64 from the exact difference zp - zq, so p ~ q does not cancel:
+// below d = 1/4 the weight is q_v (2^d - 1) with 2^d - 1 = expm1(d ln 2) from
+// its Taylor series (relative truncation error < 1e-8); above, p_v - q_v
+// itself, where p_v > 1.18 q_v bounds the cancellation.  Both -inf gives a
+// NaN d and weight 0; zq = -inf alone gives d = +inf and weight p_v.
 __device__ __forceinline__ float residual_weight(float zq, float zp, const ProbScale& s) {
-  // zp - zq is exact in fp64, so identical rows give d = 0 exactly
-  const double d64 = fma((double)zp - (double)zq, s.c, -s.dl);
-  const float d = (float)d64;
-  if (!(d > 0.0f)) return 0.0f;  // p <= q, or both -inf
-  if (zq == -__builtin_huge_valf()) return prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
-  return prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo) * exp2m1_pos(d);
+  const float d = (float)fma((double)zp - (double)zq, s.c, -s.dl);
+  const float pq = prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
+  const float pp = prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
+  const float x = d * 0.693147180559945309f;
+  const float em1 =
+      x * (1.0f + x * (0.5f + x * (1.0f / 6 + x * (1.0f / 24 + x * (1.0f / 120 + x * (1.0f / 720))))));
+  const float w = d < 0.25f ? pq * em1 : pp - pq;
+  return d > 0.0f ? w : 0.0f;
 }
 
 template <int KIND>
@@ -373,15 +475,36 @@ __device__ __forceinline__ int defer_rule(int rule, double alpha, double maxq, d
 }
 
 // ------------------------------------------------------------- row merge
-// One wavefront merges the nt tile partials of row r (fixed order: lanes take
-// tiles lane, lane+64, ...; a butterfly combines the lanes), adding the TV
+// The first 64 tile partials of row r (lane l holds tile l) and their TV
+// partials: the loads of a merge, issued ahead of it.
+struct PartHead {
+  TilePart t;
+  double tv;
+};
+
+__device__ __forceinline__ PartHead load_head(const Params& P, int r, bool tv) {
+  const int lane = threadIdx.x & 63;
+  PartHead h{{0.0, 0.0, kNegInf, kNegInf, kNegInf, kNegInf, 0x7fffffff, 0x7fffffff}, 0.0};
+  if (lane < P.nt) {
+    h.t = P.tiles[(int64_t)r * P.nt + lane];
+    if (tv) h.tv = P.tvpart[(int64_t)r * P.nt + lane];
+  }
+  return h;
+}
+
+// One wavefront merges the nt tile partials of row r in a fixed order (lane l
+// takes tiles l, l + 64, ...; butterflies combine the lanes), adding the TV
 // partials when `tv`.  Every lane returns the same RowStat.
-__device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy, bool tv) {
+__device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy, bool tv,
+                                             const PartHead& h) {
   const int lane = threadIdx.x & 63;
   const int nt = P.nt;
   const TilePart* t = P.tiles + (int64_t)r * nt;
-  float zq = kNegInf, zp = kNegInf, rq = kNegInf, rp = kNegInf;
-  for (int k = lane; k < nt; k += 64) {
+  const double* tvp = P.tvpart + (int64_t)r * nt;
+  const TilePart& t0 = h.t;
+  double tvs = h.tv;
+  float zq = t0.zmax_q, zp = t0.zmax_p, rq = t0.r_q, rp = t0.r_p;
+  for (int k = lane + 64; k < nt; k += 64) {
     zq = fmaxf(zq, t[k].zmax_q);
     zp = fmaxf(zp, t[k].zmax_p);
     rq = fmaxf(rq, t[k].r_q);
@@ -391,17 +514,21 @@ __device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy
   zp = wave_max(zp);
   rq = wave_max(rq);
   rp = wave_max(rp);
-  double sq = 0.0, sp = 0.0, tvs = 0.0;
+  double sq = 0.0, sp = 0.0;
   int aq = 0x7fffffff, ap = 0x7fffffff;
-  for (int k = lane; k < nt; k += 64) {
-    const TilePart tk = t[k];
-    if (tk.r_q != kNegInf) sq += tk.s_q * exp2((double)tk.r_q - (double)rq);
-    if (tk.r_p != kNegInf) sp += tk.s_p * exp2((double)tk.r_p - (double)rp);
+  auto add = [&](const TilePart& tk) {
+    // r_k - r is exact in fp64; an all -inf tile has s = 0
+    sq += tk.s_q * exp2_acc((double)tk.r_q - (double)rq);
+    sp += tk.s_p * exp2_acc((double)tk.r_p - (double)rp);
     if (greedy) {
       if (tk.zmax_q == zq) aq = min(aq, tk.amax_q);
       if (tk.zmax_p == zp) ap = min(ap, tk.amax_p);
     }
-    if (tv) tvs += P.tvpart[(int64_t)r * nt + k];
+  };
+  add(t0);
+  for (int k = lane + 64; k < nt; k += 64) {
+    add(t[k]);
+    if (tv) tvs += tvp[k];
   }
   sq = wave_sum(sq);
   sp = wave_sum(sp);
@@ -409,8 +536,8 @@ __device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy
   aq = wave_min(aq);
   ap = wave_min(ap);
   RowStat rs;
-  rs.lz_q = (double)rq + log2(sq);
-  rs.lz_p = (double)rp + log2(sp);
+  rs.lz_q = (double)rq + log2_acc(sq);
+  rs.lz_p = (double)rp + log2_acc(sp);
   rs.tv = tvs;
   rs.zmax_q = zq;
   rs.zmax_p = zp;
@@ -419,14 +546,47 @@ __device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy
   return rs;
 }
 
+__device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy, bool tv) {
+  return merge_row(P, r, greedy, tv, load_head(P, r, tv));
+}
+
 // ------------------------------------------------------------- decision
-// Wave 0: delta_j and the accept draws of one sequence from its merged rows,
-// j* (first-rejection search by one ballot), and the sampling state.  With
-// `write`, also the outputs that follow (every sampling workgroup of the
-// sequence computes the same decision; one writes it).
-template <int DT>
-__device__ __forceinline__ void decide(const Params& P, int b, const SeqParam& sp,
-                                       SeqShared& ss, bool write) {
+// delta_j by the rule of Table 1 and the accept draw a_j of Alg. 4 for row j
+// of a sequence, from its merged statistics.  x is the draft token x_{t+j},
+// zqx / zpx its two logits and u its uniform (lane-uniform values).
+__device__ __forceinline__ RowDecision decide_row(const SeqParam& sp, const RowStat& rs, int j,
+                                                  int gamma, int V, int x, float zqx, float zpx,
+                                                  float u) {
+  RowDecision d;
+  d.rs = rs;
+  d.u = u;
+  const double maxq = exp2_acc((double)rs.zmax_q * sp.c - rs.lz_q);
+  const double maxp = exp2_acc((double)rs.zmax_p * sp.c - rs.lz_p);
+  // greedy: one-hot q~, p~ give D_TV = 1(argmax q != argmax p)  (Lemma 6)
+  const double tv = sp.greedy ? (rs.amax_q != rs.amax_p ? 1.0 : 0.0) : rs.tv;
+  d.maxq = (float)maxq;
+  d.maxp = (float)maxp;
+  d.tv = (float)tv;
+  d.delta = defer_rule(sp.rule, sp.alpha, maxq, maxp, tv);
+  if (j >= gamma || x < 0 || x >= V) {
+    d.keep = 0;  // a_gamma = 0; a draft outside the vocabulary is rejected
+  } else if (sp.greedy) {
+    d.keep = (x == (d.delta ? rs.amax_p : rs.amax_q));
+  } else if (d.delta) {
+    // pi = p here: keep if p(x) >= q(x), else with probability p(x) / q(x)
+    const double lq = (double)zqx * sp.c - rs.lz_q;
+    const double lp = (double)zpx * sp.c - rs.lz_p;
+    d.keep = !(lp < lq) || (double)u < exp2_acc(lp - lq);
+  } else {
+    d.keep = 1;  // pi = q: accepted with probability 1
+  }
+  return d;
+}
+
+// Wave 0: j* (the first rejection, by one ballot), the outputs when `write`,
+// and the sampling state of sequence b.
+__device__ __forceinline__ void finish_seq(const Params& P, int b, const SeqParam& sp,
+                                           SeqShared& ss, bool write) {
   const int lane = threadIdx.x;
   const int gamma = P.gamma, g1 = gamma + 1;
   const bool on = lane < g1;
@@ -443,55 +603,33 @@ __device__ __forceinline__ void decide(const Params& P, int b, const SeqParam& s
     if (lane == 0) ss.seq = SeqState{-1, kNone, 0.0f, 0};
     return;
   }
-  int delta = 0, keep = 1;
-  RowStat rs{};
-  if (on) {
-    rs = ss.rows[lane];
-    const double maxq = exp2((double)rs.zmax_q * sp.c - rs.lz_q);
-    const double maxp = exp2((double)rs.zmax_p * sp.c - rs.lz_p);
-    // greedy: one-hot q~, p~ give D_TV = 1(argmax q != argmax p)  (Lemma 6)
-    const double tv = sp.greedy ? (rs.amax_q != rs.amax_p ? 1.0 : 0.0) : rs.tv;
-    delta = defer_rule(sp.rule, sp.alpha, maxq, maxp, tv);
-    if (lane < gamma) {
-      const int x = P.draft[(int64_t)b * gamma + lane];
-      if (x < 0 || x >= P.V) {
-        keep = 0;
-      } else if (sp.greedy) {
-        keep = (x == (delta ? rs.amax_p : rs.amax_q));
-      } else if (delta) {
-        // pi = p here; keep if p(x) >= q(x), else with probability p(x)/q(x)
-        const double lq = (double)load_logit<DT>(P.q, row, P.V, x) * sp.c - rs.lz_q;
-        const double lp = (double)load_logit<DT>(P.p, row, P.V, x) * sp.c - rs.lz_p;
-        if (lp < lq) keep = (double)P.uniforms[(int64_t)b * g1 + lane] < exp2(lp - lq);
-      }
-    } else {
-      keep = 0;  // a_gamma = 0
+  RowDecision d{};
+  if (on) d = ss.rows[lane];
+  if (write && on) {
+    P.out_defer[row] = (uint8_t)d.delta;
+    if (P.out_stats) {
+      const double T = sp.greedy ? 1.0 : kLog2e / sp.c;
+      float* o = P.out_stats + row * 8;
+      o[0] = (float)((double)d.rs.zmax_q / T);
+      o[1] = (float)(d.rs.lz_q * kLn2);
+      o[2] = d.maxq;
+      o[3] = (float)((double)d.rs.zmax_p / T);
+      o[4] = (float)(d.rs.lz_p * kLn2);
+      o[5] = d.maxp;
+      o[6] = d.tv;
+      o[7] = 0.0f;
     }
-    if (write) {
-      P.out_defer[row] = (uint8_t)delta;
-      if (P.out_stats) {
-        const double T = sp.greedy ? 1.0 : kLog2e / sp.c;
-        float* o = P.out_stats + row * 8;
-        o[0] = (float)((double)rs.zmax_q / T);
-        o[1] = (float)(rs.lz_q * kLn2);
-        o[2] = (float)maxq;
-        o[3] = (float)((double)rs.zmax_p / T);
-        o[4] = (float)(rs.lz_p * kLn2);
-        o[5] = (float)maxp;
-        o[6] = (float)tv;
-        o[7] = 0.0f;
-      }
-      if (P.out_argmax) {
-        P.out_argmax[row * 2 + 0] = rs.amax_q;
-        P.out_argmax[row * 2 + 1] = rs.amax_p;
-      }
+    if (P.out_argmax) {
+      P.out_argmax[row * 2 + 0] = d.rs.amax_q;
+      P.out_argmax[row * 2 + 1] = d.rs.amax_p;
     }
   }
-  const unsigned long long rej = __ballot(on && !keep);
+  const unsigned long long rej = __ballot(on && !d.keep);
   const int jstar = __ffsll(rej) - 1;  // bit gamma is always set
-  const int dstar = __shfl(delta, jstar, 64);
-  const int aq = __shfl(rs.amax_q, jstar, 64);
-  const int ap = __shfl(rs.amax_p, jstar, 64);
+  const int dstar = lane_i32(d.delta, jstar);
+  const int aq = lane_i32(d.rs.amax_q, jstar);
+  const int ap = lane_i32(d.rs.amax_p, jstar);
+  const float ug = lane_f32(d.u, gamma);
   if (lane == 0) {
     SeqState s{jstar, kNone, 0.0f, 0};
     if (sp.greedy) {
@@ -503,221 +641,310 @@ __device__ __forceinline__ void decide(const Params& P, int b, const SeqParam& s
       // a rejection with delta = 0 only happens for an out-of-range draft;
       // its residual max(0, q - q) is empty, so p is sampled instead
       s.kind = (jstar < gamma) ? (dstar ? kResidual : kP) : (dstar ? kP : kQ);
-      s.u = P.uniforms[(int64_t)b * g1 + gamma];
+      s.u = ug;
     }
     if (write) P.out_accept[b] = jstar;
     ss.seq = s;
   }
 }
 
-// Whole block: merge the rows of sequence b into ss.rows and decide it.
+// Whole block: merge and decide the rows of sequence b (wave w takes rows
+// w, w + 4, ...), then wave 0 finds j*.  With `write` the outputs are written
+// too: every sampling workgroup of a sequence reaches the same decision by
+// the same fixed-order computation, and one of them writes it.
 template <int DT>
-__device__ __forceinline__ void merge_and_decide(const Params& P, int b, const SeqParam& sp,
-                                                 SeqShared& ss, bool write) {
-  const int wv = threadIdx.x >> 6, g1 = P.gamma + 1;
-  const bool tv = needs_tv(sp);
+__device__ __forceinline__ void decide_seq(const Params& P, int b, const SeqParam& sp,
+                                           SeqShared& ss, bool write) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int gamma = P.gamma, g1 = gamma + 1, V = P.V;
   if (sp.valid) {
-    for (int j = wv; j < g1; j += kThreads / 64) {
-      const RowStat rs = merge_row(P, b * g1 + j, sp.greedy, tv);
-      if ((threadIdx.x & 63) == 0) ss.rows[j] = rs;
+    // lane l of wave wv fetches the draft data of row wv + kSampWaves * l up
+    // front, so that these loads overlap the merges
+    const int jl = wv + kSampWaves * lane;
+    int x = -1;
+    float zqx = 0.0f, zpx = 0.0f, u = 0.0f;
+    if (jl < g1) {
+      const int64_t row = (int64_t)b * g1 + jl;
+      if (!sp.greedy) u = P.uniforms[row];
+      if (jl < gamma) {
+        x = P.draft[(int64_t)b * gamma + jl];
+        if (!sp.greedy && x >= 0 && x < V) {
+          zqx = load_logit<DT>(P.q, row, V, x);
+          zpx = load_logit<DT>(P.p, row, V, x);
+        }
+      }
+    }
+    const bool tv = needs_tv(sp);
+    PartHead h{};
+    if (wv < g1) h = load_head(P, b * g1 + wv, tv);
+    for (int i = 0; wv + kSampWaves * i < g1; ++i) {
+      const int j = wv + kSampWaves * i;
+      // the next row's partials load while this row merges
+      PartHead hn{};
+      if (j + kSampWaves < g1) hn = load_head(P, b * g1 + j + kSampWaves, tv);
+      const RowStat rs = merge_row(P, b * g1 + j, sp.greedy, tv, h);
+      h = hn;
+      const RowDecision d = decide_row(sp, rs, j, gamma, V, lane_i32(x, i), lane_f32(zqx, i),
+                                       lane_f32(zpx, i), lane_f32(u, i));
+      if (lane == 0) ss.rows[j] = d;
     }
   }
   __syncthreads();
-  if (threadIdx.x < 64) decide<DT>(P, b, sp, ss, write);
+  if (threadIdx.x < 64) finish_seq(P, b, sp, ss, write);
   __syncthreads();
 }
 
 // ------------------------------------------------------------- sampling
-// Whole block: the mass of sampling tile k of a row under the sampled
-// distribution (valid in every thread).
-template <int DT, bool VEC, int KIND>
-__device__ __forceinline__ double block_tile_mass(const char* qrow, const char* prow, int V,
-                                                  int k, const ProbScale& ps, Shared& sh) {
-  using T = SampTile<DT, VEC>;
-  const int64_t t0 = (int64_t)k * T::N;
-  uint32_t wq[T::U][T::NW] = {}, wp[T::U][T::NW] = {};
-  if (KIND != kP) load_tile<DT, VEC, T::U, false, false>(qrow, t0, V, wq);
-  if (KIND != kQ) load_tile<DT, VEC, T::U, false, false>(prow, t0, V, wp);
-  double acc = 0.0;
-#pragma unroll
-  for (int i = 0; i < T::U; ++i) {
-    float t = 0.0f;
-#pragma unroll
-    for (int e = 0; e < T::VW; ++e)
-      t += weight_of<KIND>(elem<DT, VEC>(wq[i], e), elem<DT, VEC>(wp[i], e), ps);
-    acc += (double)t;
-  }
-  double unused = 0.0;
-  block_sum2(acc, unused, sh);
-  return acc;
-}
-
-// The in-tile part of the draw: each thread takes U consecutive lane loads of
-// tile pk.k, one block-wide scan of the per-thread masses finds the thread,
-// and that thread walks its entries.
-template <int DT, bool VEC, int KIND>
-__device__ __forceinline__ void pick_in_tile(const Params& P, int b, int row, const PickState& pk,
-                                             const ProbScale& ps, Shared& sh) {
-  using T = SampTile<DT, VEC>;
-  const int tid = threadIdx.x;
-  const int V = P.V;
-  const char* qrow = (const char*)P.q + (int64_t)row * V * T::EB;
-  const char* prow = (const char*)P.p + (int64_t)row * V * T::EB;
-  const int64_t t0 = (int64_t)pk.k * T::N;
-  uint32_t wq[T::U][T::NW] = {}, wp[T::U][T::NW] = {};
-  if (KIND != kP) load_tile<DT, VEC, T::U, true, false>(qrow, t0, V, wq);
-  if (KIND != kQ) load_tile<DT, VEC, T::U, true, false>(prow, t0, V, wp);
-  // per lane-load masses, in entry order
-  double slot_mass[T::U];
-  double tsum = 0.0;
-  int last_pos = -1;
-#pragma unroll
-  for (int i = 0; i < T::U; ++i) {
-    double m = 0.0;
-#pragma unroll
-    for (int e = 0; e < T::VW; ++e) {
-      const float w = weight_of<KIND>(elem<DT, VEC>(wq[i], e), elem<DT, VEC>(wp[i], e), ps);
-      m += (double)w;
-      if (w > 0.0f) last_pos = (int)entry_of<DT, VEC, T::U, true>(t0, i, e);
-    }
-    slot_mass[i] = m;
-    tsum += m;
-  }
-  double total;
-  const double incl = block_incl_scan(tsum, sh, &total);
-  if (total > pk.rem) {  // block-uniform
-    int cand = (incl > pk.rem) ? tid : 0x7fffffff, unused = 0;
-    block_min2(cand, unused, sh);
-    if (tid == cand) {
-      // the lane load where the running mass crosses, then its entries
-      double run = incl - tsum, before = 0.0;
-      int islot = -1;
-#pragma unroll
-      for (int i = 0; i < T::U; ++i) {
-        if (islot < 0 && run + slot_mass[i] > pk.rem) {
-          islot = i;
-          before = run;
-        }
-        run += slot_mass[i];
-      }
-      int hit = -1;
-      if (islot >= 0) {
-        uint32_t sq[T::NW] = {}, sp_[T::NW] = {};
-#pragma unroll
-        for (int i = 0; i < T::U; ++i)
-          if (i == islot)
-#pragma unroll
-            for (int j = 0; j < T::NW; ++j) {
-              sq[j] = wq[i][j];
-              sp_[j] = wp[i][j];
-            }
-        run = before;
-        int lastw = -1;
-        const int64_t base = entry_of<DT, VEC, T::U, true>(t0, islot, 0);
-#pragma unroll
-        for (int e = 0; e < T::VW; ++e) {
-          const float w = weight_of<KIND>(elem<DT, VEC>(sq, e), elem<DT, VEC>(sp_, e), ps);
-          run += (double)w;
-          if (w > 0.0f) lastw = (int)(base + e);
-          if (hit < 0 && run > pk.rem && w > 0.0f) hit = (int)(base + e);
-        }
-        if (hit < 0) hit = lastw;  // rounding inside the lane load
-      }
-      // rounding inside the thread: its last entry with mass
-      P.out_token[b] = hit >= 0 ? hit : last_pos;
-    }
-    return;
-  }
-  // rounding: no thread reached u*W; take the last entry of the tile with mass
-  int lp = -last_pos, unused = 0;
-  block_min2(lp, unused, sh);
-  if (tid == 0) P.out_token[b] = -lp;
-}
-
-// Wave 0 gathers the K tile masses of sequence b (into LDS when they fit);
-// returns their total W to the whole block.
-__device__ __forceinline__ double gather_masses(const Params& P, int b, SeqShared& ss,
-                                                Shared& sh) {
-  const int lane = threadIdx.x & 63, K = P.K;
-  __syncthreads();
-  if (threadIdx.x < 64) {
-    double W = 0.0;
-    for (int k0 = 0; k0 < K; k0 += 64) {
-      const int k = k0 + lane;
-      const double m = (k < K) ? ld_dev_f64(P.masses + (int64_t)b * K + k) : 0.0;
-      if (k < K && k < kPickLds) ss.mass[k] = m;
-      W += wave_sum(m);
-    }
-    if (lane == 0) sh.d[0][0] = W;
-  }
-  __syncthreads();
-  return sh.d[0][0];
-}
-
-// Whole block: inverse-CDF draw at row j* of sequence b -- the smallest entry
-// k with C_k > u * W, C the running mass in vocabulary order and W the total.
-// Wave 0 scans the tile masses (64 at a time) to find the tile, then
-// pick_in_tile finds the entry.
+// A chunk is the quarter of a tile that one wavefront covers when the tile is
+// read wave-contiguously: chunk c of tile k starts at entry k * TileN +
+// c * ChunkN, and lane l's lane load i covers entries (i * 64 + l) * VW ..
+// + VW - 1 of it.
 template <int DT, bool VEC>
-__device__ __forceinline__ void pick(const Params& P, int b, const SeqParam& sp, SeqShared& ss,
-                                     Shared& sh) {
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int K = P.K;
-  const SeqState s = ss.seq;
-  const int row = b * (P.gamma + 1) + s.row;
-  const ProbScale ps = prob_scale(sp, ss.rows[s.row]);
-  int kind = s.kind;
-  double W = gather_masses(P, b, ss, sh);
-  if (kind == kResidual && !(W > 0.0)) {
-    // empty residual (possible only through rounding): sample p instead
-    kind = kP;
-    const int V = P.V;
-    const char* qrow = (const char*)P.q + (int64_t)row * V * SampTile<DT, VEC>::EB;
-    const char* prow = (const char*)P.p + (int64_t)row * V * SampTile<DT, VEC>::EB;
-    for (int k = 0; k < K; ++k) {
-      const double m = block_tile_mass<DT, VEC, kP>(qrow, prow, V, k, ps, sh);
-      if (tid == 0) st_dev_f64(P.masses + (int64_t)b * K + k, m);
-    }
-    if (tid == 0) vmem_drain();
-    W = gather_masses(P, b, ss, sh);
+struct Chunk {
+  using T = StatTile<DT, VEC>;
+  static constexpr int U = T::U, NW = T::NW, VW = T::VW;
+  static constexpr int N = 64 * U * VW;  // entries per chunk
+};
+template <int DT, bool VEC>
+using ChunkRegs = uint32_t[Chunk<DT, VEC>::U][Chunk<DT, VEC>::NW];
+
+// Lane loads of the chunk starting at entry c0 of a row (V entries); a chunk
+// past the row reads entry 0 and masks everything.
+template <int DT, bool VEC>
+__device__ __forceinline__ void load_chunk(const char* row, int64_t c0, int V,
+                                           ChunkRegs<DT, VEC>& w) {
+  const bool live = c0 < V;
+  load_tile<DT, VEC, Chunk<DT, VEC>::U, false, false, 64>(row, live ? c0 : 0, live ? V : 0, w,
+                                                          threadIdx.x & 63);
+}
+
+// Sources of the part masses of the sampled distribution: the statistics
+// partials per tile (q or p: each tile's share of the normaliser), the TV
+// partials per tile (the residual of an OPT row, which the TV pass summed),
+// or the residual masses per chunk computed by the sampling pass.
+enum MassSrc : int { kSrcStatsQ = 0, kSrcStatsP = 1, kSrcTv = 2, kSrcPass = 3 };
+
+template <int SRC>
+__device__ __forceinline__ double part_mass(const Params& P, int64_t row, int b, int k,
+                                            const RowStat& rs) {
+  if constexpr (SRC == kSrcStatsQ) {
+    const TilePart& t = P.tiles[row * P.nt + k];
+    return t.s_q * exp2_acc((double)t.r_q - rs.lz_q);
+  } else if constexpr (SRC == kSrcStatsP) {
+    const TilePart& t = P.tiles[row * P.nt + k];
+    return t.s_p * exp2_acc((double)t.r_p - rs.lz_p);
+  } else if constexpr (SRC == kSrcTv) {
+    return P.tvpart[row * P.nt + k];
+  } else {
+    return ld_dev_f64(P.masses + ((int64_t)b * P.nt) * kChunksPerTile + k);
   }
-  if (tid < 64) {
-    const double target = (double)s.u * W;
-    double carry = 0.0, rem = 0.0;
-    int ks = -1, klast = -1;
-    for (int k0 = 0; k0 < K; k0 += 64) {
-      const int k = k0 + lane;
-      const double m = (k >= K) ? 0.0
-                       : (k < kPickLds) ? ss.mass[k] : ld_dev_f64(P.masses + (int64_t)b * K + k);
-      const double incl = carry + wave_incl_scan(m);
-      const unsigned long long pos = __ballot(m > 0.0);
-      const unsigned long long hit = __ballot(m > 0.0 && incl > target);
-      if (pos) klast = k0 + 63 - __clzll(pos);
-      if (ks < 0 && hit) {
-        const int l = __ffsll(hit) - 1;
-        ks = k0 + l;
-        rem = target - (__shfl(incl, l, 64) - __shfl(m, l, 64));
+}
+
+// Wave 0: the part (tile or chunk) of the inverse-CDF draw -- the first part
+// k with C_k > u W, C_k the running mass through part k in vocabulary order
+// and W the total -- and the target mass left at its start.  Returns W.
+template <int SRC>
+__device__ __forceinline__ double find_part(const Params& P, int64_t row, int b, int K,
+                                            const RowStat& rs, float u, int* ks_out,
+                                            double* rem_out) {
+  const int lane = threadIdx.x & 63;
+  const double m0 = lane < K ? part_mass<SRC>(P, row, b, lane, rs) : 0.0;
+  double W = wave_sum(m0);
+  for (int k0 = 64; k0 < K; k0 += 64) {
+    const int k = k0 + lane;
+    W += wave_sum(k < K ? part_mass<SRC>(P, row, b, k, rs) : 0.0);
+  }
+  const double target = (double)u * W;
+  double carry = 0.0, rem = 0.0;
+  int ks = -1, klast = -1;
+  for (int k0 = 0; k0 < K; k0 += 64) {
+    const int k = k0 + lane;
+    const double m = k0 == 0 ? m0 : k < K ? part_mass<SRC>(P, row, b, k, rs) : 0.0;
+    const double incl = carry + wave_incl_scan(m);
+    const unsigned long long pos = __ballot(m > 0.0);
+    const unsigned long long hit = __ballot(m > 0.0 && incl > target);
+    if (pos) klast = k0 + 63 - __clzll(pos);
+    if (ks < 0 && hit) {
+      const int l = __ffsll(hit) - 1;
+      ks = k0 + l;
+      rem = target - (lane_f64(incl, l) - lane_f64(m, l));
+    }
+    carry = lane_f64(incl, 63);
+  }
+  if (ks < 0) {  // rounding left u W at or past the end: the last part with mass
+    ks = klast;
+    rem = __builtin_huge_val();
+  }
+  *ks_out = ks;
+  *rem_out = rem;
+  return W;
+}
+
+// Whole block: residual masses max(0, p - q) of the chunks of tiles kw,
+// kw + K, ... of a row (K sampling workgroups per sequence).  The block's
+// wavefronts take the chunks of kSampBatch tiles per batch, one chunk each,
+// and the next batch loads while this one is summed; chunk c's mass goes to
+// masses[c].  No block barrier: every wave drains its own stores.
+template <int DT, bool VEC>
+__device__ __forceinline__ void residual_masses(const char* qrow, const char* prow, int V, int nt,
+                                                int K, int kw, const ProbScale& ps,
+                                                double* masses) {
+  using C = Chunk<DT, VEC>;
+  constexpr int TN = StatTile<DT, VEC>::N;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int sub = wv / kChunksPerTile, quarter = wv % kChunksPerTile;
+  const int step = K * kSampBatch;
+  ChunkRegs<DT, VEC> wq, wp, nq = {}, np = {};
+  {
+    const int k = kw + sub * K;
+    const int64_t c0 = k < nt ? (int64_t)k * TN + quarter * C::N : (int64_t)V;
+    load_chunk<DT, VEC>(qrow, c0, V, wq);
+    load_chunk<DT, VEC>(prow, c0, V, wp);
+  }
+  for (int k0 = kw; k0 < nt; k0 += step) {
+    if (k0 + step < nt) {  // block-uniform: prefetch the next batch
+      const int k = k0 + step + sub * K;
+      const int64_t c0 = k < nt ? (int64_t)k * TN + quarter * C::N : (int64_t)V;
+      load_chunk<DT, VEC>(qrow, c0, V, nq);
+      load_chunk<DT, VEC>(prow, c0, V, np);
+    }
+    double acc = 0.0;
+#pragma unroll
+    for (int i = 0; i < C::U; ++i) {
+      float t = 0.0f;
+#pragma unroll
+      for (int e = 0; e < C::VW; ++e)
+        t += residual_weight(elem<DT, VEC>(wq[i], e), elem<DT, VEC>(wp[i], e), ps);
+      acc += (double)t;
+    }
+    acc = wave_sum(acc);
+    const int k = k0 + sub * K;
+    if (lane == 0 && k < nt) st_dev_f64(masses + (int64_t)k * kChunksPerTile + quarter, acc);
+#pragma unroll
+    for (int i = 0; i < C::U; ++i)
+#pragma unroll
+      for (int j = 0; j < C::NW; ++j) {
+        wq[i][j] = nq[i][j];
+        wp[i][j] = np[i][j];
       }
-      carry = __shfl(incl, 63, 64);
-    }
-    if (ks < 0) {  // rounding left u*W at or past the end: last entry with mass
-      ks = klast;
-      rem = __builtin_huge_val();
-    }
-    if (lane == 0) {
-      ss.pk = PickState{ks, kind, rem};
-      if (P.out_norm) P.out_norm[b] = (float)W;
-    }
   }
-  __syncthreads();
-  const PickState pk = ss.pk;
-  if (pk.k < 0) {
-    if (tid == 0) P.out_token[b] = -1;
+  vmem_drain();
+}
+
+// Wave 0: the in-part draw over NCH consecutive chunks from entry c0 (a
+// whole tile when NCH = kChunksPerTile, one chunk when 1).  Lane loads are
+// scanned in entry order -- chunk, then lane load i, then lane -- for the
+// first one where the running mass exceeds rem; its lane then walks its VW
+// entries.  The next chunk loads while one is scanned.  Rounding that leaves
+// rem unreached takes the last entry with mass.
+template <int DT, bool VEC, int NCH, int KIND>
+__device__ __forceinline__ void pick_wave(const Params& P, int b, int64_t row, int64_t c0,
+                                          double rem, const ProbScale& ps) {
+  using C = Chunk<DT, VEC>;
+  constexpr int EB = StatTile<DT, VEC>::EB;
+  const int lane = threadIdx.x & 63;
+  const int V = P.V;
+  const char* qrow = (const char*)P.q + row * V * EB;
+  const char* prow = (const char*)P.p + row * V * EB;
+  ChunkRegs<DT, VEC> cq = {}, cp = {}, nq = {}, np = {};
+  if (KIND != kP) load_chunk<DT, VEC>(qrow, c0, V, cq);
+  if (KIND != kQ) load_chunk<DT, VEC>(prow, c0, V, cp);
+  double carry = 0.0, before = 0.0;
+  int hlane = -1, last_pos = -1;
+  int64_t hbase = 0;
+  uint32_t sq[C::NW] = {}, sp_[C::NW] = {};
+  for (int c = 0; c < NCH && hlane < 0; ++c) {
+    if (c + 1 < NCH) {
+      if (KIND != kP) load_chunk<DT, VEC>(qrow, c0 + (c + 1) * C::N, V, nq);
+      if (KIND != kQ) load_chunk<DT, VEC>(prow, c0 + (c + 1) * C::N, V, np);
+    }
+#pragma unroll
+    for (int i = 0; i < C::U; ++i) {
+      const int64_t base = c0 + c * C::N + (int64_t)(i * 64 + lane) * C::VW;
+      double m = 0.0;
+#pragma unroll
+      for (int e = 0; e < C::VW; ++e) {
+        const float w = weight_of<KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
+        m += (double)w;
+        if (w > 0.0f) last_pos = max(last_pos, (int)(base + e));
+      }
+      const double incl = carry + wave_incl_scan(m);
+      if (hlane < 0) {  // wave-uniform
+        const unsigned long long hit = __ballot(m > 0.0 && incl > rem);
+        if (hit) {
+          hlane = __ffsll(hit) - 1;
+          before = lane_f64(incl, hlane) - lane_f64(m, hlane);
+          hbase = base;
+#pragma unroll
+          for (int j = 0; j < C::NW; ++j) {
+            sq[j] = cq[i][j];
+            sp_[j] = cp[i][j];
+          }
+        }
+      }
+      carry = lane_f64(incl, 63);
+    }
+#pragma unroll
+    for (int i = 0; i < C::U; ++i)
+#pragma unroll
+      for (int j = 0; j < C::NW; ++j) {
+        cq[i][j] = nq[i][j];
+        cp[i][j] = np[i][j];
+      }
+  }
+  if (hlane < 0) {
+    const int lp = -wave_min(-last_pos);
+    if (lane == 0) P.out_token[b] = lp;
     return;
   }
-  if (pk.kind == kQ) pick_in_tile<DT, VEC, kQ>(P, b, row, pk, ps, sh);
-  else if (pk.kind == kP) pick_in_tile<DT, VEC, kP>(P, b, row, pk, ps, sh);
-  else pick_in_tile<DT, VEC, kResidual>(P, b, row, pk, ps, sh);
+  if (lane != hlane) return;
+  double run = before;
+  int hit = -1, lastw = -1;
+#pragma unroll
+  for (int e = 0; e < C::VW; ++e) {
+    const float w = weight_of<KIND>(elem<DT, VEC>(sq, e), elem<DT, VEC>(sp_, e), ps);
+    run += (double)w;
+    if (w > 0.0f) lastw = (int)(hbase + e);
+    if (hit < 0 && run > rem && w > 0.0f) hit = (int)(hbase + e);
+  }
+  P.out_token[b] = hit >= 0 ? hit : lastw;  // rounding inside the lane load
+}
+
+// Wave 0: the inverse-CDF draw of sequence b at row `row` (the row of j*)
+// from the distribution `kind`, whose part masses come from `src`.  An empty
+// residual (possible only through rounding) is replaced by p.
+template <int DT, bool VEC>
+__device__ __forceinline__ void draw(const Params& P, int b, int64_t row, int kind, int src,
+                                     float u, const SeqParam& sp, const RowStat& rs) {
+  int ks;
+  double rem, W;
+  if (src == kSrcStatsQ) W = find_part<kSrcStatsQ>(P, row, b, P.nt, rs, u, &ks, &rem);
+  else if (src == kSrcStatsP) W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
+  else if (src == kSrcTv) W = find_part<kSrcTv>(P, row, b, P.nt, rs, u, &ks, &rem);
+  else W = find_part<kSrcPass>(P, row, b, P.nt * kChunksPerTile, rs, u, &ks, &rem);
+  if (kind == kResidual && !(W > 0.0)) {
+    kind = kP;
+    src = kSrcStatsP;
+    W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
+  }
+  const int lane = threadIdx.x & 63;
+  if (lane == 0 && P.out_norm) P.out_norm[b] = (float)W;
+  if (ks < 0) {
+    if (lane == 0) P.out_token[b] = -1;
+    return;
+  }
+  const ProbScale ps = prob_scale(sp, rs);
+  constexpr int TN = StatTile<DT, VEC>::N, CN = Chunk<DT, VEC>::N;
+  if (src == kSrcPass) {
+    const int64_t c0 = (int64_t)(ks / kChunksPerTile) * TN + (ks % kChunksPerTile) * CN;
+    pick_wave<DT, VEC, 1, kResidual>(P, b, row, c0, rem, ps);
+  } else if (kind == kQ) {
+    pick_wave<DT, VEC, kChunksPerTile, kQ>(P, b, row, (int64_t)ks * TN, rem, ps);
+  } else if (kind == kP) {
+    pick_wave<DT, VEC, kChunksPerTile, kP>(P, b, row, (int64_t)ks * TN, rem, ps);
+  } else {
+    pick_wave<DT, VEC, kChunksPerTile, kResidual>(P, b, row, (int64_t)ks * TN, rem, ps);
+  }
 }
 
 // ================================================================ kernels
@@ -738,8 +965,8 @@ __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
   const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
   const int64_t t0 = (int64_t)k * T::N;
   uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
-  load_tile<DT, VEC, T::U, false, true>(qrow, t0, V, wq);
-  load_tile<DT, VEC, T::U, false, true>(prow, t0, V, wp);
+  load_tile<DT, VEC, T::U, false, true>(qrow, t0, V, wq, threadIdx.x);
+  load_tile<DT, VEC, T::U, false, true>(prow, t0, V, wp, threadIdx.x);
 
   float mq = kNegInf, mp = kNegInf;
 #pragma unroll
@@ -756,7 +983,7 @@ __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
     for (int i = 0; i < T::U; ++i)
 #pragma unroll
       for (int e = 0; e < T::VW; ++e) {
-        const int idx = (int)entry_of<DT, VEC, T::U, false>(t0, i, e);
+        const int idx = (int)entry_of<DT, VEC, T::U, false>(t0, i, e, threadIdx.x);
         if (iq == 0x7fffffff && elem<DT, VEC>(wq[i], e) == mq) iq = idx;
         if (ip == 0x7fffffff && elem<DT, VEC>(wp[i], e) == mp) ip = idx;
       }
@@ -786,8 +1013,9 @@ __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
   float Mq = mq, Mp = mp;
   block_max2(Mq, Mp, sh);
   const float Rq = Mq * sp.c_hi, Rp = Mp * sp.c_hi;
-  double dq = (mq == kNegInf) ? 0.0 : (double)sq * (double)exp2_hw(rq - Rq);
-  double dp = (mp == kNegInf) ? 0.0 : (double)spp * (double)exp2_hw(rp - Rp);
+  // rq - Rq is exact in fp64; only its rounding to float is inexact
+  double dq = (mq == kNegInf) ? 0.0 : (double)sq * (double)exp2_hw((float)((double)rq - (double)Rq));
+  double dp = (mp == kNegInf) ? 0.0 : (double)spp * (double)exp2_hw((float)((double)rp - (double)Rp));
   block_sum2(dq, dp, sh);
   if constexpr (ARGMAX) {
     iq = (mq == Mq) ? iq : 0x7fffffff;
@@ -825,8 +1053,8 @@ __global__ __launch_bounds__(kThreads) void k_tv(Params P) {
   const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
   const int64_t t0 = (int64_t)k * T::N;
   uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
-  load_tile<DT, VEC, T::U, false, true>(qrow, t0, V, wq);
-  load_tile<DT, VEC, T::U, false, true>(prow, t0, V, wp);
+  load_tile<DT, VEC, T::U, false, true>(qrow, t0, V, wq, threadIdx.x);
+  load_tile<DT, VEC, T::U, false, true>(prow, t0, V, wp, threadIdx.x);
   if (threadIdx.x < 64) {
     const RowStat rs = merge_row(P, r, false, false);
     if (threadIdx.x == 0) srow = rs;
@@ -847,31 +1075,38 @@ __global__ __launch_bounds__(kThreads) void k_tv(Params P) {
   if (threadIdx.x == 0) P.tvpart[(int64_t)r * P.nt + k] = acc;
 }
 
-// Sampling pass.  grid (K, B): every workgroup of sequence b merges the
-// sequence's rows and decides it (workgroup 0 writes the outputs); sampling
-// tile k of row j* then computes its mass and the last tile to finish draws.
+// Sampling pass.  grid (K, B) of 1024-thread workgroups: every workgroup of
+// sequence b merges the sequence's rows and decides it (workgroup 0 writes
+// the outputs).  A replacement drawn from the residual of a non-OPT row needs
+// that row's residual masses: the K workgroups sum them chunk by chunk, and
+// the last to finish draws.  Every other draw -- the extra token from q or p,
+// or an OPT residual, whose per-tile masses the earlier passes left -- is
+// made by workgroup 0 alone.  Draws run in one wavefront.
 template <int DT, bool VEC>
-__global__ __launch_bounds__(kThreads) void k_sample(Params P) {
-  __shared__ Shared sh;
+__global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
+  __shared__ SampShared sh;
   __shared__ SeqShared ss;
   const int k = blockIdx.x, b = blockIdx.y;
   const SeqParam sp = seq_param(P, b);
-  merge_and_decide<DT>(P, b, sp, ss, k == 0);
+  decide_seq<DT>(P, b, sp, ss, k == 0);
   const SeqState s = ss.seq;
   if (s.kind == kNone) return;  // block-uniform
-  const int row = b * (P.gamma + 1) + s.row;
-  const ProbScale ps = prob_scale(sp, ss.rows[s.row]);
-  const int V = P.V;
-  constexpr int EB = SampTile<DT, VEC>::EB;
-  const char* qrow = (const char*)P.q + (int64_t)row * V * EB;
-  const char* prow = (const char*)P.p + (int64_t)row * V * EB;
-  double m;
-  if (s.kind == kQ) m = block_tile_mass<DT, VEC, kQ>(qrow, prow, V, k, ps, sh);
-  else if (s.kind == kP) m = block_tile_mass<DT, VEC, kP>(qrow, prow, V, k, ps, sh);
-  else m = block_tile_mass<DT, VEC, kResidual>(qrow, prow, V, k, ps, sh);
-  if (threadIdx.x == 0) st_dev_f64(P.masses + (int64_t)b * P.K + k, m);
+  const int64_t row = (int64_t)b * (P.gamma + 1) + s.row;
+  const RowStat rs = ss.rows[s.row].rs;
+  if (s.kind != kResidual || needs_tv(sp)) {
+    if (k != 0 || threadIdx.x >= 64) return;
+    const int src = s.kind == kQ ? kSrcStatsQ : s.kind == kP ? kSrcStatsP : kSrcTv;
+    draw<DT, VEC>(P, b, row, s.kind, src, s.u, sp, rs);
+    return;
+  }
+  constexpr int EB = StatTile<DT, VEC>::EB;
+  const ProbScale ps = prob_scale(sp, rs);
+  const char* qrow = (const char*)P.q + row * P.V * EB;
+  const char* prow = (const char*)P.p + row * P.V * EB;
+  residual_masses<DT, VEC>(qrow, prow, P.V, P.nt, P.K, k, ps,
+                           P.masses + ((int64_t)b * P.nt) * kChunksPerTile);
   if (!arrive_last(P.samp_cnt + b, (uint32_t)P.K, sh)) return;
-  pick<DT, VEC>(P, b, sp, ss, sh);
+  if (threadIdx.x < 64) draw<DT, VEC>(P, b, row, kResidual, kSrcPass, s.u, sp, rs);
 }
 
 template <int DT, bool VEC>
@@ -891,7 +1126,7 @@ hipError_t launch_t(const Params& P, bool need_tv, bool need_sample, bool need_a
     if ((err = hipGetLastError()) != hipSuccess) return err;
   }
   // a batch with no sequence at temperature > 0 only needs the decisions
-  hipLaunchKernelGGL((k_sample<DT, VEC>), dim3(need_sample ? P.K : 1, P.B), dim3(kThreads), 0,
+  hipLaunchKernelGGL((k_sample<DT, VEC>), dim3(need_sample ? P.K : 1, P.B), dim3(kSampThreads), 0,
                      st, P);
   return hipGetLastError();
 }
@@ -903,10 +1138,7 @@ int stat_tile_elems(int dtype, bool vec) {
   return vec ? StatTile<0, true>::N : StatTile<0, false>::N;
 }
 
-int samp_tile_elems(int dtype, bool vec) {
-  if (dtype == 1) return vec ? SampTile<1, true>::N : SampTile<1, false>::N;
-  return vec ? SampTile<0, true>::N : SampTile<0, false>::N;
-}
+int samp_groups(int64_t nt) { return (int)((nt + 2 * kSampBatch - 1) / (2 * kSampBatch)); }
 
 hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
                          bool need_argmax, hipEvent_t e0, hipEvent_t e1, hipStream_t st) {
