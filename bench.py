@@ -1,6 +1,8 @@
 """Throughput of the speculative-cascade verify step on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--sets S] [--no-cpu-baseline]
+                    [--copy-calib-mb N]
+    python bench.py --traffic-from FETCH.csv WRITE.csv --copy-calib-mb N
 
 A step is one spc_verify call (statistics pass + residual sampling pass) on
 the Gemma-vocabulary workload: B=32 sequences, gamma=7 drafted positions,
@@ -11,11 +13,24 @@ Infinity Cache cannot serve a repeat.
 
 Prints one JSON line: verified positions/s (B*gamma per step) for the whole
 path, plus the statistics kernel's roofline (algorithmic logit bytes / its
-mean duration, from HIP events recorded around it on the launch stream) and
-the fp64 oracle's throughput on the host cores (reported baseline).
+mean duration, from HIP events recorded around it on the launch stream on
+every EVERY-th step of the timed region -- an event pair costs a few
+microseconds of step time, so not every step carries one) and the fp64
+oracle's throughput on the host cores (reported baseline).  Step-time
+percentiles come from the spacing of those events (EVERY-step windows).
+
+HBM traffic of the statistics kernel comes from two rocprofv3 counter runs of
+this script (FETCH_SIZE, then WRITE_SIZE) with --copy-calib-mb, which first
+runs an elementwise float32 negation of N MiB (reads N MiB, writes N MiB):
+each counter is scaled by the ratio of the copy's known bytes to what the same
+counter reads for it.  --traffic-from reduces the two counter tables to one
+record, stored in profiles/ with the sha256 of the kernel source; the
+benchmark line reports it only while that source is unchanged.
 """
 import argparse
+import csv
 import ctypes
+import hashlib
 import json
 import os
 import sys
@@ -25,6 +40,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, published
+KERNEL_SRC = os.path.join(ROOT, "paper_2405_19261_amd", "csrc", "spc_kernels.hip")
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_stats_gemma-vocab_b32_g7_traffic.txt")
+COPY_KERNEL_TAG = "neg_kernel"  # the calibration copy is torch.neg
 
 
 class HipEvents:
@@ -53,6 +71,64 @@ class HipEvents:
 
     def destroy(self, e):
         self.hip.hipEventDestroy(ctypes.c_void_p(e))
+
+
+def kernel_sha256():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def per_dispatch_kib(path, counter, tag):
+    """Mean counter value (KiB) per dispatch of kernels whose name holds tag."""
+    vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(path))
+            if r["Counter_Name"] == counter and tag in r["Kernel_Name"]]
+    if not vals:
+        raise SystemExit(f"no {counter} rows for kernels matching {tag!r} in {path}")
+    return sum(vals) / len(vals), len(vals)
+
+
+def traffic_record(fetch_csv, write_csv, copy_mb):
+    """HBM bytes per statistics-kernel launch from the two counter tables."""
+    copy_bytes = copy_mb * 2 ** 20
+    f_copy, n_fc = per_dispatch_kib(fetch_csv, "FETCH_SIZE", COPY_KERNEL_TAG)
+    w_copy, n_wc = per_dispatch_kib(write_csv, "WRITE_SIZE", COPY_KERNEL_TAG)
+    f_k, n_fk = per_dispatch_kib(fetch_csv, "FETCH_SIZE", "k_stats")
+    w_k, n_wk = per_dispatch_kib(write_csv, "WRITE_SIZE", "k_stats")
+    fetch_scale = copy_bytes / (f_copy * 1024.0)
+    write_scale = copy_bytes / (w_copy * 1024.0)
+    fetch_b = f_k * 1024.0 * fetch_scale
+    write_b = w_k * 1024.0 * write_scale
+    return dict(kernel="k_stats", kernel_src_sha256=kernel_sha256(), copy_mib=copy_mb,
+                copy_fetch_kib=f_copy, copy_write_kib=w_copy, fetch_scale=fetch_scale,
+                write_scale=write_scale, k_fetch_kib=f_k, k_write_kib=w_k,
+                dispatches=dict(copy_fetch=n_fc, copy_write=n_wc, k_fetch=n_fk, k_write=n_wk),
+                fetch_bytes=fetch_b, write_bytes=write_b, traffic_bytes=fetch_b + write_b)
+
+
+def stored_traffic():
+    """Traffic bytes per launch from the stored record, or None if there is
+    none or the kernel source changed since it was taken."""
+    try:
+        for line in open(TRAFFIC_RECORD):
+            if line.startswith("record: "):
+                rec = json.loads(line[len("record: "):])
+                if rec.get("kernel_src_sha256") == kernel_sha256():
+                    return rec["traffic_bytes"]
+    except OSError:
+        pass
+    return None
+
+
+def copy_calibration(mb):
+    """Elementwise float32 negation of mb MiB: reads mb MiB, writes mb MiB."""
+    import torch
+    n = mb * 2 ** 20 // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def cpu_baseline(wl, inp, gpu_out, min_seconds=10.0):
@@ -85,7 +161,15 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--sets", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calib-mb", type=int, default=0)
+    ap.add_argument("--event-every", type=int, default=4)
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     args = ap.parse_args()
+    if args.traffic_from:
+        if args.copy_calib_mb <= 0:
+            ap.error("--traffic-from needs the --copy-calib-mb the counter runs used")
+        print(json.dumps(traffic_record(*args.traffic_from, args.copy_calib_mb)))
+        return 0
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the verify path has no multi-GPU mode "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
@@ -98,6 +182,8 @@ def main():
     wl = W.WORKLOADS[3]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calib_mb > 0:
+        copy_calibration(args.copy_calib_mb)
     sets = [W.generate(wl, 1000 + i, dev) for i in range(args.sets)]
     B, gamma, V = wl.B, wl.gamma, wl.V
     outs = [(torch.empty(B, dtype=torch.int32, device=dev),
@@ -106,7 +192,9 @@ def main():
     stream = torch.cuda.current_stream()
     ev = HipEvents()
     n = args.steps
-    hot = [(ev.create(), ev.create()) for _ in range(n)]
+    every = max(1, args.event_every)
+    sampled = list(range(0, n, every))
+    hot = {i: (ev.create(), ev.create()) for i in sampled}
     outer = (ev.create(), ev.create())
 
     def step(i, events=None):
@@ -123,23 +211,29 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
-    # timed region: exactly `steps` steps, each bracketing the statistics
-    # kernel with its own pair of events
+    # timed region: exactly `steps` steps; every `every`-th one brackets the
+    # statistics kernel with its own pair of events
     torch.cuda.synchronize()
     ev.hip.hipEventRecord(ctypes.c_void_p(outer[0]), ctypes.c_void_p(stream.cuda_stream))
     t0 = time.perf_counter()
     for i in range(n):
-        step(i, hot[i])
+        step(i, hot.get(i))
     ev.hip.hipEventRecord(ctypes.c_void_p(outer[1]), ctypes.c_void_p(stream.cuda_stream))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     total_ms = ev.elapsed_ms(*outer)
-    hot_ms = [ev.elapsed_ms(a, b) for a, b in hot]
+    hot_ms = sorted(ev.elapsed_ms(*hot[i]) for i in sampled)
+    windows = sorted(ev.elapsed_ms(hot[a][0], hot[b][0]) / (b - a)
+                     for a, b in zip(sampled, sampled[1:]))
     ms_per_step = total_ms / n
-    hot_mean = sum(hot_ms) / n
+    hot_mean = sum(hot_ms) / len(hot_ms)
+
+    def pct(xs, q):
+        return xs[min(len(xs) - 1, int(q * (len(xs) - 1) + 0.5))] if xs else None
     pos_per_s = B * gamma / (ms_per_step / 1e3)
     stats_bytes = wl.logit_bytes()  # the statistics kernel reads q and p once
     achieved = stats_bytes / (hot_mean / 1e3) / 1e9
+    traffic = stored_traffic()
 
     line = dict(
         metric="verified positions/s and achieved HBM GB/s (B=32, γ=7, V=256000 bf16)",
@@ -152,11 +246,15 @@ def main():
                     global_batch=B, positions_per_step=B * gamma,
                     algorithmic_bytes_per_step=wl.algorithmic_bytes(),
                     path_gbps=wl.algorithmic_bytes() / (ms_per_step / 1e3) / 1e9,
-                    input_sets=len(sets), wall_s=wall),
+                    input_sets=len(sets), wall_s=wall,
+                    step_us_p10_p50_p90=[None if pct(windows, q) is None else pct(windows, q) * 1e3
+                                         for q in (0.1, 0.5, 0.9)],
+                    step_us_windows=f"{len(windows)} windows of {every} steps"),
         roofline=dict(bound="hbm", kernel="k_stats", achieved=achieved, peak=PEAK_HBM_GBPS,
-                      unit="GB/s", frac=achieved / PEAK_HBM_GBPS, traffic=None,
-                      mean_us=hot_mean * 1e3, min_us=min(hot_ms) * 1e3,
-                      bytes_per_launch=stats_bytes),
+                      unit="GB/s", frac=achieved / PEAK_HBM_GBPS, traffic=traffic,
+                      mean_us=hot_mean * 1e3, min_us=hot_ms[0] * 1e3,
+                      p10_p50_p90_us=[pct(hot_ms, q) * 1e3 for q in (0.1, 0.5, 0.9)],
+                      launches_timed=len(hot_ms), bytes_per_launch=stats_bytes),
     )
     if not args.no_cpu_baseline:
         torch.cuda.synchronize()
@@ -170,7 +268,7 @@ def main():
         base, rep = cpu_baseline(wl, s0, g)
         line["cpu_baseline"] = base
         line["parity_vs_oracle"] = rep
-    for a, b in hot:
+    for a, b in hot.values():
         ev.destroy(a)
         ev.destroy(b)
     print(json.dumps(line), flush=True)

@@ -40,7 +40,7 @@ def _flush(msg):
 
 # ------------------------------------------------------------ full workloads
 
-@pytest.mark.parametrize("cfg,steps", [(1, 1000), (3, 40), (4, 25)])
+@pytest.mark.parametrize("cfg,steps", [(1, 1000), (3, 100), (4, 50)])
 def test_workload_parity(cfg, steps):
     wl = W.WORKLOADS[cfg]
     _flush(f"[parity] cfg{cfg} {wl.name} steps={_steps(cfg, steps)}")
