@@ -57,7 +57,8 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
   L.zero_end = o;
   L.tiles = o; o = align_up(o + sizeof(TilePart) * R * nt, 256);
   L.tvpart = o; o = align_up(o + sizeof(double) * R * nt, 256);
-  L.masses = o; o = align_up(o + sizeof(double) * B * nt * kChunksPerTile, 256);
+  const int64_t nc = (V + samp_chunk_elems(dtype, vec) - 1) / samp_chunk_elems(dtype, vec);
+  L.masses = o; o = align_up(o + sizeof(double) * B * nc, 256);
   L.total = o;
   return L;
 }
@@ -152,7 +153,8 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   P.gamma = gamma;
   P.V = V;
   P.nt = (int32_t)((V + spc::stat_tile_elems(dtype, vec) - 1) / spc::stat_tile_elems(dtype, vec));
-  P.K = spc::samp_groups(P.nt);
+  P.nc = (int32_t)((V + spc::samp_chunk_elems(dtype, vec) - 1) / spc::samp_chunk_elems(dtype, vec));
+  P.K = spc::samp_groups(P.nc);
   P.rule = rule;
   P.alpha = alpha;
   P.temp = force_greedy ? 0.0f : temperature;

@@ -11,7 +11,8 @@
 namespace spc {
 
 constexpr int kThreads = 256;  // four 64-lane wavefronts per workgroup
-// A tile is read as kChunksPerTile wave-contiguous chunks by the sampler.
+// A statistics tile is read as kChunksPerTile wave-contiguous chunks when a
+// draw is made from it.
 constexpr int kChunksPerTile = kThreads / 64;
 
 // Sampling distribution at j* (Alg. 4): the residual max(0, p - q), or the
@@ -51,6 +52,7 @@ struct Params {
   const float* uniforms;
   int32_t B, gamma, V;
   int32_t nt;              // statistics tiles per row
+  int32_t nc;              // residual chunks per row
   int32_t K;               // sampling workgroups per sequence
   int32_t rule;
   float alpha, temp;
@@ -68,13 +70,14 @@ struct Params {
   uint32_t* samp_cnt;     // [B]   sampling workgroups of a sequence done
   TilePart* tiles;        // [R][nt] statistics partials
   double* tvpart;         // [R][nt] TV partials
-  double* masses;         // [B][nt][4] residual chunk masses of row j*
+  double* masses;         // [B][nc] residual chunk masses of row j*
 };
 
-// Entries per statistics tile for a dtype and load path, and sampling
-// workgroups per sequence for a row of nt such tiles.
+// Entries per statistics tile and per residual chunk for a dtype and load
+// path, and sampling workgroups per sequence for a row of nc chunks.
 int stat_tile_elems(int dtype, bool vec);
-int samp_groups(int64_t nt);
+int samp_chunk_elems(int dtype, bool vec);
+int samp_groups(int64_t nc);
 
 // Workspace layout for a shape; offsets in bytes from the base.
 struct WsLayout {

@@ -58,11 +58,7 @@ struct Tile {
 };
 // statistics / TV tiles: small, so that many workgroups are resident
 template <int DT, bool VEC>
-using StatTile = Tile<DT, VEC, VEC ? 2 : 8>;
-// The sampling pass works on the same tiles (so a draw can use the statistics
-// partials as tile masses); a sampling workgroup sums the residual masses of
-// kSampBatch tiles per batch, and takes two batches.
-constexpr int kSampBatch = kSampThreads / kThreads;
+using StatTile = Tile<DT, VEC, VEC ? 4 : 8>;
 
 // bfloat16 -> float32 is exact: the bf16 bits are the top half of the float.
 template <int DT, bool VEC>
@@ -695,33 +691,37 @@ __device__ __forceinline__ void decide_seq(const Params& P, int b, const SeqPara
 }
 
 // ------------------------------------------------------------- sampling
-// A chunk is the quarter of a tile that one wavefront covers when the tile is
-// read wave-contiguously: chunk c of tile k starts at entry k * TileN +
-// c * ChunkN, and lane l's lane load i covers entries (i * 64 + l) * VW ..
-// + VW - 1 of it.
-template <int DT, bool VEC>
+// A chunk is what one wavefront covers reading wave-contiguously: lane l's
+// lane load i covers entries (i * 64 + l) * VW .. + VW - 1 of it.  The
+// residual pass sums SampChunks; a statistics tile is kChunksPerTile
+// consecutive TileChunks.
+template <int DT, bool VEC, int U_>
 struct Chunk {
-  using T = StatTile<DT, VEC>;
-  static constexpr int U = T::U, NW = T::NW, VW = T::VW;
+  static constexpr int U = U_;
+  static constexpr int NW = Tile<DT, VEC, U_>::NW, VW = Tile<DT, VEC, U_>::VW;
   static constexpr int N = 64 * U * VW;  // entries per chunk
 };
 template <int DT, bool VEC>
-using ChunkRegs = uint32_t[Chunk<DT, VEC>::U][Chunk<DT, VEC>::NW];
+using TileChunk = Chunk<DT, VEC, StatTile<DT, VEC>::U>;
+template <int DT, bool VEC>
+using SampChunk = Chunk<DT, VEC, VEC ? 2 : 8>;
+
+template <class C>
+using ChunkRegs = uint32_t[C::U][C::NW];
 
 // Lane loads of the chunk starting at entry c0 of a row (V entries); a chunk
 // past the row reads entry 0 and masks everything.
-template <int DT, bool VEC>
-__device__ __forceinline__ void load_chunk(const char* row, int64_t c0, int V,
-                                           ChunkRegs<DT, VEC>& w) {
+template <int DT, bool VEC, class C>
+__device__ __forceinline__ void load_chunk(const char* row, int64_t c0, int V, ChunkRegs<C>& w) {
   const bool live = c0 < V;
-  load_tile<DT, VEC, Chunk<DT, VEC>::U, false, false, 64>(row, live ? c0 : 0, live ? V : 0, w,
-                                                          threadIdx.x & 63);
+  load_tile<DT, VEC, C::U, false, false, 64>(row, live ? c0 : 0, live ? V : 0, w,
+                                             threadIdx.x & 63);
 }
 
 // Sources of the part masses of the sampled distribution: the statistics
 // partials per tile (q or p: each tile's share of the normaliser), the TV
 // partials per tile (the residual of an OPT row, which the TV pass summed),
-// or the residual masses per chunk computed by the sampling pass.
+// or the residual masses per SampChunk computed by the sampling pass.
 enum MassSrc : int { kSrcStatsQ = 0, kSrcStatsP = 1, kSrcTv = 2, kSrcPass = 3 };
 
 template <int SRC>
@@ -736,7 +736,7 @@ __device__ __forceinline__ double part_mass(const Params& P, int64_t row, int b,
   } else if constexpr (SRC == kSrcTv) {
     return P.tvpart[row * P.nt + k];
   } else {
-    return ld_dev_f64(P.masses + ((int64_t)b * P.nt) * kChunksPerTile + k);
+    return ld_dev_f64(P.masses + (int64_t)b * P.nc + k);
   }
 }
 
@@ -780,33 +780,32 @@ __device__ __forceinline__ double find_part(const Params& P, int64_t row, int b,
   return W;
 }
 
-// Whole block: residual masses max(0, p - q) of the chunks of tiles kw,
-// kw + K, ... of a row (K sampling workgroups per sequence).  The block's
-// wavefronts take the chunks of kSampBatch tiles per batch, one chunk each,
-// and the next batch loads while this one is summed; chunk c's mass goes to
-// masses[c].  No block barrier: every wave drains its own stores.
+// Whole block: residual masses max(0, p - q) of the SampChunks of a row (K
+// sampling workgroups per sequence): wave w of workgroup kw takes chunks
+// kw * kSampWaves + w, then + K * kSampWaves, ...; the next chunk loads while
+// one is summed, and chunk c's mass goes to masses[c].  No block barrier:
+// every wave drains its own stores.
 template <int DT, bool VEC>
-__device__ __forceinline__ void residual_masses(const char* qrow, const char* prow, int V, int nt,
+__device__ __forceinline__ void residual_masses(const char* qrow, const char* prow, int V, int nc,
                                                 int K, int kw, const ProbScale& ps,
                                                 double* masses) {
-  using C = Chunk<DT, VEC>;
-  constexpr int TN = StatTile<DT, VEC>::N;
+  using C = SampChunk<DT, VEC>;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int sub = wv / kChunksPerTile, quarter = wv % kChunksPerTile;
-  const int step = K * kSampBatch;
-  ChunkRegs<DT, VEC> wq, wp, nq = {}, np = {};
+  const int step = K * kSampWaves;
+  ChunkRegs<C> wq, wp, nq = {}, np = {};
   {
-    const int k = kw + sub * K;
-    const int64_t c0 = k < nt ? (int64_t)k * TN + quarter * C::N : (int64_t)V;
-    load_chunk<DT, VEC>(qrow, c0, V, wq);
-    load_chunk<DT, VEC>(prow, c0, V, wp);
+    const int c = kw * kSampWaves + wv;
+    const int64_t c0 = c < nc ? (int64_t)c * C::N : (int64_t)V;
+    load_chunk<DT, VEC, C>(qrow, c0, V, wq);
+    load_chunk<DT, VEC, C>(prow, c0, V, wp);
   }
-  for (int k0 = kw; k0 < nt; k0 += step) {
-    if (k0 + step < nt) {  // block-uniform: prefetch the next batch
-      const int k = k0 + step + sub * K;
-      const int64_t c0 = k < nt ? (int64_t)k * TN + quarter * C::N : (int64_t)V;
-      load_chunk<DT, VEC>(qrow, c0, V, nq);
-      load_chunk<DT, VEC>(prow, c0, V, np);
+  for (int b0 = kw * kSampWaves; b0 < nc; b0 += step) {  // block-uniform
+    const int c = b0 + wv;
+    if (b0 + step < nc) {  // prefetch the next batch
+      const int cn = c + step;
+      const int64_t c0 = cn < nc ? (int64_t)cn * C::N : (int64_t)V;
+      load_chunk<DT, VEC, C>(qrow, c0, V, nq);
+      load_chunk<DT, VEC, C>(prow, c0, V, np);
     }
     double acc = 0.0;
 #pragma unroll
@@ -818,8 +817,7 @@ __device__ __forceinline__ void residual_masses(const char* qrow, const char* pr
       acc += (double)t;
     }
     acc = wave_sum(acc);
-    const int k = k0 + sub * K;
-    if (lane == 0 && k < nt) st_dev_f64(masses + (int64_t)k * kChunksPerTile + quarter, acc);
+    if (lane == 0 && c < nc) st_dev_f64(masses + c, acc);
 #pragma unroll
     for (int i = 0; i < C::U; ++i)
 #pragma unroll
@@ -837,26 +835,25 @@ __device__ __forceinline__ void residual_masses(const char* qrow, const char* pr
 // first one where the running mass exceeds rem; its lane then walks its VW
 // entries.  The next chunk loads while one is scanned.  Rounding that leaves
 // rem unreached takes the last entry with mass.
-template <int DT, bool VEC, int NCH, int KIND>
+template <int DT, bool VEC, class C, int NCH, int KIND>
 __device__ __forceinline__ void pick_wave(const Params& P, int b, int64_t row, int64_t c0,
                                           double rem, const ProbScale& ps) {
-  using C = Chunk<DT, VEC>;
   constexpr int EB = StatTile<DT, VEC>::EB;
   const int lane = threadIdx.x & 63;
   const int V = P.V;
   const char* qrow = (const char*)P.q + row * V * EB;
   const char* prow = (const char*)P.p + row * V * EB;
-  ChunkRegs<DT, VEC> cq = {}, cp = {}, nq = {}, np = {};
-  if (KIND != kP) load_chunk<DT, VEC>(qrow, c0, V, cq);
-  if (KIND != kQ) load_chunk<DT, VEC>(prow, c0, V, cp);
+  ChunkRegs<C> cq = {}, cp = {}, nq = {}, np = {};
+  if (KIND != kP) load_chunk<DT, VEC, C>(qrow, c0, V, cq);
+  if (KIND != kQ) load_chunk<DT, VEC, C>(prow, c0, V, cp);
   double carry = 0.0, before = 0.0;
   int hlane = -1, last_pos = -1;
   int64_t hbase = 0;
   uint32_t sq[C::NW] = {}, sp_[C::NW] = {};
   for (int c = 0; c < NCH && hlane < 0; ++c) {
     if (c + 1 < NCH) {
-      if (KIND != kP) load_chunk<DT, VEC>(qrow, c0 + (c + 1) * C::N, V, nq);
-      if (KIND != kQ) load_chunk<DT, VEC>(prow, c0 + (c + 1) * C::N, V, np);
+      if (KIND != kP) load_chunk<DT, VEC, C>(qrow, c0 + (c + 1) * C::N, V, nq);
+      if (KIND != kQ) load_chunk<DT, VEC, C>(prow, c0 + (c + 1) * C::N, V, np);
     }
 #pragma unroll
     for (int i = 0; i < C::U; ++i) {
@@ -921,7 +918,7 @@ __device__ __forceinline__ void draw(const Params& P, int b, int64_t row, int ki
   if (src == kSrcStatsQ) W = find_part<kSrcStatsQ>(P, row, b, P.nt, rs, u, &ks, &rem);
   else if (src == kSrcStatsP) W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
   else if (src == kSrcTv) W = find_part<kSrcTv>(P, row, b, P.nt, rs, u, &ks, &rem);
-  else W = find_part<kSrcPass>(P, row, b, P.nt * kChunksPerTile, rs, u, &ks, &rem);
+  else W = find_part<kSrcPass>(P, row, b, P.nc, rs, u, &ks, &rem);
   if (kind == kResidual && !(W > 0.0)) {
     kind = kP;
     src = kSrcStatsP;
@@ -934,16 +931,18 @@ __device__ __forceinline__ void draw(const Params& P, int b, int64_t row, int ki
     return;
   }
   const ProbScale ps = prob_scale(sp, rs);
-  constexpr int TN = StatTile<DT, VEC>::N, CN = Chunk<DT, VEC>::N;
+  using SC = SampChunk<DT, VEC>;
+  using TC = TileChunk<DT, VEC>;
+  constexpr int TN = StatTile<DT, VEC>::N;
+  static_assert(TN == kChunksPerTile * TC::N, "a tile is kChunksPerTile chunks");
   if (src == kSrcPass) {
-    const int64_t c0 = (int64_t)(ks / kChunksPerTile) * TN + (ks % kChunksPerTile) * CN;
-    pick_wave<DT, VEC, 1, kResidual>(P, b, row, c0, rem, ps);
+    pick_wave<DT, VEC, SC, 1, kResidual>(P, b, row, (int64_t)ks * SC::N, rem, ps);
   } else if (kind == kQ) {
-    pick_wave<DT, VEC, kChunksPerTile, kQ>(P, b, row, (int64_t)ks * TN, rem, ps);
+    pick_wave<DT, VEC, TC, kChunksPerTile, kQ>(P, b, row, (int64_t)ks * TN, rem, ps);
   } else if (kind == kP) {
-    pick_wave<DT, VEC, kChunksPerTile, kP>(P, b, row, (int64_t)ks * TN, rem, ps);
+    pick_wave<DT, VEC, TC, kChunksPerTile, kP>(P, b, row, (int64_t)ks * TN, rem, ps);
   } else {
-    pick_wave<DT, VEC, kChunksPerTile, kResidual>(P, b, row, (int64_t)ks * TN, rem, ps);
+    pick_wave<DT, VEC, TC, kChunksPerTile, kResidual>(P, b, row, (int64_t)ks * TN, rem, ps);
   }
 }
 
@@ -951,9 +950,10 @@ __device__ __forceinline__ void draw(const Params& P, int b, int64_t row, int ki
 
 // Statistics pass.  grid (nt, R): stats tile k of row r.  Each thread takes
 // the exact max of its entries and the sum of 2^(z c - r_t), r_t = max * c_hi
-// (a reference near its largest z c); the block combines the threads against
-// the tile max.  With ARGMAX (batches that may hold greedy rows) the lowest
-// entry attaining the max is found as well.
+// (a reference near its largest z c); each wave combines its threads against
+// the wave max, and thread 0 the waves against the tile max.  With ARGMAX
+// (batches that may hold greedy rows) the lowest entry attaining the max is
+// found as well.
 template <int DT, bool VEC, bool ARGMAX>
 __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
   using T = StatTile<DT, VEC>;
@@ -1010,28 +1010,59 @@ __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
     sq += tq[0];
     spp += tp[0];
   }
-  float Mq = mq, Mp = mp;
-  block_max2(Mq, Mp, sh);
-  const float Rq = Mq * sp.c_hi, Rp = Mp * sp.c_hi;
-  // rq - Rq is exact in fp64; only its rounding to float is inexact
-  double dq = (mq == kNegInf) ? 0.0 : (double)sq * (double)exp2_hw((float)((double)rq - (double)Rq));
-  double dp = (mp == kNegInf) ? 0.0 : (double)spp * (double)exp2_hw((float)((double)rp - (double)Rp));
-  block_sum2(dq, dp, sh);
+  // Wave partials against the wave max (r_t - r_w is exact in fp64; only its
+  // rounding to float is inexact), then one barrier and thread 0 combines the
+  // waves in order against the tile max.
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const float Wq = wave_max(mq), Wp = wave_max(mp);
+  double dq = (mq == kNegInf) ? 0.0
+              : (double)sq * (double)exp2_hw((float)((double)rq - (double)(Wq * sp.c_hi)));
+  double dp = (mp == kNegInf) ? 0.0
+              : (double)spp * (double)exp2_hw((float)((double)rp - (double)(Wp * sp.c_hi)));
+  dq = wave_sum(dq);
+  dp = wave_sum(dp);
   if constexpr (ARGMAX) {
-    iq = (mq == Mq) ? iq : 0x7fffffff;
-    ip = (mp == Mp) ? ip : 0x7fffffff;
-    block_min2(iq, ip, sh);
+    iq = wave_min((mq == Wq) ? iq : 0x7fffffff);
+    ip = wave_min((mp == Wp) ? ip : 0x7fffffff);
   }
+  if (lane == 0) {
+    sh.m[wv][0] = Wq;
+    sh.m[wv][1] = Wp;
+    sh.d[wv][0] = dq;
+    sh.d[wv][1] = dp;
+    sh.i[wv][0] = iq;
+    sh.i[wv][1] = ip;
+  }
+  __syncthreads();
   if (threadIdx.x == 0) {
+    float Mq = sh.m[0][0], Mp = sh.m[0][1];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) {
+      Mq = fmaxf(Mq, sh.m[w][0]);
+      Mp = fmaxf(Mp, sh.m[w][1]);
+    }
+    const float Rq = Mq * sp.c_hi, Rp = Mp * sp.c_hi;
+    double tq = 0.0, tp = 0.0;
+    int aq = 0x7fffffff, ap = 0x7fffffff;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float wq_ = sh.m[w][0], wp_ = sh.m[w][1];
+      if (wq_ != kNegInf)
+        tq += sh.d[w][0] * (double)exp2_hw((float)((double)(wq_ * sp.c_hi) - (double)Rq));
+      if (wp_ != kNegInf)
+        tp += sh.d[w][1] * (double)exp2_hw((float)((double)(wp_ * sp.c_hi) - (double)Rp));
+      if (ARGMAX && wq_ == Mq) aq = min(aq, sh.i[w][0]);
+      if (ARGMAX && wp_ == Mp) ap = min(ap, sh.i[w][1]);
+    }
     TilePart t;
-    t.s_q = dq;
-    t.s_p = dp;
+    t.s_q = tq;
+    t.s_p = tp;
     t.r_q = (Mq == kNegInf) ? kNegInf : Rq;
     t.r_p = (Mp == kNegInf) ? kNegInf : Rp;
     t.zmax_q = Mq;
     t.zmax_p = Mp;
-    t.amax_q = ARGMAX ? iq : -1;
-    t.amax_p = ARGMAX ? ip : -1;
+    t.amax_q = ARGMAX ? aq : -1;
+    t.amax_p = ARGMAX ? ap : -1;
     P.tiles[(int64_t)r * P.nt + k] = t;
   }
 }
@@ -1103,8 +1134,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
   const ProbScale ps = prob_scale(sp, rs);
   const char* qrow = (const char*)P.q + row * P.V * EB;
   const char* prow = (const char*)P.p + row * P.V * EB;
-  residual_masses<DT, VEC>(qrow, prow, P.V, P.nt, P.K, k, ps,
-                           P.masses + ((int64_t)b * P.nt) * kChunksPerTile);
+  residual_masses<DT, VEC>(qrow, prow, P.V, P.nc, P.K, k, ps, P.masses + (int64_t)b * P.nc);
   if (!arrive_last(P.samp_cnt + b, (uint32_t)P.K, sh)) return;
   if (threadIdx.x < 64) draw<DT, VEC>(P, b, row, kResidual, kSrcPass, s.u, sp, rs);
 }
@@ -1138,7 +1168,13 @@ int stat_tile_elems(int dtype, bool vec) {
   return vec ? StatTile<0, true>::N : StatTile<0, false>::N;
 }
 
-int samp_groups(int64_t nt) { return (int)((nt + 2 * kSampBatch - 1) / (2 * kSampBatch)); }
+int samp_chunk_elems(int dtype, bool vec) {
+  if (dtype == 1) return vec ? SampChunk<1, true>::N : SampChunk<1, false>::N;
+  return vec ? SampChunk<0, true>::N : SampChunk<0, false>::N;
+}
+
+// two chunks per wavefront
+int samp_groups(int64_t nc) { return (int)((nc + 2 * kSampWaves - 1) / (2 * kSampWaves)); }
 
 hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
                          bool need_argmax, hipEvent_t e0, hipEvent_t e1, hipStream_t st) {
