@@ -424,20 +424,27 @@ __device__ __forceinline__ float prob(float z, float c_hi, float c_lo, float l_h
   return exp2_hw(fmaf(z, c_hi, -l_hi) + fmaf(z, c_lo, -l_lo));
 }
 
+// (2^d - 1) / d for d in [0, 1/4]: a degree-4 polynomial fitted here for
+// relative error (4e-10 in exact arithmetic, about one float32 ulp as
+// evaluated), so 2^d - 1 keeps full relative precision as d -> 0.
+__device__ __forceinline__ float exp2m1_over_d(float d) {
+  float r = 0.0014333005528897047f;
+  r = fmaf(r, d, 0.009596072137355804f);
+  r = fmaf(r, d, 0.05550608038902283f);
+  r = fmaf(r, d, 0.24022644758224487f);
+  return fmaf(r, d, 0.6931471824645996f);
+}
+
 // Residual weight max(0, p_v - q_v), branch-free.  d = log2(p_v / q_v) is
 // formed in fp64 from the exact difference zp - zq, so p ~ q does not cancel:
-// below d = 1/4 the weight is q_v (2^d - 1) with 2^d - 1 = expm1(d ln 2) from
-// its Taylor series (relative truncation error < 1e-8); above, p_v - q_v
-// itself, where p_v > 1.18 q_v bounds the cancellation.  Both -inf gives a
-// NaN d and weight 0; zq = -inf alone gives d = +inf and weight p_v.
+// below d = 1/4 the weight is q_v (2^d - 1); above, p_v - q_v itself, where
+// p_v > 1.18 q_v bounds the cancellation.  Both -inf gives a NaN d and weight
+// 0; zq = -inf alone gives d = +inf and weight p_v.
 __device__ __forceinline__ float residual_weight(float zq, float zp, const ProbScale& s) {
   const float d = (float)fma((double)zp - (double)zq, s.c, -s.dl);
   const float pq = prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
   const float pp = prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
-  const float x = d * 0.693147180559945309f;
-  const float em1 =
-      x * (1.0f + x * (0.5f + x * (1.0f / 6 + x * (1.0f / 24 + x * (1.0f / 120 + x * (1.0f / 720))))));
-  const float w = d < 0.25f ? pq * em1 : pp - pq;
+  const float w = d < 0.25f ? pq * (d * exp2m1_over_d(d)) : pp - pq;
   return d > 0.0f ? w : 0.0f;
 }
 
@@ -743,33 +750,61 @@ __device__ __forceinline__ double part_mass(const Params& P, int64_t row, int b,
 // Wave 0: the part (tile or chunk) of the inverse-CDF draw -- the first part
 // k with C_k > u W, C_k the running mass through part k in vocabulary order
 // and W the total -- and the target mass left at its start.  Returns W.
+// Parts are read kFindGroup per lane at a time, all loads in flight
+// together; for at most 64 * kFindGroup parts both passes use one read.
+constexpr int kFindGroup = 4;
+
+template <int SRC>
+__device__ __forceinline__ void load_parts(const Params& P, int64_t row, int b, int K, int k0,
+                                           const RowStat& rs, double (&m)[kFindGroup]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int j = 0; j < kFindGroup; ++j) {
+    const int k = k0 + j * 64 + lane;
+    m[j] = k < K ? part_mass<SRC>(P, row, b, k, rs) : 0.0;
+  }
+}
+
 template <int SRC>
 __device__ __forceinline__ double find_part(const Params& P, int64_t row, int b, int K,
                                             const RowStat& rs, float u, int* ks_out,
                                             double* rem_out) {
-  const int lane = threadIdx.x & 63;
-  const double m0 = lane < K ? part_mass<SRC>(P, row, b, lane, rs) : 0.0;
-  double W = wave_sum(m0);
-  for (int k0 = 64; k0 < K; k0 += 64) {
-    const int k = k0 + lane;
-    W += wave_sum(k < K ? part_mass<SRC>(P, row, b, k, rs) : 0.0);
+  constexpr int GN = 64 * kFindGroup;
+  double m0[kFindGroup];
+  load_parts<SRC>(P, row, b, K, 0, rs, m0);
+  double W = 0.0;
+#pragma unroll
+  for (int j = 0; j < kFindGroup; ++j) W += wave_sum(m0[j]);
+  for (int k0 = GN; k0 < K; k0 += GN) {
+    double m[kFindGroup];
+    load_parts<SRC>(P, row, b, K, k0, rs, m);
+#pragma unroll
+    for (int j = 0; j < kFindGroup; ++j) W += wave_sum(m[j]);
   }
   const double target = (double)u * W;
   double carry = 0.0, rem = 0.0;
   int ks = -1, klast = -1;
-  for (int k0 = 0; k0 < K; k0 += 64) {
-    const int k = k0 + lane;
-    const double m = k0 == 0 ? m0 : k < K ? part_mass<SRC>(P, row, b, k, rs) : 0.0;
-    const double incl = carry + wave_incl_scan(m);
-    const unsigned long long pos = __ballot(m > 0.0);
-    const unsigned long long hit = __ballot(m > 0.0 && incl > target);
-    if (pos) klast = k0 + 63 - __clzll(pos);
-    if (ks < 0 && hit) {
-      const int l = __ffsll(hit) - 1;
-      ks = k0 + l;
-      rem = target - (lane_f64(incl, l) - lane_f64(m, l));
+  for (int k0 = 0; k0 < K && ks < 0; k0 += GN) {
+    double m[kFindGroup];
+    if (k0 == 0) {
+#pragma unroll
+      for (int j = 0; j < kFindGroup; ++j) m[j] = m0[j];
+    } else {
+      load_parts<SRC>(P, row, b, K, k0, rs, m);
     }
-    carry = lane_f64(incl, 63);
+#pragma unroll
+    for (int j = 0; j < kFindGroup; ++j) {
+      const double incl = carry + wave_incl_scan(m[j]);
+      const unsigned long long pos = __ballot(m[j] > 0.0);
+      const unsigned long long hit = __ballot(m[j] > 0.0 && incl > target);
+      if (pos) klast = k0 + j * 64 + 63 - __clzll(pos);
+      if (ks < 0 && hit) {
+        const int l = __ffsll(hit) - 1;
+        ks = k0 + j * 64 + l;
+        rem = target - (lane_f64(incl, l) - lane_f64(m[j], l));
+      }
+      carry = lane_f64(incl, 63);
+    }
   }
   if (ks < 0) {  // rounding left u W at or past the end: the last part with mass
     ks = klast;
