@@ -33,6 +33,20 @@ struct DevWorkspace {
 std::mutex g_ws_mu;
 std::map<int, DevWorkspace> g_ws;
 
+std::mutex g_cu_mu;
+std::map<int, int> g_cus;
+
+// Compute units of device dev, read once per device; 0 on failure.
+int cu_count(int dev) {
+  std::lock_guard<std::mutex> lk(g_cu_mu);
+  auto it = g_cus.find(dev);
+  if (it != g_cus.end()) return it->second;
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) n = 0;
+  if (n > 0) g_cus[dev] = n;
+  return n;
+}
+
 // Rows (gridDim.y of the statistics kernels) are capped by the launch limit.
 constexpr int64_t kMaxRows = 65535;
 
@@ -104,16 +118,20 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
 
   const bool vec = vec_path(dtype, V);
   const spc::WsLayout L = spc::ws_layout(B, gamma, V, dtype, vec);
+  // argument checks end here: no HIP call precedes them
+  if (ex && ex->workspace &&
+      (ex->workspace_bytes < L.total || ((uintptr_t)ex->workspace % 256) != 0))
+    return fail(SPC_E_WORKSPACE, "workspace of %zu bytes (need %zu, 256-byte aligned)",
+                ex->workspace_bytes, L.total);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SPC_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  const int cus = cu_count(dev);
+  if (cus <= 0) return fail(SPC_E_HIP, "cannot read the compute-unit count of device %d", dev);
   char* ws = nullptr;
   if (ex && ex->workspace) {
-    if (ex->workspace_bytes < L.total || ((uintptr_t)ex->workspace % 256) != 0)
-      return fail(SPC_E_WORKSPACE, "workspace of %zu bytes (need %zu, 256-byte aligned)",
-                  ex->workspace_bytes, L.total);
     ws = static_cast<char*>(ex->workspace);
   } else {
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return fail(SPC_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
     std::lock_guard<std::mutex> lk(g_ws_mu);
     DevWorkspace& w = g_ws[dev];
     if (w.bytes < L.total) {
@@ -154,7 +172,7 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   P.V = V;
   P.nt = (int32_t)((V + spc::stat_tile_elems(dtype, vec) - 1) / spc::stat_tile_elems(dtype, vec));
   P.nc = (int32_t)((V + spc::samp_chunk_elems(dtype, vec) - 1) / spc::samp_chunk_elems(dtype, vec));
-  P.K = spc::samp_groups(P.nc);
+  P.K = spc::samp_groups(P.nc, B, cus);
   P.rule = rule;
   P.alpha = alpha;
   P.temp = force_greedy ? 0.0f : temperature;
@@ -178,7 +196,7 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   const bool need_sample = !force_greedy && (per_temp || temperature > 0.0f);
   const bool need_tv = need_sample && (per_rule || rule == SPC_RULE_OPT);
   const bool need_argmax = force_greedy || per_temp;
-  hipError_t e = spc::launch_verify(P, dtype, vec, need_tv, need_sample, need_argmax,
+  e = spc::launch_verify(P, dtype, vec, need_tv, need_sample, need_argmax,
                                     ex ? ex->ev_hot_begin : nullptr,
                                     ex ? ex->ev_hot_end : nullptr, stream);
   if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));

@@ -74,10 +74,11 @@ struct Params {
 };
 
 // Entries per statistics tile and per residual chunk for a dtype and load
-// path, and sampling workgroups per sequence for a row of nc chunks.
+// path, and sampling workgroups per sequence for a row of nc chunks in a batch
+// of B sequences on a device of `cus` compute units.
 int stat_tile_elems(int dtype, bool vec);
 int samp_chunk_elems(int dtype, bool vec);
-int samp_groups(int64_t nc);
+int samp_groups(int64_t nc, int B, int cus);
 
 // Workspace layout for a shape; offsets in bytes from the base.
 struct WsLayout {

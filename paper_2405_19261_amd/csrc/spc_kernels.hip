@@ -1003,26 +1003,25 @@ __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
   load_tile<DT, VEC, T::U, false, true>(qrow, t0, V, wq, threadIdx.x);
   load_tile<DT, VEC, T::U, false, true>(prow, t0, V, wp, threadIdx.x);
 
+  // Thread max; with ARGMAX also the lowest entry attaining it: entries are
+  // visited in increasing index order and only a strictly larger value moves
+  // the index (indices fit 32 bits: V < 2^31).
   float mq = kNegInf, mp = kNegInf;
+  int iq = 0x7fffffff, ip = 0x7fffffff;
+  const int base = (int)t0 + (int)threadIdx.x * T::VW;
 #pragma unroll
   for (int i = 0; i < T::U; ++i)
 #pragma unroll
     for (int e = 0; e < T::VW; ++e) {
-      mq = fmaxf(mq, elem<DT, VEC>(wq[i], e));
-      mp = fmaxf(mp, elem<DT, VEC>(wp[i], e));
-    }
-  int iq = 0x7fffffff, ip = 0x7fffffff;
-  if constexpr (ARGMAX) {
-    // entries are visited in increasing index order: the first match wins
-#pragma unroll
-    for (int i = 0; i < T::U; ++i)
-#pragma unroll
-      for (int e = 0; e < T::VW; ++e) {
-        const int idx = (int)entry_of<DT, VEC, T::U, false>(t0, i, e, threadIdx.x);
-        if (iq == 0x7fffffff && elem<DT, VEC>(wq[i], e) == mq) iq = idx;
-        if (ip == 0x7fffffff && elem<DT, VEC>(wp[i], e) == mp) ip = idx;
+      const float vq = elem<DT, VEC>(wq[i], e), vp = elem<DT, VEC>(wp[i], e);
+      if constexpr (ARGMAX) {
+        const int idx = base + i * kThreads * T::VW + e;
+        if (vq > mq) iq = idx;
+        if (vp > mp) ip = idx;
       }
-  }
+      mq = fmaxf(mq, vq);
+      mp = fmaxf(mp, vp);
+    }
   const float rq = (mq == kNegInf) ? 0.0f : mq * sp.c_hi;
   const float rp = (mp == kNegInf) ? 0.0f : mp * sp.c_hi;
   float sq = 0.0f, spp = 0.0f;
@@ -1208,8 +1207,15 @@ int samp_chunk_elems(int dtype, bool vec) {
   return vec ? SampChunk<0, true>::N : SampChunk<0, false>::N;
 }
 
-// two chunks per wavefront
-int samp_groups(int64_t nc) { return (int)((nc + 2 * kSampWaves - 1) / (2 * kSampWaves)); }
+// Enough workgroups to give every compute unit one (a sampling workgroup
+// fills a CU), but no more than one chunk per wavefront: small batches spread
+// a row over several workgroups, large ones take one per sequence and loop.
+int samp_groups(int64_t nc, int B, int cus) {
+  const int64_t by_chunks = (nc + kSampWaves - 1) / kSampWaves;
+  const int64_t by_cus = (cus + B - 1) / B;
+  const int64_t k = by_chunks < by_cus ? by_chunks : by_cus;
+  return (int)(k < 1 ? 1 : k);
+}
 
 hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
                          bool need_argmax, hipEvent_t e0, hipEvent_t e1, hipStream_t st) {
