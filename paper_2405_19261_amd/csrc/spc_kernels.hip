@@ -435,7 +435,7 @@ __device__ __forceinline__ float exp2m1_over_d(float d) {
   return fmaf(r, d, 0.6931471824645996f);
 }
 
-// Residual weight max(0, p_v - q_v), branch-free.  d = log2(p_v / q_v) is
+// Residual weight max(0, p_v - q_v), without branches.  d = log2(p_v / q_v) is
 // formed in fp64 from the exact difference zp - zq, so p ~ q does not cancel:
 // below d = 1/4 the weight is q_v (2^d - 1); above, p_v - q_v itself, where
 // p_v > 1.18 q_v bounds the cancellation.  Both -inf gives a NaN d and weight
@@ -444,7 +444,11 @@ __device__ __forceinline__ float residual_weight(float zq, float zp, const ProbS
   const float d = (float)fma((double)zp - (double)zq, s.c, -s.dl);
   const float pq = prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
   const float pp = prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
-  const float w = d < 0.25f ? pq * (d * exp2m1_over_d(d)) : pp - pq;
+  float small = pq * (d * exp2m1_over_d(d)), big = pp - pq;
+  // both arms stay computed: left alone, the compiler sinks each into a
+  // divergent branch, which costs more than evaluating both
+  asm volatile("" : "+v"(small), "+v"(big));
+  const float w = d < 0.25f ? small : big;
   return d > 0.0f ? w : 0.0f;
 }
 
