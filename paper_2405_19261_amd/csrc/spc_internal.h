@@ -11,9 +11,6 @@
 namespace spc {
 
 constexpr int kThreads = 256;  // four 64-lane wavefronts per workgroup
-// A statistics tile is read as kChunksPerTile wave-contiguous chunks when a
-// draw is made from it.
-constexpr int kChunksPerTile = kThreads / 64;
 
 // Sampling distribution at j* (Alg. 4): the residual max(0, p - q), or the
 // extra-token target pi_{t+gamma}, which is q or p.

@@ -264,9 +264,18 @@ struct RowDecision {
 };
 
 // Per-sequence state built by every sampling workgroup.
+// The part of a draw found by wave 0, for the whole workgroup.
+struct PickState {
+  int k;       // part holding the sample (-1: nothing to draw)
+  int kind;    // SampleKind actually sampled
+  int src;     // MassSrc of the part masses
+  double rem;  // target mass remaining at the start of that part
+};
+
 struct SeqShared {
   RowDecision rows[SPC_MAX_GAMMA + 1];
   SeqState seq;
+  PickState pk;
 };
 
 // Block reductions: per-wave results combined in wave order (a fixed order,
@@ -704,8 +713,8 @@ __device__ __forceinline__ void decide_seq(const Params& P, int b, const SeqPara
 // ------------------------------------------------------------- sampling
 // A chunk is what one wavefront covers reading wave-contiguously: lane l's
 // lane load i covers entries (i * 64 + l) * VW .. + VW - 1 of it.  The
-// residual pass sums SampChunks; a statistics tile is kChunksPerTile
-// consecutive TileChunks.
+// residual pass sums SampChunks; a statistics tile is kSampWaves consecutive
+// SubChunks, one per wavefront of a sampling workgroup.
 template <int DT, bool VEC, int U_>
 struct Chunk {
   static constexpr int U = U_;
@@ -713,7 +722,7 @@ struct Chunk {
   static constexpr int N = 64 * U * VW;  // entries per chunk
 };
 template <int DT, bool VEC>
-using TileChunk = Chunk<DT, VEC, StatTile<DT, VEC>::U>;
+using SubChunk = Chunk<DT, VEC, StatTile<DT, VEC>::U * kThreads / (64 * kSampWaves)>;
 template <int DT, bool VEC>
 using SampChunk = Chunk<DT, VEC, VEC ? 2 : 8>;
 
@@ -868,13 +877,11 @@ __device__ __forceinline__ void residual_masses(const char* qrow, const char* pr
   vmem_drain();
 }
 
-// Wave 0: the in-part draw over NCH consecutive chunks from entry c0 (a
-// whole tile when NCH = kChunksPerTile, one chunk when 1).  Lane loads are
-// scanned in entry order -- chunk, then lane load i, then lane -- for the
-// first one where the running mass exceeds rem; its lane then walks its VW
-// entries.  The next chunk loads while one is scanned.  Rounding that leaves
-// rem unreached takes the last entry with mass.
-template <int DT, bool VEC, class C, int NCH, int KIND>
+// Wave 0: the in-chunk draw in the chunk starting at entry c0.  Lane loads
+// are scanned in entry order -- lane load i, then lane -- for the first one
+// where the running mass exceeds rem; its lane then walks its VW entries.
+// Rounding that leaves rem unreached takes the last entry with mass.
+template <int DT, bool VEC, class C, int KIND>
 __device__ __forceinline__ void pick_wave(const Params& P, int b, int64_t row, int64_t c0,
                                           double rem, const ProbScale& ps) {
   constexpr int EB = StatTile<DT, VEC>::EB;
@@ -882,51 +889,38 @@ __device__ __forceinline__ void pick_wave(const Params& P, int b, int64_t row, i
   const int V = P.V;
   const char* qrow = (const char*)P.q + row * V * EB;
   const char* prow = (const char*)P.p + row * V * EB;
-  ChunkRegs<C> cq = {}, cp = {}, nq = {}, np = {};
+  ChunkRegs<C> cq = {}, cp = {};
   if (KIND != kP) load_chunk<DT, VEC, C>(qrow, c0, V, cq);
   if (KIND != kQ) load_chunk<DT, VEC, C>(prow, c0, V, cp);
   double carry = 0.0, before = 0.0;
   int hlane = -1, last_pos = -1;
   int64_t hbase = 0;
   uint32_t sq[C::NW] = {}, sp_[C::NW] = {};
-  for (int c = 0; c < NCH && hlane < 0; ++c) {
-    if (c + 1 < NCH) {
-      if (KIND != kP) load_chunk<DT, VEC, C>(qrow, c0 + (c + 1) * C::N, V, nq);
-      if (KIND != kQ) load_chunk<DT, VEC, C>(prow, c0 + (c + 1) * C::N, V, np);
+#pragma unroll
+  for (int i = 0; i < C::U; ++i) {
+    const int64_t base = c0 + (int64_t)(i * 64 + lane) * C::VW;
+    double m = 0.0;
+#pragma unroll
+    for (int e = 0; e < C::VW; ++e) {
+      const float w = weight_of<KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
+      m += (double)w;
+      if (w > 0.0f) last_pos = max(last_pos, (int)(base + e));
     }
+    const double incl = carry + wave_incl_scan(m);
+    if (hlane < 0) {  // wave-uniform
+      const unsigned long long hit = __ballot(m > 0.0 && incl > rem);
+      if (hit) {
+        hlane = __ffsll(hit) - 1;
+        before = lane_f64(incl, hlane) - lane_f64(m, hlane);
+        hbase = base;
 #pragma unroll
-    for (int i = 0; i < C::U; ++i) {
-      const int64_t base = c0 + c * C::N + (int64_t)(i * 64 + lane) * C::VW;
-      double m = 0.0;
-#pragma unroll
-      for (int e = 0; e < C::VW; ++e) {
-        const float w = weight_of<KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
-        m += (double)w;
-        if (w > 0.0f) last_pos = max(last_pos, (int)(base + e));
-      }
-      const double incl = carry + wave_incl_scan(m);
-      if (hlane < 0) {  // wave-uniform
-        const unsigned long long hit = __ballot(m > 0.0 && incl > rem);
-        if (hit) {
-          hlane = __ffsll(hit) - 1;
-          before = lane_f64(incl, hlane) - lane_f64(m, hlane);
-          hbase = base;
-#pragma unroll
-          for (int j = 0; j < C::NW; ++j) {
-            sq[j] = cq[i][j];
-            sp_[j] = cp[i][j];
-          }
+        for (int j = 0; j < C::NW; ++j) {
+          sq[j] = cq[i][j];
+          sp_[j] = cp[i][j];
         }
       }
-      carry = lane_f64(incl, 63);
     }
-#pragma unroll
-    for (int i = 0; i < C::U; ++i)
-#pragma unroll
-      for (int j = 0; j < C::NW; ++j) {
-        cq[i][j] = nq[i][j];
-        cp[i][j] = np[i][j];
-      }
+    carry = lane_f64(incl, 63);
   }
   if (hlane < 0) {
     const int lp = -wave_min(-last_pos);
@@ -946,42 +940,93 @@ __device__ __forceinline__ void pick_wave(const Params& P, int b, int64_t row, i
   P.out_token[b] = hit >= 0 ? hit : lastw;  // rounding inside the lane load
 }
 
-// Wave 0: the inverse-CDF draw of sequence b at row `row` (the row of j*)
-// from the distribution `kind`, whose part masses come from `src`.  An empty
-// residual (possible only through rounding) is replaced by p.
+// Whole block: the draw inside statistics tile t0 (entry offset).  Each
+// wavefront sums the weights of one SubChunk; wave 0 scans the kSampWaves
+// sums for the sub-chunk where rem is crossed and draws inside it.
+template <int DT, bool VEC, int KIND>
+__device__ __forceinline__ void pick_tile(const Params& P, int b, int64_t row, int64_t t0,
+                                          double rem, const ProbScale& ps, SampShared& sh) {
+  using C = SubChunk<DT, VEC>;
+  static_assert(kSampWaves * C::N == StatTile<DT, VEC>::N, "a tile is kSampWaves sub-chunks");
+  constexpr int EB = StatTile<DT, VEC>::EB;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int V = P.V;
+  const char* qrow = (const char*)P.q + row * V * EB;
+  const char* prow = (const char*)P.p + row * V * EB;
+  ChunkRegs<C> cq = {}, cp = {};
+  if (KIND != kP) load_chunk<DT, VEC, C>(qrow, t0 + wv * C::N, V, cq);
+  if (KIND != kQ) load_chunk<DT, VEC, C>(prow, t0 + wv * C::N, V, cp);
+  double m = 0.0;
+#pragma unroll
+  for (int i = 0; i < C::U; ++i) {
+    float t = 0.0f;
+#pragma unroll
+    for (int e = 0; e < C::VW; ++e)
+      t += weight_of<KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
+    m += (double)t;
+  }
+  m = wave_sum(m);
+  if (lane == 0) sh.dv[wv] = m;
+  __syncthreads();
+  if (wv != 0) return;
+  const double ml = lane < kSampWaves ? sh.dv[lane] : 0.0;
+  const double incl = wave_incl_scan(ml);
+  const unsigned long long hit = __ballot(ml > 0.0 && incl > rem);
+  const unsigned long long pos = __ballot(ml > 0.0);
+  int c;
+  double r;
+  if (hit) {
+    c = __ffsll(hit) - 1;
+    r = rem - (lane_f64(incl, c) - lane_f64(ml, c));
+  } else {  // rounding: the last sub-chunk with mass, its last entry with mass
+    c = pos ? 63 - __clzll(pos) : 0;
+    r = __builtin_huge_val();
+  }
+  pick_wave<DT, VEC, C, KIND>(P, b, row, t0 + c * C::N, r, ps);
+}
+
+// Whole block: the inverse-CDF draw of sequence b at row `row` (the row of
+// j*) from the distribution `kind`, whose part masses come from `src`.  Wave 0
+// finds the part; the draw inside a residual chunk runs in wave 0, the draw
+// inside a statistics tile uses every wavefront.  An empty residual (possible
+// only through rounding) is replaced by p.
 template <int DT, bool VEC>
 __device__ __forceinline__ void draw(const Params& P, int b, int64_t row, int kind, int src,
-                                     float u, const SeqParam& sp, const RowStat& rs) {
-  int ks;
-  double rem, W;
-  if (src == kSrcStatsQ) W = find_part<kSrcStatsQ>(P, row, b, P.nt, rs, u, &ks, &rem);
-  else if (src == kSrcStatsP) W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
-  else if (src == kSrcTv) W = find_part<kSrcTv>(P, row, b, P.nt, rs, u, &ks, &rem);
-  else W = find_part<kSrcPass>(P, row, b, P.nc, rs, u, &ks, &rem);
-  if (kind == kResidual && !(W > 0.0)) {
-    kind = kP;
-    src = kSrcStatsP;
-    W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
+                                     float u, const SeqParam& sp, const RowStat& rs,
+                                     SeqShared& ss, SampShared& sh) {
+  if (threadIdx.x < 64) {
+    int ks;
+    double rem, W;
+    if (src == kSrcStatsQ) W = find_part<kSrcStatsQ>(P, row, b, P.nt, rs, u, &ks, &rem);
+    else if (src == kSrcStatsP) W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
+    else if (src == kSrcTv) W = find_part<kSrcTv>(P, row, b, P.nt, rs, u, &ks, &rem);
+    else W = find_part<kSrcPass>(P, row, b, P.nc, rs, u, &ks, &rem);
+    if (kind == kResidual && !(W > 0.0)) {
+      kind = kP;
+      src = kSrcStatsP;
+      W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
+    }
+    if (threadIdx.x == 0) {
+      ss.pk = PickState{ks, kind, src, rem};
+      if (P.out_norm) P.out_norm[b] = (float)W;
+      if (ks < 0) P.out_token[b] = -1;
+    }
   }
-  const int lane = threadIdx.x & 63;
-  if (lane == 0 && P.out_norm) P.out_norm[b] = (float)W;
-  if (ks < 0) {
-    if (lane == 0) P.out_token[b] = -1;
-    return;
-  }
+  __syncthreads();
+  const PickState pk = ss.pk;
+  if (pk.k < 0) return;  // block-uniform
   const ProbScale ps = prob_scale(sp, rs);
-  using SC = SampChunk<DT, VEC>;
-  using TC = TileChunk<DT, VEC>;
   constexpr int TN = StatTile<DT, VEC>::N;
-  static_assert(TN == kChunksPerTile * TC::N, "a tile is kChunksPerTile chunks");
-  if (src == kSrcPass) {
-    pick_wave<DT, VEC, SC, 1, kResidual>(P, b, row, (int64_t)ks * SC::N, rem, ps);
-  } else if (kind == kQ) {
-    pick_wave<DT, VEC, TC, kChunksPerTile, kQ>(P, b, row, (int64_t)ks * TN, rem, ps);
-  } else if (kind == kP) {
-    pick_wave<DT, VEC, TC, kChunksPerTile, kP>(P, b, row, (int64_t)ks * TN, rem, ps);
+  if (pk.src == kSrcPass) {
+    using SC = SampChunk<DT, VEC>;
+    if (threadIdx.x < 64)
+      pick_wave<DT, VEC, SC, kResidual>(P, b, row, (int64_t)pk.k * SC::N, pk.rem, ps);
+  } else if (pk.kind == kQ) {
+    pick_tile<DT, VEC, kQ>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
+  } else if (pk.kind == kP) {
+    pick_tile<DT, VEC, kP>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
   } else {
-    pick_wave<DT, VEC, TC, kChunksPerTile, kResidual>(P, b, row, (int64_t)ks * TN, rem, ps);
+    pick_tile<DT, VEC, kResidual>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
   }
 }
 
@@ -1150,7 +1195,7 @@ __global__ __launch_bounds__(kThreads) void k_tv(Params P) {
 // that row's residual masses: the K workgroups sum them chunk by chunk, and
 // the last to finish draws.  Every other draw -- the extra token from q or p,
 // or an OPT residual, whose per-tile masses the earlier passes left -- is
-// made by workgroup 0 alone.  Draws run in one wavefront.
+// made by workgroup 0 alone.
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
   __shared__ SampShared sh;
@@ -1163,9 +1208,9 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
   const int64_t row = (int64_t)b * (P.gamma + 1) + s.row;
   const RowStat rs = ss.rows[s.row].rs;
   if (s.kind != kResidual || needs_tv(sp)) {
-    if (k != 0 || threadIdx.x >= 64) return;
+    if (k != 0) return;  // block-uniform
     const int src = s.kind == kQ ? kSrcStatsQ : s.kind == kP ? kSrcStatsP : kSrcTv;
-    draw<DT, VEC>(P, b, row, s.kind, src, s.u, sp, rs);
+    draw<DT, VEC>(P, b, row, s.kind, src, s.u, sp, rs, ss, sh);
     return;
   }
   constexpr int EB = StatTile<DT, VEC>::EB;
@@ -1174,7 +1219,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
   const char* prow = (const char*)P.p + row * P.V * EB;
   residual_masses<DT, VEC>(qrow, prow, P.V, P.nc, P.K, k, ps, P.masses + (int64_t)b * P.nc);
   if (!arrive_last(P.samp_cnt + b, (uint32_t)P.K, sh)) return;
-  if (threadIdx.x < 64) draw<DT, VEC>(P, b, row, kResidual, kSrcPass, s.u, sp, rs);
+  draw<DT, VEC>(P, b, row, kResidual, kSrcPass, s.u, sp, rs, ss, sh);
 }
 
 template <int DT, bool VEC>
