@@ -674,8 +674,13 @@ __device__ __forceinline__ void decide_seq(const Params& P, int b, const SeqPara
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int gamma = P.gamma, g1 = gamma + 1, V = P.V;
   if (sp.valid) {
-    // lane l of wave wv fetches the draft data of row wv + kSampWaves * l up
-    // front, so that these loads overlap the merges
+    // Loads in dependency order: the first row's partials and the draft
+    // data (lane l of wave wv takes row wv + kSampWaves * l) go out together;
+    // the logits at the draft tokens follow the tokens and stay in flight
+    // while the rows merge.
+    const bool tv = needs_tv(sp);
+    PartHead h{};
+    if (wv < g1) h = load_head(P, b * g1 + wv, tv);
     const int jl = wv + kSampWaves * lane;
     int x = -1;
     float zqx = 0.0f, zpx = 0.0f, u = 0.0f;
@@ -690,9 +695,6 @@ __device__ __forceinline__ void decide_seq(const Params& P, int b, const SeqPara
         }
       }
     }
-    const bool tv = needs_tv(sp);
-    PartHead h{};
-    if (wv < g1) h = load_head(P, b * g1 + wv, tv);
     for (int i = 0; wv + kSampWaves * i < g1; ++i) {
       const int j = wv + kSampWaves * i;
       // the next row's partials load while this row merges
