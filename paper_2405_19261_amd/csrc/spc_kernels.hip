@@ -80,13 +80,14 @@ __device__ __forceinline__ float elem(const uint32_t* w, int e) {
 // e = t0 + (OWN ? t*U + i : i*GT + t) * VW .. + VW - 1: interleaved
 // (coalesced) when OWN is false, thread-contiguous when true.
 // Entries at or past `end` read as -inf; a lane past the end re-reads a valid
-// address and discards the value, so the loads are branch-free.
-template <int DT, bool VEC, int U, bool OWN, bool NT, int GT = kThreads>
+// address and discards the value, so the loads are branch-free.  With MASK
+// false the caller guarantees a whole tile before `end`.
+template <int DT, bool VEC, int U, bool OWN, bool NT, int GT = kThreads, bool MASK = true>
 __device__ __forceinline__ void load_tile(const char* row, int64_t t0, int64_t end,
                                           uint32_t (&w)[U][Tile<DT, VEC, U>::NW], int tid) {
   using T = Tile<DT, VEC, U>;
   constexpr uint32_t kPad = (DT == 1) ? 0xff80ff80u : 0xff800000u;
-  const bool full = t0 + (int64_t)GT * U * T::VW <= end;
+  const bool full = !MASK || t0 + (int64_t)GT * U * T::VW <= end;
 #pragma unroll
   for (int i = 0; i < U; ++i) {
     const int64_t slot = OWN ? (int64_t)tid * U + i : (int64_t)i * GT + tid;
@@ -735,9 +736,13 @@ using ChunkRegs = uint32_t[C::U][C::NW];
 // past the row reads entry 0 and masks everything.
 template <int DT, bool VEC, class C>
 __device__ __forceinline__ void load_chunk(const char* row, int64_t c0, int V, ChunkRegs<C>& w) {
-  const bool live = c0 < V;
-  load_tile<DT, VEC, C::U, false, false, 64>(row, live ? c0 : 0, live ? V : 0, w,
-                                             threadIdx.x & 63);
+  const int lane = threadIdx.x & 63;
+  if (c0 + C::N <= V) {  // a whole chunk (wave-uniform): no masking
+    load_tile<DT, VEC, C::U, false, false, 64, false>(row, c0, V, w, lane);
+  } else {
+    const bool live = c0 < V;
+    load_tile<DT, VEC, C::U, false, false, 64>(row, live ? c0 : 0, live ? V : 0, w, lane);
+  }
 }
 
 // Sources of the part masses of the sampled distribution: the statistics
