@@ -5,21 +5,23 @@
 // one position (b, j) of the logit pair (q, p); rows are cut into tiles of
 // consecutive vocabulary entries.
 //
-//   k_stats   grid (stats tiles per row, rows), one small tile per workgroup.
+//   k_stats   grid (tiles per row, rows), one tile per 256-thread workgroup.
 //             Reads every logit of q and p once and reduces the tile to
-//             {max z, sum 2^(z c - r)} for both tensors (c = log2(e) / T);
-//             the tile partial goes to the workspace with plain stores.
+//             {max z, sum 2^(z c - r), argmax} for both tensors
+//             (c = log2(e) / T); the tile partial goes to the workspace.
 //   k_tv      OPT sequences at temperature > 0 only: D_TV(p, q) of Lemma 3
 //             needs both normalisers, so it is a second pass over those rows,
 //             one partial per tile.
-//   k_sample  grid (sample tiles per row, sequences).  Every workgroup of
-//             sequence b merges that sequence's row partials and takes the
+//   k_sample  grid (K, sequences), 1024-thread workgroups.  Every workgroup
+//             of sequence b merges that sequence's row partials and takes the
 //             per-sequence decision (deferral delta_j, accept draws a_j, first
 //             rejection j*) -- a small, fixed-order computation, so every
-//             workgroup reaches the same result -- then computes the mass of
-//             its tile of row j* under the sampled distribution (residual
-//             max(0, p - q), or the extra-token target q or p).  The last tile
-//             to finish picks the token: inverse CDF in vocabulary order.
+//             workgroup reaches the same result.  A replacement from the
+//             residual max(0, p - q) of a non-OPT row needs a second look at
+//             row j*: the K workgroups sum its residual per chunk and the last
+//             to finish draws.  Every other draw takes its per-tile masses
+//             from the statistics or TV partials and is made by workgroup 0.
+//             Draws are inverse CDF in vocabulary order.
 //
 // Kernel boundaries order the passes; within k_sample one completion counter
 // per sequence ("last workgroup to arrive draws") is reset by its last
@@ -77,12 +79,12 @@ __device__ __forceinline__ float elem(const uint32_t* w, int e) {
 
 // Lane loads of one tile of one row into w[U][NW] by the GT threads of a
 // group, tid the thread's index in it.  Thread t's lane load i covers entries
-// e = t0 + (OWN ? t*U + i : i*GT + t) * VW .. + VW - 1: interleaved
-// (coalesced) when OWN is false, thread-contiguous when true.
+// e = t0 + (i*GT + t) * VW .. + VW - 1 (interleaved, so each load
+// instruction of a wavefront reads one contiguous 1 KiB).
 // Entries at or past `end` read as -inf; a lane past the end re-reads a valid
 // address and discards the value, so the loads are branch-free.  With MASK
 // false the caller guarantees a whole tile before `end`.
-template <int DT, bool VEC, int U, bool OWN, bool NT, int GT = kThreads, bool MASK = true>
+template <int DT, bool VEC, int U, bool NT, int GT = kThreads, bool MASK = true>
 __device__ __forceinline__ void load_tile(const char* row, int64_t t0, int64_t end,
                                           uint32_t (&w)[U][Tile<DT, VEC, U>::NW], int tid) {
   using T = Tile<DT, VEC, U>;
@@ -90,7 +92,7 @@ __device__ __forceinline__ void load_tile(const char* row, int64_t t0, int64_t e
   const bool full = !MASK || t0 + (int64_t)GT * U * T::VW <= end;
 #pragma unroll
   for (int i = 0; i < U; ++i) {
-    const int64_t slot = OWN ? (int64_t)tid * U + i : (int64_t)i * GT + tid;
+    const int64_t slot = (int64_t)i * GT + tid;
     const int64_t e = t0 + slot * T::VW;
     const bool ok = full || e < end;
     const int64_t ec = ok ? e : t0;  // a valid address; the value is discarded
@@ -110,14 +112,6 @@ __device__ __forceinline__ void load_tile(const char* row, int64_t t0, int64_t e
       w[i][0] = ok ? v : kPad;
     }
   }
-}
-
-// Entry index of lane load i, element e of this thread (layout as load_tile).
-template <int DT, bool VEC, int U, bool OWN, int GT = kThreads>
-__device__ __forceinline__ int64_t entry_of(int64_t t0, int i, int e, int tid) {
-  using T = Tile<DT, VEC, U>;
-  const int64_t slot = OWN ? (int64_t)tid * U + i : (int64_t)i * GT + tid;
-  return t0 + slot * T::VW + e;
 }
 
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -250,7 +244,6 @@ struct SharedT {
   double d[NWV][2];
   double dv[NWV];
   int i[NWV][2];
-  double scan[NWV];
   int flag;
 };
 using Shared = SharedT<kWaves>;
@@ -279,27 +272,8 @@ struct SeqShared {
   PickState pk;
 };
 
-// Block reductions: per-wave results combined in wave order (a fixed order,
-// so every thread and every run gets the same value).
-// All threads receive the block-wide max of (a, b).
-template <int NWV>
-__device__ __forceinline__ void block_max2(float& a, float& b, SharedT<NWV>& sh) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  a = wave_max(a);
-  b = wave_max(b);
-  __syncthreads();  // sh.m may still be read by an earlier step
-  if (lane == 0) { sh.m[wv][0] = a; sh.m[wv][1] = b; }
-  __syncthreads();
-  a = sh.m[0][0];
-  b = sh.m[0][1];
-#pragma unroll
-  for (int w = 1; w < NWV; ++w) {
-    a = fmaxf(a, sh.m[w][0]);
-    b = fmaxf(b, sh.m[w][1]);
-  }
-}
-
-// Block sums; valid in every thread.
+// Block sums: per-wave results combined in wave order (a fixed order, so
+// every thread and every run gets the same value); valid in every thread.
 template <int NWV>
 __device__ __forceinline__ void block_sum2(double& a, double& b, SharedT<NWV>& sh) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -315,41 +289,6 @@ __device__ __forceinline__ void block_sum2(double& a, double& b, SharedT<NWV>& s
     a += sh.d[w][0];
     b += sh.d[w][1];
   }
-}
-
-template <int NWV>
-__device__ __forceinline__ void block_min2(int& a, int& b, SharedT<NWV>& sh) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  a = wave_min(a);
-  b = wave_min(b);
-  __syncthreads();
-  if (lane == 0) { sh.i[wv][0] = a; sh.i[wv][1] = b; }
-  __syncthreads();
-  a = sh.i[0][0];
-  b = sh.i[0][1];
-#pragma unroll
-  for (int w = 1; w < NWV; ++w) {
-    a = min(a, sh.i[w][0]);
-    b = min(b, sh.i[w][1]);
-  }
-}
-
-// Inclusive prefix sum over the block's threads in thread order (fp64); the
-// last thread's value equals *total bit for bit.
-template <int NWV>
-__device__ __forceinline__ double block_incl_scan(double v, SharedT<NWV>& sh, double* total) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  v = wave_incl_scan(v);
-  __syncthreads();
-  if (lane == 63) sh.scan[wv] = v;
-  __syncthreads();
-  double off = 0.0;
-  for (int w = 0; w < wv; ++w) off += sh.scan[w];
-  double tot = 0.0;
-#pragma unroll
-  for (int w = 0; w < NWV; ++w) tot += sh.scan[w];
-  *total = tot;
-  return off + v;
 }
 
 // "Am I the last of `n` arrivals?" for the whole block.  Thread 0 wrote the
@@ -738,10 +677,10 @@ template <int DT, bool VEC, class C>
 __device__ __forceinline__ void load_chunk(const char* row, int64_t c0, int V, ChunkRegs<C>& w) {
   const int lane = threadIdx.x & 63;
   if (c0 + C::N <= V) {  // a whole chunk (wave-uniform): no masking
-    load_tile<DT, VEC, C::U, false, false, 64, false>(row, c0, V, w, lane);
+    load_tile<DT, VEC, C::U, false, 64, false>(row, c0, V, w, lane);
   } else {
     const bool live = c0 < V;
-    load_tile<DT, VEC, C::U, false, false, 64>(row, live ? c0 : 0, live ? V : 0, w, lane);
+    load_tile<DT, VEC, C::U, false, 64>(row, live ? c0 : 0, live ? V : 0, w, lane);
   }
 }
 
@@ -1056,8 +995,8 @@ __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
   const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
   const int64_t t0 = (int64_t)k * T::N;
   uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
-  load_tile<DT, VEC, T::U, false, true>(qrow, t0, V, wq, threadIdx.x);
-  load_tile<DT, VEC, T::U, false, true>(prow, t0, V, wp, threadIdx.x);
+  load_tile<DT, VEC, T::U, true>(qrow, t0, V, wq, threadIdx.x);
+  load_tile<DT, VEC, T::U, true>(prow, t0, V, wp, threadIdx.x);
 
   // Thread max; with ARGMAX also the lowest entry attaining it: entries are
   // visited in increasing index order and only a strictly larger value moves
@@ -1174,8 +1113,8 @@ __global__ __launch_bounds__(kThreads) void k_tv(Params P) {
   const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
   const int64_t t0 = (int64_t)k * T::N;
   uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
-  load_tile<DT, VEC, T::U, false, true>(qrow, t0, V, wq, threadIdx.x);
-  load_tile<DT, VEC, T::U, false, true>(prow, t0, V, wp, threadIdx.x);
+  load_tile<DT, VEC, T::U, true>(qrow, t0, V, wq, threadIdx.x);
+  load_tile<DT, VEC, T::U, true>(prow, t0, V, wp, threadIdx.x);
   if (threadIdx.x < 64) {
     const RowStat rs = merge_row(P, r, false, false);
     if (threadIdx.x == 0) srow = rs;
