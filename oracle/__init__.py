@@ -15,6 +15,7 @@ _lib = None
 
 F32, BF16, F64 = 0, 1, 2
 CHOW, DIFF, OPT, ALWAYS, NEVER = 0, 1, 2, 3, 4
+TOKEN_V1, TOKEN_V2, TOKEN_V3 = 5, 6, 7
 FLAG_DRAFT_OUT_OF_RANGE, FLAG_EMPTY_RESIDUAL = 1, 2
 
 _P = ctypes.c_void_p
@@ -45,6 +46,10 @@ def lib():
         L.orc_accept.restype = ctypes.c_int
         L.orc_residual.argtypes = [_P, _P, _I64, _P]
         L.orc_residual.restype = _D
+        L.orc_token_r.argtypes = [ctypes.c_int, _D, _D, _D, _D, ctypes.POINTER(_D)]
+        L.orc_token_r.restype = ctypes.c_int
+        L.orc_token_target.argtypes = [ctypes.c_int, _D, _P, _P, _I64, _D, _P, ctypes.POINTER(_D)]
+        L.orc_token_target.restype = _D
         L.orc_sample.argtypes = [_P, _I64, _D, ctypes.POINTER(_D)]
         L.orc_sample.restype = _I32
         L.orc_verify.argtypes = [_P, _P, ctypes.c_int, _P, _P, _I32, _I32, _I64, _P, _P, _P,
@@ -114,6 +119,23 @@ def target(delta, q, p):
     pi = np.empty_like(q)
     lib().orc_target(int(delta), _ptr(q), _ptr(p), q.size, _ptr(pi))
     return pi
+
+
+def token_r(rule, alpha, qv, pv, maxp):
+    mg = _D()
+    r = lib().orc_token_r(rule, float(alpha), float(qv), float(pv), float(maxp), ctypes.byref(mg))
+    return r, mg.value
+
+
+def token_target(rule, alpha, q, p, maxp):
+    """(pi, eta, rmargin) of the token-specific target for one row."""
+    q = np.ascontiguousarray(q, np.float64)
+    p = np.ascontiguousarray(p, np.float64)
+    pi = np.empty_like(q)
+    mg = _D()
+    eta = lib().orc_token_target(rule, float(alpha), _ptr(q), _ptr(p), q.size, float(maxp),
+                                 _ptr(pi), ctypes.byref(mg))
+    return pi, eta, mg.value
 
 
 def accept(pi_x, q_x, u):

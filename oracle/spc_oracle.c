@@ -9,6 +9,7 @@
  *   D_TV              Lemma 3 (Section 4.3)
  *   deferral delta    Table 1; eq. (2) Chow, eq. (5) Diff, eq. (11) OPT
  *   target pi         eq. (6), T_delta of Alg. 5
+ *   token rules       Section 4.4 (TokenV1/V2/V3), target of Alg. 6
  *   accept / j* / residual / sample    Alg. 4 (GenSpecSample)
  *   greedy step       Lemma 6 (Appendix, greedy special case)
  *
@@ -19,6 +20,10 @@
  *   - the bonus target pi_{t+gamma} needs a drafter row at position gamma, so
  *     the drafter supplies gamma+1 rows.
  *   - one uniform per draft position and one more for the single sample.
+ *   - token rules report delta_j = r(x_j), the rule's verdict on the draft
+ *     token (0 at the bonus position); at temperature 0 r is read at the
+ *     drafter's argmax with temperature-1 probabilities, so the one-hot
+ *     target sits at argmax p when r = 1 and at argmax q otherwise.
  */
 #include "spc_oracle.h"
 
@@ -115,6 +120,36 @@ int orc_accept(double pi_x, double q_x, double u, double* margin) {
   return u < r ? 1 : 0;
 }
 
+int orc_token_r(int rule, double alpha, double qv, double pv, double maxp, double* margin) {
+  double lhs, rhs;
+  switch (rule) {
+    case ORC_TOKEN_V1: lhs = qv; rhs = maxp - alpha; break;
+    case ORC_TOKEN_V2: lhs = pv; rhs = maxp - alpha; break;
+    case ORC_TOKEN_V3: lhs = pv; rhs = maxp * (1.0 - alpha); break;
+    default: *margin = NAN; return -1;
+  }
+  double scale = fabs(lhs) > fabs(rhs) ? fabs(lhs) : fabs(rhs);
+  *margin = scale > 0.0 ? fabs(lhs - rhs) / scale : 0.0;
+  return lhs < rhs ? 1 : 0;
+}
+
+double orc_token_target(int rule, double alpha, const double* q, const double* p, int64_t V,
+                        double maxp, double* pi, double* rmargin) {
+  double eta = 0.0, mmin = INFINITY;
+  for (int64_t v = 0; v < V; ++v) {
+    double mg;
+    if (orc_token_r(rule, alpha, q[v], p[v], maxp, &mg)) eta += q[v];
+    if (mg < mmin) mmin = mg;
+  }
+  for (int64_t v = 0; v < V; ++v) {
+    double mg;
+    int r = orc_token_r(rule, alpha, q[v], p[v], maxp, &mg);
+    pi[v] = q[v] * (1.0 - r) + p[v] * eta;
+  }
+  *rmargin = mmin;
+  return eta;
+}
+
 double orc_residual(const double* pi, const double* q, int64_t V, double* w) {
   double W = 0.0;
   for (int64_t v = 0; v < V; ++v) {
@@ -161,7 +196,8 @@ int orc_num_threads(void) {
 #endif
 }
 
-static int rule_ok(int r) { return r >= ORC_CHOW && r <= ORC_NEVER; }
+static int rule_ok(int r) { return r >= ORC_CHOW && r <= ORC_TOKEN_V3; }
+static int is_token(int r) { return r >= ORC_TOKEN_V1 && r <= ORC_TOKEN_V3; }
 
 int orc_verify(const void* q_logits, const void* p_logits, int dtype, const int32_t* draft,
                const float* uniforms, int32_t B, int32_t gamma, int64_t V,
@@ -205,10 +241,18 @@ int orc_verify(const void* q_logits, const void* p_logits, int dtype, const int3
       orc_row_stats sq, sp;
       orc_softmax_row(row_ptr(q_logits, dtype, row, V), dtype, V, T, qj, &sq);
       orc_softmax_row(row_ptr(p_logits, dtype, row, V), dtype, V, T, pj, &sp);
-      double tv = orc_tv(pj, qj, V);
-      double mg;
-      dl[j] = orc_defer(rule[b], al, sq.maxprob, sp.maxprob, tv, &mg);
-      orc_target(dl[j], qj, pj, V, pi + (size_t)j * V);
+      double tv, mg;
+      if (is_token(rule[b])) {
+        /* Alg. 6: pi = q (1 - r) + p eta; reported delta_j = r(x_j) */
+        tv = orc_token_target(rule[b], al, qj, pj, V, sp.maxprob, pi + (size_t)j * V, &mg);
+        int32_t x = j < gamma ? draft[(int64_t)b * gamma + j] : -1;
+        double xmg;
+        dl[j] = (x >= 0 && x < V) ? orc_token_r(rule[b], al, qj[x], pj[x], sp.maxprob, &xmg) : 0;
+      } else {
+        tv = orc_tv(pj, qj, V);
+        dl[j] = orc_defer(rule[b], al, sq.maxprob, sp.maxprob, tv, &mg);
+        orc_target(dl[j], qj, pj, V, pi + (size_t)j * V);
+      }
       defer[row] = (uint8_t)dl[j];
       if (defer_margin) defer_margin[row] = mg;
       if (row_stats) {
@@ -302,7 +346,15 @@ int orc_greedy_verify(const void* q_logits, const void* p_logits, int dtype,
       /* one-hot q~, p~: D_TV(p~, q~) = 1(argmax q != argmax p) */
       double tv = (aq[j] != ap[j]) ? 1.0 : 0.0;
       double mg;
-      dl[j] = orc_defer(rule[b], (double)alpha[b], sq.maxprob, sp.maxprob, tv, &mg);
+      if (is_token(rule[b])) {
+        /* r at the drafter's argmax; eta~ = r(argmax q) for the one-hot q~ */
+        const void* prow = row_ptr(p_logits, dtype, row, V);
+        double pa = exp(logit_at(prow, dtype, aq[j]) - sp.lse);
+        dl[j] = orc_token_r(rule[b], (double)alpha[b], sq.maxprob, pa, sp.maxprob, &mg);
+        tv = (double)dl[j];
+      } else {
+        dl[j] = orc_defer(rule[b], (double)alpha[b], sq.maxprob, sp.maxprob, tv, &mg);
+      }
       defer[row] = (uint8_t)dl[j];
       if (defer_margin) defer_margin[row] = mg;
       if (row_stats) {

@@ -37,7 +37,8 @@ enum { ORC_F32 = 0, ORC_BF16 = 1, ORC_F64 = 2 };
 /* Deferral rules of Table 1 (Section 4.2 and eq. (2), (5), (11)), plus the two
  * constant rules: ALWAYS (delta = 1: standard speculative decoding, Alg. 1)
  * and NEVER (delta = 0: the drafter alone). */
-enum { ORC_CHOW = 0, ORC_DIFF = 1, ORC_OPT = 2, ORC_ALWAYS = 3, ORC_NEVER = 4 };
+enum { ORC_CHOW = 0, ORC_DIFF = 1, ORC_OPT = 2, ORC_ALWAYS = 3, ORC_NEVER = 4,
+       ORC_TOKEN_V1 = 5, ORC_TOKEN_V2 = 6, ORC_TOKEN_V3 = 7 };
 
 /* Per-sequence flags reported by orc_verify / orc_greedy_verify. */
 enum {
@@ -75,6 +76,19 @@ int orc_accept(double pi_x, double q_x, double u, double* margin);
 
 /* Unnormalised residual w = max(0, pi - q) (Alg. 4); returns sum_v w_v. */
 double orc_residual(const double* pi, const double* q, int64_t V, double* w);
+
+/* Token-specific deferral (Section 4.4, the TokenV1/V2/V3 plug-in rules):
+ * r(v) = 1 marks token v as not acceptable.
+ *   V1: q(v) < max p - alpha;  V2: p(v) < max p - alpha;
+ *   V3: p(v) < max p (1 - alpha).
+ * margin = |lhs - rhs| / max(|lhs|, |rhs|) (relative). */
+int orc_token_r(int rule, double alpha, double qv, double pv, double maxp, double* margin);
+
+/* Target of Alg. 6 (TokenSpecCascade): pi(v) = q(v) (1 - r(v)) + p(v) eta with
+ * eta = sum_v r(v) q(v) (vocabulary order).  Returns eta; *rmargin is the
+ * smallest r-margin over the row (any r(v) that flips moves eta). */
+double orc_token_target(int rule, double alpha, const double* q, const double* p, int64_t V,
+                        double maxp, double* pi, double* rmargin);
 
 /* Inverse-CDF draw from norm(w): the smallest k with C_k / W > u, where
  * C_k = sum_{v<=k} w_v in index order and W = C_{V-1}.  Returns -1 when W is
