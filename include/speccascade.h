@@ -54,13 +54,24 @@ extern "C" {
 
 typedef enum { SPC_F32 = 0, SPC_BF16 = 1 } spc_dtype;
 
-/* Deferral rules of Table 1 plus two constant rules. */
+/* Deferral rules of Table 1, two constant rules, and the token-specific rules
+ * of Section 4.4.  A token rule r(v) marks token v as not acceptable and uses
+ * the target of Alg. 6 (TokenSpecCascade) in place of T_delta:
+ *   pi(v) = q(v) (1 - r(v)) + p(v) eta,   eta = sum_v r(v) q(v).
+ * For a token rule, out_defer_mask[b][j] reports r(x_j), the rule's verdict
+ * on the draft token (0 at the bonus position j = gamma), and row statistic
+ * column 6 holds eta.  At temperature 0 r is read at the drafter's argmax
+ * with temperature-1 probabilities; the one-hot target then sits at argmax p
+ * when r = 1 and at argmax q otherwise. */
 typedef enum {
-  SPC_RULE_CHOW = 0,   /* delta = 1(max_v q(v) < 1 - alpha)                 eq. (2)  */
-  SPC_RULE_DIFF = 1,   /* delta = 1(max_v q(v) < max_v p(v) - alpha)        eq. (5)  */
-  SPC_RULE_OPT = 2,    /* delta = 1(max_v q(v) < max_v p(v) - alpha D_TV)   eq. (11) */
-  SPC_RULE_ALWAYS = 3, /* delta = 1: standard speculative decoding (Alg. 1)          */
-  SPC_RULE_NEVER = 4   /* delta = 0: the drafter's own distribution                  */
+  SPC_RULE_CHOW = 0,     /* delta = 1(max_v q(v) < 1 - alpha)                 eq. (2)  */
+  SPC_RULE_DIFF = 1,     /* delta = 1(max_v q(v) < max_v p(v) - alpha)        eq. (5)  */
+  SPC_RULE_OPT = 2,      /* delta = 1(max_v q(v) < max_v p(v) - alpha D_TV)   eq. (11) */
+  SPC_RULE_ALWAYS = 3,   /* delta = 1: standard speculative decoding (Alg. 1)          */
+  SPC_RULE_NEVER = 4,    /* delta = 0: the drafter's own distribution                  */
+  SPC_RULE_TOKEN_V1 = 5, /* r(v) = 1(q(v) < max_v p(v) - alpha)          TokenV1, 4.4  */
+  SPC_RULE_TOKEN_V2 = 6, /* r(v) = 1(p(v) < max_v p(v) - alpha)          TokenV2, 4.4  */
+  SPC_RULE_TOKEN_V3 = 7  /* r(v) = 1(p(v) < max_v p(v) (1 - alpha))      TokenV3, 4.4  */
 } spc_rule;
 
 typedef enum {
@@ -126,7 +137,8 @@ spc_status spc_greedy_verify(const void* q_logits, const void* p_logits, spc_dty
  *   out_row_stats  [B][gamma+1][8] float32: {m_q, lse_q, maxprob_q, m_p,
  *       lse_p, maxprob_p, tv, 0} with m = max_v z_v / T and lse = log sum_v
  *       exp(z_v / T); greedy rows hold the temperature-1 values and the
- *       one-hot TV.  tv is computed for OPT rows only (0 elsewhere).
+ *       one-hot TV (for a token rule, r at argmax q).  tv is computed for OPT
+ *       rows only (0 elsewhere); token-rule rows hold eta there.
  *   out_argmax     [B][gamma+1][2] int32: argmax of raw q and p logits
  *       (filled for greedy rows; -1 elsewhere).
  *   out_sample_norm [B] float32: the total mass W of the distribution

@@ -128,7 +128,14 @@ int orc_token_r(int rule, double alpha, double qv, double pv, double maxp, doubl
     case ORC_TOKEN_V3: lhs = pv; rhs = maxp * (1.0 - alpha); break;
     default: *margin = NAN; return -1;
   }
+  if (rule != ORC_TOKEN_V1 && pv == maxp) {
+    /* a token attaining max p meets max p (1 - alpha) or max p - alpha:
+     * the verdict is 1(alpha < 0) exactly, with nothing rounded */
+    *margin = INFINITY;
+    return alpha < 0.0 ? 1 : 0;
+  }
   double scale = fabs(lhs) > fabs(rhs) ? fabs(lhs) : fabs(rhs);
+  if (rule != ORC_TOKEN_V3 && maxp > scale) scale = maxp; /* max p - alpha */
   *margin = scale > 0.0 ? fabs(lhs - rhs) / scale : 0.0;
   return lhs < rhs ? 1 : 0;
 }

@@ -81,7 +81,11 @@ double orc_residual(const double* pi, const double* q, int64_t V, double* w);
  * r(v) = 1 marks token v as not acceptable.
  *   V1: q(v) < max p - alpha;  V2: p(v) < max p - alpha;
  *   V3: p(v) < max p (1 - alpha).
- * margin = |lhs - rhs| / max(|lhs|, |rhs|) (relative). */
+ * margin = |lhs - rhs| / scale with scale = max(|lhs|, |rhs|), and for V1
+ * and V2 also max p: there the threshold max p - alpha inherits the rounding
+ * of max p itself, which is relative to max p, not to the (possibly much
+ * smaller) difference.  Under V2 and V3 a token with p(v) = max p gets
+ * 1(alpha < 0), exact, with an infinite margin. */
 int orc_token_r(int rule, double alpha, double qv, double pv, double maxp, double* margin);
 
 /* Target of Alg. 6 (TokenSpecCascade): pi(v) = q(v) (1 - r(v)) + p(v) eta with

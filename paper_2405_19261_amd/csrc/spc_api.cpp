@@ -107,7 +107,7 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   const bool per_rule = ex && ex->rule_per_seq;
   const bool per_alpha = ex && ex->alpha_per_seq;
   const bool per_temp = ex && ex->temp_per_seq;
-  if (!per_rule && (rule < SPC_RULE_CHOW || rule > SPC_RULE_NEVER))
+  if (!per_rule && (rule < SPC_RULE_CHOW || rule > SPC_RULE_TOKEN_V3))
     return fail(SPC_E_RULE, "unknown rule %d", rule);
   if (!per_alpha && !isfinite(alpha)) return fail(SPC_E_PARAM, "alpha is not finite");
   if (!force_greedy && !per_temp && !(isfinite(temperature) && temperature >= 1e-20f))
@@ -194,7 +194,8 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   // sequences at temperature > 0 may exist unless the whole batch is greedy;
   // OPT at temperature > 0 needs the TV pass
   const bool need_sample = !force_greedy && (per_temp || temperature > 0.0f);
-  const bool need_tv = need_sample && (per_rule || rule == SPC_RULE_OPT);
+  // OPT (D_TV) and the token rules (eta) need the second pass over their rows
+  const bool need_tv = need_sample && (per_rule || rule == SPC_RULE_OPT || rule >= SPC_RULE_TOKEN_V1);
   const bool need_argmax = force_greedy || per_temp;
   e = spc::launch_verify(P, dtype, vec, need_tv, need_sample, need_argmax,
                                     ex ? ex->ev_hot_begin : nullptr,

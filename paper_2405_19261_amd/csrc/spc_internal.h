@@ -13,8 +13,9 @@ namespace spc {
 constexpr int kThreads = 256;  // four 64-lane wavefronts per workgroup
 
 // Sampling distribution at j* (Alg. 4): the residual max(0, p - q), or the
-// extra-token target pi_{t+gamma}, which is q or p.
-enum SampleKind : int32_t { kNone = -1, kResidual = 0, kQ = 1, kP = 2 };
+// extra-token target pi_{t+gamma}, which is q or p; for a token rule the
+// residual max(0, pi - q) or pi_{t+gamma} of the target of Alg. 6.
+enum SampleKind : int32_t { kNone = -1, kResidual = 0, kQ = 1, kP = 2, kTokRes = 3, kTokPi = 4 };
 
 // Partial statistics of one (row, stats tile), both tensors.  With c the
 // per-sequence log2(e)/T:  s = sum over the tile of 2^(z*c - r),  r the
@@ -29,7 +30,7 @@ struct TilePart {
 // Per-row statistics after merging the tiles of a row.
 struct RowStat {
   double lz_q, lz_p;      // log2 sum_v 2^(z_v * c)  (= lse / ln 2)
-  double tv;              // D_TV(p, q) for OPT rows, else 0
+  double tv;              // D_TV(p, q) for OPT rows, eta for token-rule rows, else 0
   float zmax_q, zmax_p;
   int32_t amax_q, amax_p;
 };
@@ -66,7 +67,7 @@ struct Params {
   // workspace
   uint32_t* samp_cnt;     // [B]   sampling workgroups of a sequence done
   TilePart* tiles;        // [R][nt] statistics partials
-  double* tvpart;         // [R][nt] TV partials
+  double* tvpart;         // [R][nt] TV partials (OPT) or eta partials (token rules)
   double* masses;         // [B][nc] residual chunk masses of row j*
 };
 
@@ -84,8 +85,8 @@ struct WsLayout {
 };
 WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec);
 
-// Enqueue the kernels of one verify call.  need_tv: the batch may hold OPT
-// sequences at temperature > 0; need_sample: it may hold sequences at
+// Enqueue the kernels of one verify call.  need_tv: the batch may hold OPT or
+// token-rule sequences at temperature > 0; need_sample: it may hold sequences at
 // temperature > 0; need_argmax: it may hold greedy (temperature 0)
 // sequences.  Returns the first launch error.
 hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,

@@ -331,7 +331,7 @@ __device__ __forceinline__ SeqParam seq_param(const Params& P, int b) {
   const float alpha = P.alpha_ps ? P.alpha_ps[b] : P.alpha;
   const float T = P.temp_ps ? P.temp_ps[b] : P.temp;
   s.alpha = (double)alpha;
-  s.valid = s.rule >= SPC_RULE_CHOW && s.rule <= SPC_RULE_NEVER && isfinite(alpha) &&
+  s.valid = s.rule >= SPC_RULE_CHOW && s.rule <= SPC_RULE_TOKEN_V3 && isfinite(alpha) &&
             isfinite(T) && T >= 0.0f && (T == 0.0f || T >= 1e-20f);
   s.greedy = P.force_greedy || T == 0.0f;
   s.c = kLog2e / ((s.greedy || !s.valid) ? 1.0 : (double)T);
@@ -344,8 +344,58 @@ __device__ __forceinline__ SeqParam seq_param(const Params& P, int b) {
   return s;
 }
 
-__device__ __forceinline__ bool needs_tv(const SeqParam& s) {
-  return s.valid && !s.greedy && s.rule == SPC_RULE_OPT;
+__device__ __forceinline__ bool is_token(int rule) {
+  return rule >= SPC_RULE_TOKEN_V1 && rule <= SPC_RULE_TOKEN_V3;
+}
+
+// Sequences whose rows need the second pass: OPT (D_TV of Lemma 3) and the
+// token rules (eta of Alg. 6) at temperature > 0.
+__device__ __forceinline__ bool needs_pass2(const SeqParam& s) {
+  return s.valid && !s.greedy && (s.rule == SPC_RULE_OPT || is_token(s.rule));
+}
+
+// Token-specific rules (Section 4.4) as a threshold on one logit of the row:
+// r(v) = 1 iff z(v) < theta, z the drafter's logit for TokenV1 (q(v) <
+// max p - alpha) and the verifier's for TokenV2 (p(v) < max p - alpha) and
+// TokenV3 (p(v) < max p (1 - alpha)).  theta is solved in fp64 from the row
+// statistics and rounded upward to float, so that z < theta in float equals
+// the comparison against the fp64 threshold; a threshold at or below zero
+// probability gives theta = -inf (r = 0 everywhere).
+struct TokenRule {
+  float theta;
+  bool on_p;
+};
+
+// The threshold is written as max p * f, f = 1 - alpha (V3) or
+// 1 - alpha / max p (V1, V2), and moved into logit space relative to the
+// largest p logit: p(v) < max p f  <=>  z_p(v) < zmax_p + log2(f) / c, and
+// for V1 q(v) < max p f  <=>  z_q(v) < zmax_p + (lz_q - lz_p + log2 f) / c.
+// Rounding up to float keeps the comparison exact for float logits.  Tokens
+// attaining max p (V2, V3) get the exact verdict 1(alpha < 0) whatever the
+// rounding of log2 f.
+__device__ __forceinline__ TokenRule token_rule(const SeqParam& s, const RowStat& rs,
+                                                double maxp) {
+  TokenRule t;
+  t.on_p = s.rule != SPC_RULE_TOKEN_V1;
+  const double f = s.rule == SPC_RULE_TOKEN_V3 ? 1.0 - s.alpha : 1.0 - s.alpha / maxp;
+  double th = -__builtin_huge_val();
+  if (f > 0.0) {
+    const double g = log2(f) + (t.on_p ? 0.0 : rs.lz_q - rs.lz_p);
+    th = (double)rs.zmax_p + g / s.c;
+  }
+  float theta = __double2float_ru(th);
+  if (t.on_p) {
+    if (s.alpha < 0.0f)
+      theta = fmaxf(theta, nextafterf(rs.zmax_p, __builtin_huge_valf()));
+    else
+      theta = fminf(theta, rs.zmax_p);
+  }
+  t.theta = theta;
+  return t;
+}
+
+__device__ __forceinline__ bool token_r(const TokenRule& t, float zq, float zp) {
+  return (t.on_p ? zp : zq) < t.theta;
 }
 
 // log2 of a normalised probability, evaluated as two float32 halves:
@@ -354,18 +404,29 @@ struct ProbScale {
   float c_hi, c_lo, q_hi, q_lo, p_hi, p_lo;
   double c;   // log2(e) / T
   double dl;  // lz_p - lz_q
+  TokenRule tok;  // token rules only
 };
 
-__device__ __forceinline__ ProbScale prob_scale(const SeqParam& s, const RowStat& rs) {
+// With `token` (a token rule's distributions) the p scale carries eta:
+// p(v) eta = 2^(z c - (lz_p - log2 eta)), so the weights of Alg. 6's target
+// reuse the p-side formulas (eta = 0 leaves every p-side weight at 0).
+__device__ __forceinline__ ProbScale prob_scale(const SeqParam& s, const RowStat& rs,
+                                                bool token = false) {
   ProbScale ps;
   ps.c_hi = s.c_hi;
   ps.c_lo = s.c_lo;
   ps.q_hi = (float)rs.lz_q;
   ps.q_lo = (float)(rs.lz_q - (double)ps.q_hi);
-  ps.p_hi = (float)rs.lz_p;
-  ps.p_lo = (float)(rs.lz_p - (double)ps.p_hi);
   ps.c = s.c;
-  ps.dl = rs.lz_p - rs.lz_q;
+  double lzp = rs.lz_p;
+  ps.tok = TokenRule{kNegInf, false};
+  if (token) {
+    ps.tok = token_rule(s, rs, exp2_acc((double)rs.zmax_p * s.c - rs.lz_p));
+    lzp = rs.tv > 0.0 ? rs.lz_p - log2(rs.tv) : __builtin_huge_val();
+  }
+  ps.p_hi = (float)lzp;
+  ps.p_lo = isfinite(lzp) ? (float)(lzp - (double)ps.p_hi) : 0.0f;
+  ps.dl = lzp - rs.lz_q;
   return ps;
 }
 
@@ -401,11 +462,27 @@ __device__ __forceinline__ float residual_weight(float zq, float zp, const ProbS
   return d > 0.0f ? w : 0.0f;
 }
 
+// Weight of one entry under a sampled distribution.  With a token rule the p
+// scale carries eta (prob_scale): the residual max(0, pi - q) of Alg. 6's
+// target is p eta where r = 0 and max(0, p eta - q) where r = 1, and the
+// target itself is p eta where r = 1 and q + p eta where r = 0.
 template <int KIND>
 __device__ __forceinline__ float weight_of(float zq, float zp, const ProbScale& s) {
-  if constexpr (KIND == kQ) return prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
-  else if constexpr (KIND == kP) return prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
-  else return residual_weight(zq, zp, s);
+  if constexpr (KIND == kQ) {
+    return prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
+  } else if constexpr (KIND == kP) {
+    return prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
+  } else if constexpr (KIND == kResidual) {
+    return residual_weight(zq, zp, s);
+  } else if constexpr (KIND == kTokRes) {
+    float res = residual_weight(zq, zp, s), pe = prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
+    asm volatile("" : "+v"(res), "+v"(pe));
+    return token_r(s.tok, zq, zp) ? res : pe;
+  } else {
+    const float pe = prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
+    const float qe = prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
+    return token_r(s.tok, zq, zp) ? pe : qe + pe;
+  }
 }
 
 template <int DT>
@@ -417,6 +494,7 @@ __device__ __forceinline__ float load_logit(const void* base, int64_t row, int V
     return reinterpret_cast<const float*>(base)[i];
   }
 }
+
 
 // Table 1 deferral rules (strict inequalities as printed).
 __device__ __forceinline__ int defer_rule(int rule, double alpha, double maxq, double maxp,
@@ -509,7 +587,8 @@ __device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy
 // ------------------------------------------------------------- decision
 // delta_j by the rule of Table 1 and the accept draw a_j of Alg. 4 for row j
 // of a sequence, from its merged statistics.  x is the draft token x_{t+j},
-// zqx / zpx its two logits and u its uniform (lane-uniform values).
+// zqx / zpx its two logits and u its uniform (lane-uniform values).  For a
+// greedy token-rule row, zpx is p's logit at the drafter's argmax instead.
 __device__ __forceinline__ RowDecision decide_row(const SeqParam& sp, const RowStat& rs, int j,
                                                   int gamma, int V, int x, float zqx, float zpx,
                                                   float u) {
@@ -518,10 +597,40 @@ __device__ __forceinline__ RowDecision decide_row(const SeqParam& sp, const RowS
   d.u = u;
   const double maxq = exp2_acc((double)rs.zmax_q * sp.c - rs.lz_q);
   const double maxp = exp2_acc((double)rs.zmax_p * sp.c - rs.lz_p);
-  // greedy: one-hot q~, p~ give D_TV = 1(argmax q != argmax p)  (Lemma 6)
-  const double tv = sp.greedy ? (rs.amax_q != rs.amax_p ? 1.0 : 0.0) : rs.tv;
   d.maxq = (float)maxq;
   d.maxp = (float)maxp;
+  if (is_token(sp.rule)) {
+    // Alg. 6's target pi = q (1 - r) + p eta; reported delta_j = r(x_j)
+    const TokenRule tr = token_rule(sp, rs, maxp);
+    if (sp.greedy) {
+      // r at argmax q (temperature-1 statistics): one-hot pi~ at argmax p
+      // when r = 1, else at argmax q; eta~ = r
+      // (TokenV1 there is max q < max p - alpha: Diff's comparison, made alike)
+      d.delta = tr.on_p ? zpx < tr.theta
+                        : defer_rule(SPC_RULE_DIFF, sp.alpha, maxq, maxp, 0.0);
+      d.tv = (float)d.delta;
+      d.keep = j < gamma && x >= 0 && x < V && x == (d.delta ? rs.amax_p : rs.amax_q);
+      return d;
+    }
+    d.tv = (float)rs.tv;
+    if (j >= gamma || x < 0 || x >= V) {
+      d.delta = 0;
+      d.keep = 0;  // a_gamma = 0; a draft outside the vocabulary is rejected
+    } else {
+      d.delta = token_r(tr, zqx, zpx);
+      if (!d.delta || zqx == kNegInf) {
+        d.keep = 1;  // pi(x) >= q(x)
+      } else {
+        // pi(x) / q(x) = p(x) eta / q(x) = 2^dd
+        const double le = rs.tv > 0.0 ? log2(rs.tv) : -__builtin_huge_val();
+        const double dd = ((double)zpx - (double)zqx) * sp.c - (rs.lz_p - rs.lz_q) + le;
+        d.keep = !(dd < 0.0) || (double)u < exp2_acc(dd);
+      }
+    }
+    return d;
+  }
+  // greedy: one-hot q~, p~ give D_TV = 1(argmax q != argmax p)  (Lemma 6)
+  const double tv = sp.greedy ? (rs.amax_q != rs.amax_p ? 1.0 : 0.0) : rs.tv;
   d.tv = (float)tv;
   d.delta = defer_rule(sp.rule, sp.alpha, maxq, maxp, tv);
   if (j >= gamma || x < 0 || x >= V) {
@@ -594,9 +703,13 @@ __device__ __forceinline__ void finish_seq(const Params& P, int b, const SeqPara
         if (P.out_norm) P.out_norm[b] = 1.0f;
       }
     } else {
-      // a rejection with delta = 0 only happens for an out-of-range draft;
-      // its residual max(0, q - q) is empty, so p is sampled instead
-      s.kind = (jstar < gamma) ? (dstar ? kResidual : kP) : (dstar ? kP : kQ);
+      if (is_token(sp.rule)) {
+        s.kind = (jstar < gamma) ? kTokRes : kTokPi;
+      } else {
+        // a rejection with delta = 0 only happens for an out-of-range draft;
+        // its residual max(0, q - q) is empty, so p is sampled instead
+        s.kind = (jstar < gamma) ? (dstar ? kResidual : kP) : (dstar ? kP : kQ);
+      }
       s.u = ug;
     }
     if (write) P.out_accept[b] = jstar;
@@ -618,7 +731,8 @@ __device__ __forceinline__ void decide_seq(const Params& P, int b, const SeqPara
     // data (lane l of wave wv takes row wv + kSampWaves * l) go out together;
     // the logits at the draft tokens follow the tokens and stay in flight
     // while the rows merge.
-    const bool tv = needs_tv(sp);
+    const bool tv = needs_pass2(sp);
+    const bool greedy_tok = sp.greedy && is_token(sp.rule) && sp.rule != SPC_RULE_TOKEN_V1;
     PartHead h{};
     if (wv < g1) h = load_head(P, b * g1 + wv, tv);
     const int jl = wv + kSampWaves * lane;
@@ -642,8 +756,12 @@ __device__ __forceinline__ void decide_seq(const Params& P, int b, const SeqPara
       if (j + kSampWaves < g1) hn = load_head(P, b * g1 + j + kSampWaves, tv);
       const RowStat rs = merge_row(P, b * g1 + j, sp.greedy, tv, h);
       h = hn;
+      // greedy TokenV2/V3: the rule reads p at the drafter's argmax
+      const float zpa = (greedy_tok && rs.amax_q >= 0 && rs.amax_q < V)
+                            ? load_logit<DT>(P.p, (int64_t)b * g1 + j, V, rs.amax_q)
+                            : lane_f32(zpx, i);
       const RowDecision d = decide_row(sp, rs, j, gamma, V, lane_i32(x, i), lane_f32(zqx, i),
-                                       lane_f32(zpx, i), lane_f32(u, i));
+                                       zpa, lane_f32(u, i));
       if (lane == 0) ss.rows[j] = d;
     }
   }
@@ -686,9 +804,10 @@ __device__ __forceinline__ void load_chunk(const char* row, int64_t c0, int V, C
 
 // Sources of the part masses of the sampled distribution: the statistics
 // partials per tile (q or p: each tile's share of the normaliser), the TV
-// partials per tile (the residual of an OPT row, which the TV pass summed),
+// partials per tile (the residual of an OPT row, which the second pass
+// summed), the statistics and eta partials together (a token rule's target),
 // or the residual masses per SampChunk computed by the sampling pass.
-enum MassSrc : int { kSrcStatsQ = 0, kSrcStatsP = 1, kSrcTv = 2, kSrcPass = 3 };
+enum MassSrc : int { kSrcStatsQ = 0, kSrcStatsP = 1, kSrcTv = 2, kSrcPass = 3, kSrcTokPi = 4 };
 
 template <int SRC>
 __device__ __forceinline__ double part_mass(const Params& P, int64_t row, int b, int k,
@@ -701,6 +820,13 @@ __device__ __forceinline__ double part_mass(const Params& P, int64_t row, int b,
     return t.s_p * exp2_acc((double)t.r_p - rs.lz_p);
   } else if constexpr (SRC == kSrcTv) {
     return P.tvpart[row * P.nt + k];
+  } else if constexpr (SRC == kSrcTokPi) {
+    // Alg. 6's target over a tile: its q mass less the eta partial (the q
+    // mass where r = 1), plus eta times its p mass
+    const TilePart& t = P.tiles[row * P.nt + k];
+    const double qm = t.s_q * exp2_acc((double)t.r_q - rs.lz_q);
+    const double pm = t.s_p * exp2_acc((double)t.r_p - rs.lz_p);
+    return fmax(qm - P.tvpart[row * P.nt + k], 0.0) + rs.tv * pm;
   } else {
     return ld_dev_f64(P.masses + (int64_t)b * P.nc + k);
   }
@@ -774,12 +900,12 @@ __device__ __forceinline__ double find_part(const Params& P, int64_t row, int b,
   return W;
 }
 
-// Whole block: residual masses max(0, p - q) of the SampChunks of a row (K
+// Whole block: residual masses (KIND) of the SampChunks of a row (K
 // sampling workgroups per sequence): wave w of workgroup kw takes chunks
 // kw * kSampWaves + w, then + K * kSampWaves, ...; the next chunk loads while
 // one is summed, and chunk c's mass goes to masses[c].  No block barrier:
 // every wave drains its own stores.
-template <int DT, bool VEC>
+template <int DT, bool VEC, int KIND>
 __device__ __forceinline__ void residual_masses(const char* qrow, const char* prow, int V, int nc,
                                                 int K, int kw, const ProbScale& ps,
                                                 double* masses) {
@@ -807,7 +933,7 @@ __device__ __forceinline__ void residual_masses(const char* qrow, const char* pr
       float t = 0.0f;
 #pragma unroll
       for (int e = 0; e < C::VW; ++e)
-        t += residual_weight(elem<DT, VEC>(wq[i], e), elem<DT, VEC>(wp[i], e), ps);
+        t += weight_of<KIND>(elem<DT, VEC>(wq[i], e), elem<DT, VEC>(wp[i], e), ps);
       acc += (double)t;
     }
     acc = wave_sum(acc);
@@ -946,8 +1072,9 @@ __device__ __forceinline__ void draw(const Params& P, int b, int64_t row, int ki
     if (src == kSrcStatsQ) W = find_part<kSrcStatsQ>(P, row, b, P.nt, rs, u, &ks, &rem);
     else if (src == kSrcStatsP) W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
     else if (src == kSrcTv) W = find_part<kSrcTv>(P, row, b, P.nt, rs, u, &ks, &rem);
+    else if (src == kSrcTokPi) W = find_part<kSrcTokPi>(P, row, b, P.nt, rs, u, &ks, &rem);
     else W = find_part<kSrcPass>(P, row, b, P.nc, rs, u, &ks, &rem);
-    if (kind == kResidual && !(W > 0.0)) {
+    if ((kind == kResidual || kind == kTokRes) && !(W > 0.0)) {
       kind = kP;
       src = kSrcStatsP;
       W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
@@ -961,16 +1088,22 @@ __device__ __forceinline__ void draw(const Params& P, int b, int64_t row, int ki
   __syncthreads();
   const PickState pk = ss.pk;
   if (pk.k < 0) return;  // block-uniform
-  const ProbScale ps = prob_scale(sp, rs);
+  const ProbScale ps = prob_scale(sp, rs, pk.kind == kTokRes || pk.kind == kTokPi);
   constexpr int TN = StatTile<DT, VEC>::N;
   if (pk.src == kSrcPass) {
     using SC = SampChunk<DT, VEC>;
-    if (threadIdx.x < 64)
-      pick_wave<DT, VEC, SC, kResidual>(P, b, row, (int64_t)pk.k * SC::N, pk.rem, ps);
+    if (threadIdx.x < 64) {
+      if (pk.kind == kTokRes)
+        pick_wave<DT, VEC, SC, kTokRes>(P, b, row, (int64_t)pk.k * SC::N, pk.rem, ps);
+      else
+        pick_wave<DT, VEC, SC, kResidual>(P, b, row, (int64_t)pk.k * SC::N, pk.rem, ps);
+    }
   } else if (pk.kind == kQ) {
     pick_tile<DT, VEC, kQ>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
   } else if (pk.kind == kP) {
     pick_tile<DT, VEC, kP>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
+  } else if (pk.kind == kTokPi) {
+    pick_tile<DT, VEC, kTokPi>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
   } else {
     pick_tile<DT, VEC, kResidual>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
   }
@@ -1107,7 +1240,7 @@ __global__ __launch_bounds__(kThreads) void k_tv(Params P) {
   __shared__ RowStat srow;
   const int k = blockIdx.x, r = blockIdx.y;
   const SeqParam sp = seq_param(P, r / (P.gamma + 1));
-  if (!needs_tv(sp)) return;  // block-uniform
+  if (!needs_pass2(sp)) return;  // block-uniform
   const int V = P.V;
   const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
   const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
@@ -1120,14 +1253,20 @@ __global__ __launch_bounds__(kThreads) void k_tv(Params P) {
     if (threadIdx.x == 0) srow = rs;
   }
   __syncthreads();
-  const ProbScale ps = prob_scale(sp, srow);
+  const bool tok = is_token(sp.rule);  // block-uniform
+  const ProbScale ps = prob_scale(sp, srow, tok);
   double acc = 0.0;
 #pragma unroll
   for (int i = 0; i < T::U; ++i) {
     float t = 0.0f;
 #pragma unroll
-    for (int e = 0; e < T::VW; ++e)
-      t += residual_weight(elem<DT, VEC>(wq[i], e), elem<DT, VEC>(wp[i], e), ps);
+    for (int e = 0; e < T::VW; ++e) {
+      const float zq = elem<DT, VEC>(wq[i], e), zp = elem<DT, VEC>(wp[i], e);
+      if (tok)  // eta: the q mass of the entries the rule marks
+        t += token_r(ps.tok, zq, zp) ? prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo) : 0.0f;
+      else
+        t += residual_weight(zq, zp, ps);
+    }
     acc += (double)t;
   }
   double unused = 0.0;
@@ -1153,19 +1292,27 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
   if (s.kind == kNone) return;  // block-uniform
   const int64_t row = (int64_t)b * (P.gamma + 1) + s.row;
   const RowStat rs = ss.rows[s.row].rs;
-  if (s.kind != kResidual || needs_tv(sp)) {
+  const bool pass = s.kind == kTokRes || (s.kind == kResidual && sp.rule != SPC_RULE_OPT);
+  if (!pass) {
     if (k != 0) return;  // block-uniform
-    const int src = s.kind == kQ ? kSrcStatsQ : s.kind == kP ? kSrcStatsP : kSrcTv;
+    const int src = s.kind == kQ     ? kSrcStatsQ
+                    : s.kind == kP   ? kSrcStatsP
+                    : s.kind == kTokPi ? kSrcTokPi
+                                       : kSrcTv;
     draw<DT, VEC>(P, b, row, s.kind, src, s.u, sp, rs, ss, sh);
     return;
   }
   constexpr int EB = StatTile<DT, VEC>::EB;
-  const ProbScale ps = prob_scale(sp, rs);
+  const ProbScale ps = prob_scale(sp, rs, s.kind == kTokRes);
   const char* qrow = (const char*)P.q + row * P.V * EB;
   const char* prow = (const char*)P.p + row * P.V * EB;
-  residual_masses<DT, VEC>(qrow, prow, P.V, P.nc, P.K, k, ps, P.masses + (int64_t)b * P.nc);
+  double* masses = P.masses + (int64_t)b * P.nc;
+  if (s.kind == kTokRes)
+    residual_masses<DT, VEC, kTokRes>(qrow, prow, P.V, P.nc, P.K, k, ps, masses);
+  else
+    residual_masses<DT, VEC, kResidual>(qrow, prow, P.V, P.nc, P.K, k, ps, masses);
   if (!arrive_last(P.samp_cnt + b, (uint32_t)P.K, sh)) return;
-  draw<DT, VEC>(P, b, row, kResidual, kSrcPass, s.u, sp, rs, ss, sh);
+  draw<DT, VEC>(P, b, row, s.kind, kSrcPass, s.u, sp, rs, ss, sh);
 }
 
 template <int DT, bool VEC>

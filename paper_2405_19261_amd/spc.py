@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspeccasc
 
 SPC_F32, SPC_BF16 = 0, 1
 SPC_RULE_CHOW, SPC_RULE_DIFF, SPC_RULE_OPT, SPC_RULE_ALWAYS, SPC_RULE_NEVER = range(5)
+SPC_RULE_TOKEN_V1, SPC_RULE_TOKEN_V2, SPC_RULE_TOKEN_V3 = 5, 6, 7
 SPC_MAX_GAMMA = 63
 STATUS = {0: "SPC_OK", -1: "SPC_E_NULL", -2: "SPC_E_SHAPE", -3: "SPC_E_RULE",
           -4: "SPC_E_PARAM", -5: "SPC_E_ALIGN", -6: "SPC_E_WORKSPACE", -7: "SPC_E_HIP"}

@@ -22,7 +22,9 @@ import torch
 
 # Rule codes (same numbering as the C interface).
 CHOW, DIFF, OPT, ALWAYS, NEVER = 0, 1, 2, 3, 4
-RULE_NAMES = {CHOW: "chow", DIFF: "diff", OPT: "opt", ALWAYS: "always", NEVER: "never"}
+TOKEN_V1, TOKEN_V2, TOKEN_V3 = 5, 6, 7
+RULE_NAMES = {CHOW: "chow", DIFF: "diff", OPT: "opt", ALWAYS: "always", NEVER: "never",
+              TOKEN_V1: "token-v1", TOKEN_V2: "token-v2", TOKEN_V3: "token-v3"}
 
 
 @dataclass(frozen=True)

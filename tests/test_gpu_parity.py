@@ -47,7 +47,7 @@ def test_workload_parity(cfg, steps):
     rep = parity.parity_workload(wl, _steps(cfg, steps))
     _flush(f"[parity] cfg{cfg} {dict(rep)}")
     assert rep["exact"] + rep["excused_defer"] + rep["excused_accept"] + \
-        rep["excused_token"] == rep["sequences"]
+        rep["excused_token"] + rep["excused_eta"] == rep["sequences"]
 
 
 @pytest.mark.parametrize("part", range(4))
@@ -238,3 +238,112 @@ def test_run_to_run_determinism_full_size():
         for k in a:
             np.testing.assert_array_equal(a[k], b[k])
         del inp
+
+
+# ------------------------------------------------- token-specific rules (4.4)
+
+TOKEN_ALPHAS = {W.TOKEN_V1: (0.0, 0.05, 0.3), W.TOKEN_V2: (0.0, 0.05, 0.3),
+                W.TOKEN_V3: (0.1, 0.5, 0.9)}
+
+
+@pytest.mark.parametrize("rule", [W.TOKEN_V1, W.TOKEN_V2, W.TOKEN_V3])
+@pytest.mark.parametrize("cfg,steps", [(2, 40), (3, 6)])
+def test_token_rule_parity(rule, cfg, steps):
+    """Alg. 6 target on the T5-vocabulary float32 shape and the Gemma-vocabulary
+    bfloat16 shape, several alpha per rule."""
+    for alpha in TOKEN_ALPHAS[rule]:
+        wl = W.WORKLOADS[cfg].with_(rule=rule, alpha=alpha, temperature=1.0)
+        name = f"cfg{cfg}.{W.RULE_NAMES[rule]}.{alpha}"
+        _flush(f"[token] {name} steps={steps}")
+        rep = parity.parity_workload(wl, steps, step0=900, report_name=name)
+        _flush(f"[token] {name} {dict(rep)}")
+
+
+@pytest.mark.parametrize("rule", [W.TOKEN_V1, W.TOKEN_V2, W.TOKEN_V3])
+def test_token_rule_plain_entry_point(rule):
+    """The batch-wide entry point without statistics, at the benchmark's shape."""
+    wl = W.WORKLOADS[3].with_(rule=rule, alpha=0.3 if rule == W.TOKEN_V3 else 0.05)
+    rep = parity.parity_workload(wl, 3, stats=False, step0=700,
+                                 report_name=f"cfg3.plain.{W.RULE_NAMES[rule]}")
+    assert rep["sequences"] == 3 * 32
+
+
+@pytest.mark.parametrize("rule", [W.TOKEN_V1, W.TOKEN_V2, W.TOKEN_V3])
+def test_token_rule_greedy_parity(rule):
+    """Temperature 0: r read at the drafter's argmax, one-hot target."""
+    for alpha in (0.0, 0.05, 0.3):
+        wl = W.WORKLOADS[4].with_(B=64, V=50000, rule=rule, alpha=alpha)
+        _flush(f"[token] greedy {W.RULE_NAMES[rule]} alpha={alpha}")
+        parity.parity_workload(wl, 4, step0=300, report_name=f"greedy.{W.RULE_NAMES[rule]}")
+
+
+def test_token_greedy_v1_equals_diff_on_gpu():
+    """At T = 0 the drafter's argmax carries max q, so TokenV1 is the Diff rule."""
+    wl = W.WORKLOADS[4].with_(B=64, V=50000)
+    inp = W.generate(wl, 6, DEV)
+    for alpha in (0.0, 0.05, 0.3):
+        outs = []
+        for rule in (W.TOKEN_V1, W.DIFF):
+            inp["rule"][:] = rule
+            inp["alpha"][:] = alpha
+            outs.append(parity.run_gpu(inp, greedy=True, stats=False))
+        for k in ("accept_len", "next_token", "defer"):
+            np.testing.assert_array_equal(outs[0][k], outs[1][k])
+
+
+@pytest.mark.parametrize("rule,alpha", [(W.TOKEN_V2, -0.5), (W.TOKEN_V3, -0.5),
+                                        (W.TOKEN_V1, 1.0), (W.TOKEN_V2, 1.5),
+                                        (W.TOKEN_V3, 1.0), (W.TOKEN_V3, 2.0)])
+def test_token_rule_extremes(rule, alpha):
+    """alpha < 0 defers every token under V2/V3 (eta = 1, the target is p);
+    alpha >= 1 under V1/V2 and V3 at alpha >= 1 (threshold <= 0) defers none
+    (eta = 0, the target is q)."""
+    for cfg in (3, 2):
+        wl = W.WORKLOADS[cfg].with_(B=8, V=30000, rule=rule, alpha=alpha)
+        inp = W.generate(wl, 12, DEV)
+        g = parity.run_gpu(inp)
+        h = parity.host_inputs(inp)
+        parity.compare(g, parity.run_oracle(h), h, wl.dtype)
+        eta = g["row_stats"][..., 6]
+        if alpha < 0:
+            np.testing.assert_allclose(eta, 1.0, rtol=0, atol=1e-5)
+            assert (g["defer"][:, :-1] == 1).all()
+        else:
+            assert (eta == 0).all()
+            assert (g["defer"] == 0).all()
+            assert (g["accept_len"] == wl.gamma).all()
+
+
+def test_token_rules_mixed_per_sequence():
+    """Token rules next to sequence-level rules and per-sequence temperatures."""
+    wl = W.WORKLOADS[5].with_(B=24, V=30000)
+    inp = W.generate(wl, 8, DEV)
+    rules = [W.TOKEN_V1, W.TOKEN_V2, W.TOKEN_V3, W.OPT, W.DIFF, W.CHOW]
+    inp["rule"][:] = torch.tensor([rules[i % 6] for i in range(24)], dtype=torch.int32,
+                                  device=DEV)
+    inp["alpha"][:] = torch.tensor([0.05, 0.05, 0.3, 0.1, 0.05, 0.3] * 4, device=DEV)
+    g = parity.run_gpu(inp)
+    h = parity.host_inputs(inp)
+    rep = parity.compare(g, parity.run_oracle(h), h, wl.dtype)
+    _flush(f"[token] mixed {dict(rep)}")
+
+
+def test_token_rule_identical_models():
+    """p = q: V1 and V2 coincide (both compare q(v) with max q - alpha), and a
+    draft the rule accepts is always kept, since pi(v) = q(v) (1 + eta) there."""
+    wl = W.WORKLOADS[3].with_(B=16, V=20000)
+    inp = W.generate(wl, 3, DEV)
+    inp["p"] = inp["q"].clone()
+    outs = {}
+    for rule in (W.TOKEN_V1, W.TOKEN_V2, W.TOKEN_V3):
+        inp["rule"][:] = rule
+        inp["alpha"][:] = 0.05
+        g = outs[rule] = parity.run_gpu(inp)
+        for b in range(wl.B):
+            j = int(g["accept_len"][b])
+            if j < wl.gamma:  # a rejected draft must carry r = 1
+                assert g["defer"][b, j] == 1
+        h = parity.host_inputs(inp)
+        parity.compare(g, parity.run_oracle(h), h, wl.dtype)
+    for k in ("accept_len", "next_token", "defer", "row_stats"):
+        np.testing.assert_array_equal(outs[W.TOKEN_V1][k], outs[W.TOKEN_V2][k])

@@ -68,8 +68,17 @@ def test_token_rule_hand_cases(orc):
     # V3: p(v) < max p (1 - alpha)
     assert orc.token_r(V3, 0.5, 0.0, 0.24, 0.5)[0] == 1
     assert orc.token_r(V3, 0.5, 0.0, 0.25, 0.5)[0] == 0
-    # relative margin: |0.3 - 0.4| / 0.4
-    assert orc.token_r(V1, 0.1, 0.3, 0.0, 0.5)[1] == pytest.approx(0.25)
+    # margins: |0.3 - 0.4| / max(0.3, 0.4, max p = 0.5) for V1 (the threshold
+    # max p - alpha carries the rounding of max p), |0.2 - 0.3| / 0.3 for V3
+    assert orc.token_r(V1, 0.1, 0.3, 0.0, 0.5)[1] == pytest.approx(0.2)
+    assert orc.token_r(V3, 0.4, 0.0, 0.2, 0.5)[1] == pytest.approx(1.0 / 3.0)
+    # a token attaining max p: max p < max p - alpha  <=>  alpha < 0, exactly
+    for rule in (V2, V3):
+        assert orc.token_r(rule, 0.0, 0.9, 0.5, 0.5) == (0, np.inf)
+        assert orc.token_r(rule, -1e-30, 0.9, 0.5, 0.5) == (1, np.inf)
+        assert orc.token_r(rule, 1e-30, 0.9, 0.5, 0.5) == (0, np.inf)
+    # V1 has no such tie: q(v) = max p at alpha = 0 is a plain equality
+    assert orc.token_r(V1, 0.0, 0.5, 0.1, 0.5) == (0, 0.0)
 
 
 @pytest.mark.parametrize("rule", [V2, V3])
