@@ -1,13 +1,15 @@
 """Throughput of the speculative-cascade verify step on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--sets S] [--no-cpu-baseline]
-                    [--copy-calib-mb N]
+                    [--copy-calib-mb N] [--rule NAME --alpha A]
     python bench.py --traffic-from FETCH.csv WRITE.csv --copy-calib-mb N
 
 A step is one spc_verify call (statistics pass + residual sampling pass) on
 the Gemma-vocabulary workload: B=32 sequences, gamma=7 drafted positions,
 V=256000, bfloat16 logits, Diff rule alpha=0.05, temperature 1 (seeded
-synthetic Zipf(1.2) logits).  Inputs are resident in HBM before timing; S
+synthetic Zipf(1.2) logits).  --rule / --alpha time the same shape under
+another rule (opt, or a token-specific rule token-v1/v2/v3, which add the
+second statistics pass).  Inputs are resident in HBM before timing; S
 distinct input sets (default 3 x 262 MB) are rotated so the 256 MB
 Infinity Cache cannot serve a repeat.
 
@@ -164,6 +166,10 @@ def main():
     ap.add_argument("--copy-calib-mb", type=int, default=0)
     ap.add_argument("--event-every", type=int, default=4)
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
+    ap.add_argument("--rule", default="diff",
+                    choices=["chow", "diff", "opt", "always", "never",
+                             "token-v1", "token-v2", "token-v3"])
+    ap.add_argument("--alpha", type=float, default=None)
     args = ap.parse_args()
     if args.traffic_from:
         if args.copy_calib_mb <= 0:
@@ -180,6 +186,10 @@ def main():
     from paper_2405_19261_amd import workloads as W
 
     wl = W.WORKLOADS[3]
+    rule = {v: k for k, v in W.RULE_NAMES.items()}[args.rule]
+    if rule != wl.rule or args.alpha is not None:
+        wl = wl.with_(rule=rule, alpha=wl.alpha if args.alpha is None else args.alpha)
+    rule_desc = f"{args.rule} alpha={wl.alpha:g}"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     if args.copy_calib_mb > 0:
@@ -241,7 +251,7 @@ def main():
         ms_per_step=ms_per_step, higher_is_better=True, scaling="weak", vs_baseline=None,
         dtype="f32", data="synthetic",
         config=dict(workload="gemma-vocab verify step: B=32 gamma=7 V=256000 bf16 logits, "
-                             "Diff alpha=0.05, T=1, Zipf(1.2)+N(0,1) verifier, "
+                             f"{rule_desc}, T=1, Zipf(1.2)+N(0,1) verifier, "
                              "0.8*verifier+N(0,1) drafter (10% rows +N(0,3))",
                     global_batch=B, positions_per_step=B * gamma,
                     algorithmic_bytes_per_step=wl.algorithmic_bytes(),

@@ -132,18 +132,20 @@ def test_out_of_range_drafts():
     inp["draft"][:, 2] = torch.tensor([-1, 3000, 1 << 30, -(1 << 30), 2999, 0, -5, 3001],
                                       dtype=torch.int32, device=DEV)
     inp["uniforms"][:, :2] = 0.0
-    for rule in (W.DIFF, W.NEVER, W.ALWAYS):
+    for rule in (W.DIFF, W.NEVER, W.ALWAYS, W.TOKEN_V1, W.TOKEN_V2, W.TOKEN_V3):
         inp["rule"][:] = rule
+        inp["alpha"][:] = 0.3 if rule == W.TOKEN_V3 else 0.05
         g = parity.run_gpu(inp)
         h = parity.host_inputs(inp)
         o = parity.run_oracle(h)
         parity.compare(g, o, h, wl.dtype)
 
 
-def test_masked_logits():
+@pytest.mark.parametrize("rule,alpha", [(W.OPT, 0.1), (W.TOKEN_V2, 0.05), (W.TOKEN_V3, 0.3)])
+def test_masked_logits(rule, alpha):
     """-inf entries (masked tokens) in both tensors."""
     for cfg, dtype in ((3, "bf16"), (2, "f32")):
-        wl = W.WORKLOADS[cfg].with_(B=8, V=12345, dtype=dtype, rule=W.OPT, alpha=0.1)
+        wl = W.WORKLOADS[cfg].with_(B=8, V=12345, dtype=dtype, rule=rule, alpha=alpha)
         inp = W.generate(wl, 2, DEV)
         g0 = torch.Generator(device=DEV).manual_seed(99)
         for k in ("q", "p"):
