@@ -16,6 +16,7 @@ _lib = None
 F32, BF16, F64 = 0, 1, 2
 CHOW, DIFF, OPT, ALWAYS, NEVER = 0, 1, 2, 3, 4
 TOKEN_V1, TOKEN_V2, TOKEN_V3 = 5, 6, 7
+LOSSY, BILD, CHOWLOG, DIFFLOG, OPTLOG = 8, 9, 10, 11, 12
 FLAG_DRAFT_OUT_OF_RANGE, FLAG_EMPTY_RESIDUAL = 1, 2
 
 _P = ctypes.c_void_p
@@ -50,6 +51,15 @@ def lib():
         L.orc_token_r.restype = ctypes.c_int
         L.orc_token_target.argtypes = [ctypes.c_int, _D, _P, _P, _I64, _D, _P, ctypes.POINTER(_D)]
         L.orc_token_target.restype = _D
+        L.orc_entropy_row.argtypes = [_P, ctypes.c_int, _I64, _D, ctypes.POINTER(RowStats)]
+        L.orc_entropy_row.restype = _D
+        L.orc_cross_entropy_row.argtypes = [_P, _P, ctypes.c_int, _I64, _D,
+                                            ctypes.POINTER(RowStats), ctypes.POINTER(RowStats)]
+        L.orc_cross_entropy_row.restype = _D
+        L.orc_log_defer.argtypes = [_D, _D, ctypes.POINTER(_D)]
+        L.orc_log_defer.restype = ctypes.c_int
+        L.orc_lossy_target.argtypes = [_D, _P, _P, _I64, _P]
+        L.orc_lossy_target.restype = None
         L.orc_sample.argtypes = [_P, _I64, _D, ctypes.POINTER(_D)]
         L.orc_sample.restype = _I32
         L.orc_verify.argtypes = [_P, _P, ctypes.c_int, _P, _P, _I32, _I32, _I64, _P, _P, _P,
@@ -99,6 +109,43 @@ def softmax_row(z, T=1.0):
     st = RowStats()
     lib().orc_softmax_row(_ptr(z), dt, V, float(T), _ptr(prob), ctypes.byref(st))
     return prob, st.m, st.lse, st.maxprob, st.argmax
+
+
+def _row_stats(z, dt, T):
+    st = RowStats()
+    lib().orc_softmax_row(_ptr(z), dt, z.shape[-1], float(T), None, ctypes.byref(st))
+    return st
+
+
+def entropy_row(z, T=1.0):
+    """H(softmax(z / T)) in nats."""
+    z, dt = _logits(z)
+    st = _row_stats(z, dt, T)
+    return lib().orc_entropy_row(_ptr(z), dt, z.shape[-1], float(T), ctypes.byref(st))
+
+
+def cross_entropy_row(zq, zp, T=1.0):
+    """-sum_v q(v) log p(v) for q = softmax(zq / T), p = softmax(zp / T)."""
+    zq, dt = _logits(zq)
+    zp, dt2 = _logits(zp)
+    assert dt == dt2 and zq.shape == zp.shape
+    sq, sp = _row_stats(zq, dt, T), _row_stats(zp, dt, T)
+    return lib().orc_cross_entropy_row(_ptr(zq), _ptr(zp), dt, zq.shape[-1], float(T),
+                                       ctypes.byref(sq), ctypes.byref(sp))
+
+
+def log_defer(s, threshold):
+    mg = _D()
+    d = lib().orc_log_defer(float(s), float(threshold), ctypes.byref(mg))
+    return d, mg.value
+
+
+def lossy_target(alpha, q, p):
+    q = np.ascontiguousarray(q, np.float64)
+    p = np.ascontiguousarray(p, np.float64)
+    pi = np.empty_like(q)
+    lib().orc_lossy_target(float(alpha), _ptr(q), _ptr(p), q.size, _ptr(pi))
+    return pi
 
 
 def tv(p, q):

@@ -10,6 +10,11 @@
  *   deferral delta    Table 1; eq. (2) Chow, eq. (5) Diff, eq. (11) OPT
  *   target pi         eq. (6), T_delta of Alg. 5
  *   token rules       Section 4.4 (TokenV1/V2/V3), target of Alg. 6
+ *   lossy target      Section 2 (lossy speculative decoding), Lemma 2, beta = 1
+ *   BiLD*             Table 1 (D > alpha); D as the cross-entropy of the
+ *                     experimental setup (temperature 0: -log p(argmax q))
+ *   log-loss rules    Table 3, eq. of ChowLog (App. B), DiffLog and OPTLog
+ *                     (App. D), with the entropy H(q) = -sum q log q
  *   accept / j* / residual / sample    Alg. 4 (GenSpecSample)
  *   greedy step       Lemma 6 (Appendix, greedy special case)
  *
@@ -24,6 +29,14 @@
  *     token (0 at the bonus position); at temperature 0 r is read at the
  *     drafter's argmax with temperature-1 probabilities, so the one-hot
  *     target sits at argmax p when r = 1 and at argmax q otherwise.
+ *   - the lossy target is not normalised; when every draft is kept the extra
+ *     token comes from p_{t+gamma}, as in the lossy procedure that Lemma 2
+ *     identifies Alg. 4 with.  alpha >= 1 is rejected.  The lossy rule has no
+ *     deferral decision: delta is reported as 0.
+ *   - BiLD's discrepancy at temperature 0 is -log p(argmax q) (a
+ *     non-negative discrepancy), as printed in the experimental setup.
+ *   - the log-loss rules at temperature 0 read the entropies of the
+ *     temperature-1 softmax, as the Table 1 rules read its max-probabilities.
  */
 #include "spc_oracle.h"
 
@@ -89,6 +102,50 @@ double orc_tv(const double* p, const double* q, int64_t V) {
     if (d > 0.0) tv += d;
   }
   return tv;
+}
+
+static double logprob_at(const void* z, int dtype, int64_t v, double T, double lse) {
+  return logit_at(z, dtype, v) / T - lse;
+}
+
+double orc_entropy_row(const void* z, int dtype, int64_t V, double T, const orc_row_stats* st) {
+  double h = 0.0;
+  for (int64_t v = 0; v < V; ++v) {
+    double lq = logprob_at(z, dtype, v, T, st->lse);
+    double qv = exp(lq);
+    if (qv > 0.0) h -= qv * lq; /* 0 log 0 = 0 */
+  }
+  return h;
+}
+
+double orc_cross_entropy_row(const void* zq, const void* zp, int dtype, int64_t V, double T,
+                             const orc_row_stats* sq, const orc_row_stats* sp) {
+  double d = 0.0;
+  for (int64_t v = 0; v < V; ++v) {
+    if (logit_at(zq, dtype, v) == -INFINITY) continue; /* q(v) = 0 */
+    double lp = logprob_at(zp, dtype, v, T, sp->lse);
+    if (lp == -INFINITY) return INFINITY; /* q(v) > 0 = p(v) */
+    d -= exp(logprob_at(zq, dtype, v, T, sq->lse)) * lp;
+  }
+  return d;
+}
+
+int orc_log_defer(double s, double threshold, double* margin) {
+  double scale = 1.0;
+  if (fabs(s) > scale) scale = fabs(s);
+  if (fabs(threshold) > scale) scale = fabs(threshold);
+  *margin = isinf(s) ? INFINITY : fabs(s - threshold) / scale;
+  return s > threshold ? 1 : 0;
+}
+
+void orc_lossy_target(double alpha, const double* q, const double* p, int64_t V, double* pi) {
+  const double beta = 1.0;
+  for (int64_t v = 0; v < V; ++v) {
+    double a = p[v] / (1.0 - alpha);
+    double lo = q[v] < a ? q[v] : a;
+    double b = p[v] / beta;
+    pi[v] = lo > b ? lo : b;
+  }
 }
 
 int orc_defer(int rule, double alpha, double maxq, double maxp, double tv, double* margin) {
@@ -203,8 +260,28 @@ int orc_num_threads(void) {
 #endif
 }
 
-static int rule_ok(int r) { return r >= ORC_CHOW && r <= ORC_TOKEN_V3; }
+static int rule_ok(int r, float alpha) {
+  if (r == ORC_LOSSY) return alpha < 1.0f;
+  return r >= ORC_CHOW && r <= ORC_OPTLOG;
+}
 static int is_token(int r) { return r >= ORC_TOKEN_V1 && r <= ORC_TOKEN_V3; }
+static int is_log(int r) { return r >= ORC_BILD && r <= ORC_OPTLOG; }
+
+/* the statistic s and threshold of a log-loss rule for one row */
+static void log_rule_stat(int rule, double alpha, double tv, const void* zq, const void* zp,
+                          int dtype, int64_t V, double T, const orc_row_stats* sq,
+                          const orc_row_stats* sp, double* s, double* threshold) {
+  if (rule == ORC_BILD) {
+    *s = orc_cross_entropy_row(zq, zp, dtype, V, T, sq, sp);
+    *threshold = alpha;
+  } else if (rule == ORC_CHOWLOG) {
+    *s = orc_entropy_row(zq, dtype, V, T, sq);
+    *threshold = alpha;
+  } else { /* H(p) < H(q) - alpha [D_TV]  <=>  H(q) - H(p) > alpha [D_TV] */
+    *s = orc_entropy_row(zq, dtype, V, T, sq) - orc_entropy_row(zp, dtype, V, T, sp);
+    *threshold = rule == ORC_OPTLOG ? alpha * tv : alpha;
+  }
+}
 
 int orc_verify(const void* q_logits, const void* p_logits, int dtype, const int32_t* draft,
                const float* uniforms, int32_t B, int32_t gamma, int64_t V,
@@ -218,7 +295,7 @@ int orc_verify(const void* q_logits, const void* p_logits, int dtype, const int3
   if (B < 1 || gamma < 1 || gamma > ORC_MAX_GAMMA || V < 1) return -1;
   if (dtype != ORC_F32 && dtype != ORC_BF16 && dtype != ORC_F64) return -1;
   for (int32_t b = 0; b < B; ++b)
-    if (!rule_ok(rule[b]) || !(temperature[b] > 0.0f)) return -1;
+    if (!rule_ok(rule[b], alpha[b]) || !(temperature[b] > 0.0f)) return -1;
 
   const int32_t G = gamma + 1; /* positions t .. t+gamma */
   int err = 0;
@@ -248,16 +325,30 @@ int orc_verify(const void* q_logits, const void* p_logits, int dtype, const int3
       orc_row_stats sq, sp;
       orc_softmax_row(row_ptr(q_logits, dtype, row, V), dtype, V, T, qj, &sq);
       orc_softmax_row(row_ptr(p_logits, dtype, row, V), dtype, V, T, pj, &sp);
-      double tv, mg;
+      double tv, mg, s = 0.0;
+      const void* zq = row_ptr(q_logits, dtype, row, V);
+      const void* zp = row_ptr(p_logits, dtype, row, V);
       if (is_token(rule[b])) {
         /* Alg. 6: pi = q (1 - r) + p eta; reported delta_j = r(x_j) */
         tv = orc_token_target(rule[b], al, qj, pj, V, sp.maxprob, pi + (size_t)j * V, &mg);
         int32_t x = j < gamma ? draft[(int64_t)b * gamma + j] : -1;
         double xmg;
         dl[j] = (x >= 0 && x < V) ? orc_token_r(rule[b], al, qj[x], pj[x], sp.maxprob, &xmg) : 0;
+      } else if (rule[b] == ORC_LOSSY) {
+        /* Lemma 2: no deferral decision, the target itself is lossy */
+        tv = 0.0;
+        dl[j] = 0;
+        mg = INFINITY;
+        orc_lossy_target(al, qj, pj, V, pi + (size_t)j * V);
       } else {
         tv = orc_tv(pj, qj, V);
-        dl[j] = orc_defer(rule[b], al, sq.maxprob, sp.maxprob, tv, &mg);
+        if (is_log(rule[b])) {
+          double th;
+          log_rule_stat(rule[b], al, tv, zq, zp, dtype, V, T, &sq, &sp, &s, &th);
+          dl[j] = orc_log_defer(s, th, &mg);
+        } else {
+          dl[j] = orc_defer(rule[b], al, sq.maxprob, sp.maxprob, tv, &mg);
+        }
         orc_target(dl[j], qj, pj, V, pi + (size_t)j * V);
       }
       defer[row] = (uint8_t)dl[j];
@@ -266,7 +357,7 @@ int orc_verify(const void* q_logits, const void* p_logits, int dtype, const int3
         double* rs = row_stats + (size_t)row * 8;
         rs[0] = sq.m; rs[1] = sq.lse; rs[2] = sq.maxprob;
         rs[3] = sp.m; rs[4] = sp.lse; rs[5] = sp.maxprob;
-        rs[6] = tv; rs[7] = 0.0;
+        rs[6] = tv; rs[7] = s;
       }
     }
 
@@ -282,7 +373,7 @@ int orc_verify(const void* q_logits, const void* p_logits, int dtype, const int3
         a = 0;
         mg = INFINITY;
         flag |= ORC_FLAG_DRAFT_OUT_OF_RANGE;
-      } else if (dl[j] == 0) { /* pi = q: the ratio is exactly 1 */
+      } else if (dl[j] == 0 && rule[b] != ORC_LOSSY) { /* pi >= q at x: the ratio is 1 */
         a = 1;
         mg = INFINITY;
       } else {
@@ -306,7 +397,8 @@ int orc_verify(const void* q_logits, const void* p_logits, int dtype, const int3
         for (int64_t v = 0; v < V; ++v) W += target[v];
       }
     } else {
-      target = pi + (size_t)gamma * V;
+      /* pi_{t+gamma}; for the (unnormalised) lossy target, p_{t+gamma} */
+      target = (rule[b] == ORC_LOSSY ? p : pi) + (size_t)gamma * V;
       W = 0.0;
       for (int64_t v = 0; v < V; ++v) W += target[v];
     }
@@ -334,12 +426,12 @@ int orc_greedy_verify(const void* q_logits, const void* p_logits, int dtype,
   if (B < 1 || gamma < 1 || gamma > ORC_MAX_GAMMA || V < 1) return -1;
   if (dtype != ORC_F32 && dtype != ORC_BF16 && dtype != ORC_F64) return -1;
   for (int32_t b = 0; b < B; ++b)
-    if (!rule_ok(rule[b])) return -1;
+    if (!rule_ok(rule[b], alpha[b])) return -1;
   const int32_t G = gamma + 1;
 
 #pragma omp parallel for schedule(dynamic, 1)
   for (int32_t b = 0; b < B; ++b) {
-    int32_t aq[ORC_MAX_GAMMA + 1], ap[ORC_MAX_GAMMA + 1];
+    int32_t aq[ORC_MAX_GAMMA + 1], ap[ORC_MAX_GAMMA + 1], tgt[ORC_MAX_GAMMA + 1];
     int dl[ORC_MAX_GAMMA + 1];
     int32_t flag = 0;
     for (int32_t j = 0; j < G; ++j) {
@@ -352,8 +444,23 @@ int orc_greedy_verify(const void* q_logits, const void* p_logits, int dtype,
       ap[j] = sp.argmax;
       /* one-hot q~, p~: D_TV(p~, q~) = 1(argmax q != argmax p) */
       double tv = (aq[j] != ap[j]) ? 1.0 : 0.0;
-      double mg;
-      if (is_token(rule[b])) {
+      double mg, s = 0.0;
+      const void* zq = row_ptr(q_logits, dtype, row, V);
+      const void* zp = row_ptr(p_logits, dtype, row, V);
+      if (rule[b] == ORC_LOSSY) {
+        /* max{min{q~, p~/(1-alpha)}, p~} is one-hot at argmax p */
+        dl[j] = 0;
+        mg = INFINITY;
+        tgt[j] = ap[j];
+      } else if (rule[b] == ORC_BILD) {
+        /* D = -log p(argmax q), temperature 1 */
+        s = sp.lse - logit_at(zp, dtype, aq[j]);
+        dl[j] = orc_log_defer(s, (double)alpha[b], &mg);
+      } else if (is_log(rule[b])) {
+        double th;
+        log_rule_stat(rule[b], (double)alpha[b], tv, zq, zp, dtype, V, 1.0, &sq, &sp, &s, &th);
+        dl[j] = orc_log_defer(s, th, &mg);
+      } else if (is_token(rule[b])) {
         /* r at the drafter's argmax; eta~ = r(argmax q) for the one-hot q~ */
         const void* prow = row_ptr(p_logits, dtype, row, V);
         double pa = exp(logit_at(prow, dtype, aq[j]) - sp.lse);
@@ -362,13 +469,14 @@ int orc_greedy_verify(const void* q_logits, const void* p_logits, int dtype,
       } else {
         dl[j] = orc_defer(rule[b], (double)alpha[b], sq.maxprob, sp.maxprob, tv, &mg);
       }
+      if (rule[b] != ORC_LOSSY) tgt[j] = dl[j] ? ap[j] : aq[j];
       defer[row] = (uint8_t)dl[j];
       if (defer_margin) defer_margin[row] = mg;
       if (row_stats) {
         double* rs = row_stats + (size_t)row * 8;
         rs[0] = sq.m; rs[1] = sq.lse; rs[2] = sq.maxprob;
         rs[3] = sp.m; rs[4] = sp.lse; rs[5] = sp.maxprob;
-        rs[6] = tv; rs[7] = 0.0;
+        rs[6] = tv; rs[7] = s;
       }
       if (argmax_qp) {
         argmax_qp[row * 2 + 0] = aq[j];
@@ -381,8 +489,7 @@ int orc_greedy_verify(const void* q_logits, const void* p_logits, int dtype,
     for (int32_t j = 0; j < gamma; ++j) {
       int32_t x = draft[(int64_t)b * gamma + j];
       if (x < 0 || x >= V) flag |= ORC_FLAG_DRAFT_OUT_OF_RANGE;
-      int32_t keep = dl[j] ? ap[j] : aq[j];
-      if (x != keep) {
+      if (x != tgt[j]) {
         jstar = j;
         break;
       }
@@ -390,7 +497,7 @@ int orc_greedy_verify(const void* q_logits, const void* p_logits, int dtype,
     /* residual max(0, pi~ - q~) (or the bonus pi~_gamma) is one-hot at the
      * same token */
     accept_len[b] = jstar;
-    next_token[b] = dl[jstar] ? ap[jstar] : aq[jstar];
+    next_token[b] = tgt[jstar];
     if (flags) flags[b] = flag;
   }
   return 0;

@@ -36,9 +36,19 @@ enum { ORC_F32 = 0, ORC_BF16 = 1, ORC_F64 = 2 };
 
 /* Deferral rules of Table 1 (Section 4.2 and eq. (2), (5), (11)), plus the two
  * constant rules: ALWAYS (delta = 1: standard speculative decoding, Alg. 1)
- * and NEVER (delta = 0: the drafter alone). */
+ * and NEVER (delta = 0: the drafter alone); the token-specific rules of
+ * Section 4.4; and the other targets of Tables 1 and 3:
+ *   LOSSY    lossy speculative decoding, pi = max{min{q, p/(1-alpha)}, p/beta}
+ *            with beta = 1 (Lemma 2), alpha < 1
+ *   BILD     BiLD*: delta = 1(D(q,p) > alpha), D the cross-entropy -sum q log p
+ *            (temperature 0: -log p(argmax q))
+ *   CHOWLOG  delta = 1(H(q) > alpha)
+ *   DIFFLOG  delta = 1(H(p) < H(q) - alpha)
+ *   OPTLOG   delta = 1(H(p) < H(q) - alpha D_TV(p,q))
+ * with the mixture target T_delta of eq. (6) for BILD and the log rules. */
 enum { ORC_CHOW = 0, ORC_DIFF = 1, ORC_OPT = 2, ORC_ALWAYS = 3, ORC_NEVER = 4,
-       ORC_TOKEN_V1 = 5, ORC_TOKEN_V2 = 6, ORC_TOKEN_V3 = 7 };
+       ORC_TOKEN_V1 = 5, ORC_TOKEN_V2 = 6, ORC_TOKEN_V3 = 7, ORC_LOSSY = 8, ORC_BILD = 9,
+       ORC_CHOWLOG = 10, ORC_DIFFLOG = 11, ORC_OPTLOG = 12 };
 
 /* Per-sequence flags reported by orc_verify / orc_greedy_verify. */
 enum {
@@ -61,6 +71,28 @@ void orc_softmax_row(const void* z, int dtype, int64_t V, double T, double* prob
 
 /* D_TV(p, q) = sum_v max(0, p_v - q_v)  (Lemma 3). */
 double orc_tv(const double* p, const double* q, int64_t V);
+
+/* Entropy H(q) = -sum_v q(v) log q(v) (natural log, 0 log 0 = 0) of the row
+ * softmax(z / T), with log q(v) = z_v / T - lse taken from the logits. */
+double orc_entropy_row(const void* z, int dtype, int64_t V, double T, const orc_row_stats* st);
+
+/* Cross-entropy D(q, p) = -sum_v q(v) log p(v) of BiLD*'s temperature-sampling
+ * discrepancy; +infinity when some v has q(v) > 0 (a finite drafter logit)
+ * and p(v) = 0 (a verifier logit of -infinity). */
+double orc_cross_entropy_row(const void* zq, const void* zp, int dtype, int64_t V, double T,
+                             const orc_row_stats* sq, const orc_row_stats* sp);
+
+/* delta of a log-loss rule (BILD, CHOWLOG, DIFFLOG, OPTLOG) from its statistic
+ * s (D for BILD, H(q) for CHOWLOG, H(q) - H(p) for DIFFLOG and OPTLOG) and
+ * the threshold alpha (alpha D_TV for OPTLOG): delta = 1(s > threshold),
+ * strict.  *margin = |s - threshold| / max(1, |s|, |threshold|): the
+ * statistics are sums of terms up to log V in size, rounded relative to
+ * that size. */
+int orc_log_defer(double s, double threshold, double* margin);
+
+/* Lossy target of Lemma 2 with beta = 1: pi(v) = max{min{q(v), p(v)/(1-alpha)},
+ * p(v)} (not normalised).  alpha < 1. */
+void orc_lossy_target(double alpha, const double* q, const double* p, int64_t V, double* pi);
 
 /* delta(q, p) of Table 1 for one position; *margin = |lhs - rhs| of the
  * defining inequality (infinity for ALWAYS / NEVER). Returns 0 or 1, or -1 for
@@ -105,7 +137,9 @@ int32_t orc_sample(const double* w, int64_t V, double u, double* margin);
  *   next_token [B]            the token emitted at position j*
  *   defer      [B][gamma+1]   delta at every position
  * Optional outputs (may be NULL):
- *   row_stats     [B][gamma+1][8] = {m_q, lse_q, maxprob_q, m_p, lse_p, maxprob_p, tv, 0}
+ *   row_stats     [B][gamma+1][8] = {m_q, lse_q, maxprob_q, m_p, lse_p, maxprob_p, c6, c7}
+ *                 c6 = D_TV (OPT, OPTLOG), eta (token rules), else 0;
+ *                 c7 = the log-loss statistic s of orc_log_defer, else 0
  *   defer_margin  [B][gamma+1]
  *   accept_margin [B][gamma]      (infinity where the draw is exact)
  *   sample_margin [B]
@@ -122,7 +156,9 @@ int orc_verify(const void* q_logits, const void* p_logits, int dtype, const int3
 /* The greedy (temperature 0) step of Lemma 6: one-hot q~ and p~ at the
  * argmaxes of the raw logits, max-probabilities from the temperature-1
  * softmax, D_TV(p~, q~) = 1(argmax q != argmax p).  No uniforms.  row_stats
- * holds the temperature-1 statistics and the one-hot TV. */
+ * holds the temperature-1 statistics and the one-hot TV.  The log-loss rules
+ * read entropies of the temperature-1 softmax; BILD reads D = -log p(argmax q)
+ * (temperature 1).  LOSSY's one-hot target is at argmax p, as for ALWAYS. */
 int orc_greedy_verify(const void* q_logits, const void* p_logits, int dtype,
                       const int32_t* draft, int32_t B, int32_t gamma, int64_t V,
                       const int32_t* rule, const float* alpha, int32_t* accept_len,

@@ -441,6 +441,8 @@ def test_greedy_identical_models(orc):
 def test_argument_errors(orc):
     qz, pz, draft, u = _random_step(50, 2, 2, 8)
     with pytest.raises(ValueError):
-        orc.verify(qz, pz, draft, u, 8, 0.1, 1.0)
+        orc.verify(qz, pz, draft, u, 13, 0.1, 1.0)
+    with pytest.raises(ValueError):  # the lossy target needs alpha < 1
+        orc.verify(qz, pz, draft, u, 8, 1.0, 1.0)
     with pytest.raises(ValueError):
         orc.verify(qz, pz, draft, u, 1, 0.1, 0.0)
