@@ -56,7 +56,7 @@ def lib():
         L.orc_cross_entropy_row.argtypes = [_P, _P, ctypes.c_int, _I64, _D,
                                             ctypes.POINTER(RowStats), ctypes.POINTER(RowStats)]
         L.orc_cross_entropy_row.restype = _D
-        L.orc_log_defer.argtypes = [_D, _D, ctypes.POINTER(_D)]
+        L.orc_log_defer.argtypes = [_D, _D, _D, ctypes.POINTER(_D)]
         L.orc_log_defer.restype = ctypes.c_int
         L.orc_lossy_target.argtypes = [_D, _P, _P, _I64, _P]
         L.orc_lossy_target.restype = None
@@ -134,9 +134,10 @@ def cross_entropy_row(zq, zp, T=1.0):
                                        ctypes.byref(sq), ctypes.byref(sp))
 
 
-def log_defer(s, threshold):
+def log_defer(s, threshold, mag=None):
     mg = _D()
-    d = lib().orc_log_defer(float(s), float(threshold), ctypes.byref(mg))
+    d = lib().orc_log_defer(float(s), float(threshold), float(s if mag is None else mag),
+                            ctypes.byref(mg))
     return d, mg.value
 
 

@@ -130,9 +130,9 @@ double orc_cross_entropy_row(const void* zq, const void* zp, int dtype, int64_t 
   return d;
 }
 
-int orc_log_defer(double s, double threshold, double* margin) {
+int orc_log_defer(double s, double threshold, double mag, double* margin) {
   double scale = 1.0;
-  if (fabs(s) > scale) scale = fabs(s);
+  if (fabs(mag) > scale) scale = fabs(mag);
   if (fabs(threshold) > scale) scale = fabs(threshold);
   *margin = isinf(s) ? INFINITY : fabs(s - threshold) / scale;
   return s > threshold ? 1 : 0;
@@ -270,15 +270,18 @@ static int is_log(int r) { return r >= ORC_BILD && r <= ORC_OPTLOG; }
 /* the statistic s and threshold of a log-loss rule for one row */
 static void log_rule_stat(int rule, double alpha, double tv, const void* zq, const void* zp,
                           int dtype, int64_t V, double T, const orc_row_stats* sq,
-                          const orc_row_stats* sp, double* s, double* threshold) {
+                          const orc_row_stats* sp, double* s, double* threshold,
+                          double* mag) {
   if (rule == ORC_BILD) {
-    *s = orc_cross_entropy_row(zq, zp, dtype, V, T, sq, sp);
+    *s = *mag = orc_cross_entropy_row(zq, zp, dtype, V, T, sq, sp);
     *threshold = alpha;
   } else if (rule == ORC_CHOWLOG) {
-    *s = orc_entropy_row(zq, dtype, V, T, sq);
+    *s = *mag = orc_entropy_row(zq, dtype, V, T, sq);
     *threshold = alpha;
   } else { /* H(p) < H(q) - alpha [D_TV]  <=>  H(q) - H(p) > alpha [D_TV] */
-    *s = orc_entropy_row(zq, dtype, V, T, sq) - orc_entropy_row(zp, dtype, V, T, sp);
+    double hq = orc_entropy_row(zq, dtype, V, T, sq), hp = orc_entropy_row(zp, dtype, V, T, sp);
+    *s = hq - hp;
+    *mag = hq > hp ? hq : hp;
     *threshold = rule == ORC_OPTLOG ? alpha * tv : alpha;
   }
 }
@@ -343,9 +346,9 @@ int orc_verify(const void* q_logits, const void* p_logits, int dtype, const int3
       } else {
         tv = orc_tv(pj, qj, V);
         if (is_log(rule[b])) {
-          double th;
-          log_rule_stat(rule[b], al, tv, zq, zp, dtype, V, T, &sq, &sp, &s, &th);
-          dl[j] = orc_log_defer(s, th, &mg);
+          double th, mag;
+          log_rule_stat(rule[b], al, tv, zq, zp, dtype, V, T, &sq, &sp, &s, &th, &mag);
+          dl[j] = orc_log_defer(s, th, mag, &mg);
         } else {
           dl[j] = orc_defer(rule[b], al, sq.maxprob, sp.maxprob, tv, &mg);
         }
@@ -455,11 +458,12 @@ int orc_greedy_verify(const void* q_logits, const void* p_logits, int dtype,
       } else if (rule[b] == ORC_BILD) {
         /* D = -log p(argmax q), temperature 1 */
         s = sp.lse - logit_at(zp, dtype, aq[j]);
-        dl[j] = orc_log_defer(s, (double)alpha[b], &mg);
+        dl[j] = orc_log_defer(s, (double)alpha[b], s, &mg);
       } else if (is_log(rule[b])) {
-        double th;
-        log_rule_stat(rule[b], (double)alpha[b], tv, zq, zp, dtype, V, 1.0, &sq, &sp, &s, &th);
-        dl[j] = orc_log_defer(s, th, &mg);
+        double th, mag;
+        log_rule_stat(rule[b], (double)alpha[b], tv, zq, zp, dtype, V, 1.0, &sq, &sp, &s, &th,
+                      &mag);
+        dl[j] = orc_log_defer(s, th, mag, &mg);
       } else if (is_token(rule[b])) {
         /* r at the drafter's argmax; eta~ = r(argmax q) for the one-hot q~ */
         const void* prow = row_ptr(p_logits, dtype, row, V);

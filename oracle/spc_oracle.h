@@ -85,10 +85,11 @@ double orc_cross_entropy_row(const void* zq, const void* zp, int dtype, int64_t 
 /* delta of a log-loss rule (BILD, CHOWLOG, DIFFLOG, OPTLOG) from its statistic
  * s (D for BILD, H(q) for CHOWLOG, H(q) - H(p) for DIFFLOG and OPTLOG) and
  * the threshold alpha (alpha D_TV for OPTLOG): delta = 1(s > threshold),
- * strict.  *margin = |s - threshold| / max(1, |s|, |threshold|): the
- * statistics are sums of terms up to log V in size, rounded relative to
- * that size. */
-int orc_log_defer(double s, double threshold, double* margin);
+ * strict.  *margin = |s - threshold| / max(1, mag, |threshold|), mag the size
+ * of the entropies s is made of (s itself, max(H(q), H(p)) for a
+ * difference): they are sums of terms up to log V in size, rounded relative
+ * to that size. */
+int orc_log_defer(double s, double threshold, double mag, double* margin);
 
 /* Lossy target of Lemma 2 with beta = 1: pi(v) = max{min{q(v), p(v)/(1-alpha)},
  * p(v)} (not normalised).  alpha < 1. */

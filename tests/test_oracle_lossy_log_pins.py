@@ -87,6 +87,8 @@ def test_log_defer_strict_and_margin(orc):
     assert orc.log_defer(2.0, 2.0) == (0, 0.0)                    # strict: no deferral
     assert orc.log_defer(0.1, 0.3) == (0, pytest.approx(0.2))     # scale floor 1
     assert orc.log_defer(np.inf, 5.0) == (1, np.inf)
+    # a difference of entropies is rounded relative to the entropies
+    assert orc.log_defer(0.5, 0.4, 8.0) == (1, pytest.approx(0.1 / 8.0))
 
 
 # ------------------------------------------------------------- lossy (Lemma 2)
