@@ -166,9 +166,13 @@ def main():
     ap.add_argument("--copy-calib-mb", type=int, default=0)
     ap.add_argument("--event-every", type=int, default=4)
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
-    ap.add_argument("--rule", default="diff",
+    ap.add_argument("--rule", default=None,
                     choices=["chow", "diff", "opt", "always", "never",
-                             "token-v1", "token-v2", "token-v3"])
+                             "token-v1", "token-v2", "token-v3", "lossy", "bild", "chowlog",
+                             "difflog", "optlog"])
+    ap.add_argument("--cfg", type=int, default=3, choices=[1, 2, 3, 4, 5],
+                    help="workload (default 3, the Gemma-vocabulary step); 4 and 5 run "
+                         "through spc_verify_ex with per-sequence arrays")
     ap.add_argument("--alpha", type=float, default=None)
     args = ap.parse_args()
     if args.traffic_from:
@@ -185,11 +189,15 @@ def main():
     from paper_2405_19261_amd import spc
     from paper_2405_19261_amd import workloads as W
 
-    wl = W.WORKLOADS[3]
-    rule = {v: k for k, v in W.RULE_NAMES.items()}[args.rule]
-    if rule != wl.rule or args.alpha is not None:
+    wl = W.WORKLOADS[args.cfg]
+    if args.rule is not None or args.alpha is not None:
+        rule = wl.rule if args.rule is None else {v: k for k, v in W.RULE_NAMES.items()}[args.rule]
         wl = wl.with_(rule=rule, alpha=wl.alpha if args.alpha is None else args.alpha)
-    rule_desc = f"{args.rule} alpha={wl.alpha:g}"
+    rule_desc = (f"{W.RULE_NAMES[wl.rule]} alpha={wl.alpha:g}" if wl.rule in W.RULE_NAMES
+                 else "per-sequence rules")
+    per_seq = args.cfg in (4, 5)  # greedy / mixed batches: per-sequence arrays
+    if args.cfg != 3:
+        args.no_cpu_baseline = True
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     if args.copy_calib_mb > 0:
@@ -209,7 +217,14 @@ def main():
 
     def step(i, events=None):
         s = sets[i % len(sets)]
-        if events is None:
+        if per_seq:
+            temp = torch.zeros_like(s["temperature"]) if wl.greedy else s["temperature"]
+            ev0, ev1 = events if events is not None else (None, None)
+            spc.spc_verify_ex(s["q"], s["p"], s["draft"], s["uniforms"], 0, 0.0, 1.0,
+                              rule_per_seq=s["rule"], alpha_per_seq=s["alpha"],
+                              temp_per_seq=temp, ev_hot_begin=ev0, ev_hot_end=ev1,
+                              out=outs[i % len(sets)], stream=stream)
+        elif events is None:
             spc.spc_verify(s["q"], s["p"], s["draft"], s["uniforms"], wl.rule, wl.alpha,
                            wl.temperature, out=outs[i % len(sets)], stream=stream)
         else:
@@ -250,9 +265,10 @@ def main():
         value=pos_per_s, unit="positions/s", n_gpus=1, steps=n, warmup=args.warmup,
         ms_per_step=ms_per_step, higher_is_better=True, scaling="weak", vs_baseline=None,
         dtype="f32", data="synthetic",
-        config=dict(workload="gemma-vocab verify step: B=32 gamma=7 V=256000 bf16 logits, "
-                             f"{rule_desc}, T=1, Zipf(1.2)+N(0,1) verifier, "
-                             "0.8*verifier+N(0,1) drafter (10% rows +N(0,3))",
+        config=dict(workload=(("gemma-vocab verify step: B=32 gamma=7 V=256000 bf16 logits, "
+                              f"{rule_desc}, T=1, Zipf(1.2)+N(0,1) verifier, "
+                              "0.8*verifier+N(0,1) drafter (10% rows +N(0,3))")
+                             if args.cfg == 3 else f"{wl.name} ({rule_desc})"),
                     global_batch=B, positions_per_step=B * gamma,
                     algorithmic_bytes_per_step=wl.algorithmic_bytes(),
                     path_gbps=wl.algorithmic_bytes() / (ms_per_step / 1e3) / 1e9,

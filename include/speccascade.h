@@ -62,7 +62,18 @@ typedef enum { SPC_F32 = 0, SPC_BF16 = 1 } spc_dtype;
  * on the draft token (0 at the bonus position j = gamma), and row statistic
  * column 6 holds eta.  At temperature 0 r is read at the drafter's argmax
  * with temperature-1 probabilities; the one-hot target then sits at argmax p
- * when r = 1 and at argmax q otherwise. */
+ * when r = 1 and at argmax q otherwise.
+ *
+ * The other targets of Tables 1 and 3: LOSSY is lossy speculative decoding
+ * with beta = 1, whose target (Lemma 2) needs no deferral decision (the mask
+ * reports 0): a draft is kept with probability min(1, p(x) / ((1 - alpha)
+ * q(x))), a rejection draws from max(0, p - q), and the extra token comes
+ * from p (the target is not a normalised distribution).  BILD and the
+ * log-loss rules defer with the mixture target T_delta of eq. (6); their
+ * statistic (D, H(q), or H(q) - H(p), in nats) is row statistic column 7.
+ * At temperature 0 the log-loss rules read the entropies of the
+ * temperature-1 softmax, BILD reads D = lse_p - z_p(argmax q) (temperature
+ * 1), and LOSSY's one-hot target sits at argmax p. */
 typedef enum {
   SPC_RULE_CHOW = 0,     /* delta = 1(max_v q(v) < 1 - alpha)                 eq. (2)  */
   SPC_RULE_DIFF = 1,     /* delta = 1(max_v q(v) < max_v p(v) - alpha)        eq. (5)  */
@@ -71,7 +82,14 @@ typedef enum {
   SPC_RULE_NEVER = 4,    /* delta = 0: the drafter's own distribution                  */
   SPC_RULE_TOKEN_V1 = 5, /* r(v) = 1(q(v) < max_v p(v) - alpha)          TokenV1, 4.4  */
   SPC_RULE_TOKEN_V2 = 6, /* r(v) = 1(p(v) < max_v p(v) - alpha)          TokenV2, 4.4  */
-  SPC_RULE_TOKEN_V3 = 7  /* r(v) = 1(p(v) < max_v p(v) (1 - alpha))      TokenV3, 4.4  */
+  SPC_RULE_TOKEN_V3 = 7, /* r(v) = 1(p(v) < max_v p(v) (1 - alpha))      TokenV3, 4.4  */
+  SPC_RULE_LOSSY = 8,    /* lossy speculative decoding with beta = 1 (Lemma 2):
+                            pi = max{min{q, p / (1 - alpha)}, p}; alpha < 1            */
+  SPC_RULE_BILD = 9,     /* BiLD*: delta = 1(D(q, p) > alpha), D = -sum_v q(v) log p(v)
+                            (temperature 0: -log p(argmax q))          Table 1, Sec. 6 */
+  SPC_RULE_CHOWLOG = 10, /* delta = 1(H(q) > alpha)                     Table 3, App. B */
+  SPC_RULE_DIFFLOG = 11, /* delta = 1(H(p) < H(q) - alpha)              Table 3, App. D */
+  SPC_RULE_OPTLOG = 12   /* delta = 1(H(p) < H(q) - alpha D_TV(p, q))   Table 3, App. D */
 } spc_rule;
 
 typedef enum {
@@ -135,10 +153,11 @@ spc_status spc_greedy_verify(const void* q_logits, const void* p_logits, spc_dty
  *       are checked by the kernels: an invalid one makes that sequence emit
  *       accept_len = -1 and next_token = -1.
  *   out_row_stats  [B][gamma+1][8] float32: {m_q, lse_q, maxprob_q, m_p,
- *       lse_p, maxprob_p, tv, 0} with m = max_v z_v / T and lse = log sum_v
+ *       lse_p, maxprob_p, tv, s} with m = max_v z_v / T and lse = log sum_v
  *       exp(z_v / T); greedy rows hold the temperature-1 values and the
  *       one-hot TV (for a token rule, r at argmax q).  tv is computed for OPT
- *       rows only (0 elsewhere); token-rule rows hold eta there.
+ *       and OPTLOG rows only (0 elsewhere); token-rule rows hold eta there.
+ *       s is the statistic of BILD and the log-loss rules (0 elsewhere).
  *   out_argmax     [B][gamma+1][2] int32: argmax of raw q and p logits
  *       (filled for greedy rows; -1 elsewhere).
  *   out_sample_norm [B] float32: the total mass W of the distribution

@@ -73,6 +73,7 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
   L.tvpart = o; o = align_up(o + sizeof(double) * R * nt, 256);
   const int64_t nc = (V + samp_chunk_elems(dtype, vec) - 1) / samp_chunk_elems(dtype, vec);
   L.masses = o; o = align_up(o + sizeof(double) * B * nc, 256);
+  L.moms = o; o = align_up(o + sizeof(TileMom) * R * nt, 256);
   L.total = o;
   return L;
 }
@@ -107,9 +108,11 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   const bool per_rule = ex && ex->rule_per_seq;
   const bool per_alpha = ex && ex->alpha_per_seq;
   const bool per_temp = ex && ex->temp_per_seq;
-  if (!per_rule && (rule < SPC_RULE_CHOW || rule > SPC_RULE_TOKEN_V3))
+  if (!per_rule && (rule < SPC_RULE_CHOW || rule > SPC_RULE_OPTLOG))
     return fail(SPC_E_RULE, "unknown rule %d", rule);
   if (!per_alpha && !isfinite(alpha)) return fail(SPC_E_PARAM, "alpha is not finite");
+  if (!per_rule && !per_alpha && rule == SPC_RULE_LOSSY && !(alpha < 1.0f))
+    return fail(SPC_E_PARAM, "the lossy rule needs alpha < 1 (got %g)", (double)alpha);
   if (!force_greedy && !per_temp && !(isfinite(temperature) && temperature >= 1e-20f))
     return fail(SPC_E_PARAM, "temperature must be finite and >= 1e-20 (got %g)",
                 (double)temperature);
@@ -190,16 +193,21 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   P.tiles = reinterpret_cast<spc::TilePart*>(ws + L.tiles);
   P.tvpart = reinterpret_cast<double*>(ws + L.tvpart);
   P.masses = reinterpret_cast<double*>(ws + L.masses);
+  P.moms = reinterpret_cast<spc::TileMom*>(ws + L.moms);
 
   // sequences at temperature > 0 may exist unless the whole batch is greedy;
   // OPT at temperature > 0 needs the TV pass
   const bool need_sample = !force_greedy && (per_temp || temperature > 0.0f);
-  // OPT (D_TV) and the token rules (eta) need the second pass over their rows
-  const bool need_tv = need_sample && (per_rule || rule == SPC_RULE_OPT || rule >= SPC_RULE_TOKEN_V1);
+  // OPT, OPTLOG (D_TV) and the token rules (eta) need the second pass over
+  // their rows; BiLD* and the log-loss rules take first moments
+  const bool token = rule >= SPC_RULE_TOKEN_V1 && rule <= SPC_RULE_TOKEN_V3;
+  const bool need_tv = need_sample && (per_rule || rule == SPC_RULE_OPT ||
+                                       rule == SPC_RULE_OPTLOG || token);
   const bool need_argmax = force_greedy || per_temp;
-  e = spc::launch_verify(P, dtype, vec, need_tv, need_sample, need_argmax,
-                                    ex ? ex->ev_hot_begin : nullptr,
-                                    ex ? ex->ev_hot_end : nullptr, stream);
+  const bool need_mom = per_rule || (rule >= SPC_RULE_BILD && rule <= SPC_RULE_OPTLOG);
+  e = spc::launch_verify(P, dtype, vec, need_tv, need_sample, need_argmax, need_mom,
+                         ex ? ex->ev_hot_begin : nullptr, ex ? ex->ev_hot_end : nullptr,
+                         stream);
   if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
   return SPC_OK;
 }

@@ -27,10 +27,18 @@ struct TilePart {
   int32_t amax_q, amax_p; // lowest row index attaining it (greedy batches), else -1
 };
 
+// First moments of one (row, stats tile) for the log-loss rules and BiLD*,
+// against the same references as its TilePart:  with a = z c - r,
+//   hq = sum 2^a_q a_q,  hp = sum 2^a_p a_p,  x = sum 2^a_q a_p.
+struct TileMom {
+  double hq, hp, x;
+};
+
 // Per-row statistics after merging the tiles of a row.
 struct RowStat {
   double lz_q, lz_p;      // log2 sum_v 2^(z_v * c)  (= lse / ln 2)
-  double tv;              // D_TV(p, q) for OPT rows, eta for token-rule rows, else 0
+  double tv;              // D_TV(p, q) for OPT / OPTLOG rows, eta for token-rule rows, else 0
+  double slog;            // a log-loss rule's statistic (nats): D(q,p), H(q) or H(q) - H(p)
   float zmax_q, zmax_p;
   int32_t amax_q, amax_p;
 };
@@ -69,6 +77,7 @@ struct Params {
   TilePart* tiles;        // [R][nt] statistics partials
   double* tvpart;         // [R][nt] TV partials (OPT) or eta partials (token rules)
   double* masses;         // [B][nc] residual chunk masses of row j*
+  TileMom* moms;          // [R][nt] first moments (log-loss rules and BiLD*)
 };
 
 // Entries per statistics tile and per residual chunk for a dtype and load
@@ -81,16 +90,17 @@ int samp_groups(int64_t nc, int B, int cus);
 // Workspace layout for a shape; offsets in bytes from the base.
 struct WsLayout {
   size_t samp_cnt, zero_end;
-  size_t tiles, tvpart, masses, total;
+  size_t tiles, tvpart, masses, moms, total;
 };
 WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec);
 
-// Enqueue the kernels of one verify call.  need_tv: the batch may hold OPT or
-// token-rule sequences at temperature > 0; need_sample: it may hold sequences at
-// temperature > 0; need_argmax: it may hold greedy (temperature 0)
-// sequences.  Returns the first launch error.
+// Enqueue the kernels of one verify call.  need_tv: the batch may hold OPT,
+// OPTLOG or token-rule sequences at temperature > 0; need_sample: it may hold
+// sequences at temperature > 0; need_argmax: it may hold greedy (temperature
+// 0) sequences; need_mom: it may hold log-loss or BiLD* sequences.  Returns
+// the first launch error.
 hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
-                         bool need_argmax, hipEvent_t ev_begin, hipEvent_t ev_end,
-                         hipStream_t stream);
+                         bool need_argmax, bool need_mom, hipEvent_t ev_begin,
+                         hipEvent_t ev_end, hipStream_t stream);
 
 }  // namespace spc

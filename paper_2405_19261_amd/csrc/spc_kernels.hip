@@ -141,6 +141,25 @@ __device__ __forceinline__ double log2_acc(double S) {
   return (double)e + (double)log2_hw(mh) + tail * (double)__builtin_amdgcn_rcpf(mh) * kLog2e;
 }
 
+// First moments h = sum 2^a a (a = z c - r) moved from reference r to a
+// reference r' >= r: with d = r - r' (exact in fp64) and f = 2^d, every weight
+// scales by f and every argument grows by d, so h' = f (h + d s), s the sum
+// of the weights.  For x = sum 2^(a_q) a_p, f is the q factor and d the p
+// shift.  An empty side (s = 0) stays 0 and a -inf moment stays -inf.
+// Floating-point contraction is off here and in mom_add, so that the q and
+// p moments of identical rows take identical operations at every call site
+// (H(q) - H(p) is then exactly 0 for p = q).
+__device__ __forceinline__ double mom_move(double h, double s, double f, double d) {
+#pragma clang fp contract(off)
+  if (s == 0.0) return 0.0;
+  if (h == -__builtin_huge_val()) return h;
+  return f * (h + d * s);
+}
+__device__ __forceinline__ void mom_add(double& acc, double h, double s, double f, double d) {
+#pragma clang fp contract(off)
+  acc = acc + mom_move(h, s, f, d);
+}
+
 // ------------------------------------------- cross-workgroup communication
 // Agent-scope fences on gfx950 write back and invalidate the whole L2, which
 // is ruinous when thousands of workgroups each publish a few bytes.  Instead,
@@ -243,6 +262,7 @@ struct SharedT {
   float m[NWV][2];
   double d[NWV][2];
   double dv[NWV];
+  double h[NWV][3];
   int i[NWV][2];
   int flag;
 };
@@ -331,8 +351,9 @@ __device__ __forceinline__ SeqParam seq_param(const Params& P, int b) {
   const float alpha = P.alpha_ps ? P.alpha_ps[b] : P.alpha;
   const float T = P.temp_ps ? P.temp_ps[b] : P.temp;
   s.alpha = (double)alpha;
-  s.valid = s.rule >= SPC_RULE_CHOW && s.rule <= SPC_RULE_TOKEN_V3 && isfinite(alpha) &&
-            isfinite(T) && T >= 0.0f && (T == 0.0f || T >= 1e-20f);
+  s.valid = s.rule >= SPC_RULE_CHOW && s.rule <= SPC_RULE_OPTLOG && isfinite(alpha) &&
+            isfinite(T) && T >= 0.0f && (T == 0.0f || T >= 1e-20f) &&
+            (s.rule != SPC_RULE_LOSSY || alpha < 1.0f);
   s.greedy = P.force_greedy || T == 0.0f;
   s.c = kLog2e / ((s.greedy || !s.valid) ? 1.0 : (double)T);
   // split c so that z*c_hi + z*c_lo carries ~48 bits of c; c_lo > 0 keeps
@@ -348,10 +369,28 @@ __device__ __forceinline__ bool is_token(int rule) {
   return rule >= SPC_RULE_TOKEN_V1 && rule <= SPC_RULE_TOKEN_V3;
 }
 
-// Sequences whose rows need the second pass: OPT (D_TV of Lemma 3) and the
-// token rules (eta of Alg. 6) at temperature > 0.
+// BiLD* and the log-loss rules of Table 3: delta from a statistic in nats.
+__device__ __forceinline__ bool is_log(int rule) {
+  return rule >= SPC_RULE_BILD && rule <= SPC_RULE_OPTLOG;
+}
+
+// Rules whose residual at a rejection is max(0, p - q) summed per tile by the
+// second pass (their D_TV partials).
+__device__ __forceinline__ bool has_tv_parts(int rule) {
+  return rule == SPC_RULE_OPT || rule == SPC_RULE_OPTLOG;
+}
+
+// Sequences whose rows need the second pass: OPT and OPTLOG (D_TV of
+// Lemma 3) and the token rules (eta of Alg. 6) at temperature > 0.
 __device__ __forceinline__ bool needs_pass2(const SeqParam& s) {
-  return s.valid && !s.greedy && (s.rule == SPC_RULE_OPT || is_token(s.rule));
+  return s.valid && !s.greedy && (has_tv_parts(s.rule) || is_token(s.rule));
+}
+
+// Sequences whose statistics tiles also take first moments: the entropies of
+// the log-loss rules (at temperature 0, of the temperature-1 softmax) and
+// BiLD*'s cross-entropy at temperature > 0.
+__device__ __forceinline__ bool needs_mom(const SeqParam& s) {
+  return s.valid && is_log(s.rule) && !(s.rule == SPC_RULE_BILD && s.greedy);
 }
 
 // Token-specific rules (Section 4.4) as a threshold on one logit of the row:
@@ -514,23 +553,41 @@ __device__ __forceinline__ int defer_rule(int rule, double alpha, double maxq, d
 struct PartHead {
   TilePart t;
   double tv;
+  TileMom m;
 };
 
-__device__ __forceinline__ PartHead load_head(const Params& P, int r, bool tv) {
+__device__ __forceinline__ PartHead load_head(const Params& P, int r, bool tv, bool mom) {
   const int lane = threadIdx.x & 63;
-  PartHead h{{0.0, 0.0, kNegInf, kNegInf, kNegInf, kNegInf, 0x7fffffff, 0x7fffffff}, 0.0};
+  PartHead h{{0.0, 0.0, kNegInf, kNegInf, kNegInf, kNegInf, 0x7fffffff, 0x7fffffff}, 0.0,
+             {0.0, 0.0, 0.0}};
   if (lane < P.nt) {
     h.t = P.tiles[(int64_t)r * P.nt + lane];
     if (tv) h.tv = P.tvpart[(int64_t)r * P.nt + lane];
+    if (mom) h.m = P.moms[(int64_t)r * P.nt + lane];
   }
   return h;
 }
 
+// A log-loss rule's statistic (nats) from row sums S and moments against the
+// row references (contraction off, as in mom_move).
+__device__ __forceinline__ double log_stat(int rule, double lq2, double lp2, double sq, double sp,
+                                           double mhq, double mhp, double mx) {
+#pragma clang fp contract(off)
+  const double Hq = kLn2 * (lq2 - mhq / sq), Hp = kLn2 * (lp2 - mhp / sp);
+  return rule == SPC_RULE_BILD      ? kLn2 * (lp2 - mx / sq)
+         : rule == SPC_RULE_CHOWLOG ? Hq
+                                    : Hq - Hp;
+}
+
 // One wavefront merges the nt tile partials of row r in a fixed order (lane l
 // takes tiles l, l + 64, ...; butterflies combine the lanes), adding the TV
-// partials when `tv`.  Every lane returns the same RowStat.
+// partials when `tv`, and with mrule (a log-loss rule or BiLD*) its
+// statistic from the tiles' first moments: against the row references,
+//   H(q) = ln 2 (log2 S_q - H_q / S_q),  H(p) = ln 2 (log2 S_p - H_p / S_p),
+//   D(q, p) = -sum q log p = ln 2 (log2 S_p - X / S_q),
+// each a sum of two non-negative terms.  Every lane returns the same RowStat.
 __device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy, bool tv,
-                                             const PartHead& h) {
+                                             int mrule, const PartHead& h) {
   const int lane = threadIdx.x & 63;
   const int nt = P.nt;
   const TilePart* t = P.tiles + (int64_t)r * nt;
@@ -548,20 +605,27 @@ __device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy
   zp = wave_max(zp);
   rq = wave_max(rq);
   rp = wave_max(rp);
-  double sq = 0.0, sp = 0.0;
+  double sq = 0.0, sp = 0.0, mhq = 0.0, mhp = 0.0, mx = 0.0;
   int aq = 0x7fffffff, ap = 0x7fffffff;
-  auto add = [&](const TilePart& tk) {
+  auto add = [&](const TilePart& tk, const TileMom& mk) {
     // r_k - r is exact in fp64; an all -inf tile has s = 0
-    sq += tk.s_q * exp2_acc((double)tk.r_q - (double)rq);
-    sp += tk.s_p * exp2_acc((double)tk.r_p - (double)rp);
+    const double gq = (double)tk.r_q - (double)rq, gp = (double)tk.r_p - (double)rp;
+    const double fq = exp2_acc(gq), fp = exp2_acc(gp);
+    sq += tk.s_q * fq;
+    sp += tk.s_p * fp;
     if (greedy) {
       if (tk.zmax_q == zq) aq = min(aq, tk.amax_q);
       if (tk.zmax_p == zp) ap = min(ap, tk.amax_p);
     }
+    if (mrule) {
+      mom_add(mhq, mk.hq, tk.s_q, fq, gq);
+      mom_add(mhp, mk.hp, tk.s_p, fp, gp);
+      mom_add(mx, mk.x, tk.s_q, fq, gp);
+    }
   };
-  add(t0);
+  add(t0, h.m);
   for (int k = lane + 64; k < nt; k += 64) {
-    add(t[k]);
+    add(t[k], mrule ? P.moms[(int64_t)r * nt + k] : TileMom{0.0, 0.0, 0.0});
     if (tv) tvs += tvp[k];
   }
   sq = wave_sum(sq);
@@ -570,9 +634,17 @@ __device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy
   aq = wave_min(aq);
   ap = wave_min(ap);
   RowStat rs;
-  rs.lz_q = (double)rq + log2_acc(sq);
-  rs.lz_p = (double)rp + log2_acc(sp);
+  const double lq2 = log2_acc(sq), lp2 = log2_acc(sp);
+  rs.lz_q = (double)rq + lq2;
+  rs.lz_p = (double)rp + lp2;
   rs.tv = tvs;
+  rs.slog = 0.0;
+  if (mrule) {
+    mhq = wave_sum(mhq);
+    mhp = wave_sum(mhp);
+    mx = wave_sum(mx);
+    rs.slog = log_stat(mrule, lq2, lp2, sq, sp, mhq, mhp, mx);
+  }
   rs.zmax_q = zq;
   rs.zmax_p = zp;
   rs.amax_q = greedy ? aq : -1;
@@ -581,7 +653,7 @@ __device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy
 }
 
 __device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy, bool tv) {
-  return merge_row(P, r, greedy, tv, load_head(P, r, tv));
+  return merge_row(P, r, greedy, tv, 0, load_head(P, r, tv, false));
 }
 
 // ------------------------------------------------------------- decision
@@ -632,7 +704,31 @@ __device__ __forceinline__ RowDecision decide_row(const SeqParam& sp, const RowS
   // greedy: one-hot q~, p~ give D_TV = 1(argmax q != argmax p)  (Lemma 6)
   const double tv = sp.greedy ? (rs.amax_q != rs.amax_p ? 1.0 : 0.0) : rs.tv;
   d.tv = (float)tv;
-  d.delta = defer_rule(sp.rule, sp.alpha, maxq, maxp, tv);
+  if (sp.rule == SPC_RULE_LOSSY) {
+    // Lemma 2 (beta = 1): no deferral; pi(x) / q(x) = min(1, p(x) / ((1 -
+    // alpha) q(x))) where p(x) < q(x) (alpha < 0: p(x) / q(x)), and >= 1
+    // elsewhere; the one-hot greedy target sits at argmax p
+    d.delta = 0;
+    if (j >= gamma || x < 0 || x >= V) {
+      d.keep = 0;
+    } else if (sp.greedy) {
+      d.keep = x == rs.amax_p;
+    } else {
+      const double L = sp.alpha > 0.0 ? -log2(1.0 - sp.alpha) : 0.0;
+      const double dd = (((double)zpx * sp.c - rs.lz_p) - ((double)zqx * sp.c - rs.lz_q)) + L;
+      d.keep = !(dd < 0.0) || (double)u < exp2_acc(dd);
+    }
+    return d;
+  }
+  if (is_log(sp.rule)) {
+    // statistic in nats against alpha (OPTLOG: alpha D_TV); greedy BiLD* reads
+    // D = lse_p - z_p(argmax q) at temperature 1, zpx being that logit
+    if (sp.rule == SPC_RULE_BILD && sp.greedy) d.rs.slog = rs.lz_p * kLn2 - (double)zpx;
+    const double th = sp.rule == SPC_RULE_OPTLOG ? sp.alpha * tv : sp.alpha;
+    d.delta = d.rs.slog > th;
+  } else {
+    d.delta = defer_rule(sp.rule, sp.alpha, maxq, maxp, tv);
+  }
   if (j >= gamma || x < 0 || x >= V) {
     d.keep = 0;  // a_gamma = 0; a draft outside the vocabulary is rejected
   } else if (sp.greedy) {
@@ -682,7 +778,7 @@ __device__ __forceinline__ void finish_seq(const Params& P, int b, const SeqPara
       o[4] = (float)(d.rs.lz_p * kLn2);
       o[5] = d.maxp;
       o[6] = d.tv;
-      o[7] = 0.0f;
+      o[7] = (float)d.rs.slog;
     }
     if (P.out_argmax) {
       P.out_argmax[row * 2 + 0] = d.rs.amax_q;
@@ -699,12 +795,15 @@ __device__ __forceinline__ void finish_seq(const Params& P, int b, const SeqPara
     SeqState s{jstar, kNone, 0.0f, 0};
     if (sp.greedy) {
       if (write) {
-        P.out_token[b] = dstar ? ap : aq;
+        P.out_token[b] = (dstar || sp.rule == SPC_RULE_LOSSY) ? ap : aq;
         if (P.out_norm) P.out_norm[b] = 1.0f;
       }
     } else {
       if (is_token(sp.rule)) {
         s.kind = (jstar < gamma) ? kTokRes : kTokPi;
+      } else if (sp.rule == SPC_RULE_LOSSY) {
+        // residual max(0, pi - q) = max(0, p - q); extra token from p
+        s.kind = (jstar < gamma) ? kResidual : kP;
       } else {
         // a rejection with delta = 0 only happens for an out-of-range draft;
         // its residual max(0, q - q) is empty, so p is sampled instead
@@ -732,9 +831,12 @@ __device__ __forceinline__ void decide_seq(const Params& P, int b, const SeqPara
     // the logits at the draft tokens follow the tokens and stay in flight
     // while the rows merge.
     const bool tv = needs_pass2(sp);
-    const bool greedy_tok = sp.greedy && is_token(sp.rule) && sp.rule != SPC_RULE_TOKEN_V1;
+    const bool mom = needs_mom(sp);
+    // greedy TokenV2/V3 and BiLD* read p at the drafter's argmax
+    const bool greedy_pa = sp.greedy && ((is_token(sp.rule) && sp.rule != SPC_RULE_TOKEN_V1) ||
+                                         sp.rule == SPC_RULE_BILD);
     PartHead h{};
-    if (wv < g1) h = load_head(P, b * g1 + wv, tv);
+    if (wv < g1) h = load_head(P, b * g1 + wv, tv, mom);
     const int jl = wv + kSampWaves * lane;
     int x = -1;
     float zqx = 0.0f, zpx = 0.0f, u = 0.0f;
@@ -753,11 +855,10 @@ __device__ __forceinline__ void decide_seq(const Params& P, int b, const SeqPara
       const int j = wv + kSampWaves * i;
       // the next row's partials load while this row merges
       PartHead hn{};
-      if (j + kSampWaves < g1) hn = load_head(P, b * g1 + j + kSampWaves, tv);
-      const RowStat rs = merge_row(P, b * g1 + j, sp.greedy, tv, h);
+      if (j + kSampWaves < g1) hn = load_head(P, b * g1 + j + kSampWaves, tv, mom);
+      const RowStat rs = merge_row(P, b * g1 + j, sp.greedy, tv, mom ? sp.rule : 0, h);
       h = hn;
-      // greedy TokenV2/V3: the rule reads p at the drafter's argmax
-      const float zpa = (greedy_tok && rs.amax_q >= 0 && rs.amax_q < V)
+      const float zpa = (greedy_pa && rs.amax_q >= 0 && rs.amax_q < V)
                             ? load_logit<DT>(P.p, (int64_t)b * g1 + j, V, rs.amax_q)
                             : lane_f32(zpx, i);
       const RowDecision d = decide_row(sp, rs, j, gamma, V, lane_i32(x, i), lane_f32(zqx, i),
@@ -1117,8 +1218,61 @@ __device__ __forceinline__ void draw(const Params& P, int b, int64_t row, int ki
 // the wave max, and thread 0 the waves against the tile max.  With ARGMAX
 // (batches that may hold greedy rows) the lowest entry attaining the max is
 // found as well.
-template <int DT, bool VEC, bool ARGMAX>
-__global__ __launch_bounds__(kThreads) void k_stats(Params P) {
+// Thread sums of one statistics tile: s = sum 2^a over the thread's entries,
+// a = z c - r (r the thread reference); with MOM also the first moments
+// hq = sum 2^a_q a_q, hp = sum 2^a_p a_p and x = sum 2^a_q a_p (entries of
+// zero weight contribute nothing, so -inf logits never meet an infinite
+// factor; a finite-weight q entry facing a -inf p logit makes x = -inf).
+template <int DT, bool VEC, bool MOM>
+__device__ __forceinline__ void tile_sums(const uint32_t (&wq)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
+                                          const uint32_t (&wp)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
+                                          const SeqParam& sp, float rq, float rp, float& sq,
+                                          float& spp, float& hq, float& hp, float& xq) {
+  using T = StatTile<DT, VEC>;
+  if constexpr (MOM) {
+    // one running sum per quantity: the moments' extra values stay short-lived
+#pragma unroll
+    for (int i = 0; i < T::U; ++i)
+#pragma unroll
+      for (int e = 0; e < T::VW; ++e) {
+        const float zq = elem<DT, VEC>(wq[i], e), zp = elem<DT, VEC>(wp[i], e);
+        const float aq = fmaf(zq, sp.c_lo, fmaf(zq, sp.c_hi, -rq));
+        const float ap = fmaf(zp, sp.c_lo, fmaf(zp, sp.c_hi, -rp));
+        const float tq = exp2_hw(aq), tp = exp2_hw(ap);
+        const bool wq_pos = tq > 0.0f;
+        sq += tq;
+        spp += tp;
+        hq = fmaf(tq, wq_pos ? aq : 0.0f, hq);
+        xq = fmaf(tq, wq_pos ? ap : 0.0f, xq);
+        hp = fmaf(tp, tp > 0.0f ? ap : 0.0f, hp);
+        // keep the scheduler from hoisting every exponential of the tile
+        if ((e & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+      }
+  } else {
+#pragma unroll
+    for (int i = 0; i < T::U; ++i) {
+      float tq[T::VW], tp[T::VW];
+#pragma unroll
+      for (int e = 0; e < T::VW; ++e) {
+        const float zq = elem<DT, VEC>(wq[i], e), zp = elem<DT, VEC>(wp[i], e);
+        tq[e] = exp2_hw(fmaf(zq, sp.c_lo, fmaf(zq, sp.c_hi, -rq)));
+        tp[e] = exp2_hw(fmaf(zp, sp.c_lo, fmaf(zp, sp.c_hi, -rp)));
+      }
+#pragma unroll
+      for (int h = 1; h < T::VW; h <<= 1)
+#pragma unroll
+        for (int e = 0; e + h < T::VW; e += 2 * h) {
+          tq[e] += tq[e + h];
+          tp[e] += tp[e + h];
+        }
+      sq += tq[0];
+      spp += tp[0];
+    }
+  }
+}
+
+template <int DT, bool VEC, bool ARGMAX, bool MOM>
+__device__ __forceinline__ void stats_tile(const Params& P) {
   using T = StatTile<DT, VEC>;
   __shared__ Shared sh;
   const int k = blockIdx.x, r = blockIdx.y;
@@ -1142,7 +1296,7 @@ __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
 #pragma unroll
     for (int e = 0; e < T::VW; ++e) {
       const float vq = elem<DT, VEC>(wq[i], e), vp = elem<DT, VEC>(wp[i], e);
-      if constexpr (ARGMAX) {
+      if constexpr (ARGMAX && !MOM) {
         const int idx = base + i * kThreads * T::VW + e;
         if (vq > mq) iq = idx;
         if (vp > mp) ip = idx;
@@ -1150,39 +1304,44 @@ __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
       mq = fmaxf(mq, vq);
       mp = fmaxf(mp, vp);
     }
+  if constexpr (MOM) __builtin_amdgcn_sched_barrier(0);
   const float rq = (mq == kNegInf) ? 0.0f : mq * sp.c_hi;
   const float rp = (mp == kNegInf) ? 0.0f : mp * sp.c_hi;
-  float sq = 0.0f, spp = 0.0f;
+  float sq = 0.0f, spp = 0.0f, hq = 0.0f, hp = 0.0f, xq = 0.0f;
+  const bool mom = MOM && needs_mom(sp);  // block-uniform
+  if (mom)
+    tile_sums<DT, VEC, true>(wq, wp, sp, rq, rp, sq, spp, hq, hp, xq);
+  else
+    tile_sums<DT, VEC, false>(wq, wp, sp, rq, rp, sq, spp, hq, hp, xq);
+  if constexpr (ARGMAX && MOM) {
+    // the lowest entry equal to the thread max, in a pass of its own
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-  for (int i = 0; i < T::U; ++i) {
-    float tq[T::VW], tp[T::VW];
+    for (int i = T::U - 1; i >= 0; --i)
 #pragma unroll
-    for (int e = 0; e < T::VW; ++e) {
-      const float zq = elem<DT, VEC>(wq[i], e), zp = elem<DT, VEC>(wp[i], e);
-      tq[e] = exp2_hw(fmaf(zq, sp.c_lo, fmaf(zq, sp.c_hi, -rq)));
-      tp[e] = exp2_hw(fmaf(zp, sp.c_lo, fmaf(zp, sp.c_hi, -rp)));
-    }
-#pragma unroll
-    for (int h = 1; h < T::VW; h <<= 1)
-#pragma unroll
-      for (int e = 0; e + h < T::VW; e += 2 * h) {
-        tq[e] += tq[e + h];
-        tp[e] += tp[e + h];
+      for (int e = T::VW - 1; e >= 0; --e) {
+        const int idx = base + i * kThreads * T::VW + e;
+        if (elem<DT, VEC>(wq[i], e) == mq) iq = idx;
+        if (elem<DT, VEC>(wp[i], e) == mp) ip = idx;
       }
-    sq += tq[0];
-    spp += tp[0];
   }
   // Wave partials against the wave max (r_t - r_w is exact in fp64; only its
   // rounding to float is inexact), then one barrier and thread 0 combines the
   // waves in order against the tile max.
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const float Wq = wave_max(mq), Wp = wave_max(mp);
-  double dq = (mq == kNegInf) ? 0.0
-              : (double)sq * (double)exp2_hw((float)((double)rq - (double)(Wq * sp.c_hi)));
-  double dp = (mp == kNegInf) ? 0.0
-              : (double)spp * (double)exp2_hw((float)((double)rp - (double)(Wp * sp.c_hi)));
+  const double eq = (double)rq - (double)(Wq * sp.c_hi), ep = (double)rp - (double)(Wp * sp.c_hi);
+  const double fq = (double)exp2_hw((float)eq), fp = (double)exp2_hw((float)ep);
+  double dq = (mq == kNegInf) ? 0.0 : (double)sq * fq;
+  double dp = (mp == kNegInf) ? 0.0 : (double)spp * fp;
   dq = wave_sum(dq);
   dp = wave_sum(dp);
+  double mhq = 0.0, mhp = 0.0, mx = 0.0;
+  if (mom) {
+    mhq = wave_sum(mq == kNegInf ? 0.0 : mom_move(hq, sq, fq, eq));
+    mhp = wave_sum(mp == kNegInf ? 0.0 : mom_move(hp, spp, fp, ep));
+    mx = wave_sum(mq == kNegInf ? 0.0 : mom_move(xq, sq, fq, ep));
+  }
   if constexpr (ARGMAX) {
     iq = wave_min((mq == Wq) ? iq : 0x7fffffff);
     ip = wave_min((mp == Wp) ? ip : 0x7fffffff);
@@ -1194,6 +1353,11 @@ __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
     sh.d[wv][1] = dp;
     sh.i[wv][0] = iq;
     sh.i[wv][1] = ip;
+    if (mom) {
+      sh.h[wv][0] = mhq;
+      sh.h[wv][1] = mhp;
+      sh.h[wv][2] = mx;
+    }
   }
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -1226,7 +1390,40 @@ __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
     t.amax_q = ARGMAX ? aq : -1;
     t.amax_p = ARGMAX ? ap : -1;
     P.tiles[(int64_t)r * P.nt + k] = t;
+    if (mom) {
+      // the waves' moments against the tile references, in wave order
+      TileMom m{0.0, 0.0, 0.0};
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const float wq_ = sh.m[w][0], wp_ = sh.m[w][1];
+        const double gq = (wq_ == kNegInf) ? 0.0 : (double)(wq_ * sp.c_hi) - (double)Rq;
+        const double gp = (wp_ == kNegInf) ? 0.0 : (double)(wp_ * sp.c_hi) - (double)Rp;
+        const double fq_ = (double)exp2_hw((float)gq), fp_ = (double)exp2_hw((float)gp);
+        // a wave's sums d_w are against the wave max, as its moments are
+        if (wq_ != kNegInf) mom_add(m.hq, sh.h[w][0], sh.d[w][0], fq_, gq);
+        if (wp_ != kNegInf) mom_add(m.hp, sh.h[w][1], sh.d[w][1], fp_, gp);
+        if (wq_ != kNegInf)
+          mom_add(m.x, sh.h[w][2], sh.d[w][0], fq_, wp_ == kNegInf ? -__builtin_huge_val() : gp);
+      }
+      P.moms[(int64_t)r * P.nt + k] = m;
+    }
   }
+}
+
+template <int DT, bool VEC, bool ARGMAX>
+__global__ __launch_bounds__(kThreads) void k_stats(Params P) {
+  stats_tile<DT, VEC, ARGMAX, false>(P);
+}
+
+// With first moments (batches that may hold BiLD* or log-loss sequences).
+// Held to SPC_MOM_OCCUPANCY resident workgroups per CU: left free, the
+// compiler keeps every exponential of the tile live at once.
+#ifndef SPC_MOM_OCCUPANCY
+#define SPC_MOM_OCCUPANCY 6
+#endif
+template <int DT, bool VEC, bool ARGMAX>
+__global__ __launch_bounds__(kThreads, SPC_MOM_OCCUPANCY) void k_stats_mom(Params P) {
+  stats_tile<DT, VEC, ARGMAX, true>(P);
 }
 
 // TV pass (OPT rows at temperature > 0): D_TV(p, q) of Lemma 3, which needs
@@ -1292,7 +1489,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
   if (s.kind == kNone) return;  // block-uniform
   const int64_t row = (int64_t)b * (P.gamma + 1) + s.row;
   const RowStat rs = ss.rows[s.row].rs;
-  const bool pass = s.kind == kTokRes || (s.kind == kResidual && sp.rule != SPC_RULE_OPT);
+  const bool pass = s.kind == kTokRes || (s.kind == kResidual && !has_tv_parts(sp.rule));
   if (!pass) {
     if (k != 0) return;  // block-uniform
     const int src = s.kind == kQ     ? kSrcStatsQ
@@ -1317,14 +1514,21 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
 
 template <int DT, bool VEC>
 hipError_t launch_t(const Params& P, bool need_tv, bool need_sample, bool need_argmax,
-                    hipEvent_t e0, hipEvent_t e1, hipStream_t st) {
+                    bool need_mom, hipEvent_t e0, hipEvent_t e1, hipStream_t st) {
   const unsigned R = (unsigned)(P.B * (P.gamma + 1));
+  const dim3 grid(P.nt, R);
   hipError_t err;
   if (e0 && (err = hipEventRecord(e0, st)) != hipSuccess) return err;
-  if (need_argmax)
-    hipLaunchKernelGGL((k_stats<DT, VEC, true>), dim3(P.nt, R), dim3(kThreads), 0, st, P);
-  else
-    hipLaunchKernelGGL((k_stats<DT, VEC, false>), dim3(P.nt, R), dim3(kThreads), 0, st, P);
+  if (need_mom) {
+    if (need_argmax)
+      hipLaunchKernelGGL((k_stats_mom<DT, VEC, true>), grid, dim3(kThreads), 0, st, P);
+    else
+      hipLaunchKernelGGL((k_stats_mom<DT, VEC, false>), grid, dim3(kThreads), 0, st, P);
+  } else if (need_argmax) {
+    hipLaunchKernelGGL((k_stats<DT, VEC, true>), grid, dim3(kThreads), 0, st, P);
+  } else {
+    hipLaunchKernelGGL((k_stats<DT, VEC, false>), grid, dim3(kThreads), 0, st, P);
+  }
   if ((err = hipGetLastError()) != hipSuccess) return err;
   if (e1 && (err = hipEventRecord(e1, st)) != hipSuccess) return err;
   if (need_tv) {
@@ -1360,13 +1564,14 @@ int samp_groups(int64_t nc, int B, int cus) {
 }
 
 hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
-                         bool need_argmax, hipEvent_t e0, hipEvent_t e1, hipStream_t st) {
+                         bool need_argmax, bool need_mom, hipEvent_t e0, hipEvent_t e1,
+                         hipStream_t st) {
   if (dtype == 1) {
-    return vec ? launch_t<1, true>(P, need_tv, need_sample, need_argmax, e0, e1, st)
-               : launch_t<1, false>(P, need_tv, need_sample, need_argmax, e0, e1, st);
+    return vec ? launch_t<1, true>(P, need_tv, need_sample, need_argmax, need_mom, e0, e1, st)
+               : launch_t<1, false>(P, need_tv, need_sample, need_argmax, need_mom, e0, e1, st);
   }
-  return vec ? launch_t<0, true>(P, need_tv, need_sample, need_argmax, e0, e1, st)
-             : launch_t<0, false>(P, need_tv, need_sample, need_argmax, e0, e1, st);
+  return vec ? launch_t<0, true>(P, need_tv, need_sample, need_argmax, need_mom, e0, e1, st)
+             : launch_t<0, false>(P, need_tv, need_sample, need_argmax, need_mom, e0, e1, st);
 }
 
 }  // namespace spc

@@ -11,11 +11,14 @@ import os
 
 import torch
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspeccascade.so")
+# SPC_LIB_PATH selects another build of the library (e.g. a tuning variant)
+LIB_PATH = os.environ.get("SPC_LIB_PATH") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libspeccascade.so")
 
 SPC_F32, SPC_BF16 = 0, 1
 SPC_RULE_CHOW, SPC_RULE_DIFF, SPC_RULE_OPT, SPC_RULE_ALWAYS, SPC_RULE_NEVER = range(5)
 SPC_RULE_TOKEN_V1, SPC_RULE_TOKEN_V2, SPC_RULE_TOKEN_V3 = 5, 6, 7
+SPC_RULE_LOSSY, SPC_RULE_BILD, SPC_RULE_CHOWLOG, SPC_RULE_DIFFLOG, SPC_RULE_OPTLOG = range(8, 13)
 SPC_MAX_GAMMA = 63
 STATUS = {0: "SPC_OK", -1: "SPC_E_NULL", -2: "SPC_E_SHAPE", -3: "SPC_E_RULE",
           -4: "SPC_E_PARAM", -5: "SPC_E_ALIGN", -6: "SPC_E_WORKSPACE", -7: "SPC_E_HIP"}

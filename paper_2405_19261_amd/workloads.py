@@ -23,8 +23,11 @@ import torch
 # Rule codes (same numbering as the C interface).
 CHOW, DIFF, OPT, ALWAYS, NEVER = 0, 1, 2, 3, 4
 TOKEN_V1, TOKEN_V2, TOKEN_V3 = 5, 6, 7
+LOSSY, BILD, CHOWLOG, DIFFLOG, OPTLOG = 8, 9, 10, 11, 12
 RULE_NAMES = {CHOW: "chow", DIFF: "diff", OPT: "opt", ALWAYS: "always", NEVER: "never",
-              TOKEN_V1: "token-v1", TOKEN_V2: "token-v2", TOKEN_V3: "token-v3"}
+              TOKEN_V1: "token-v1", TOKEN_V2: "token-v2", TOKEN_V3: "token-v3",
+              LOSSY: "lossy", BILD: "bild", CHOWLOG: "chowlog", DIFFLOG: "difflog",
+              OPTLOG: "optlog"}
 
 
 @dataclass(frozen=True)

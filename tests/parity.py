@@ -33,7 +33,12 @@ FLOAT_TOL = {"f32": 1e-5, "bf16": 2e-3}
 # ~1e-7 absolute); near 0 they are held to tol * 0.1 absolute (1e-6 for
 # float32 inputs) -- at most the decision near-tie margin once scaled by
 # alpha <= 1.
-FLOOR = {0: 1.0, 1: 1.0, 2: 1e-6, 3: 1.0, 4: 1.0, 5: 1e-6, 6: 0.1}
+# Column 7 is a log-loss statistic in nats (D, H(q) or H(q) - H(p)): its
+# entropies carry absolute errors of about tol times their size, so it takes
+# the log-scale floor.
+FLOOR = {0: 1.0, 1: 1.0, 2: 1e-6, 3: 1.0, 4: 1.0, 5: 1e-6, 6: 0.1, 7: 1.0}
+LOG_RULES = (W.BILD, W.CHOWLOG, W.DIFFLOG, W.OPTLOG)
+TV_RULES = (W.OPT, W.OPTLOG)
 
 
 def host_logits(t):
@@ -139,7 +144,7 @@ def compare(g, o, h, dtype, greedy=False, rep=None):
         rep["exact"] += 1
     if "row_stats" in g:
         gs, os_ = g["row_stats"].astype(np.float64), o["row_stats"]
-        opt_rows = np.isin(h["rule"], (W.OPT,) + TOKEN_RULES)[:, None] & np.ones((1, g1), bool)
+        opt_rows = np.isin(h["rule"], TV_RULES + TOKEN_RULES)[:, None] & np.ones((1, g1), bool)
         # eta of a token row with a near-tie r(v) is the exact sum only up to
         # the q mass of the tied tokens (greedy: column 6 is r at argmax q,
         # whose near-tie the defer check excused): such rows, and the
@@ -148,9 +153,14 @@ def compare(g, o, h, dtype, greedy=False, rep=None):
         opt_rows &= ~tok_near
         rep["near_eta_rows"] += int(tok_near.sum())
         cols = [0, 1, 2, 3, 4, 5]
-        for c in cols + [6]:
+        for c in cols + [6, 7]:
             sel = np.ones(gs.shape[:2], bool) if c != 6 else (opt_rows if not greedy else
                                                              ~tok_near)
+            if c == 7:
+                # the same infinite cross-entropy (q mass where p is 0) agrees
+                same_inf = np.isinf(gs[..., 7]) & (gs[..., 7] == os_[..., 7])
+                sel = sel & ~same_inf
+                rep["inf_stat7"] += int(same_inf.sum())
             if not sel.any():
                 continue
             err = np.abs(gs[..., c] - os_[..., c])[sel] / np.maximum(np.abs(os_[..., c][sel]),

@@ -46,7 +46,7 @@ def _verify(**kw):
     (dict(acc=None), -1), (dict(tok=None), -1), (dict(dm=None), -1),
     (dict(B=0), -2), (dict(gamma=0), -2), (dict(gamma=64), -2), (dict(V=1), -2),
     (dict(B=10000, gamma=7), -2),
-    (dict(rule=8), -3), (dict(rule=-1), -3),
+    (dict(rule=13), -3), (dict(rule=-1), -3), (dict(rule=8, alpha=1.0), -4),
     (dict(alpha=float("nan")), -4), (dict(alpha=float("inf")), -4),
     (dict(T=0.0), -4), (dict(T=-1.0), -4), (dict(T=float("nan")), -4),
     (dict(T=float("inf")), -4), (dict(dtype=7), -4),
@@ -60,7 +60,7 @@ def test_argument_errors(kw, status):
 def test_greedy_argument_errors():
     L = spc.lib()
     # no uniforms needed; bad rule / shape still rejected
-    assert L.spc_greedy_verify(FAKE, FAKE, 1, FAKE, 2, 3, 100, 9, 0.1, FAKE, FAKE, FAKE,
+    assert L.spc_greedy_verify(FAKE, FAKE, 1, FAKE, 2, 3, 100, 13, 0.1, FAKE, FAKE, FAKE,
                                None) == -3
     assert L.spc_greedy_verify(FAKE, FAKE, 1, FAKE, 2, 0, 100, 1, 0.1, FAKE, FAKE, FAKE,
                                None) == -2

@@ -191,7 +191,7 @@ def test_mixed_greedy_and_sampled_sequences():
 def test_invalid_per_sequence_values():
     wl = W.WORKLOADS[3].with_(B=6, V=4000)
     inp = W.generate(wl, 0, DEV)
-    inp["rule"][1] = 9
+    inp["rule"][1] = 13
     inp["alpha"][2] = float("nan")
     inp["temperature"][3] = -1.0
     g = parity.run_gpu(inp)
@@ -349,3 +349,153 @@ def test_token_rule_identical_models():
         parity.compare(g, parity.run_oracle(h), h, wl.dtype)
     for k in ("accept_len", "next_token", "defer", "row_stats"):
         np.testing.assert_array_equal(outs[W.TOKEN_V1][k], outs[W.TOKEN_V2][k])
+
+
+# --------------------------- other targets of Tables 1 and 3 (lossy, BiLD*, log)
+
+NEXT2_RULES = (W.LOSSY, W.BILD, W.CHOWLOG, W.DIFFLOG, W.OPTLOG)
+LOSSY_ALPHAS = (0.0, 0.3, 0.7)
+
+
+def _log_alphas(inp, rule, greedy):
+    """Three alphas for a log-loss rule (or BiLD*) at the quartiles of its
+    statistic on these inputs, taken from the oracle, so that both deferral
+    outcomes occur; for OPTLOG the statistic is divided by D_TV."""
+    h = parity.host_inputs(inp)
+    h["rule"][:] = rule
+    h["alpha"][:] = 0.0
+    o = parity.run_oracle(h, greedy=greedy)
+    s, tv = o["row_stats"][..., 7].ravel(), o["row_stats"][..., 6].ravel()
+    keep = np.isfinite(s) & ((tv > 1e-3) if rule == W.OPTLOG else True)
+    s = s[keep] / tv[keep] if rule == W.OPTLOG else s[keep]
+    return [float(np.float32(x)) for x in np.quantile(s, (0.25, 0.5, 0.75))]
+
+
+def _alphas(rule, inp, greedy=False):
+    return LOSSY_ALPHAS if rule == W.LOSSY else _log_alphas(inp, rule, greedy)
+
+
+@pytest.mark.parametrize("rule", NEXT2_RULES)
+@pytest.mark.parametrize("cfg,steps", [(2, 12), (3, 3)])
+def test_next2_rule_parity(rule, cfg, steps):
+    """Lossy speculative decoding (Lemma 2), BiLD* and the log-loss rules on the
+    T5-vocabulary float32 shape and the Gemma-vocabulary bfloat16 shape."""
+    wl = W.WORKLOADS[cfg].with_(rule=rule, temperature=1.0)
+    for alpha in _alphas(rule, W.generate(wl, 950, DEV)):
+        wa = wl.with_(alpha=alpha)
+        name = f"cfg{cfg}.{W.RULE_NAMES[rule]}.{alpha:.4g}"
+        _flush(f"[next2] {name} steps={steps}")
+        rep = parity.parity_workload(wa, steps, step0=950, report_name=name)
+        _flush(f"[next2] {name} {dict(rep)}")
+        assert rep["exact"] + rep["excused_defer"] + rep["excused_accept"] + \
+            rep["excused_token"] == rep["sequences"]
+
+
+@pytest.mark.parametrize("rule", NEXT2_RULES)
+def test_next2_plain_entry_point(rule):
+    """Batch-wide spc_verify at the benchmark's shape (moments without the
+    per-sequence path)."""
+    wl = W.WORKLOADS[3].with_(rule=rule)
+    alpha = _alphas(rule, W.generate(wl, 720, DEV))[1]
+    rep = parity.parity_workload(wl.with_(alpha=alpha), 2, stats=False, step0=720,
+                                 report_name=f"cfg3.plain.{W.RULE_NAMES[rule]}")
+    assert rep["sequences"] == 2 * 32
+
+
+@pytest.mark.parametrize("rule", NEXT2_RULES)
+def test_next2_greedy_parity(rule):
+    """Temperature 0: log-loss rules on temperature-1 entropies, BiLD* with
+    D = -log p(argmax q), lossy's one-hot target at argmax p."""
+    wl = W.WORKLOADS[4].with_(B=64, V=50000, rule=rule)
+    for alpha in _alphas(rule, W.generate(wl, 310, DEV), greedy=True):
+        _flush(f"[next2] greedy {W.RULE_NAMES[rule]} alpha={alpha:.4g}")
+        parity.parity_workload(wl.with_(alpha=alpha), 3, step0=310,
+                               report_name=f"greedy.{W.RULE_NAMES[rule]}")
+
+
+def test_lossy_alpha0_is_speculative_sampling():
+    """Lemma 2 at alpha = 0 (beta = 1): the target is p, so every draw matches
+    the always-defer rule (standard speculative sampling) exactly."""
+    for cfg in (3, 2):
+        wl = W.WORKLOADS[cfg].with_(B=16, V=40000)
+        inp = W.generate(wl, 21, DEV)
+        out = {}
+        for rule in (W.LOSSY, W.ALWAYS):
+            inp["rule"][:] = rule
+            inp["alpha"][:] = 0.0
+            out[rule] = parity.run_gpu(inp)
+        for k in ("accept_len", "next_token", "sample_norm"):
+            np.testing.assert_array_equal(out[W.LOSSY][k], out[W.ALWAYS][k])
+        assert (out[W.LOSSY]["defer"] == 0).all() and (out[W.ALWAYS]["defer"] == 1).all()
+
+
+def test_next2_mixed_per_sequence():
+    """The new rules next to Table 1 and token rules, with per-sequence
+    temperatures including 0 (the argmax-and-moments statistics kernel)."""
+    wl = W.WORKLOADS[5].with_(B=30, V=30000)
+    inp = W.generate(wl, 17, DEV)
+    rules = [W.LOSSY, W.BILD, W.CHOWLOG, W.DIFFLOG, W.OPTLOG, W.DIFF, W.TOKEN_V2, W.OPT]
+    alphas = {W.LOSSY: 0.3, W.BILD: 7.5, W.CHOWLOG: 6.5, W.DIFFLOG: 0.5, W.OPTLOG: 1.5,
+              W.DIFF: 0.05, W.TOKEN_V2: 0.05, W.OPT: 0.1}
+    sel = [rules[i % len(rules)] for i in range(wl.B)]
+    inp["rule"][:] = torch.tensor(sel, dtype=torch.int32, device=DEV)
+    inp["alpha"][:] = torch.tensor([alphas[r] for r in sel], device=DEV)
+    inp["temperature"][::4] = 0.0
+    g = parity.run_gpu(inp)
+    h = parity.host_inputs(inp)
+    greedy = h["temperature"] == 0
+    for s, gr in ((greedy, True), (~greedy, False)):
+        hs = {k: v[s] for k, v in h.items()}
+        gs = {k: v[s] for k, v in g.items()}
+        rep = parity.compare(gs, parity.run_oracle(hs, greedy=gr), hs, wl.dtype, greedy=gr)
+        _flush(f"[next2] mixed greedy={gr} {dict(rep)}")
+
+
+@pytest.mark.parametrize("rule,alpha", [(W.BILD, 6.0), (W.OPTLOG, 1.0), (W.LOSSY, 0.3),
+                                        (W.CHOWLOG, 5.0)])
+def test_next2_masked_logits(rule, alpha):
+    """-inf entries in both tensors: BiLD*'s cross-entropy is infinite where q
+    keeps mass on a token p masks."""
+    for cfg, dtype in ((3, "bf16"), (2, "f32")):
+        wl = W.WORKLOADS[cfg].with_(B=8, V=12345, dtype=dtype, rule=rule, alpha=alpha)
+        inp = W.generate(wl, 2, DEV)
+        g0 = torch.Generator(device=DEV).manual_seed(98)
+        for k in ("q", "p"):
+            m = torch.rand(inp[k].shape, generator=g0, device=DEV) < 0.3
+            m[..., 0] = False
+            if k == "p" and rule == W.BILD:
+                m[::2] = False  # half the sequences keep a finite cross-entropy
+            inp[k][m] = float("-inf")
+        inp["draft"] = W.draw_drafts(inp["q"], inp["temperature"], g0)
+        g = parity.run_gpu(inp)
+        h = parity.host_inputs(inp)
+        rep = parity.compare(g, parity.run_oracle(h), h, wl.dtype)
+        if rule == W.BILD:
+            assert rep["inf_stat7"] > 0
+
+
+def test_next2_out_of_range_and_identical():
+    """Out-of-range drafts are rejected under every new rule; with p = q the
+    log-loss difference is 0 and lossy decoding keeps every draft."""
+    wl = W.WORKLOADS[3].with_(B=8, V=3000)
+    inp = W.generate(wl, 1, DEV)
+    inp["draft"][:, 2] = torch.tensor([-1, 3000, 1 << 30, -(1 << 30), 2999, 0, -5, 3001],
+                                      dtype=torch.int32, device=DEV)
+    inp["uniforms"][:, :2] = 0.0
+    for rule, alpha in ((W.LOSSY, 0.3), (W.BILD, 5.0), (W.CHOWLOG, 4.0), (W.DIFFLOG, 0.2),
+                        (W.OPTLOG, 0.5)):
+        inp["rule"][:] = rule
+        inp["alpha"][:] = alpha
+        g = parity.run_gpu(inp)
+        h = parity.host_inputs(inp)
+        parity.compare(g, parity.run_oracle(h), h, wl.dtype)
+    same = W.generate(wl.with_(B=16, V=20000), 3, DEV)
+    same["p"] = same["q"].clone()
+    for rule, alpha in ((W.LOSSY, 0.3), (W.DIFFLOG, 0.0), (W.OPTLOG, 0.5)):
+        same["rule"][:] = rule
+        same["alpha"][:] = alpha
+        g = parity.run_gpu(same)
+        assert (g["accept_len"] == wl.gamma).all()
+        assert (g["defer"] == 0).all()
+        h = parity.host_inputs(same)
+        parity.compare(g, parity.run_oracle(h), h, wl.dtype)
