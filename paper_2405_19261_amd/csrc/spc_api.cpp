@@ -204,8 +204,14 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   const bool need_tv = need_sample && (per_rule || rule == SPC_RULE_OPT ||
                                        rule == SPC_RULE_OPTLOG || token);
   const bool need_argmax = force_greedy || per_temp;
-  const bool need_mom = per_rule || (rule >= SPC_RULE_BILD && rule <= SPC_RULE_OPTLOG);
-  e = spc::launch_verify(P, dtype, vec, need_tv, need_sample, need_argmax, need_mom,
+  // rows that need first moments (log-loss rules; BiLD* at temperature > 0)
+  // and rows that do not each get their statistics kernel
+  const bool log_rule = rule >= SPC_RULE_BILD && rule <= SPC_RULE_OPTLOG;
+  const bool bild_greedy_only = rule == SPC_RULE_BILD && force_greedy;
+  const bool need_mom = per_rule || (log_rule && !bild_greedy_only);
+  const bool need_plain = per_rule || per_temp || !log_rule || bild_greedy_only;
+  P.mom_split = (need_mom && need_plain) ? 1 : 0;
+  e = spc::launch_verify(P, dtype, vec, need_tv, need_sample, need_argmax, need_plain, need_mom,
                          ex ? ex->ev_hot_begin : nullptr, ex ? ex->ev_hot_end : nullptr,
                          stream);
   if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));

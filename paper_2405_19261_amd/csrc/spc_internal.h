@@ -63,6 +63,8 @@ struct Params {
   int32_t rule;
   float alpha, temp;
   int32_t force_greedy;    // spc_greedy_verify: every sequence at temperature 0
+  int32_t mom_split;       // the moment statistics kernel runs too: the plain one
+                           // leaves it the rows that need first moments
   const int32_t* rule_ps;
   const float* alpha_ps;
   const float* temp_ps;
@@ -97,10 +99,11 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec);
 // Enqueue the kernels of one verify call.  need_tv: the batch may hold OPT,
 // OPTLOG or token-rule sequences at temperature > 0; need_sample: it may hold
 // sequences at temperature > 0; need_argmax: it may hold greedy (temperature
-// 0) sequences; need_mom: it may hold log-loss or BiLD* sequences.  Returns
-// the first launch error.
+// 0) sequences; need_plain / need_mom: it may hold rows that need no first
+// moments / rows that do (log-loss rules, BiLD* at temperature > 0), each
+// kind handled by its own statistics kernel.  Returns the first launch error.
 hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
-                         bool need_argmax, bool need_mom, hipEvent_t ev_begin,
+                         bool need_argmax, bool need_plain, bool need_mom, hipEvent_t ev_begin,
                          hipEvent_t ev_end, hipStream_t stream);
 
 }  // namespace spc

@@ -1277,6 +1277,8 @@ __device__ __forceinline__ void stats_tile(const Params& P) {
   __shared__ Shared sh;
   const int k = blockIdx.x, r = blockIdx.y;
   const SeqParam sp = seq_param(P, r / (P.gamma + 1));
+  // rows that need first moments belong to the moment kernel (block-uniform)
+  if (MOM ? !needs_mom(sp) : (P.mom_split && needs_mom(sp))) return;
   const int V = P.V;
   const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
   const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
@@ -1304,15 +1306,15 @@ __device__ __forceinline__ void stats_tile(const Params& P) {
       mq = fmaxf(mq, vq);
       mp = fmaxf(mp, vp);
     }
-  if constexpr (MOM) __builtin_amdgcn_sched_barrier(0);
   const float rq = (mq == kNegInf) ? 0.0f : mq * sp.c_hi;
   const float rp = (mp == kNegInf) ? 0.0f : mp * sp.c_hi;
   float sq = 0.0f, spp = 0.0f, hq = 0.0f, hp = 0.0f, xq = 0.0f;
-  const bool mom = MOM && needs_mom(sp);  // block-uniform
-  if (mom)
-    tile_sums<DT, VEC, true>(wq, wp, sp, rq, rp, sq, spp, hq, hp, xq);
-  else
-    tile_sums<DT, VEC, false>(wq, wp, sp, rq, rp, sq, spp, hq, hp, xq);
+  constexpr bool mom = MOM;
+  tile_sums<DT, VEC, MOM>(wq, wp, sp, rq, rp, sq, spp, hq, hp, xq);
+  // the moments are complete here: left free, the compiler sinks their
+  // accumulation into the conditional combine below and keeps every
+  // exponential of the tile live until then
+  if constexpr (MOM) asm volatile("" : "+v"(hq), "+v"(hp), "+v"(xq), "+v"(sq), "+v"(spp));
   if constexpr (ARGMAX && MOM) {
     // the lowest entry equal to the thread max, in a pass of its own
     __builtin_amdgcn_sched_barrier(0);
@@ -1324,6 +1326,7 @@ __device__ __forceinline__ void stats_tile(const Params& P) {
         if (elem<DT, VEC>(wq[i], e) == mq) iq = idx;
         if (elem<DT, VEC>(wp[i], e) == mp) ip = idx;
       }
+    asm volatile("" : "+v"(iq), "+v"(ip));
   }
   // Wave partials against the wave max (r_t - r_w is exact in fp64; only its
   // rounding to float is inexact), then one barrier and thread 0 combines the
@@ -1337,7 +1340,7 @@ __device__ __forceinline__ void stats_tile(const Params& P) {
   dq = wave_sum(dq);
   dp = wave_sum(dp);
   double mhq = 0.0, mhp = 0.0, mx = 0.0;
-  if (mom) {
+  if constexpr (mom) {
     mhq = wave_sum(mq == kNegInf ? 0.0 : mom_move(hq, sq, fq, eq));
     mhp = wave_sum(mp == kNegInf ? 0.0 : mom_move(hp, spp, fp, ep));
     mx = wave_sum(mq == kNegInf ? 0.0 : mom_move(xq, sq, fq, ep));
@@ -1353,7 +1356,7 @@ __device__ __forceinline__ void stats_tile(const Params& P) {
     sh.d[wv][1] = dp;
     sh.i[wv][0] = iq;
     sh.i[wv][1] = ip;
-    if (mom) {
+    if constexpr (mom) {
       sh.h[wv][0] = mhq;
       sh.h[wv][1] = mhp;
       sh.h[wv][2] = mx;
@@ -1390,7 +1393,7 @@ __device__ __forceinline__ void stats_tile(const Params& P) {
     t.amax_q = ARGMAX ? aq : -1;
     t.amax_p = ARGMAX ? ap : -1;
     P.tiles[(int64_t)r * P.nt + k] = t;
-    if (mom) {
+    if constexpr (mom) {
       // the waves' moments against the tile references, in wave order
       TileMom m{0.0, 0.0, 0.0};
 #pragma unroll
@@ -1415,9 +1418,10 @@ __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
   stats_tile<DT, VEC, ARGMAX, false>(P);
 }
 
-// With first moments (batches that may hold BiLD* or log-loss sequences).
-// Held to SPC_MOM_OCCUPANCY resident workgroups per CU: left free, the
-// compiler keeps every exponential of the tile live at once.
+// With first moments, for the rows of BiLD* (temperature > 0) and log-loss
+// sequences only; the plain kernel takes every other row.  Held to
+// SPC_MOM_OCCUPANCY resident workgroups per CU: left free, the compiler
+// keeps every exponential of the tile live at once.
 #ifndef SPC_MOM_OCCUPANCY
 #define SPC_MOM_OCCUPANCY 6
 #endif
@@ -1514,22 +1518,26 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
 
 template <int DT, bool VEC>
 hipError_t launch_t(const Params& P, bool need_tv, bool need_sample, bool need_argmax,
-                    bool need_mom, hipEvent_t e0, hipEvent_t e1, hipStream_t st) {
+                    bool need_plain, bool need_mom, hipEvent_t e0, hipEvent_t e1,
+                    hipStream_t st) {
   const unsigned R = (unsigned)(P.B * (P.gamma + 1));
   const dim3 grid(P.nt, R);
   hipError_t err;
   if (e0 && (err = hipEventRecord(e0, st)) != hipSuccess) return err;
+  if (need_plain) {
+    if (need_argmax)
+      hipLaunchKernelGGL((k_stats<DT, VEC, true>), grid, dim3(kThreads), 0, st, P);
+    else
+      hipLaunchKernelGGL((k_stats<DT, VEC, false>), grid, dim3(kThreads), 0, st, P);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+  }
   if (need_mom) {
     if (need_argmax)
       hipLaunchKernelGGL((k_stats_mom<DT, VEC, true>), grid, dim3(kThreads), 0, st, P);
     else
       hipLaunchKernelGGL((k_stats_mom<DT, VEC, false>), grid, dim3(kThreads), 0, st, P);
-  } else if (need_argmax) {
-    hipLaunchKernelGGL((k_stats<DT, VEC, true>), grid, dim3(kThreads), 0, st, P);
-  } else {
-    hipLaunchKernelGGL((k_stats<DT, VEC, false>), grid, dim3(kThreads), 0, st, P);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
   }
-  if ((err = hipGetLastError()) != hipSuccess) return err;
   if (e1 && (err = hipEventRecord(e1, st)) != hipSuccess) return err;
   if (need_tv) {
     hipLaunchKernelGGL((k_tv<DT, VEC>), dim3(P.nt, R), dim3(kThreads), 0, st, P);
@@ -1564,14 +1572,18 @@ int samp_groups(int64_t nc, int B, int cus) {
 }
 
 hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
-                         bool need_argmax, bool need_mom, hipEvent_t e0, hipEvent_t e1,
-                         hipStream_t st) {
+                         bool need_argmax, bool need_plain, bool need_mom, hipEvent_t e0,
+                         hipEvent_t e1, hipStream_t st) {
   if (dtype == 1) {
-    return vec ? launch_t<1, true>(P, need_tv, need_sample, need_argmax, need_mom, e0, e1, st)
-               : launch_t<1, false>(P, need_tv, need_sample, need_argmax, need_mom, e0, e1, st);
+    return vec ? launch_t<1, true>(P, need_tv, need_sample, need_argmax, need_plain, need_mom,
+                                   e0, e1, st)
+               : launch_t<1, false>(P, need_tv, need_sample, need_argmax, need_plain, need_mom,
+                                    e0, e1, st);
   }
-  return vec ? launch_t<0, true>(P, need_tv, need_sample, need_argmax, need_mom, e0, e1, st)
-             : launch_t<0, false>(P, need_tv, need_sample, need_argmax, need_mom, e0, e1, st);
+  return vec ? launch_t<0, true>(P, need_tv, need_sample, need_argmax, need_plain, need_mom, e0,
+                                 e1, st)
+             : launch_t<0, false>(P, need_tv, need_sample, need_argmax, need_plain, need_mom, e0,
+                                  e1, st);
 }
 
 }  // namespace spc
