@@ -196,6 +196,9 @@ def main():
     rule_desc = (f"{W.RULE_NAMES[wl.rule]} alpha={wl.alpha:g}" if wl.rule in W.RULE_NAMES
                  else "per-sequence rules")
     per_seq = args.cfg in (4, 5)  # greedy / mixed batches: per-sequence arrays
+    # the rules the per-sequence arrays hold (the library skips passes for the others)
+    rule_mask = (sum(1 << r for r, _ in W.CFG5_RULES) if args.cfg == 5 else 1 << wl.rule) \
+        if per_seq else 0
     if args.cfg != 3:
         args.no_cpu_baseline = True
     dev = torch.device("cuda:0")
@@ -223,7 +226,7 @@ def main():
             spc.spc_verify_ex(s["q"], s["p"], s["draft"], s["uniforms"], 0, 0.0, 1.0,
                               rule_per_seq=s["rule"], alpha_per_seq=s["alpha"],
                               temp_per_seq=temp, ev_hot_begin=ev0, ev_hot_end=ev1,
-                              out=outs[i % len(sets)], stream=stream)
+                              rules_present=rule_mask, out=outs[i % len(sets)], stream=stream)
         elif events is None:
             spc.spc_verify(s["q"], s["p"], s["draft"], s["uniforms"], wl.rule, wl.alpha,
                            wl.temperature, out=outs[i % len(sets)], stream=stream)

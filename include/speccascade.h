@@ -170,7 +170,13 @@ spc_status spc_greedy_verify(const void* q_logits, const void* p_logits, spc_dty
  *       use and grown as needed.
  *   ev_hot_begin, ev_hot_end  optional HIP events recorded on `stream`
  *       immediately before and after the vocabulary-streaming statistics
- *       kernel, for timing it alone.
+ *       kernel(s), for timing them alone.
+ *   rules_present  with rule_per_seq: a bitmask (bit i = rule i) of the
+ *       rules the array may hold, 0 = any.  It lets the library skip the
+ *       passes no sequence needs (the second pass of OPT, OPTLOG and the
+ *       token rules; the first moments of BiLD* and the log-loss rules).  A
+ *       sequence whose rule lies outside a nonzero mask is invalid (it
+ *       reports accept_len = -1 and next_token = -1).
  */
 typedef struct {
   const int32_t* rule_per_seq;
@@ -183,6 +189,7 @@ typedef struct {
   size_t workspace_bytes;
   hipEvent_t ev_hot_begin;
   hipEvent_t ev_hot_end;
+  uint32_t rules_present;
 } spc_verify_ex_args;
 
 /* spc_verify with extended arguments; `ex` may be NULL.  `temperature`

@@ -198,18 +198,25 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   // sequences at temperature > 0 may exist unless the whole batch is greedy;
   // OPT at temperature > 0 needs the TV pass
   const bool need_sample = !force_greedy && (per_temp || temperature > 0.0f);
-  // OPT, OPTLOG (D_TV) and the token rules (eta) need the second pass over
-  // their rows; BiLD* and the log-loss rules take first moments
-  const bool token = rule >= SPC_RULE_TOKEN_V1 && rule <= SPC_RULE_TOKEN_V3;
-  const bool need_tv = need_sample && (per_rule || rule == SPC_RULE_OPT ||
-                                       rule == SPC_RULE_OPTLOG || token);
+  // The rules the batch may hold decide the passes.  OPT, OPTLOG (D_TV) and
+  // the token rules (eta) need the second pass over their rows at
+  // temperature > 0; rows that need first moments (log-loss rules, BiLD* at
+  // temperature > 0) and rows that do not each get their statistics kernel.
+  constexpr uint32_t kAll = (1u << (SPC_RULE_OPTLOG + 1)) - 1u;
+  constexpr uint32_t kTv = (1u << SPC_RULE_OPT) | (1u << SPC_RULE_OPTLOG) |
+                           (1u << SPC_RULE_TOKEN_V1) | (1u << SPC_RULE_TOKEN_V2) |
+                           (1u << SPC_RULE_TOKEN_V3);
+  constexpr uint32_t kLog = (1u << SPC_RULE_BILD) | (1u << SPC_RULE_CHOWLOG) |
+                            (1u << SPC_RULE_DIFFLOG) | (1u << SPC_RULE_OPTLOG);
+  const uint32_t mask = ex ? ex->rules_present & kAll : 0u;
+  const uint32_t rules = per_rule ? (mask ? mask : kAll) : (1u << rule);
+  P.rule_mask = per_rule ? mask : 0u;
+  const bool need_tv = need_sample && (rules & kTv);
   const bool need_argmax = force_greedy || per_temp;
-  // rows that need first moments (log-loss rules; BiLD* at temperature > 0)
-  // and rows that do not each get their statistics kernel
-  const bool log_rule = rule >= SPC_RULE_BILD && rule <= SPC_RULE_OPTLOG;
-  const bool bild_greedy_only = rule == SPC_RULE_BILD && force_greedy;
-  const bool need_mom = per_rule || (log_rule && !bild_greedy_only);
-  const bool need_plain = per_rule || per_temp || !log_rule || bild_greedy_only;
+  // BiLD* at temperature 0 reads one logit instead of moments
+  const bool bild_t0 = (rules & (1u << SPC_RULE_BILD)) && (force_greedy || per_temp);
+  const bool need_mom = (rules & kLog) && !(rules == (1u << SPC_RULE_BILD) && force_greedy);
+  const bool need_plain = (rules & ~kLog) || per_temp || bild_t0;
   P.mom_split = (need_mom && need_plain) ? 1 : 0;
   e = spc::launch_verify(P, dtype, vec, need_tv, need_sample, need_argmax, need_plain, need_mom,
                          ex ? ex->ev_hot_begin : nullptr, ex ? ex->ev_hot_end : nullptr,

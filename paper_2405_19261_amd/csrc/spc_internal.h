@@ -65,6 +65,7 @@ struct Params {
   int32_t force_greedy;    // spc_greedy_verify: every sequence at temperature 0
   int32_t mom_split;       // the moment statistics kernel runs too: the plain one
                            // leaves it the rows that need first moments
+  uint32_t rule_mask;      // rules per-sequence arrays may hold (0: any)
   const int32_t* rule_ps;
   const float* alpha_ps;
   const float* temp_ps;

@@ -353,7 +353,8 @@ __device__ __forceinline__ SeqParam seq_param(const Params& P, int b) {
   s.alpha = (double)alpha;
   s.valid = s.rule >= SPC_RULE_CHOW && s.rule <= SPC_RULE_OPTLOG && isfinite(alpha) &&
             isfinite(T) && T >= 0.0f && (T == 0.0f || T >= 1e-20f) &&
-            (s.rule != SPC_RULE_LOSSY || alpha < 1.0f);
+            (s.rule != SPC_RULE_LOSSY || alpha < 1.0f) &&
+            (!P.rule_ps || !P.rule_mask || ((P.rule_mask >> s.rule) & 1u));
   s.greedy = P.force_greedy || T == 0.0f;
   s.c = kLog2e / ((s.greedy || !s.valid) ? 1.0 : (double)T);
   // split c so that z*c_hi + z*c_lo carries ~48 bits of c; c_lo > 0 keeps

@@ -32,7 +32,7 @@ class ExArgs(ctypes.Structure):
     _fields_ = [("rule_per_seq", _P), ("alpha_per_seq", _P), ("temp_per_seq", _P),
                 ("out_row_stats", _P), ("out_argmax", _P), ("out_sample_norm", _P),
                 ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
-                ("ev_hot_begin", _P), ("ev_hot_end", _P)]
+                ("ev_hot_begin", _P), ("ev_hot_end", _P), ("rules_present", ctypes.c_uint32)]
 
 
 class SpcError(RuntimeError):
@@ -155,11 +155,12 @@ def spc_greedy_verify(q, p, draft, rule, alpha, out=None, stream=None):
 def spc_verify_ex(q, p, draft, uniforms, rule, alpha, temperature, rule_per_seq=None,
                   alpha_per_seq=None, temp_per_seq=None, out_row_stats=None, out_argmax=None,
                   out_sample_norm=None, workspace=None, ev_hot_begin=None, ev_hot_end=None,
-                  out=None, stream=None):
+                  rules_present=0, out=None, stream=None):
     """spc_verify with per-sequence parameters and optional outputs.
     ev_hot_begin / ev_hot_end: hipEvent_t handles (ints or objects with a
     ``handle`` / ``cuda_event`` attribute) recorded around the statistics
-    kernel."""
+    kernel.  rules_present: bitmask of the rule ids rule_per_seq may hold
+    (0 = any)."""
     B, gamma, V = _shape(q, p, draft)
     acc, tok, dm = _outputs(q, B, gamma, out)
     ex = ExArgs()
@@ -174,6 +175,7 @@ def spc_verify_ex(q, p, draft, uniforms, rule, alpha, temperature, rule_per_seq=
         ex.workspace_bytes = workspace.numel() * workspace.element_size()
     ex.ev_hot_begin = _event(ev_hot_begin)
     ex.ev_hot_end = _event(ev_hot_end)
+    ex.rules_present = int(rules_present)
     _check(lib().spc_verify_ex(_ptr(q), _ptr(p), _dtype_code(q), _ptr(draft), _ptr(uniforms), B,
                                gamma, V, int(rule), float(alpha), float(temperature), _ptr(acc),
                                _ptr(tok), _ptr(dm), ctypes.byref(ex), _stream(stream)))

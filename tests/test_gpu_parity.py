@@ -499,3 +499,30 @@ def test_next2_out_of_range_and_identical():
         assert (g["defer"] == 0).all()
         h = parity.host_inputs(same)
         parity.compare(g, parity.run_oracle(h), h, wl.dtype)
+
+
+def test_rules_present_hint():
+    """A rules_present mask that covers the per-sequence rules changes nothing;
+    a sequence whose rule lies outside it is invalid."""
+    wl = W.WORKLOADS[5].with_(B=24, V=30000)
+    inp = W.generate(wl, 5, DEV)
+    inp["temperature"][::5] = 0.0
+    mask = sum(1 << r for r, _ in W.CFG5_RULES)
+    out = {}
+    for m in (0, mask):
+        acc, tok, dm = spc.spc_verify_ex(inp["q"], inp["p"], inp["draft"], inp["uniforms"], 0,
+                                         0.0, 1.0, rule_per_seq=inp["rule"],
+                                         alpha_per_seq=inp["alpha"],
+                                         temp_per_seq=inp["temperature"], rules_present=m)
+        torch.cuda.synchronize()
+        out[m] = (acc.cpu().numpy(), tok.cpu().numpy(), dm.cpu().numpy())
+    for a, b in zip(out[0], out[mask]):
+        np.testing.assert_array_equal(a, b)
+    inp["rule"][3] = W.BILD  # outside the mask
+    acc, tok, _ = spc.spc_verify_ex(inp["q"], inp["p"], inp["draft"], inp["uniforms"], 0, 0.0,
+                                    1.0, rule_per_seq=inp["rule"], alpha_per_seq=inp["alpha"],
+                                    temp_per_seq=inp["temperature"], rules_present=mask)
+    torch.cuda.synchronize()
+    assert acc[3].item() == -1 and tok[3].item() == -1
+    keep = [b for b in range(wl.B) if b != 3]
+    np.testing.assert_array_equal(acc.cpu().numpy()[keep], out[0][0][keep])
