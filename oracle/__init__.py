@@ -62,6 +62,8 @@ def lib():
         L.orc_lossy_target.restype = None
         L.orc_sample.argtypes = [_P, _I64, _D, ctypes.POINTER(_D)]
         L.orc_sample.restype = _I32
+        L.orc_draft_sample.argtypes = [_P, ctypes.c_int, _I32, _I64, _P, _P, _P, _P]
+        L.orc_draft_sample.restype = ctypes.c_int
         L.orc_verify.argtypes = [_P, _P, ctypes.c_int, _P, _P, _I32, _I32, _I64, _P, _P, _P,
                                  _P, _P, _P, _P, _P, _P, _P, _P, _P]
         L.orc_verify.restype = ctypes.c_int
@@ -261,3 +263,20 @@ def greedy_verify(q, p, draft, rule, alpha):
     if rc != 0:
         raise ValueError("orc_greedy_verify rejected its arguments")
     return out
+
+
+def draft_sample(logits, temperature, uniforms=None):
+    """The drafter's sampling step: one token per row of ``logits`` [B, V]
+    from softmax(z / T_b) by the inverse CDF at ``uniforms[b]``, or the argmax
+    where T_b = 0.  Returns (tokens [B] int32, margins [B])."""
+    z, dt = _logits(logits)
+    B, V = z.shape
+    T = np.ascontiguousarray(np.broadcast_to(np.asarray(temperature, np.float32), (B,)))
+    u = None if uniforms is None else np.ascontiguousarray(uniforms, np.float32)
+    tok = np.empty(B, np.int32)
+    mg = np.empty(B, np.float64)
+    rc = lib().orc_draft_sample(_ptr(z), dt, B, V, _ptr(T), None if u is None else _ptr(u),
+                                _ptr(tok), _ptr(mg))
+    if rc != 0:
+        raise ValueError("orc_draft_sample: bad arguments")
+    return tok, mg

@@ -418,6 +418,39 @@ int orc_verify(const void* q_logits, const void* p_logits, int dtype, const int3
   return err ? -1 : 0;
 }
 
+int orc_draft_sample(const void* logits, int dtype, int32_t B, int64_t V,
+                     const float* temperature, const float* uniforms, int32_t* tokens,
+                     double* margin) {
+  if (!logits || !temperature || !tokens || B < 1 || V < 1) return -1;
+  if (dtype != ORC_F32 && dtype != ORC_BF16 && dtype != ORC_F64) return -1;
+  for (int32_t b = 0; b < B; ++b)
+    if (!(temperature[b] >= 0.0f) || (temperature[b] > 0.0f && !uniforms)) return -1;
+  int err = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int32_t b = 0; b < B; ++b) {
+    const void* z = row_ptr(logits, dtype, b, V);
+    orc_row_stats st;
+    if (temperature[b] == 0.0f) { /* greedy: argmax of the raw logits */
+      orc_softmax_row(z, dtype, V, 1.0, NULL, &st);
+      tokens[b] = st.argmax;
+      if (margin) margin[b] = INFINITY;
+      continue;
+    }
+    double* q = malloc(sizeof(double) * (size_t)V);
+    if (!q) {
+#pragma omp atomic write
+      err = 1;
+      continue;
+    }
+    orc_softmax_row(z, dtype, V, (double)temperature[b], q, &st);
+    double mg;
+    tokens[b] = orc_sample(q, V, (double)uniforms[b], &mg);
+    if (margin) margin[b] = mg;
+    free(q);
+  }
+  return err ? -1 : 0;
+}
+
 int orc_greedy_verify(const void* q_logits, const void* p_logits, int dtype,
                       const int32_t* draft, int32_t B, int32_t gamma, int64_t V,
                       const int32_t* rule, const float* alpha, int32_t* accept_len,

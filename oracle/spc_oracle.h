@@ -166,6 +166,16 @@ int orc_greedy_verify(const void* q_logits, const void* p_logits, int dtype,
                       int32_t* next_token, uint8_t* defer, double* row_stats,
                       int32_t* argmax_qp, double* defer_margin, int32_t* flags);
 
+/* The drafter's sampling step of Alg. 4, x_{t+j} ~ q_{t+j}: for each of B
+ * rows of V logits, the inverse-CDF draw (orc_sample) from softmax(z / T_b)
+ * with uniform u[b], or at T_b = 0 the argmax of the raw logits (smallest
+ * index).  uniforms may be NULL when every T_b is 0.  tokens [B]; margin [B]
+ * (may be NULL) is orc_sample's margin (infinity for an argmax).  Returns 0,
+ * or -1 on an argument error. */
+int orc_draft_sample(const void* logits, int dtype, int32_t B, int64_t V,
+                     const float* temperature, const float* uniforms, int32_t* tokens,
+                     double* margin);
+
 /* Number of OpenMP threads orc_verify uses. */
 int orc_num_threads(void);
 
