@@ -202,6 +202,28 @@ spc_status spc_verify_ex(const void* q_logits, const void* p_logits, spc_dtype d
                          uint8_t* out_defer_mask, const spc_verify_ex_args* ex,
                          hipStream_t stream);
 
+/*
+ * spc_draft_sample -- the drafter's sampling step of GenSpecSample (Alg. 4):
+ * x_{t+j} ~ q_{t+j} = softmax(z / T) for one position of each of B sequences.
+ *
+ *   logits        [B][V] drafter logits, `dtype`, rows contiguous
+ *   temperature   T for every sequence (T = 0: the argmax of the raw logits,
+ *                 lowest index on a tie), unless temp_per_seq is given
+ *   temp_per_seq  [B] float32 per-sequence temperatures, or NULL
+ *   uniforms      [B] float32 in [0,1): the token is the smallest k whose
+ *                 cumulative mass (vocabulary order) exceeds u times the
+ *                 total; may be NULL when every temperature is 0
+ *   out_token     [B] int32
+ * Uses the statistics pass and the tile-mass draw of spc_verify (one pass
+ * over the logits); needs the internal workspace (a γ = 0 step of size
+ * spc_workspace_bytes(B, 1, V, dtype) suffices).  Errors as spc_verify; a
+ * negative or non-finite temperature is SPC_E_PARAM, an invalid per-sequence
+ * one gives out_token = -1.
+ */
+spc_status spc_draft_sample(const void* logits, spc_dtype dtype, int32_t B, int32_t V,
+                            float temperature, const float* temp_per_seq,
+                            const float* uniforms, int32_t* out_token, hipStream_t stream);
+
 /* Bytes of device workspace one call of this shape needs. */
 size_t spc_workspace_bytes(int32_t B, int32_t gamma, int32_t V, spc_dtype dtype);
 

@@ -74,6 +74,8 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
   const int64_t nc = (V + samp_chunk_elems(dtype, vec) - 1) / samp_chunk_elems(dtype, vec);
   L.masses = o; o = align_up(o + sizeof(double) * B * nc, 256);
   L.moms = o; o = align_up(o + sizeof(TileMom) * R * nt, 256);
+  // accepted lengths and masks of a drafter sampling step (not returned)
+  L.draft_out = o; o = align_up(o + 5 * (size_t)B, 256);
   L.total = o;
   return L;
 }
@@ -93,16 +95,19 @@ spc_status check_shape(int32_t B, int32_t gamma, int32_t V) {
   return SPC_OK;
 }
 
+// draft_mode: the drafter's sampling step, run as a gamma = 0 step of rule
+// NEVER on one logit tensor (q = p); its accepted lengths and masks go to
+// the workspace.
 spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int32_t* draft,
                        const float* uniforms, int32_t B, int32_t gamma, int32_t V, int32_t rule,
                        float alpha, float temperature, bool force_greedy, int32_t* out_accept,
                        int32_t* out_token, uint8_t* out_defer, const spc_verify_ex_args* ex,
-                       hipStream_t stream) {
+                       hipStream_t stream, bool draft_mode = false) {
   g_err.clear();
-  if (!q || !p || !draft || !out_accept || !out_token || !out_defer)
+  if (!q || !p || (!draft_mode && (!draft || !out_accept || !out_defer)) || !out_token)
     return fail(SPC_E_NULL, "a required pointer is NULL");
   if (!force_greedy && !uniforms) return fail(SPC_E_NULL, "uniforms is NULL");
-  spc_status st = check_shape(B, gamma, V);
+  spc_status st = draft_mode ? check_shape(B, 1, V) : check_shape(B, gamma, V);
   if (st != SPC_OK) return st;
   if (dtype != SPC_F32 && dtype != SPC_BF16) return fail(SPC_E_PARAM, "unknown dtype %d", dtype);
   const bool per_rule = ex && ex->rule_per_seq;
@@ -116,6 +121,7 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   if (!force_greedy && !per_temp && !(isfinite(temperature) && temperature >= 1e-20f))
     return fail(SPC_E_PARAM, "temperature must be finite and >= 1e-20 (got %g)",
                 (double)temperature);
+  if (draft_mode) gamma = 0;
   if (((uintptr_t)q | (uintptr_t)p) % 16 != 0)
     return fail(SPC_E_ALIGN, "logit base pointers must be 16-byte aligned");
 
@@ -194,6 +200,10 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   P.tvpart = reinterpret_cast<double*>(ws + L.tvpart);
   P.masses = reinterpret_cast<double*>(ws + L.masses);
   P.moms = reinterpret_cast<spc::TileMom*>(ws + L.moms);
+  if (draft_mode) {
+    P.out_accept = reinterpret_cast<int32_t*>(ws + L.draft_out);
+    P.out_defer = reinterpret_cast<uint8_t*>(ws + L.draft_out + 4 * (size_t)B);
+  }
 
   // sequences at temperature > 0 may exist unless the whole batch is greedy;
   // OPT at temperature > 0 needs the TV pass
@@ -257,6 +267,22 @@ spc_status spc_verify_ex(const void* q_logits, const void* p_logits, spc_dtype d
   return verify_impl(q_logits, p_logits, dtype, draft_tokens, uniforms, B, gamma, V, rule, alpha,
                      temperature, false, out_accept_len, out_next_token, out_defer_mask, ex,
                      stream);
+}
+
+spc_status spc_draft_sample(const void* logits, spc_dtype dtype, int32_t B, int32_t V,
+                            float temperature, const float* temp_per_seq,
+                            const float* uniforms, int32_t* out_token, hipStream_t stream) {
+  g_err.clear();
+  if (!temp_per_seq && !(isfinite(temperature) && temperature >= 0.0f))
+    return fail(SPC_E_PARAM, "temperature must be finite and >= 0 (got %g)",
+                (double)temperature);
+  const bool greedy = !temp_per_seq && temperature == 0.0f;
+  spc_verify_ex_args ex{};
+  ex.temp_per_seq = temp_per_seq;
+  ex.rules_present = 1u << SPC_RULE_NEVER;
+  return verify_impl(logits, logits, dtype, nullptr, uniforms, B, 0, V, SPC_RULE_NEVER, 0.0f,
+                     greedy ? 0.0f : (temp_per_seq ? 1.0f : temperature), greedy, nullptr,
+                     out_token, nullptr, temp_per_seq ? &ex : nullptr, stream, true);
 }
 
 size_t spc_workspace_bytes(int32_t B, int32_t gamma, int32_t V, spc_dtype dtype) {

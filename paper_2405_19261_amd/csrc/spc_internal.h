@@ -93,7 +93,7 @@ int samp_groups(int64_t nc, int B, int cus);
 // Workspace layout for a shape; offsets in bytes from the base.
 struct WsLayout {
   size_t samp_cnt, zero_end;
-  size_t tiles, tvpart, masses, moms, total;
+  size_t tiles, tvpart, masses, moms, draft_out, total;
 };
 WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec);
 

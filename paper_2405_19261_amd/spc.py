@@ -63,6 +63,9 @@ def lib():
                                              ctypes.c_float, _P, _P, _P,
                                              ctypes.POINTER(ExArgs), _P]
         L.spc_verify_ex.restype = ctypes.c_int
+        L.spc_draft_sample.argtypes = [_P, ctypes.c_int, _I32, _I32, ctypes.c_float, _P, _P, _P,
+                                       _P]
+        L.spc_draft_sample.restype = ctypes.c_int
         L.spc_workspace_bytes.argtypes = [_I32, _I32, _I32, ctypes.c_int]
         L.spc_workspace_bytes.restype = ctypes.c_size_t
         L.spc_workspace_zero_bytes.argtypes = [_I32, _I32, _I32, ctypes.c_int]
@@ -180,6 +183,21 @@ def spc_verify_ex(q, p, draft, uniforms, rule, alpha, temperature, rule_per_seq=
                                gamma, V, int(rule), float(alpha), float(temperature), _ptr(acc),
                                _ptr(tok), _ptr(dm), ctypes.byref(ex), _stream(stream)))
     return acc, tok, dm
+
+
+def spc_draft_sample(logits, temperature, uniforms=None, temp_per_seq=None, out=None,
+                     stream=None):
+    """The drafter's sampling step: one token per row of ``logits`` [B, V]
+    (float32 or bfloat16, contiguous) from softmax(z / T), T = 0 giving the
+    argmax.  Returns the tokens [B] int32 (``out`` if given)."""
+    if logits.dim() != 2 or not logits.is_contiguous():
+        raise ValueError("logits must be a contiguous [B, V] tensor")
+    B, V = logits.shape
+    tok = out if out is not None else torch.empty(B, dtype=torch.int32, device=logits.device)
+    _check(lib().spc_draft_sample(_ptr(logits), _dtype_code(logits), B, V, float(temperature),
+                                  _ptr(temp_per_seq), _ptr(uniforms), _ptr(tok),
+                                  _stream(stream)))
+    return tok
 
 
 def spc_workspace_bytes(B, gamma, V, dtype_code):

@@ -98,3 +98,25 @@ def test_ex_per_sequence_arrays_skip_scalar_checks():
     st = L.spc_verify_ex(FAKE_ODD, FAKE, 1, FAKE, FAKE, 4, 3, 1000, 99, float("nan"), 0.0,
                          FAKE, FAKE, FAKE, ctypes.byref(ex), None)
     assert st == -5
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(z=None), -1), (dict(tok=None), -1), (dict(u=None), -1),
+    (dict(B=0), -2), (dict(V=1), -2), (dict(B=40000), -2),
+    (dict(T=-0.5), -4), (dict(T=float("nan")), -4), (dict(T=float("inf")), -4),
+    (dict(dtype=3), -4), (dict(z=FAKE_ODD), -5),
+])
+def test_draft_sample_argument_errors(kw, status):
+    a = dict(z=FAKE, dtype=spc.SPC_BF16, B=4, V=1000, T=1.0, tps=None, u=FAKE, tok=FAKE)
+    a.update(kw)
+    st = spc.lib().spc_draft_sample(a["z"], a["dtype"], a["B"], a["V"], a["T"], a["tps"],
+                                    a["u"], a["tok"], None)
+    assert st == status
+    assert spc.spc_last_error() != ""
+
+
+def test_draft_sample_greedy_needs_no_uniforms():
+    """T = 0 takes no uniforms: the call gets past every argument check (here
+    it stops at the misaligned logits, before any HIP call)."""
+    st = spc.lib().spc_draft_sample(FAKE_ODD, spc.SPC_BF16, 4, 1000, 0.0, None, None, FAKE, None)
+    assert st == -5
