@@ -156,6 +156,65 @@ def cpu_baseline(wl, inp, gpu_out, min_seconds=10.0):
                 logit_gbps=n * wl.logit_bytes() / el / 1e9), dict(rep)
 
 
+def bench_draft(args, wl, dev):
+    """The drafter's sampling step on B rows of V logits (one position per
+    sequence), at the workload's temperature."""
+    import torch
+    from paper_2405_19261_amd import spc
+    from paper_2405_19261_amd import workloads as W
+    sets = [W.generate(wl, 2000 + i, dev)["q"][:, 0].contiguous() for i in range(max(args.sets, 8))]
+    u = torch.rand(wl.B, generator=torch.Generator(device=dev).manual_seed(1), device=dev)
+    out = torch.empty(wl.B, dtype=torch.int32, device=dev)
+    for i in range(args.warmup):
+        spc.spc_draft_sample(sets[i % len(sets)], wl.temperature, uniforms=u, out=out)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.steps):
+        spc.spc_draft_sample(sets[i % len(sets)], wl.temperature, uniforms=u, out=out)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / args.steps
+    nbytes = wl.B * wl.V * (2 if wl.dtype == "bf16" else 4)
+    print(json.dumps(dict(
+        metric="drafter sampling steps/s", value=1e6 / us, unit="steps/s", n_gpus=1,
+        steps=args.steps, warmup=args.warmup, us_per_step=us, higher_is_better=True,
+        dtype="f32", data="synthetic",
+        config=dict(workload=f"draft sampling: B={wl.B} rows of V={wl.V} {wl.dtype}, "
+                             f"T={wl.temperature}", input_sets=len(sets)),
+        roofline=dict(bound="hbm", achieved=nbytes / us / 1e3, peak=PEAK_HBM_GBPS, unit="GB/s",
+                      frac=nbytes / us / 1e3 / PEAK_HBM_GBPS, bytes_per_step=nbytes))), flush=True)
+    return 0
+
+
+def bench_decode(args, wl, dev):
+    """Rounds of the decoding loop (draft gamma tokens, score, verify, roll
+    back) on synthetic models of the workload's vocabulary; emitted tokens/s
+    over the whole loop, host bookkeeping included."""
+    import torch
+    from paper_2405_19261_amd import decode
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    q_lm, p_lm = decode.synthetic_pair(wl.V, seed=1, dtype=dt, device=dev)
+    first = torch.randint(0, wl.V, (wl.B,), generator=torch.Generator().manual_seed(0))
+    kw = dict(gamma=wl.gamma, rule=wl.rule, alpha=wl.alpha, temperature=wl.temperature)
+    decode.spec_decode(q_lm, p_lm, first, rounds=2, seed=5, **kw)  # warm-up
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    res = decode.spec_decode(q_lm, p_lm, first, rounds=args.decode, seed=6, **kw)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    n = sum(len(t) for t in res.tokens)
+    print(json.dumps(dict(
+        metric="emitted tokens/s (decoding loop, synthetic models)", value=n / el,
+        unit="tokens/s", n_gpus=1, rounds=args.decode, higher_is_better=True, dtype="f32",
+        data="synthetic", ms_per_round=el * 1e3 / args.decode,
+        tokens_per_round=res.tokens_per_round(),
+        config=dict(workload=f"decoding loop: B={wl.B} gamma={wl.gamma} V={wl.V} {wl.dtype}, "
+                             f"rule {wl.rule} alpha={wl.alpha:g} T={wl.temperature}; "
+                             "synthetic Markov drafter/verifier (table lookups)"))), flush=True)
+    return 0
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -174,6 +233,12 @@ def main():
                     help="workload (default 3, the Gemma-vocabulary step); 4 and 5 run "
                          "through spc_verify_ex with per-sequence arrays")
     ap.add_argument("--alpha", type=float, default=None)
+    ap.add_argument("--draft", action="store_true",
+                    help="time the drafter's sampling step (spc_draft_sample) on the "
+                         "workload's drafter rows [B, V] instead of the verify step")
+    ap.add_argument("--decode", type=int, default=0, metavar="ROUNDS",
+                    help="time ROUNDS rounds of the decoding loop (decode.py) on synthetic "
+                         "models of the workload's shape")
     args = ap.parse_args()
     if args.traffic_from:
         if args.copy_calib_mb <= 0:
@@ -205,6 +270,10 @@ def main():
     torch.cuda.set_device(dev)
     if args.copy_calib_mb > 0:
         copy_calibration(args.copy_calib_mb)
+    if args.draft:
+        return bench_draft(args, wl, dev)
+    if args.decode:
+        return bench_decode(args, wl, dev)
     sets = [W.generate(wl, 1000 + i, dev) for i in range(args.sets)]
     B, gamma, V = wl.B, wl.gamma, wl.V
     outs = [(torch.empty(B, dtype=torch.int32, device=dev),

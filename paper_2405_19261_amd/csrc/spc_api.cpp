@@ -68,14 +68,15 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
   WsLayout L;
   L.samp_cnt = 0;
   size_t o = align_up(4 * (size_t)(kMaxRows + 1), 256);
+  // the drafter kernel's per-row counters, one per 128-byte line
+  L.draft_cnt = o;
+  o = align_up(o + 4 * (size_t)kDraftCntStride * (kMaxRows / 2 + 1), 256);
   L.zero_end = o;
   L.tiles = o; o = align_up(o + sizeof(TilePart) * R * nt, 256);
   L.tvpart = o; o = align_up(o + sizeof(double) * R * nt, 256);
   const int64_t nc = (V + samp_chunk_elems(dtype, vec) - 1) / samp_chunk_elems(dtype, vec);
   L.masses = o; o = align_up(o + sizeof(double) * B * nc, 256);
   L.moms = o; o = align_up(o + sizeof(TileMom) * R * nt, 256);
-  // accepted lengths and masks of a drafter sampling step (not returned)
-  L.draft_out = o; o = align_up(o + 5 * (size_t)B, 256);
   L.total = o;
   return L;
 }
@@ -95,19 +96,53 @@ spc_status check_shape(int32_t B, int32_t gamma, int32_t V) {
   return SPC_OK;
 }
 
-// draft_mode: the drafter's sampling step, run as a gamma = 0 step of rule
-// NEVER on one logit tensor (q = p); its accepted lengths and masks go to
-// the workspace.
+// The internal workspace of the current device, grown to L.total if needed
+// (its counters zeroed on `stream` before any kernel that uses them).
+spc_status internal_workspace(const spc::WsLayout& L, hipStream_t stream, char** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SPC_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  DevWorkspace& w = g_ws[dev];
+  if (w.bytes < L.total) {
+    // growing: the old buffer may still be in use by work on `stream`
+    if (w.ptr) {
+      e = hipStreamSynchronize(stream);
+      if (e == hipSuccess) e = hipFree(w.ptr);
+      w.ptr = nullptr;
+      w.bytes = 0;
+      if (e != hipSuccess) return fail(SPC_E_HIP, "workspace release: %s", hipGetErrorString(e));
+    }
+    const size_t want = L.total + L.total / 4;  // headroom for nearby shapes
+    e = hipMalloc(&w.ptr, want);
+    if (e != hipSuccess) {
+      w.ptr = nullptr;
+      return fail(SPC_E_HIP, "hipMalloc(%zu): %s", want, hipGetErrorString(e));
+    }
+    // zero counters, ordered before this call's kernels on the same stream;
+    // the kernels leave them zero
+    e = hipMemsetAsync(w.ptr, 0, L.zero_end, stream);
+    if (e != hipSuccess) {
+      (void)hipFree(w.ptr);
+      w.ptr = nullptr;
+      return fail(SPC_E_HIP, "hipMemsetAsync: %s", hipGetErrorString(e));
+    }
+    w.bytes = want;
+  }
+  *out = static_cast<char*>(w.ptr);
+  return SPC_OK;
+}
+
 spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int32_t* draft,
                        const float* uniforms, int32_t B, int32_t gamma, int32_t V, int32_t rule,
                        float alpha, float temperature, bool force_greedy, int32_t* out_accept,
                        int32_t* out_token, uint8_t* out_defer, const spc_verify_ex_args* ex,
-                       hipStream_t stream, bool draft_mode = false) {
+                       hipStream_t stream) {
   g_err.clear();
-  if (!q || !p || (!draft_mode && (!draft || !out_accept || !out_defer)) || !out_token)
+  if (!q || !p || !draft || !out_accept || !out_token || !out_defer)
     return fail(SPC_E_NULL, "a required pointer is NULL");
   if (!force_greedy && !uniforms) return fail(SPC_E_NULL, "uniforms is NULL");
-  spc_status st = draft_mode ? check_shape(B, 1, V) : check_shape(B, gamma, V);
+  spc_status st = check_shape(B, gamma, V);
   if (st != SPC_OK) return st;
   if (dtype != SPC_F32 && dtype != SPC_BF16) return fail(SPC_E_PARAM, "unknown dtype %d", dtype);
   const bool per_rule = ex && ex->rule_per_seq;
@@ -121,7 +156,6 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   if (!force_greedy && !per_temp && !(isfinite(temperature) && temperature >= 1e-20f))
     return fail(SPC_E_PARAM, "temperature must be finite and >= 1e-20 (got %g)",
                 (double)temperature);
-  if (draft_mode) gamma = 0;
   if (((uintptr_t)q | (uintptr_t)p) % 16 != 0)
     return fail(SPC_E_ALIGN, "logit base pointers must be 16-byte aligned");
 
@@ -141,34 +175,8 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   if (ex && ex->workspace) {
     ws = static_cast<char*>(ex->workspace);
   } else {
-    std::lock_guard<std::mutex> lk(g_ws_mu);
-    DevWorkspace& w = g_ws[dev];
-    if (w.bytes < L.total) {
-      // growing: the old buffer may still be in use by work on `stream`
-      if (w.ptr) {
-        e = hipStreamSynchronize(stream);
-        if (e == hipSuccess) e = hipFree(w.ptr);
-        w.ptr = nullptr;
-        w.bytes = 0;
-        if (e != hipSuccess) return fail(SPC_E_HIP, "workspace release: %s", hipGetErrorString(e));
-      }
-      const size_t want = L.total + L.total / 4;  // headroom for nearby shapes
-      e = hipMalloc(&w.ptr, want);
-      if (e != hipSuccess) {
-        w.ptr = nullptr;
-        return fail(SPC_E_HIP, "hipMalloc(%zu): %s", want, hipGetErrorString(e));
-      }
-      // zero counters, ordered before this call's kernels on the same stream;
-      // the kernels leave them zero
-      e = hipMemsetAsync(w.ptr, 0, L.zero_end, stream);
-      if (e != hipSuccess) {
-        (void)hipFree(w.ptr);
-        w.ptr = nullptr;
-        return fail(SPC_E_HIP, "hipMemsetAsync: %s", hipGetErrorString(e));
-      }
-      w.bytes = want;
-    }
-    ws = static_cast<char*>(w.ptr);
+    const spc_status wst = internal_workspace(L, stream, &ws);
+    if (wst != SPC_OK) return wst;
   }
 
   spc::Params P{};
@@ -200,10 +208,6 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   P.tvpart = reinterpret_cast<double*>(ws + L.tvpart);
   P.masses = reinterpret_cast<double*>(ws + L.masses);
   P.moms = reinterpret_cast<spc::TileMom*>(ws + L.moms);
-  if (draft_mode) {
-    P.out_accept = reinterpret_cast<int32_t*>(ws + L.draft_out);
-    P.out_defer = reinterpret_cast<uint8_t*>(ws + L.draft_out + 4 * (size_t)B);
-  }
 
   // sequences at temperature > 0 may exist unless the whole batch is greedy;
   // OPT at temperature > 0 needs the TV pass
@@ -273,16 +277,44 @@ spc_status spc_draft_sample(const void* logits, spc_dtype dtype, int32_t B, int3
                             float temperature, const float* temp_per_seq,
                             const float* uniforms, int32_t* out_token, hipStream_t stream) {
   g_err.clear();
+  if (!logits || !out_token) return fail(SPC_E_NULL, "a required pointer is NULL");
   if (!temp_per_seq && !(isfinite(temperature) && temperature >= 0.0f))
     return fail(SPC_E_PARAM, "temperature must be finite and >= 0 (got %g)",
                 (double)temperature);
   const bool greedy = !temp_per_seq && temperature == 0.0f;
-  spc_verify_ex_args ex{};
-  ex.temp_per_seq = temp_per_seq;
-  ex.rules_present = 1u << SPC_RULE_NEVER;
-  return verify_impl(logits, logits, dtype, nullptr, uniforms, B, 0, V, SPC_RULE_NEVER, 0.0f,
-                     greedy ? 0.0f : (temp_per_seq ? 1.0f : temperature), greedy, nullptr,
-                     out_token, nullptr, temp_per_seq ? &ex : nullptr, stream, true);
+  if (!greedy && !uniforms) return fail(SPC_E_NULL, "uniforms is NULL");
+  if (B < 1 || V < 2 || (int64_t)B > kMaxRows / 2)
+    return fail(SPC_E_SHAPE, "bad shape B=%d V=%d (need 1<=B<=%lld, V>=2)", B, V,
+                (long long)(kMaxRows / 2));
+  if (dtype != SPC_F32 && dtype != SPC_BF16) return fail(SPC_E_PARAM, "unknown dtype %d", dtype);
+  if ((uintptr_t)logits % 16 != 0)
+    return fail(SPC_E_ALIGN, "logit base pointer must be 16-byte aligned");
+  const bool vec = vec_path(dtype, V);
+  const spc::WsLayout L = spc::ws_layout(B, 0, V, dtype, vec);
+  // argument checks end here: no HIP call precedes them
+  char* ws = nullptr;
+  const spc_status wst = internal_workspace(L, stream, &ws);
+  if (wst != SPC_OK) return wst;
+  spc::Params P{};
+  P.q = logits;
+  P.p = logits;
+  P.uniforms = uniforms;
+  P.B = B;
+  P.gamma = 0;
+  P.V = V;
+  // the drafter kernel's tiles are twice as long (fewer partials than the
+  // workspace holds for this shape)
+  P.nt = (int32_t)((V + spc::draft_tile_elems(dtype, vec) - 1) / spc::draft_tile_elems(dtype, vec));
+  P.rule = SPC_RULE_NEVER;
+  P.temp = greedy ? 0.0f : temperature;
+  P.force_greedy = greedy ? 1 : 0;
+  P.temp_ps = temp_per_seq;
+  P.out_token = out_token;
+  P.samp_cnt = reinterpret_cast<uint32_t*>(ws + L.draft_cnt);
+  P.tiles = reinterpret_cast<spc::TilePart*>(ws + L.tiles);
+  const hipError_t e = spc::launch_draft(P, dtype, vec, greedy || temp_per_seq, stream);
+  if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
+  return SPC_OK;
 }
 
 size_t spc_workspace_bytes(int32_t B, int32_t gamma, int32_t V, spc_dtype dtype) {

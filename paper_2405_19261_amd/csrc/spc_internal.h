@@ -87,15 +87,25 @@ struct Params {
 // path, and sampling workgroups per sequence for a row of nc chunks in a batch
 // of B sequences on a device of `cus` compute units.
 int stat_tile_elems(int dtype, bool vec);
+int draft_tile_elems(int dtype, bool vec);
 int samp_chunk_elems(int dtype, bool vec);
 int samp_groups(int64_t nc, int B, int cus);
 
 // Workspace layout for a shape; offsets in bytes from the base.
 struct WsLayout {
-  size_t samp_cnt, zero_end;
-  size_t tiles, tvpart, masses, moms, draft_out, total;
+  size_t samp_cnt, draft_cnt, zero_end;
+  size_t tiles, tvpart, masses, moms, total;
 };
 WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec);
+
+// Words between the drafter kernel's per-row completion counters (one
+// counter per 128-byte line: arrivals on a shared line serialise).
+constexpr int kDraftCntStride = 32;
+
+// Enqueue the drafter sampling kernel (Params: q = the logits [B][V], nt,
+// uniforms [B], temp_ps or temp, out_token, samp_cnt with kDraftCntStride,
+// tiles).  argmax: some row may be at temperature 0.
+hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, hipStream_t stream);
 
 // Enqueue the kernels of one verify call.  need_tv: the batch may hold OPT,
 // OPTLOG or token-rule sequences at temperature > 0; need_sample: it may hold

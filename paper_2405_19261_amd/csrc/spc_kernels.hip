@@ -62,6 +62,11 @@ struct Tile {
 template <int DT, bool VEC>
 using StatTile = Tile<DT, VEC, VEC ? 4 : 8>;
 
+// drafter tiles: one tensor, so twice the lane loads of a statistics tile
+// (the same bytes per workgroup)
+template <int DT, bool VEC>
+using DraftTile = Tile<DT, VEC, 2 * StatTile<DT, VEC>::U>;
+
 // bfloat16 -> float32 is exact: the bf16 bits are the top half of the float.
 template <int DT, bool VEC>
 __device__ __forceinline__ float elem(const uint32_t* w, int e) {
@@ -179,6 +184,28 @@ __device__ __forceinline__ double ld_dev_f64(const double* src) {
       __HIP_MEMORY_SCOPE_AGENT));
 }
 
+// A tile partial written and read within one launch: five 64-bit words with
+// agent-scope atomics.
+static_assert(sizeof(TilePart) == 40, "TilePart is five 64-bit words");
+__device__ __forceinline__ void st_tile(TilePart* dst, const TilePart& t) {
+  uint64_t w[5];
+  __builtin_memcpy(w, &t, sizeof w);
+#pragma unroll
+  for (int i = 0; i < 5; ++i)
+    __hip_atomic_store(reinterpret_cast<uint64_t*>(dst) + i, w[i], __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ TilePart ld_tile(const TilePart* src) {
+  uint64_t w[5];
+#pragma unroll
+  for (int i = 0; i < 5; ++i)
+    w[i] = __hip_atomic_load(reinterpret_cast<uint64_t*>(const_cast<TilePart*>(src)) + i,
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  TilePart t;
+  __builtin_memcpy(&t, w, sizeof w);
+  return t;
+}
+
 // Every vector-memory operation issued so far by this wave has completed.
 __device__ __forceinline__ void vmem_drain() {
   __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));  // vmcnt(0)
@@ -261,7 +288,7 @@ struct SharedT {
   static constexpr int kNW = NWV;
   float m[NWV][2];
   double d[NWV][2];
-  double dv[NWV];
+  double dv[64];  // per sub-chunk sums of a tile draw
   double h[NWV][3];
   int i[NWV][2];
   int flag;
@@ -883,8 +910,12 @@ struct Chunk {
   static constexpr int NW = Tile<DT, VEC, U_>::NW, VW = Tile<DT, VEC, U_>::VW;
   static constexpr int N = 64 * U * VW;  // entries per chunk
 };
-template <int DT, bool VEC>
-using SubChunk = Chunk<DT, VEC, StatTile<DT, VEC>::U * kThreads / (64 * kSampWaves)>;
+// A sub-chunk of a TN-entry tile drawn from by NWV wavefronts: one per
+// wavefront, or several of at most 4 lane loads each.
+template <int DT, bool VEC, int NWV, int TN = StatTile<DT, VEC>::N>
+using SubChunk = Chunk<DT, VEC, (TN / (64 * NWV * Tile<DT, VEC, 1>::VW) < 4)
+                                    ? TN / (64 * NWV * Tile<DT, VEC, 1>::VW)
+                                    : 4>;
 template <int DT, bool VEC>
 using SampChunk = Chunk<DT, VEC, VEC ? 2 : 8>;
 
@@ -909,7 +940,8 @@ __device__ __forceinline__ void load_chunk(const char* row, int64_t c0, int V, C
 // partials per tile (the residual of an OPT row, which the second pass
 // summed), the statistics and eta partials together (a token rule's target),
 // or the residual masses per SampChunk computed by the sampling pass.
-enum MassSrc : int { kSrcStatsQ = 0, kSrcStatsP = 1, kSrcTv = 2, kSrcPass = 3, kSrcTokPi = 4 };
+enum MassSrc : int { kSrcStatsQ = 0, kSrcStatsP = 1, kSrcTv = 2, kSrcPass = 3, kSrcTokPi = 4,
+                     kSrcDraft = 5 };
 
 template <int SRC>
 __device__ __forceinline__ double part_mass(const Params& P, int64_t row, int b, int k,
@@ -929,6 +961,10 @@ __device__ __forceinline__ double part_mass(const Params& P, int64_t row, int b,
     const double qm = t.s_q * exp2_acc((double)t.r_q - rs.lz_q);
     const double pm = t.s_p * exp2_acc((double)t.r_p - rs.lz_p);
     return fmax(qm - P.tvpart[row * P.nt + k], 0.0) + rs.tv * pm;
+  } else if constexpr (SRC == kSrcDraft) {
+    // the q statistics partials of the drafter kernel's own launch
+    const TilePart t = ld_tile(P.tiles + row * P.nt + k);
+    return t.s_q * exp2_acc((double)t.r_q - rs.lz_q);
   } else {
     return ld_dev_f64(P.masses + (int64_t)b * P.nc + k);
   }
@@ -1117,33 +1153,37 @@ __device__ __forceinline__ void pick_wave(const Params& P, int b, int64_t row, i
 // Whole block: the draw inside statistics tile t0 (entry offset).  Each
 // wavefront sums the weights of one SubChunk; wave 0 scans the kSampWaves
 // sums for the sub-chunk where rem is crossed and draws inside it.
-template <int DT, bool VEC, int KIND>
+template <int DT, bool VEC, int KIND, int NWV, int TN = StatTile<DT, VEC>::N>
 __device__ __forceinline__ void pick_tile(const Params& P, int b, int64_t row, int64_t t0,
-                                          double rem, const ProbScale& ps, SampShared& sh) {
-  using C = SubChunk<DT, VEC>;
-  static_assert(kSampWaves * C::N == StatTile<DT, VEC>::N, "a tile is kSampWaves sub-chunks");
+                                          double rem, const ProbScale& ps, SharedT<NWV>& sh) {
+  using C = SubChunk<DT, VEC, NWV, TN>;
+  constexpr int NS = TN / C::N;  // sub-chunks of the tile
+  static_assert(NS * C::N == TN && NS % NWV == 0 && NS <= 64,
+                "a tile is a whole number of sub-chunks per wavefront");
   constexpr int EB = StatTile<DT, VEC>::EB;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int V = P.V;
   const char* qrow = (const char*)P.q + row * V * EB;
   const char* prow = (const char*)P.p + row * V * EB;
-  ChunkRegs<C> cq = {}, cp = {};
-  if (KIND != kP) load_chunk<DT, VEC, C>(qrow, t0 + wv * C::N, V, cq);
-  if (KIND != kQ) load_chunk<DT, VEC, C>(prow, t0 + wv * C::N, V, cp);
-  double m = 0.0;
+  for (int sc = wv; sc < NS; sc += NWV) {  // wave wv sums sub-chunks wv, wv + NWV, ...
+    ChunkRegs<C> cq = {}, cp = {};
+    if (KIND != kP) load_chunk<DT, VEC, C>(qrow, t0 + sc * C::N, V, cq);
+    if (KIND != kQ) load_chunk<DT, VEC, C>(prow, t0 + sc * C::N, V, cp);
+    double m = 0.0;
 #pragma unroll
-  for (int i = 0; i < C::U; ++i) {
-    float t = 0.0f;
+    for (int i = 0; i < C::U; ++i) {
+      float t = 0.0f;
 #pragma unroll
-    for (int e = 0; e < C::VW; ++e)
-      t += weight_of<KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
-    m += (double)t;
+      for (int e = 0; e < C::VW; ++e)
+        t += weight_of<KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
+      m += (double)t;
+    }
+    m = wave_sum(m);
+    if (lane == 0) sh.dv[sc] = m;
   }
-  m = wave_sum(m);
-  if (lane == 0) sh.dv[wv] = m;
   __syncthreads();
   if (wv != 0) return;
-  const double ml = lane < kSampWaves ? sh.dv[lane] : 0.0;
+  const double ml = lane < NS ? sh.dv[lane] : 0.0;
   const double incl = wave_incl_scan(ml);
   const unsigned long long hit = __ballot(ml > 0.0 && incl > rem);
   const unsigned long long pos = __ballot(ml > 0.0);
@@ -1201,13 +1241,13 @@ __device__ __forceinline__ void draw(const Params& P, int b, int64_t row, int ki
         pick_wave<DT, VEC, SC, kResidual>(P, b, row, (int64_t)pk.k * SC::N, pk.rem, ps);
     }
   } else if (pk.kind == kQ) {
-    pick_tile<DT, VEC, kQ>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
+    pick_tile<DT, VEC, kQ, kSampWaves>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
   } else if (pk.kind == kP) {
-    pick_tile<DT, VEC, kP>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
+    pick_tile<DT, VEC, kP, kSampWaves>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
   } else if (pk.kind == kTokPi) {
-    pick_tile<DT, VEC, kTokPi>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
+    pick_tile<DT, VEC, kTokPi, kSampWaves>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
   } else {
-    pick_tile<DT, VEC, kResidual>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
+    pick_tile<DT, VEC, kResidual, kSampWaves>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
   }
 }
 
@@ -1517,6 +1557,147 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
   draw<DT, VEC>(P, b, row, s.kind, kSrcPass, s.u, sp, rs, ss, sh);
 }
 
+// Drafter sampling step (Alg. 4: x_{t+j} ~ q_{t+j}), one launch.  grid
+// (nt, B): statistics tile k of row b of the drafter's logits, as in k_stats
+// for one tensor.  The last tile of a row to finish (a per-row counter on a
+// line of its own) merges the row's partials and draws the token: the tile
+// masses give the tile where u W falls, then the tile's sub-chunks and
+// lanes are scanned in vocabulary order.  A greedy row (temperature 0)
+// takes the lowest index attaining its max instead.
+template <int DT, bool VEC, bool ARGMAX>
+__global__ __launch_bounds__(kThreads) void k_draft(Params P) {
+  using T = DraftTile<DT, VEC>;
+  __shared__ Shared sh;
+  __shared__ RowStat srow;
+  __shared__ PickState pks;
+  const int k = blockIdx.x, b = blockIdx.y;
+  const SeqParam sp = seq_param(P, b);
+  const int V = P.V;
+  const char* row = (const char*)P.q + (int64_t)b * V * T::EB;
+  const int64_t t0 = (int64_t)k * T::N;
+  uint32_t w[T::U][T::NW];
+  load_tile<DT, VEC, T::U, true>(row, t0, V, w, threadIdx.x);
+  float m = kNegInf;
+  int im = 0x7fffffff;
+  const int base = (int)t0 + (int)threadIdx.x * T::VW;
+#pragma unroll
+  for (int i = 0; i < T::U; ++i)
+#pragma unroll
+    for (int e = 0; e < T::VW; ++e) {
+      const float v = elem<DT, VEC>(w[i], e);
+      if constexpr (ARGMAX) {
+        if (v > m) im = base + i * kThreads * T::VW + e;
+      }
+      m = fmaxf(m, v);
+    }
+  const float r = (m == kNegInf) ? 0.0f : m * sp.c_hi;
+  float s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < T::U; ++i) {
+    float t[T::VW];
+#pragma unroll
+    for (int e = 0; e < T::VW; ++e) {
+      const float z = elem<DT, VEC>(w[i], e);
+      t[e] = exp2_hw(fmaf(z, sp.c_lo, fmaf(z, sp.c_hi, -r)));
+    }
+#pragma unroll
+    for (int h = 1; h < T::VW; h <<= 1)
+#pragma unroll
+      for (int e = 0; e + h < T::VW; e += 2 * h) t[e] += t[e + h];
+    s += t[0];
+  }
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const float Wm = wave_max(m);
+  double d = (m == kNegInf)
+                 ? 0.0
+                 : (double)s * (double)exp2_hw((float)((double)r - (double)(Wm * sp.c_hi)));
+  d = wave_sum(d);
+  if constexpr (ARGMAX) im = wave_min((m == Wm) ? im : 0x7fffffff);
+  if (lane == 0) {
+    sh.m[wv][0] = Wm;
+    sh.d[wv][0] = d;
+    sh.i[wv][0] = im;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float M = sh.m[0][0];
+#pragma unroll
+    for (int x = 1; x < kWaves; ++x) M = fmaxf(M, sh.m[x][0]);
+    const float R = M * sp.c_hi;
+    double tot = 0.0;
+    int am = 0x7fffffff;
+#pragma unroll
+    for (int x = 0; x < kWaves; ++x) {
+      const float wm = sh.m[x][0];
+      if (wm != kNegInf)
+        tot += sh.d[x][0] * (double)exp2_hw((float)((double)(wm * sp.c_hi) - (double)R));
+      if (ARGMAX && wm == M) am = min(am, sh.i[x][0]);
+    }
+    TilePart t{tot, 0.0, (M == kNegInf) ? kNegInf : R, kNegInf, M, kNegInf,
+               ARGMAX ? am : -1, -1};
+    st_tile(P.tiles + (int64_t)b * P.nt + k, t);
+  }
+  if (!arrive_last(P.samp_cnt + (int64_t)b * kDraftCntStride, (uint32_t)P.nt, sh)) return;
+  // the last tile of row b: merge the row (wave 0, a tile per lane)
+  if (threadIdx.x < 64) {
+    TilePart h{0.0, 0.0, kNegInf, kNegInf, kNegInf, kNegInf, 0x7fffffff, 0x7fffffff};
+    float zq = kNegInf, rq = kNegInf;
+    for (int kk = lane; kk < P.nt; kk += 64) {
+      const TilePart tk = ld_tile(P.tiles + (int64_t)b * P.nt + kk);
+      zq = fmaxf(zq, tk.zmax_q);
+      rq = fmaxf(rq, tk.r_q);
+    }
+    zq = wave_max(zq);
+    rq = wave_max(rq);
+    double sq = 0.0;
+    int aq = 0x7fffffff;
+    for (int kk = lane; kk < P.nt; kk += 64) {
+      h = ld_tile(P.tiles + (int64_t)b * P.nt + kk);
+      sq += h.s_q * exp2_acc((double)h.r_q - (double)rq);
+      if (ARGMAX && h.zmax_q == zq) aq = min(aq, h.amax_q);
+    }
+    sq = wave_sum(sq);
+    if constexpr (ARGMAX) aq = wave_min(aq);
+    if (threadIdx.x == 0) {
+      RowStat rs{};
+      rs.lz_q = (double)rq + log2_acc(sq);
+      rs.zmax_q = zq;
+      rs.amax_q = ARGMAX ? aq : -1;
+      srow = rs;
+    }
+  }
+  __syncthreads();
+  const RowStat rs = srow;
+  if (!sp.valid || sp.greedy) {  // block-uniform
+    if (threadIdx.x == 0) P.out_token[b] = sp.valid ? rs.amax_q : -1;
+    return;
+  }
+  if (threadIdx.x < 64) {
+    int ks;
+    double rem;
+    find_part<kSrcDraft>(P, b, b, P.nt, rs, P.uniforms[b], &ks, &rem);
+    if (threadIdx.x == 0) {
+      pks = PickState{ks, kQ, kSrcDraft, rem};
+      if (ks < 0) P.out_token[b] = -1;
+    }
+  }
+  __syncthreads();
+  const PickState pk = pks;
+  if (pk.k < 0) return;  // block-uniform
+  pick_tile<DT, VEC, kQ, kWaves, T::N>(P, b, b, (int64_t)pk.k * T::N, pk.rem, prob_scale(sp, rs),
+                                       sh);
+}
+
+template <int DT, bool VEC>
+hipError_t launch_draft_t(const Params& P, bool argmax, hipStream_t st) {
+  const dim3 grid(P.nt, P.B);
+  if (argmax)
+    hipLaunchKernelGGL((k_draft<DT, VEC, true>), grid, dim3(kThreads), 0, st, P);
+  else
+    hipLaunchKernelGGL((k_draft<DT, VEC, false>), grid, dim3(kThreads), 0, st, P);
+  return hipGetLastError();
+}
+
 template <int DT, bool VEC>
 hipError_t launch_t(const Params& P, bool need_tv, bool need_sample, bool need_argmax,
                     bool need_plain, bool need_mom, hipEvent_t e0, hipEvent_t e1,
@@ -1557,6 +1738,11 @@ int stat_tile_elems(int dtype, bool vec) {
   return vec ? StatTile<0, true>::N : StatTile<0, false>::N;
 }
 
+int draft_tile_elems(int dtype, bool vec) {
+  if (dtype == 1) return vec ? DraftTile<1, true>::N : DraftTile<1, false>::N;
+  return vec ? DraftTile<0, true>::N : DraftTile<0, false>::N;
+}
+
 int samp_chunk_elems(int dtype, bool vec) {
   if (dtype == 1) return vec ? SampChunk<1, true>::N : SampChunk<1, false>::N;
   return vec ? SampChunk<0, true>::N : SampChunk<0, false>::N;
@@ -1570,6 +1756,12 @@ int samp_groups(int64_t nc, int B, int cus) {
   const int64_t by_cus = (cus + B - 1) / B;
   const int64_t k = by_chunks < by_cus ? by_chunks : by_cus;
   return (int)(k < 1 ? 1 : k);
+}
+
+hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, hipStream_t st) {
+  if (dtype == 1)
+    return vec ? launch_draft_t<1, true>(P, argmax, st) : launch_draft_t<1, false>(P, argmax, st);
+  return vec ? launch_draft_t<0, true>(P, argmax, st) : launch_draft_t<0, false>(P, argmax, st);
 }
 
 hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
