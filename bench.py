@@ -149,11 +149,33 @@ def cpu_baseline(wl, inp, gpu_out, min_seconds=10.0):
         if el >= min_seconds:
             break
     rep = parity.compare(gpu_out, o, h, wl.dtype)
+    cores = oracle.num_threads()
+    # the same step on one thread (the oracle's results do not depend on the
+    # thread count), for a per-core figure
+    oracle.set_num_threads(1)
+    try:
+        t1 = time.perf_counter()
+        parity.run_oracle(h)
+        el1 = time.perf_counter() - t1
+    finally:
+        oracle.set_num_threads(cores)
     return dict(value=n * wl.B * wl.gamma / el, unit="positions/s",
-                cores=oracle.num_threads(), kind="oracle",
+                cores=cores, kind="oracle",
                 sample=f"{n} whole step(s) of the timed workload (B={wl.B}, gamma={wl.gamma}, "
-                       f"V={wl.V} bf16), fp64, OpenMP over sequences, {el:.1f} s",
-                logit_gbps=n * wl.logit_bytes() / el / 1e9), dict(rep)
+                       f"V={wl.V} bf16), fp64, OpenMP over sequences, {el:.1f} s; "
+                       f"one_thread: 1 step, {el1:.1f} s",
+                logit_gbps=n * wl.logit_bytes() / el / 1e9,
+                one_thread_value=wl.B * wl.gamma / el1, cpu_model=cpu_model()), dict(rep)
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def bench_draft(args, wl, dev):

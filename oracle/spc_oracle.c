@@ -260,6 +260,14 @@ int orc_num_threads(void) {
 #endif
 }
 
+void orc_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 static int rule_ok(int r, float alpha) {
   if (r == ORC_LOSSY) return alpha < 1.0f;
   return r >= ORC_CHOW && r <= ORC_OPTLOG;

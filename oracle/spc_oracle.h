@@ -178,6 +178,8 @@ int orc_draft_sample(const void* logits, int dtype, int32_t B, int64_t V,
 
 /* Number of OpenMP threads orc_verify uses. */
 int orc_num_threads(void);
+/* Sets that number (n > 0); timing only, the results do not depend on it. */
+void orc_set_num_threads(int n);
 
 #ifdef __cplusplus
 }
