@@ -39,6 +39,13 @@
  *   buffer per device: calls that use it must not overlap in time on one
  *   device (issue them on one stream).  Calls with distinct caller
  *   workspaces may run concurrently.
+ * - Environment: SPC_ONE_READ=1 (read on every call) makes the verify calls
+ *   compute the second pass of OPT and token-rule rows (D_TV, eta) inside the
+ *   statistics launch, over tiles still held in registers, instead of reading
+ *   those rows again: one cooperative launch whose workgroups wait per row
+ *   for the row's other tiles.  It applies to batches without log-loss rules
+ *   or BiLD* of at most 8192 rows; the outputs are bitwise the same.  It is
+ *   off by default because it is slower on MI355X.
  */
 #ifndef SPECCASCADE_H
 #define SPECCASCADE_H

@@ -1,9 +1,11 @@
 // spc_api.cpp -- the C interface of libspeccascade (declared in
 // include/speccascade.h): argument checks, workspace, kernel dispatch.
 #include <math.h>
+#include <stdlib.h>
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <algorithm>
 #include <map>
 #include <mutex>
 #include <string>
@@ -50,6 +52,14 @@ int cu_count(int dev) {
 // Rows (gridDim.y of the statistics kernels) are capped by the launch limit.
 constexpr int64_t kMaxRows = 65535;
 
+// SPC_ONE_READ=1 in the environment selects the one-read statistics kernel
+// for batches it can take (read on every call).  It is off by default: on
+// MI355X it is slower than reading the second-pass rows again.
+bool one_read_requested() {
+  const char* v = getenv("SPC_ONE_READ");
+  return v && v[0] && v[0] != '0';
+}
+
 bool vec_path(int dtype, int64_t V) {
   const int64_t eb = dtype == SPC_BF16 ? 2 : 4;
   return (V * eb) % 16 == 0;  // every row starts on a 16-byte boundary
@@ -71,6 +81,9 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
   // the drafter kernel's per-row counters, one per 128-byte line
   L.draft_cnt = o;
   o = align_up(o + 4 * (size_t)kDraftCntStride * (kMaxRows / 2 + 1), 256);
+  // the one-read statistics kernel's per-row counters, one per 128-byte line
+  L.row_cnt = o;
+  o = align_up(o + 4 * (size_t)kRowCntStride * kResRows, 256);
   L.zero_end = o;
   L.tiles = o; o = align_up(o + sizeof(TilePart) * R * nt, 256);
   L.tvpart = o; o = align_up(o + sizeof(double) * R * nt, 256);
@@ -204,6 +217,7 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   P.out_argmax = ex ? ex->out_argmax : nullptr;
   P.out_norm = ex ? ex->out_sample_norm : nullptr;
   P.samp_cnt = reinterpret_cast<uint32_t*>(ws + L.samp_cnt);
+  P.row_cnt = reinterpret_cast<uint32_t*>(ws + L.row_cnt);
   P.tiles = reinterpret_cast<spc::TilePart*>(ws + L.tiles);
   P.tvpart = reinterpret_cast<double*>(ws + L.tvpart);
   P.masses = reinterpret_cast<double*>(ws + L.masses);
@@ -232,9 +246,19 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   const bool need_mom = (rules & kLog) && !(rules == (1u << SPC_RULE_BILD) && force_greedy);
   const bool need_plain = (rules & ~kLog) || per_temp || bild_t0;
   P.mom_split = (need_mom && need_plain) ? 1 : 0;
+  // The second pass reads its rows again, unless the one-read kernel is
+  // requested and fits: a resident grid holding at least one whole row of
+  // tiles per round.
+  int res_grid = 0;
+  const int64_t R = (int64_t)B * (gamma + 1);
+  if (need_tv && !need_mom && R <= spc::kResRows && one_read_requested()) {
+    const int nb = spc::res_blocks_per_cu(dtype, vec, need_argmax);
+    const int64_t rows_per_round = (int64_t)nb * cus / P.nt;
+    if (rows_per_round >= 1) res_grid = (int)(std::min<int64_t>(rows_per_round, R) * P.nt);
+  }
   e = spc::launch_verify(P, dtype, vec, need_tv, need_sample, need_argmax, need_plain, need_mom,
-                         ex ? ex->ev_hot_begin : nullptr, ex ? ex->ev_hot_end : nullptr,
-                         stream);
+                         res_grid, ex ? ex->ev_hot_begin : nullptr,
+                         ex ? ex->ev_hot_end : nullptr, stream);
   if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
   return SPC_OK;
 }

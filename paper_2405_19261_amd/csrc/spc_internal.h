@@ -77,6 +77,7 @@ struct Params {
   float* out_norm;
   // workspace
   uint32_t* samp_cnt;     // [B]   sampling workgroups of a sequence done
+  uint32_t* row_cnt;      // [R][kRowCntStride] arrivals / departures per row (one read)
   TilePart* tiles;        // [R][nt] statistics partials
   double* tvpart;         // [R][nt] TV partials (OPT) or eta partials (token rules)
   double* masses;         // [B][nc] residual chunk masses of row j*
@@ -93,7 +94,7 @@ int samp_groups(int64_t nc, int B, int cus);
 
 // Workspace layout for a shape; offsets in bytes from the base.
 struct WsLayout {
-  size_t samp_cnt, draft_cnt, zero_end;
+  size_t samp_cnt, draft_cnt, row_cnt, zero_end;
   size_t tiles, tvpart, masses, moms, total;
 };
 WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec);
@@ -101,6 +102,15 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec);
 // Words between the drafter kernel's per-row completion counters (one
 // counter per 128-byte line: arrivals on a shared line serialise).
 constexpr int kDraftCntStride = 32;
+
+// The one-read statistics kernel's per-row counters (arrivals, departures),
+// one 128-byte line per row, for batches of at most kResRows rows.
+constexpr int kRowCntStride = 32;
+constexpr int64_t kResRows = 8192;
+
+// Workgroups of the one-read statistics kernel resident per compute unit
+// (0 if it cannot run).
+int res_blocks_per_cu(int dtype, bool vec, bool argmax);
 
 // Enqueue the drafter sampling kernel (Params: q = the logits [B][V], nt,
 // uniforms [B], temp_ps or temp, out_token, samp_cnt with kDraftCntStride,
@@ -112,9 +122,12 @@ hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, hipSt
 // sequences at temperature > 0; need_argmax: it may hold greedy (temperature
 // 0) sequences; need_plain / need_mom: it may hold rows that need no first
 // moments / rows that do (log-loss rules, BiLD* at temperature > 0), each
-// kind handled by its own statistics kernel.  Returns the first launch error.
+// kind handled by its own statistics kernel.  res_grid > 0 (a multiple of
+// nt; only with need_tv and without need_mom): statistics and second pass in
+// one cooperative launch of res_grid workgroups instead of two kernels.
+// Returns the first launch error.
 hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
-                         bool need_argmax, bool need_plain, bool need_mom, hipEvent_t ev_begin,
-                         hipEvent_t ev_end, hipStream_t stream);
+                         bool need_argmax, bool need_plain, bool need_mom, int res_grid,
+                         hipEvent_t ev_begin, hipEvent_t ev_end, hipStream_t stream);
 
 }  // namespace spc

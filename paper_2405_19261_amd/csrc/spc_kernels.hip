@@ -584,12 +584,21 @@ struct PartHead {
   TileMom m;
 };
 
+// Tile partial k of row r; with DEV written earlier in the same launch (read
+// with agent-scope loads).
+template <bool DEV>
+__device__ __forceinline__ TilePart part_at(const Params& P, int r, int k) {
+  if constexpr (DEV) return ld_tile(P.tiles + (int64_t)r * P.nt + k);
+  else return P.tiles[(int64_t)r * P.nt + k];
+}
+
+template <bool DEV = false>
 __device__ __forceinline__ PartHead load_head(const Params& P, int r, bool tv, bool mom) {
   const int lane = threadIdx.x & 63;
   PartHead h{{0.0, 0.0, kNegInf, kNegInf, kNegInf, kNegInf, 0x7fffffff, 0x7fffffff}, 0.0,
              {0.0, 0.0, 0.0}};
   if (lane < P.nt) {
-    h.t = P.tiles[(int64_t)r * P.nt + lane];
+    h.t = part_at<DEV>(P, r, lane);
     if (tv) h.tv = P.tvpart[(int64_t)r * P.nt + lane];
     if (mom) h.m = P.moms[(int64_t)r * P.nt + lane];
   }
@@ -614,20 +623,21 @@ __device__ __forceinline__ double log_stat(int rule, double lq2, double lp2, dou
 //   H(q) = ln 2 (log2 S_q - H_q / S_q),  H(p) = ln 2 (log2 S_p - H_p / S_p),
 //   D(q, p) = -sum q log p = ln 2 (log2 S_p - X / S_q),
 // each a sum of two non-negative terms.  Every lane returns the same RowStat.
+template <bool DEV = false>
 __device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy, bool tv,
                                              int mrule, const PartHead& h) {
   const int lane = threadIdx.x & 63;
   const int nt = P.nt;
-  const TilePart* t = P.tiles + (int64_t)r * nt;
   const double* tvp = P.tvpart + (int64_t)r * nt;
   const TilePart& t0 = h.t;
   double tvs = h.tv;
   float zq = t0.zmax_q, zp = t0.zmax_p, rq = t0.r_q, rp = t0.r_p;
   for (int k = lane + 64; k < nt; k += 64) {
-    zq = fmaxf(zq, t[k].zmax_q);
-    zp = fmaxf(zp, t[k].zmax_p);
-    rq = fmaxf(rq, t[k].r_q);
-    rp = fmaxf(rp, t[k].r_p);
+    const TilePart tk = part_at<DEV>(P, r, k);
+    zq = fmaxf(zq, tk.zmax_q);
+    zp = fmaxf(zp, tk.zmax_p);
+    rq = fmaxf(rq, tk.r_q);
+    rp = fmaxf(rp, tk.r_p);
   }
   zq = wave_max(zq);
   zp = wave_max(zp);
@@ -653,7 +663,7 @@ __device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy
   };
   add(t0, h.m);
   for (int k = lane + 64; k < nt; k += 64) {
-    add(t[k], mrule ? P.moms[(int64_t)r * nt + k] : TileMom{0.0, 0.0, 0.0});
+    add(part_at<DEV>(P, r, k), mrule ? P.moms[(int64_t)r * nt + k] : TileMom{0.0, 0.0, 0.0});
     if (tv) tvs += tvp[k];
   }
   sq = wave_sum(sq);
@@ -780,7 +790,12 @@ __device__ __forceinline__ void finish_seq(const Params& P, int b, const SeqPara
   const int gamma = P.gamma, g1 = gamma + 1;
   const bool on = lane < g1;
   const int64_t row = (int64_t)b * g1 + lane;
-  if (!sp.valid) {
+  RowDecision d{};
+  if (on && sp.valid) d = ss.rows[lane];
+  // a NaN second-pass statistic marks a row whose one-read pass gave up
+  // waiting for its tiles: the sequence is reported invalid
+  const bool lost = needs_pass2(sp) && __ballot(on && d.tv != d.tv) != 0;
+  if (!sp.valid || lost) {
     if (write) {
       if (on) P.out_defer[row] = 0;
       if (lane == 0) {
@@ -792,8 +807,6 @@ __device__ __forceinline__ void finish_seq(const Params& P, int b, const SeqPara
     if (lane == 0) ss.seq = SeqState{-1, kNone, 0.0f, 0};
     return;
   }
-  RowDecision d{};
-  if (on) d = ss.rows[lane];
   if (write && on) {
     P.out_defer[row] = (uint8_t)d.delta;
     if (P.out_stats) {
@@ -1312,22 +1325,16 @@ __device__ __forceinline__ void tile_sums(const uint32_t (&wq)[StatTile<DT, VEC>
   }
 }
 
-template <int DT, bool VEC, bool ARGMAX, bool MOM>
-__device__ __forceinline__ void stats_tile(const Params& P) {
+// The partial of statistics tile k of row r from its loaded entries (wq, wp),
+// written by thread 0: with DEV through agent-scope stores, for readers in
+// the same launch.
+template <int DT, bool VEC, bool ARGMAX, bool MOM, bool DEV>
+__device__ __forceinline__ void tile_partial(const Params& P, int r, int k, const SeqParam& sp,
+                                             const uint32_t (&wq)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
+                                             const uint32_t (&wp)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
+                                             Shared& sh) {
   using T = StatTile<DT, VEC>;
-  __shared__ Shared sh;
-  const int k = blockIdx.x, r = blockIdx.y;
-  const SeqParam sp = seq_param(P, r / (P.gamma + 1));
-  // rows that need first moments belong to the moment kernel (block-uniform)
-  if (MOM ? !needs_mom(sp) : (P.mom_split && needs_mom(sp))) return;
-  const int V = P.V;
-  const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
-  const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
   const int64_t t0 = (int64_t)k * T::N;
-  uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
-  load_tile<DT, VEC, T::U, true>(qrow, t0, V, wq, threadIdx.x);
-  load_tile<DT, VEC, T::U, true>(prow, t0, V, wp, threadIdx.x);
-
   // Thread max; with ARGMAX also the lowest entry attaining it: entries are
   // visited in increasing index order and only a strictly larger value moves
   // the index (indices fit 32 bits: V < 2^31).
@@ -1349,6 +1356,15 @@ __device__ __forceinline__ void stats_tile(const Params& P) {
     }
   const float rq = (mq == kNegInf) ? 0.0f : mq * sp.c_hi;
   const float rp = (mp == kNegInf) ? 0.0f : mp * sp.c_hi;
+  if constexpr (DEV) {
+    // the packed words outlive this tile's statistics (the one-read second
+    // pass uses them): unpack again below rather than hold all the entries
+#pragma unroll
+    for (int i = 0; i < T::U; ++i)
+#pragma unroll
+      for (int j = 0; j < T::NW; ++j)
+        asm volatile("" : "+v"(const_cast<uint32_t&>(wq[i][j])), "+v"(const_cast<uint32_t&>(wp[i][j])));
+  }
   float sq = 0.0f, spp = 0.0f, hq = 0.0f, hp = 0.0f, xq = 0.0f;
   constexpr bool mom = MOM;
   tile_sums<DT, VEC, MOM>(wq, wp, sp, rq, rp, sq, spp, hq, hp, xq);
@@ -1433,7 +1449,10 @@ __device__ __forceinline__ void stats_tile(const Params& P) {
     t.zmax_p = Mp;
     t.amax_q = ARGMAX ? aq : -1;
     t.amax_p = ARGMAX ? ap : -1;
-    P.tiles[(int64_t)r * P.nt + k] = t;
+    if constexpr (DEV)
+      st_tile(P.tiles + (int64_t)r * P.nt + k, t);
+    else
+      P.tiles[(int64_t)r * P.nt + k] = t;
     if constexpr (mom) {
       // the waves' moments against the tile references, in wave order
       TileMom m{0.0, 0.0, 0.0};
@@ -1454,6 +1473,24 @@ __device__ __forceinline__ void stats_tile(const Params& P) {
   }
 }
 
+template <int DT, bool VEC, bool ARGMAX, bool MOM>
+__device__ __forceinline__ void stats_tile(const Params& P) {
+  using T = StatTile<DT, VEC>;
+  __shared__ Shared sh;
+  const int k = blockIdx.x, r = blockIdx.y;
+  const SeqParam sp = seq_param(P, r / (P.gamma + 1));
+  // rows that need first moments belong to the moment kernel (block-uniform)
+  if (MOM ? !needs_mom(sp) : (P.mom_split && needs_mom(sp))) return;
+  const int V = P.V;
+  const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
+  const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
+  const int64_t t0 = (int64_t)k * T::N;
+  uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
+  load_tile<DT, VEC, T::U, true>(qrow, t0, V, wq, threadIdx.x);
+  load_tile<DT, VEC, T::U, true>(prow, t0, V, wp, threadIdx.x);
+  tile_partial<DT, VEC, ARGMAX, MOM, false>(P, r, k, sp, wq, wp, sh);
+}
+
 template <int DT, bool VEC, bool ARGMAX>
 __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
   stats_tile<DT, VEC, ARGMAX, false>(P);
@@ -1469,6 +1506,34 @@ __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
 template <int DT, bool VEC, bool ARGMAX>
 __global__ __launch_bounds__(kThreads, SPC_MOM_OCCUPANCY) void k_stats_mom(Params P) {
   stats_tile<DT, VEC, ARGMAX, true>(P);
+}
+
+// The second-pass weight summed over a thread's entries of one statistics
+// tile: for a token rule eta's share (the q mass of the entries the rule
+// marks), else the residual max(0, p - q) (D_TV of Lemma 3).
+template <int DT, bool VEC>
+__device__ __forceinline__ double pass2_sum(const uint32_t (&wq)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
+                                            const uint32_t (&wp)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
+                                            const ProbScale& ps, bool tok) {
+  using T = StatTile<DT, VEC>;
+  double acc = 0.0;
+#pragma unroll
+  for (int i = 0; i < T::U; ++i) {
+    float t = 0.0f;
+#pragma unroll
+    for (int e = 0; e < T::VW; ++e) {
+      const float zq = elem<DT, VEC>(wq[i], e), zp = elem<DT, VEC>(wp[i], e);
+      if (tok)
+        t += token_r(ps.tok, zq, zp) ? prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo) : 0.0f;
+      else
+        t += residual_weight(zq, zp, ps);
+    }
+    acc += (double)t;
+    // one lane load at a time: with the whole tile already in registers the
+    // scheduler would otherwise start every entry's exponentials at once
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  return acc;
 }
 
 // TV pass (OPT rows at temperature > 0): D_TV(p, q) of Lemma 3, which needs
@@ -1496,24 +1561,115 @@ __global__ __launch_bounds__(kThreads) void k_tv(Params P) {
   }
   __syncthreads();
   const bool tok = is_token(sp.rule);  // block-uniform
-  const ProbScale ps = prob_scale(sp, srow, tok);
-  double acc = 0.0;
-#pragma unroll
-  for (int i = 0; i < T::U; ++i) {
-    float t = 0.0f;
-#pragma unroll
-    for (int e = 0; e < T::VW; ++e) {
-      const float zq = elem<DT, VEC>(wq[i], e), zp = elem<DT, VEC>(wp[i], e);
-      if (tok)  // eta: the q mass of the entries the rule marks
-        t += token_r(ps.tok, zq, zp) ? prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo) : 0.0f;
-      else
-        t += residual_weight(zq, zp, ps);
-    }
-    acc += (double)t;
-  }
+  double acc = pass2_sum<DT, VEC>(wq, wp, prob_scale(sp, srow, tok), tok);
   double unused = 0.0;
   block_sum2(acc, unused, sh);
   if (threadIdx.x == 0) P.tvpart[(int64_t)r * P.nt + k] = acc;
+}
+
+// ------------------------------------------- one read for the second pass
+// Statistics and the second pass in one launch, for batches whose rows need
+// no first moments.  A resident grid of G workgroups (G a multiple of nt,
+// all co-resident: a cooperative launch) takes tiles t = g, g + G, ... in
+// row-major order, so the nt tiles of a row always fall in one round of G.
+// A workgroup computes its tile's partial; on a row that needs the second
+// pass it then waits for the row's other nt - 1 partials (a per-row arrival
+// counter), merges them, and sums the TV or eta weight over the entries it
+// still holds in registers, so the row is read from HBM once.  The wait is
+// bounded: a workgroup that gives up writes a NaN partial, which makes its
+// sequence invalid (the sampling pass reports -1), instead of hanging.
+// Measured on MI355X it is slower than the second read it saves (each round
+// of resident tiles waits through publish, arrival and merge with its loads
+// idle, and a cooperative launch costs more to start), so it runs only on
+// request.
+constexpr uint32_t kRowSpinLimit = 1u << 16;  // about 0.1 s
+
+// Thread 0 has written the tile's partial (agent-scope stores).  Arrive on
+// the row's counter and wait until all n tiles have; returns false after the
+// spin limit.
+__device__ __forceinline__ bool row_arrive_wait(uint32_t* cnt, uint32_t n, Shared& sh) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    vmem_drain();  // the partial's stores are complete
+    uint32_t seen =
+        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u;
+    uint32_t it = 0;
+    while (seen < n && it < kRowSpinLimit) {
+      __builtin_amdgcn_s_sleep(2);
+      seen = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      ++it;
+    }
+    sh.flag = seen >= n;
+  }
+  __syncthreads();
+  const bool ok = sh.flag;
+  vmem_drain();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  return ok;
+}
+
+// Leave the row: the last of its n tiles to leave resets both counters
+// (every tile has arrived and stopped waiting by then).
+__device__ __forceinline__ void row_depart(uint32_t* cnt, uint32_t n) {
+  if (threadIdx.x == 0) {
+    const uint32_t prev =
+        __hip_atomic_fetch_add(cnt + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (prev == n - 1) {
+      __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(cnt + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+// Held to SPC_RES_OCCUPANCY resident workgroups per CU (no spill at 5).
+#ifndef SPC_RES_OCCUPANCY
+#define SPC_RES_OCCUPANCY 5
+#endif
+template <int DT, bool VEC, bool ARGMAX>
+__global__ __launch_bounds__(kThreads, SPC_RES_OCCUPANCY) void k_stats_res(Params P) {
+  using T = StatTile<DT, VEC>;
+  __shared__ Shared sh;
+  __shared__ RowStat srow;
+  const int nt = P.nt, V = P.V;
+  const int64_t ntiles = (int64_t)P.B * (P.gamma + 1) * nt;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {  // block-uniform
+    const int r = (int)(t / nt), k = (int)(t - (int64_t)r * nt);
+    const SeqParam sp = seq_param(P, r / (P.gamma + 1));
+    const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
+    const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
+    // the thread's load offsets are recomputed per tile rather than held
+    // across the loop in registers
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
+    load_tile<DT, VEC, T::U, true>(qrow, (int64_t)k * T::N, V, wq, tid);
+    load_tile<DT, VEC, T::U, true>(prow, (int64_t)k * T::N, V, wp, tid);
+    tile_partial<DT, VEC, ARGMAX, false, true>(P, r, k, sp, wq, wp, sh);
+    if (needs_pass2(sp)) {  // block-uniform
+      // only the packed words stay live across the wait: left free, the
+      // compiler keeps every unpacked entry of the statistics for reuse
+#pragma unroll
+      for (int i = 0; i < T::U; ++i)
+#pragma unroll
+        for (int j = 0; j < T::NW; ++j) asm volatile("" : "+v"(wq[i][j]), "+v"(wp[i][j]));
+      uint32_t* cnt = P.row_cnt + (int64_t)r * kRowCntStride;
+      const bool ok = row_arrive_wait(cnt, (uint32_t)nt, sh);
+      if (threadIdx.x < 64) {
+        const RowStat rs = merge_row<true>(P, r, false, false, 0, load_head<true>(P, r, false, false));
+        if (threadIdx.x == 0) srow = rs;
+      }
+      __syncthreads();
+      const bool tok = is_token(sp.rule);
+      double acc = pass2_sum<DT, VEC>(wq, wp, prob_scale(sp, srow, tok), tok);
+      double unused = 0.0;
+      block_sum2(acc, unused, sh);
+      if (threadIdx.x == 0)
+        P.tvpart[(int64_t)r * nt + k] = ok ? acc : __builtin_nan("");
+      row_depart(cnt, (uint32_t)nt);
+    }
+    __syncthreads();  // the block's shared scratch is reused by the next tile
+  }
 }
 
 // Sampling pass.  grid (K, B) of 1024-thread workgroups: every workgroup of
@@ -1698,14 +1854,38 @@ hipError_t launch_draft_t(const Params& P, bool argmax, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int DT, bool VEC, bool ARGMAX>
+const void* res_kernel() {
+  return reinterpret_cast<const void*>(&k_stats_res<DT, VEC, ARGMAX>);
+}
+
+template <int DT, bool VEC>
+const void* res_kernel(bool argmax) {
+  return argmax ? res_kernel<DT, VEC, true>() : res_kernel<DT, VEC, false>();
+}
+
 template <int DT, bool VEC>
 hipError_t launch_t(const Params& P, bool need_tv, bool need_sample, bool need_argmax,
-                    bool need_plain, bool need_mom, hipEvent_t e0, hipEvent_t e1,
+                    bool need_plain, bool need_mom, int res_grid, hipEvent_t e0, hipEvent_t e1,
                     hipStream_t st) {
   const unsigned R = (unsigned)(P.B * (P.gamma + 1));
   const dim3 grid(P.nt, R);
   hipError_t err;
   if (e0 && (err = hipEventRecord(e0, st)) != hipSuccess) return err;
+  if (res_grid > 0 && need_tv && !need_mom) {
+    // statistics and second pass, one read: every workgroup must be resident
+    void* args[] = {const_cast<Params*>(&P)};
+    err = hipLaunchCooperativeKernel(res_kernel<DT, VEC>(need_argmax), dim3((unsigned)res_grid),
+                                     dim3(kThreads), args, 0, st);
+    if (err == hipSuccess) {
+      if (e1 && (err = hipEventRecord(e1, st)) != hipSuccess) return err;
+      hipLaunchKernelGGL((k_sample<DT, VEC>), dim3(need_sample ? P.K : 1, P.B),
+                         dim3(kSampThreads), 0, st, P);
+      return hipGetLastError();
+    }
+    if (err != hipErrorCooperativeLaunchTooLarge && err != hipErrorNotSupported) return err;
+    (void)hipGetLastError();  // not launchable here: the two-kernel path below
+  }
   if (need_plain) {
     if (need_argmax)
       hipLaunchKernelGGL((k_stats<DT, VEC, true>), grid, dim3(kThreads), 0, st, P);
@@ -1765,18 +1945,35 @@ hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, hipSt
 }
 
 hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
-                         bool need_argmax, bool need_plain, bool need_mom, hipEvent_t e0,
-                         hipEvent_t e1, hipStream_t st) {
+                         bool need_argmax, bool need_plain, bool need_mom, int res_grid,
+                         hipEvent_t e0, hipEvent_t e1, hipStream_t st) {
   if (dtype == 1) {
     return vec ? launch_t<1, true>(P, need_tv, need_sample, need_argmax, need_plain, need_mom,
-                                   e0, e1, st)
+                                   res_grid, e0, e1, st)
                : launch_t<1, false>(P, need_tv, need_sample, need_argmax, need_plain, need_mom,
-                                    e0, e1, st);
+                                    res_grid, e0, e1, st);
   }
-  return vec ? launch_t<0, true>(P, need_tv, need_sample, need_argmax, need_plain, need_mom, e0,
-                                 e1, st)
-             : launch_t<0, false>(P, need_tv, need_sample, need_argmax, need_plain, need_mom, e0,
-                                  e1, st);
+  return vec ? launch_t<0, true>(P, need_tv, need_sample, need_argmax, need_plain, need_mom,
+                                 res_grid, e0, e1, st)
+             : launch_t<0, false>(P, need_tv, need_sample, need_argmax, need_plain, need_mom,
+                                  res_grid, e0, e1, st);
+}
+
+int res_blocks_per_cu(int dtype, bool vec, bool argmax) {
+  // per variant; queried once per process (every device here is the same part)
+  static int cache[2][2][2] = {{{-1, -1}, {-1, -1}}, {{-1, -1}, {-1, -1}}};
+  int& c = cache[dtype == 1][vec][argmax];
+  if (c < 0) {
+    const void* f = dtype == 1 ? (vec ? res_kernel<1, true>(argmax) : res_kernel<1, false>(argmax))
+                               : (vec ? res_kernel<0, true>(argmax) : res_kernel<0, false>(argmax));
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, f, kThreads, 0) != hipSuccess) {
+      (void)hipGetLastError();
+      nb = 0;
+    }
+    c = nb;
+  }
+  return c;
 }
 
 }  // namespace spc

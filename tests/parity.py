@@ -55,10 +55,17 @@ def _uniform_params(inp):
     return None
 
 
+def rules_mask(rule):
+    """rules_present bitmask of the valid rule ids in a per-sequence array."""
+    return sum(1 << r for r in set(int(x) for x in rule.tolist()) if 0 <= r <= W.OPTLOG)
+
+
 def run_gpu(inp, greedy=False, stats=True, stream=None):
     """One call through the C interface; returns numpy outputs.  Without
     statistics, batch-wide parameters go through spc_verify /
-    spc_greedy_verify (the entry points the benchmark times)."""
+    spc_greedy_verify (the entry points the benchmark times).  With them,
+    spc_verify_ex declares the rules the batch holds (rules_present), as the
+    benchmark's mixed workload does."""
     q, p = inp["q"], inp["p"]
     B, g1, V = q.shape
     dev = q.device
@@ -75,7 +82,8 @@ def run_gpu(inp, greedy=False, stats=True, stream=None):
         acc, tok, dm = spc.spc_verify_ex(
             q, p, inp["draft"], inp["uniforms"], 0, 0.0, 1.0, rule_per_seq=inp["rule"],
             alpha_per_seq=inp["alpha"], temp_per_seq=(torch.zeros_like(temp) if greedy else temp),
-            out_row_stats=row_stats, out_argmax=argmax, out_sample_norm=norm, stream=stream)
+            out_row_stats=row_stats, out_argmax=argmax, out_sample_norm=norm, stream=stream,
+            rules_present=rules_mask(inp["rule"]))
     torch.cuda.synchronize()
     out = dict(accept_len=acc.cpu().numpy(), next_token=tok.cpu().numpy(),
                defer=dm.cpu().numpy())

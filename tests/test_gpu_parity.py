@@ -526,3 +526,51 @@ def test_rules_present_hint():
     assert acc[3].item() == -1 and tok[3].item() == -1
     keep = [b for b in range(wl.B) if b != 3]
     np.testing.assert_array_equal(acc.cpu().numpy()[keep], out[0][0][keep])
+
+
+# ------------------------------------------- one read vs two for the second pass
+
+def _ex_outputs(inp, mask):
+    B, g1, _ = inp["q"].shape
+    stats = torch.full((B, g1, 8), float("nan"), device=DEV)
+    am = torch.full((B, g1, 2), -7, dtype=torch.int32, device=DEV)
+    norm = torch.full((B,), float("nan"), device=DEV)
+    acc, tok, dm = spc.spc_verify_ex(inp["q"], inp["p"], inp["draft"], inp["uniforms"], 0, 0.0,
+                                     1.0, rule_per_seq=inp["rule"], alpha_per_seq=inp["alpha"],
+                                     temp_per_seq=inp["temperature"], out_row_stats=stats,
+                                     out_argmax=am, out_sample_norm=norm, rules_present=mask)
+    torch.cuda.synchronize()
+    return [x.cpu().numpy() for x in (acc, tok, dm, stats, am, norm)]
+
+
+@pytest.mark.parametrize("case", ["opt", "token-v1", "token-v2", "token-v3", "mixed",
+                                  "opt-f32", "opt-full"])
+def test_one_read_second_pass_equals_two_reads(case, monkeypatch):
+    """The one-read statistics kernel (second pass over register-resident
+    tiles, selected with SPC_ONE_READ=1) and the default two-kernel path
+    compute the same partials in the same order: every output agrees
+    bitwise."""
+    rules = {"opt": (W.OPT, 0.1), "token-v1": (W.TOKEN_V1, 0.05),
+             "token-v2": (W.TOKEN_V2, 0.05), "token-v3": (W.TOKEN_V3, 0.3)}
+    if case == "mixed":
+        wl = W.WORKLOADS[5].with_(B=24, V=30000)
+    elif case == "opt-f32":
+        wl = W.WORKLOADS[2]
+    elif case == "opt-full":
+        wl = W.WORKLOADS[3].with_(rule=W.OPT, alpha=0.1, temperature=0.7)
+    else:
+        rule, alpha = rules[case]
+        wl = W.WORKLOADS[3].with_(B=16, V=70001 if case == "token-v2" else 70000, rule=rule,
+                                  alpha=alpha, temperature=0.7)
+    inp = W.generate(wl, 7, DEV)
+    if case == "mixed":
+        inp["temperature"][::7] = 0.0
+    mask = parity.rules_mask(inp["rule"])
+    _flush(f"[one-read] {case} B={wl.B} gamma={wl.gamma} V={wl.V} {wl.dtype} mask={mask:#x}")
+    monkeypatch.setenv("SPC_ONE_READ", "1")
+    one = _ex_outputs(inp, mask)
+    monkeypatch.delenv("SPC_ONE_READ")
+    two = _ex_outputs(inp, mask)
+    for a, b in zip(one, two):
+        np.testing.assert_array_equal(a, b)
+    assert (one[0] >= 0).all()
