@@ -32,9 +32,11 @@ def lib():
     """Load the oracle library, compiling it first if it is not built."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB):
+        # SPC_ORACLE_LIB: another build of the oracle (e.g. with sanitizers)
+        path = os.environ.get("SPC_ORACLE_LIB") or LIB
+        if path == LIB and not os.path.exists(LIB):
             build()
-        L = ctypes.CDLL(LIB)
+        L = ctypes.CDLL(path)
         L.orc_softmax_row.argtypes = [_P, ctypes.c_int, _I64, _D, _P, ctypes.POINTER(RowStats)]
         L.orc_softmax_row.restype = None
         L.orc_tv.argtypes = [_P, _P, _I64]
