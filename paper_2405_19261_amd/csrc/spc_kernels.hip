@@ -119,6 +119,32 @@ __device__ __forceinline__ void load_tile(const char* row, int64_t t0, int64_t e
   }
 }
 
+// The lowest entry attaining m among a thread's U lane loads w (lane load i
+// holds entries base + i * GT * VW + e, e < VW), given each lane load's
+// maximum g[i]: the first lane load whose maximum is m, then the first entry
+// of it equal to m.  INT_MAX when m = -inf (no finite entry).
+template <int DT, bool VEC, int U, int GT>
+__device__ __forceinline__ int first_max_index(const uint32_t (&w)[U][Tile<DT, VEC, U>::NW],
+                                               const float (&g)[U], float m, int base) {
+  using T = Tile<DT, VEC, U>;
+  int gi = 0;
+#pragma unroll
+  for (int i = U - 1; i >= 0; --i)
+    if (g[i] == m) gi = i;
+  uint32_t s[T::NW];
+#pragma unroll
+  for (int j = 0; j < T::NW; ++j) s[j] = w[0][j];
+#pragma unroll
+  for (int i = 1; i < U; ++i)
+#pragma unroll
+    for (int j = 0; j < T::NW; ++j) s[j] = (gi == i) ? w[i][j] : s[j];
+  int ei = 0;
+#pragma unroll
+  for (int e = T::VW - 1; e >= 0; --e)
+    if (elem<DT, VEC>(s, e) == m) ei = e;
+  return m == kNegInf ? 0x7fffffff : base + gi * GT * T::VW + ei;
+}
+
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float log2_hw(float x) { return __builtin_amdgcn_logf(x); }
 
@@ -1335,25 +1361,39 @@ __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, cons
                                              Shared& sh) {
   using T = StatTile<DT, VEC>;
   const int64_t t0 = (int64_t)k * T::N;
-  // Thread max; with ARGMAX also the lowest entry attaining it: entries are
-  // visited in increasing index order and only a strictly larger value moves
-  // the index (indices fit 32 bits: V < 2^31).
-  float mq = kNegInf, mp = kNegInf;
-  int iq = 0x7fffffff, ip = 0x7fffffff;
-  const int base = (int)t0 + (int)threadIdx.x * T::VW;
+  // Thread max, from the maxima of its lane loads; with ARGMAX also the
+  // lowest entry attaining it (indices fit 32 bits: V < 2^31).
+  float gq[T::U], gp[T::U];
 #pragma unroll
-  for (int i = 0; i < T::U; ++i)
+  for (int i = 0; i < T::U; ++i) {
+    float a = kNegInf, b = kNegInf;
 #pragma unroll
     for (int e = 0; e < T::VW; ++e) {
-      const float vq = elem<DT, VEC>(wq[i], e), vp = elem<DT, VEC>(wp[i], e);
-      if constexpr (ARGMAX && !MOM) {
-        const int idx = base + i * kThreads * T::VW + e;
-        if (vq > mq) iq = idx;
-        if (vp > mp) ip = idx;
-      }
-      mq = fmaxf(mq, vq);
-      mp = fmaxf(mp, vp);
+      a = fmaxf(a, elem<DT, VEC>(wq[i], e));
+      b = fmaxf(b, elem<DT, VEC>(wp[i], e));
     }
+    gq[i] = a;
+    gp[i] = b;
+  }
+  float mq = gq[0], mp = gp[0];
+#pragma unroll
+  for (int i = 1; i < T::U; ++i) {
+    mq = fmaxf(mq, gq[i]);
+    mp = fmaxf(mp, gp[i]);
+  }
+  int iq = 0x7fffffff, ip = 0x7fffffff;
+  const int base = (int)t0 + (int)threadIdx.x * T::VW;
+  if constexpr (ARGMAX && !MOM) {
+    iq = first_max_index<DT, VEC, T::U, kThreads>(wq, gq, mq, base);
+    ip = first_max_index<DT, VEC, T::U, kThreads>(wp, gp, mp, base);
+    // The packed words stay live for the selection above: the sums unpack
+    // them again instead of holding every unpacked entry as well.
+#pragma unroll
+    for (int i = 0; i < T::U; ++i)
+#pragma unroll
+      for (int j = 0; j < T::NW; ++j)
+        asm volatile("" : "+v"(const_cast<uint32_t&>(wq[i][j])), "+v"(const_cast<uint32_t&>(wp[i][j])));
+  }
   const float rq = (mq == kNegInf) ? 0.0f : mq * sp.c_hi;
   const float rp = (mp == kNegInf) ? 0.0f : mp * sp.c_hi;
   if constexpr (DEV) {
@@ -1373,7 +1413,8 @@ __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, cons
   // exponential of the tile live until then
   if constexpr (MOM) asm volatile("" : "+v"(hq), "+v"(hp), "+v"(xq), "+v"(sq), "+v"(spp));
   if constexpr (ARGMAX && MOM) {
-    // the lowest entry equal to the thread max, in a pass of its own
+    // the lowest entry equal to the thread max, in a pass of its own after
+    // the sums
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = T::U - 1; i >= 0; --i)
@@ -1733,19 +1774,27 @@ __global__ __launch_bounds__(kThreads) void k_draft(Params P) {
   const int64_t t0 = (int64_t)k * T::N;
   uint32_t w[T::U][T::NW];
   load_tile<DT, VEC, T::U, true>(row, t0, V, w, threadIdx.x);
-  float m = kNegInf;
+  float g[T::U];
+#pragma unroll
+  for (int i = 0; i < T::U; ++i) {
+    float a = kNegInf;
+#pragma unroll
+    for (int e = 0; e < T::VW; ++e) a = fmaxf(a, elem<DT, VEC>(w[i], e));
+    g[i] = a;
+  }
+  float m = g[0];
+#pragma unroll
+  for (int i = 1; i < T::U; ++i) m = fmaxf(m, g[i]);
   int im = 0x7fffffff;
   const int base = (int)t0 + (int)threadIdx.x * T::VW;
+  if constexpr (ARGMAX) {
+    im = first_max_index<DT, VEC, T::U, kThreads>(w, g, m, base);
+    // unpack again for the sums rather than hold every entry with the words
 #pragma unroll
-  for (int i = 0; i < T::U; ++i)
+    for (int i = 0; i < T::U; ++i)
 #pragma unroll
-    for (int e = 0; e < T::VW; ++e) {
-      const float v = elem<DT, VEC>(w[i], e);
-      if constexpr (ARGMAX) {
-        if (v > m) im = base + i * kThreads * T::VW + e;
-      }
-      m = fmaxf(m, v);
-    }
+      for (int j = 0; j < T::NW; ++j) asm volatile("" : "+v"(w[i][j]));
+  }
   const float r = (m == kNegInf) ? 0.0f : m * sp.c_hi;
   float s = 0.0f;
 #pragma unroll

@@ -574,3 +574,56 @@ def test_one_read_second_pass_equals_two_reads(case, monkeypatch):
     for a, b in zip(one, two):
         np.testing.assert_array_equal(a, b)
     assert (one[0] >= 0).all()
+
+
+# ------------------------------------------------------------- argmax ties
+
+def _plant_ties(t, seed):
+    """Give every row of t [B, g1, V] a new maximum repeated at positions that
+    tie within one lane load, across the lane loads of one thread, across
+    threads, workgroups and tiles, and at the row ends; returns the lowest
+    index of each row's maximum."""
+    B, g1, V = t.shape
+    g = np.random.default_rng(seed)
+    x = t.float().cpu().numpy().reshape(B * g1, V)
+    low = np.empty(B * g1, np.int64)
+    for r in range(B * g1):
+        kind = r % 4
+        if kind == 0:    # a tie at both row ends
+            pos = [V - 1, 0, V - 2]
+        elif kind == 1:  # ties inside one 8-entry lane load and one thread
+            b0 = int(g.integers(0, V - 20000)) & ~7
+            pos = [b0 + 5, b0 + 3, b0 + 3 + 2048, b0 + 3 + 6144, b0 + 7]
+        elif kind == 2:  # ties in other threads, workgroups and tiles
+            b0 = int(g.integers(0, V - 20000))
+            pos = [b0 + 8192 + 1, b0 + 9, b0 + 8 * 64 + 9, b0 + 8192 * 2]
+        else:            # many random ties
+            pos = list(g.choice(V, size=40, replace=False))
+        m = float(np.ceil(x[r].max())) + 1.0
+        x[r, pos] = m
+        low[r] = min(pos)
+    t.copy_(torch.from_numpy(x.reshape(B, g1, V)).to(t.dtype))
+    return low.reshape(B, g1)
+
+
+@pytest.mark.parametrize("dtype,V", [("bf16", 50000), ("f32", 50000), ("bf16", 50003)])
+def test_argmax_ties_lowest_index(dtype, V):
+    """Greedy rows (per-sequence temperatures 0 and >0 mixed, and the
+    batch-wide greedy entry point) take the lowest index attaining the
+    maximum on both tensors, as the oracle does."""
+    wl = W.WORKLOADS[4].with_(B=16, V=V, dtype=dtype)
+    inp = W.generate(wl, 9, DEV)
+    lq = _plant_ties(inp["q"], 1)
+    lp = _plant_ties(inp["p"], 2)
+    _flush(f"[ties] {dtype} V={V}")
+    g = parity.run_gpu(inp, greedy=True)
+    np.testing.assert_array_equal(g["argmax"][..., 0], lq)
+    np.testing.assert_array_equal(g["argmax"][..., 1], lp)
+    h = parity.host_inputs(inp)
+    parity.compare(g, parity.run_oracle(h, greedy=True), h, dtype, greedy=True)
+    # the same rows inside a batch that also samples
+    inp["temperature"][1::2] = 0.7
+    g2 = parity.run_gpu(inp)
+    sel = np.arange(wl.B) % 2 == 0
+    np.testing.assert_array_equal(g2["argmax"][sel][..., 0], lq[sel])
+    np.testing.assert_array_equal(g2["argmax"][sel][..., 1], lp[sel])
