@@ -239,7 +239,11 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   const uint32_t mask = ex ? ex->rules_present & kAll : 0u;
   const uint32_t rules = per_rule ? (mask ? mask : kAll) : (1u << rule);
   P.rule_mask = per_rule ? mask : 0u;
-  const bool need_tv = need_sample && (rules & kTv);
+  constexpr uint32_t kEta = (1u << SPC_RULE_TOKEN_V1) | (1u << SPC_RULE_TOKEN_V2) |
+                            (1u << SPC_RULE_TOKEN_V3);
+  const int tv_kinds = !need_sample ? 0
+                                    : ((rules & (kTv & ~kEta)) ? spc::kPassTv : 0) |
+                                          ((rules & kEta) ? spc::kPassEta : 0);
   const bool need_argmax = force_greedy || per_temp;
   // BiLD* at temperature 0 reads one logit instead of moments
   const bool bild_t0 = (rules & (1u << SPC_RULE_BILD)) && (force_greedy || per_temp);
@@ -251,12 +255,12 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   // tiles per round.
   int res_grid = 0;
   const int64_t R = (int64_t)B * (gamma + 1);
-  if (need_tv && !need_mom && R <= spc::kResRows && one_read_requested()) {
+  if (tv_kinds && !need_mom && R <= spc::kResRows && one_read_requested()) {
     const int nb = spc::res_blocks_per_cu(dtype, vec, need_argmax);
     const int64_t rows_per_round = (int64_t)nb * cus / P.nt;
     if (rows_per_round >= 1) res_grid = (int)(std::min<int64_t>(rows_per_round, R) * P.nt);
   }
-  e = spc::launch_verify(P, dtype, vec, need_tv, need_sample, need_argmax, need_plain, need_mom,
+  e = spc::launch_verify(P, dtype, vec, tv_kinds, need_sample, need_argmax, need_plain, need_mom,
                          res_grid, ex ? ex->ev_hot_begin : nullptr,
                          ex ? ex->ev_hot_end : nullptr, stream);
   if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));

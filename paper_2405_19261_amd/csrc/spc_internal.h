@@ -117,16 +117,20 @@ int res_blocks_per_cu(int dtype, bool vec, bool argmax);
 // tiles).  argmax: some row may be at temperature 0.
 hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, hipStream_t stream);
 
-// Enqueue the kernels of one verify call.  need_tv: the batch may hold OPT,
-// OPTLOG or token-rule sequences at temperature > 0; need_sample: it may hold
+// Second passes a batch may need (bits of tv_kinds): D_TV of OPT and OPTLOG
+// rows, eta of token-rule rows, each at temperature > 0.
+constexpr int kPassTv = 1, kPassEta = 2;
+
+// Enqueue the kernels of one verify call.  tv_kinds: the second passes the
+// batch may need (kPassTv | kPassEta); need_sample: it may hold
 // sequences at temperature > 0; need_argmax: it may hold greedy (temperature
 // 0) sequences; need_plain / need_mom: it may hold rows that need no first
 // moments / rows that do (log-loss rules, BiLD* at temperature > 0), each
 // kind handled by its own statistics kernel.  res_grid > 0 (a multiple of
-// nt; only with need_tv and without need_mom): statistics and second pass in
+// nt; only with tv_kinds and without need_mom): statistics and second pass in
 // one cooperative launch of res_grid workgroups instead of two kernels.
 // Returns the first launch error.
-hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
+hipError_t launch_verify(const Params& P, int dtype, bool vec, int tv_kinds, bool need_sample,
                          bool need_argmax, bool need_plain, bool need_mom, int res_grid,
                          hipEvent_t ev_begin, hipEvent_t ev_end, hipStream_t stream);
 

@@ -1577,32 +1577,65 @@ __device__ __forceinline__ double pass2_sum(const uint32_t (&wq)[StatTile<DT, VE
   return acc;
 }
 
+// eta's share of a token-rule tile when the statistics already fix it: the
+// rule marks every entry of a tile whose largest logit (p's for TokenV2/V3,
+// q's for TokenV1) lies below the threshold, so the share is the tile's q
+// mass -- the same expression the sampling pass evaluates for that tile's q
+// mass, so the two cancel exactly there -- and a threshold of -inf marks no
+// entry.  False when the tile's entries must be visited.
+__device__ __forceinline__ bool eta_from_stats(const TokenRule& tr, const TilePart& t,
+                                               double lz_q, double* out) {
+  if (tr.theta == kNegInf) {
+    *out = 0.0;
+    return true;
+  }
+  if ((tr.on_p ? t.zmax_p : t.zmax_q) < tr.theta) {
+    *out = t.s_q * exp2_acc((double)t.r_q - lz_q);
+    return true;
+  }
+  return false;
+}
+
 // TV pass (OPT rows at temperature > 0): D_TV(p, q) of Lemma 3, which needs
 // both normalisers.  grid (nt, R): stats tile k of row r; wave 0 merges the
 // row's statistics first (a fixed-order computation every tile of the row
 // repeats identically).
-template <int DT, bool VEC>
+template <int DT, bool VEC, bool TOK>
 __global__ __launch_bounds__(kThreads) void k_tv(Params P) {
   using T = StatTile<DT, VEC>;
   __shared__ Shared sh;
   __shared__ RowStat srow;
   const int k = blockIdx.x, r = blockIdx.y;
   const SeqParam sp = seq_param(P, r / (P.gamma + 1));
-  if (!needs_pass2(sp)) return;  // block-uniform
+  // token-rule rows (eta) and D_TV rows each have their own variant
+  if (!needs_pass2(sp) || is_token(sp.rule) != TOK) return;  // block-uniform
   const int V = P.V;
   const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
   const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
   const int64_t t0 = (int64_t)k * T::N;
+  constexpr bool tok = TOK;
   uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
-  load_tile<DT, VEC, T::U, true>(qrow, t0, V, wq, threadIdx.x);
-  load_tile<DT, VEC, T::U, true>(prow, t0, V, wp, threadIdx.x);
+  if constexpr (!tok) {  // D_TV visits every tile: its loads overlap the merge
+    load_tile<DT, VEC, T::U, true>(qrow, t0, V, wq, threadIdx.x);
+    load_tile<DT, VEC, T::U, true>(prow, t0, V, wp, threadIdx.x);
+  }
   if (threadIdx.x < 64) {
     const RowStat rs = merge_row(P, r, false, false);
     if (threadIdx.x == 0) srow = rs;
   }
   __syncthreads();
-  const bool tok = is_token(sp.rule);  // block-uniform
-  double acc = pass2_sum<DT, VEC>(wq, wp, prob_scale(sp, srow, tok), tok);
+  const ProbScale ps = prob_scale(sp, srow, tok);
+  if constexpr (tok) {
+    // eta: most tiles need no second look at their entries
+    double eta;
+    if (eta_from_stats(ps.tok, P.tiles[(int64_t)r * P.nt + k], srow.lz_q, &eta)) {
+      if (threadIdx.x == 0) P.tvpart[(int64_t)r * P.nt + k] = eta;
+      return;  // block-uniform
+    }
+    load_tile<DT, VEC, T::U, true>(qrow, t0, V, wq, threadIdx.x);
+    load_tile<DT, VEC, T::U, true>(prow, t0, V, wp, threadIdx.x);
+  }
+  double acc = pass2_sum<DT, VEC>(wq, wp, ps, tok);
   double unused = 0.0;
   block_sum2(acc, unused, sh);
   if (threadIdx.x == 0) P.tvpart[(int64_t)r * P.nt + k] = acc;
@@ -1702,11 +1735,18 @@ __global__ __launch_bounds__(kThreads, SPC_RES_OCCUPANCY) void k_stats_res(Param
       }
       __syncthreads();
       const bool tok = is_token(sp.rule);
-      double acc = pass2_sum<DT, VEC>(wq, wp, prob_scale(sp, srow, tok), tok);
-      double unused = 0.0;
-      block_sum2(acc, unused, sh);
-      if (threadIdx.x == 0)
-        P.tvpart[(int64_t)r * nt + k] = ok ? acc : __builtin_nan("");
+      const ProbScale ps = prob_scale(sp, srow, tok);
+      double eta;
+      if (tok && eta_from_stats(ps.tok, ld_tile(P.tiles + (int64_t)r * nt + k), srow.lz_q,
+                                &eta)) {
+        if (threadIdx.x == 0) P.tvpart[(int64_t)r * nt + k] = ok ? eta : __builtin_nan("");
+      } else {
+        double acc = pass2_sum<DT, VEC>(wq, wp, ps, tok);
+        double unused = 0.0;
+        block_sum2(acc, unused, sh);
+        if (threadIdx.x == 0)
+          P.tvpart[(int64_t)r * nt + k] = ok ? acc : __builtin_nan("");
+      }
       row_depart(cnt, (uint32_t)nt);
     }
     __syncthreads();  // the block's shared scratch is reused by the next tile
@@ -1914,14 +1954,14 @@ const void* res_kernel(bool argmax) {
 }
 
 template <int DT, bool VEC>
-hipError_t launch_t(const Params& P, bool need_tv, bool need_sample, bool need_argmax,
+hipError_t launch_t(const Params& P, int tv_kinds, bool need_sample, bool need_argmax,
                     bool need_plain, bool need_mom, int res_grid, hipEvent_t e0, hipEvent_t e1,
                     hipStream_t st) {
   const unsigned R = (unsigned)(P.B * (P.gamma + 1));
   const dim3 grid(P.nt, R);
   hipError_t err;
   if (e0 && (err = hipEventRecord(e0, st)) != hipSuccess) return err;
-  if (res_grid > 0 && need_tv && !need_mom) {
+  if (res_grid > 0 && tv_kinds && !need_mom) {
     // statistics and second pass, one read: every workgroup must be resident
     void* args[] = {const_cast<Params*>(&P)};
     err = hipLaunchCooperativeKernel(res_kernel<DT, VEC>(need_argmax), dim3((unsigned)res_grid),
@@ -1950,8 +1990,12 @@ hipError_t launch_t(const Params& P, bool need_tv, bool need_sample, bool need_a
     if ((err = hipGetLastError()) != hipSuccess) return err;
   }
   if (e1 && (err = hipEventRecord(e1, st)) != hipSuccess) return err;
-  if (need_tv) {
-    hipLaunchKernelGGL((k_tv<DT, VEC>), dim3(P.nt, R), dim3(kThreads), 0, st, P);
+  if (tv_kinds & kPassTv) {
+    hipLaunchKernelGGL((k_tv<DT, VEC, false>), dim3(P.nt, R), dim3(kThreads), 0, st, P);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+  }
+  if (tv_kinds & kPassEta) {
+    hipLaunchKernelGGL((k_tv<DT, VEC, true>), dim3(P.nt, R), dim3(kThreads), 0, st, P);
     if ((err = hipGetLastError()) != hipSuccess) return err;
   }
   // a batch with no sequence at temperature > 0 only needs the decisions
@@ -1993,18 +2037,18 @@ hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, hipSt
   return vec ? launch_draft_t<0, true>(P, argmax, st) : launch_draft_t<0, false>(P, argmax, st);
 }
 
-hipError_t launch_verify(const Params& P, int dtype, bool vec, bool need_tv, bool need_sample,
+hipError_t launch_verify(const Params& P, int dtype, bool vec, int tv_kinds, bool need_sample,
                          bool need_argmax, bool need_plain, bool need_mom, int res_grid,
                          hipEvent_t e0, hipEvent_t e1, hipStream_t st) {
   if (dtype == 1) {
-    return vec ? launch_t<1, true>(P, need_tv, need_sample, need_argmax, need_plain, need_mom,
+    return vec ? launch_t<1, true>(P, tv_kinds, need_sample, need_argmax, need_plain, need_mom,
                                    res_grid, e0, e1, st)
-               : launch_t<1, false>(P, need_tv, need_sample, need_argmax, need_plain, need_mom,
+               : launch_t<1, false>(P, tv_kinds, need_sample, need_argmax, need_plain, need_mom,
                                     res_grid, e0, e1, st);
   }
-  return vec ? launch_t<0, true>(P, need_tv, need_sample, need_argmax, need_plain, need_mom,
+  return vec ? launch_t<0, true>(P, tv_kinds, need_sample, need_argmax, need_plain, need_mom,
                                  res_grid, e0, e1, st)
-             : launch_t<0, false>(P, need_tv, need_sample, need_argmax, need_plain, need_mom,
+             : launch_t<0, false>(P, tv_kinds, need_sample, need_argmax, need_plain, need_mom,
                                   res_grid, e0, e1, st);
 }
 
