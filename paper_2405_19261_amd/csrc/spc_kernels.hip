@@ -428,8 +428,7 @@ __device__ __forceinline__ bool is_log(int rule) {
   return rule >= SPC_RULE_BILD && rule <= SPC_RULE_OPTLOG;
 }
 
-// Rules whose residual at a rejection is max(0, p - q) summed per tile by the
-// second pass (their D_TV partials).
+// Rules whose deferral reads D_TV (Lemma 3), which the second pass sums.
 __device__ __forceinline__ bool has_tv_parts(int rule) {
   return rule == SPC_RULE_OPT || rule == SPC_RULE_OPTLOG;
 }
@@ -975,11 +974,10 @@ __device__ __forceinline__ void load_chunk(const char* row, int64_t c0, int V, C
 }
 
 // Sources of the part masses of the sampled distribution: the statistics
-// partials per tile (q or p: each tile's share of the normaliser), the TV
-// partials per tile (the residual of an OPT row, which the second pass
-// summed), the statistics and eta partials together (a token rule's target),
-// or the residual masses per SampChunk computed by the sampling pass.
-enum MassSrc : int { kSrcStatsQ = 0, kSrcStatsP = 1, kSrcTv = 2, kSrcPass = 3, kSrcTokPi = 4,
+// partials per tile (q or p: each tile's share of the normaliser), the
+// statistics and eta partials together (a token rule's target), or the
+// residual masses per SampChunk computed by the sampling pass.
+enum MassSrc : int { kSrcStatsQ = 0, kSrcStatsP = 1, kSrcPass = 3, kSrcTokPi = 4,
                      kSrcDraft = 5 };
 
 template <int SRC>
@@ -991,8 +989,6 @@ __device__ __forceinline__ double part_mass(const Params& P, int64_t row, int b,
   } else if constexpr (SRC == kSrcStatsP) {
     const TilePart& t = P.tiles[row * P.nt + k];
     return t.s_p * exp2_acc((double)t.r_p - rs.lz_p);
-  } else if constexpr (SRC == kSrcTv) {
-    return P.tvpart[row * P.nt + k];
   } else if constexpr (SRC == kSrcTokPi) {
     // Alg. 6's target over a tile: its q mass less the eta partial (the q
     // mass where r = 1), plus eta times its p mass
@@ -1252,7 +1248,6 @@ __device__ __forceinline__ void draw(const Params& P, int b, int64_t row, int ki
     double rem, W;
     if (src == kSrcStatsQ) W = find_part<kSrcStatsQ>(P, row, b, P.nt, rs, u, &ks, &rem);
     else if (src == kSrcStatsP) W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
-    else if (src == kSrcTv) W = find_part<kSrcTv>(P, row, b, P.nt, rs, u, &ks, &rem);
     else if (src == kSrcTokPi) W = find_part<kSrcTokPi>(P, row, b, P.nt, rs, u, &ks, &rem);
     else W = find_part<kSrcPass>(P, row, b, P.nc, rs, u, &ks, &rem);
     if ((kind == kResidual || kind == kTokRes) && !(W > 0.0)) {
@@ -1551,7 +1546,7 @@ __global__ __launch_bounds__(kThreads, SPC_MOM_OCCUPANCY) void k_stats_mom(Param
 
 // The second-pass weight summed over a thread's entries of one statistics
 // tile: for a token rule eta's share (the q mass of the entries the rule
-// marks), else the residual max(0, p - q) (D_TV of Lemma 3).
+// marks), else max(0, p - q) (D_TV of Lemma 3) in float32.
 template <int DT, bool VEC>
 __device__ __forceinline__ double pass2_sum(const uint32_t (&wq)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
                                             const uint32_t (&wp)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
@@ -1564,10 +1559,16 @@ __device__ __forceinline__ double pass2_sum(const uint32_t (&wq)[StatTile<DT, VE
 #pragma unroll
     for (int e = 0; e < T::VW; ++e) {
       const float zq = elem<DT, VEC>(wq[i], e), zp = elem<DT, VEC>(wp[i], e);
-      if (tok)
+      if (tok) {
         t += token_r(ps.tok, zq, zp) ? prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo) : 0.0f;
-      else
-        t += residual_weight(zq, zp, ps);
+      } else {
+        // D_TV for the deferral decision only, where an absolute error of
+        // about 1e-7 is far inside the decision margin; the replacement draw
+        // of a rejected row sums its own cancellation-free residual
+        const float pq = prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo);
+        const float pp = prob(zp, ps.c_hi, ps.c_lo, ps.p_hi, ps.p_lo);
+        t += fmaxf(pp - pq, 0.0f);
+      }
     }
     acc += (double)t;
     // one lane load at a time: with the whole tile already in registers the
@@ -1755,11 +1756,11 @@ __global__ __launch_bounds__(kThreads, SPC_RES_OCCUPANCY) void k_stats_res(Param
 
 // Sampling pass.  grid (K, B) of 1024-thread workgroups: every workgroup of
 // sequence b merges the sequence's rows and decides it (workgroup 0 writes
-// the outputs).  A replacement drawn from the residual of a non-OPT row needs
-// that row's residual masses: the K workgroups sum them chunk by chunk, and
-// the last to finish draws.  Every other draw -- the extra token from q or p,
-// or an OPT residual, whose per-tile masses the earlier passes left -- is
-// made by workgroup 0 alone.
+// the outputs).  A replacement drawn from a residual needs that row's
+// residual masses: the K workgroups sum them chunk by chunk, and the last to
+// finish draws.  Every other draw -- the extra token from q, p or a token
+// rule's target, whose per-tile masses the earlier passes left -- is made by
+// workgroup 0 alone.
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
   __shared__ SampShared sh;
@@ -1771,13 +1772,10 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
   if (s.kind == kNone) return;  // block-uniform
   const int64_t row = (int64_t)b * (P.gamma + 1) + s.row;
   const RowStat rs = ss.rows[s.row].rs;
-  const bool pass = s.kind == kTokRes || (s.kind == kResidual && !has_tv_parts(sp.rule));
+  const bool pass = s.kind == kTokRes || s.kind == kResidual;
   if (!pass) {
     if (k != 0) return;  // block-uniform
-    const int src = s.kind == kQ     ? kSrcStatsQ
-                    : s.kind == kP   ? kSrcStatsP
-                    : s.kind == kTokPi ? kSrcTokPi
-                                       : kSrcTv;
+    const int src = s.kind == kQ ? kSrcStatsQ : s.kind == kP ? kSrcStatsP : kSrcTokPi;
     draw<DT, VEC>(P, b, row, s.kind, src, s.u, sp, rs, ss, sh);
     return;
   }
