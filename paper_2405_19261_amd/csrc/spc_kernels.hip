@@ -1601,45 +1601,74 @@ __device__ __forceinline__ bool eta_from_stats(const TokenRule& tr, const TilePa
 // both normalisers.  grid (nt, R): stats tile k of row r; wave 0 merges the
 // row's statistics first (a fixed-order computation every tile of the row
 // repeats identically).
-template <int DT, bool VEC, bool TOK>
+template <int DT, bool VEC>
 __global__ __launch_bounds__(kThreads) void k_tv(Params P) {
   using T = StatTile<DT, VEC>;
   __shared__ Shared sh;
   __shared__ RowStat srow;
   const int k = blockIdx.x, r = blockIdx.y;
   const SeqParam sp = seq_param(P, r / (P.gamma + 1));
-  // token-rule rows (eta) and D_TV rows each have their own variant
-  if (!needs_pass2(sp) || is_token(sp.rule) != TOK) return;  // block-uniform
+  // D_TV rows only: token-rule rows take k_eta
+  if (!needs_pass2(sp) || is_token(sp.rule)) return;  // block-uniform
   const int V = P.V;
   const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
   const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
   const int64_t t0 = (int64_t)k * T::N;
-  constexpr bool tok = TOK;
   uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
-  if constexpr (!tok) {  // D_TV visits every tile: its loads overlap the merge
-    load_tile<DT, VEC, T::U, true>(qrow, t0, V, wq, threadIdx.x);
-    load_tile<DT, VEC, T::U, true>(prow, t0, V, wp, threadIdx.x);
-  }
+  // D_TV visits every tile: its loads overlap the merge
+  load_tile<DT, VEC, T::U, true>(qrow, t0, V, wq, threadIdx.x);
+  load_tile<DT, VEC, T::U, true>(prow, t0, V, wp, threadIdx.x);
   if (threadIdx.x < 64) {
     const RowStat rs = merge_row(P, r, false, false);
     if (threadIdx.x == 0) srow = rs;
   }
   __syncthreads();
-  const ProbScale ps = prob_scale(sp, srow, tok);
-  if constexpr (tok) {
-    // eta: most tiles need no second look at their entries
-    double eta;
-    if (eta_from_stats(ps.tok, P.tiles[(int64_t)r * P.nt + k], srow.lz_q, &eta)) {
-      if (threadIdx.x == 0) P.tvpart[(int64_t)r * P.nt + k] = eta;
-      return;  // block-uniform
-    }
-    load_tile<DT, VEC, T::U, true>(qrow, t0, V, wq, threadIdx.x);
-    load_tile<DT, VEC, T::U, true>(prow, t0, V, wp, threadIdx.x);
-  }
-  double acc = pass2_sum<DT, VEC>(wq, wp, ps, tok);
+  double acc = pass2_sum<DT, VEC>(wq, wp, prob_scale(sp, srow, false), false);
   double unused = 0.0;
   block_sum2(acc, unused, sh);
   if (threadIdx.x == 0) P.tvpart[(int64_t)r * P.nt + k] = acc;
+}
+
+// Eta pass (token-rule rows at temperature > 0).  grid (ceil(nt /
+// kEtaTiles), R): a workgroup merges row r once and takes its tiles
+// x kEtaTiles .. + kEtaTiles - 1 in turn.  A tile wholly below the rule's
+// threshold takes its share from the statistics (eta_from_stats); any other
+// tile is read again and summed exactly as by the TV pass's tile code.
+constexpr int kEtaTiles = 8;
+
+template <int DT, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_eta(Params P) {
+  using T = StatTile<DT, VEC>;
+  __shared__ Shared sh;
+  __shared__ RowStat srow;
+  const int r = blockIdx.y;
+  const SeqParam sp = seq_param(P, r / (P.gamma + 1));
+  if (!needs_pass2(sp) || !is_token(sp.rule)) return;  // block-uniform
+  const int V = P.V, nt = P.nt;
+  const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
+  const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
+  if (threadIdx.x < 64) {
+    const RowStat rs = merge_row(P, r, false, false);
+    if (threadIdx.x == 0) srow = rs;
+  }
+  __syncthreads();
+  const ProbScale ps = prob_scale(sp, srow, true);
+  const int k1 = min(nt, ((int)blockIdx.x + 1) * kEtaTiles);
+  for (int k = (int)blockIdx.x * kEtaTiles; k < k1; ++k) {  // block-uniform
+    double eta;
+    if (eta_from_stats(ps.tok, P.tiles[(int64_t)r * nt + k], srow.lz_q, &eta)) {
+      if (threadIdx.x == 0) P.tvpart[(int64_t)r * nt + k] = eta;
+      continue;
+    }
+    uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
+    load_tile<DT, VEC, T::U, true>(qrow, (int64_t)k * T::N, V, wq, threadIdx.x);
+    load_tile<DT, VEC, T::U, true>(prow, (int64_t)k * T::N, V, wp, threadIdx.x);
+    double acc = pass2_sum<DT, VEC>(wq, wp, ps, true);
+    double unused = 0.0;
+    block_sum2(acc, unused, sh);
+    if (threadIdx.x == 0) P.tvpart[(int64_t)r * nt + k] = acc;
+    __syncthreads();  // the block's shared scratch is reused by the next tile
+  }
 }
 
 // ------------------------------------------- one read for the second pass
@@ -1989,11 +2018,12 @@ hipError_t launch_t(const Params& P, int tv_kinds, bool need_sample, bool need_a
   }
   if (e1 && (err = hipEventRecord(e1, st)) != hipSuccess) return err;
   if (tv_kinds & kPassTv) {
-    hipLaunchKernelGGL((k_tv<DT, VEC, false>), dim3(P.nt, R), dim3(kThreads), 0, st, P);
+    hipLaunchKernelGGL((k_tv<DT, VEC>), dim3(P.nt, R), dim3(kThreads), 0, st, P);
     if ((err = hipGetLastError()) != hipSuccess) return err;
   }
   if (tv_kinds & kPassEta) {
-    hipLaunchKernelGGL((k_tv<DT, VEC, true>), dim3(P.nt, R), dim3(kThreads), 0, st, P);
+    hipLaunchKernelGGL((k_eta<DT, VEC>), dim3((P.nt + kEtaTiles - 1) / kEtaTiles, R),
+                       dim3(kThreads), 0, st, P);
     if ((err = hipGetLastError()) != hipSuccess) return err;
   }
   // a batch with no sequence at temperature > 0 only needs the decisions
