@@ -250,6 +250,12 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
   const bool need_mom = (rules & kLog) && !(rules == (1u << SPC_RULE_BILD) && force_greedy);
   const bool need_plain = (rules & ~kLog) || per_temp || bild_t0;
   P.mom_split = (need_mom && need_plain) ? 1 : 0;
+  // moments by rule: BiLD* reads x, ChowLog H(q), DiffLog and OPTLog H(q) - H(p)
+  P.mom_set = ((rules & (1u << SPC_RULE_BILD)) ? spc::kMomX : 0) |
+              ((rules & (1u << SPC_RULE_CHOWLOG)) ? spc::kMomHQ : 0) |
+              ((rules & ((1u << SPC_RULE_DIFFLOG) | (1u << SPC_RULE_OPTLOG)))
+                   ? spc::kMomHQ | spc::kMomHP
+                   : 0);
   // The second pass reads its rows again, unless the one-read kernel is
   // requested and fits: a resident grid holding at least one whole row of
   // tiles per round.

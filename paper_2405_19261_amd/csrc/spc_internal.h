@@ -34,6 +34,10 @@ struct TileMom {
   double hq, hp, x;
 };
 
+// First moments (TileMom) a statistics pass may sum: x for BiLD*'s
+// cross-entropy, hq for H(q), hp for H(p).
+constexpr int kMomX = 1, kMomHQ = 2, kMomHP = 4;
+
 // Per-row statistics after merging the tiles of a row.
 struct RowStat {
   double lz_q, lz_p;      // log2 sum_v 2^(z_v * c)  (= lse / ln 2)
@@ -66,6 +70,7 @@ struct Params {
   int32_t mom_split;       // the moment statistics kernel runs too: the plain one
                            // leaves it the rows that need first moments
   uint32_t rule_mask;      // rules per-sequence arrays may hold (0: any)
+  int32_t mom_set;         // first moments the moment kernel sums (kMom* bits)
   const int32_t* rule_ps;
   const float* alpha_ps;
   const float* temp_ps;

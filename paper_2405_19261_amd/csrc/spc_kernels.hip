@@ -1294,11 +1294,12 @@ __device__ __forceinline__ void draw(const Params& P, int b, int64_t row, int ki
 // (batches that may hold greedy rows) the lowest entry attaining the max is
 // found as well.
 // Thread sums of one statistics tile: s = sum 2^a over the thread's entries,
-// a = z c - r (r the thread reference); with MOM also the first moments
-// hq = sum 2^a_q a_q, hp = sum 2^a_p a_p and x = sum 2^a_q a_p (entries of
-// zero weight contribute nothing, so -inf logits never meet an infinite
-// factor; a finite-weight q entry facing a -inf p logit makes x = -inf).
-template <int DT, bool VEC, bool MOM>
+// a = z c - r (r the thread reference); with MOM (a set of kMom* bits) also
+// the first moments it names: hq = sum 2^a_q a_q, hp = sum 2^a_p a_p and
+// x = sum 2^a_q a_p (entries of zero weight contribute nothing, so -inf
+// logits never meet an infinite factor; a finite-weight q entry facing a -inf
+// p logit makes x = -inf).  Moments outside the set stay 0.
+template <int DT, bool VEC, int MOM>
 __device__ __forceinline__ void tile_sums(const uint32_t (&wq)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
                                           const uint32_t (&wp)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
                                           const SeqParam& sp, float rq, float rp, float& sq,
@@ -1317,9 +1318,9 @@ __device__ __forceinline__ void tile_sums(const uint32_t (&wq)[StatTile<DT, VEC>
         const bool wq_pos = tq > 0.0f;
         sq += tq;
         spp += tp;
-        hq = fmaf(tq, wq_pos ? aq : 0.0f, hq);
-        xq = fmaf(tq, wq_pos ? ap : 0.0f, xq);
-        hp = fmaf(tp, tp > 0.0f ? ap : 0.0f, hp);
+        if constexpr ((MOM & kMomHQ) != 0) hq = fmaf(tq, wq_pos ? aq : 0.0f, hq);
+        if constexpr ((MOM & kMomX) != 0) xq = fmaf(tq, wq_pos ? ap : 0.0f, xq);
+        if constexpr ((MOM & kMomHP) != 0) hp = fmaf(tp, tp > 0.0f ? ap : 0.0f, hp);
         // keep the scheduler from hoisting every exponential of the tile
         if ((e & 3) == 3) __builtin_amdgcn_sched_barrier(0);
       }
@@ -1349,7 +1350,7 @@ __device__ __forceinline__ void tile_sums(const uint32_t (&wq)[StatTile<DT, VEC>
 // The partial of statistics tile k of row r from its loaded entries (wq, wp),
 // written by thread 0: with DEV through agent-scope stores, for readers in
 // the same launch.
-template <int DT, bool VEC, bool ARGMAX, bool MOM, bool DEV>
+template <int DT, bool VEC, bool ARGMAX, int MOM, bool DEV>
 __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, const SeqParam& sp,
                                              const uint32_t (&wq)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
                                              const uint32_t (&wp)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
@@ -1509,7 +1510,7 @@ __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, cons
   }
 }
 
-template <int DT, bool VEC, bool ARGMAX, bool MOM>
+template <int DT, bool VEC, bool ARGMAX, int MOM>
 __device__ __forceinline__ void stats_tile(const Params& P) {
   using T = StatTile<DT, VEC>;
   __shared__ Shared sh;
@@ -1529,7 +1530,7 @@ __device__ __forceinline__ void stats_tile(const Params& P) {
 
 template <int DT, bool VEC, bool ARGMAX>
 __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
-  stats_tile<DT, VEC, ARGMAX, false>(P);
+  stats_tile<DT, VEC, ARGMAX, 0>(P);
 }
 
 // With first moments, for the rows of BiLD* (temperature > 0) and log-loss
@@ -1539,9 +1540,17 @@ __global__ __launch_bounds__(kThreads) void k_stats(Params P) {
 #ifndef SPC_MOM_OCCUPANCY
 #define SPC_MOM_OCCUPANCY 6
 #endif
-template <int DT, bool VEC, bool ARGMAX>
+template <int DT, bool VEC, bool ARGMAX, int MS>
 __global__ __launch_bounds__(kThreads, SPC_MOM_OCCUPANCY) void k_stats_mom(Params P) {
-  stats_tile<DT, VEC, ARGMAX, true>(P);
+  stats_tile<DT, VEC, ARGMAX, MS>(P);
+}
+
+template <int DT, bool VEC, int MS>
+void launch_mom(const Params& P, bool argmax, dim3 grid, hipStream_t st) {
+  if (argmax)
+    hipLaunchKernelGGL((k_stats_mom<DT, VEC, true, MS>), grid, dim3(kThreads), 0, st, P);
+  else
+    hipLaunchKernelGGL((k_stats_mom<DT, VEC, false, MS>), grid, dim3(kThreads), 0, st, P);
 }
 
 // The second-pass weight summed over a thread's entries of one statistics
@@ -1749,7 +1758,7 @@ __global__ __launch_bounds__(kThreads, SPC_RES_OCCUPANCY) void k_stats_res(Param
     uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
     load_tile<DT, VEC, T::U, true>(qrow, (int64_t)k * T::N, V, wq, tid);
     load_tile<DT, VEC, T::U, true>(prow, (int64_t)k * T::N, V, wp, tid);
-    tile_partial<DT, VEC, ARGMAX, false, true>(P, r, k, sp, wq, wp, sh);
+    tile_partial<DT, VEC, ARGMAX, 0, true>(P, r, k, sp, wq, wp, sh);
     if (needs_pass2(sp)) {  // block-uniform
       // only the packed words stay live across the wait: left free, the
       // compiler keeps every unpacked entry of the statistics for reuse
@@ -2010,10 +2019,14 @@ hipError_t launch_t(const Params& P, int tv_kinds, bool need_sample, bool need_a
     if ((err = hipGetLastError()) != hipSuccess) return err;
   }
   if (need_mom) {
-    if (need_argmax)
-      hipLaunchKernelGGL((k_stats_mom<DT, VEC, true>), grid, dim3(kThreads), 0, st, P);
+    // the moments the batch's rules read: x alone (BiLD*), H_q alone
+    // (ChowLog), or all three
+    if (P.mom_set == kMomX)
+      launch_mom<DT, VEC, kMomX>(P, need_argmax, grid, st);
+    else if (P.mom_set == kMomHQ)
+      launch_mom<DT, VEC, kMomHQ>(P, need_argmax, grid, st);
     else
-      hipLaunchKernelGGL((k_stats_mom<DT, VEC, false>), grid, dim3(kThreads), 0, st, P);
+      launch_mom<DT, VEC, kMomX | kMomHQ | kMomHP>(P, need_argmax, grid, st);
     if ((err = hipGetLastError()) != hipSuccess) return err;
   }
   if (e1 && (err = hipEventRecord(e1, st)) != hipSuccess) return err;
