@@ -57,7 +57,8 @@ def test_draft_sample_parity(cfg, T):
 
 
 @pytest.mark.parametrize("dtype,V", [("bf16", 2), ("bf16", 1001), ("bf16", 16385),
-                                     ("f32", 3), ("f32", 999), ("f32", 8193)])
+                                     ("f32", 3), ("f32", 999), ("f32", 8193),
+                                     ("bf16", 2000000), ("bf16", 1100001)])
 def test_draft_sample_ragged_and_masked(dtype, V):
     wl = W.WORKLOADS[3].with_(B=16, V=V, dtype=dtype)
     inp = W.generate(wl, 5, DEV)

@@ -627,3 +627,23 @@ def test_argmax_ties_lowest_index(dtype, V):
     sel = np.arange(wl.B) % 2 == 0
     np.testing.assert_array_equal(g2["argmax"][sel][..., 0], lq[sel])
     np.testing.assert_array_equal(g2["argmax"][sel][..., 1], lp[sel])
+
+
+# ------------------------------------------------- more than 64 tiles per row
+
+@pytest.mark.parametrize("dtype,V,rule,alpha", [
+    ("bf16", 600000, W.DIFF, 0.05),      # 74 tiles per row
+    ("bf16", 600001, W.OPT, 0.1),        # unaligned rows: 293 tiles, 3 groups of part loads
+    ("f32", 1100000, W.TOKEN_V3, 0.3),   # 269 tiles
+    ("bf16", 600000, W.DIFFLOG, 0.5),    # moments merged over 74 tiles
+])
+def test_large_vocabulary(dtype, V, rule, alpha):
+    """Rows of more than 64 statistics tiles: the merge takes several partials
+    per lane and the draw's part search loads several groups."""
+    wl = W.WORKLOADS[3].with_(B=3, gamma=3, V=V, dtype=dtype, rule=rule, alpha=alpha)
+    _flush(f"[large] {dtype} V={V} rule={rule}")
+    rep = parity.parity_workload(wl, 2, report_name=f"large.{dtype}.{V}.{rule}")
+    assert rep["sequences"] == 2 * wl.B
+    greedy = parity.parity_workload(wl.with_(temperature=0.0, cfg=4), 1,
+                                    report_name=f"large.{dtype}.{V}.{rule}.g")
+    assert greedy["sequences"] == wl.B
