@@ -1,0 +1,114 @@
+"""HIP graph capture of the library's calls: a verify step (and a drafter
+sampling step) captured once and replayed on new inputs copied into the
+captured buffers gives, on every replay, exactly what the eager call gives.
+Eager calls and synchronisations run between the replays.  The library's
+internal workspace is sized by an eager call before the capture, so the
+captured calls allocate nothing."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2405_19261_amd import spc
+from paper_2405_19261_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.init()
+    yield
+    torch.cuda.synchronize()
+
+
+def _host(t):
+    return [x.cpu().numpy() for x in t]
+
+
+@pytest.mark.parametrize("rule,alpha,T", [(W.DIFF, 0.05, 1.0), (W.OPT, 0.1, 0.7),
+                                          (W.TOKEN_V3, 0.3, 1.0), (W.BILD, 9.6, 1.0),
+                                          (W.CHOW, 0.4, 0.0)])
+def test_verify_graph_replays_match_eager(rule, alpha, T):
+    wl = W.WORKLOADS[3].with_(B=8, gamma=5, V=20000, rule=rule, alpha=alpha, temperature=T)
+    inputs = [W.generate(wl, s, DEV) for s in range(4)]
+    keys = ("q", "p", "draft", "uniforms")
+    greedy = T == 0.0
+
+    def call(inp, out=None):
+        if greedy:
+            return spc.spc_greedy_verify(inp["q"], inp["p"], inp["draft"], rule, alpha, out=out)
+        return spc.spc_verify(inp["q"], inp["p"], inp["draft"], inp["uniforms"], rule, alpha, T,
+                              out=out)
+
+    ref = []
+    for inp in inputs:  # eager results; the first call also sizes the workspace
+        r = call(inp)
+        torch.cuda.synchronize()
+        ref.append(_host(r))
+    static = {k: inputs[0][k].clone() for k in keys}
+    out = (torch.full((wl.B,), -9, dtype=torch.int32, device=DEV),
+           torch.full((wl.B,), -9, dtype=torch.int32, device=DEV),
+           torch.full((wl.B, wl.gamma + 1), 9, dtype=torch.uint8, device=DEV))
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # a warm-up call on the capture's stream
+        call(static, out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call(static, out)
+    torch.cuda.synchronize()
+    for rnd in range(2):
+        for i, inp in enumerate(inputs):
+            for k in keys:
+                static[k].copy_(inp[k])
+            for x in out:
+                x.fill_(7)
+            g.replay()
+            torch.cuda.synchronize()
+            got = _host(out)
+            for a, b in zip(got, ref[i]):
+                np.testing.assert_array_equal(a, b, err_msg=f"replay {rnd}.{i}")
+            # eager work between replays
+            e = call(inputs[(i + 1) % len(inputs)])
+            torch.cuda.synchronize()
+            for a, b in zip(_host(e), ref[(i + 1) % len(inputs)]):
+                np.testing.assert_array_equal(a, b)
+
+
+def test_draft_sample_graph_replays_match_eager():
+    wl = W.WORKLOADS[3].with_(B=16, V=30000)
+    rows = [W.generate(wl, s, DEV)["q"][:, 0].contiguous() for s in range(3)]
+    u = torch.rand(wl.B, generator=torch.Generator(device=DEV).manual_seed(3), device=DEV)
+    temps = torch.tensor([1.0, 0.0, 0.7, 2.0] * 4, device=DEV)
+    ref = []
+    for z in rows:
+        ref.append(spc.spc_draft_sample(z, 0.0, uniforms=u, temp_per_seq=temps).cpu().numpy())
+    torch.cuda.synchronize()
+    static = rows[0].clone()
+    out = torch.full((wl.B,), -9, dtype=torch.int32, device=DEV)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        spc.spc_draft_sample(static, 0.0, uniforms=u, temp_per_seq=temps, out=out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        spc.spc_draft_sample(static, 0.0, uniforms=u, temp_per_seq=temps, out=out)
+    torch.cuda.synchronize()
+    for rnd in range(3):
+        for i, z in enumerate(rows):
+            static.copy_(z)
+            out.fill_(-1)
+            g.replay()
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(out.cpu().numpy(), ref[i], err_msg=f"replay {rnd}.{i}")
+            e = spc.spc_draft_sample(rows[(i + 1) % 3], 0.0, uniforms=u, temp_per_seq=temps)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(e.cpu().numpy(), ref[(i + 1) % 3])
