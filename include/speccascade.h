@@ -59,6 +59,9 @@
 extern "C" {
 #endif
 
+/* Element type of the logit tensors.  Entry points take it as an int32_t
+ * `dtype` holding one of these values (any other value is rejected), so that
+ * an out-of-range value never reaches the library as an enum. */
 typedef enum { SPC_F32 = 0, SPC_BF16 = 1 } spc_dtype;
 
 /* Deferral rules of Table 1, two constant rules, and the token-specific rules
@@ -131,7 +134,7 @@ typedef enum {
  *   out_next_token      [B] int32: the token emitted at position t + j*
  *   out_defer_mask      [B][gamma+1] uint8: delta_j at every position
  */
-spc_status spc_verify(const void* q_logits, const void* p_logits, spc_dtype dtype,
+spc_status spc_verify(const void* q_logits, const void* p_logits, int32_t dtype,
                       const int32_t* draft_tokens, const float* uniforms, int32_t B,
                       int32_t gamma, int32_t V, int32_t rule, float alpha, float temperature,
                       int32_t* out_accept_len, int32_t* out_next_token,
@@ -146,7 +149,7 @@ spc_status spc_verify(const void* q_logits, const void* p_logits, spc_dtype dtyp
  * emitted token is that argmax at position j*.  No uniforms are used; the
  * result is a deterministic function of the inputs.
  */
-spc_status spc_greedy_verify(const void* q_logits, const void* p_logits, spc_dtype dtype,
+spc_status spc_greedy_verify(const void* q_logits, const void* p_logits, int32_t dtype,
                              const int32_t* draft_tokens, int32_t B, int32_t gamma, int32_t V,
                              int32_t rule, float alpha, int32_t* out_accept_len,
                              int32_t* out_next_token, uint8_t* out_defer_mask,
@@ -202,7 +205,7 @@ typedef struct {
 /* spc_verify with extended arguments; `ex` may be NULL.  `temperature`
  * applies where temp_per_seq is NULL and must then be > 0 (use
  * spc_greedy_verify for a batch-wide temperature 0). */
-spc_status spc_verify_ex(const void* q_logits, const void* p_logits, spc_dtype dtype,
+spc_status spc_verify_ex(const void* q_logits, const void* p_logits, int32_t dtype,
                          const int32_t* draft_tokens, const float* uniforms, int32_t B,
                          int32_t gamma, int32_t V, int32_t rule, float alpha, float temperature,
                          int32_t* out_accept_len, int32_t* out_next_token,
@@ -227,17 +230,17 @@ spc_status spc_verify_ex(const void* q_logits, const void* p_logits, spc_dtype d
  * negative or non-finite temperature is SPC_E_PARAM, an invalid per-sequence
  * one gives out_token = -1.
  */
-spc_status spc_draft_sample(const void* logits, spc_dtype dtype, int32_t B, int32_t V,
+spc_status spc_draft_sample(const void* logits, int32_t dtype, int32_t B, int32_t V,
                             float temperature, const float* temp_per_seq,
                             const float* uniforms, int32_t* out_token, hipStream_t stream);
 
 /* Bytes of device workspace one call of this shape needs. */
-size_t spc_workspace_bytes(int32_t B, int32_t gamma, int32_t V, spc_dtype dtype);
+size_t spc_workspace_bytes(int32_t B, int32_t gamma, int32_t V, int32_t dtype);
 
 /* Leading bytes of a workspace that must be zero before its first use
  * (completion counters at fixed offsets: the same for every shape, so one
  * zeroed workspace serves calls of any shape it is large enough for). */
-size_t spc_workspace_zero_bytes(int32_t B, int32_t gamma, int32_t V, spc_dtype dtype);
+size_t spc_workspace_zero_bytes(int32_t B, int32_t gamma, int32_t V, int32_t dtype);
 
 /* Thread-local description of the last non-OK status ("" if none). */
 const char* spc_last_error(void);

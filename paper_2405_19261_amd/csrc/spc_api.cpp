@@ -146,7 +146,7 @@ spc_status internal_workspace(const spc::WsLayout& L, hipStream_t stream, char**
   return SPC_OK;
 }
 
-spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int32_t* draft,
+spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_t* draft,
                        const float* uniforms, int32_t B, int32_t gamma, int32_t V, int32_t rule,
                        float alpha, float temperature, bool force_greedy, int32_t* out_accept,
                        int32_t* out_token, uint8_t* out_defer, const spc_verify_ex_args* ex,
@@ -277,7 +277,7 @@ spc_status verify_impl(const void* q, const void* p, spc_dtype dtype, const int3
 
 extern "C" {
 
-spc_status spc_verify(const void* q_logits, const void* p_logits, spc_dtype dtype,
+spc_status spc_verify(const void* q_logits, const void* p_logits, int32_t dtype,
                       const int32_t* draft_tokens, const float* uniforms, int32_t B,
                       int32_t gamma, int32_t V, int32_t rule, float alpha, float temperature,
                       int32_t* out_accept_len, int32_t* out_next_token,
@@ -287,7 +287,7 @@ spc_status spc_verify(const void* q_logits, const void* p_logits, spc_dtype dtyp
                      nullptr, stream);
 }
 
-spc_status spc_greedy_verify(const void* q_logits, const void* p_logits, spc_dtype dtype,
+spc_status spc_greedy_verify(const void* q_logits, const void* p_logits, int32_t dtype,
                              const int32_t* draft_tokens, int32_t B, int32_t gamma, int32_t V,
                              int32_t rule, float alpha, int32_t* out_accept_len,
                              int32_t* out_next_token, uint8_t* out_defer_mask,
@@ -296,7 +296,7 @@ spc_status spc_greedy_verify(const void* q_logits, const void* p_logits, spc_dty
                      0.0f, true, out_accept_len, out_next_token, out_defer_mask, nullptr, stream);
 }
 
-spc_status spc_verify_ex(const void* q_logits, const void* p_logits, spc_dtype dtype,
+spc_status spc_verify_ex(const void* q_logits, const void* p_logits, int32_t dtype,
                          const int32_t* draft_tokens, const float* uniforms, int32_t B,
                          int32_t gamma, int32_t V, int32_t rule, float alpha, float temperature,
                          int32_t* out_accept_len, int32_t* out_next_token,
@@ -307,7 +307,7 @@ spc_status spc_verify_ex(const void* q_logits, const void* p_logits, spc_dtype d
                      stream);
 }
 
-spc_status spc_draft_sample(const void* logits, spc_dtype dtype, int32_t B, int32_t V,
+spc_status spc_draft_sample(const void* logits, int32_t dtype, int32_t B, int32_t V,
                             float temperature, const float* temp_per_seq,
                             const float* uniforms, int32_t* out_token, hipStream_t stream) {
   g_err.clear();
@@ -351,12 +351,12 @@ spc_status spc_draft_sample(const void* logits, spc_dtype dtype, int32_t B, int3
   return SPC_OK;
 }
 
-size_t spc_workspace_bytes(int32_t B, int32_t gamma, int32_t V, spc_dtype dtype) {
+size_t spc_workspace_bytes(int32_t B, int32_t gamma, int32_t V, int32_t dtype) {
   if (check_shape(B, gamma, V) != SPC_OK || (dtype != SPC_F32 && dtype != SPC_BF16)) return 0;
   return spc::ws_layout(B, gamma, V, dtype, vec_path(dtype, V)).total;
 }
 
-size_t spc_workspace_zero_bytes(int32_t B, int32_t gamma, int32_t V, spc_dtype dtype) {
+size_t spc_workspace_zero_bytes(int32_t B, int32_t gamma, int32_t V, int32_t dtype) {
   if (check_shape(B, gamma, V) != SPC_OK || (dtype != SPC_F32 && dtype != SPC_BF16)) return 0;
   return spc::ws_layout(B, gamma, V, dtype, vec_path(dtype, V)).zero_end;
 }
