@@ -90,7 +90,13 @@ def spec_decode(drafter, verifier, first_tokens, rounds, gamma, rule, alpha, tem
     ``alpha`` and ``temperature`` are scalars or [B] tensors (temperature 0:
     greedy).  Uniforms come from a torch.Generator seeded with ``seed``;
     ``rounds_inputs`` (a list), when given, receives each round's inputs so a
-    test can replay them through another backend."""
+    test can replay them through another backend.
+
+    The rounds run without waiting for the device: emitted tokens are
+    scattered into a device buffer (a round writes its gamma+1 candidates at
+    the sequence's length and advances the length by j* + 1, so the
+    candidates past j* are overwritten by the next round), and the host reads
+    the buffer and the accept lengths once, after the last round."""
     backend = backend or GpuBackend()
     dev = verifier.device
     B = first_tokens.numel()
@@ -104,13 +110,16 @@ def spec_decode(drafter, verifier, first_tokens, rounds, gamma, rule, alpha, tem
     alpha_t = per_seq(alpha, torch.float32)
     temp_t = per_seq(temperature, torch.float32)
     gen = torch.Generator(device=dev).manual_seed(seed)
+    # round state, updated in place by every round
     last = first_tokens.to(dev, torch.int32).clone()
     pos = torch.zeros(B, dtype=torch.int64, device=dev)
-    out = [[] for _ in range(B)]
-    res = DecodeResult(tokens=out)
-    for _ in range(rounds):
+    buf = torch.zeros(B, rounds * g1 + g1, dtype=torch.int32, device=dev)
+    length = torch.zeros(B, dtype=torch.int64, device=dev)
+    acc_out = torch.zeros(B, dtype=torch.int64, device=dev)
+    ar = torch.arange(g1, device=dev)
+
+    def one_round(u_draft, u):
         # 1. draft gamma tokens from q, and q's logits at the extra position
-        u_draft = torch.rand(gamma, B, generator=gen, device=dev)
         q_rows, drafts = [], []
         tok = last
         for j in range(g1):
@@ -123,25 +132,40 @@ def spec_decode(drafter, verifier, first_tokens, rounds, gamma, rule, alpha, tem
         x = torch.stack(drafts, dim=1).to(torch.int32).contiguous()  # [B, gamma]
         # 2. score the gamma+1 prefixes with p in one batch
         ctx = torch.cat([last[:, None], x], dim=1)             # last tokens of x_{<t+j}
-        p = verifier(ctx.reshape(-1), (pos[:, None] + torch.arange(g1, device=dev)).reshape(-1))
+        p = verifier(ctx.reshape(-1), (pos[:, None] + ar).reshape(-1))
         p = p.reshape(B, g1, -1).contiguous()
         # 3. verify
-        u = torch.rand(B, g1, generator=gen, device=dev)
         if rounds_inputs is not None:
             rounds_inputs.append(dict(q=q, p=p, draft=x, uniforms=u, u_draft=u_draft,
                                       rule=rule_t, alpha=alpha_t, temperature=temp_t))
         acc, nxt = backend.verify(q, p, x, u, rule_t, alpha_t, temp_t)
-        # 4. emit and roll back to t + j* + 1
-        acc_h, nxt_h, x_h = acc.cpu(), nxt.cpu(), x.cpu()
-        for b in range(B):
-            j = int(acc_h[b])
-            if j < 0:
-                raise RuntimeError(f"sequence {b}: invalid parameters (accept_len {j})")
-            out[b].extend(int(t) for t in x_h[b, :j])
-            out[b].append(int(nxt_h[b]))
-        res.accept_len.append(acc_h)
-        last = nxt.to(torch.int32)
-        pos = pos + acc.long() + 1
+        # 4. emit x_t .. x_{t+j*-1} and the new token, roll back to t + j* + 1
+        acc = acc.to(dev).long()
+        nxt = nxt.to(dev, torch.int32)
+        j = acc.clamp(min=0)
+        cand = torch.cat([x, nxt[:, None]], dim=1)
+        cand = torch.where(ar[None, :] == j[:, None], nxt[:, None], cand)
+        buf.scatter_(1, length[:, None] + ar[None, :], cand)
+        length.add_(j + 1)
+        pos.add_(j + 1)
+        last.copy_(nxt)
+        acc_out.copy_(acc)
+
+    def uniforms():
+        return (torch.rand(gamma, B, generator=gen, device=dev),
+                torch.rand(B, g1, generator=gen, device=dev))
+
+    accs = torch.zeros(rounds, B, dtype=torch.int64, device=dev)
+    for r in range(rounds):
+        one_round(*uniforms())
+        accs[r].copy_(acc_out)
+    acc_h = accs.cpu()
+    bad = (acc_h < 0).nonzero()
+    if bad.numel():
+        raise RuntimeError(f"sequence {int(bad[0, 1])}: invalid parameters (accept_len -1)")
+    buf_h, len_h = buf.cpu(), length.cpu()
+    res = DecodeResult(tokens=[buf_h[b, :int(len_h[b])].tolist() for b in range(B)])
+    res.accept_len = [a.to(torch.int32) for a in acc_h]
     return res
 
 
