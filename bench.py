@@ -44,6 +44,7 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, published
 KERNEL_SRC = os.path.join(ROOT, "paper_2405_19261_amd", "csrc", "spc_kernels.hip")
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_stats_gemma-vocab_b32_g7_traffic.txt")
+MALL_BYTES = 256 << 20  # MI355X Infinity Cache
 COPY_KERNEL_TAG = "neg_kernel"  # the calibration copy is torch.neg
 
 
@@ -367,6 +368,9 @@ def main():
                     algorithmic_bytes_per_step=wl.algorithmic_bytes(),
                     path_gbps=wl.algorithmic_bytes() / (ms_per_step / 1e3) / 1e9,
                     input_sets=len(sets), wall_s=wall,
+                    cache=("cold: the rotated input sets exceed twice the 256 MB Infinity Cache"
+                           if len(sets) * wl.logit_bytes() > 2 * MALL_BYTES else
+                           "hot: every input set fits in the 256 MB Infinity Cache"),
                     step_us_p10_p50_p90=[None if pct(windows, q) is None else pct(windows, q) * 1e3
                                          for q in (0.1, 0.5, 0.9)],
                     step_us_windows=f"{len(windows)} windows of {every} steps"),
