@@ -283,7 +283,7 @@ def main():
         wl = wl.with_(rule=rule, alpha=wl.alpha if args.alpha is None else args.alpha)
     rule_desc = (f"{W.RULE_NAMES[wl.rule]} alpha={wl.alpha:g}" if wl.rule in W.RULE_NAMES
                  else "per-sequence rules")
-    per_seq = args.cfg in (4, 5)  # greedy / mixed batches: per-sequence arrays
+    per_seq = args.cfg == 5  # the mixed batch: per-sequence arrays
     # the rules the per-sequence arrays hold (the library skips passes for the others)
     rule_mask = (sum(1 << r for r, _ in W.CFG5_RULES) if args.cfg == 5 else 1 << wl.rule) \
         if per_seq else 0
@@ -319,10 +319,13 @@ def main():
                               rule_per_seq=s["rule"], alpha_per_seq=s["alpha"],
                               temp_per_seq=temp, ev_hot_begin=ev0, ev_hot_end=ev1,
                               rules_present=rule_mask, out=outs[i % len(sets)], stream=stream)
+        elif events is None and wl.greedy:
+            spc.spc_greedy_verify(s["q"], s["p"], s["draft"], wl.rule, wl.alpha,
+                                  out=outs[i % len(sets)], stream=stream)
         elif events is None:
             spc.spc_verify(s["q"], s["p"], s["draft"], s["uniforms"], wl.rule, wl.alpha,
                            wl.temperature, out=outs[i % len(sets)], stream=stream)
-        else:
+        else:  # the same step with timing events (temperature 0: the greedy step)
             spc.spc_verify_ex(s["q"], s["p"], s["draft"], s["uniforms"], wl.rule, wl.alpha,
                               wl.temperature, ev_hot_begin=events[0], ev_hot_end=events[1],
                               out=outs[i % len(sets)], stream=stream)

@@ -203,8 +203,9 @@ typedef struct {
 } spc_verify_ex_args;
 
 /* spc_verify with extended arguments; `ex` may be NULL.  `temperature`
- * applies where temp_per_seq is NULL and must then be > 0 (use
- * spc_greedy_verify for a batch-wide temperature 0). */
+ * applies where temp_per_seq is NULL.  There it must be > 0, or exactly 0 for
+ * the batch-wide greedy step of spc_greedy_verify (uniforms may then be
+ * NULL), which this entry point then runs with its optional outputs. */
 spc_status spc_verify_ex(const void* q_logits, const void* p_logits, int32_t dtype,
                          const int32_t* draft_tokens, const float* uniforms, int32_t B,
                          int32_t gamma, int32_t V, int32_t rule, float alpha, float temperature,

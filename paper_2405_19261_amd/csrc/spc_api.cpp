@@ -302,8 +302,11 @@ spc_status spc_verify_ex(const void* q_logits, const void* p_logits, int32_t dty
                          int32_t* out_accept_len, int32_t* out_next_token,
                          uint8_t* out_defer_mask, const spc_verify_ex_args* ex,
                          hipStream_t stream) {
+  // a scalar temperature of exactly 0 (no per-sequence array) is the
+  // batch-wide greedy step of spc_greedy_verify
+  const bool greedy = !(ex && ex->temp_per_seq) && temperature == 0.0f;
   return verify_impl(q_logits, p_logits, dtype, draft_tokens, uniforms, B, gamma, V, rule, alpha,
-                     temperature, false, out_accept_len, out_next_token, out_defer_mask, ex,
+                     temperature, greedy, out_accept_len, out_next_token, out_defer_mask, ex,
                      stream);
 }
 

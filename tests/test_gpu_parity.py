@@ -647,3 +647,21 @@ def test_large_vocabulary(dtype, V, rule, alpha):
     greedy = parity.parity_workload(wl.with_(temperature=0.0, cfg=4), 1,
                                     report_name=f"large.{dtype}.{V}.{rule}.g")
     assert greedy["sequences"] == wl.B
+
+
+def test_verify_ex_scalar_temperature_zero_is_greedy_step():
+    """spc_verify_ex with a scalar temperature of 0 runs spc_greedy_verify's
+    step (uniforms not needed) and fills the optional outputs."""
+    wl = W.WORKLOADS[4].with_(B=16, V=30000)
+    inp = W.generate(wl, 3, DEV)
+    a = spc.spc_greedy_verify(inp["q"], inp["p"], inp["draft"], wl.rule, wl.alpha)
+    stats = torch.full((wl.B, wl.gamma + 1, 8), float("nan"), device=DEV)
+    am = torch.full((wl.B, wl.gamma + 1, 2), -7, dtype=torch.int32, device=DEV)
+    b = spc.spc_verify_ex(inp["q"], inp["p"], inp["draft"], None, wl.rule, wl.alpha, 0.0,
+                          out_row_stats=stats, out_argmax=am)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x.cpu().numpy(), y.cpu().numpy())
+    g = parity.run_gpu(inp, greedy=True)  # per-sequence zero temperatures
+    np.testing.assert_array_equal(am.cpu().numpy(), g["argmax"])
+    np.testing.assert_allclose(stats.cpu().numpy(), g["row_stats"], rtol=0, atol=0)
