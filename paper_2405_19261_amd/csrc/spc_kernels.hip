@@ -1382,13 +1382,6 @@ __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, cons
   if constexpr (ARGMAX && !MOM) {
     iq = first_max_index<DT, VEC, T::U, kThreads>(wq, gq, mq, base);
     ip = first_max_index<DT, VEC, T::U, kThreads>(wp, gp, mp, base);
-    // The packed words stay live for the selection above: the sums unpack
-    // them again instead of holding every unpacked entry as well.
-#pragma unroll
-    for (int i = 0; i < T::U; ++i)
-#pragma unroll
-      for (int j = 0; j < T::NW; ++j)
-        asm volatile("" : "+v"(const_cast<uint32_t&>(wq[i][j])), "+v"(const_cast<uint32_t&>(wp[i][j])));
   }
   const float rq = (mq == kNegInf) ? 0.0f : mq * sp.c_hi;
   const float rp = (mp == kNegInf) ? 0.0f : mp * sp.c_hi;
