@@ -220,7 +220,9 @@ spc_status spc_verify_ex(const void* q_logits, const void* p_logits, int32_t dty
  *   logits        [B][V] drafter logits, `dtype`, rows contiguous
  *   temperature   T for every sequence (T = 0: the argmax of the raw logits,
  *                 lowest index on a tie), unless temp_per_seq is given
- *   temp_per_seq  [B] float32 per-sequence temperatures, or NULL
+ *   temp_per_seq  [B] float32 per-sequence temperatures, or NULL; a row
+ *                 whose temperature is negative or not finite gets
+ *                 out_token = -1
  *   uniforms      [B] float32 in [0,1): the token is the smallest k whose
  *                 cumulative mass (vocabulary order) exceeds u times the
  *                 total; may be NULL when every temperature is 0

@@ -116,3 +116,20 @@ def test_greedy_decode_loop_equals_oracle_loop(rule, alpha):
     assert a.tokens == b.tokens
     for x, y in zip(a.accept_len, b.accept_len):
         np.testing.assert_array_equal(x.numpy(), y.cpu().numpy())
+
+
+def test_draft_sample_invalid_row_temperatures():
+    """A per-row temperature that is negative or not finite gives that row
+    token -1; the other rows draw as with valid temperatures alone."""
+    wl = W.WORKLOADS[3].with_(B=8, V=30000)
+    z = W.generate(wl, 6, DEV)["q"][:, 0].contiguous()
+    u = torch.rand(8, generator=torch.Generator(device=DEV).manual_seed(6), device=DEV)
+    temps = torch.tensor([1.0, float("nan"), 0.7, -1.0, 0.0, float("inf"), 2.0, 1.0],
+                         device=DEV)
+    tok = spc.spc_draft_sample(z, 0.0, uniforms=u, temp_per_seq=temps).cpu().numpy()
+    bad = [1, 3, 5]
+    assert (tok[bad] == -1).all()
+    ok = [b for b in range(8) if b not in bad]
+    t_ok = temps[ok].cpu().numpy()
+    o_tok, o_mg = oracle.draft_sample(_host(z[ok]), t_ok, u[ok].cpu().numpy())
+    _check_tokens(tok[ok], o_tok, o_mg, {"draws": 0, "excused": 0})
