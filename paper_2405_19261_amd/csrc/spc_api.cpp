@@ -339,9 +339,14 @@ spc_status spc_draft_sample(const void* logits, int32_t dtype, int32_t B, int32_
   P.B = B;
   P.gamma = 0;
   P.V = V;
-  // the drafter kernel's tiles are twice as long (fewer partials than the
-  // workspace holds for this shape)
-  P.nt = (int32_t)((V + spc::draft_tile_elems(dtype, vec) - 1) / spc::draft_tile_elems(dtype, vec));
+  // Tiles twice as long as the statistics tiles once that still gives at
+  // least 4 workgroups per CU; small batches take the statistics tile
+  // length, for twice the workgroups (either way no more partials per row
+  // than the workspace holds for this shape).
+  const int64_t long_n = spc::draft_tile_elems(dtype, vec, true);
+  const bool long_tiles = (int64_t)B * ((V + long_n - 1) / long_n) >= 1024;
+  const int64_t tile_n = long_tiles ? long_n : spc::draft_tile_elems(dtype, vec, false);
+  P.nt = (int32_t)((V + tile_n - 1) / tile_n);
   P.rule = SPC_RULE_NEVER;
   P.temp = greedy ? 0.0f : temperature;
   P.force_greedy = greedy ? 1 : 0;
@@ -349,7 +354,8 @@ spc_status spc_draft_sample(const void* logits, int32_t dtype, int32_t B, int32_
   P.out_token = out_token;
   P.samp_cnt = reinterpret_cast<uint32_t*>(ws + L.draft_cnt);
   P.tiles = reinterpret_cast<spc::TilePart*>(ws + L.tiles);
-  const hipError_t e = spc::launch_draft(P, dtype, vec, greedy || temp_per_seq, stream);
+  const hipError_t e =
+      spc::launch_draft(P, dtype, vec, greedy || temp_per_seq, long_tiles, stream);
   if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
   return SPC_OK;
 }

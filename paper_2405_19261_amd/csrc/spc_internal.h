@@ -93,7 +93,7 @@ struct Params {
 // path, and sampling workgroups per sequence for a row of nc chunks in a batch
 // of B sequences on a device of `cus` compute units.
 int stat_tile_elems(int dtype, bool vec);
-int draft_tile_elems(int dtype, bool vec);
+int draft_tile_elems(int dtype, bool vec, bool long_tiles);
 int samp_chunk_elems(int dtype, bool vec);
 int samp_groups(int64_t nc, int B, int cus);
 
@@ -120,7 +120,10 @@ int res_blocks_per_cu(int dtype, bool vec, bool argmax);
 // Enqueue the drafter sampling kernel (Params: q = the logits [B][V], nt,
 // uniforms [B], temp_ps or temp, out_token, samp_cnt with kDraftCntStride,
 // tiles).  argmax: some row may be at temperature 0.
-hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, hipStream_t stream);
+// long_tiles: tiles of twice the statistics tile's lane loads (large
+// batches) rather than the statistics tile's (small ones).
+hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, bool long_tiles,
+                        hipStream_t stream);
 
 // Second passes a batch may need (bits of tv_kinds): D_TV of OPT and OPTLOG
 // rows, eta of token-rule rows, each at temperature > 0.

@@ -62,10 +62,11 @@ struct Tile {
 template <int DT, bool VEC>
 using StatTile = Tile<DT, VEC, VEC ? 4 : 8>;
 
-// drafter tiles: one tensor, so twice the lane loads of a statistics tile
-// (the same bytes per workgroup)
-template <int DT, bool VEC>
-using DraftTile = Tile<DT, VEC, 2 * StatTile<DT, VEC>::U>;
+// drafter tiles: one tensor, M times the lane loads of a statistics tile
+// (M = 2: the same bytes per workgroup, for large batches; M = 1: twice the
+// workgroups, for small ones)
+template <int DT, bool VEC, int M>
+using DraftTile = Tile<DT, VEC, M * StatTile<DT, VEC>::U>;
 
 // bfloat16 -> float32 is exact: the bf16 bits are the top half of the float.
 template <int DT, bool VEC>
@@ -1830,9 +1831,9 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
 // masses give the tile where u W falls, then the tile's sub-chunks and
 // lanes are scanned in vocabulary order.  A greedy row (temperature 0)
 // takes the lowest index attaining its max instead.
-template <int DT, bool VEC, bool ARGMAX>
+template <int DT, bool VEC, bool ARGMAX, int TM>
 __global__ __launch_bounds__(kThreads) void k_draft(Params P) {
-  using T = DraftTile<DT, VEC>;
+  using T = DraftTile<DT, VEC, TM>;
   __shared__ Shared sh;
   __shared__ RowStat srow;
   __shared__ PickState pks;
@@ -1962,13 +1963,13 @@ __global__ __launch_bounds__(kThreads) void k_draft(Params P) {
                                        sh);
 }
 
-template <int DT, bool VEC>
+template <int DT, bool VEC, int TM>
 hipError_t launch_draft_t(const Params& P, bool argmax, hipStream_t st) {
   const dim3 grid(P.nt, P.B);
   if (argmax)
-    hipLaunchKernelGGL((k_draft<DT, VEC, true>), grid, dim3(kThreads), 0, st, P);
+    hipLaunchKernelGGL((k_draft<DT, VEC, true, TM>), grid, dim3(kThreads), 0, st, P);
   else
-    hipLaunchKernelGGL((k_draft<DT, VEC, false>), grid, dim3(kThreads), 0, st, P);
+    hipLaunchKernelGGL((k_draft<DT, VEC, false, TM>), grid, dim3(kThreads), 0, st, P);
   return hipGetLastError();
 }
 
@@ -2045,9 +2046,13 @@ int stat_tile_elems(int dtype, bool vec) {
   return vec ? StatTile<0, true>::N : StatTile<0, false>::N;
 }
 
-int draft_tile_elems(int dtype, bool vec) {
-  if (dtype == 1) return vec ? DraftTile<1, true>::N : DraftTile<1, false>::N;
-  return vec ? DraftTile<0, true>::N : DraftTile<0, false>::N;
+int draft_tile_elems(int dtype, bool vec, bool long_tiles) {
+  if (long_tiles) {
+    if (dtype == 1) return vec ? DraftTile<1, true, 2>::N : DraftTile<1, false, 2>::N;
+    return vec ? DraftTile<0, true, 2>::N : DraftTile<0, false, 2>::N;
+  }
+  if (dtype == 1) return vec ? DraftTile<1, true, 1>::N : DraftTile<1, false, 1>::N;
+  return vec ? DraftTile<0, true, 1>::N : DraftTile<0, false, 1>::N;
 }
 
 int samp_chunk_elems(int dtype, bool vec) {
@@ -2065,10 +2070,19 @@ int samp_groups(int64_t nc, int B, int cus) {
   return (int)(k < 1 ? 1 : k);
 }
 
-hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, hipStream_t st) {
+hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, bool long_tiles,
+                        hipStream_t st) {
+  if (long_tiles) {
+    if (dtype == 1)
+      return vec ? launch_draft_t<1, true, 2>(P, argmax, st)
+                 : launch_draft_t<1, false, 2>(P, argmax, st);
+    return vec ? launch_draft_t<0, true, 2>(P, argmax, st)
+               : launch_draft_t<0, false, 2>(P, argmax, st);
+  }
   if (dtype == 1)
-    return vec ? launch_draft_t<1, true>(P, argmax, st) : launch_draft_t<1, false>(P, argmax, st);
-  return vec ? launch_draft_t<0, true>(P, argmax, st) : launch_draft_t<0, false>(P, argmax, st);
+    return vec ? launch_draft_t<1, true, 1>(P, argmax, st)
+               : launch_draft_t<1, false, 1>(P, argmax, st);
+  return vec ? launch_draft_t<0, true, 1>(P, argmax, st) : launch_draft_t<0, false, 1>(P, argmax, st);
 }
 
 hipError_t launch_verify(const Params& P, int dtype, bool vec, int tv_kinds, bool need_sample,
