@@ -76,6 +76,21 @@ def test_draft_sample_ragged_and_masked(dtype, V):
         assert not m.gather(1, tok.long()[:, None]).any()  # never a masked token
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_draft_sample_maximum_rows(dtype):
+    """The drafter at its row limit (32767 rows)."""
+    B = 32767
+    wl = W.WORKLOADS[3].with_(B=B, gamma=1, V=41, dtype=dtype)
+    z = W.generate(wl, 9, DEV)["q"][:, 0].contiguous()
+    g = torch.Generator(device=DEV).manual_seed(9)
+    u = torch.rand(B, generator=g, device=DEV)
+    for T in (1.0, 0.0):
+        tok = spc.spc_draft_sample(z, T, uniforms=u)
+        torch.cuda.synchronize()
+        o_tok, o_mg = oracle.draft_sample(_host(z), np.full(B, T, np.float32), u.cpu().numpy())
+        _check_tokens(tok.cpu().numpy(), o_tok, o_mg, {"draws": 0, "excused": 0})
+
+
 def test_decode_loop_rounds_match_oracle():
     """Every round of the GPU loop, replayed through the oracle on the same
     inputs: the drafts are the oracle's draws from the drafter rows, and the

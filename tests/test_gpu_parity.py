@@ -109,6 +109,15 @@ def test_block_size_extremes(gamma, B):
     parity.parity_workload(wl.with_(temperature=0.0, cfg=4), 2, report_name=f"gamma{gamma}.g")
 
 
+@pytest.mark.parametrize("dtype,rule,alpha", [("bf16", W.DIFF, 0.05), ("f32", W.OPT, 0.1)])
+def test_maximum_rows(dtype, rule, alpha):
+    """B*(gamma+1) at the library's row limit (65535 = the grid's y extent)."""
+    wl = W.WORKLOADS[3].with_(B=13107, gamma=4, V=37, dtype=dtype, rule=rule, alpha=alpha)
+    _flush(f"[edge] maximum rows {dtype} rule={rule}")
+    parity.parity_workload(wl, 1, report_name=f"maxrows.{dtype}")
+    parity.parity_workload(wl.with_(temperature=0.0, cfg=4), 1, report_name=f"maxrows.{dtype}.g")
+
+
 def test_identical_models_accept_all():
     wl = W.WORKLOADS[3].with_(B=16, V=20000)
     for rule, alpha in ((W.DIFF, 0.0), (W.OPT, 0.1), (W.ALWAYS, 0.0), (W.CHOW, 0.3)):
