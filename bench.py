@@ -219,7 +219,8 @@ def bench_decode(args, wl, dev):
     dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     q_lm, p_lm = decode.synthetic_pair(wl.V, seed=1, dtype=dt, device=dev)
     first = torch.randint(0, wl.V, (wl.B,), generator=torch.Generator().manual_seed(0))
-    kw = dict(gamma=wl.gamma, rule=wl.rule, alpha=wl.alpha, temperature=wl.temperature)
+    kw = dict(gamma=wl.gamma, rule=wl.rule, alpha=wl.alpha, temperature=wl.temperature,
+              graph=args.graph)
     decode.spec_decode(q_lm, p_lm, first, rounds=2, seed=5, **kw)  # warm-up
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -234,7 +235,9 @@ def bench_decode(args, wl, dev):
         tokens_per_round=res.tokens_per_round(),
         config=dict(workload=f"decoding loop: B={wl.B} gamma={wl.gamma} V={wl.V} {wl.dtype}, "
                              f"rule {wl.rule} alpha={wl.alpha:g} T={wl.temperature}; "
-                             "synthetic Markov drafter/verifier (table lookups)"))), flush=True)
+                             "synthetic Markov drafter/verifier (table lookups)"
+                             + ("; one HIP graph replay per round (capture included)"
+                                if args.graph else "")))), flush=True)
     return 0
 
 
@@ -262,6 +265,8 @@ def main():
     ap.add_argument("--decode", type=int, default=0, metavar="ROUNDS",
                     help="time ROUNDS rounds of the decoding loop (decode.py) on synthetic "
                          "models of the workload's shape")
+    ap.add_argument("--graph", action="store_true",
+                    help="with --decode: capture one round into a HIP graph and replay it")
     args = ap.parse_args()
     if args.traffic_from:
         if args.copy_calib_mb <= 0:

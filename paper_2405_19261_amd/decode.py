@@ -61,14 +61,39 @@ class SyntheticLM:
 
 
 class GpuBackend:
-    """Sampling and verification through libspeccascade."""
+    """Sampling and verification through libspeccascade.
+
+    ``prepare`` (called once by ``spec_decode`` before the rounds) reads the
+    per-sequence parameters on the host.  When every sequence shares one
+    rule, alpha and temperature the calls take the scalar forms, so the
+    library launches only the kernels that rule needs (no argmax at T > 0);
+    otherwise the per-sequence arrays go with the ``rules_present`` mask of
+    the rules they hold."""
+
+    def __init__(self):
+        self._scalar = None
+        self._rules_present = 0
+
+    def prepare(self, rule, alpha, temperature):
+        r, a, t = rule.cpu(), alpha.cpu(), temperature.cpu()
+        self._rules_present = sum(1 << int(x) for x in set(r.tolist()) if 0 <= x < 31)
+        same = bool((r == r[0]).all() and (a == a[0]).all() and (t == t[0]).all())
+        self._scalar = (int(r[0]), float(a[0]), float(t[0])) if same else None
 
     def draft_sample(self, logits, temperature, uniforms):
+        if self._scalar is not None:
+            T = self._scalar[2]
+            return spc.spc_draft_sample(logits, T, uniforms=uniforms if T > 0 else None)
         return spc.spc_draft_sample(logits, 0.0, uniforms=uniforms, temp_per_seq=temperature)
 
     def verify(self, q, p, drafts, uniforms, rule, alpha, temperature):
-        acc, tok, _ = spc.spc_verify_ex(q, p, drafts, uniforms, 0, 0.0, 1.0, rule_per_seq=rule,
-                                        alpha_per_seq=alpha, temp_per_seq=temperature)
+        if self._scalar is not None:
+            acc, tok, _ = spc.spc_verify_ex(q, p, drafts, uniforms, *self._scalar)
+        else:
+            acc, tok, _ = spc.spc_verify_ex(q, p, drafts, uniforms, 0, 0.0, 1.0,
+                                            rule_per_seq=rule, alpha_per_seq=alpha,
+                                            temp_per_seq=temperature,
+                                            rules_present=self._rules_present)
         return acc, tok
 
 
@@ -84,7 +109,7 @@ class DecodeResult:
 
 
 def spec_decode(drafter, verifier, first_tokens, rounds, gamma, rule, alpha, temperature,
-                seed=0, backend=None, rounds_inputs=None):
+                seed=0, backend=None, rounds_inputs=None, graph=False):
     """Run ``rounds`` rounds of GenSpecSample for B sequences whose last
     prefix token is ``first_tokens`` [B] (at position 0).  ``rule``,
     ``alpha`` and ``temperature`` are scalars or [B] tensors (temperature 0:
@@ -96,8 +121,19 @@ def spec_decode(drafter, verifier, first_tokens, rounds, gamma, rule, alpha, tem
     scattered into a device buffer (a round writes its gamma+1 candidates at
     the sequence's length and advances the length by j* + 1, so the
     candidates past j* are overwritten by the next round), and the host reads
-    the buffer and the accept lengths once, after the last round."""
+    the buffer and the accept lengths once, after the last round.
+
+    ``graph=True`` captures one round (the 2*gamma+1 model and sampling calls,
+    the verification and the emission) into a HIP graph and replays it once
+    per round, so a round costs one launch instead of dozens.  The round's
+    uniforms are drawn up front in the eager order and copied into the
+    graph's input buffers before each replay, so the tokens equal the eager
+    loop's.  The models and the backend must be capturable (no host syncs,
+    no allocation outside torch's allocator); one eager round, whose effects
+    are undone, sizes the library's workspace before the capture."""
     backend = backend or GpuBackend()
+    if graph and rounds_inputs is not None:
+        raise ValueError("rounds_inputs needs the eager loop (graph=False)")
     dev = verifier.device
     B = first_tokens.numel()
     g1 = gamma + 1
@@ -109,6 +145,8 @@ def spec_decode(drafter, verifier, first_tokens, rounds, gamma, rule, alpha, tem
     rule_t = per_seq(rule, torch.int32)
     alpha_t = per_seq(alpha, torch.float32)
     temp_t = per_seq(temperature, torch.float32)
+    if hasattr(backend, "prepare"):
+        backend.prepare(rule_t, alpha_t, temp_t)
     gen = torch.Generator(device=dev).manual_seed(seed)
     # round state, updated in place by every round
     last = first_tokens.to(dev, torch.int32).clone()
@@ -156,9 +194,35 @@ def spec_decode(drafter, verifier, first_tokens, rounds, gamma, rule, alpha, tem
                 torch.rand(B, g1, generator=gen, device=dev))
 
     accs = torch.zeros(rounds, B, dtype=torch.int64, device=dev)
-    for r in range(rounds):
-        one_round(*uniforms())
-        accs[r].copy_(acc_out)
+    if graph:
+        drawn = [uniforms() for _ in range(rounds)]
+        ud_in, u_in = torch.empty_like(drawn[0][0]), torch.empty_like(drawn[0][1])
+        # warm-up on a side stream (the library sizes its workspace here);
+        # the round state is restored afterwards
+        state = [t.clone() for t in (last, pos, buf, length, acc_out)]
+        side = torch.cuda.Stream(device=dev)
+        side.wait_stream(torch.cuda.current_stream(dev))
+        with torch.cuda.stream(side):
+            ud_in.copy_(drawn[0][0])
+            u_in.copy_(drawn[0][1])
+            one_round(ud_in, u_in)
+            for t, t0 in zip((last, pos, buf, length, acc_out), state):
+                t.copy_(t0)
+        torch.cuda.current_stream(dev).wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            one_round(ud_in, u_in)
+        for r in range(rounds):
+            ud_in.copy_(drawn[r][0])
+            u_in.copy_(drawn[r][1])
+            g.replay()
+            accs[r].copy_(acc_out)
+        torch.cuda.current_stream(dev).synchronize()
+        del g
+    else:
+        for r in range(rounds):
+            one_round(*uniforms())
+            accs[r].copy_(acc_out)
     acc_h = accs.cpu()
     bad = (acc_h < 0).nonzero()
     if bad.numel():

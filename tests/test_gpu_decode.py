@@ -118,6 +118,31 @@ def test_decode_loop_rounds_match_oracle():
           flush=True)
 
 
+@pytest.mark.parametrize("mode", ["mixed", "greedy"])
+def test_graph_decode_equals_eager(mode):
+    """One captured round replayed per round emits exactly the eager loop's
+    tokens and accept lengths; every round's output feeds the next replay, and
+    eager copies run between the replays."""
+    q_lm, p_lm = decode.synthetic_pair(V=256000, seed=4, dtype=torch.bfloat16, device=DEV)
+    B, gamma = 16, 5
+    first = torch.randint(0, 256000, (B,), generator=torch.Generator().manual_seed(3))
+    if mode == "mixed":
+        kw = dict(rule=torch.tensor([W.DIFF, W.OPT, W.TOKEN_V3, W.BILD] * 4, dtype=torch.int32),
+                  alpha=torch.tensor([0.05, 0.1, 0.3, 2.5] * 4),
+                  temperature=torch.tensor([1.0, 0.7, 0.5, 0.0] * 4))
+    else:
+        kw = dict(rule=W.DIFF, alpha=0.05, temperature=0.0)
+    eager = decode.spec_decode(q_lm, p_lm, first, rounds=7, gamma=gamma, seed=21, **kw)
+    for _ in range(2):
+        torch.cuda.synchronize()
+        graphed = decode.spec_decode(q_lm, p_lm, first, rounds=7, gamma=gamma, seed=21,
+                                     graph=True, **kw)
+        assert graphed.tokens == eager.tokens
+        for a, b in zip(graphed.accept_len, eager.accept_len):
+            assert torch.equal(a, b)
+    print(f"[decode-graph] {mode} tokens/round {eager.tokens_per_round():.2f}", flush=True)
+
+
 @pytest.mark.parametrize("rule,alpha", [(W.DIFF, 0.05), (W.OPT, 0.1), (W.TOKEN_V1, 0.05),
                                         (W.BILD, 2.5), (W.LOSSY, 0.3)])
 def test_greedy_decode_loop_equals_oracle_loop(rule, alpha):
