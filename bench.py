@@ -312,35 +312,41 @@ def main():
     n = args.steps
     every = max(1, args.event_every)
     sampled = list(range(0, n, every))
-    hot = {i: (ev.create(), ev.create()) for i in sampled}
+    hot = {i: tuple(ev.create() for _ in range(4)) for i in sampled}
     outer = (ev.create(), ev.create())
 
-    def step(i, events=None):
+    def call(i, ev_tiles=None):
         s = sets[i % len(sets)]
         if per_seq:
             temp = torch.zeros_like(s["temperature"]) if wl.greedy else s["temperature"]
-            ev0, ev1 = events if events is not None else (None, None)
             spc.spc_verify_ex(s["q"], s["p"], s["draft"], s["uniforms"], 0, 0.0, 1.0,
                               rule_per_seq=s["rule"], alpha_per_seq=s["alpha"],
-                              temp_per_seq=temp, ev_hot_begin=ev0, ev_hot_end=ev1,
-                              rules_present=rule_mask, out=outs[i % len(sets)], stream=stream)
-        elif events is None and wl.greedy:
-            spc.spc_greedy_verify(s["q"], s["p"], s["draft"], wl.rule, wl.alpha,
-                                  out=outs[i % len(sets)], stream=stream)
-        elif events is None:
-            spc.spc_verify(s["q"], s["p"], s["draft"], s["uniforms"], wl.rule, wl.alpha,
-                           wl.temperature, out=outs[i % len(sets)], stream=stream)
-        else:  # the same step with timing events (temperature 0: the greedy step)
-            spc.spc_verify_ex(s["q"], s["p"], s["draft"], s["uniforms"], wl.rule, wl.alpha,
-                              wl.temperature, ev_hot_begin=events[0], ev_hot_end=events[1],
+                              temp_per_seq=temp, rules_present=rule_mask, ev_tiles=ev_tiles,
                               out=outs[i % len(sets)], stream=stream)
+        else:
+            # temperature 0 is the batch-wide greedy step (spc_greedy_verify)
+            spc.spc_verify_ex(s["q"], s["p"], s["draft"], None if wl.greedy else s["uniforms"],
+                              wl.rule, wl.alpha, 0.0 if wl.greedy else wl.temperature,
+                              ev_tiles=ev_tiles, out=outs[i % len(sets)], stream=stream)
+
+    sraw = ctypes.c_void_p(stream.cuda_stream)
+
+    def step(i, events=None):
+        # a sampled step records four events on the call's stream: around the
+        # whole call, and (inside the library) around its statistics kernel
+        if events is None:
+            call(i)
+            return
+        ev.hip.hipEventRecord(ctypes.c_void_p(events[0]), sraw)
+        call(i, (events[1], events[2]))
+        ev.hip.hipEventRecord(ctypes.c_void_p(events[3]), sraw)
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
 
     # timed region: exactly `steps` steps; every `every`-th one brackets the
-    # statistics kernel with its own pair of events
+    # call and its statistics kernel with events
     torch.cuda.synchronize()
     ev.hip.hipEventRecord(ctypes.c_void_p(outer[0]), ctypes.c_void_p(stream.cuda_stream))
     t0 = time.perf_counter()
@@ -350,7 +356,8 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     total_ms = ev.elapsed_ms(*outer)
-    hot_ms = sorted(ev.elapsed_ms(*hot[i]) for i in sampled)
+    hot_ms = sorted(ev.elapsed_ms(hot[i][1], hot[i][2]) for i in sampled)
+    call_ms = sorted(ev.elapsed_ms(hot[i][0], hot[i][3]) for i in sampled)
     windows = sorted(ev.elapsed_ms(hot[a][0], hot[b][0]) / (b - a)
                      for a, b in zip(sampled, sampled[1:]))
     ms_per_step = total_ms / n
@@ -382,11 +389,17 @@ def main():
                     step_us_p10_p50_p90=[None if pct(windows, q) is None else pct(windows, q) * 1e3
                                          for q in (0.1, 0.5, 0.9)],
                     step_us_windows=f"{len(windows)} windows of {every} steps"),
-        roofline=dict(bound="hbm", kernel="k_stats", achieved=achieved, peak=PEAK_HBM_GBPS,
+        roofline=dict(bound="hbm", kernel="k_tiles", achieved=achieved, peak=PEAK_HBM_GBPS,
                       unit="GB/s", frac=achieved / PEAK_HBM_GBPS, traffic=traffic,
                       mean_us=hot_mean * 1e3, min_us=hot_ms[0] * 1e3,
                       p10_p50_p90_us=[pct(hot_ms, q) * 1e3 for q in (0.1, 0.5, 0.9)],
                       launches_timed=len(hot_ms), bytes_per_launch=stats_bytes),
+        # the whole step against the same roof: algorithmic bytes of the step
+        # (both logit tensors once, drafts, uniforms, outputs) / step time
+        step_roofline=dict(bound="hbm", achieved=wl.algorithmic_bytes() / (ms_per_step / 1e3) / 1e9,
+                           peak=PEAK_HBM_GBPS, unit="GB/s",
+                           frac=wl.algorithmic_bytes() / (ms_per_step / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                           call_us_p10_p50_p90=[pct(call_ms, q) * 1e3 for q in (0.1, 0.5, 0.9)]),
     )
     if not args.no_cpu_baseline:
         torch.cuda.synchronize()
@@ -400,9 +413,9 @@ def main():
         base, rep = cpu_baseline(wl, s0, g)
         line["cpu_baseline"] = base
         line["parity_vs_oracle"] = rep
-    for a, b in hot.values():
-        ev.destroy(a)
-        ev.destroy(b)
+    for evs in hot.values():
+        for e in evs:
+            ev.destroy(e)
     print(json.dumps(line), flush=True)
     return 0
 

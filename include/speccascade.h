@@ -39,13 +39,6 @@
  *   buffer per device: calls that use it must not overlap in time on one
  *   device (issue them on one stream).  Calls with distinct caller
  *   workspaces may run concurrently.
- * - Environment: SPC_ONE_READ=1 (read on every call) makes the verify calls
- *   compute the second pass of OPT and token-rule rows (D_TV, eta) inside the
- *   statistics launch, over tiles still held in registers, instead of reading
- *   those rows again: one cooperative launch whose workgroups wait per row
- *   for the row's other tiles.  It applies to batches without log-loss rules
- *   or BiLD* of at most 8192 rows; the outputs are bitwise the same.  It is
- *   off by default because it is slower on MI355X.
  */
 #ifndef SPECCASCADE_H
 #define SPECCASCADE_H
@@ -178,15 +171,18 @@ spc_status spc_greedy_verify(const void* q_logits, const void* p_logits, int32_t
  *       zero before its first use (the kernels leave them zero again).
  *       NULL selects the internal per-device workspace, allocated on first
  *       use and grown as needed.
- *   ev_hot_begin, ev_hot_end  optional HIP events recorded on `stream`
- *       immediately before and after the vocabulary-streaming statistics
- *       kernel(s), for timing them alone.
  *   rules_present  with rule_per_seq: a bitmask (bit i = rule i) of the
  *       rules the array may hold, 0 = any.  It lets the library skip the
  *       passes no sequence needs (the second pass of OPT, OPTLOG and the
  *       token rules; the first moments of BiLD* and the log-loss rules).  A
  *       sequence whose rule lies outside a nonzero mask is invalid (it
  *       reports accept_len = -1 and next_token = -1).
+ *   ev_tiles_begin, ev_tiles_end  for profiling: events (owned by the
+ *       caller) recorded on `stream` right before and right after the
+ *       statistics kernel of the call's first launch, so that their elapsed
+ *       time is that kernel's duration; NULL records nothing.  A record
+ *       that fails makes the call return SPC_E_HIP before any kernel of
+ *       that launch.
  */
 typedef struct {
   const int32_t* rule_per_seq;
@@ -197,9 +193,9 @@ typedef struct {
   float* out_sample_norm;
   void* workspace;
   size_t workspace_bytes;
-  hipEvent_t ev_hot_begin;
-  hipEvent_t ev_hot_end;
   uint32_t rules_present;
+  hipEvent_t ev_tiles_begin;
+  hipEvent_t ev_tiles_end;
 } spc_verify_ex_args;
 
 /* spc_verify with extended arguments; `ex` may be NULL.  `temperature`
@@ -227,15 +223,30 @@ spc_status spc_verify_ex(const void* q_logits, const void* p_logits, int32_t dty
  *                 cumulative mass (vocabulary order) exceeds u times the
  *                 total; may be NULL when every temperature is 0
  *   out_token     [B] int32
- * Uses the statistics pass and the tile-mass draw of spc_verify (one pass
- * over the logits); needs the internal workspace (a γ = 0 step of size
- * spc_workspace_bytes(B, 1, V, dtype) suffices).  Errors as spc_verify; a
+ * Uses the statistics tiles and the tile-mass draw of spc_verify (one pass
+ * over the logits) and the internal workspace.  Errors as spc_verify; a
  * negative or non-finite temperature is SPC_E_PARAM, an invalid per-sequence
  * one gives out_token = -1.
  */
 spc_status spc_draft_sample(const void* logits, int32_t dtype, int32_t B, int32_t V,
                             float temperature, const float* temp_per_seq,
                             const float* uniforms, int32_t* out_token, hipStream_t stream);
+
+/*
+ * spc_draft_sample_ws -- spc_draft_sample with a caller workspace of
+ * workspace_bytes >= spc_draft_workspace_bytes(B, V, dtype) bytes, 256-byte
+ * aligned, whose first spc_workspace_zero_bytes(1, 1, 2, dtype) bytes are zero
+ * before its first use (the kernels leave them zero).  NULL selects the
+ * internal workspace.  A too-small or misaligned workspace is SPC_E_WORKSPACE.
+ * Calls with distinct workspaces may run concurrently.
+ */
+spc_status spc_draft_sample_ws(const void* logits, int32_t dtype, int32_t B, int32_t V,
+                               float temperature, const float* temp_per_seq,
+                               const float* uniforms, int32_t* out_token, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of device workspace one spc_draft_sample_ws call of this shape needs. */
+size_t spc_draft_workspace_bytes(int32_t B, int32_t V, int32_t dtype);
 
 /* Bytes of device workspace one call of this shape needs. */
 size_t spc_workspace_bytes(int32_t B, int32_t gamma, int32_t V, int32_t dtype);

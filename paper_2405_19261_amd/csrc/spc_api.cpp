@@ -1,14 +1,15 @@
 // spc_api.cpp -- the C interface of libspeccascade (declared in
 // include/speccascade.h): argument checks, workspace, kernel dispatch.
 #include <math.h>
-#include <stdlib.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 
 #include <algorithm>
 #include <map>
 #include <mutex>
 #include <string>
+#include <vector>
 
 #include "spc_internal.h"
 
@@ -28,9 +29,13 @@ spc_status fail(spc_status s, const char* fmt, ...) {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// The internal workspace of each device.  A buffer that had to grow is kept
+// (not freed) until spc_release: kernels already enqueued, or captured in a
+// graph, may still refer to it.
 struct DevWorkspace {
   void* ptr = nullptr;
   size_t bytes = 0;
+  std::vector<void*> retired;
 };
 std::mutex g_ws_mu;
 std::map<int, DevWorkspace> g_ws;
@@ -49,20 +54,21 @@ int cu_count(int dev) {
   return n;
 }
 
-// Rows (gridDim.y of the statistics kernels) are capped by the launch limit.
-constexpr int64_t kMaxRows = 65535;
-
-// SPC_ONE_READ=1 in the environment selects the one-read statistics kernel
-// for batches it can take (read on every call).  It is off by default: on
-// MI355X it is slower than reading the second-pass rows again.
-bool one_read_requested() {
-  const char* v = getenv("SPC_ONE_READ");
-  return v && v[0] && v[0] != '0';
-}
-
 bool vec_path(int dtype, int64_t V) {
   const int64_t eb = dtype == SPC_BF16 ? 2 : 4;
   return (V * eb) % 16 == 0;  // every row starts on a 16-byte boundary
+}
+
+int64_t stat_tiles(int dtype, bool vec, int64_t V) {
+  const int64_t n = spc::stat_tile_elems(dtype, vec);
+  return (V + n - 1) / n;
+}
+
+// Sequences per launch: whole sequences, at most kMaxRows rows (the
+// statistics grid is tiles x rows; a row of V < 2^31 entries has fewer than
+// 2^31 tiles).
+int64_t seqs_per_launch(int64_t B, int64_t gamma) {
+  return std::max<int64_t>(1, std::min(B, spc::kMaxRows / (gamma + 1)));
 }
 
 }  // namespace
@@ -70,26 +76,32 @@ bool vec_path(int dtype, int64_t V) {
 namespace spc {
 
 WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
-  // The completion counters sit at a fixed offset sized for the largest batch
-  // the interface accepts, so a workspace reused across shapes never has one
-  // call's data overlap another call's counters; they stay zero between calls.
+  // The zero region (job counter lines, per-row lines) has the same size
+  // and offset for every shape, so one zeroed workspace serves calls of any
+  // shape it is large enough for; launches leave it as found.
   const int64_t R = B * (gamma + 1);
-  const int64_t nt = (V + stat_tile_elems(dtype, vec) - 1) / stat_tile_elems(dtype, vec);
+  const int64_t nt = stat_tiles(dtype, vec, V);
   WsLayout L;
-  L.samp_cnt = 0;
-  size_t o = align_up(4 * (size_t)(kMaxRows + 1), 256);
-  // the drafter kernel's per-row counters, one per 128-byte line
-  L.draft_cnt = o;
-  o = align_up(o + 4 * (size_t)kDraftCntStride * (kMaxRows / 2 + 1), 256);
-  // the one-read statistics kernel's per-row counters, one per 128-byte line
-  L.row_cnt = o;
-  o = align_up(o + 4 * (size_t)kRowCntStride * kResRows, 256);
+  size_t o = 0;
+  L.hdr = o;
+  o = align_up(o + 4 * (size_t)(kHdrLines * kLineWords), 256);
+  L.rowline = o;
+  o = align_up(o + 4 * (size_t)(kMaxRows * kLineWords), 256);
   L.zero_end = o;
+  // two job passes, each with R + B row jobs and 2 R + B single jobs at most
+  L.jobs = o; o = align_up(o + 8 * (size_t)(2 * ((R + B) + (2 * R + B))), 256);
+  L.jobline = o; o = align_up(o + 4 * (size_t)kLineWords * 2 * (R + B), 256);
   L.tiles = o; o = align_up(o + sizeof(TilePart) * R * nt, 256);
-  L.tvpart = o; o = align_up(o + sizeof(double) * R * nt, 256);
-  const int64_t nc = (V + samp_chunk_elems(dtype, vec) - 1) / samp_chunk_elems(dtype, vec);
-  L.masses = o; o = align_up(o + sizeof(double) * B * nc, 256);
+  L.tvpart = o; o = align_up(o + sizeof(double) * R * nt * kParts, 256);
+  L.masses = o; o = align_up(o + sizeof(double) * B * nt * kParts, 256);
+  L.submass = o; o = align_up(o + sizeof(double) * B * nt * kParts * kMaxSub, 256);
   L.moms = o; o = align_up(o + sizeof(TileMom) * R * nt, 256);
+  L.rowstat = o; o = align_up(o + sizeof(RowStat) * R, 256);
+  L.rowdec = o; o = align_up(o + sizeof(int32_t) * R, 256);
+  L.etalist = o; o = align_up(o + sizeof(int32_t) * R * nt, 256);
+  L.argres = o; o = align_up(o + sizeof(int32_t) * 4 * R, 256);
+  L.etacnt = o; o = align_up(o + sizeof(int32_t) * R, 256);
+  L.seqinfo = o; o = align_up(o + sizeof(int32_t) * 2 * B, 256);
   L.total = o;
   return L;
 }
@@ -102,48 +114,61 @@ spc_status check_shape(int32_t B, int32_t gamma, int32_t V) {
   if (B < 1 || gamma < 1 || gamma > SPC_MAX_GAMMA || V < 2)
     return fail(SPC_E_SHAPE, "bad shape B=%d gamma=%d V=%d (need B>=1, 1<=gamma<=%d, V>=2)", B,
                 gamma, V, SPC_MAX_GAMMA);
-  const int64_t R = (int64_t)B * (gamma + 1);
-  if (R > kMaxRows)
-    return fail(SPC_E_SHAPE, "B*(gamma+1)=%lld exceeds %lld rows", (long long)R,
-                (long long)kMaxRows);
   return SPC_OK;
 }
 
-// The internal workspace of the current device, grown to L.total if needed
-// (its counters zeroed on `stream` before any kernel that uses them).
-spc_status internal_workspace(const spc::WsLayout& L, hipStream_t stream, char** out) {
+// The layout of one launch of a verify call of this shape.
+spc::WsLayout launch_layout(int32_t B, int32_t gamma, int32_t V, int dtype) {
+  return spc::ws_layout(seqs_per_launch(B, gamma), gamma, V, dtype, vec_path(dtype, V));
+}
+
+bool capturing(hipStream_t stream) {
+  hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &st) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return st != hipStreamCaptureStatusNone;
+}
+
+// The internal workspace of the current device, at least `bytes` long.  A
+// new buffer has its zero region cleared on `stream` before any kernel that
+// uses it; that cannot be recorded into a graph, so a call being captured
+// that would need a larger buffer fails instead (make one eager call of the
+// largest shape first, or pass a caller workspace).
+spc_status internal_workspace(size_t bytes, size_t zero_bytes, hipStream_t stream, char** out) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(SPC_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
   std::lock_guard<std::mutex> lk(g_ws_mu);
   DevWorkspace& w = g_ws[dev];
-  if (w.bytes < L.total) {
-    // growing: the old buffer may still be in use by work on `stream`
-    if (w.ptr) {
-      e = hipStreamSynchronize(stream);
-      if (e == hipSuccess) e = hipFree(w.ptr);
-      w.ptr = nullptr;
-      w.bytes = 0;
-      if (e != hipSuccess) return fail(SPC_E_HIP, "workspace release: %s", hipGetErrorString(e));
-    }
-    const size_t want = L.total + L.total / 4;  // headroom for nearby shapes
-    e = hipMalloc(&w.ptr, want);
+  if (w.bytes < bytes) {
+    if (capturing(stream))
+      return fail(SPC_E_WORKSPACE,
+                  "the internal workspace must grow to %zu bytes, which a stream capture cannot "
+                  "record: make an eager call of this shape first, or pass a workspace",
+                  bytes);
+    const size_t want = bytes + bytes / 4;  // headroom for nearby shapes
+    void* ptr = nullptr;
+    e = hipMalloc(&ptr, want);
+    if (e != hipSuccess) return fail(SPC_E_HIP, "hipMalloc(%zu): %s", want, hipGetErrorString(e));
+    // zero the counters, ordered before this call's kernels on the same stream
+    e = hipMemsetAsync(ptr, 0, zero_bytes, stream);
     if (e != hipSuccess) {
-      w.ptr = nullptr;
-      return fail(SPC_E_HIP, "hipMalloc(%zu): %s", want, hipGetErrorString(e));
-    }
-    // zero counters, ordered before this call's kernels on the same stream;
-    // the kernels leave them zero
-    e = hipMemsetAsync(w.ptr, 0, L.zero_end, stream);
-    if (e != hipSuccess) {
-      (void)hipFree(w.ptr);
-      w.ptr = nullptr;
+      (void)hipFree(ptr);
       return fail(SPC_E_HIP, "hipMemsetAsync: %s", hipGetErrorString(e));
     }
+    if (w.ptr) w.retired.push_back(w.ptr);
+    w.ptr = ptr;
     w.bytes = want;
   }
   *out = static_cast<char*>(w.ptr);
   return SPC_OK;
+}
+
+template <class T>
+T* offset(T* p, int64_t n) {
+  return p ? p + n : p;
 }
 
 spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_t* draft,
@@ -166,14 +191,15 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
   if (!per_alpha && !isfinite(alpha)) return fail(SPC_E_PARAM, "alpha is not finite");
   if (!per_rule && !per_alpha && rule == SPC_RULE_LOSSY && !(alpha < 1.0f))
     return fail(SPC_E_PARAM, "the lossy rule needs alpha < 1 (got %g)", (double)alpha);
-  if (!force_greedy && !per_temp && !(isfinite(temperature) && temperature >= 1e-20f))
-    return fail(SPC_E_PARAM, "temperature must be finite and >= 1e-20 (got %g)",
-                (double)temperature);
+  if (!force_greedy && !per_temp && !(isfinite(temperature) && temperature > 0.0f))
+    return fail(SPC_E_PARAM, "temperature must be finite and > 0 (got %g)", (double)temperature);
   if (((uintptr_t)q | (uintptr_t)p) % 16 != 0)
     return fail(SPC_E_ALIGN, "logit base pointers must be 16-byte aligned");
 
   const bool vec = vec_path(dtype, V);
-  const spc::WsLayout L = spc::ws_layout(B, gamma, V, dtype, vec);
+  const int64_t g1 = (int64_t)gamma + 1;
+  const int64_t b_launch = seqs_per_launch(B, gamma);
+  const spc::WsLayout L = spc::ws_layout(b_launch, gamma, V, dtype, vec);
   // argument checks end here: no HIP call precedes them
   if (ex && ex->workspace &&
       (ex->workspace_bytes < L.total || ((uintptr_t)ex->workspace % 256) != 0))
@@ -188,88 +214,159 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
   if (ex && ex->workspace) {
     ws = static_cast<char*>(ex->workspace);
   } else {
-    const spc_status wst = internal_workspace(L, stream, &ws);
+    const spc_status wst = internal_workspace(L.total, L.zero_end, stream, &ws);
     if (wst != SPC_OK) return wst;
   }
 
-  spc::Params P{};
-  P.q = q;
-  P.p = p;
-  P.draft = draft;
-  P.uniforms = uniforms;
-  P.B = B;
-  P.gamma = gamma;
-  P.V = V;
-  P.nt = (int32_t)((V + spc::stat_tile_elems(dtype, vec) - 1) / spc::stat_tile_elems(dtype, vec));
-  P.nc = (int32_t)((V + spc::samp_chunk_elems(dtype, vec) - 1) / spc::samp_chunk_elems(dtype, vec));
-  P.K = spc::samp_groups(P.nc, B, cus);
-  P.rule = rule;
-  P.alpha = alpha;
-  P.temp = force_greedy ? 0.0f : temperature;
-  P.force_greedy = force_greedy ? 1 : 0;
-  P.rule_ps = per_rule ? ex->rule_per_seq : nullptr;
-  P.alpha_ps = per_alpha ? ex->alpha_per_seq : nullptr;
-  P.temp_ps = (per_temp && !force_greedy) ? ex->temp_per_seq : nullptr;
-  P.out_accept = out_accept;
-  P.out_token = out_token;
-  P.out_defer = out_defer;
-  P.out_stats = ex ? ex->out_row_stats : nullptr;
-  P.out_argmax = ex ? ex->out_argmax : nullptr;
-  P.out_norm = ex ? ex->out_sample_norm : nullptr;
-  P.samp_cnt = reinterpret_cast<uint32_t*>(ws + L.samp_cnt);
-  P.row_cnt = reinterpret_cast<uint32_t*>(ws + L.row_cnt);
-  P.tiles = reinterpret_cast<spc::TilePart*>(ws + L.tiles);
-  P.tvpart = reinterpret_cast<double*>(ws + L.tvpart);
-  P.masses = reinterpret_cast<double*>(ws + L.masses);
-  P.moms = reinterpret_cast<spc::TileMom*>(ws + L.moms);
-
-  // sequences at temperature > 0 may exist unless the whole batch is greedy;
-  // OPT at temperature > 0 needs the TV pass
-  const bool need_sample = !force_greedy && (per_temp || temperature > 0.0f);
-  // The rules the batch may hold decide the passes.  OPT, OPTLOG (D_TV) and
-  // the token rules (eta) need the second pass over their rows at
-  // temperature > 0; rows that need first moments (log-loss rules, BiLD* at
-  // temperature > 0) and rows that do not each get their statistics kernel.
+  // The rules the batch may hold decide what each launch computes.
   constexpr uint32_t kAll = (1u << (SPC_RULE_OPTLOG + 1)) - 1u;
-  constexpr uint32_t kTv = (1u << SPC_RULE_OPT) | (1u << SPC_RULE_OPTLOG) |
-                           (1u << SPC_RULE_TOKEN_V1) | (1u << SPC_RULE_TOKEN_V2) |
-                           (1u << SPC_RULE_TOKEN_V3);
+  constexpr uint32_t kTv = (1u << SPC_RULE_OPT) | (1u << SPC_RULE_OPTLOG);
   constexpr uint32_t kLog = (1u << SPC_RULE_BILD) | (1u << SPC_RULE_CHOWLOG) |
                             (1u << SPC_RULE_DIFFLOG) | (1u << SPC_RULE_OPTLOG);
   const uint32_t mask = ex ? ex->rules_present & kAll : 0u;
   const uint32_t rules = per_rule ? (mask ? mask : kAll) : (1u << rule);
-  P.rule_mask = per_rule ? mask : 0u;
-  constexpr uint32_t kEta = (1u << SPC_RULE_TOKEN_V1) | (1u << SPC_RULE_TOKEN_V2) |
-                            (1u << SPC_RULE_TOKEN_V3);
-  const int tv_kinds = !need_sample ? 0
-                                    : ((rules & (kTv & ~kEta)) ? spc::kPassTv : 0) |
-                                          ((rules & kEta) ? spc::kPassEta : 0);
-  const bool need_argmax = force_greedy || per_temp;
-  // BiLD* at temperature 0 reads one logit instead of moments
-  const bool bild_t0 = (rules & (1u << SPC_RULE_BILD)) && (force_greedy || per_temp);
+  const bool may_sample = !force_greedy && (per_temp || temperature > 0.0f);
+  // first moments of the log-loss rules (BiLD* at temperature 0 reads one
+  // logit instead): x for BiLD*, H(q) for ChowLog, H(q) and H(p) otherwise
   const bool need_mom = (rules & kLog) && !(rules == (1u << SPC_RULE_BILD) && force_greedy);
-  const bool need_plain = (rules & ~kLog) || per_temp || bild_t0;
-  P.mom_split = (need_mom && need_plain) ? 1 : 0;
-  // moments by rule: BiLD* reads x, ChowLog H(q), DiffLog and OPTLog H(q) - H(p)
-  P.mom_set = ((rules & (1u << SPC_RULE_BILD)) ? spc::kMomX : 0) |
-              ((rules & (1u << SPC_RULE_CHOWLOG)) ? spc::kMomHQ : 0) |
-              ((rules & ((1u << SPC_RULE_DIFFLOG) | (1u << SPC_RULE_OPTLOG)))
-                   ? spc::kMomHQ | spc::kMomHP
-                   : 0);
-  // The second pass reads its rows again, unless the one-read kernel is
-  // requested and fits: a resident grid holding at least one whole row of
-  // tiles per round.
-  int res_grid = 0;
-  const int64_t R = (int64_t)B * (gamma + 1);
-  if (tv_kinds && !need_mom && R <= spc::kResRows && one_read_requested()) {
-    const int nb = spc::res_blocks_per_cu(dtype, vec, need_argmax);
-    const int64_t rows_per_round = (int64_t)nb * cus / P.nt;
-    if (rows_per_round >= 1) res_grid = (int)(std::min<int64_t>(rows_per_round, R) * P.nt);
+  const int mom_set = !need_mom ? 0
+                                : ((rules & (1u << SPC_RULE_BILD)) ? spc::kMomX : 0) |
+                                      ((rules & (1u << SPC_RULE_CHOWLOG)) ? spc::kMomHQ : 0) |
+                                      ((rules & ((1u << SPC_RULE_DIFFLOG) | (1u << SPC_RULE_OPTLOG)))
+                                           ? spc::kMomHQ | spc::kMomHP
+                                           : 0);
+  // What the job passes may hold.  Rows of OPT / OPTLOG or a token rule at
+  // T > 0 are decided in the first job pass (after their TV or eta pass), so
+  // their draws fall to a second; every other row is decided by its last
+  // statistics tile, or (T = 0) after its argmax in the first pass.
+  constexpr uint32_t kTok = (1u << SPC_RULE_TOKEN_V1) | (1u << SPC_RULE_TOKEN_V2) |
+                            (1u << SPC_RULE_TOKEN_V3);
+  const bool pass2_rows = may_sample && (rules & (kTv | kTok));
+  const bool may_greedy = force_greedy || per_temp;
+  const int job_passes = pass2_rows ? 2 : 1;
+  // rows a TV job reads again are loaded through the caches
+  const bool nt_loads = !(may_sample && (rules & kTv));
+  const int64_t nt = stat_tiles(dtype, vec, V);
+  const int64_t eb = dtype == SPC_BF16 ? 2 : 4;
+
+  for (int64_t b0 = 0; b0 < B; b0 += b_launch) {
+    const int64_t bl = std::min<int64_t>(b_launch, B - b0);
+    const int64_t R = bl * g1;
+    spc::Params P{};
+    P.q = static_cast<const char*>(q) + b0 * g1 * V * eb;
+    P.p = static_cast<const char*>(p) + b0 * g1 * V * eb;
+    P.draft = draft + b0 * gamma;
+    P.uniforms = offset(uniforms, b0 * g1);
+    P.B = (int32_t)bl;
+    P.gamma = gamma;
+    P.V = V;
+    P.nt = (int32_t)nt;
+    P.rule = rule;
+    P.alpha = alpha;
+    P.temp = force_greedy ? 0.0f : temperature;
+    P.force_greedy = force_greedy ? 1 : 0;
+    P.rule_mask = per_rule ? mask : 0u;
+    P.mom_set = mom_set;
+    P.rule_ps = per_rule ? ex->rule_per_seq + b0 : nullptr;
+    P.alpha_ps = per_alpha ? ex->alpha_per_seq + b0 : nullptr;
+    P.temp_ps = (per_temp && !force_greedy) ? ex->temp_per_seq + b0 : nullptr;
+    P.out_accept = out_accept + b0;
+    P.out_token = out_token + b0;
+    P.out_defer = out_defer + b0 * g1;
+    P.out_stats = ex ? offset(ex->out_row_stats, b0 * g1 * 8) : nullptr;
+    P.out_argmax = ex ? offset(ex->out_argmax, b0 * g1 * 2) : nullptr;
+    P.out_norm = ex ? offset(ex->out_sample_norm, b0) : nullptr;
+    P.job_slots = R + bl;
+    P.single_slots = 2 * R + bl;
+    // workgroups of a job pass: a wavefront per item of its largest possible
+    // list, at most two workgroups per compute unit
+    const int64_t np = nt * spc::kParts;
+    const int64_t items1 = np * ((pass2_rows ? R : 0) + (may_sample ? bl : 0)) +
+                           (may_greedy ? 2 * R : 0) + (may_sample ? bl : 0);
+    const int64_t items2 = pass2_rows ? np * bl + bl : 0;
+    constexpr int64_t kW = spc::kJobThreads / 64;
+    const int job_groups = (int)std::max<int64_t>(
+        1, std::min<int64_t>((std::max(items1, items2) + kW - 1) / kW, 2 * (int64_t)cus));
+    P.hdr = reinterpret_cast<uint32_t*>(ws + L.hdr);
+    P.rowline = reinterpret_cast<uint32_t*>(ws + L.rowline);
+    P.jobs = reinterpret_cast<uint64_t*>(ws + L.jobs);
+    P.jobline = reinterpret_cast<uint32_t*>(ws + L.jobline);
+    P.tiles = reinterpret_cast<spc::TilePart*>(ws + L.tiles);
+    P.tvpart = reinterpret_cast<double*>(ws + L.tvpart);
+    P.masses = reinterpret_cast<double*>(ws + L.masses);
+    P.submass = reinterpret_cast<double*>(ws + L.submass);
+    P.moms = reinterpret_cast<spc::TileMom*>(ws + L.moms);
+    P.rowstat = reinterpret_cast<spc::RowStat*>(ws + L.rowstat);
+    P.rowdec = reinterpret_cast<int32_t*>(ws + L.rowdec);
+    P.etalist = reinterpret_cast<int32_t*>(ws + L.etalist);
+    P.argres = reinterpret_cast<int32_t*>(ws + L.argres);
+    P.etacnt = reinterpret_cast<int32_t*>(ws + L.etacnt);
+    P.seqinfo = reinterpret_cast<int32_t*>(ws + L.seqinfo);
+    const bool first = b0 == 0;
+    e = spc::launch_step(P, dtype, vec, nt_loads, job_passes, job_groups,
+                         first && ex ? ex->ev_tiles_begin : nullptr,
+                         first && ex ? ex->ev_tiles_end : nullptr, stream);
+    if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
   }
-  e = spc::launch_verify(P, dtype, vec, tv_kinds, need_sample, need_argmax, need_plain, need_mom,
-                         res_grid, ex ? ex->ev_hot_begin : nullptr,
-                         ex ? ex->ev_hot_end : nullptr, stream);
-  if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
+  return SPC_OK;
+}
+
+spc_status draft_impl(const void* logits, int32_t dtype, int32_t B, int32_t V, float temperature,
+                      const float* temp_per_seq, const float* uniforms, int32_t* out_token,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  g_err.clear();
+  if (!logits || !out_token) return fail(SPC_E_NULL, "a required pointer is NULL");
+  if (!temp_per_seq && !(isfinite(temperature) && temperature >= 0.0f))
+    return fail(SPC_E_PARAM, "temperature must be finite and >= 0 (got %g)",
+                (double)temperature);
+  const bool greedy = !temp_per_seq && temperature == 0.0f;
+  if (!greedy && !uniforms) return fail(SPC_E_NULL, "uniforms is NULL");
+  if (B < 1 || V < 2) return fail(SPC_E_SHAPE, "bad shape B=%d V=%d (need B>=1, V>=2)", B, V);
+  if (dtype != SPC_F32 && dtype != SPC_BF16) return fail(SPC_E_PARAM, "unknown dtype %d", dtype);
+  if ((uintptr_t)logits % 16 != 0)
+    return fail(SPC_E_ALIGN, "logit base pointer must be 16-byte aligned");
+  const bool vec = vec_path(dtype, V);
+  // rows per launch, as a verify step of gamma = 1 with as many sequences
+  const int64_t b_launch = seqs_per_launch(B, 1);
+  const spc::WsLayout L = spc::ws_layout(b_launch, 1, V, dtype, vec);
+  // argument checks end here: no HIP call precedes them
+  if (workspace && (workspace_bytes < L.total || ((uintptr_t)workspace % 256) != 0))
+    return fail(SPC_E_WORKSPACE, "workspace of %zu bytes (need %zu, 256-byte aligned)",
+                workspace_bytes, L.total);
+  char* ws = static_cast<char*>(workspace);
+  if (!ws) {
+    const spc_status wst = internal_workspace(L.total, L.zero_end, stream, &ws);
+    if (wst != SPC_OK) return wst;
+  }
+  const int64_t eb = dtype == SPC_BF16 ? 2 : 4;
+  for (int64_t b0 = 0; b0 < B; b0 += b_launch) {
+    const int64_t bl = std::min<int64_t>(b_launch, B - b0);
+    spc::Params P{};
+    P.q = static_cast<const char*>(logits) + b0 * V * eb;
+    P.p = P.q;
+    P.uniforms = offset(uniforms, b0);
+    P.B = (int32_t)bl;
+    P.gamma = 0;
+    P.V = V;
+    // Tiles twice as long as the statistics tiles once that still gives at
+    // least 4 workgroups per CU; small batches take the statistics tile
+    // length, for twice the workgroups (either way no more partials per row
+    // than the workspace holds for this shape).
+    const int64_t long_n = spc::draft_tile_elems(dtype, vec, true);
+    const bool long_tiles = bl * ((V + long_n - 1) / long_n) >= 1024;
+    const int64_t tile_n = long_tiles ? long_n : spc::draft_tile_elems(dtype, vec, false);
+    P.nt = (int32_t)((V + tile_n - 1) / tile_n);
+    P.rule = SPC_RULE_NEVER;
+    P.temp = greedy ? 0.0f : temperature;
+    P.force_greedy = greedy ? 1 : 0;
+    P.temp_ps = offset(temp_per_seq, b0);
+    P.out_token = out_token + b0;
+    P.samp_cnt = reinterpret_cast<uint32_t*>(ws + L.rowline) + spc::kDraftArrive;
+    P.tiles = reinterpret_cast<spc::TilePart*>(ws + L.tiles);
+    const hipError_t e =
+        spc::launch_draft(P, dtype, vec, greedy || temp_per_seq, long_tiles, stream);
+    if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
+  }
   return SPC_OK;
 }
 
@@ -313,61 +410,31 @@ spc_status spc_verify_ex(const void* q_logits, const void* p_logits, int32_t dty
 spc_status spc_draft_sample(const void* logits, int32_t dtype, int32_t B, int32_t V,
                             float temperature, const float* temp_per_seq,
                             const float* uniforms, int32_t* out_token, hipStream_t stream) {
-  g_err.clear();
-  if (!logits || !out_token) return fail(SPC_E_NULL, "a required pointer is NULL");
-  if (!temp_per_seq && !(isfinite(temperature) && temperature >= 0.0f))
-    return fail(SPC_E_PARAM, "temperature must be finite and >= 0 (got %g)",
-                (double)temperature);
-  const bool greedy = !temp_per_seq && temperature == 0.0f;
-  if (!greedy && !uniforms) return fail(SPC_E_NULL, "uniforms is NULL");
-  if (B < 1 || V < 2 || (int64_t)B > kMaxRows / 2)
-    return fail(SPC_E_SHAPE, "bad shape B=%d V=%d (need 1<=B<=%lld, V>=2)", B, V,
-                (long long)(kMaxRows / 2));
-  if (dtype != SPC_F32 && dtype != SPC_BF16) return fail(SPC_E_PARAM, "unknown dtype %d", dtype);
-  if ((uintptr_t)logits % 16 != 0)
-    return fail(SPC_E_ALIGN, "logit base pointer must be 16-byte aligned");
-  const bool vec = vec_path(dtype, V);
-  const spc::WsLayout L = spc::ws_layout(B, 0, V, dtype, vec);
-  // argument checks end here: no HIP call precedes them
-  char* ws = nullptr;
-  const spc_status wst = internal_workspace(L, stream, &ws);
-  if (wst != SPC_OK) return wst;
-  spc::Params P{};
-  P.q = logits;
-  P.p = logits;
-  P.uniforms = uniforms;
-  P.B = B;
-  P.gamma = 0;
-  P.V = V;
-  // Tiles twice as long as the statistics tiles once that still gives at
-  // least 4 workgroups per CU; small batches take the statistics tile
-  // length, for twice the workgroups (either way no more partials per row
-  // than the workspace holds for this shape).
-  const int64_t long_n = spc::draft_tile_elems(dtype, vec, true);
-  const bool long_tiles = (int64_t)B * ((V + long_n - 1) / long_n) >= 1024;
-  const int64_t tile_n = long_tiles ? long_n : spc::draft_tile_elems(dtype, vec, false);
-  P.nt = (int32_t)((V + tile_n - 1) / tile_n);
-  P.rule = SPC_RULE_NEVER;
-  P.temp = greedy ? 0.0f : temperature;
-  P.force_greedy = greedy ? 1 : 0;
-  P.temp_ps = temp_per_seq;
-  P.out_token = out_token;
-  P.samp_cnt = reinterpret_cast<uint32_t*>(ws + L.draft_cnt);
-  P.tiles = reinterpret_cast<spc::TilePart*>(ws + L.tiles);
-  const hipError_t e =
-      spc::launch_draft(P, dtype, vec, greedy || temp_per_seq, long_tiles, stream);
-  if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
-  return SPC_OK;
+  return draft_impl(logits, dtype, B, V, temperature, temp_per_seq, uniforms, out_token, nullptr,
+                    0, stream);
+}
+
+spc_status spc_draft_sample_ws(const void* logits, int32_t dtype, int32_t B, int32_t V,
+                               float temperature, const float* temp_per_seq,
+                               const float* uniforms, int32_t* out_token, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream) {
+  return draft_impl(logits, dtype, B, V, temperature, temp_per_seq, uniforms, out_token,
+                    workspace, workspace_bytes, stream);
 }
 
 size_t spc_workspace_bytes(int32_t B, int32_t gamma, int32_t V, int32_t dtype) {
   if (check_shape(B, gamma, V) != SPC_OK || (dtype != SPC_F32 && dtype != SPC_BF16)) return 0;
-  return spc::ws_layout(B, gamma, V, dtype, vec_path(dtype, V)).total;
+  return launch_layout(B, gamma, V, dtype).total;
 }
 
 size_t spc_workspace_zero_bytes(int32_t B, int32_t gamma, int32_t V, int32_t dtype) {
   if (check_shape(B, gamma, V) != SPC_OK || (dtype != SPC_F32 && dtype != SPC_BF16)) return 0;
-  return spc::ws_layout(B, gamma, V, dtype, vec_path(dtype, V)).zero_end;
+  return launch_layout(B, gamma, V, dtype).zero_end;
+}
+
+size_t spc_draft_workspace_bytes(int32_t B, int32_t V, int32_t dtype) {
+  if (B < 1 || V < 2 || (dtype != SPC_F32 && dtype != SPC_BF16)) return 0;
+  return spc::ws_layout(seqs_per_launch(B, 1), 1, V, dtype, vec_path(dtype, V)).total;
 }
 
 const char* spc_last_error(void) { return g_err.c_str(); }
@@ -377,12 +444,14 @@ void spc_release(void) {
   int cur = 0;
   if (hipGetDevice(&cur) != hipSuccess) cur = 0;
   for (auto& kv : g_ws) {
-    if (kv.second.ptr && hipSetDevice(kv.first) == hipSuccess) (void)hipFree(kv.second.ptr);
+    if (hipSetDevice(kv.first) != hipSuccess) continue;
+    if (kv.second.ptr) (void)hipFree(kv.second.ptr);
+    for (void* r : kv.second.retired) (void)hipFree(r);
   }
   g_ws.clear();
   (void)hipSetDevice(cur);
 }
 
-const char* spc_version(void) { return "libspeccascade 0.1 (gfx950)"; }
+const char* spc_version(void) { return "libspeccascade 0.2 (gfx950)"; }
 
 }  // extern "C"

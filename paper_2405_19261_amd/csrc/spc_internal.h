@@ -47,14 +47,6 @@ struct RowStat {
   int32_t amax_q, amax_p;
 };
 
-// Per-sequence decision, as the sampler needs it.
-struct SeqState {
-  int32_t row;   // j*
-  int32_t kind;  // SampleKind
-  float u;       // the sample's uniform u[b][gamma]
-  int32_t pad;
-};
-
 struct Params {
   const void* q;
   const void* p;
@@ -62,15 +54,11 @@ struct Params {
   const float* uniforms;
   int32_t B, gamma, V;
   int32_t nt;              // statistics tiles per row
-  int32_t nc;              // residual chunks per row
-  int32_t K;               // sampling workgroups per sequence
   int32_t rule;
   float alpha, temp;
   int32_t force_greedy;    // spc_greedy_verify: every sequence at temperature 0
-  int32_t mom_split;       // the moment statistics kernel runs too: the plain one
-                           // leaves it the rows that need first moments
   uint32_t rule_mask;      // rules per-sequence arrays may hold (0: any)
-  int32_t mom_set;         // first moments the moment kernel sums (kMom* bits)
+  int32_t mom_set;         // first moments the statistics tiles sum (kMom* bits; 0: none)
   const int32_t* rule_ps;
   const float* alpha_ps;
   const float* temp_ps;
@@ -80,42 +68,67 @@ struct Params {
   float* out_stats;
   int32_t* out_argmax;
   float* out_norm;
-  // workspace
-  uint32_t* samp_cnt;     // [B]   sampling workgroups of a sequence done
-  uint32_t* row_cnt;      // [R][kRowCntStride] arrivals / departures per row (one read)
-  TilePart* tiles;        // [R][nt] statistics partials
-  double* tvpart;         // [R][nt] TV partials (OPT) or eta partials (token rules)
-  double* masses;         // [B][nc] residual chunk masses of row j*
-  TileMom* moms;          // [R][nt] first moments (log-loss rules and BiLD*)
+  // launch layout
+  int32_t phase;           // job pass of a k_jobs launch (1 or 2)
+  int64_t job_slots;       // row jobs a job pass may hold: R + B
+  int64_t single_slots;    // single jobs a job pass may hold: 2 R + B
+  // workspace: zero region (counters; every launch leaves it as it found it)
+  uint32_t* hdr;           // [kHdrLines][kLineWords] job counters
+  uint32_t* rowline;       // [kMaxRows][kLineWords] per-row and per-sequence counters
+  uint32_t* samp_cnt;      // drafter kernel: per-row completion counters (kDraftCntStride)
+  // workspace: data (written before it is read in every launch)
+  uint64_t* jobs;          // [2 passes][job_slots + single_slots] job entries
+  uint32_t* jobline;       // [2 passes][job_slots][kLineWords] row-job completion counters
+  TilePart* tiles;         // [R][nt] statistics partials
+  double* tvpart;          // [R][nt * kParts] TV partials (OPT) or eta partials (token rules)
+  double* masses;          // [B][nt * kParts] residual masses per part of row j*
+  double* submass;         // [B][nt * kParts][kMaxSub] residual masses per sub-chunk
+  TileMom* moms;           // [R][nt] first moments (log-loss rules and BiLD*)
+  RowStat* rowstat;        // [R] merged row statistics
+  int32_t* rowdec;         // [R] bit 0 a_j, bit 1 delta_j
+  int32_t* etalist;        // [R][nt] tiles whose eta share needs a second look
+  int32_t* argres;         // [R][4] first tile of the q / p maximum, then its lowest index
+  int32_t* etacnt;         // [R] tiles listed in etalist
+  int32_t* seqinfo;        // [B][2] j* and sample kind of a residual job
 };
 
-// Entries per statistics tile and per residual chunk for a dtype and load
-// path, and sampling workgroups per sequence for a row of nc chunks in a batch
-// of B sequences on a device of `cus` compute units.
+// Entries per statistics tile and per drafter tile for a dtype and load path.
 int stat_tile_elems(int dtype, bool vec);
 int draft_tile_elems(int dtype, bool vec, bool long_tiles);
-int samp_chunk_elems(int dtype, bool vec);
-int samp_groups(int64_t nc, int B, int cus);
 
-// Workspace layout for a shape; offsets in bytes from the base.
+// Counters live on 128-byte lines of 32-bit words: arrivals on a shared line
+// serialise.
+constexpr int kLineWords = 32;
+constexpr int64_t kMaxRows = 16384;    // rows (and sequences) per launch
+// Job passes: workgroups of kJobThreads threads whose wavefronts take items
+// independently; a row job has kParts items (half tiles) per statistics tile,
+// each of at most kMaxSub sub-chunks.
+constexpr int kJobThreads = 512;
+constexpr int kParts = 2;
+constexpr int kMaxSub = 16;
+// Header lines: row and single jobs published for pass 1 and pass 2, then per
+// pass kExitLeaves + 1 lines counting the workgroups that have read its counts
+// (a two-level tree; the last arrival clears the pass's counts).
+constexpr int kExitLeaves = 16;
+constexpr int kHdrExit = 4;
+constexpr int kHdrLines = kHdrExit + 2 * (kExitLeaves + 1);
+
+// Words of a row line (counters only): the row's tile arrivals, the
+// decided-row mask of the sequence with the same index (64 bits), the row's
+// argmax-half arrivals, and the drafter kernel's per-row arrivals.
+constexpr int kRowArrive = 0, kSeqMask = 2, kRowJobDone = 4, kDraftArrive = 8;
+
+// Words between the drafter kernel's per-row completion counters.
+constexpr int kDraftCntStride = kLineWords;
+
+// Workspace layout for a shape; offsets in bytes from the base.  The zero
+// region (header lines, row lines) has the same size for every shape.
 struct WsLayout {
-  size_t samp_cnt, draft_cnt, row_cnt, zero_end;
-  size_t tiles, tvpart, masses, moms, total;
+  size_t hdr, rowline, zero_end;
+  size_t jobs, jobline, tiles, tvpart, masses, submass, moms, rowstat, rowdec, etalist, argres, etacnt,
+      seqinfo, total;
 };
 WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec);
-
-// Words between the drafter kernel's per-row completion counters (one
-// counter per 128-byte line: arrivals on a shared line serialise).
-constexpr int kDraftCntStride = 32;
-
-// The one-read statistics kernel's per-row counters (arrivals, departures),
-// one 128-byte line per row, for batches of at most kResRows rows.
-constexpr int kRowCntStride = 32;
-constexpr int64_t kResRows = 8192;
-
-// Workgroups of the one-read statistics kernel resident per compute unit
-// (0 if it cannot run).
-int res_blocks_per_cu(int dtype, bool vec, bool argmax);
 
 // Enqueue the drafter sampling kernel (Params: q = the logits [B][V], nt,
 // uniforms [B], temp_ps or temp, out_token, samp_cnt with kDraftCntStride,
@@ -125,21 +138,13 @@ int res_blocks_per_cu(int dtype, bool vec, bool argmax);
 hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, bool long_tiles,
                         hipStream_t stream);
 
-// Second passes a batch may need (bits of tv_kinds): D_TV of OPT and OPTLOG
-// rows, eta of token-rule rows, each at temperature > 0.
-constexpr int kPassTv = 1, kPassEta = 2;
-
-// Enqueue the kernels of one verify call.  tv_kinds: the second passes the
-// batch may need (kPassTv | kPassEta); need_sample: it may hold
-// sequences at temperature > 0; need_argmax: it may hold greedy (temperature
-// 0) sequences; need_plain / need_mom: it may hold rows that need no first
-// moments / rows that do (log-loss rules, BiLD* at temperature > 0), each
-// kind handled by its own statistics kernel.  res_grid > 0 (a multiple of
-// nt; only with tv_kinds and without need_mom): statistics and second pass in
-// one cooperative launch of res_grid workgroups instead of two kernels.
-// Returns the first launch error.
-hipError_t launch_verify(const Params& P, int dtype, bool vec, int tv_kinds, bool need_sample,
-                         bool need_argmax, bool need_plain, bool need_mom, int res_grid,
-                         hipEvent_t ev_begin, hipEvent_t ev_end, hipStream_t stream);
+// Enqueue one verify launch: the statistics tiles (k_tiles), then
+// `job_passes` job passes (k_jobs) of `job_groups` workgroups each.
+// nt_loads: the tiles read the logits non-temporally (no job reads a whole
+// row again).
+// ev_begin / ev_end (may be null): recorded right before and after k_tiles.
+hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, int job_passes,
+                       int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end,
+                       hipStream_t stream);
 
 }  // namespace spc

@@ -1,32 +1,46 @@
 // spc_kernels.hip -- gfx950 kernels of the speculative-cascade verify step.
 //
 // The step (GenSpecSample, Alg. 4, with the cascade target T_delta of eq. (6)
-// and the deferral rules of Table 1) runs as two or three kernels.  A row is
-// one position (b, j) of the logit pair (q, p); rows are cut into tiles of
-// consecutive vocabulary entries.
+// and the deferral rules of Table 1) runs as a statistics launch and one or
+// two job launches; no workgroup ever waits for another.  A row is one
+// position (b, j) of the logit pair (q, p); rows are cut into statistics
+// tiles of consecutive vocabulary entries.
 //
-//   k_stats   grid (tiles per row, rows), one tile per 256-thread workgroup.
-//             Reads every logit of q and p once and reduces the tile to
-//             {max z, sum 2^(z c - r), argmax} for both tensors
-//             (c = log2(e) / T); the tile partial goes to the workspace.
-//   k_tv      OPT sequences at temperature > 0 only: D_TV(p, q) of Lemma 3
-//             needs both normalisers, so it is a second pass over those rows,
-//             one partial per tile.
-//   k_sample  grid (K, sequences), 1024-thread workgroups.  Every workgroup
-//             of sequence b merges that sequence's row partials and takes the
-//             per-sequence decision (deferral delta_j, accept draws a_j, first
-//             rejection j*) -- a small, fixed-order computation, so every
-//             workgroup reaches the same result.  A replacement from the
-//             residual max(0, p - q) of a non-OPT row needs a second look at
-//             row j*: the K workgroups sum its residual per chunk and the last
-//             to finish draws.  Every other draw takes its per-tile masses
-//             from the statistics or TV partials and is made by workgroup 0.
-//             Draws are inverse CDF in vocabulary order.
+//   k_tiles      grid (tile, row).  A tile reduces its entries of q and p to
+//                {max z, sum 2^(z c - r)} (c = log2(e) / T); its first
+//                wavefront then arrives on the row's counter, and the last
+//                tile of the row merges the row.  Then, per row:
+//                  OPT / OPTLOG at T > 0   publishes a TV job (D_TV of Lemma 3
+//                                          needs both normalisers: one chunk
+//                                          per tile, the row read again);
+//                  token rules at T > 0    settles eta (Alg. 6) for the tiles
+//                                          wholly below the rule's threshold
+//                                          from their statistics and
+//                                          publishes a job for the others;
+//                  T = 0                   publishes the two halves of its
+//                                          argmax (the lowest index of a row
+//                                          maximum lies in the first tile
+//                                          whose maximum it is);
+//                  otherwise               decides the row at once.
+//   row decision delta_j and a_j of the row, then an atomic OR of the row into
+//                its sequence's decided-row mask.  The decision that completes
+//                the prefix 0..j* of decided rows containing the first
+//                rejection j* finishes the sequence: the greedy token, or a
+//                draw published to the next job pass (from the statistics
+//                partials, for an extra token from q, p or a token rule's
+//                target; else a residual job over row j*).
+//   k_jobs       a static walk over the jobs the launches before it
+//                published: every chunk of every row job, then the single
+//                jobs.  The last chunk of a job continues it (the row's
+//                decision, which may publish to the next pass, or the
+//                residual draw).
 //
-// Kernel boundaries order the passes; within k_sample one completion counter
-// per sequence ("last workgroup to arrive draws") is reset by its last
-// arriver, so the zeroed workspace is zero again after every call.  All
-// merges run in a fixed order: results do not depend on scheduling.
+// Draws are inverse CDF in vocabulary order.  Merges and sums run in fixed
+// orders, so results do not depend on scheduling.  Counters sit in a zeroed
+// region of the workspace and every launch leaves them at zero: arrival
+// counters are reset by their last arrival, a pass's job counts by the last
+// of its workgroups to read them.  So a call replayed from a graph finds the
+// counters as the captured call did.
 #include <math.h>
 
 #include "spc_internal.h"
@@ -41,10 +55,6 @@ constexpr double kLn2 = 0.69314718055994530942;   // ln(2)
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = kThreads / 64;
-// The sampling pass runs 1024-thread workgroups: a wavefront per row while
-// deciding, a 256-thread group per tile while summing residual masses.
-constexpr int kSampThreads = 1024;
-constexpr int kSampWaves = kSampThreads / 64;
 
 // ------------------------------------------------------------------ geometry
 // A lane load is one 16-byte vector (8 bf16 or 4 f32 entries) on the vector
@@ -87,22 +97,24 @@ __device__ __forceinline__ float elem(const uint32_t* w, int e) {
 // group, tid the thread's index in it.  Thread t's lane load i covers entries
 // e = t0 + (i*GT + t) * VW .. + VW - 1 (interleaved, so each load
 // instruction of a wavefront reads one contiguous 1 KiB).
-// Entries at or past `end` read as -inf; a lane past the end re-reads a valid
-// address and discards the value, so the loads are branch-free.  With MASK
-// false the caller guarantees a whole tile before `end`.
+// Entries at or past `end` read as -inf; a lane past the end re-reads the
+// tile's first entry and discards the value, so the loads are branch-free.
+// With MASK false the caller guarantees a whole tile before `end`.  Addresses
+// are a uniform tile base plus a 32-bit lane offset.
 template <int DT, bool VEC, int U, bool NT, int GT = kThreads, bool MASK = true>
 __device__ __forceinline__ void load_tile(const char* row, int64_t t0, int64_t end,
                                           uint32_t (&w)[U][Tile<DT, VEC, U>::NW], int tid) {
   using T = Tile<DT, VEC, U>;
   constexpr uint32_t kPad = (DT == 1) ? 0xff80ff80u : 0xff800000u;
-  const bool full = !MASK || t0 + (int64_t)GT * U * T::VW <= end;
+  constexpr int kSpan = GT * U * T::VW;  // entries of a whole tile
+  const char* base = row + t0 * T::EB;
+  const int left = (int)(end - t0 < (int64_t)kSpan ? end - t0 : (int64_t)kSpan);
+  const bool full = !MASK || left == kSpan;
 #pragma unroll
   for (int i = 0; i < U; ++i) {
-    const int64_t slot = (int64_t)i * GT + tid;
-    const int64_t e = t0 + slot * T::VW;
-    const bool ok = full || e < end;
-    const int64_t ec = ok ? e : t0;  // a valid address; the value is discarded
-    const char* a = row + ec * T::EB;
+    const int e = (i * GT + tid) * T::VW;
+    const bool ok = full || e < left;
+    const char* a = base + (uint32_t)((ok ? e : 0) * T::EB);
     if constexpr (VEC) {
       const u32x4* src = reinterpret_cast<const u32x4*>(a);
       const u32x4 v = NT ? __builtin_nontemporal_load(src) : *src;
@@ -238,6 +250,67 @@ __device__ __forceinline__ void vmem_drain() {
   __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));  // vmcnt(0)
 }
 
+// First moments of a tile, written and read within one launch.
+static_assert(sizeof(TileMom) == 24, "TileMom is three doubles");
+__device__ __forceinline__ void st_mom(TileMom* dst, const TileMom& m) {
+  st_dev_f64(&dst->hq, m.hq);
+  st_dev_f64(&dst->hp, m.hp);
+  st_dev_f64(&dst->x, m.x);
+}
+__device__ __forceinline__ TileMom ld_mom(const TileMom* src) {
+  return TileMom{ld_dev_f64(&src->hq), ld_dev_f64(&src->hp), ld_dev_f64(&src->x)};
+}
+
+// Merged row statistics, written and read within one launch: six 64-bit words.
+static_assert(sizeof(RowStat) == 48, "RowStat is six 64-bit words");
+__device__ __forceinline__ void st_rowstat(RowStat* dst, const RowStat& s) {
+  uint64_t w[6];
+  __builtin_memcpy(w, &s, sizeof w);
+#pragma unroll
+  for (int i = 0; i < 6; ++i)
+    __hip_atomic_store(reinterpret_cast<uint64_t*>(dst) + i, w[i], __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ RowStat ld_rowstat(const RowStat* src) {
+  uint64_t w[6];
+#pragma unroll
+  for (int i = 0; i < 6; ++i)
+    w[i] = __hip_atomic_load(reinterpret_cast<uint64_t*>(const_cast<RowStat*>(src)) + i,
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  RowStat s;
+  __builtin_memcpy(&s, w, sizeof w);
+  return s;
+}
+
+// 32- and 64-bit words shared within one launch (agent scope, relaxed).
+__device__ __forceinline__ uint32_t ld_u32(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_u32(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_u64(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_u64(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int32_t ld_i32(const int32_t* p) {
+  return (int32_t)ld_u32(reinterpret_cast<const uint32_t*>(p));
+}
+__device__ __forceinline__ void st_i32(int32_t* p, int32_t v) {
+  st_u32(reinterpret_cast<uint32_t*>(p), (uint32_t)v);
+}
+__device__ __forceinline__ uint32_t add_u32(uint32_t* p, uint32_t v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void max_u32(uint32_t* p, uint32_t v) {
+  (void)__hip_atomic_fetch_max(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t or_u64(uint64_t* p, uint64_t v) {
+  return __hip_atomic_fetch_or(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ------------------------------------------------------- wavefront reductions
 // DPP row operations combine the lanes of each 16-lane row without going
 // through LDS; readlane then brings the four row results to every lane in a
@@ -321,7 +394,6 @@ struct SharedT {
   int flag;
 };
 using Shared = SharedT<kWaves>;
-using SampShared = SharedT<kSampWaves>;
 
 // Merged statistics and decision of one row of a sequence.
 struct RowDecision {
@@ -331,19 +403,12 @@ struct RowDecision {
   int delta, keep;       // delta_j and a_j
 };
 
-// Per-sequence state built by every sampling workgroup.
 // The part of a draw found by wave 0, for the whole workgroup.
 struct PickState {
   int k;       // part holding the sample (-1: nothing to draw)
   int kind;    // SampleKind actually sampled
   int src;     // MassSrc of the part masses
   double rem;  // target mass remaining at the start of that part
-};
-
-struct SeqShared {
-  RowDecision rows[SPC_MAX_GAMMA + 1];
-  SeqState seq;
-  PickState pk;
 };
 
 // Block sums: per-wave results combined in wave order (a fixed order, so
@@ -390,6 +455,12 @@ __device__ __forceinline__ bool arrive_last(uint32_t* cnt, uint32_t n, SharedT<N
 }
 
 // ------------------------------------------------------ per-sequence params
+// Temperatures below 2^-107 are taken as 2^-107: z / T then stays finite in
+// float32 for logits up to about 10^6 in magnitude, and the tempered softmax
+// is already the T -> 0 limit (uniform over the tied maxima) for any logits
+// whose distinct values differ by more than about 10^-30.
+constexpr double kTempFloor = 0x1p-107;
+
 struct SeqParam {
   int rule;
   double alpha;
@@ -406,11 +477,10 @@ __device__ __forceinline__ SeqParam seq_param(const Params& P, int b) {
   const float T = P.temp_ps ? P.temp_ps[b] : P.temp;
   s.alpha = (double)alpha;
   s.valid = s.rule >= SPC_RULE_CHOW && s.rule <= SPC_RULE_OPTLOG && isfinite(alpha) &&
-            isfinite(T) && T >= 0.0f && (T == 0.0f || T >= 1e-20f) &&
-            (s.rule != SPC_RULE_LOSSY || alpha < 1.0f) &&
+            isfinite(T) && T >= 0.0f && (s.rule != SPC_RULE_LOSSY || alpha < 1.0f) &&
             (!P.rule_ps || !P.rule_mask || ((P.rule_mask >> s.rule) & 1u));
   s.greedy = P.force_greedy || T == 0.0f;
-  s.c = kLog2e / ((s.greedy || !s.valid) ? 1.0 : (double)T);
+  s.c = kLog2e / ((s.greedy || !s.valid) ? 1.0 : fmax((double)T, kTempFloor));
   // split c so that z*c_hi + z*c_lo carries ~48 bits of c; c_lo > 0 keeps
   // -inf logits at -inf (never -inf + inf)
   float hi = __double2float_rd(s.c);
@@ -602,35 +672,6 @@ __device__ __forceinline__ int defer_rule(int rule, double alpha, double maxq, d
 }
 
 // ------------------------------------------------------------- row merge
-// The first 64 tile partials of row r (lane l holds tile l) and their TV
-// partials: the loads of a merge, issued ahead of it.
-struct PartHead {
-  TilePart t;
-  double tv;
-  TileMom m;
-};
-
-// Tile partial k of row r; with DEV written earlier in the same launch (read
-// with agent-scope loads).
-template <bool DEV>
-__device__ __forceinline__ TilePart part_at(const Params& P, int r, int k) {
-  if constexpr (DEV) return ld_tile(P.tiles + (int64_t)r * P.nt + k);
-  else return P.tiles[(int64_t)r * P.nt + k];
-}
-
-template <bool DEV = false>
-__device__ __forceinline__ PartHead load_head(const Params& P, int r, bool tv, bool mom) {
-  const int lane = threadIdx.x & 63;
-  PartHead h{{0.0, 0.0, kNegInf, kNegInf, kNegInf, kNegInf, 0x7fffffff, 0x7fffffff}, 0.0,
-             {0.0, 0.0, 0.0}};
-  if (lane < P.nt) {
-    h.t = part_at<DEV>(P, r, lane);
-    if (tv) h.tv = P.tvpart[(int64_t)r * P.nt + lane];
-    if (mom) h.m = P.moms[(int64_t)r * P.nt + lane];
-  }
-  return h;
-}
-
 // A log-loss rule's statistic (nats) from row sums S and moments against the
 // row references (contraction off, as in mom_move).
 __device__ __forceinline__ double log_stat(int rule, double lq2, double lp2, double sq, double sp,
@@ -642,24 +683,30 @@ __device__ __forceinline__ double log_stat(int rule, double lq2, double lp2, dou
                                     : Hq - Hp;
 }
 
-// One wavefront merges the nt tile partials of row r in a fixed order (lane l
-// takes tiles l, l + 64, ...; butterflies combine the lanes), adding the TV
-// partials when `tv`, and with mrule (a log-loss rule or BiLD*) its
-// statistic from the tiles' first moments: against the row references,
+// Wave 0 merges the nt tile partials of row r (written earlier in the same
+// launch) in a fixed order: lane l takes tiles l, l + 64, ...; butterflies
+// combine the lanes.  With mrule (a log-loss rule or BiLD*) it also forms the
+// rule's statistic from the tiles' first moments: against the row references,
 //   H(q) = ln 2 (log2 S_q - H_q / S_q),  H(p) = ln 2 (log2 S_p - H_p / S_p),
 //   D(q, p) = -sum q log p = ln 2 (log2 S_p - X / S_q),
-// each a sum of two non-negative terms.  Every lane returns the same RowStat.
-template <bool DEV = false>
-__device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy, bool tv,
-                                             int mrule, const PartHead& h) {
+// each a sum of two non-negative terms.  kq / kp: the first tile whose
+// largest logit is the row's (it holds the lowest index of the row maximum).
+// Every lane returns the same RowStat.
+__device__ __forceinline__ RowStat merge_row(const Params& P, int r, int mrule, int* kq_out,
+                                             int* kp_out) {
   const int lane = threadIdx.x & 63;
   const int nt = P.nt;
-  const double* tvp = P.tvpart + (int64_t)r * nt;
-  const TilePart& t0 = h.t;
-  double tvs = h.tv;
+  const TilePart* tp = P.tiles + (int64_t)r * nt;
+  const TileMom* mp = P.moms + (int64_t)r * nt;
+  TilePart t0{0.0, 0.0, kNegInf, kNegInf, kNegInf, kNegInf, -1, -1};
+  TileMom m0{0.0, 0.0, 0.0};
+  if (lane < nt) {
+    t0 = ld_tile(tp + lane);
+    if (mrule) m0 = ld_mom(mp + lane);
+  }
   float zq = t0.zmax_q, zp = t0.zmax_p, rq = t0.r_q, rp = t0.r_p;
   for (int k = lane + 64; k < nt; k += 64) {
-    const TilePart tk = part_at<DEV>(P, r, k);
+    const TilePart tk = ld_tile(tp + k);
     zq = fmaxf(zq, tk.zmax_q);
     zp = fmaxf(zp, tk.zmax_p);
     rq = fmaxf(rq, tk.r_q);
@@ -670,38 +717,33 @@ __device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy
   rq = wave_max(rq);
   rp = wave_max(rp);
   double sq = 0.0, sp = 0.0, mhq = 0.0, mhp = 0.0, mx = 0.0;
-  int aq = 0x7fffffff, ap = 0x7fffffff;
-  auto add = [&](const TilePart& tk, const TileMom& mk) {
+  int kq = 0x7fffffff, kp = 0x7fffffff;
+  auto add = [&](const TilePart& tk, const TileMom& mk, int k) {
     // r_k - r is exact in fp64; an all -inf tile has s = 0
     const double gq = (double)tk.r_q - (double)rq, gp = (double)tk.r_p - (double)rp;
     const double fq = exp2_acc(gq), fp = exp2_acc(gp);
     sq += tk.s_q * fq;
     sp += tk.s_p * fp;
-    if (greedy) {
-      if (tk.zmax_q == zq) aq = min(aq, tk.amax_q);
-      if (tk.zmax_p == zp) ap = min(ap, tk.amax_p);
-    }
+    if (tk.zmax_q == zq) kq = min(kq, k);
+    if (tk.zmax_p == zp) kp = min(kp, k);
     if (mrule) {
       mom_add(mhq, mk.hq, tk.s_q, fq, gq);
       mom_add(mhp, mk.hp, tk.s_p, fp, gp);
       mom_add(mx, mk.x, tk.s_q, fq, gp);
     }
   };
-  add(t0, h.m);
-  for (int k = lane + 64; k < nt; k += 64) {
-    add(part_at<DEV>(P, r, k), mrule ? P.moms[(int64_t)r * nt + k] : TileMom{0.0, 0.0, 0.0});
-    if (tv) tvs += tvp[k];
-  }
+  if (lane < nt) add(t0, m0, lane);
+  for (int k = lane + 64; k < nt; k += 64)
+    add(ld_tile(tp + k), mrule ? ld_mom(mp + k) : TileMom{0.0, 0.0, 0.0}, k);
   sq = wave_sum(sq);
   sp = wave_sum(sp);
-  tvs = wave_sum(tvs);
-  aq = wave_min(aq);
-  ap = wave_min(ap);
+  *kq_out = wave_min(kq);
+  *kp_out = wave_min(kp);
   RowStat rs;
   const double lq2 = log2_acc(sq), lp2 = log2_acc(sp);
   rs.lz_q = (double)rq + lq2;
   rs.lz_p = (double)rp + lp2;
-  rs.tv = tvs;
+  rs.tv = 0.0;
   rs.slog = 0.0;
   if (mrule) {
     mhq = wave_sum(mhq);
@@ -711,13 +753,9 @@ __device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy
   }
   rs.zmax_q = zq;
   rs.zmax_p = zp;
-  rs.amax_q = greedy ? aq : -1;
-  rs.amax_p = greedy ? ap : -1;
+  rs.amax_q = -1;
+  rs.amax_p = -1;
   return rs;
-}
-
-__device__ __forceinline__ RowStat merge_row(const Params& P, int r, bool greedy, bool tv) {
-  return merge_row(P, r, greedy, tv, 0, load_head(P, r, tv, false));
 }
 
 // ------------------------------------------------------------- decision
@@ -808,141 +846,11 @@ __device__ __forceinline__ RowDecision decide_row(const SeqParam& sp, const RowS
   return d;
 }
 
-// Wave 0: j* (the first rejection, by one ballot), the outputs when `write`,
-// and the sampling state of sequence b.
-__device__ __forceinline__ void finish_seq(const Params& P, int b, const SeqParam& sp,
-                                           SeqShared& ss, bool write) {
-  const int lane = threadIdx.x;
-  const int gamma = P.gamma, g1 = gamma + 1;
-  const bool on = lane < g1;
-  const int64_t row = (int64_t)b * g1 + lane;
-  RowDecision d{};
-  if (on && sp.valid) d = ss.rows[lane];
-  // a NaN second-pass statistic marks a row whose one-read pass gave up
-  // waiting for its tiles: the sequence is reported invalid
-  const bool lost = needs_pass2(sp) && __ballot(on && d.tv != d.tv) != 0;
-  if (!sp.valid || lost) {
-    if (write) {
-      if (on) P.out_defer[row] = 0;
-      if (lane == 0) {
-        P.out_accept[b] = -1;
-        P.out_token[b] = -1;
-        if (P.out_norm) P.out_norm[b] = 0.0f;
-      }
-    }
-    if (lane == 0) ss.seq = SeqState{-1, kNone, 0.0f, 0};
-    return;
-  }
-  if (write && on) {
-    P.out_defer[row] = (uint8_t)d.delta;
-    if (P.out_stats) {
-      const double T = sp.greedy ? 1.0 : kLog2e / sp.c;
-      float* o = P.out_stats + row * 8;
-      o[0] = (float)((double)d.rs.zmax_q / T);
-      o[1] = (float)(d.rs.lz_q * kLn2);
-      o[2] = d.maxq;
-      o[3] = (float)((double)d.rs.zmax_p / T);
-      o[4] = (float)(d.rs.lz_p * kLn2);
-      o[5] = d.maxp;
-      o[6] = d.tv;
-      o[7] = (float)d.rs.slog;
-    }
-    if (P.out_argmax) {
-      P.out_argmax[row * 2 + 0] = d.rs.amax_q;
-      P.out_argmax[row * 2 + 1] = d.rs.amax_p;
-    }
-  }
-  const unsigned long long rej = __ballot(on && !d.keep);
-  const int jstar = __ffsll(rej) - 1;  // bit gamma is always set
-  const int dstar = lane_i32(d.delta, jstar);
-  const int aq = lane_i32(d.rs.amax_q, jstar);
-  const int ap = lane_i32(d.rs.amax_p, jstar);
-  const float ug = lane_f32(d.u, gamma);
-  if (lane == 0) {
-    SeqState s{jstar, kNone, 0.0f, 0};
-    if (sp.greedy) {
-      if (write) {
-        P.out_token[b] = (dstar || sp.rule == SPC_RULE_LOSSY) ? ap : aq;
-        if (P.out_norm) P.out_norm[b] = 1.0f;
-      }
-    } else {
-      if (is_token(sp.rule)) {
-        s.kind = (jstar < gamma) ? kTokRes : kTokPi;
-      } else if (sp.rule == SPC_RULE_LOSSY) {
-        // residual max(0, pi - q) = max(0, p - q); extra token from p
-        s.kind = (jstar < gamma) ? kResidual : kP;
-      } else {
-        // a rejection with delta = 0 only happens for an out-of-range draft;
-        // its residual max(0, q - q) is empty, so p is sampled instead
-        s.kind = (jstar < gamma) ? (dstar ? kResidual : kP) : (dstar ? kP : kQ);
-      }
-      s.u = ug;
-    }
-    if (write) P.out_accept[b] = jstar;
-    ss.seq = s;
-  }
-}
-
-// Whole block: merge and decide the rows of sequence b (wave w takes rows
-// w, w + 4, ...), then wave 0 finds j*.  With `write` the outputs are written
-// too: every sampling workgroup of a sequence reaches the same decision by
-// the same fixed-order computation, and one of them writes it.
-template <int DT>
-__device__ __forceinline__ void decide_seq(const Params& P, int b, const SeqParam& sp,
-                                           SeqShared& ss, bool write) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int gamma = P.gamma, g1 = gamma + 1, V = P.V;
-  if (sp.valid) {
-    // Loads in dependency order: the first row's partials and the draft
-    // data (lane l of wave wv takes row wv + kSampWaves * l) go out together;
-    // the logits at the draft tokens follow the tokens and stay in flight
-    // while the rows merge.
-    const bool tv = needs_pass2(sp);
-    const bool mom = needs_mom(sp);
-    // greedy TokenV2/V3 and BiLD* read p at the drafter's argmax
-    const bool greedy_pa = sp.greedy && ((is_token(sp.rule) && sp.rule != SPC_RULE_TOKEN_V1) ||
-                                         sp.rule == SPC_RULE_BILD);
-    PartHead h{};
-    if (wv < g1) h = load_head(P, b * g1 + wv, tv, mom);
-    const int jl = wv + kSampWaves * lane;
-    int x = -1;
-    float zqx = 0.0f, zpx = 0.0f, u = 0.0f;
-    if (jl < g1) {
-      const int64_t row = (int64_t)b * g1 + jl;
-      if (!sp.greedy) u = P.uniforms[row];
-      if (jl < gamma) {
-        x = P.draft[(int64_t)b * gamma + jl];
-        if (!sp.greedy && x >= 0 && x < V) {
-          zqx = load_logit<DT>(P.q, row, V, x);
-          zpx = load_logit<DT>(P.p, row, V, x);
-        }
-      }
-    }
-    for (int i = 0; wv + kSampWaves * i < g1; ++i) {
-      const int j = wv + kSampWaves * i;
-      // the next row's partials load while this row merges
-      PartHead hn{};
-      if (j + kSampWaves < g1) hn = load_head(P, b * g1 + j + kSampWaves, tv, mom);
-      const RowStat rs = merge_row(P, b * g1 + j, sp.greedy, tv, mom ? sp.rule : 0, h);
-      h = hn;
-      const float zpa = (greedy_pa && rs.amax_q >= 0 && rs.amax_q < V)
-                            ? load_logit<DT>(P.p, (int64_t)b * g1 + j, V, rs.amax_q)
-                            : lane_f32(zpx, i);
-      const RowDecision d = decide_row(sp, rs, j, gamma, V, lane_i32(x, i), lane_f32(zqx, i),
-                                       zpa, lane_f32(u, i));
-      if (lane == 0) ss.rows[j] = d;
-    }
-  }
-  __syncthreads();
-  if (threadIdx.x < 64) finish_seq(P, b, sp, ss, write);
-  __syncthreads();
-}
-
 // ------------------------------------------------------------- sampling
 // A chunk is what one wavefront covers reading wave-contiguously: lane l's
-// lane load i covers entries (i * 64 + l) * VW .. + VW - 1 of it.  The
-// residual pass sums SampChunks; a statistics tile is kSampWaves consecutive
-// SubChunks, one per wavefront of a sampling workgroup.
+// lane load i covers entries (i * 64 + l) * VW .. + VW - 1 of it.  A
+// statistics tile is a whole number of SubChunks; the residual job and the
+// in-tile draw sum them in the same order.
 template <int DT, bool VEC, int U_>
 struct Chunk {
   static constexpr int U = U_;
@@ -950,13 +858,12 @@ struct Chunk {
   static constexpr int N = 64 * U * VW;  // entries per chunk
 };
 // A sub-chunk of a TN-entry tile drawn from by NWV wavefronts: one per
-// wavefront, or several of at most 4 lane loads each.
+// wavefront, or several of at most 2 lane loads each (few registers: the
+// draw shares its launch with the statistics tiles).
 template <int DT, bool VEC, int NWV, int TN = StatTile<DT, VEC>::N>
-using SubChunk = Chunk<DT, VEC, (TN / (64 * NWV * Tile<DT, VEC, 1>::VW) < 4)
+using SubChunk = Chunk<DT, VEC, (TN / (64 * NWV * Tile<DT, VEC, 1>::VW) < 2)
                                     ? TN / (64 * NWV * Tile<DT, VEC, 1>::VW)
-                                    : 4>;
-template <int DT, bool VEC>
-using SampChunk = Chunk<DT, VEC, VEC ? 2 : 8>;
+                                    : 2>;
 
 template <class C>
 using ChunkRegs = uint32_t[C::U][C::NW];
@@ -977,32 +884,30 @@ __device__ __forceinline__ void load_chunk(const char* row, int64_t c0, int V, C
 // Sources of the part masses of the sampled distribution: the statistics
 // partials per tile (q or p: each tile's share of the normaliser), the
 // statistics and eta partials together (a token rule's target), or the
-// residual masses per SampChunk computed by the sampling pass.
+// residual masses per tile summed by the residual job.
 enum MassSrc : int { kSrcStatsQ = 0, kSrcStatsP = 1, kSrcPass = 3, kSrcTokPi = 4,
                      kSrcDraft = 5 };
 
 template <int SRC>
 __device__ __forceinline__ double part_mass(const Params& P, int64_t row, int b, int k,
                                             const RowStat& rs) {
-  if constexpr (SRC == kSrcStatsQ) {
-    const TilePart& t = P.tiles[row * P.nt + k];
+  // every partial was written earlier in the same launch: agent-scope loads
+  if constexpr (SRC == kSrcStatsQ || SRC == kSrcDraft) {
+    const TilePart t = ld_tile(P.tiles + row * P.nt + k);
     return t.s_q * exp2_acc((double)t.r_q - rs.lz_q);
   } else if constexpr (SRC == kSrcStatsP) {
-    const TilePart& t = P.tiles[row * P.nt + k];
+    const TilePart t = ld_tile(P.tiles + row * P.nt + k);
     return t.s_p * exp2_acc((double)t.r_p - rs.lz_p);
   } else if constexpr (SRC == kSrcTokPi) {
     // Alg. 6's target over a tile: its q mass less the eta partial (the q
     // mass where r = 1), plus eta times its p mass
-    const TilePart& t = P.tiles[row * P.nt + k];
+    const TilePart t = ld_tile(P.tiles + row * P.nt + k);
     const double qm = t.s_q * exp2_acc((double)t.r_q - rs.lz_q);
     const double pm = t.s_p * exp2_acc((double)t.r_p - rs.lz_p);
-    return fmax(qm - P.tvpart[row * P.nt + k], 0.0) + rs.tv * pm;
-  } else if constexpr (SRC == kSrcDraft) {
-    // the q statistics partials of the drafter kernel's own launch
-    const TilePart t = ld_tile(P.tiles + row * P.nt + k);
-    return t.s_q * exp2_acc((double)t.r_q - rs.lz_q);
+    const double* ep = P.tvpart + (row * P.nt + k) * kParts;  // the tile's eta partials
+    return fmax(qm - (ld_dev_f64(ep) + ld_dev_f64(ep + 1)), 0.0) + rs.tv * pm;
   } else {
-    return ld_dev_f64(P.masses + (int64_t)b * P.nc + k);
+    return ld_dev_f64(P.masses + (int64_t)b * P.nt * kParts + k);
   }
 }
 
@@ -1074,55 +979,6 @@ __device__ __forceinline__ double find_part(const Params& P, int64_t row, int b,
   return W;
 }
 
-// Whole block: residual masses (KIND) of the SampChunks of a row (K
-// sampling workgroups per sequence): wave w of workgroup kw takes chunks
-// kw * kSampWaves + w, then + K * kSampWaves, ...; the next chunk loads while
-// one is summed, and chunk c's mass goes to masses[c].  No block barrier:
-// every wave drains its own stores.
-template <int DT, bool VEC, int KIND>
-__device__ __forceinline__ void residual_masses(const char* qrow, const char* prow, int V, int nc,
-                                                int K, int kw, const ProbScale& ps,
-                                                double* masses) {
-  using C = SampChunk<DT, VEC>;
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int step = K * kSampWaves;
-  ChunkRegs<C> wq, wp, nq = {}, np = {};
-  {
-    const int c = kw * kSampWaves + wv;
-    const int64_t c0 = c < nc ? (int64_t)c * C::N : (int64_t)V;
-    load_chunk<DT, VEC, C>(qrow, c0, V, wq);
-    load_chunk<DT, VEC, C>(prow, c0, V, wp);
-  }
-  for (int b0 = kw * kSampWaves; b0 < nc; b0 += step) {  // block-uniform
-    const int c = b0 + wv;
-    if (b0 + step < nc) {  // prefetch the next batch
-      const int cn = c + step;
-      const int64_t c0 = cn < nc ? (int64_t)cn * C::N : (int64_t)V;
-      load_chunk<DT, VEC, C>(qrow, c0, V, nq);
-      load_chunk<DT, VEC, C>(prow, c0, V, np);
-    }
-    double acc = 0.0;
-#pragma unroll
-    for (int i = 0; i < C::U; ++i) {
-      float t = 0.0f;
-#pragma unroll
-      for (int e = 0; e < C::VW; ++e)
-        t += weight_of<KIND>(elem<DT, VEC>(wq[i], e), elem<DT, VEC>(wp[i], e), ps);
-      acc += (double)t;
-    }
-    acc = wave_sum(acc);
-    if (lane == 0 && c < nc) st_dev_f64(masses + c, acc);
-#pragma unroll
-    for (int i = 0; i < C::U; ++i)
-#pragma unroll
-      for (int j = 0; j < C::NW; ++j) {
-        wq[i][j] = nq[i][j];
-        wp[i][j] = np[i][j];
-      }
-  }
-  vmem_drain();
-}
-
 // Wave 0: the in-chunk draw in the chunk starting at entry c0.  Lane loads
 // are scanned in entry order -- lane load i, then lane -- for the first one
 // where the running mass exceeds rem; its lane then walks its VW entries.
@@ -1151,6 +1007,7 @@ __device__ __forceinline__ void pick_wave(const Params& P, int b, int64_t row, i
       const float w = weight_of<KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
       m += (double)w;
       if (w > 0.0f) last_pos = max(last_pos, (int)(base + e));
+      if (e & 1) __builtin_amdgcn_sched_barrier(0);
     }
     const double incl = carry + wave_incl_scan(m);
     if (hlane < 0) {  // wave-uniform
@@ -1182,16 +1039,17 @@ __device__ __forceinline__ void pick_wave(const Params& P, int b, int64_t row, i
     run += (double)w;
     if (w > 0.0f) lastw = (int)(hbase + e);
     if (hit < 0 && run > rem && w > 0.0f) hit = (int)(hbase + e);
+    if (e & 1) __builtin_amdgcn_sched_barrier(0);
   }
   P.out_token[b] = hit >= 0 ? hit : lastw;  // rounding inside the lane load
 }
 
-// Whole block: the draw inside statistics tile t0 (entry offset).  Each
-// wavefront sums the weights of one SubChunk; wave 0 scans the kSampWaves
-// sums for the sub-chunk where rem is crossed and draws inside it.
+// Whole block: the masses of the sub-chunks of the TN-entry tile at entry t0
+// of a row under the distribution KIND, in sh.dv[0 .. NS-1] (wave w sums
+// sub-chunks w, w + NWV, ...).  Ends with a block barrier.
 template <int DT, bool VEC, int KIND, int NWV, int TN = StatTile<DT, VEC>::N>
-__device__ __forceinline__ void pick_tile(const Params& P, int b, int64_t row, int64_t t0,
-                                          double rem, const ProbScale& ps, SharedT<NWV>& sh) {
+__device__ __forceinline__ void subchunk_masses(const Params& P, int64_t row, int64_t t0,
+                                                const ProbScale& ps, SharedT<NWV>& sh) {
   using C = SubChunk<DT, VEC, NWV, TN>;
   constexpr int NS = TN / C::N;  // sub-chunks of the tile
   static_assert(NS * C::N == TN && NS % NWV == 0 && NS <= 64,
@@ -1201,7 +1059,7 @@ __device__ __forceinline__ void pick_tile(const Params& P, int b, int64_t row, i
   const int V = P.V;
   const char* qrow = (const char*)P.q + row * V * EB;
   const char* prow = (const char*)P.p + row * V * EB;
-  for (int sc = wv; sc < NS; sc += NWV) {  // wave wv sums sub-chunks wv, wv + NWV, ...
+  for (int sc = wv; sc < NS; sc += NWV) {
     ChunkRegs<C> cq = {}, cp = {};
     if (KIND != kP) load_chunk<DT, VEC, C>(qrow, t0 + sc * C::N, V, cq);
     if (KIND != kQ) load_chunk<DT, VEC, C>(prow, t0 + sc * C::N, V, cp);
@@ -1210,14 +1068,38 @@ __device__ __forceinline__ void pick_tile(const Params& P, int b, int64_t row, i
     for (int i = 0; i < C::U; ++i) {
       float t = 0.0f;
 #pragma unroll
-      for (int e = 0; e < C::VW; ++e)
+      for (int e = 0; e < C::VW; ++e) {
         t += weight_of<KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
+        // two entries at a time keep the weights' temporaries few
+        if (e & 1) __builtin_amdgcn_sched_barrier(0);
+      }
       m += (double)t;
     }
     m = wave_sum(m);
     if (lane == 0) sh.dv[sc] = m;
   }
   __syncthreads();
+}
+
+// Wave 0: the total of a tile's sub-chunk masses (after subchunk_masses),
+// summed by the same scan the in-tile draw runs, so a draw whose target falls
+// in this tile by the tile masses finds it among the sub-chunks.
+template <int DT, bool VEC, int NWV, int TN = StatTile<DT, VEC>::N>
+__device__ __forceinline__ double tile_mass(const SharedT<NWV>& sh) {
+  constexpr int NS = TN / SubChunk<DT, VEC, NWV, TN>::N;
+  const int lane = threadIdx.x & 63;
+  return lane_f64(wave_incl_scan(lane < NS ? sh.dv[lane] : 0.0), NS - 1);
+}
+
+// Whole block: the draw inside the tile at entry t0.  Wave 0 scans the
+// sub-chunk masses for the sub-chunk where rem is crossed and draws inside it.
+template <int DT, bool VEC, int KIND, int NWV, int TN = StatTile<DT, VEC>::N>
+__device__ __forceinline__ void pick_tile(const Params& P, int b, int64_t row, int64_t t0,
+                                          double rem, const ProbScale& ps, SharedT<NWV>& sh) {
+  using C = SubChunk<DT, VEC, NWV, TN>;
+  constexpr int NS = TN / C::N;
+  subchunk_masses<DT, VEC, KIND, NWV, TN>(P, row, t0, ps, sh);
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   if (wv != 0) return;
   const double ml = lane < NS ? sh.dv[lane] : 0.0;
   const double incl = wave_incl_scan(ml);
@@ -1235,65 +1117,7 @@ __device__ __forceinline__ void pick_tile(const Params& P, int b, int64_t row, i
   pick_wave<DT, VEC, C, KIND>(P, b, row, t0 + c * C::N, r, ps);
 }
 
-// Whole block: the inverse-CDF draw of sequence b at row `row` (the row of
-// j*) from the distribution `kind`, whose part masses come from `src`.  Wave 0
-// finds the part; the draw inside a residual chunk runs in wave 0, the draw
-// inside a statistics tile uses every wavefront.  An empty residual (possible
-// only through rounding) is replaced by p.
-template <int DT, bool VEC>
-__device__ __forceinline__ void draw(const Params& P, int b, int64_t row, int kind, int src,
-                                     float u, const SeqParam& sp, const RowStat& rs,
-                                     SeqShared& ss, SampShared& sh) {
-  if (threadIdx.x < 64) {
-    int ks;
-    double rem, W;
-    if (src == kSrcStatsQ) W = find_part<kSrcStatsQ>(P, row, b, P.nt, rs, u, &ks, &rem);
-    else if (src == kSrcStatsP) W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
-    else if (src == kSrcTokPi) W = find_part<kSrcTokPi>(P, row, b, P.nt, rs, u, &ks, &rem);
-    else W = find_part<kSrcPass>(P, row, b, P.nc, rs, u, &ks, &rem);
-    if ((kind == kResidual || kind == kTokRes) && !(W > 0.0)) {
-      kind = kP;
-      src = kSrcStatsP;
-      W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
-    }
-    if (threadIdx.x == 0) {
-      ss.pk = PickState{ks, kind, src, rem};
-      if (P.out_norm) P.out_norm[b] = (float)W;
-      if (ks < 0) P.out_token[b] = -1;
-    }
-  }
-  __syncthreads();
-  const PickState pk = ss.pk;
-  if (pk.k < 0) return;  // block-uniform
-  const ProbScale ps = prob_scale(sp, rs, pk.kind == kTokRes || pk.kind == kTokPi);
-  constexpr int TN = StatTile<DT, VEC>::N;
-  if (pk.src == kSrcPass) {
-    using SC = SampChunk<DT, VEC>;
-    if (threadIdx.x < 64) {
-      if (pk.kind == kTokRes)
-        pick_wave<DT, VEC, SC, kTokRes>(P, b, row, (int64_t)pk.k * SC::N, pk.rem, ps);
-      else
-        pick_wave<DT, VEC, SC, kResidual>(P, b, row, (int64_t)pk.k * SC::N, pk.rem, ps);
-    }
-  } else if (pk.kind == kQ) {
-    pick_tile<DT, VEC, kQ, kSampWaves>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
-  } else if (pk.kind == kP) {
-    pick_tile<DT, VEC, kP, kSampWaves>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
-  } else if (pk.kind == kTokPi) {
-    pick_tile<DT, VEC, kTokPi, kSampWaves>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
-  } else {
-    pick_tile<DT, VEC, kResidual, kSampWaves>(P, b, row, (int64_t)pk.k * TN, pk.rem, ps, sh);
-  }
-}
-
-// ================================================================ kernels
-
-// Statistics pass.  grid (nt, R): stats tile k of row r.  Each thread takes
-// the exact max of its entries and the sum of 2^(z c - r_t), r_t = max * c_hi
-// (a reference near its largest z c); each wave combines its threads against
-// the wave max, and thread 0 the waves against the tile max.  With ARGMAX
-// (batches that may hold greedy rows) the lowest entry attaining the max is
-// found as well.
+// ================================================================ statistics tiles
 // Thread sums of one statistics tile: s = sum 2^a over the thread's entries,
 // a = z c - r (r the thread reference); with MOM (a set of kMom* bits) also
 // the first moments it names: hq = sum 2^a_q a_q, hp = sum 2^a_p a_p and
@@ -1349,17 +1173,15 @@ __device__ __forceinline__ void tile_sums(const uint32_t (&wq)[StatTile<DT, VEC>
 }
 
 // The partial of statistics tile k of row r from its loaded entries (wq, wp),
-// written by thread 0: with DEV through agent-scope stores, for readers in
-// the same launch.
-template <int DT, bool VEC, bool ARGMAX, int MOM, bool DEV>
+// written by thread 0 through agent-scope stores, for readers in the same
+// launch.
+template <int DT, bool VEC, int MOM>
 __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, const SeqParam& sp,
                                              const uint32_t (&wq)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
                                              const uint32_t (&wp)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
                                              Shared& sh) {
   using T = StatTile<DT, VEC>;
-  const int64_t t0 = (int64_t)k * T::N;
-  // Thread max, from the maxima of its lane loads; with ARGMAX also the
-  // lowest entry attaining it (indices fit 32 bits: V < 2^31).
+  // Thread max, from the maxima of its lane loads.
   float gq[T::U], gp[T::U];
 #pragma unroll
   for (int i = 0; i < T::U; ++i) {
@@ -1378,23 +1200,8 @@ __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, cons
     mq = fmaxf(mq, gq[i]);
     mp = fmaxf(mp, gp[i]);
   }
-  int iq = 0x7fffffff, ip = 0x7fffffff;
-  const int base = (int)t0 + (int)threadIdx.x * T::VW;
-  if constexpr (ARGMAX && !MOM) {
-    iq = first_max_index<DT, VEC, T::U, kThreads>(wq, gq, mq, base);
-    ip = first_max_index<DT, VEC, T::U, kThreads>(wp, gp, mp, base);
-  }
   const float rq = (mq == kNegInf) ? 0.0f : mq * sp.c_hi;
   const float rp = (mp == kNegInf) ? 0.0f : mp * sp.c_hi;
-  if constexpr (DEV) {
-    // the packed words outlive this tile's statistics (the one-read second
-    // pass uses them): unpack again below rather than hold all the entries
-#pragma unroll
-    for (int i = 0; i < T::U; ++i)
-#pragma unroll
-      for (int j = 0; j < T::NW; ++j)
-        asm volatile("" : "+v"(const_cast<uint32_t&>(wq[i][j])), "+v"(const_cast<uint32_t&>(wp[i][j])));
-  }
   float sq = 0.0f, spp = 0.0f, hq = 0.0f, hp = 0.0f, xq = 0.0f;
   constexpr bool mom = MOM;
   tile_sums<DT, VEC, MOM>(wq, wp, sp, rq, rp, sq, spp, hq, hp, xq);
@@ -1402,20 +1209,6 @@ __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, cons
   // accumulation into the conditional combine below and keeps every
   // exponential of the tile live until then
   if constexpr (MOM) asm volatile("" : "+v"(hq), "+v"(hp), "+v"(xq), "+v"(sq), "+v"(spp));
-  if constexpr (ARGMAX && MOM) {
-    // the lowest entry equal to the thread max, in a pass of its own after
-    // the sums
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int i = T::U - 1; i >= 0; --i)
-#pragma unroll
-      for (int e = T::VW - 1; e >= 0; --e) {
-        const int idx = base + i * kThreads * T::VW + e;
-        if (elem<DT, VEC>(wq[i], e) == mq) iq = idx;
-        if (elem<DT, VEC>(wp[i], e) == mp) ip = idx;
-      }
-    asm volatile("" : "+v"(iq), "+v"(ip));
-  }
   // Wave partials against the wave max (r_t - r_w is exact in fp64; only its
   // rounding to float is inexact), then one barrier and thread 0 combines the
   // waves in order against the tile max.
@@ -1433,17 +1226,11 @@ __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, cons
     mhp = wave_sum(mp == kNegInf ? 0.0 : mom_move(hp, spp, fp, ep));
     mx = wave_sum(mq == kNegInf ? 0.0 : mom_move(xq, sq, fq, ep));
   }
-  if constexpr (ARGMAX) {
-    iq = wave_min((mq == Wq) ? iq : 0x7fffffff);
-    ip = wave_min((mp == Wp) ? ip : 0x7fffffff);
-  }
   if (lane == 0) {
     sh.m[wv][0] = Wq;
     sh.m[wv][1] = Wp;
     sh.d[wv][0] = dq;
     sh.d[wv][1] = dp;
-    sh.i[wv][0] = iq;
-    sh.i[wv][1] = ip;
     if constexpr (mom) {
       sh.h[wv][0] = mhq;
       sh.h[wv][1] = mhp;
@@ -1460,7 +1247,6 @@ __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, cons
     }
     const float Rq = Mq * sp.c_hi, Rp = Mp * sp.c_hi;
     double tq = 0.0, tp = 0.0;
-    int aq = 0x7fffffff, ap = 0x7fffffff;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
       const float wq_ = sh.m[w][0], wp_ = sh.m[w][1];
@@ -1468,8 +1254,6 @@ __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, cons
         tq += sh.d[w][0] * (double)exp2_hw((float)((double)(wq_ * sp.c_hi) - (double)Rq));
       if (wp_ != kNegInf)
         tp += sh.d[w][1] * (double)exp2_hw((float)((double)(wp_ * sp.c_hi) - (double)Rp));
-      if (ARGMAX && wq_ == Mq) aq = min(aq, sh.i[w][0]);
-      if (ARGMAX && wp_ == Mp) ap = min(ap, sh.i[w][1]);
     }
     TilePart t;
     t.s_q = tq;
@@ -1478,12 +1262,9 @@ __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, cons
     t.r_p = (Mp == kNegInf) ? kNegInf : Rp;
     t.zmax_q = Mq;
     t.zmax_p = Mp;
-    t.amax_q = ARGMAX ? aq : -1;
-    t.amax_p = ARGMAX ? ap : -1;
-    if constexpr (DEV)
-      st_tile(P.tiles + (int64_t)r * P.nt + k, t);
-    else
-      P.tiles[(int64_t)r * P.nt + k] = t;
+    t.amax_q = -1;
+    t.amax_p = -1;
+    st_tile(P.tiles + (int64_t)r * P.nt + k, t);
     if constexpr (mom) {
       // the waves' moments against the tile references, in wave order
       TileMom m{0.0, 0.0, 0.0};
@@ -1499,61 +1280,19 @@ __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, cons
         if (wq_ != kNegInf)
           mom_add(m.x, sh.h[w][2], sh.d[w][0], fq_, wp_ == kNegInf ? -__builtin_huge_val() : gp);
       }
-      P.moms[(int64_t)r * P.nt + k] = m;
+      st_mom(P.moms + (int64_t)r * P.nt + k, m);
     }
   }
 }
 
-template <int DT, bool VEC, bool ARGMAX, int MOM>
-__device__ __forceinline__ void stats_tile(const Params& P) {
-  using T = StatTile<DT, VEC>;
-  __shared__ Shared sh;
-  const int k = blockIdx.x, r = blockIdx.y;
-  const SeqParam sp = seq_param(P, r / (P.gamma + 1));
-  // rows that need first moments belong to the moment kernel (block-uniform)
-  if (MOM ? !needs_mom(sp) : (P.mom_split && needs_mom(sp))) return;
-  const int V = P.V;
-  const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
-  const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
-  const int64_t t0 = (int64_t)k * T::N;
-  uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
-  load_tile<DT, VEC, T::U, true>(qrow, t0, V, wq, threadIdx.x);
-  load_tile<DT, VEC, T::U, true>(prow, t0, V, wp, threadIdx.x);
-  tile_partial<DT, VEC, ARGMAX, MOM, false>(P, r, k, sp, wq, wp, sh);
-}
-
-template <int DT, bool VEC, bool ARGMAX>
-__global__ __launch_bounds__(kThreads) void k_stats(Params P) {
-  stats_tile<DT, VEC, ARGMAX, 0>(P);
-}
-
-// With first moments, for the rows of BiLD* (temperature > 0) and log-loss
-// sequences only; the plain kernel takes every other row.  Held to
-// SPC_MOM_OCCUPANCY resident workgroups per CU: left free, the compiler
-// keeps every exponential of the tile live at once.
-#ifndef SPC_MOM_OCCUPANCY
-#define SPC_MOM_OCCUPANCY 6
-#endif
-template <int DT, bool VEC, bool ARGMAX, int MS>
-__global__ __launch_bounds__(kThreads, SPC_MOM_OCCUPANCY) void k_stats_mom(Params P) {
-  stats_tile<DT, VEC, ARGMAX, MS>(P);
-}
-
-template <int DT, bool VEC, int MS>
-void launch_mom(const Params& P, bool argmax, dim3 grid, hipStream_t st) {
-  if (argmax)
-    hipLaunchKernelGGL((k_stats_mom<DT, VEC, true, MS>), grid, dim3(kThreads), 0, st, P);
-  else
-    hipLaunchKernelGGL((k_stats_mom<DT, VEC, false, MS>), grid, dim3(kThreads), 0, st, P);
-}
 
 // The second-pass weight summed over a thread's entries of one statistics
 // tile: for a token rule eta's share (the q mass of the entries the rule
 // marks), else max(0, p - q) (D_TV of Lemma 3) in float32.
-template <int DT, bool VEC>
+template <int DT, bool VEC, bool TOK>
 __device__ __forceinline__ double pass2_sum(const uint32_t (&wq)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
                                             const uint32_t (&wp)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
-                                            const ProbScale& ps, bool tok) {
+                                            const ProbScale& ps) {
   using T = StatTile<DT, VEC>;
   double acc = 0.0;
 #pragma unroll
@@ -1562,7 +1301,7 @@ __device__ __forceinline__ double pass2_sum(const uint32_t (&wq)[StatTile<DT, VE
 #pragma unroll
     for (int e = 0; e < T::VW; ++e) {
       const float zq = elem<DT, VEC>(wq[i], e), zp = elem<DT, VEC>(wp[i], e);
-      if (tok) {
+      if constexpr (TOK) {
         t += token_r(ps.tok, zq, zp) ? prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo) : 0.0f;
       } else {
         // D_TV for the deferral decision only, where an absolute error of
@@ -1572,6 +1311,7 @@ __device__ __forceinline__ double pass2_sum(const uint32_t (&wq)[StatTile<DT, VE
         const float pp = prob(zp, ps.c_hi, ps.c_lo, ps.p_hi, ps.p_lo);
         t += fmaxf(pp - pq, 0.0f);
       }
+      if (e & 1) __builtin_amdgcn_sched_barrier(0);
     }
     acc += (double)t;
     // one lane load at a time: with the whole tile already in registers the
@@ -1600,228 +1340,680 @@ __device__ __forceinline__ bool eta_from_stats(const TokenRule& tr, const TilePa
   return false;
 }
 
-// TV pass (OPT rows at temperature > 0): D_TV(p, q) of Lemma 3, which needs
-// both normalisers.  grid (nt, R): stats tile k of row r; wave 0 merges the
-// row's statistics first (a fixed-order computation every tile of the row
-// repeats identically).
-template <int DT, bool VEC>
-__global__ __launch_bounds__(kThreads) void k_tv(Params P) {
+
+// ================================================================ the step
+// Jobs a row or a sequence publishes for the job pass that follows: a TV or
+// eta second pass over a row and the residual masses of row j* of a sequence
+// are "row jobs" of nt chunks (one per tile); the two halves of a greedy
+// row's argmax and the draws from statistics partials are single chunks.
+enum JobKind : int { kJobTv = 1, kJobEta = 2, kJobRes = 3, kJobArg = 4, kJobDraw = 5 };
+
+// A job entry: kind (bits 60..63), an extra field (bits 32..59: the argmax
+// tensor, or a draw's sample kind and j*) and the row or sequence it belongs
+// to (bits 0..31).
+__device__ __forceinline__ uint64_t job_entry(int kind, uint32_t extra, uint32_t id) {
+  return ((uint64_t)kind << 60) | ((uint64_t)(extra & 0x0fffffffu) << 32) | (uint64_t)id;
+}
+__device__ __forceinline__ int job_kind(uint64_t e) { return (int)(e >> 60); }
+__device__ __forceinline__ uint32_t job_extra(uint64_t e) {
+  return (uint32_t)(e >> 32) & 0x0fffffffu;
+}
+__device__ __forceinline__ uint32_t job_id(uint64_t e) { return (uint32_t)e; }
+
+// Job counters: jobs published per pass and list, workgroups per pass that
+// have read them.
+__device__ __forceinline__ uint32_t* hdr_word(const Params& P, int line) {
+  return P.hdr + (int64_t)line * kLineWords;
+}
+__device__ __forceinline__ int hdr_line(int phase, bool single) { return 2 * (phase - 1) + single; }
+// The job entries of a pass: its row jobs, then its single jobs.
+__device__ __forceinline__ uint64_t* job_list(const Params& P, int phase, bool single) {
+  return P.jobs + (int64_t)(phase - 1) * (P.job_slots + P.single_slots) +
+         (single ? P.job_slots : 0);
+}
+__device__ __forceinline__ uint32_t* row_word(const Params& P, int64_t r, int w) {
+  return P.rowline + r * kLineWords + w;
+}
+__device__ __forceinline__ uint64_t* seq_mask(const Params& P, int64_t b) {
+  return reinterpret_cast<uint64_t*>(row_word(P, b, kSeqMask));
+}
+// The completion counter of row job `s` of a phase.
+__device__ __forceinline__ uint32_t* job_done(const Params& P, int phase, int64_t s) {
+  return P.jobline + ((int64_t)(phase - 1) * P.job_slots + s) * kLineWords;
+}
+__device__ __forceinline__ uint64_t lane_u64(uint64_t v, int l) {
+  return ((uint64_t)(uint32_t)lane_i32((int)(v >> 32), l) << 32) |
+         (uint64_t)(uint32_t)lane_i32((int)(uint32_t)v, l);
+}
+
+// One lane: publish a row job (whose inputs are stored) and initialise its
+// completion counter; the job pass that reads them is a later launch.  A
+// pass never holds more jobs than its lists have slots (at most one TV or
+// eta job per row and one draw per sequence); the bounds only keep a broken
+// count from writing past them.
+__device__ __forceinline__ void publish_row_job(const Params& P, int phase, int kind,
+                                                uint32_t id) {
+  if (phase > 2) return;
+  const uint32_t s = add_u32(hdr_word(P, hdr_line(phase, false)), 1u);
+  if ((int64_t)s >= P.job_slots) return;
+  st_u32(job_done(P, phase, s), 0u);
+  st_u64(job_list(P, phase, false) + s, job_entry(kind, 0u, id));
+}
+__device__ __forceinline__ void publish_single(const Params& P, int phase, int kind,
+                                               uint32_t extra, uint32_t id) {
+  if (phase > 2) return;
+  const uint32_t s = add_u32(hdr_word(P, hdr_line(phase, true)), 1u);
+  if ((int64_t)s >= P.single_slots) return;
+  st_u64(job_list(P, phase, true) + s, job_entry(kind, extra, id));
+}
+
+// Shared state of a job workgroup.
+struct StepShared {
+  Shared sh;
+  RowStat rs;
+  PickState pk;
+  int a[4];  // values thread 0 or wave 0 hands to the block
+};
+
+// Wave: sequence b's first rejection is j* = f.  Writes its accept length,
+// then the greedy token, or publishes the draw -- from the statistics
+// partials (a single job) or from the residual of row f (a row job) -- to
+// the job pass `phase`.
+template <int DT>
+__device__ __forceinline__ void seq_finish_w(const Params& P, int b, int f, const SeqParam& sp,
+                                             int phase) {
+  const int gamma = P.gamma, g1 = gamma + 1;
+  const int64_t row = (int64_t)b * g1 + f;
+  if ((threadIdx.x & 63) != 0) return;
+  if (!sp.valid) {
+    P.out_accept[b] = -1;
+    P.out_token[b] = -1;
+    if (P.out_norm) P.out_norm[b] = 0.0f;
+    return;
+  }
+  P.out_accept[b] = f;
+  const int dstar = (ld_i32(P.rowdec + row) >> 1) & 1;
+  if (sp.greedy) {
+    const RowStat rs = ld_rowstat(P.rowstat + row);
+    P.out_token[b] = (dstar || sp.rule == SPC_RULE_LOSSY) ? rs.amax_p : rs.amax_q;
+    if (P.out_norm) P.out_norm[b] = 1.0f;
+    return;
+  }
+  int kind;
+  if (is_token(sp.rule)) {
+    kind = (f < gamma) ? kTokRes : kTokPi;
+  } else if (sp.rule == SPC_RULE_LOSSY) {
+    // residual max(0, pi - q) = max(0, p - q); extra token from p
+    kind = (f < gamma) ? kResidual : kP;
+  } else {
+    // a rejection with delta = 0 only happens for an out-of-range draft; its
+    // residual max(0, q - q) is empty, so p is sampled instead
+    kind = (f < gamma) ? (dstar ? kResidual : kP) : (dstar ? kP : kQ);
+  }
+  if (kind == kResidual || kind == kTokRes) {
+    st_i32(P.seqinfo + (int64_t)b * 2 + 0, f);
+    st_i32(P.seqinfo + (int64_t)b * 2 + 1, kind);
+    publish_row_job(P, phase, kJobRes, (uint32_t)b);
+  } else {
+    publish_single(P, phase, kJobDraw, ((uint32_t)kind << 8) | (uint32_t)f, (uint32_t)b);
+  }
+}
+
+// Wave: decide row r = (b, j) from its statistics rs (delta_j by the rule,
+// a_j by the acceptance test), write its outputs and add it to the
+// sequence's decided-row mask.  Returns j* when this decision completes the
+// prefix of decided rows 0 .. j* (j* the first rejection; row gamma always
+// rejects), else -1; every lane returns the same value.
+template <int DT>
+__device__ __forceinline__ int row_decide_w(const Params& P, int r, int b, int j,
+                                            const SeqParam& sp, const RowStat& rs) {
+  const int gamma = P.gamma, g1 = gamma + 1, V = P.V;
+  const int lane = threadIdx.x & 63;
+  RowDecision d{};
+  int keep = 0;
+  if (sp.valid) {
+    int x = -1;
+    float zqx = 0.0f, zpx = 0.0f, u = 0.0f;
+    if (j < gamma) x = P.draft[(int64_t)b * gamma + j];
+    if (!sp.greedy) {
+      u = P.uniforms[r];
+      if (x >= 0 && x < V) {
+        zqx = load_logit<DT>(P.q, r, V, x);
+        zpx = load_logit<DT>(P.p, r, V, x);
+      }
+    } else if (((is_token(sp.rule) && sp.rule != SPC_RULE_TOKEN_V1) ||
+                sp.rule == SPC_RULE_BILD) &&
+               rs.amax_q >= 0 && rs.amax_q < V) {
+      // greedy TokenV2/V3 and BiLD* read p at the drafter's argmax
+      zpx = load_logit<DT>(P.p, r, V, rs.amax_q);
+    }
+    d = decide_row(sp, rs, j, gamma, V, x, zqx, zpx, u);
+    keep = d.keep;
+  }
+  uint64_t old = 0;
+  if (lane == 0) {
+    P.out_defer[r] = sp.valid ? (uint8_t)d.delta : (uint8_t)0;
+    if (sp.valid && P.out_stats) {
+      const double T = sp.greedy ? 1.0 : kLog2e / sp.c;
+      float* o = P.out_stats + (int64_t)r * 8;
+      o[0] = (float)((double)d.rs.zmax_q / T);
+      o[1] = (float)(d.rs.lz_q * kLn2);
+      o[2] = d.maxq;
+      o[3] = (float)((double)d.rs.zmax_p / T);
+      o[4] = (float)(d.rs.lz_p * kLn2);
+      o[5] = d.maxp;
+      o[6] = d.tv;
+      o[7] = (float)d.rs.slog;
+    }
+    if (sp.valid && P.out_argmax) {
+      P.out_argmax[(int64_t)r * 2 + 0] = d.rs.amax_q;
+      P.out_argmax[(int64_t)r * 2 + 1] = d.rs.amax_p;
+    }
+    if (sp.valid) st_rowstat(P.rowstat + r, d.rs);
+    st_i32(P.rowdec + r, keep | (d.delta << 1));
+    vmem_drain();  // the row's record is stored before its bit is set
+    old = or_u64(seq_mask(P, b), 1ull << j);
+  }
+  old = lane_u64(old, 0);
+  const uint64_t full = (g1 == 64) ? ~0ull : ((1ull << g1) - 1ull);
+  const uint64_t now = old | (1ull << j);
+  if (lane == 0 && now == full) st_u64(seq_mask(P, b), 0ull);  // the last row resets it
+  const int p_old = __builtin_ctzll(~old);
+  const int p_now = (now == ~0ull) ? 64 : __builtin_ctzll(~now);
+  if (p_now <= p_old) return -1;
+  // rows 0 .. p_now - 1 are decided (their records were stored before their
+  // bits were set); the first rejection among them, if it lies in the rows
+  // this decision added to the prefix, is j*
+  const int kp = lane < p_now ? (ld_i32(P.rowdec + (int64_t)b * g1 + lane) & 1) : 1;
+  const unsigned long long rej = __ballot(!kp);
+  if (!rej) return -1;
+  const int f = __ffsll(rej) - 1;
+  return f >= p_old ? f : -1;
+}
+
+// Wave, after the last tile of row r = (b, j) arrived: merge the row, then
+// publish its second pass (TV, or eta for the tiles its statistics leave
+// open) or its argmax to job pass 1, or decide it and, when that settles
+// j*, finish the sequence.
+template <int DT, int MS>
+__device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int j,
+                                             const SeqParam& sp) {
+  const int lane = threadIdx.x & 63;
+  const int nt = P.nt;
+  int kq, kp;
+  RowStat rs = merge_row(P, r, (MS != 0 && needs_mom(sp)) ? sp.rule : 0, &kq, &kp);
+  if (sp.valid && sp.greedy) {
+    // the lowest index of each row maximum, from the first tile holding it
+    if (lane == 0) {
+      st_rowstat(P.rowstat + r, rs);
+      st_i32(P.argres + (int64_t)r * 4 + 0, kq);
+      st_i32(P.argres + (int64_t)r * 4 + 1, kp);
+      publish_single(P, 1, kJobArg, 0u, (uint32_t)r);
+      publish_single(P, 1, kJobArg, 1u, (uint32_t)r);
+    }
+    return;
+  }
+  if (sp.valid && has_tv_parts(sp.rule)) {
+    if (lane == 0) {
+      st_rowstat(P.rowstat + r, rs);
+      publish_row_job(P, 1, kJobTv, (uint32_t)r);
+    }
+    return;
+  }
+  if (sp.valid && is_token(sp.rule)) {
+    // eta's share of every tile wholly below the rule's threshold comes from
+    // its statistics; the other tiles are listed for a second look (the job's
+    // chunks past the list do nothing).  With none listed, eta is summed
+    // here in the order the job's last chunk would sum it.
+    const TokenRule tr = token_rule(sp, rs, exp2_acc((double)rs.zmax_p * sp.c - rs.lz_p));
+    double eta = 0.0;
+    uint32_t count = 0;
+    for (int k0 = 0; k0 < nt; k0 += 64) {
+      const int k = k0 + lane;
+      double e = 0.0;
+      bool need = false;
+      if (k < nt) {
+        need = !eta_from_stats(tr, ld_tile(P.tiles + (int64_t)r * nt + k), rs.lz_q, &e);
+        if (!need) {  // the tile's share, on its first part
+          st_dev_f64(P.tvpart + ((int64_t)r * nt + k) * kParts, e);
+          st_dev_f64(P.tvpart + ((int64_t)r * nt + k) * kParts + 1, 0.0);
+        }
+      }
+      const unsigned long long nm = __ballot(need);
+      if (need)
+        st_i32(P.etalist + (int64_t)r * nt + count + __popcll(nm & ((1ull << lane) - 1ull)), k);
+      count += (uint32_t)__popcll(nm);
+      if (k < nt) eta += e;
+    }
+    if (count != 0) {
+      if (lane == 0) {
+        st_rowstat(P.rowstat + r, rs);
+        st_i32(P.etacnt + r, (int32_t)count);
+        publish_row_job(P, 1, kJobEta, (uint32_t)r);
+      }
+      return;
+    }
+    rs.tv = wave_sum(eta);
+  }
+  const int f = row_decide_w<DT>(P, r, b, j, sp, rs);
+  if (f >= 0) seq_finish_w<DT>(P, b, f, sp, 1);
+}
+
+// The statistics tiles.  grid (nt, R): tile k of row r; NT: read the logits
+// non-temporally (rows that no job reads again), else through the caches (a
+// TV job reads the row again right after).  After the tile partial only wave
+// 0 stays: it arrives on the row's counter, and the last tile of the row
+// merges and decides it.
+template <int DT, bool VEC, int MS, bool NT>
+__global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
   using T = StatTile<DT, VEC>;
   __shared__ Shared sh;
-  __shared__ RowStat srow;
   const int k = blockIdx.x, r = blockIdx.y;
-  const SeqParam sp = seq_param(P, r / (P.gamma + 1));
-  // D_TV rows only: token-rule rows take k_eta
-  if (!needs_pass2(sp) || is_token(sp.rule)) return;  // block-uniform
-  const int V = P.V;
+  const int nt = P.nt, g1 = P.gamma + 1, V = P.V;
+  const int b = r / g1, j = r - b * g1;
+  const SeqParam sp = seq_param(P, b);
   const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
   const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
   const int64_t t0 = (int64_t)k * T::N;
   uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
-  // D_TV visits every tile: its loads overlap the merge
-  load_tile<DT, VEC, T::U, true>(qrow, t0, V, wq, threadIdx.x);
-  load_tile<DT, VEC, T::U, true>(prow, t0, V, wp, threadIdx.x);
-  if (threadIdx.x < 64) {
-    const RowStat rs = merge_row(P, r, false, false);
-    if (threadIdx.x == 0) srow = rs;
-  }
-  __syncthreads();
-  double acc = pass2_sum<DT, VEC>(wq, wp, prob_scale(sp, srow, false), false);
-  double unused = 0.0;
-  block_sum2(acc, unused, sh);
-  if (threadIdx.x == 0) P.tvpart[(int64_t)r * P.nt + k] = acc;
-}
-
-// Eta pass (token-rule rows at temperature > 0).  grid (ceil(nt /
-// kEtaTiles), R): a workgroup merges row r once and takes its tiles
-// x kEtaTiles .. + kEtaTiles - 1 in turn.  A tile wholly below the rule's
-// threshold takes its share from the statistics (eta_from_stats); any other
-// tile is read again and summed exactly as by the TV pass's tile code.
-constexpr int kEtaTiles = 8;
-
-template <int DT, bool VEC>
-__global__ __launch_bounds__(kThreads) void k_eta(Params P) {
-  using T = StatTile<DT, VEC>;
-  __shared__ Shared sh;
-  __shared__ RowStat srow;
-  const int r = blockIdx.y;
-  const SeqParam sp = seq_param(P, r / (P.gamma + 1));
-  if (!needs_pass2(sp) || !is_token(sp.rule)) return;  // block-uniform
-  const int V = P.V, nt = P.nt;
-  const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
-  const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
-  if (threadIdx.x < 64) {
-    const RowStat rs = merge_row(P, r, false, false);
-    if (threadIdx.x == 0) srow = rs;
-  }
-  __syncthreads();
-  const ProbScale ps = prob_scale(sp, srow, true);
-  const int k1 = min(nt, ((int)blockIdx.x + 1) * kEtaTiles);
-  for (int k = (int)blockIdx.x * kEtaTiles; k < k1; ++k) {  // block-uniform
-    double eta;
-    if (eta_from_stats(ps.tok, P.tiles[(int64_t)r * nt + k], srow.lz_q, &eta)) {
-      if (threadIdx.x == 0) P.tvpart[(int64_t)r * nt + k] = eta;
-      continue;
-    }
-    uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
-    load_tile<DT, VEC, T::U, true>(qrow, (int64_t)k * T::N, V, wq, threadIdx.x);
-    load_tile<DT, VEC, T::U, true>(prow, (int64_t)k * T::N, V, wp, threadIdx.x);
-    double acc = pass2_sum<DT, VEC>(wq, wp, ps, true);
-    double unused = 0.0;
-    block_sum2(acc, unused, sh);
-    if (threadIdx.x == 0) P.tvpart[(int64_t)r * nt + k] = acc;
-    __syncthreads();  // the block's shared scratch is reused by the next tile
-  }
-}
-
-// ------------------------------------------- one read for the second pass
-// Statistics and the second pass in one launch, for batches whose rows need
-// no first moments.  A resident grid of G workgroups (G a multiple of nt,
-// all co-resident: a cooperative launch) takes tiles t = g, g + G, ... in
-// row-major order, so the nt tiles of a row always fall in one round of G.
-// A workgroup computes its tile's partial; on a row that needs the second
-// pass it then waits for the row's other nt - 1 partials (a per-row arrival
-// counter), merges them, and sums the TV or eta weight over the entries it
-// still holds in registers, so the row is read from HBM once.  The wait is
-// bounded: a workgroup that gives up writes a NaN partial, which makes its
-// sequence invalid (the sampling pass reports -1), instead of hanging.
-// Measured on MI355X it is slower than the second read it saves (each round
-// of resident tiles waits through publish, arrival and merge with its loads
-// idle, and a cooperative launch costs more to start), so it runs only on
-// request.
-constexpr uint32_t kRowSpinLimit = 1u << 16;  // about 0.1 s
-
-// Thread 0 has written the tile's partial (agent-scope stores).  Arrive on
-// the row's counter and wait until all n tiles have; returns false after the
-// spin limit.
-__device__ __forceinline__ bool row_arrive_wait(uint32_t* cnt, uint32_t n, Shared& sh) {
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    vmem_drain();  // the partial's stores are complete
-    uint32_t seen =
-        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u;
-    uint32_t it = 0;
-    while (seen < n && it < kRowSpinLimit) {
-      __builtin_amdgcn_s_sleep(2);
-      seen = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      ++it;
-    }
-    sh.flag = seen >= n;
-  }
-  __syncthreads();
-  const bool ok = sh.flag;
-  vmem_drain();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-  return ok;
-}
-
-// Leave the row: the last of its n tiles to leave resets both counters
-// (every tile has arrived and stopped waiting by then).
-__device__ __forceinline__ void row_depart(uint32_t* cnt, uint32_t n) {
-  if (threadIdx.x == 0) {
-    const uint32_t prev =
-        __hip_atomic_fetch_add(cnt + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (prev == n - 1) {
-      __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(cnt + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-  }
-}
-
-// Held to SPC_RES_OCCUPANCY resident workgroups per CU (no spill at 5).
-#ifndef SPC_RES_OCCUPANCY
-#define SPC_RES_OCCUPANCY 5
-#endif
-template <int DT, bool VEC, bool ARGMAX>
-__global__ __launch_bounds__(kThreads, SPC_RES_OCCUPANCY) void k_stats_res(Params P) {
-  using T = StatTile<DT, VEC>;
-  __shared__ Shared sh;
-  __shared__ RowStat srow;
-  const int nt = P.nt, V = P.V;
-  const int64_t ntiles = (int64_t)P.B * (P.gamma + 1) * nt;
-  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {  // block-uniform
-    const int r = (int)(t / nt), k = (int)(t - (int64_t)r * nt);
-    const SeqParam sp = seq_param(P, r / (P.gamma + 1));
-    const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
-    const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
-    // the thread's load offsets are recomputed per tile rather than held
-    // across the loop in registers
-    int tid = threadIdx.x;
-    asm volatile("" : "+v"(tid));
-    uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
-    load_tile<DT, VEC, T::U, true>(qrow, (int64_t)k * T::N, V, wq, tid);
-    load_tile<DT, VEC, T::U, true>(prow, (int64_t)k * T::N, V, wp, tid);
-    tile_partial<DT, VEC, ARGMAX, 0, true>(P, r, k, sp, wq, wp, sh);
-    if (needs_pass2(sp)) {  // block-uniform
-      // only the packed words stay live across the wait: left free, the
-      // compiler keeps every unpacked entry of the statistics for reuse
-#pragma unroll
-      for (int i = 0; i < T::U; ++i)
-#pragma unroll
-        for (int j = 0; j < T::NW; ++j) asm volatile("" : "+v"(wq[i][j]), "+v"(wp[i][j]));
-      uint32_t* cnt = P.row_cnt + (int64_t)r * kRowCntStride;
-      const bool ok = row_arrive_wait(cnt, (uint32_t)nt, sh);
-      if (threadIdx.x < 64) {
-        const RowStat rs = merge_row<true>(P, r, false, false, 0, load_head<true>(P, r, false, false));
-        if (threadIdx.x == 0) srow = rs;
-      }
-      __syncthreads();
-      const bool tok = is_token(sp.rule);
-      const ProbScale ps = prob_scale(sp, srow, tok);
-      double eta;
-      if (tok && eta_from_stats(ps.tok, ld_tile(P.tiles + (int64_t)r * nt + k), srow.lz_q,
-                                &eta)) {
-        if (threadIdx.x == 0) P.tvpart[(int64_t)r * nt + k] = ok ? eta : __builtin_nan("");
-      } else {
-        double acc = pass2_sum<DT, VEC>(wq, wp, ps, tok);
-        double unused = 0.0;
-        block_sum2(acc, unused, sh);
-        if (threadIdx.x == 0)
-          P.tvpart[(int64_t)r * nt + k] = ok ? acc : __builtin_nan("");
-      }
-      row_depart(cnt, (uint32_t)nt);
-    }
-    __syncthreads();  // the block's shared scratch is reused by the next tile
-  }
-}
-
-// Sampling pass.  grid (K, B) of 1024-thread workgroups: every workgroup of
-// sequence b merges the sequence's rows and decides it (workgroup 0 writes
-// the outputs).  A replacement drawn from a residual needs that row's
-// residual masses: the K workgroups sum them chunk by chunk, and the last to
-// finish draws.  Every other draw -- the extra token from q, p or a token
-// rule's target, whose per-tile masses the earlier passes left -- is made by
-// workgroup 0 alone.
-template <int DT, bool VEC>
-__global__ __launch_bounds__(kSampThreads) void k_sample(Params P) {
-  __shared__ SampShared sh;
-  __shared__ SeqShared ss;
-  const int k = blockIdx.x, b = blockIdx.y;
-  const SeqParam sp = seq_param(P, b);
-  decide_seq<DT>(P, b, sp, ss, k == 0);
-  const SeqState s = ss.seq;
-  if (s.kind == kNone) return;  // block-uniform
-  const int64_t row = (int64_t)b * (P.gamma + 1) + s.row;
-  const RowStat rs = ss.rows[s.row].rs;
-  const bool pass = s.kind == kTokRes || s.kind == kResidual;
-  if (!pass) {
-    if (k != 0) return;  // block-uniform
-    const int src = s.kind == kQ ? kSrcStatsQ : s.kind == kP ? kSrcStatsP : kSrcTokPi;
-    draw<DT, VEC>(P, b, row, s.kind, src, s.u, sp, rs, ss, sh);
-    return;
-  }
-  constexpr int EB = StatTile<DT, VEC>::EB;
-  const ProbScale ps = prob_scale(sp, rs, s.kind == kTokRes);
-  const char* qrow = (const char*)P.q + row * P.V * EB;
-  const char* prow = (const char*)P.p + row * P.V * EB;
-  double* masses = P.masses + (int64_t)b * P.nc;
-  if (s.kind == kTokRes)
-    residual_masses<DT, VEC, kTokRes>(qrow, prow, P.V, P.nc, P.K, k, ps, masses);
+  load_tile<DT, VEC, T::U, NT>(qrow, t0, V, wq, threadIdx.x);
+  load_tile<DT, VEC, T::U, NT>(prow, t0, V, wp, threadIdx.x);
+  if (MS != 0 && needs_mom(sp))
+    tile_partial<DT, VEC, MS>(P, r, k, sp, wq, wp, sh);
   else
-    residual_masses<DT, VEC, kResidual>(qrow, prow, P.V, P.nc, P.K, k, ps, masses);
-  if (!arrive_last(P.samp_cnt + b, (uint32_t)P.K, sh)) return;
-  draw<DT, VEC>(P, b, row, s.kind, kSrcPass, s.u, sp, rs, ss, sh);
+    tile_partial<DT, VEC, 0>(P, r, k, sp, wq, wp, sh);
+  if (threadIdx.x >= 64) return;
+  // wave 0: thread 0 stored the partial; arrive on the row's counter
+  uint32_t prev = 0;
+  if (threadIdx.x == 0) {
+    vmem_drain();
+    prev = add_u32(row_word(P, r, kRowArrive), 1u);
+    if (prev == (uint32_t)nt - 1u) st_u32(row_word(P, r, kRowArrive), 0u);
+  }
+  if ((uint32_t)lane_i32((int)prev, 0) != (uint32_t)nt - 1u) return;
+  vmem_drain();
+  row_merged_w<DT, MS>(P, r, b, j, sp);
+}
+
+// ---------------------------------------------------------------- job pass
+// The job pass works in wavefronts: every item is one wavefront's, and the
+// wavefronts of a workgroup take items independently (no block barriers
+// after the start).  A row job (a TV or eta pass over a row, a sequence's
+// residual over row j*) has kParts items per statistics tile: a part is half
+// a tile, read by one wavefront, lane load i of lane l covering entries
+// (i * 64 + l) * VW .. + VW - 1; each of its lane-load rows (64 VW entries)
+// is a sub-chunk.
+template <int DT, bool VEC>
+using PartC = Chunk<DT, VEC, 2 * StatTile<DT, VEC>::U>;
+template <int DT, bool VEC>
+using SubC = Chunk<DT, VEC, 1>;
+static_assert(kParts == 2, "a part is half a statistics tile");
+
+// Wave: "am I the last of n arrivals on cnt?" after this wavefront's item
+// (its results stored by its own lanes).  On true the counter is reset and
+// the wavefront reads the other items' results with ld_dev_*.
+__device__ __forceinline__ bool arrive_last_w(uint32_t* cnt, uint32_t n) {
+  uint32_t prev = 0;
+  if ((threadIdx.x & 63) == 0) {
+    vmem_drain();  // every lane's stores of this item are complete
+    prev = add_u32(cnt, 1u);
+    if (prev == n - 1u) st_u32(cnt, 0u);
+  }
+  const bool last = (uint32_t)lane_i32((int)prev, 0) == n - 1u;
+  if (last) vmem_drain();
+  return last;
+}
+
+// Wave: the masses of the NS sub-chunks of the part at entry e0 of a row
+// under the distribution KIND; lane base + i returns sub-chunk i's (float
+// sums per lane load, fp64 across lanes), other lanes 0.
+template <int DT, bool VEC, int KIND>
+__device__ __forceinline__ double part_masses_w(const Params& P, int64_t row, int64_t e0,
+                                                const ProbScale& ps, int base = 0) {
+  using C = PartC<DT, VEC>;
+  constexpr int EB = StatTile<DT, VEC>::EB;
+  const int lane = threadIdx.x & 63, V = P.V;
+  ChunkRegs<C> cq = {}, cp = {};
+  if (KIND != kP) load_chunk<DT, VEC, C>((const char*)P.q + row * V * EB, e0, V, cq);
+  if (KIND != kQ) load_chunk<DT, VEC, C>((const char*)P.p + row * V * EB, e0, V, cp);
+  double mine = 0.0;
+#pragma unroll
+  for (int i = 0; i < C::U; ++i) {
+    float t = 0.0f;
+#pragma unroll
+    for (int e = 0; e < C::VW; ++e) {
+      t += weight_of<KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
+      if (e & 1) __builtin_amdgcn_sched_barrier(0);
+    }
+    const double s = wave_sum((double)t);
+    if (lane == base + i) mine = s;
+  }
+  return mine;
+}
+
+// Wave: the draw inside the NSUB sub-chunks starting at entry e0 whose
+// masses lane i < NSUB holds: the first sub-chunk where the running mass
+// exceeds rem (rounding that leaves rem unreached takes the last sub-chunk
+// with mass), then the entry inside it.
+template <int DT, bool VEC, int KIND>
+__device__ __forceinline__ void draw_in_subs_w(const Params& P, int b, int64_t row, int64_t e0,
+                                               double ml, int nsub, double rem,
+                                               const ProbScale& ps) {
+  const int lane = threadIdx.x & 63;
+  ml = lane < nsub ? ml : 0.0;
+  const double incl = wave_incl_scan(ml);
+  const unsigned long long hit = __ballot(ml > 0.0 && incl > rem);
+  const unsigned long long pos = __ballot(ml > 0.0);
+  int c;
+  double r;
+  if (hit) {
+    c = __ffsll(hit) - 1;
+    r = rem - (lane_f64(incl, c) - lane_f64(ml, c));
+  } else {
+    c = pos ? 63 - __clzll(pos) : 0;
+    r = __builtin_huge_val();
+  }
+  pick_wave<DT, VEC, SubC<DT, VEC>, KIND>(P, b, row, e0 + (int64_t)c * SubC<DT, VEC>::N, r, ps);
+}
+
+// Wave: the inverse-CDF draw of sequence b at row `row` (the row of j*) from
+// the distribution `kind`, its part masses from `src`: the statistics
+// partials per tile, or the residual job's masses per part (whose sub-chunk
+// masses the job stored).  An empty residual (possible only through
+// rounding) is replaced by p.
+template <int DT, bool VEC, int KIND>
+__device__ __forceinline__ void draw_kind_w(const Params& P, int b, int64_t row, int src, int ks,
+                                            double rem, const ProbScale& ps) {
+  const int lane = threadIdx.x & 63;
+  constexpr int NS = PartC<DT, VEC>::U;
+  if (src == kSrcPass) {
+    const int np = P.nt * kParts;
+    const double ml = lane < NS ? ld_dev_f64(P.submass + ((int64_t)b * np + ks) * kMaxSub + lane)
+                                : 0.0;
+    draw_in_subs_w<DT, VEC, KIND>(P, b, row, (int64_t)ks * PartC<DT, VEC>::N, ml, NS, rem, ps);
+  } else {
+    // a statistics tile: the sub-chunk masses of both its parts
+    const int64_t t0 = (int64_t)ks * StatTile<DT, VEC>::N;
+    double m = 0.0;
+#pragma unroll 1
+    for (int part = 0; part < kParts; ++part)
+      m += part_masses_w<DT, VEC, KIND>(P, row, t0 + part * PartC<DT, VEC>::N, ps, part * NS);
+    draw_in_subs_w<DT, VEC, KIND>(P, b, row, t0, m, kParts * NS, rem, ps);
+  }
+}
+
+template <int DT, bool VEC>
+__device__ __forceinline__ void draw_w(const Params& P, int b, int64_t row, int kind, int src,
+                                       const SeqParam& sp, const RowStat& rs) {
+  const int lane = threadIdx.x & 63;
+  const float u = P.uniforms[(int64_t)b * (P.gamma + 1) + P.gamma];
+  const int np = P.nt * kParts;
+  int ks;
+  double rem, W;
+  if (src == kSrcStatsQ) W = find_part<kSrcStatsQ>(P, row, b, P.nt, rs, u, &ks, &rem);
+  else if (src == kSrcStatsP) W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
+  else if (src == kSrcTokPi) W = find_part<kSrcTokPi>(P, row, b, P.nt, rs, u, &ks, &rem);
+  else W = find_part<kSrcPass>(P, row, b, np, rs, u, &ks, &rem);
+  if ((kind == kResidual || kind == kTokRes) && !(W > 0.0)) {
+    kind = kP;
+    src = kSrcStatsP;
+    W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
+  }
+  if (lane == 0) {
+    if (P.out_norm) P.out_norm[b] = (float)W;
+    if (ks < 0) P.out_token[b] = -1;
+  }
+  if (ks < 0) return;  // wave-uniform
+  const ProbScale ps = prob_scale(sp, rs, kind == kTokRes || kind == kTokPi);
+  if (kind == kQ) draw_kind_w<DT, VEC, kQ>(P, b, row, src, ks, rem, ps);
+  else if (kind == kP) draw_kind_w<DT, VEC, kP>(P, b, row, src, ks, rem, ps);
+  else if (kind == kTokPi) draw_kind_w<DT, VEC, kTokPi>(P, b, row, src, ks, rem, ps);
+  else if (kind == kTokRes) draw_kind_w<DT, VEC, kTokRes>(P, b, row, src, ks, rem, ps);
+  else draw_kind_w<DT, VEC, kResidual>(P, b, row, src, ks, rem, ps);
+}
+
+// Wave: part c of a TV or eta row job of row r -- the TV weight
+// max(0, p - q), or eta's share (for eta, the half c % kParts of the
+// (c / kParts)-th listed tile; a part past the list does nothing).
+template <int DT, bool VEC, bool TOK>
+__device__ __forceinline__ void pass2_part_w(const Params& P, int r, int c) {
+  using C = PartC<DT, VEC>;
+  constexpr int EB = StatTile<DT, VEC>::EB;
+  const int nt = P.nt, g1 = P.gamma + 1, V = P.V;
+  int part = c;
+  if (TOK) {
+    if (c >= kParts * ld_i32(P.etacnt + r)) return;  // wave-uniform
+    part = kParts * ld_i32(P.etalist + (int64_t)r * nt + c / kParts) + c % kParts;
+  }
+  const int64_t e0 = (int64_t)part * C::N;
+  ChunkRegs<C> wq, wp;
+  load_chunk<DT, VEC, C>((const char*)P.q + (int64_t)r * V * EB, e0, V, wq);
+  load_chunk<DT, VEC, C>((const char*)P.p + (int64_t)r * V * EB, e0, V, wp);
+  const RowStat rs = ld_rowstat(P.rowstat + r);
+  const SeqParam sp = seq_param(P, r / g1);
+  const ProbScale ps = prob_scale(sp, rs, TOK);
+  double acc = 0.0;
+#pragma unroll
+  for (int i = 0; i < C::U; ++i) {
+    float t = 0.0f;
+#pragma unroll
+    for (int e = 0; e < C::VW; ++e) {
+      const float zq = elem<DT, VEC>(wq[i], e), zp = elem<DT, VEC>(wp[i], e);
+      if constexpr (TOK) {
+        t += token_r(ps.tok, zq, zp) ? prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo) : 0.0f;
+      } else {
+        // D_TV for the deferral decision only, where an absolute error of
+        // about 1e-7 is far inside the decision margin; the replacement draw
+        // of a rejected row sums its own cancellation-free residual
+        const float pq = prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo);
+        const float pp = prob(zp, ps.c_hi, ps.c_lo, ps.p_hi, ps.p_lo);
+        t += fmaxf(pp - pq, 0.0f);
+      }
+      if (e & 1) __builtin_amdgcn_sched_barrier(0);
+    }
+    acc += (double)t;
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  acc = wave_sum(acc);
+  if ((threadIdx.x & 63) == 0) st_dev_f64(P.tvpart + (int64_t)r * nt * kParts + part, acc);
+}
+
+// Wave: half h of the argmax of greedy row r: the lowest index of the row
+// maximum of q (h = 0) or p (h = 1), in the first tile holding it.
+template <int DT, bool VEC>
+__device__ __forceinline__ void arg_half_w(const Params& P, int r, int h) {
+  using C = PartC<DT, VEC>;
+  constexpr int EB = StatTile<DT, VEC>::EB;
+  const int V = P.V;
+  int k = ld_i32(P.argres + (int64_t)r * 4 + h);
+  k = (k >= 0 && k < P.nt) ? k : 0;
+  const RowStat rs = ld_rowstat(P.rowstat + r);
+  const float z = h ? rs.zmax_p : rs.zmax_q;
+  const char* row = (const char*)(h ? P.p : P.q) + (int64_t)r * V * EB;
+  int idx = 0x7fffffff;
+#pragma unroll 1
+  for (int part = 0; part < kParts && idx == 0x7fffffff; ++part) {  // wave-uniform
+    const int64_t e0 = (int64_t)k * StatTile<DT, VEC>::N + (int64_t)part * C::N;
+    ChunkRegs<C> w;
+    load_chunk<DT, VEC, C>(row, e0, V, w);
+    float g[C::U];
+    float m = kNegInf;
+#pragma unroll
+    for (int i = 0; i < C::U; ++i) {
+      float a = kNegInf;
+#pragma unroll
+      for (int e = 0; e < C::VW; ++e) a = fmaxf(a, elem<DT, VEC>(w[i], e));
+      g[i] = a;
+      m = fmaxf(m, a);
+    }
+    const int lane = threadIdx.x & 63;
+    int mine = (m == z) ? first_max_index<DT, VEC, C::U, 64>(w, g, z, (int)e0 + lane * C::VW)
+                        : 0x7fffffff;
+    idx = wave_min(mine);
+  }
+  if ((threadIdx.x & 63) == 0) st_i32(P.argres + (int64_t)r * 4 + 2 + h, idx);
+}
+
+// Wave: part c of sequence b's residual job: the residual masses of the
+// sub-chunks of part c of row j* and, by the scan the draw repeats, the
+// part's mass.
+template <int DT, bool VEC>
+__device__ __forceinline__ void res_part_w(const Params& P, int b, int c) {
+  constexpr int NS = PartC<DT, VEC>::U;
+  const int g1 = P.gamma + 1, np = P.nt * kParts;
+  const int f = ld_i32(P.seqinfo + (int64_t)b * 2 + 0);
+  const int kind = ld_i32(P.seqinfo + (int64_t)b * 2 + 1);
+  const int64_t row = (int64_t)b * g1 + f;
+  const RowStat rs = ld_rowstat(P.rowstat + row);
+  const SeqParam sp = seq_param(P, b);
+  const ProbScale ps = prob_scale(sp, rs, kind == kTokRes);
+  const int64_t e0 = (int64_t)c * PartC<DT, VEC>::N;
+  const double ml = kind == kTokRes ? part_masses_w<DT, VEC, kTokRes>(P, row, e0, ps)
+                                    : part_masses_w<DT, VEC, kResidual>(P, row, e0, ps);
+  const int lane = threadIdx.x & 63;
+  const double tot = lane_f64(wave_incl_scan(lane < NS ? ml : 0.0), NS - 1);
+  if (lane < NS) st_dev_f64(P.submass + ((int64_t)b * np + c) * kMaxSub + lane, ml);
+  if (lane == 0) st_dev_f64(P.masses + (int64_t)b * np + c, tot);
+}
+
+// Wave: the row's decision once its TV, eta or argmax is known; when it
+// settles j*, the sequence's finish publishes to the next job pass.
+template <int DT>
+__device__ __forceinline__ void row_job_decide(const Params& P, int kind, int r, int phase) {
+  const int g1 = P.gamma + 1, np = P.nt * kParts;
+  const int b = r / g1, j = r - b * g1;
+  RowStat rs = ld_rowstat(P.rowstat + r);
+  if (kind == kJobArg) {
+    rs.amax_q = ld_i32(P.argres + (int64_t)r * 4 + 2);
+    rs.amax_p = ld_i32(P.argres + (int64_t)r * 4 + 3);
+  } else {
+    // the TV or eta partials of every part, in part order
+    double s = 0.0;
+    for (int k = threadIdx.x & 63; k < np; k += 64)
+      s += ld_dev_f64(P.tvpart + (int64_t)r * np + k);
+    rs.tv = wave_sum(s);
+  }
+  const SeqParam sp = seq_param(P, b);
+  const int f = row_decide_w<DT>(P, r, b, j, sp, rs);
+  if (f >= 0) seq_finish_w<DT>(P, b, f, sp, phase + 1);
+}
+
+// Thread 0 of each workgroup, after reading the pass's job counts: arrive
+// on one of kExitLeaves leaf counters; the last of a leaf arrives on the
+// top counter, and the last there clears the pass's counts (every workgroup
+// has read them by then).  Two levels keep the arrivals on one line few.
+__device__ __forceinline__ void exit_tree(const Params& P, int phase) {
+  const uint32_t G = gridDim.x, g = blockIdx.x;
+  const uint32_t leaf = g % kExitLeaves;
+  const uint32_t n_leaf = (G - leaf + kExitLeaves - 1) / kExitLeaves;
+  const uint32_t n_top = G < (uint32_t)kExitLeaves ? G : (uint32_t)kExitLeaves;
+  uint32_t* lc = hdr_word(P, kHdrExit + (phase - 1) * (kExitLeaves + 1) + (int)leaf);
+  uint32_t* tc = hdr_word(P, kHdrExit + (phase - 1) * (kExitLeaves + 1) + kExitLeaves);
+  if (add_u32(lc, 1u) != n_leaf - 1u) return;
+  st_u32(lc, 0u);
+  if (add_u32(tc, 1u) != n_top - 1u) return;
+  st_u32(tc, 0u);
+  st_u32(hdr_word(P, hdr_line(phase, false)), 0u);
+  st_u32(hdr_word(P, hdr_line(phase, true)), 0u);
+}
+
+// The job pass `phase` (1 or 2): a static walk over the jobs the earlier
+// launches of this call published for it -- every part of every row job
+// (newest job first: its rows are the likeliest still in the caches), then
+// every single job.  Wavefront w of the grid takes items w, w + W, ...  The
+// item that completes a job continues it: a row decision (jobs of the next
+// pass may follow) or the draw.
+template <int DT, bool VEC>
+__global__ __launch_bounds__(kJobThreads) void k_jobs(Params P) {
+  __shared__ uint32_t counts[2];
+  const int phase = P.phase, nt = P.nt, g1 = P.gamma + 1;
+  if (threadIdx.x == 0) {
+    counts[0] = ld_u32(hdr_word(P, hdr_line(phase, false)));
+    counts[1] = ld_u32(hdr_word(P, hdr_line(phase, true)));
+    vmem_drain();  // both counts have arrived before this workgroup counts itself
+    exit_tree(P, phase);
+  }
+  __syncthreads();
+  const int64_t n_row = min((int64_t)counts[0], P.job_slots);
+  const int64_t n_single = min((int64_t)counts[1], P.single_slots);
+  const int np = nt * kParts;
+  const int64_t n_row_items = n_row * np;
+  const int64_t n_items = n_row_items + n_single;
+  const uint64_t* rows = job_list(P, phase, false);
+  const uint64_t* singles = job_list(P, phase, true);
+  constexpr int kW = kJobThreads / 64;
+  const int64_t W = (int64_t)gridDim.x * kW;
+  for (int64_t g = (int64_t)blockIdx.x * kW + (threadIdx.x >> 6); g < n_items; g += W) {
+    if (g < n_row_items) {  // wave-uniform
+      const int64_t s = n_row - 1 - g / np;
+      const int c = (int)(g - (g / np) * np);
+      const uint64_t e = ld_u64(rows + s);
+      const int kind = job_kind(e);
+      const int id = (int)job_id(e);
+      if (kind == kJobTv) pass2_part_w<DT, VEC, false>(P, id, c);
+      else if (kind == kJobEta) pass2_part_w<DT, VEC, true>(P, id, c);
+      else res_part_w<DT, VEC>(P, id, c);
+      if (arrive_last_w(job_done(P, phase, s), (uint32_t)np)) {
+        if (kind == kJobRes) {
+          const int f = ld_i32(P.seqinfo + (int64_t)id * 2 + 0);
+          const int skind = ld_i32(P.seqinfo + (int64_t)id * 2 + 1);
+          const int64_t row = (int64_t)id * g1 + f;
+          draw_w<DT, VEC>(P, id, row, skind, kSrcPass, seq_param(P, id),
+                          ld_rowstat(P.rowstat + row));
+        } else {
+          row_job_decide<DT>(P, kind, id, phase);
+        }
+      }
+    } else {
+      const uint64_t e = ld_u64(singles + (g - n_row_items));
+      const int kind = job_kind(e);
+      const int id = (int)job_id(e);
+      if (kind == kJobArg) {
+        arg_half_w<DT, VEC>(P, id, (int)job_extra(e));
+        if (arrive_last_w(row_word(P, id, kRowJobDone), 2u)) row_job_decide<DT>(P, kind, id, phase);
+      } else {  // a draw from the statistics partials
+        const int skind = (int)(job_extra(e) >> 8), f = (int)(job_extra(e) & 0xff);
+        const int64_t row = (int64_t)id * g1 + f;
+        const int src = skind == kQ ? kSrcStatsQ : skind == kP ? kSrcStatsP : kSrcTokPi;
+        draw_w<DT, VEC>(P, id, row, skind, src, seq_param(P, id), ld_rowstat(P.rowstat + row));
+      }
+    }
+  }
+}
+
+template <int DT, bool VEC>
+hipError_t launch_step_t(const Params& P, hipStream_t st, bool nt_loads, int job_passes,
+                         int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end) {
+  const dim3 grid((unsigned)P.nt, (unsigned)(P.B * (P.gamma + 1))), block(kThreads);
+  if (ev_begin) {
+    const hipError_t e = hipEventRecord(ev_begin, st);
+    if (e != hipSuccess) return e;
+  }
+  if (nt_loads) {
+    if (P.mom_set == 0)
+      hipLaunchKernelGGL((k_tiles<DT, VEC, 0, true>), grid, block, 0, st, P);
+    else if (P.mom_set == kMomX)
+      hipLaunchKernelGGL((k_tiles<DT, VEC, kMomX, true>), grid, block, 0, st, P);
+    else if (P.mom_set == kMomHQ)
+      hipLaunchKernelGGL((k_tiles<DT, VEC, kMomHQ, true>), grid, block, 0, st, P);
+    else
+      hipLaunchKernelGGL((k_tiles<DT, VEC, kMomX | kMomHQ | kMomHP, true>), grid, block, 0, st, P);
+  } else {
+    if (P.mom_set == 0)
+      hipLaunchKernelGGL((k_tiles<DT, VEC, 0, false>), grid, block, 0, st, P);
+    else
+      hipLaunchKernelGGL((k_tiles<DT, VEC, kMomX | kMomHQ | kMomHP, false>), grid, block, 0, st, P);
+  }
+  hipError_t err = hipGetLastError();
+  if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, st);
+  for (int phase = 1; phase <= job_passes && err == hipSuccess; ++phase) {
+    Params Q = P;
+    Q.phase = phase;
+    hipLaunchKernelGGL((k_jobs<DT, VEC>), dim3((unsigned)job_groups), dim3(kJobThreads), 0, st,
+                       Q);
+    err = hipGetLastError();
+  }
+  return err;
 }
 
 // Drafter sampling step (Alg. 4: x_{t+j} ~ q_{t+j}), one launch.  grid
@@ -1973,71 +2165,6 @@ hipError_t launch_draft_t(const Params& P, bool argmax, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int DT, bool VEC, bool ARGMAX>
-const void* res_kernel() {
-  return reinterpret_cast<const void*>(&k_stats_res<DT, VEC, ARGMAX>);
-}
-
-template <int DT, bool VEC>
-const void* res_kernel(bool argmax) {
-  return argmax ? res_kernel<DT, VEC, true>() : res_kernel<DT, VEC, false>();
-}
-
-template <int DT, bool VEC>
-hipError_t launch_t(const Params& P, int tv_kinds, bool need_sample, bool need_argmax,
-                    bool need_plain, bool need_mom, int res_grid, hipEvent_t e0, hipEvent_t e1,
-                    hipStream_t st) {
-  const unsigned R = (unsigned)(P.B * (P.gamma + 1));
-  const dim3 grid(P.nt, R);
-  hipError_t err;
-  if (e0 && (err = hipEventRecord(e0, st)) != hipSuccess) return err;
-  if (res_grid > 0 && tv_kinds && !need_mom) {
-    // statistics and second pass, one read: every workgroup must be resident
-    void* args[] = {const_cast<Params*>(&P)};
-    err = hipLaunchCooperativeKernel(res_kernel<DT, VEC>(need_argmax), dim3((unsigned)res_grid),
-                                     dim3(kThreads), args, 0, st);
-    if (err == hipSuccess) {
-      if (e1 && (err = hipEventRecord(e1, st)) != hipSuccess) return err;
-      hipLaunchKernelGGL((k_sample<DT, VEC>), dim3(need_sample ? P.K : 1, P.B),
-                         dim3(kSampThreads), 0, st, P);
-      return hipGetLastError();
-    }
-    if (err != hipErrorCooperativeLaunchTooLarge && err != hipErrorNotSupported) return err;
-    (void)hipGetLastError();  // not launchable here: the two-kernel path below
-  }
-  if (need_plain) {
-    if (need_argmax)
-      hipLaunchKernelGGL((k_stats<DT, VEC, true>), grid, dim3(kThreads), 0, st, P);
-    else
-      hipLaunchKernelGGL((k_stats<DT, VEC, false>), grid, dim3(kThreads), 0, st, P);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
-  }
-  if (need_mom) {
-    // the moments the batch's rules read: x alone (BiLD*), H_q alone
-    // (ChowLog), or all three
-    if (P.mom_set == kMomX)
-      launch_mom<DT, VEC, kMomX>(P, need_argmax, grid, st);
-    else if (P.mom_set == kMomHQ)
-      launch_mom<DT, VEC, kMomHQ>(P, need_argmax, grid, st);
-    else
-      launch_mom<DT, VEC, kMomX | kMomHQ | kMomHP>(P, need_argmax, grid, st);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
-  }
-  if (e1 && (err = hipEventRecord(e1, st)) != hipSuccess) return err;
-  if (tv_kinds & kPassTv) {
-    hipLaunchKernelGGL((k_tv<DT, VEC>), dim3(P.nt, R), dim3(kThreads), 0, st, P);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
-  }
-  if (tv_kinds & kPassEta) {
-    hipLaunchKernelGGL((k_eta<DT, VEC>), dim3((P.nt + kEtaTiles - 1) / kEtaTiles, R),
-                       dim3(kThreads), 0, st, P);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
-  }
-  // a batch with no sequence at temperature > 0 only needs the decisions
-  hipLaunchKernelGGL((k_sample<DT, VEC>), dim3(need_sample ? P.K : 1, P.B), dim3(kSampThreads), 0,
-                     st, P);
-  return hipGetLastError();
-}
 
 }  // namespace
 
@@ -2055,21 +2182,6 @@ int draft_tile_elems(int dtype, bool vec, bool long_tiles) {
   return vec ? DraftTile<0, true, 1>::N : DraftTile<0, false, 1>::N;
 }
 
-int samp_chunk_elems(int dtype, bool vec) {
-  if (dtype == 1) return vec ? SampChunk<1, true>::N : SampChunk<1, false>::N;
-  return vec ? SampChunk<0, true>::N : SampChunk<0, false>::N;
-}
-
-// Enough workgroups to give every compute unit one (a sampling workgroup
-// fills a CU), but no more than one chunk per wavefront: small batches spread
-// a row over several workgroups, large ones take one per sequence and loop.
-int samp_groups(int64_t nc, int B, int cus) {
-  const int64_t by_chunks = (nc + kSampWaves - 1) / kSampWaves;
-  const int64_t by_cus = (cus + B - 1) / B;
-  const int64_t k = by_chunks < by_cus ? by_chunks : by_cus;
-  return (int)(k < 1 ? 1 : k);
-}
-
 hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, bool long_tiles,
                         hipStream_t st) {
   if (long_tiles) {
@@ -2085,36 +2197,15 @@ hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, bool 
   return vec ? launch_draft_t<0, true, 1>(P, argmax, st) : launch_draft_t<0, false, 1>(P, argmax, st);
 }
 
-hipError_t launch_verify(const Params& P, int dtype, bool vec, int tv_kinds, bool need_sample,
-                         bool need_argmax, bool need_plain, bool need_mom, int res_grid,
-                         hipEvent_t e0, hipEvent_t e1, hipStream_t st) {
-  if (dtype == 1) {
-    return vec ? launch_t<1, true>(P, tv_kinds, need_sample, need_argmax, need_plain, need_mom,
-                                   res_grid, e0, e1, st)
-               : launch_t<1, false>(P, tv_kinds, need_sample, need_argmax, need_plain, need_mom,
-                                    res_grid, e0, e1, st);
-  }
-  return vec ? launch_t<0, true>(P, tv_kinds, need_sample, need_argmax, need_plain, need_mom,
-                                 res_grid, e0, e1, st)
-             : launch_t<0, false>(P, tv_kinds, need_sample, need_argmax, need_plain, need_mom,
-                                  res_grid, e0, e1, st);
-}
-
-int res_blocks_per_cu(int dtype, bool vec, bool argmax) {
-  // per variant; queried once per process (every device here is the same part)
-  static int cache[2][2][2] = {{{-1, -1}, {-1, -1}}, {{-1, -1}, {-1, -1}}};
-  int& c = cache[dtype == 1][vec][argmax];
-  if (c < 0) {
-    const void* f = dtype == 1 ? (vec ? res_kernel<1, true>(argmax) : res_kernel<1, false>(argmax))
-                               : (vec ? res_kernel<0, true>(argmax) : res_kernel<0, false>(argmax));
-    int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, f, kThreads, 0) != hipSuccess) {
-      (void)hipGetLastError();
-      nb = 0;
-    }
-    c = nb;
-  }
-  return c;
+hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, int job_passes,
+                       int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end,
+                       hipStream_t st) {
+  if (dtype == 1)
+    return vec ? launch_step_t<1, true>(P, st, nt_loads, job_passes, job_groups, ev_begin, ev_end)
+               : launch_step_t<1, false>(P, st, nt_loads, job_passes, job_groups, ev_begin,
+                                         ev_end);
+  return vec ? launch_step_t<0, true>(P, st, nt_loads, job_passes, job_groups, ev_begin, ev_end)
+             : launch_step_t<0, false>(P, st, nt_loads, job_passes, job_groups, ev_begin, ev_end);
 }
 
 }  // namespace spc

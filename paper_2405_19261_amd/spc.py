@@ -32,7 +32,8 @@ class ExArgs(ctypes.Structure):
     _fields_ = [("rule_per_seq", _P), ("alpha_per_seq", _P), ("temp_per_seq", _P),
                 ("out_row_stats", _P), ("out_argmax", _P), ("out_sample_norm", _P),
                 ("workspace", _P), ("workspace_bytes", ctypes.c_size_t),
-                ("ev_hot_begin", _P), ("ev_hot_end", _P), ("rules_present", ctypes.c_uint32)]
+                ("rules_present", ctypes.c_uint32), ("ev_tiles_begin", _P),
+                ("ev_tiles_end", _P)]
 
 
 class SpcError(RuntimeError):
@@ -66,6 +67,11 @@ def lib():
         L.spc_draft_sample.argtypes = [_P, ctypes.c_int, _I32, _I32, ctypes.c_float, _P, _P, _P,
                                        _P]
         L.spc_draft_sample.restype = ctypes.c_int
+        L.spc_draft_sample_ws.argtypes = [_P, ctypes.c_int, _I32, _I32, ctypes.c_float, _P, _P,
+                                          _P, _P, ctypes.c_size_t, _P]
+        L.spc_draft_sample_ws.restype = ctypes.c_int
+        L.spc_draft_workspace_bytes.argtypes = [_I32, _I32, ctypes.c_int]
+        L.spc_draft_workspace_bytes.restype = ctypes.c_size_t
         L.spc_workspace_bytes.argtypes = [_I32, _I32, _I32, ctypes.c_int]
         L.spc_workspace_bytes.restype = ctypes.c_size_t
         L.spc_workspace_zero_bytes.argtypes = [_I32, _I32, _I32, ctypes.c_int]
@@ -98,20 +104,6 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
-def _event(ev):
-    """A raw hipEvent_t: an int handle, or an object with a ``handle`` or
-    ``cuda_event`` attribute."""
-    if ev is None:
-        return None
-    for attr in ("handle", "cuda_event"):
-        if hasattr(ev, attr):
-            ev = getattr(ev, attr)
-            break
-    if not ev:
-        raise ValueError("event is not created")
-    return ctypes.c_void_p(int(ev))
-
-
 def _check(status):
     if status != 0:
         raise SpcError(status, lib().spc_last_error().decode())
@@ -129,15 +121,33 @@ def _outputs(q, B, gamma, out):
 def _shape(q, p, draft):
     if q.dim() != 3 or q.shape != p.shape or q.dtype != p.dtype:
         raise ValueError("q and p must both be [B, gamma+1, V] of one dtype")
-    if not (q.is_contiguous() and p.is_contiguous() and draft.is_contiguous()):
+    if not (q.is_contiguous() and p.is_contiguous()):
         raise ValueError("inputs must be contiguous")
+    if p.device != q.device:
+        raise ValueError("q and p must be on one device")
     B, g1, V = q.shape
+    _check_arg("draft", draft, torch.int32, q.device, (B, g1 - 1))
     return B, g1 - 1, V
+
+
+def _check_arg(name, t, dtype, device, shape=None):
+    """Raise unless t is a contiguous tensor of dtype on device (of shape)."""
+    if t is None:
+        return
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, not {t.dtype}")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, not {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, not {tuple(t.shape)}")
 
 
 def spc_verify(q, p, draft, uniforms, rule, alpha, temperature, out=None, stream=None):
     """One verify step; returns (accept_len [B], next_token [B], defer_mask [B, gamma+1])."""
     B, gamma, V = _shape(q, p, draft)
+    _check_arg("uniforms", uniforms, torch.float32, q.device, (B, gamma + 1))
     acc, tok, dm = _outputs(q, B, gamma, out)
     _check(lib().spc_verify(_ptr(q), _ptr(p), _dtype_code(q), _ptr(draft), _ptr(uniforms), B,
                             gamma, V, int(rule), float(alpha), float(temperature), _ptr(acc),
@@ -157,14 +167,21 @@ def spc_greedy_verify(q, p, draft, rule, alpha, out=None, stream=None):
 
 def spc_verify_ex(q, p, draft, uniforms, rule, alpha, temperature, rule_per_seq=None,
                   alpha_per_seq=None, temp_per_seq=None, out_row_stats=None, out_argmax=None,
-                  out_sample_norm=None, workspace=None, ev_hot_begin=None, ev_hot_end=None,
-                  rules_present=0, out=None, stream=None):
+                  out_sample_norm=None, workspace=None, rules_present=0, ev_tiles=None, out=None,
+                  stream=None):
     """spc_verify with per-sequence parameters and optional outputs.
-    ev_hot_begin / ev_hot_end: hipEvent_t handles (ints or objects with a
-    ``handle`` / ``cuda_event`` attribute) recorded around the statistics
-    kernel.  rules_present: bitmask of the rule ids rule_per_seq may hold
-    (0 = any)."""
+    rules_present: bitmask of the rule ids rule_per_seq may hold (0 = any).
+    ev_tiles: for profiling, a pair of raw hipEvent_t handles (integers)
+    recorded around the statistics kernel of the call's first launch."""
     B, gamma, V = _shape(q, p, draft)
+    dev = q.device
+    _check_arg("uniforms", uniforms, torch.float32, dev, (B, gamma + 1))
+    _check_arg("rule_per_seq", rule_per_seq, torch.int32, dev, (B,))
+    _check_arg("alpha_per_seq", alpha_per_seq, torch.float32, dev, (B,))
+    _check_arg("temp_per_seq", temp_per_seq, torch.float32, dev, (B,))
+    _check_arg("out_row_stats", out_row_stats, torch.float32, dev, (B, gamma + 1, 8))
+    _check_arg("out_argmax", out_argmax, torch.int32, dev, (B, gamma + 1, 2))
+    _check_arg("out_sample_norm", out_sample_norm, torch.float32, dev, (B,))
     acc, tok, dm = _outputs(q, B, gamma, out)
     ex = ExArgs()
     ex.rule_per_seq = _ptr(rule_per_seq)
@@ -174,11 +191,13 @@ def spc_verify_ex(q, p, draft, uniforms, rule, alpha, temperature, rule_per_seq=
     ex.out_argmax = _ptr(out_argmax)
     ex.out_sample_norm = _ptr(out_sample_norm)
     if workspace is not None:
+        if workspace.device != dev or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous tensor on the logits' device")
         ex.workspace = _ptr(workspace)
         ex.workspace_bytes = workspace.numel() * workspace.element_size()
-    ex.ev_hot_begin = _event(ev_hot_begin)
-    ex.ev_hot_end = _event(ev_hot_end)
     ex.rules_present = int(rules_present)
+    if ev_tiles is not None:
+        ex.ev_tiles_begin, ex.ev_tiles_end = int(ev_tiles[0]), int(ev_tiles[1])
     _check(lib().spc_verify_ex(_ptr(q), _ptr(p), _dtype_code(q), _ptr(draft), _ptr(uniforms), B,
                                gamma, V, int(rule), float(alpha), float(temperature), _ptr(acc),
                                _ptr(tok), _ptr(dm), ctypes.byref(ex), _stream(stream)))
@@ -186,17 +205,32 @@ def spc_verify_ex(q, p, draft, uniforms, rule, alpha, temperature, rule_per_seq=
 
 
 def spc_draft_sample(logits, temperature, uniforms=None, temp_per_seq=None, out=None,
-                     stream=None):
+                     workspace=None, stream=None):
     """The drafter's sampling step: one token per row of ``logits`` [B, V]
     (float32 or bfloat16, contiguous) from softmax(z / T), T = 0 giving the
-    argmax.  Returns the tokens [B] int32 (``out`` if given)."""
+    argmax.  Returns the tokens [B] int32 (``out`` if given).  ``workspace``:
+    an optional caller workspace (a uint8 tensor of at least
+    spc_draft_workspace_bytes bytes, zeroed before its first use)."""
     if logits.dim() != 2 or not logits.is_contiguous():
         raise ValueError("logits must be a contiguous [B, V] tensor")
     B, V = logits.shape
-    tok = out if out is not None else torch.empty(B, dtype=torch.int32, device=logits.device)
-    _check(lib().spc_draft_sample(_ptr(logits), _dtype_code(logits), B, V, float(temperature),
-                                  _ptr(temp_per_seq), _ptr(uniforms), _ptr(tok),
-                                  _stream(stream)))
+    dev = logits.device
+    _check_arg("uniforms", uniforms, torch.float32, dev, (B,))
+    _check_arg("temp_per_seq", temp_per_seq, torch.float32, dev, (B,))
+    tok = out if out is not None else torch.empty(B, dtype=torch.int32, device=dev)
+    _check_arg("out", tok, torch.int32, dev, (B,))
+    if workspace is None:
+        _check(lib().spc_draft_sample(_ptr(logits), _dtype_code(logits), B, V, float(temperature),
+                                      _ptr(temp_per_seq), _ptr(uniforms), _ptr(tok),
+                                      _stream(stream)))
+    else:
+        if workspace.device != dev or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous tensor on the logits' device")
+        _check(lib().spc_draft_sample_ws(_ptr(logits), _dtype_code(logits), B, V,
+                                         float(temperature), _ptr(temp_per_seq), _ptr(uniforms),
+                                         _ptr(tok), _ptr(workspace),
+                                         workspace.numel() * workspace.element_size(),
+                                         _stream(stream)))
     return tok
 
 
@@ -206,6 +240,10 @@ def spc_workspace_bytes(B, gamma, V, dtype_code):
 
 def spc_workspace_zero_bytes(B, gamma, V, dtype_code):
     return lib().spc_workspace_zero_bytes(B, gamma, V, dtype_code)
+
+
+def spc_draft_workspace_bytes(B, V, dtype_code):
+    return lib().spc_draft_workspace_bytes(B, V, dtype_code)
 
 
 def spc_last_error():

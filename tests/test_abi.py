@@ -45,7 +45,6 @@ def _verify(**kw):
     (dict(q=None), -1), (dict(p=None), -1), (dict(draft=None), -1), (dict(u=None), -1),
     (dict(acc=None), -1), (dict(tok=None), -1), (dict(dm=None), -1),
     (dict(B=0), -2), (dict(gamma=0), -2), (dict(gamma=64), -2), (dict(V=1), -2),
-    (dict(B=10000, gamma=7), -2),
     (dict(rule=13), -3), (dict(rule=-1), -3), (dict(rule=8, alpha=1.0), -4),
     (dict(alpha=float("nan")), -4), (dict(alpha=float("inf")), -4),
     (dict(T=0.0), -4), (dict(T=-1.0), -4), (dict(T=float("nan")), -4),
@@ -55,6 +54,17 @@ def _verify(**kw):
 def test_argument_errors(kw, status):
     assert _verify(**kw) == status
     assert spc.spc_last_error() != ""
+
+
+@pytest.mark.parametrize("kw", [
+    dict(B=10000, gamma=7),      # 80000 rows: consecutive launches of whole sequences
+    dict(B=2_000_000, gamma=63),
+    dict(T=1e-30), dict(T=1.17549435e-38), dict(T=1e-45),  # tiny positive temperatures
+])
+def test_accepted_shapes_and_temperatures(kw):
+    """Large batches and tiny positive temperatures pass every shape and
+    parameter check: the call stops at the misaligned logits instead."""
+    assert _verify(q=FAKE_ODD, **kw) == -5
 
 
 def test_greedy_argument_errors():
@@ -102,7 +112,7 @@ def test_ex_per_sequence_arrays_skip_scalar_checks():
 
 @pytest.mark.parametrize("kw,status", [
     (dict(z=None), -1), (dict(tok=None), -1), (dict(u=None), -1),
-    (dict(B=0), -2), (dict(V=1), -2), (dict(B=40000), -2),
+    (dict(B=0), -2), (dict(V=1), -2),
     (dict(T=-0.5), -4), (dict(T=float("nan")), -4), (dict(T=float("inf")), -4),
     (dict(dtype=3), -4), (dict(z=FAKE_ODD), -5),
 ])
@@ -119,4 +129,21 @@ def test_draft_sample_greedy_needs_no_uniforms():
     """T = 0 takes no uniforms: the call gets past every argument check (here
     it stops at the misaligned logits, before any HIP call)."""
     st = spc.lib().spc_draft_sample(FAKE_ODD, spc.SPC_BF16, 4, 1000, 0.0, None, None, FAKE, None)
+    assert st == -5
+
+
+def test_draft_workspace_errors_and_sizes():
+    L = spc.lib()
+    n = spc.spc_draft_workspace_bytes(32, 256000, spc.SPC_BF16)
+    z = spc.spc_workspace_zero_bytes(1, 1, 2, spc.SPC_BF16)
+    assert 0 < z < n and n % 256 == 0
+    assert spc.spc_draft_workspace_bytes(0, 256000, spc.SPC_BF16) == 0
+    for ws, nb in ((0x100000, n - 1), (0x100010, n)):  # too small; misaligned
+        st = L.spc_draft_sample_ws(FAKE, spc.SPC_BF16, 32, 256000, 1.0, None, FAKE, FAKE,
+                                   ctypes.c_void_p(ws), nb, None)
+        assert st == -6
+        assert spc.spc_last_error() != ""
+    # a large batch passes the shape check (consecutive launches)
+    st = L.spc_draft_sample_ws(FAKE_ODD, spc.SPC_BF16, 100000, 1000, 1.0, None, FAKE, FAKE,
+                               None, 0, None)
     assert st == -5

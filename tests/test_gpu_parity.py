@@ -111,8 +111,9 @@ def test_block_size_extremes(gamma, B):
 
 @pytest.mark.parametrize("dtype,rule,alpha", [("bf16", W.DIFF, 0.05), ("f32", W.OPT, 0.1)])
 def test_maximum_rows(dtype, rule, alpha):
-    """B*(gamma+1) at the library's row limit (65535 = the grid's y extent)."""
-    wl = W.WORKLOADS[3].with_(B=13107, gamma=4, V=37, dtype=dtype, rule=rule, alpha=alpha)
+    """B*(gamma+1) = 100000 rows: more than one launch holds (16384 rows), so
+    the call runs consecutive launches of whole sequences."""
+    wl = W.WORKLOADS[3].with_(B=20000, gamma=4, V=37, dtype=dtype, rule=rule, alpha=alpha)
     _flush(f"[edge] maximum rows {dtype} rule={rule}")
     parity.parity_workload(wl, 1, report_name=f"maxrows.{dtype}")
     parity.parity_workload(wl.with_(temperature=0.0, cfg=4), 1, report_name=f"maxrows.{dtype}.g")
@@ -550,39 +551,6 @@ def _ex_outputs(inp, mask):
                                      out_argmax=am, out_sample_norm=norm, rules_present=mask)
     torch.cuda.synchronize()
     return [x.cpu().numpy() for x in (acc, tok, dm, stats, am, norm)]
-
-
-@pytest.mark.parametrize("case", ["opt", "token-v1", "token-v2", "token-v3", "mixed",
-                                  "opt-f32", "opt-full"])
-def test_one_read_second_pass_equals_two_reads(case, monkeypatch):
-    """The one-read statistics kernel (second pass over register-resident
-    tiles, selected with SPC_ONE_READ=1) and the default two-kernel path
-    compute the same partials in the same order: every output agrees
-    bitwise."""
-    rules = {"opt": (W.OPT, 0.1), "token-v1": (W.TOKEN_V1, 0.05),
-             "token-v2": (W.TOKEN_V2, 0.05), "token-v3": (W.TOKEN_V3, 0.3)}
-    if case == "mixed":
-        wl = W.WORKLOADS[5].with_(B=24, V=30000)
-    elif case == "opt-f32":
-        wl = W.WORKLOADS[2]
-    elif case == "opt-full":
-        wl = W.WORKLOADS[3].with_(rule=W.OPT, alpha=0.1, temperature=0.7)
-    else:
-        rule, alpha = rules[case]
-        wl = W.WORKLOADS[3].with_(B=16, V=70001 if case == "token-v2" else 70000, rule=rule,
-                                  alpha=alpha, temperature=0.7)
-    inp = W.generate(wl, 7, DEV)
-    if case == "mixed":
-        inp["temperature"][::7] = 0.0
-    mask = parity.rules_mask(inp["rule"])
-    _flush(f"[one-read] {case} B={wl.B} gamma={wl.gamma} V={wl.V} {wl.dtype} mask={mask:#x}")
-    monkeypatch.setenv("SPC_ONE_READ", "1")
-    one = _ex_outputs(inp, mask)
-    monkeypatch.delenv("SPC_ONE_READ")
-    two = _ex_outputs(inp, mask)
-    for a, b in zip(one, two):
-        np.testing.assert_array_equal(a, b)
-    assert (one[0] >= 0).all()
 
 
 # ------------------------------------------------------------- argmax ties
