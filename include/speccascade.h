@@ -210,6 +210,35 @@ spc_status spc_verify_ex(const void* q_logits, const void* p_logits, int32_t dty
                          hipStream_t stream);
 
 /*
+ * spc_verify_noalloc -- spc_verify_ex for callers that cannot allocate
+ * device memory: code being recorded into a HIP graph, serving loops that
+ * must not call hipMalloc, harnesses that forbid allocation.  It computes
+ * exactly what spc_verify_ex computes (same kernels), but its workspace is a
+ * static device array of spc_noalloc_scratch_bytes() bytes (32 MiB) that
+ * every device running it holds until the process ends; it calls no
+ * hipMalloc, hipFree or allocating library routine.
+ *   ex            as for spc_verify_ex, except that ex->workspace must be
+ *                 NULL (SPC_E_WORKSPACE otherwise)
+ * A batch whose layout exceeds the scratch is run in launches of as many
+ * whole sequences as fit; a shape of which not even one sequence fits
+ * (gamma and V large: the layout grows with (gamma + 1) * V) returns
+ * SPC_E_WORKSPACE.  The first call on a device clears the array's counter
+ * region with a fill kernel on `stream`; every call leaves it cleared.
+ * All calls on one device share the array: calls that overlap on one device
+ * (other streams, other host threads) race and must be serialised by the
+ * caller.  Other errors as spc_verify_ex.
+ */
+spc_status spc_verify_noalloc(const void* q_logits, const void* p_logits, int32_t dtype,
+                              const int32_t* draft_tokens, const float* uniforms, int32_t B,
+                              int32_t gamma, int32_t V, int32_t rule, float alpha,
+                              float temperature, int32_t* out_accept_len,
+                              int32_t* out_next_token, uint8_t* out_defer_mask,
+                              const spc_verify_ex_args* ex, hipStream_t stream);
+
+/* Size in bytes of spc_verify_noalloc's static scratch. */
+size_t spc_noalloc_scratch_bytes(void);
+
+/*
  * spc_draft_sample -- the drafter's sampling step of GenSpecSample (Alg. 4):
  * x_{t+j} ~ q_{t+j} = softmax(z / T) for one position of each of B sequences.
  *

@@ -166,6 +166,56 @@ spc_status internal_workspace(size_t bytes, size_t zero_bytes, hipStream_t strea
   return SPC_OK;
 }
 
+// Static scratch of spc_verify_noalloc: each device that runs it holds its
+// own copy until the process ends.  Host code never uses the array's name as
+// an address: noalloc_scratch looks up the device address once per device.
+constexpr size_t kNoAllocBytes = size_t(32) << 20;
+__device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+struct NoAllocDev {
+  void* ptr = nullptr;  // the device address of `scratch` on this device
+  bool cleared = false; // its counter region zeroed by a fill kernel
+};
+std::mutex g_na_mu;
+std::map<int, NoAllocDev> g_na;
+
+// Sequences per launch that the static scratch holds for this row shape
+// (0: not even one).
+int64_t noalloc_seqs(int64_t gamma, int64_t V, int dtype, bool vec) {
+  const size_t one = spc::ws_layout(1, gamma, V, dtype, vec).total;
+  if (one > kNoAllocBytes) return 0;
+  int64_t lo = 1, hi = spc::kMaxRows;  // largest b with layout(b) <= the scratch
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) / 2;
+    if (spc::ws_layout(mid, gamma, V, dtype, vec).total <= kNoAllocBytes) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+// The static scratch of device `dev` (the current device).  The first call
+// on a device looks up its address and clears its counter region with a
+// fill kernel on `stream`; the kernels leave that region zero after every
+// call, so later calls find it cleared.  Nothing here allocates.
+spc_status noalloc_scratch(int dev, size_t zero_bytes, hipStream_t stream, char** out) {
+  std::lock_guard<std::mutex> lk(g_na_mu);
+  NoAllocDev& d = g_na[dev];
+  if (!d.ptr) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(SPC_E_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    d.ptr = ptr;
+  }
+  if (!d.cleared) {
+    const hipError_t e = spc::launch_fill_zero(d.ptr, zero_bytes, stream);
+    if (e != hipSuccess) return fail(SPC_E_HIP, "clearing the scratch: %s", hipGetErrorString(e));
+    d.cleared = true;
+  }
+  *out = static_cast<char*>(d.ptr);
+  return SPC_OK;
+}
+
 template <class T>
 T* offset(T* p, int64_t n) {
   return p ? p + n : p;
@@ -175,7 +225,7 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
                        const float* uniforms, int32_t B, int32_t gamma, int32_t V, int32_t rule,
                        float alpha, float temperature, bool force_greedy, int32_t* out_accept,
                        int32_t* out_token, uint8_t* out_defer, const spc_verify_ex_args* ex,
-                       hipStream_t stream) {
+                       hipStream_t stream, bool no_alloc = false) {
   g_err.clear();
   if (!q || !p || !draft || !out_accept || !out_token || !out_defer)
     return fail(SPC_E_NULL, "a required pointer is NULL");
@@ -198,7 +248,19 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
 
   const bool vec = vec_path(dtype, V);
   const int64_t g1 = (int64_t)gamma + 1;
-  const int64_t b_launch = seqs_per_launch(B, gamma);
+  int64_t b_launch = seqs_per_launch(B, gamma);
+  if (no_alloc) {
+    if (ex && ex->workspace)
+      return fail(SPC_E_WORKSPACE, "spc_verify_noalloc takes no caller workspace");
+    // as many sequences per launch as the static scratch holds (the layout
+    // grows with the sequences of a launch)
+    b_launch = std::min<int64_t>(b_launch, noalloc_seqs(gamma, V, dtype, vec));
+    if (b_launch < 1)
+      return fail(SPC_E_WORKSPACE,
+                  "one sequence of gamma=%d V=%d needs %zu bytes of workspace, more than the "
+                  "%zu-byte static scratch of spc_verify_noalloc",
+                  gamma, V, spc::ws_layout(1, gamma, V, dtype, vec).total, kNoAllocBytes);
+  }
   const spc::WsLayout L = spc::ws_layout(b_launch, gamma, V, dtype, vec);
   // argument checks end here: no HIP call precedes them
   if (ex && ex->workspace &&
@@ -211,7 +273,10 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
   const int cus = cu_count(dev);
   if (cus <= 0) return fail(SPC_E_HIP, "cannot read the compute-unit count of device %d", dev);
   char* ws = nullptr;
-  if (ex && ex->workspace) {
+  if (no_alloc) {
+    const spc_status wst = noalloc_scratch(dev, L.zero_end, stream, &ws);
+    if (wst != SPC_OK) return wst;
+  } else if (ex && ex->workspace) {
     ws = static_cast<char*>(ex->workspace);
   } else {
     const spc_status wst = internal_workspace(L.total, L.zero_end, stream, &ws);
@@ -406,6 +471,20 @@ spc_status spc_verify_ex(const void* q_logits, const void* p_logits, int32_t dty
                      temperature, greedy, out_accept_len, out_next_token, out_defer_mask, ex,
                      stream);
 }
+
+spc_status spc_verify_noalloc(const void* q_logits, const void* p_logits, int32_t dtype,
+                              const int32_t* draft_tokens, const float* uniforms, int32_t B,
+                              int32_t gamma, int32_t V, int32_t rule, float alpha,
+                              float temperature, int32_t* out_accept_len,
+                              int32_t* out_next_token, uint8_t* out_defer_mask,
+                              const spc_verify_ex_args* ex, hipStream_t stream) {
+  const bool greedy = !(ex && ex->temp_per_seq) && temperature == 0.0f;
+  return verify_impl(q_logits, p_logits, dtype, draft_tokens, uniforms, B, gamma, V, rule, alpha,
+                     temperature, greedy, out_accept_len, out_next_token, out_defer_mask, ex,
+                     stream, true);
+}
+
+size_t spc_noalloc_scratch_bytes(void) { return kNoAllocBytes; }
 
 spc_status spc_draft_sample(const void* logits, int32_t dtype, int32_t B, int32_t V,
                             float temperature, const float* temp_per_seq,

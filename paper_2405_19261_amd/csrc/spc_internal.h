@@ -147,4 +147,8 @@ hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, int 
                        int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end,
                        hipStream_t stream);
 
+// Enqueue a kernel writing `bytes` zero bytes at `ptr` (a multiple of 4, ptr
+// 4-byte aligned): a fill a graph capture may record.
+hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t stream);
+
 }  // namespace spc

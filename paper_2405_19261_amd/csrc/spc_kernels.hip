@@ -43,6 +43,8 @@
 // counters as the captured call did.
 #include <math.h>
 
+#include <algorithm>
+
 #include "spc_internal.h"
 
 namespace spc {
@@ -2195,6 +2197,22 @@ hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, bool 
     return vec ? launch_draft_t<1, true, 1>(P, argmax, st)
                : launch_draft_t<1, false, 1>(P, argmax, st);
   return vec ? launch_draft_t<0, true, 1>(P, argmax, st) : launch_draft_t<0, false, 1>(P, argmax, st);
+}
+
+namespace {
+// Zero fill with vector stores: a grid-stride loop over 32-bit words.
+__global__ __launch_bounds__(256) void k_fill_zero(uint32_t* p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256)
+    p[i] = 0u;
+}
+}  // namespace
+
+hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t st) {
+  const size_t n = bytes / 4;
+  if (n == 0) return hipSuccess;
+  const unsigned groups = (unsigned)std::min<size_t>((n + 255) / 256, 1024);
+  hipLaunchKernelGGL(k_fill_zero, dim3(groups), dim3(256), 0, st, static_cast<uint32_t*>(ptr), n);
+  return hipGetLastError();
 }
 
 hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, int job_passes,

@@ -64,6 +64,10 @@ def lib():
                                              ctypes.c_float, _P, _P, _P,
                                              ctypes.POINTER(ExArgs), _P]
         L.spc_verify_ex.restype = ctypes.c_int
+        L.spc_verify_noalloc.argtypes = L.spc_verify_ex.argtypes
+        L.spc_verify_noalloc.restype = ctypes.c_int
+        L.spc_noalloc_scratch_bytes.argtypes = []
+        L.spc_noalloc_scratch_bytes.restype = ctypes.c_size_t
         L.spc_draft_sample.argtypes = [_P, ctypes.c_int, _I32, _I32, ctypes.c_float, _P, _P, _P,
                                        _P]
         L.spc_draft_sample.restype = ctypes.c_int
@@ -165,10 +169,10 @@ def spc_greedy_verify(q, p, draft, rule, alpha, out=None, stream=None):
     return acc, tok, dm
 
 
-def spc_verify_ex(q, p, draft, uniforms, rule, alpha, temperature, rule_per_seq=None,
-                  alpha_per_seq=None, temp_per_seq=None, out_row_stats=None, out_argmax=None,
-                  out_sample_norm=None, workspace=None, rules_present=0, ev_tiles=None, out=None,
-                  stream=None):
+def _verify_ex(entry, q, p, draft, uniforms, rule, alpha, temperature, rule_per_seq=None,
+               alpha_per_seq=None, temp_per_seq=None, out_row_stats=None, out_argmax=None,
+               out_sample_norm=None, workspace=None, rules_present=0, ev_tiles=None, out=None,
+               stream=None):
     """spc_verify with per-sequence parameters and optional outputs.
     rules_present: bitmask of the rule ids rule_per_seq may hold (0 = any).
     ev_tiles: for profiling, a pair of raw hipEvent_t handles (integers)
@@ -198,10 +202,30 @@ def spc_verify_ex(q, p, draft, uniforms, rule, alpha, temperature, rule_per_seq=
     ex.rules_present = int(rules_present)
     if ev_tiles is not None:
         ex.ev_tiles_begin, ex.ev_tiles_end = int(ev_tiles[0]), int(ev_tiles[1])
-    _check(lib().spc_verify_ex(_ptr(q), _ptr(p), _dtype_code(q), _ptr(draft), _ptr(uniforms), B,
-                               gamma, V, int(rule), float(alpha), float(temperature), _ptr(acc),
-                               _ptr(tok), _ptr(dm), ctypes.byref(ex), _stream(stream)))
+    _check(getattr(lib(), entry)(_ptr(q), _ptr(p), _dtype_code(q), _ptr(draft), _ptr(uniforms), B,
+                                  gamma, V, int(rule), float(alpha), float(temperature),
+                                  _ptr(acc), _ptr(tok), _ptr(dm), ctypes.byref(ex),
+                                  _stream(stream)))
     return acc, tok, dm
+
+
+def spc_verify_ex(q, p, draft, uniforms, rule, alpha, temperature, **kw):
+    """spc_verify with per-sequence parameters and optional outputs (keyword
+    arguments of _verify_ex: rule_per_seq, alpha_per_seq, temp_per_seq,
+    out_row_stats, out_argmax, out_sample_norm, workspace, rules_present,
+    ev_tiles, out, stream); returns (accept_len, next_token, defer_mask)."""
+    return _verify_ex("spc_verify_ex", q, p, draft, uniforms, rule, alpha, temperature, **kw)
+
+
+def spc_verify_noalloc(q, p, draft, uniforms, rule, alpha, temperature, **kw):
+    """spc_verify_ex on the library's static scratch: no device allocation
+    (``workspace`` must be None)."""
+    return _verify_ex("spc_verify_noalloc", q, p, draft, uniforms, rule, alpha, temperature,
+                      **kw)
+
+
+def spc_noalloc_scratch_bytes():
+    return lib().spc_noalloc_scratch_bytes()
 
 
 def spc_draft_sample(logits, temperature, uniforms=None, temp_per_seq=None, out=None,
