@@ -88,20 +88,20 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
   L.rowline = o;
   o = align_up(o + 4 * (size_t)(kMaxRows * kLineWords), 256);
   L.zero_end = o;
-  // two job passes, each with R + B row jobs and 2 R + B single jobs at most
-  L.jobs = o; o = align_up(o + 8 * (size_t)(2 * ((R + B) + (2 * R + B))), 256);
+  // two job passes, each with at most R + B row jobs and 2 R + B + R nt
+  // single jobs (argmax halves, draws, TV tiles handed back by the tiles)
+  L.jobs = o; o = align_up(o + 8 * (size_t)(2 * ((R + B) + (2 * R + B + R * nt))), 256);
   L.jobline = o; o = align_up(o + 4 * (size_t)kLineWords * 2 * (R + B), 256);
   L.tiles = o; o = align_up(o + sizeof(TilePart) * R * nt, 256);
-  L.tvpart = o; o = align_up(o + sizeof(double) * R * nt * kParts, 256);
-  L.masses = o; o = align_up(o + sizeof(double) * B * nt * kParts, 256);
-  L.submass = o; o = align_up(o + sizeof(double) * B * nt * kParts * kMaxSub, 256);
+  L.tvpart = o; o = align_up(o + sizeof(double) * R * nt * kSlices, 256);
+  L.submass = o;
+  o = align_up(o + sizeof(double) * B * nt * tile_subchunks(dtype, vec), 256);
   L.moms = o; o = align_up(o + sizeof(TileMom) * R * nt, 256);
   L.rowstat = o; o = align_up(o + sizeof(RowStat) * R, 256);
   L.rowdec = o; o = align_up(o + sizeof(int32_t) * R, 256);
   L.etalist = o; o = align_up(o + sizeof(int32_t) * R * nt, 256);
   L.argres = o; o = align_up(o + sizeof(int32_t) * 4 * R, 256);
   L.etacnt = o; o = align_up(o + sizeof(int32_t) * R, 256);
-  L.seqinfo = o; o = align_up(o + sizeof(int32_t) * 2 * B, 256);
   L.total = o;
   return L;
 }
@@ -308,7 +308,11 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
                             (1u << SPC_RULE_TOKEN_V3);
   const bool pass2_rows = may_sample && (rules & (kTv | kTok));
   const bool may_greedy = force_greedy || per_temp;
-  const int job_passes = pass2_rows ? 2 : 1;
+  // Sequences the statistics kernel finishes are drawn by the draw pass;
+  // job pass 1 takes TV and eta passes and argmax halves, pass 2 the draws of
+  // sequences decided in pass 1 (greedy ones write their token directly).
+  const bool draw_pass = may_sample;
+  const int job_passes = pass2_rows ? 2 : (may_greedy ? 1 : 0);
   // rows a TV job reads again are loaded through the caches
   const bool nt_loads = !(may_sample && (rules & kTv));
   const int64_t nt = stat_tiles(dtype, vec, V);
@@ -342,12 +346,17 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
     P.out_argmax = ex ? offset(ex->out_argmax, b0 * g1 * 2) : nullptr;
     P.out_norm = ex ? offset(ex->out_sample_norm, b0) : nullptr;
     P.job_slots = R + bl;
-    P.single_slots = 2 * R + bl;
+    // TV rows far enough from the end get their TV pass from statistics
+    // workgroups issued about 640 tiles later (a few microseconds of the
+    // stream: the row is merged by then and still in the caches)
+    P.lag = (may_sample && (rules & kTv)) ? (int32_t)std::max<int64_t>(1, (640 + nt - 1) / nt) : 0;
+    // singles: argmax halves, draws, and TV tiles whose stealer gave up
+    P.single_slots = 2 * R + bl + (P.lag > 0 ? R * nt : 0);
+    P.nsub = (int32_t)(nt * spc::tile_subchunks(dtype, vec));
     // workgroups of a job pass: a wavefront per item of its largest possible
     // list, at most two workgroups per compute unit
-    const int64_t np = nt * spc::kParts;
-    const int64_t items1 = np * ((pass2_rows ? R : 0) + (may_sample ? bl : 0)) +
-                           (may_greedy ? 2 * R : 0) + (may_sample ? bl : 0);
+    const int64_t np = nt * spc::kSlices;
+    const int64_t items1 = np * (pass2_rows ? R : 0) + (may_greedy ? 2 * R : 0);
     const int64_t items2 = pass2_rows ? np * bl + bl : 0;
     constexpr int64_t kW = spc::kJobThreads / 64;
     const int job_groups = (int)std::max<int64_t>(
@@ -358,7 +367,6 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
     P.jobline = reinterpret_cast<uint32_t*>(ws + L.jobline);
     P.tiles = reinterpret_cast<spc::TilePart*>(ws + L.tiles);
     P.tvpart = reinterpret_cast<double*>(ws + L.tvpart);
-    P.masses = reinterpret_cast<double*>(ws + L.masses);
     P.submass = reinterpret_cast<double*>(ws + L.submass);
     P.moms = reinterpret_cast<spc::TileMom*>(ws + L.moms);
     P.rowstat = reinterpret_cast<spc::RowStat*>(ws + L.rowstat);
@@ -366,9 +374,8 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
     P.etalist = reinterpret_cast<int32_t*>(ws + L.etalist);
     P.argres = reinterpret_cast<int32_t*>(ws + L.argres);
     P.etacnt = reinterpret_cast<int32_t*>(ws + L.etacnt);
-    P.seqinfo = reinterpret_cast<int32_t*>(ws + L.seqinfo);
     const bool first = b0 == 0;
-    e = spc::launch_step(P, dtype, vec, nt_loads, job_passes, job_groups,
+    e = spc::launch_step(P, dtype, vec, nt_loads, draw_pass, job_passes, job_groups,
                          first && ex ? ex->ev_tiles_begin : nullptr,
                          first && ex ? ex->ev_tiles_end : nullptr, stream);
     if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));

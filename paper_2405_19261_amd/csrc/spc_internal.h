@@ -72,6 +72,8 @@ struct Params {
   int32_t phase;           // job pass of a k_jobs launch (1 or 2)
   int64_t job_slots;       // row jobs a job pass may hold: R + B
   int64_t single_slots;    // single jobs a job pass may hold: 2 R + B
+  int32_t nsub;            // sub-chunks of a row: nt * tile_subchunks
+  int32_t lag;             // TV rows r < R - lag get their TV pass from the tiles of row r + lag
   // workspace: zero region (counters; every launch leaves it as it found it)
   uint32_t* hdr;           // [kHdrLines][kLineWords] job counters
   uint32_t* rowline;       // [kMaxRows][kLineWords] per-row and per-sequence counters
@@ -80,20 +82,20 @@ struct Params {
   uint64_t* jobs;          // [2 passes][job_slots + single_slots] job entries
   uint32_t* jobline;       // [2 passes][job_slots][kLineWords] row-job completion counters
   TilePart* tiles;         // [R][nt] statistics partials
-  double* tvpart;          // [R][nt * kParts] TV partials (OPT) or eta partials (token rules)
-  double* masses;          // [B][nt * kParts] residual masses per part of row j*
-  double* submass;         // [B][nt * kParts][kMaxSub] residual masses per sub-chunk
+  double* tvpart;          // [R][nt][kSlices] TV partials (OPT) or eta partials (token rules)
+  double* submass;         // [B][nsub] residual masses per sub-chunk of row j*
   TileMom* moms;           // [R][nt] first moments (log-loss rules and BiLD*)
   RowStat* rowstat;        // [R] merged row statistics
   int32_t* rowdec;         // [R] bit 0 a_j, bit 1 delta_j
   int32_t* etalist;        // [R][nt] tiles whose eta share needs a second look
   int32_t* argres;         // [R][4] first tile of the q / p maximum, then its lowest index
   int32_t* etacnt;         // [R] tiles listed in etalist
-  int32_t* seqinfo;        // [B][2] j* and sample kind of a residual job
 };
 
 // Entries per statistics tile and per drafter tile for a dtype and load path.
 int stat_tile_elems(int dtype, bool vec);
+// Sub-chunks (lane-load rows of a wavefront) per statistics tile.
+int tile_subchunks(int dtype, bool vec);
 int draft_tile_elems(int dtype, bool vec, bool long_tiles);
 
 // Counters live on 128-byte lines of 32-bit words: arrivals on a shared line
@@ -101,11 +103,11 @@ int draft_tile_elems(int dtype, bool vec, bool long_tiles);
 constexpr int kLineWords = 32;
 constexpr int64_t kMaxRows = 16384;    // rows (and sequences) per launch
 // Job passes: workgroups of kJobThreads threads whose wavefronts take items
-// independently; a row job has kParts items (half tiles) per statistics tile,
-// each of at most kMaxSub sub-chunks.
+// independently; a row job has kSlices items per statistics tile.
 constexpr int kJobThreads = 512;
-constexpr int kParts = 2;
-constexpr int kMaxSub = 16;
+// A statistics tile splits into kSlices slices, one per wavefront of its
+// workgroup (the unit of second-pass partials and residual jobs).
+constexpr int kSlices = kThreads / 64;
 // Header lines: row and single jobs published for pass 1 and pass 2, then per
 // pass kExitLeaves + 1 lines counting the workgroups that have read its counts
 // (a two-level tree; the last arrival clears the pass's counts).
@@ -113,10 +115,15 @@ constexpr int kExitLeaves = 16;
 constexpr int kHdrExit = 4;
 constexpr int kHdrLines = kHdrExit + 2 * (kExitLeaves + 1);
 
-// Words of a row line (counters only): the row's tile arrivals, the
-// decided-row mask of the sequence with the same index (64 bits), the row's
-// argmax-half arrivals, and the drafter kernel's per-row arrivals.
-constexpr int kRowArrive = 0, kSeqMask = 2, kRowJobDone = 4, kDraftArrive = 8;
+// Words of a row line (counters and flags, zero between calls): the row's
+// tile arrivals, the decided-row mask of the sequence with the same index (64
+// bits), the row's argmax-half arrivals, its "merged, TV pass open" flag and
+// TV slice arrivals, the draw pass's arrivals for the sequence, the drafter
+// kernel's per-row arrivals, and the sequence's outcome for the draw pass.
+constexpr int kRowArrive = 0, kSeqMask = 2, kRowJobDone = 4, kRowReady = 5, kRowTvArrive = 6,
+              kSeqResArrive = 7, kDraftArrive = 8, kSeqInfo = 9;
+// A sequence's outcome word (kSeqInfo): kSeqInfoSet | sample kind << 8 | j*.
+constexpr uint32_t kSeqInfoSet = 0x80000000u;
 
 // Words between the drafter kernel's per-row completion counters.
 constexpr int kDraftCntStride = kLineWords;
@@ -125,8 +132,8 @@ constexpr int kDraftCntStride = kLineWords;
 // region (header lines, row lines) has the same size for every shape.
 struct WsLayout {
   size_t hdr, rowline, zero_end;
-  size_t jobs, jobline, tiles, tvpart, masses, submass, moms, rowstat, rowdec, etalist, argres, etacnt,
-      seqinfo, total;
+  size_t jobs, jobline, tiles, tvpart, submass, moms, rowstat, rowdec, etalist, argres, etacnt,
+      total;
 };
 WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec);
 
@@ -138,13 +145,14 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec);
 hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, bool long_tiles,
                         hipStream_t stream);
 
-// Enqueue one verify launch: the statistics tiles (k_tiles), then
-// `job_passes` job passes (k_jobs) of `job_groups` workgroups each.
+// Enqueue one verify launch: the statistics tiles (k_tiles), the draw pass
+// (k_res) when `draw_pass`, then `job_passes` job passes (k_jobs) of
+// `job_groups` workgroups each.
 // nt_loads: the tiles read the logits non-temporally (no job reads a whole
 // row again).
 // ev_begin / ev_end (may be null): recorded right before and after k_tiles.
-hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, int job_passes,
-                       int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end,
+hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, bool draw_pass,
+                       int job_passes, int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end,
                        hipStream_t stream);
 
 // Enqueue a kernel writing `bytes` zero bytes at `ptr` (a multiple of 4, ptr

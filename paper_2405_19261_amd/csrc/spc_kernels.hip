@@ -569,6 +569,7 @@ struct ProbScale {
   float c_hi, c_lo, q_hi, q_lo, p_hi, p_lo;
   double c;   // log2(e) / T
   double dl;  // lz_p - lz_q
+  float dl_hi, dl_lo;  // dl = dl_hi + dl_lo (dl_lo = 0 when dl is not finite)
   TokenRule tok;  // token rules only
 };
 
@@ -592,6 +593,8 @@ __device__ __forceinline__ ProbScale prob_scale(const SeqParam& s, const RowStat
   ps.p_hi = (float)lzp;
   ps.p_lo = isfinite(lzp) ? (float)(lzp - (double)ps.p_hi) : 0.0f;
   ps.dl = lzp - rs.lz_q;
+  ps.dl_hi = (float)ps.dl;
+  ps.dl_lo = isfinite(ps.dl) ? (float)(ps.dl - (double)ps.dl_hi) : 0.0f;
   return ps;
 }
 
@@ -610,16 +613,27 @@ __device__ __forceinline__ float exp2m1_over_d(float d) {
   return fmaf(r, d, 0.6931471824645996f);
 }
 
-// Residual weight max(0, p_v - q_v), without branches.  d = log2(p_v / q_v) is
-// formed in fp64 from the exact difference zp - zq, so p ~ q does not cancel:
-// below d = 1/4 the weight is q_v (2^d - 1); above, p_v - q_v itself, where
-// p_v > 1.18 q_v bounds the cancellation.  Both -inf gives a NaN d and weight
-// 0; zq = -inf alone gives d = +inf and weight p_v.
-__device__ __forceinline__ float residual_weight(float zq, float zp, const ProbScale& s) {
-  const float d = (float)fma((double)zp - (double)zq, s.c, -s.dl);
-  const float pq = prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
-  const float pp = prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
-  float small = pq * (d * exp2m1_over_d(d)), big = pp - pq;
+// Residual weight max(0, p_v - q_v), without branches, from p_v and
+// d = log2(p_v / q_v): p_v (1 - 2^-d) for d >= 1/4, where 2^-d <= 0.85 bounds
+// the cancellation, and below it q_v d (2^d - 1) / d with q_v = p_v 2^-d, so
+// the weight keeps full relative precision as d -> 0.  d comes from the exact
+// difference zp - zq: bf16 logits differ exactly in float32, and d is then
+// formed with the split constants (c_hi + c_lo, dl_hi + dl_lo) to about an
+// ulp; float32 logits take the difference in fp64.  zq = -inf gives d = +inf
+// and weight p_v; zp = -inf gives d = -inf, and both -inf a NaN d: weight 0.
+// pp is p_v (the caller's, shared with the token-rule target).
+template <int DT>
+__device__ __forceinline__ float residual_from_pp(float zq, float zp, float pp,
+                                                  const ProbScale& s) {
+  float d;
+  if constexpr (DT == 1) {
+    const float dz = zp - zq;
+    d = fmaf(dz, s.c_hi, -s.dl_hi) + fmaf(dz, s.c_lo, -s.dl_lo);
+  } else {
+    d = (float)fma((double)zp - (double)zq, s.c, -s.dl);
+  }
+  const float e = exp2_hw(-d);  // q_v / p_v
+  float small = (pp * e) * (d * exp2m1_over_d(d)), big = fmaf(-pp, e, pp);
   // both arms stay computed: left alone, the compiler sinks each into a
   // divergent branch, which costs more than evaluating both
   asm volatile("" : "+v"(small), "+v"(big));
@@ -627,22 +641,26 @@ __device__ __forceinline__ float residual_weight(float zq, float zp, const ProbS
   return d > 0.0f ? w : 0.0f;
 }
 
+template <int DT>
+__device__ __forceinline__ float residual_weight(float zq, float zp, const ProbScale& s) {
+  return residual_from_pp<DT>(zq, zp, prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo), s);
+}
+
 // Weight of one entry under a sampled distribution.  With a token rule the p
 // scale carries eta (prob_scale): the residual max(0, pi - q) of Alg. 6's
 // target is p eta where r = 0 and max(0, p eta - q) where r = 1, and the
 // target itself is p eta where r = 1 and q + p eta where r = 0.
-template <int KIND>
+template <int DT, int KIND>
 __device__ __forceinline__ float weight_of(float zq, float zp, const ProbScale& s) {
   if constexpr (KIND == kQ) {
     return prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
   } else if constexpr (KIND == kP) {
     return prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
   } else if constexpr (KIND == kResidual) {
-    return residual_weight(zq, zp, s);
+    return residual_weight<DT>(zq, zp, s);
   } else if constexpr (KIND == kTokRes) {
-    float res = residual_weight(zq, zp, s), pe = prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
-    asm volatile("" : "+v"(res), "+v"(pe));
-    return token_r(s.tok, zq, zp) ? res : pe;
+    const float pe = prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
+    return token_r(s.tok, zq, zp) ? residual_from_pp<DT>(zq, zp, pe, s) : pe;
   } else {
     const float pe = prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
     const float qe = prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
@@ -906,60 +924,61 @@ __device__ __forceinline__ double part_mass(const Params& P, int64_t row, int b,
     const TilePart t = ld_tile(P.tiles + row * P.nt + k);
     const double qm = t.s_q * exp2_acc((double)t.r_q - rs.lz_q);
     const double pm = t.s_p * exp2_acc((double)t.r_p - rs.lz_p);
-    const double* ep = P.tvpart + (row * P.nt + k) * kParts;  // the tile's eta partials
-    return fmax(qm - (ld_dev_f64(ep) + ld_dev_f64(ep + 1)), 0.0) + rs.tv * pm;
+    const double* ep = P.tvpart + (row * P.nt + k) * kSlices;  // the tile's eta partials
+    const double eta_k = (ld_dev_f64(ep) + ld_dev_f64(ep + 1)) + (ld_dev_f64(ep + 2) + ld_dev_f64(ep + 3));
+    return fmax(qm - eta_k, 0.0) + rs.tv * pm;
   } else {
-    return ld_dev_f64(P.masses + (int64_t)b * P.nt * kParts + k);
+    return ld_dev_f64(P.submass + (int64_t)b * P.nsub + k);
   }
 }
 
 // Wave 0: the part (tile or chunk) of the inverse-CDF draw -- the first part
 // k with C_k > u W, C_k the running mass through part k in vocabulary order
 // and W the total -- and the target mass left at its start.  Returns W.
-// Parts are read kFindGroup per lane at a time, all loads in flight
-// together; for at most 64 * kFindGroup parts both passes use one read.
+// Parts are read G per lane at a time, all loads in flight together; for at
+// most 64 G parts both passes use one read.
 constexpr int kFindGroup = 4;
 
-template <int SRC>
+template <int SRC, int G>
 __device__ __forceinline__ void load_parts(const Params& P, int64_t row, int b, int K, int k0,
-                                           const RowStat& rs, double (&m)[kFindGroup]) {
+                                           const RowStat& rs, double (&m)[G]) {
   const int lane = threadIdx.x & 63;
 #pragma unroll
-  for (int j = 0; j < kFindGroup; ++j) {
+  for (int j = 0; j < G; ++j) {
     const int k = k0 + j * 64 + lane;
     m[j] = k < K ? part_mass<SRC>(P, row, b, k, rs) : 0.0;
   }
 }
 
-template <int SRC>
+template <int SRC, int G = kFindGroup>
 __device__ __forceinline__ double find_part(const Params& P, int64_t row, int b, int K,
                                             const RowStat& rs, float u, int* ks_out,
                                             double* rem_out) {
-  constexpr int GN = 64 * kFindGroup;
-  double m0[kFindGroup];
-  load_parts<SRC>(P, row, b, K, 0, rs, m0);
+  constexpr int GN = 64 * G;
+  double m0[G];
+  load_parts<SRC, G>(P, row, b, K, 0, rs, m0);
   double W = 0.0;
 #pragma unroll
-  for (int j = 0; j < kFindGroup; ++j) W += wave_sum(m0[j]);
+  for (int j = 0; j < G; ++j) W += wave_sum(m0[j]);
   for (int k0 = GN; k0 < K; k0 += GN) {
-    double m[kFindGroup];
-    load_parts<SRC>(P, row, b, K, k0, rs, m);
+    double m[G];
+    load_parts<SRC, G>(P, row, b, K, k0, rs, m);
 #pragma unroll
-    for (int j = 0; j < kFindGroup; ++j) W += wave_sum(m[j]);
+    for (int j = 0; j < G; ++j) W += wave_sum(m[j]);
   }
   const double target = (double)u * W;
   double carry = 0.0, rem = 0.0;
   int ks = -1, klast = -1;
   for (int k0 = 0; k0 < K && ks < 0; k0 += GN) {
-    double m[kFindGroup];
+    double m[G];
     if (k0 == 0) {
 #pragma unroll
-      for (int j = 0; j < kFindGroup; ++j) m[j] = m0[j];
+      for (int j = 0; j < G; ++j) m[j] = m0[j];
     } else {
-      load_parts<SRC>(P, row, b, K, k0, rs, m);
+      load_parts<SRC, G>(P, row, b, K, k0, rs, m);
     }
 #pragma unroll
-    for (int j = 0; j < kFindGroup; ++j) {
+    for (int j = 0; j < G; ++j) {
       const double incl = carry + wave_incl_scan(m[j]);
       const unsigned long long pos = __ballot(m[j] > 0.0);
       const unsigned long long hit = __ballot(m[j] > 0.0 && incl > target);
@@ -1006,7 +1025,7 @@ __device__ __forceinline__ void pick_wave(const Params& P, int b, int64_t row, i
     double m = 0.0;
 #pragma unroll
     for (int e = 0; e < C::VW; ++e) {
-      const float w = weight_of<KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
+      const float w = weight_of<DT, KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
       m += (double)w;
       if (w > 0.0f) last_pos = max(last_pos, (int)(base + e));
       if (e & 1) __builtin_amdgcn_sched_barrier(0);
@@ -1037,7 +1056,7 @@ __device__ __forceinline__ void pick_wave(const Params& P, int b, int64_t row, i
   int hit = -1, lastw = -1;
 #pragma unroll
   for (int e = 0; e < C::VW; ++e) {
-    const float w = weight_of<KIND>(elem<DT, VEC>(sq, e), elem<DT, VEC>(sp_, e), ps);
+    const float w = weight_of<DT, KIND>(elem<DT, VEC>(sq, e), elem<DT, VEC>(sp_, e), ps);
     run += (double)w;
     if (w > 0.0f) lastw = (int)(hbase + e);
     if (hit < 0 && run > rem && w > 0.0f) hit = (int)(hbase + e);
@@ -1071,7 +1090,7 @@ __device__ __forceinline__ void subchunk_masses(const Params& P, int64_t row, in
       float t = 0.0f;
 #pragma unroll
       for (int e = 0; e < C::VW; ++e) {
-        t += weight_of<KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
+        t += weight_of<DT, KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
         // two entries at a time keep the weights' temporaries few
         if (e & 1) __builtin_amdgcn_sched_barrier(0);
       }
@@ -1343,12 +1362,89 @@ __device__ __forceinline__ bool eta_from_stats(const TokenRule& tr, const TilePa
 }
 
 
+// ---------------------------------------------------------------- slices
+// A slice is wavefront w's share of a statistics tile in the tile's own
+// layout: lane loads i = 0 .. U-1 of threads w*64 .. w*64+63, lane load i
+// covering the 64 VW consecutive entries at t0 + (i * 4 + w) * 64 VW -- the
+// tile's sub-chunk i * 4 + w.  A statistics workgroup that takes a second
+// pass over a tile (its wavefront w computing slice w) and a job-pass
+// wavefront that takes one slice compute the same partial with the same
+// arithmetic, so a row's result does not depend on which did it.
+static_assert(kSlices == kWaves, "a tile has one slice per wavefront of its workgroup");
+template <int DT, bool VEC>
+using PartC = Chunk<DT, VEC, 2 * StatTile<DT, VEC>::U>;  // half a tile, wave-contiguous
+template <int DT, bool VEC>
+using SubC = Chunk<DT, VEC, 1>;
+
+// Wave: "am I the last of n arrivals on cnt?" after this wavefront's item
+// (its results stored by its own lanes), arriving with weight w.  On true
+// the counter is reset and the wavefront reads the other items' results with
+// ld_dev_*.
+__device__ __forceinline__ bool arrive_last_w(uint32_t* cnt, uint32_t n, uint32_t w = 1u) {
+  uint32_t prev = 0;
+  if ((threadIdx.x & 63) == 0) {
+    vmem_drain();  // every lane's stores of this item are complete
+    prev = add_u32(cnt, w);
+    if (prev == n - w) st_u32(cnt, 0u);
+  }
+  const bool last = (uint32_t)lane_i32((int)prev, 0) == n - w;
+  if (last) vmem_drain();
+  return last;
+}
+
+// Wave: the masses of the sub-chunks of slice w of the tile at entry t0 of
+// a row under the distribution KIND; lane i < U returns sub-chunk i * 4 + w's
+// (float sums per lane load, fp64 across lanes), other lanes 0.
+template <int DT, bool VEC, int KIND>
+__device__ __forceinline__ double slice_masses_w(const Params& P, int64_t row, int64_t t0, int w,
+                                                 const ProbScale& ps) {
+  using T = StatTile<DT, VEC>;
+  const int lane = threadIdx.x & 63, V = P.V;
+  uint32_t cq[T::U][T::NW] = {}, cp[T::U][T::NW] = {};
+  if (KIND != kP)
+    load_tile<DT, VEC, T::U, true>((const char*)P.q + row * V * T::EB, t0, V, cq, w * 64 + lane);
+  if (KIND != kQ)
+    load_tile<DT, VEC, T::U, true>((const char*)P.p + row * V * T::EB, t0, V, cp, w * 64 + lane);
+  double mine = 0.0;
+#pragma unroll
+  for (int i = 0; i < T::U; ++i) {
+    float t = 0.0f;
+#pragma unroll
+    for (int e = 0; e < T::VW; ++e) {
+      t += weight_of<DT, KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
+      if (e & 1) __builtin_amdgcn_sched_barrier(0);
+    }
+    const double s = wave_sum((double)t);
+    if (lane == i) mine = s;
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  return mine;
+}
+
+// Wave: the second-pass partial of slice w of tile k of row r -- the TV
+// weight max(0, p - q), or eta's share (the q mass of the entries the rule
+// marks) -- into tvpart[r][k * 4 + w].
+template <int DT, bool VEC, bool TOK, bool NT = true>
+__device__ __forceinline__ void pass2_slice_w(const Params& P, int r, int k, int w,
+                                              const ProbScale& ps) {
+  using T = StatTile<DT, VEC>;
+  const int lane = threadIdx.x & 63, V = P.V;
+  const int64_t t0 = (int64_t)k * T::N;
+  uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
+  load_tile<DT, VEC, T::U, NT>((const char*)P.q + (int64_t)r * V * T::EB, t0, V, wq, w * 64 + lane);
+  load_tile<DT, VEC, T::U, NT>((const char*)P.p + (int64_t)r * V * T::EB, t0, V, wp, w * 64 + lane);
+  double acc = pass2_sum<DT, VEC, TOK>(wq, wp, ps);
+  acc = wave_sum(acc);
+  if (lane == 0) st_dev_f64(P.tvpart + ((int64_t)r * P.nt + k) * kSlices + w, acc);
+}
+
 // ================================================================ the step
 // Jobs a row or a sequence publishes for the job pass that follows: a TV or
 // eta second pass over a row and the residual masses of row j* of a sequence
 // are "row jobs" of nt chunks (one per tile); the two halves of a greedy
 // row's argmax and the draws from statistics partials are single chunks.
-enum JobKind : int { kJobTv = 1, kJobEta = 2, kJobRes = 3, kJobArg = 4, kJobDraw = 5 };
+enum JobKind : int { kJobTv = 1, kJobEta = 2, kJobRes = 3, kJobArg = 4, kJobDraw = 5,
+                     kJobTvTile = 6 };
 
 // A job entry: kind (bits 60..63), an extra field (bits 32..59: the argmax
 // tensor, or a draw's sample kind and j*) and the row or sequence it belongs
@@ -1394,12 +1490,12 @@ __device__ __forceinline__ uint64_t lane_u64(uint64_t v, int l) {
 // eta job per row and one draw per sequence); the bounds only keep a broken
 // count from writing past them.
 __device__ __forceinline__ void publish_row_job(const Params& P, int phase, int kind,
-                                                uint32_t id) {
+                                                uint32_t id, uint32_t extra = 0u) {
   if (phase > 2) return;
   const uint32_t s = add_u32(hdr_word(P, hdr_line(phase, false)), 1u);
   if ((int64_t)s >= P.job_slots) return;
   st_u32(job_done(P, phase, s), 0u);
-  st_u64(job_list(P, phase, false) + s, job_entry(kind, 0u, id));
+  st_u64(job_list(P, phase, false) + s, job_entry(kind, extra, id));
 }
 __device__ __forceinline__ void publish_single(const Params& P, int phase, int kind,
                                                uint32_t extra, uint32_t id) {
@@ -1418,8 +1514,9 @@ struct StepShared {
 };
 
 // Wave: sequence b's first rejection is j* = f.  Writes its accept length,
-// then the greedy token, or publishes the draw -- from the statistics
-// partials (a single job) or from the residual of row f (a row job) -- to
+// then the greedy token; or, for a draw (from the statistics partials, or
+// from the residual of row f), records it for the draw pass when the
+// statistics kernel finished the sequence (phase 1), else publishes it to
 // the job pass `phase`.
 template <int DT>
 __device__ __forceinline__ void seq_finish_w(const Params& P, int b, int f, const SeqParam& sp,
@@ -1452,10 +1549,12 @@ __device__ __forceinline__ void seq_finish_w(const Params& P, int b, int f, cons
     // residual max(0, q - q) is empty, so p is sampled instead
     kind = (f < gamma) ? (dstar ? kResidual : kP) : (dstar ? kP : kQ);
   }
-  if (kind == kResidual || kind == kTokRes) {
-    st_i32(P.seqinfo + (int64_t)b * 2 + 0, f);
-    st_i32(P.seqinfo + (int64_t)b * 2 + 1, kind);
-    publish_row_job(P, phase, kJobRes, (uint32_t)b);
+  if (phase == 1) {
+    // finished by the statistics kernel: the draw pass (k_res) reads the
+    // sequence's outcome from its line
+    st_u32(row_word(P, b, kSeqInfo), kSeqInfoSet | ((uint32_t)kind << 8) | (uint32_t)f);
+  } else if (kind == kResidual || kind == kTokRes) {
+    publish_row_job(P, phase, kJobRes, (uint32_t)b, ((uint32_t)kind << 8) | (uint32_t)f);
   } else {
     publish_single(P, phase, kJobDraw, ((uint32_t)kind << 8) | (uint32_t)f, (uint32_t)b);
   }
@@ -1558,7 +1657,14 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
   if (sp.valid && has_tv_parts(sp.rule)) {
     if (lane == 0) {
       st_rowstat(P.rowstat + r, rs);
-      publish_row_job(P, 1, kJobTv, (uint32_t)r);
+      if (r < P.B * (P.gamma + 1) - P.lag) {
+        // the statistics workgroups of row r + lag take its TV pass, one
+        // tile each, once they see the row merged
+        vmem_drain();
+        st_u32(row_word(P, r, kRowReady), 1u);
+      } else {
+        publish_row_job(P, 1, kJobTv, (uint32_t)r);
+      }
     }
     return;
   }
@@ -1576,9 +1682,12 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
       bool need = false;
       if (k < nt) {
         need = !eta_from_stats(tr, ld_tile(P.tiles + (int64_t)r * nt + k), rs.lz_q, &e);
-        if (!need) {  // the tile's share, on its first part
-          st_dev_f64(P.tvpart + ((int64_t)r * nt + k) * kParts, e);
-          st_dev_f64(P.tvpart + ((int64_t)r * nt + k) * kParts + 1, 0.0);
+        if (!need) {  // the tile's share, on its first slice
+          double* ep = P.tvpart + ((int64_t)r * nt + k) * kSlices;
+          st_dev_f64(ep, e);
+          st_dev_f64(ep + 1, 0.0);
+          st_dev_f64(ep + 2, 0.0);
+          st_dev_f64(ep + 3, 0.0);
         }
       }
       const unsigned long long nm = __ballot(need);
@@ -1601,11 +1710,81 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
   if (f >= 0) seq_finish_w<DT>(P, b, f, sp, 1);
 }
 
+// Wave: the row's decision once its TV, eta or argmax is known; when it
+// settles j*, the sequence's finish publishes to the next job pass.
+template <int DT>
+__device__ __forceinline__ void row_job_decide(const Params& P, int kind, int r, int phase) {
+  const int g1 = P.gamma + 1, np = P.nt * kSlices;
+  const int b = r / g1, j = r - b * g1;
+  RowStat rs = ld_rowstat(P.rowstat + r);
+  if (kind == kJobArg) {
+    rs.amax_q = ld_i32(P.argres + (int64_t)r * 4 + 2);
+    rs.amax_p = ld_i32(P.argres + (int64_t)r * 4 + 3);
+  } else {
+    // the TV or eta partials of every slice, in slice order
+    double s = 0.0;
+    for (int k = threadIdx.x & 63; k < np; k += 64)
+      s += ld_dev_f64(P.tvpart + (int64_t)r * np + k);
+    rs.tv = wave_sum(s);
+  }
+  const SeqParam sp = seq_param(P, b);
+  const int f = row_decide_w<DT>(P, r, b, j, sp, rs);
+  if (f >= 0) seq_finish_w<DT>(P, b, f, sp, phase + 1);
+}
+
+// The wait of a stealing workgroup for its row's merge is bounded: 40 us of
+// the 100 MHz real-time clock, far beyond the usual lag; past it the tile
+// goes to the job pass.
+constexpr uint64_t kStealWait = 4000;
+
+// Wave: the last of the 4 nt slices of TV row rv arrived: its decision (and
+// the sequence's finish, publishing to job pass 1), then the row's ready
+// flag is cleared for the next call.
+template <int DT>
+__device__ __forceinline__ void tv_row_done(const Params& P, int rv, int phase) {
+  row_job_decide<DT>(P, kJobTv, rv, phase);
+  if ((threadIdx.x & 63) == 0) st_u32(row_word(P, rv, kRowReady), 0u);
+}
+
+// Whole block: the TV pass over tile k of row rv, whose statistics tiles
+// were issued lag rows before this workgroup's.  Once the row's merge has set
+// its ready flag, wavefront w computes slice w; the workgroup then arrives
+// with all four, and the last arrival decides the row.  The workgroups of row
+// rv were all dispatched before this one, so the wait depends only on
+// workgroups that are running or done.
+template <int DT, bool VEC>
+__device__ __forceinline__ void tv_steal(const Params& P, int rv, int k, const SeqParam& spv,
+                                         Shared& sh) {
+  if (threadIdx.x == 0) {
+    const uint32_t* flag = row_word(P, rv, kRowReady);
+    uint32_t f = ld_u32(flag);
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    while (f == 0u && __builtin_amdgcn_s_memrealtime() - t0 < kStealWait) {
+      __builtin_amdgcn_s_sleep(4);
+      f = ld_u32(flag);
+    }
+    sh.flag = f != 0u;
+  }
+  __syncthreads();
+  if (!sh.flag) {  // block-uniform: the merge is late, the job pass takes the tile
+    if (threadIdx.x == 0) publish_single(P, 1, kJobTvTile, (uint32_t)k, (uint32_t)rv);
+    return;
+  }
+  const RowStat rs = ld_rowstat(P.rowstat + rv);
+  pass2_slice_w<DT, VEC, false>(P, rv, k, threadIdx.x >> 6, prob_scale(spv, rs, false));
+  vmem_drain();
+  __syncthreads();  // all four slices are stored
+  if (threadIdx.x < 64 &&
+      arrive_last_w(row_word(P, rv, kRowTvArrive), (uint32_t)(kSlices * P.nt), kSlices))
+    tv_row_done<DT>(P, rv, 0);
+}
+
 // The statistics tiles.  grid (nt, R): tile k of row r; NT: read the logits
-// non-temporally (rows that no job reads again), else through the caches (a
-// TV job reads the row again right after).  After the tile partial only wave
-// 0 stays: it arrives on the row's counter, and the last tile of the row
-// merges and decides it.
+// non-temporally (no TV pass reads the rows again), else through the caches.
+// After the tile partial wave 0 arrives on the row's counter, and the last
+// tile of the row merges and decides it.  Without NT, a workgroup of row r
+// then takes tile k of the TV pass of row r - lag when that is a TV row
+// (tv_steal); otherwise waves 1-3 leave after the partial.
 template <int DT, bool VEC, int MS, bool NT>
 __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
   using T = StatTile<DT, VEC>;
@@ -1614,6 +1793,15 @@ __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
   const int nt = P.nt, g1 = P.gamma + 1, V = P.V;
   const int b = r / g1, j = r - b * g1;
   const SeqParam sp = seq_param(P, b);
+  // the TV pass over tile k of row r - lag (OPT / OPTLOG at T > 0) is this
+  // workgroup's second job
+  const int rv = r - P.lag;
+  SeqParam spv = sp;
+  bool steal = false;
+  if (!NT && P.lag > 0 && rv >= 0) {  // batches that may hold TV rows read through the caches
+    spv = seq_param(P, rv / g1);
+    steal = spv.valid && !spv.greedy && has_tv_parts(spv.rule);
+  }
   const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
   const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
   const int64_t t0 = (int64_t)k * T::N;
@@ -1624,48 +1812,25 @@ __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
     tile_partial<DT, VEC, MS>(P, r, k, sp, wq, wp, sh);
   else
     tile_partial<DT, VEC, 0>(P, r, k, sp, wq, wp, sh);
-  if (threadIdx.x >= 64) return;
-  // wave 0: thread 0 stored the partial; arrive on the row's counter
-  uint32_t prev = 0;
-  if (threadIdx.x == 0) {
-    vmem_drain();
-    prev = add_u32(row_word(P, r, kRowArrive), 1u);
-    if (prev == (uint32_t)nt - 1u) st_u32(row_word(P, r, kRowArrive), 0u);
+  if (threadIdx.x < 64) {
+    // wave 0: thread 0 stored the partial; arrive on the row's counter
+    uint32_t prev = 0;
+    if (threadIdx.x == 0) {
+      vmem_drain();
+      prev = add_u32(row_word(P, r, kRowArrive), 1u);
+      if (prev == (uint32_t)nt - 1u) st_u32(row_word(P, r, kRowArrive), 0u);
+    }
+    if ((uint32_t)lane_i32((int)prev, 0) == (uint32_t)nt - 1u) {
+      vmem_drain();
+      row_merged_w<DT, MS>(P, r, b, j, sp);
+    }
   }
-  if ((uint32_t)lane_i32((int)prev, 0) != (uint32_t)nt - 1u) return;
-  vmem_drain();
-  row_merged_w<DT, MS>(P, r, b, j, sp);
+  if constexpr (!NT) {
+    if (steal) tv_steal<DT, VEC>(P, rv, k, spv, sh);
+  }
 }
 
 // ---------------------------------------------------------------- job pass
-// The job pass works in wavefronts: every item is one wavefront's, and the
-// wavefronts of a workgroup take items independently (no block barriers
-// after the start).  A row job (a TV or eta pass over a row, a sequence's
-// residual over row j*) has kParts items per statistics tile: a part is half
-// a tile, read by one wavefront, lane load i of lane l covering entries
-// (i * 64 + l) * VW .. + VW - 1; each of its lane-load rows (64 VW entries)
-// is a sub-chunk.
-template <int DT, bool VEC>
-using PartC = Chunk<DT, VEC, 2 * StatTile<DT, VEC>::U>;
-template <int DT, bool VEC>
-using SubC = Chunk<DT, VEC, 1>;
-static_assert(kParts == 2, "a part is half a statistics tile");
-
-// Wave: "am I the last of n arrivals on cnt?" after this wavefront's item
-// (its results stored by its own lanes).  On true the counter is reset and
-// the wavefront reads the other items' results with ld_dev_*.
-__device__ __forceinline__ bool arrive_last_w(uint32_t* cnt, uint32_t n) {
-  uint32_t prev = 0;
-  if ((threadIdx.x & 63) == 0) {
-    vmem_drain();  // every lane's stores of this item are complete
-    prev = add_u32(cnt, 1u);
-    if (prev == n - 1u) st_u32(cnt, 0u);
-  }
-  const bool last = (uint32_t)lane_i32((int)prev, 0) == n - 1u;
-  if (last) vmem_drain();
-  return last;
-}
-
 // Wave: the masses of the NS sub-chunks of the part at entry e0 of a row
 // under the distribution KIND; lane base + i returns sub-chunk i's (float
 // sums per lane load, fp64 across lanes), other lanes 0.
@@ -1684,11 +1849,12 @@ __device__ __forceinline__ double part_masses_w(const Params& P, int64_t row, in
     float t = 0.0f;
 #pragma unroll
     for (int e = 0; e < C::VW; ++e) {
-      t += weight_of<KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
+      t += weight_of<DT, KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
       if (e & 1) __builtin_amdgcn_sched_barrier(0);
     }
     const double s = wave_sum((double)t);
     if (lane == base + i) mine = s;
+    __builtin_amdgcn_sched_barrier(0);  // one lane load's weights at a time
   }
   return mine;
 }
@@ -1720,27 +1886,37 @@ __device__ __forceinline__ void draw_in_subs_w(const Params& P, int b, int64_t r
 
 // Wave: the inverse-CDF draw of sequence b at row `row` (the row of j*) from
 // the distribution `kind`, its part masses from `src`: the statistics
-// partials per tile, or the residual job's masses per part (whose sub-chunk
-// masses the job stored).  An empty residual (possible only through
-// rounding) is replaced by p.
+// partials per tile (then the tile's sub-chunk masses are summed here), or
+// the residual job's sub-chunk masses, searched directly.  An empty residual
+// (possible only through rounding) is replaced by p.
 template <int DT, bool VEC, int KIND>
-__device__ __forceinline__ void draw_kind_w(const Params& P, int b, int64_t row, int src, int ks,
+__device__ __forceinline__ void draw_kind_w(const Params& P, int b, int64_t row, int ks,
                                             double rem, const ProbScale& ps) {
-  const int lane = threadIdx.x & 63;
-  constexpr int NS = PartC<DT, VEC>::U;
-  if (src == kSrcPass) {
-    const int np = P.nt * kParts;
-    const double ml = lane < NS ? ld_dev_f64(P.submass + ((int64_t)b * np + ks) * kMaxSub + lane)
-                                : 0.0;
-    draw_in_subs_w<DT, VEC, KIND>(P, b, row, (int64_t)ks * PartC<DT, VEC>::N, ml, NS, rem, ps);
+  if constexpr (KIND == kResidual || KIND == kTokRes) {
+    // the residual job's sub-chunk masses were searched: ks is a sub-chunk
+    pick_wave<DT, VEC, SubC<DT, VEC>, KIND>(P, b, row, (int64_t)ks * SubC<DT, VEC>::N, rem, ps);
   } else {
-    // a statistics tile: the sub-chunk masses of both its parts
+    // a statistics tile: the masses of its sub-chunks, in tile order
     const int64_t t0 = (int64_t)ks * StatTile<DT, VEC>::N;
     double m = 0.0;
+    if constexpr (KIND == kTokPi) {
+      // both tensors: one slice (sub-chunks i * 4 + w) at a time
+      const int lane = threadIdx.x & 63;
 #pragma unroll 1
-    for (int part = 0; part < kParts; ++part)
-      m += part_masses_w<DT, VEC, KIND>(P, row, t0 + part * PartC<DT, VEC>::N, ps, part * NS);
-    draw_in_subs_w<DT, VEC, KIND>(P, b, row, t0, m, kParts * NS, rem, ps);
+      for (int w = 0; w < kSlices; ++w) {
+        const double mw = slice_masses_w<DT, VEC, KIND>(P, row, t0, w, ps);
+        const int i = lane / kSlices;  // lane i * 4 + w takes sub-chunk i of slice w
+        const double v = __shfl(mw, i);
+        if (lane % kSlices == w && i < StatTile<DT, VEC>::U) m = v;
+      }
+    } else {
+      // one tensor: the tile's two wave-contiguous halves
+      constexpr int NS = PartC<DT, VEC>::U;
+#pragma unroll 1
+      for (int half = 0; half < 2; ++half)
+        m += part_masses_w<DT, VEC, KIND>(P, row, t0 + half * PartC<DT, VEC>::N, ps, half * NS);
+    }
+    draw_in_subs_w<DT, VEC, KIND>(P, b, row, t0, m, StatTile<DT, VEC>::U * kSlices, rem, ps);
   }
 }
 
@@ -1749,13 +1925,12 @@ __device__ __forceinline__ void draw_w(const Params& P, int b, int64_t row, int 
                                        const SeqParam& sp, const RowStat& rs) {
   const int lane = threadIdx.x & 63;
   const float u = P.uniforms[(int64_t)b * (P.gamma + 1) + P.gamma];
-  const int np = P.nt * kParts;
   int ks;
   double rem, W;
   if (src == kSrcStatsQ) W = find_part<kSrcStatsQ>(P, row, b, P.nt, rs, u, &ks, &rem);
   else if (src == kSrcStatsP) W = find_part<kSrcStatsP>(P, row, b, P.nt, rs, u, &ks, &rem);
   else if (src == kSrcTokPi) W = find_part<kSrcTokPi>(P, row, b, P.nt, rs, u, &ks, &rem);
-  else W = find_part<kSrcPass>(P, row, b, np, rs, u, &ks, &rem);
+  else W = find_part<kSrcPass, 8>(P, row, b, P.nsub, rs, u, &ks, &rem);
   if ((kind == kResidual || kind == kTokRes) && !(W > 0.0)) {
     kind = kP;
     src = kSrcStatsP;
@@ -1767,57 +1942,26 @@ __device__ __forceinline__ void draw_w(const Params& P, int b, int64_t row, int 
   }
   if (ks < 0) return;  // wave-uniform
   const ProbScale ps = prob_scale(sp, rs, kind == kTokRes || kind == kTokPi);
-  if (kind == kQ) draw_kind_w<DT, VEC, kQ>(P, b, row, src, ks, rem, ps);
-  else if (kind == kP) draw_kind_w<DT, VEC, kP>(P, b, row, src, ks, rem, ps);
-  else if (kind == kTokPi) draw_kind_w<DT, VEC, kTokPi>(P, b, row, src, ks, rem, ps);
-  else if (kind == kTokRes) draw_kind_w<DT, VEC, kTokRes>(P, b, row, src, ks, rem, ps);
-  else draw_kind_w<DT, VEC, kResidual>(P, b, row, src, ks, rem, ps);
+  if (kind == kQ) draw_kind_w<DT, VEC, kQ>(P, b, row, ks, rem, ps);
+  else if (kind == kP) draw_kind_w<DT, VEC, kP>(P, b, row, ks, rem, ps);
+  else if (kind == kTokPi) draw_kind_w<DT, VEC, kTokPi>(P, b, row, ks, rem, ps);
+  else if (kind == kTokRes) draw_kind_w<DT, VEC, kTokRes>(P, b, row, ks, rem, ps);
+  else draw_kind_w<DT, VEC, kResidual>(P, b, row, ks, rem, ps);
 }
 
-// Wave: part c of a TV or eta row job of row r -- the TV weight
-// max(0, p - q), or eta's share (for eta, the half c % kParts of the
-// (c / kParts)-th listed tile; a part past the list does nothing).
+// Wave: item c = k * 4 + w of a TV or eta row job of row r: slice w of tile
+// k (for eta, of the k-th listed tile; an item past the list does nothing).
 template <int DT, bool VEC, bool TOK>
-__device__ __forceinline__ void pass2_part_w(const Params& P, int r, int c) {
-  using C = PartC<DT, VEC>;
-  constexpr int EB = StatTile<DT, VEC>::EB;
-  const int nt = P.nt, g1 = P.gamma + 1, V = P.V;
-  int part = c;
+__device__ __forceinline__ void pass2_item_w(const Params& P, int r, int c) {
+  int k = c / kSlices;
+  const int w = c % kSlices;
   if (TOK) {
-    if (c >= kParts * ld_i32(P.etacnt + r)) return;  // wave-uniform
-    part = kParts * ld_i32(P.etalist + (int64_t)r * nt + c / kParts) + c % kParts;
+    if (k >= ld_i32(P.etacnt + r)) return;  // wave-uniform
+    k = ld_i32(P.etalist + (int64_t)r * P.nt + k);
   }
-  const int64_t e0 = (int64_t)part * C::N;
-  ChunkRegs<C> wq, wp;
-  load_chunk<DT, VEC, C>((const char*)P.q + (int64_t)r * V * EB, e0, V, wq);
-  load_chunk<DT, VEC, C>((const char*)P.p + (int64_t)r * V * EB, e0, V, wp);
   const RowStat rs = ld_rowstat(P.rowstat + r);
-  const SeqParam sp = seq_param(P, r / g1);
-  const ProbScale ps = prob_scale(sp, rs, TOK);
-  double acc = 0.0;
-#pragma unroll
-  for (int i = 0; i < C::U; ++i) {
-    float t = 0.0f;
-#pragma unroll
-    for (int e = 0; e < C::VW; ++e) {
-      const float zq = elem<DT, VEC>(wq[i], e), zp = elem<DT, VEC>(wp[i], e);
-      if constexpr (TOK) {
-        t += token_r(ps.tok, zq, zp) ? prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo) : 0.0f;
-      } else {
-        // D_TV for the deferral decision only, where an absolute error of
-        // about 1e-7 is far inside the decision margin; the replacement draw
-        // of a rejected row sums its own cancellation-free residual
-        const float pq = prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo);
-        const float pp = prob(zp, ps.c_hi, ps.c_lo, ps.p_hi, ps.p_lo);
-        t += fmaxf(pp - pq, 0.0f);
-      }
-      if (e & 1) __builtin_amdgcn_sched_barrier(0);
-    }
-    acc += (double)t;
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  acc = wave_sum(acc);
-  if ((threadIdx.x & 63) == 0) st_dev_f64(P.tvpart + (int64_t)r * nt * kParts + part, acc);
+  const SeqParam sp = seq_param(P, r / (P.gamma + 1));
+  pass2_slice_w<DT, VEC, TOK>(P, r, k, w, prob_scale(sp, rs, TOK));
 }
 
 // Wave: half h of the argmax of greedy row r: the lowest index of the row
@@ -1834,7 +1978,7 @@ __device__ __forceinline__ void arg_half_w(const Params& P, int r, int h) {
   const char* row = (const char*)(h ? P.p : P.q) + (int64_t)r * V * EB;
   int idx = 0x7fffffff;
 #pragma unroll 1
-  for (int part = 0; part < kParts && idx == 0x7fffffff; ++part) {  // wave-uniform
+  for (int part = 0; part < 2 && idx == 0x7fffffff; ++part) {  // wave-uniform
     const int64_t e0 = (int64_t)k * StatTile<DT, VEC>::N + (int64_t)part * C::N;
     ChunkRegs<C> w;
     load_chunk<DT, VEC, C>(row, e0, V, w);
@@ -1856,48 +2000,68 @@ __device__ __forceinline__ void arg_half_w(const Params& P, int r, int h) {
   if ((threadIdx.x & 63) == 0) st_i32(P.argres + (int64_t)r * 4 + 2 + h, idx);
 }
 
-// Wave: part c of sequence b's residual job: the residual masses of the
-// sub-chunks of part c of row j* and, by the scan the draw repeats, the
-// part's mass.
-template <int DT, bool VEC>
-__device__ __forceinline__ void res_part_w(const Params& P, int b, int c) {
-  constexpr int NS = PartC<DT, VEC>::U;
-  const int g1 = P.gamma + 1, np = P.nt * kParts;
-  const int f = ld_i32(P.seqinfo + (int64_t)b * 2 + 0);
-  const int kind = ld_i32(P.seqinfo + (int64_t)b * 2 + 1);
-  const int64_t row = (int64_t)b * g1 + f;
+// Wave: item c = k * 4 + w of sequence b's residual job over row f (= j*),
+// sampling kind KIND: the residual masses of the sub-chunks of slice w of
+// tile k, stored at their place in the row's sub-chunk order, which the draw
+// searches directly.
+template <int DT, bool VEC, int KIND>
+__device__ __forceinline__ void res_slice_w(const Params& P, int b, int c, int f) {
+  constexpr int U = StatTile<DT, VEC>::U;
+  const int k = c / kSlices, w = c % kSlices;
+  const int64_t row = (int64_t)b * (P.gamma + 1) + f;
   const RowStat rs = ld_rowstat(P.rowstat + row);
   const SeqParam sp = seq_param(P, b);
-  const ProbScale ps = prob_scale(sp, rs, kind == kTokRes);
-  const int64_t e0 = (int64_t)c * PartC<DT, VEC>::N;
-  const double ml = kind == kTokRes ? part_masses_w<DT, VEC, kTokRes>(P, row, e0, ps)
-                                    : part_masses_w<DT, VEC, kResidual>(P, row, e0, ps);
+  const ProbScale ps = prob_scale(sp, rs, KIND == kTokRes);
+  const int64_t t0 = (int64_t)k * StatTile<DT, VEC>::N;
+  const double ml = slice_masses_w<DT, VEC, KIND>(P, row, t0, w, ps);
   const int lane = threadIdx.x & 63;
-  const double tot = lane_f64(wave_incl_scan(lane < NS ? ml : 0.0), NS - 1);
-  if (lane < NS) st_dev_f64(P.submass + ((int64_t)b * np + c) * kMaxSub + lane, ml);
-  if (lane == 0) st_dev_f64(P.masses + (int64_t)b * np + c, tot);
+  if (lane < U)
+    st_dev_f64(P.submass + (int64_t)b * P.nsub + (int64_t)k * (U * kSlices) + lane * kSlices + w,
+               ml);
 }
 
-// Wave: the row's decision once its TV, eta or argmax is known; when it
-// settles j*, the sequence's finish publishes to the next job pass.
-template <int DT>
-__device__ __forceinline__ void row_job_decide(const Params& P, int kind, int r, int phase) {
-  const int g1 = P.gamma + 1, np = P.nt * kParts;
-  const int b = r / g1, j = r - b * g1;
-  RowStat rs = ld_rowstat(P.rowstat + r);
-  if (kind == kJobArg) {
-    rs.amax_q = ld_i32(P.argres + (int64_t)r * 4 + 2);
-    rs.amax_p = ld_i32(P.argres + (int64_t)r * 4 + 3);
-  } else {
-    // the TV or eta partials of every part, in part order
-    double s = 0.0;
-    for (int k = threadIdx.x & 63; k < np; k += 64)
-      s += ld_dev_f64(P.tvpart + (int64_t)r * np + k);
-    rs.tv = wave_sum(s);
-  }
+// (a branch per kind, each with its own stores, so that the compiler does
+// not evaluate both)
+template <int DT, bool VEC>
+__device__ __forceinline__ void res_item_w(const Params& P, int b, int c, int f, int kind) {
+  if (kind == kTokRes) res_slice_w<DT, VEC, kTokRes>(P, b, c, f);
+  else res_slice_w<DT, VEC, kResidual>(P, b, c, f);
+}
+
+// ---------------------------------------------------------------- draw pass
+// k_res: grid (nt, B), after the statistics kernel.  For a sequence that
+// kernel finished with a residual draw, workgroup (k, b) sums the residual
+// masses of the sub-chunks of tile k of row j* (wavefront w its slice w);
+// the last of the sequence's workgroups to arrive draws.  A draw from the
+// statistics partials is made by workgroup (0, b).  The last arrival clears
+// the sequence's outcome word for the next call.  Sequences finished
+// elsewhere (later passes) have no outcome here and are skipped.
+template <int DT, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_res(Params P) {
+  const int k = blockIdx.x, b = blockIdx.y;
+  const uint32_t info = ld_u32(row_word(P, b, kSeqInfo));
+  if (!(info & kSeqInfoSet)) return;  // block-uniform
+  const int f = (int)(info & 0xffu), kind = (int)((info >> 8) & 0xffu);
+  const int64_t row = (int64_t)b * (P.gamma + 1) + f;
   const SeqParam sp = seq_param(P, b);
-  const int f = row_decide_w<DT>(P, r, b, j, sp, rs);
-  if (f >= 0) seq_finish_w<DT>(P, b, f, sp, phase + 1);
+  const bool residual = kind == kResidual || kind == kTokRes;
+  if (residual) {
+    const int w = threadIdx.x >> 6;
+    if (kind == kTokRes) res_slice_w<DT, VEC, kTokRes>(P, b, k * kSlices + w, f);
+    else res_slice_w<DT, VEC, kResidual>(P, b, k * kSlices + w, f);
+    vmem_drain();
+  }
+  __syncthreads();  // every wavefront's masses are stored
+  if (threadIdx.x >= 64) return;
+  if (!residual && k == 0) {
+    const int src = kind == kQ ? kSrcStatsQ : kind == kP ? kSrcStatsP : kSrcTokPi;
+    draw_w<DT, VEC>(P, b, row, kind, src, sp, ld_rowstat(P.rowstat + row));
+    vmem_drain();
+  }
+  if (arrive_last_w(row_word(P, b, kSeqResArrive), (uint32_t)P.nt)) {
+    if (residual) draw_w<DT, VEC>(P, b, row, kind, kSrcPass, sp, ld_rowstat(P.rowstat + row));
+    if ((threadIdx.x & 63) == 0) st_u32(row_word(P, b, kSeqInfo), 0u);
+  }
 }
 
 // Thread 0 of each workgroup, after reading the pass's job counts: arrive
@@ -1938,7 +2102,7 @@ __global__ __launch_bounds__(kJobThreads) void k_jobs(Params P) {
   __syncthreads();
   const int64_t n_row = min((int64_t)counts[0], P.job_slots);
   const int64_t n_single = min((int64_t)counts[1], P.single_slots);
-  const int np = nt * kParts;
+  const int np = nt * kSlices;
   const int64_t n_row_items = n_row * np;
   const int64_t n_items = n_row_items + n_single;
   const uint64_t* rows = job_list(P, phase, false);
@@ -1952,13 +2116,12 @@ __global__ __launch_bounds__(kJobThreads) void k_jobs(Params P) {
       const uint64_t e = ld_u64(rows + s);
       const int kind = job_kind(e);
       const int id = (int)job_id(e);
-      if (kind == kJobTv) pass2_part_w<DT, VEC, false>(P, id, c);
-      else if (kind == kJobEta) pass2_part_w<DT, VEC, true>(P, id, c);
-      else res_part_w<DT, VEC>(P, id, c);
+      if (kind == kJobTv) pass2_item_w<DT, VEC, false>(P, id, c);
+      else if (kind == kJobEta) pass2_item_w<DT, VEC, true>(P, id, c);
+      else res_item_w<DT, VEC>(P, id, c, (int)(job_extra(e) & 0xff), (int)(job_extra(e) >> 8));
       if (arrive_last_w(job_done(P, phase, s), (uint32_t)np)) {
         if (kind == kJobRes) {
-          const int f = ld_i32(P.seqinfo + (int64_t)id * 2 + 0);
-          const int skind = ld_i32(P.seqinfo + (int64_t)id * 2 + 1);
+          const int f = (int)(job_extra(e) & 0xff), skind = (int)(job_extra(e) >> 8);
           const int64_t row = (int64_t)id * g1 + f;
           draw_w<DT, VEC>(P, id, row, skind, kSrcPass, seq_param(P, id),
                           ld_rowstat(P.rowstat + row));
@@ -1970,7 +2133,16 @@ __global__ __launch_bounds__(kJobThreads) void k_jobs(Params P) {
       const uint64_t e = ld_u64(singles + (g - n_row_items));
       const int kind = job_kind(e);
       const int id = (int)job_id(e);
-      if (kind == kJobArg) {
+      if (kind == kJobTvTile) {
+        // a tile whose stealing workgroup gave up waiting: its four slices
+        const RowStat rs = ld_rowstat(P.rowstat + id);
+        const ProbScale ps = prob_scale(seq_param(P, id / g1), rs, false);
+#pragma unroll 1
+        for (int w = 0; w < kSlices; ++w)
+          pass2_slice_w<DT, VEC, false>(P, id, (int)job_extra(e), w, ps);
+        if (arrive_last_w(row_word(P, id, kRowTvArrive), (uint32_t)(kSlices * nt), kSlices))
+          tv_row_done<DT>(P, id, phase);
+      } else if (kind == kJobArg) {
         arg_half_w<DT, VEC>(P, id, (int)job_extra(e));
         if (arrive_last_w(row_word(P, id, kRowJobDone), 2u)) row_job_decide<DT>(P, kind, id, phase);
       } else {  // a draw from the statistics partials
@@ -1984,8 +2156,9 @@ __global__ __launch_bounds__(kJobThreads) void k_jobs(Params P) {
 }
 
 template <int DT, bool VEC>
-hipError_t launch_step_t(const Params& P, hipStream_t st, bool nt_loads, int job_passes,
-                         int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end) {
+hipError_t launch_step_t(const Params& P, hipStream_t st, bool nt_loads, bool draw_pass,
+                         int job_passes, int job_groups, hipEvent_t ev_begin,
+                         hipEvent_t ev_end) {
   const dim3 grid((unsigned)P.nt, (unsigned)(P.B * (P.gamma + 1))), block(kThreads);
   if (ev_begin) {
     const hipError_t e = hipEventRecord(ev_begin, st);
@@ -2008,6 +2181,10 @@ hipError_t launch_step_t(const Params& P, hipStream_t st, bool nt_loads, int job
   }
   hipError_t err = hipGetLastError();
   if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, st);
+  if (err == hipSuccess && draw_pass) {
+    hipLaunchKernelGGL((k_res<DT, VEC>), dim3((unsigned)P.nt, (unsigned)P.B), block, 0, st, P);
+    err = hipGetLastError();
+  }
   for (int phase = 1; phase <= job_passes && err == hipSuccess; ++phase) {
     Params Q = P;
     Q.phase = phase;
@@ -2175,6 +2352,11 @@ int stat_tile_elems(int dtype, bool vec) {
   return vec ? StatTile<0, true>::N : StatTile<0, false>::N;
 }
 
+int tile_subchunks(int dtype, bool vec) {
+  if (dtype == 1) return kSlices * (vec ? StatTile<1, true>::U : StatTile<1, false>::U);
+  return kSlices * (vec ? StatTile<0, true>::U : StatTile<0, false>::U);
+}
+
 int draft_tile_elems(int dtype, bool vec, bool long_tiles) {
   if (long_tiles) {
     if (dtype == 1) return vec ? DraftTile<1, true, 2>::N : DraftTile<1, false, 2>::N;
@@ -2215,15 +2397,18 @@ hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, int job_passes,
-                       int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end,
+hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, bool draw_pass,
+                       int job_passes, int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end,
                        hipStream_t st) {
   if (dtype == 1)
-    return vec ? launch_step_t<1, true>(P, st, nt_loads, job_passes, job_groups, ev_begin, ev_end)
-               : launch_step_t<1, false>(P, st, nt_loads, job_passes, job_groups, ev_begin,
-                                         ev_end);
-  return vec ? launch_step_t<0, true>(P, st, nt_loads, job_passes, job_groups, ev_begin, ev_end)
-             : launch_step_t<0, false>(P, st, nt_loads, job_passes, job_groups, ev_begin, ev_end);
+    return vec ? launch_step_t<1, true>(P, st, nt_loads, draw_pass, job_passes, job_groups,
+                                        ev_begin, ev_end)
+               : launch_step_t<1, false>(P, st, nt_loads, draw_pass, job_passes, job_groups,
+                                         ev_begin, ev_end);
+  return vec ? launch_step_t<0, true>(P, st, nt_loads, draw_pass, job_passes, job_groups,
+                                      ev_begin, ev_end)
+             : launch_step_t<0, false>(P, st, nt_loads, draw_pass, job_passes, job_groups,
+                                       ev_begin, ev_end);
 }
 
 }  // namespace spc
