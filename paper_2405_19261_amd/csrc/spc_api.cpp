@@ -94,8 +94,10 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
   L.jobline = o; o = align_up(o + 4 * (size_t)kLineWords * 2 * (R + B), 256);
   L.tiles = o; o = align_up(o + sizeof(TilePart) * R * nt, 256);
   L.tvpart = o; o = align_up(o + sizeof(double) * R * nt * kSlices, 256);
+  // residual sub-chunk masses per sequence, or (small path) two sets per row
   L.submass = o;
-  o = align_up(o + sizeof(double) * B * nt * tile_subchunks(dtype, vec), 256);
+  o = align_up(o + sizeof(double) * std::max<int64_t>(B * nt * tile_subchunks(dtype, vec),
+                                                       R * 2 * kSmallSub), 256);
   L.moms = o; o = align_up(o + sizeof(TileMom) * R * nt, 256);
   L.rowstat = o; o = align_up(o + sizeof(RowStat) * R, 256);
   L.rowdec = o; o = align_up(o + sizeof(int32_t) * R, 256);
@@ -313,6 +315,10 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
   // sequences decided in pass 1 (greedy ones write their token directly).
   const bool draw_pass = may_sample;
   const int job_passes = pass2_rows ? 2 : (may_greedy ? 1 : 0);
+  // Small problems (rows that fit one workgroup's registers, at most two
+  // rows per compute unit, no first moments) take the single-launch path.
+  const bool small = !need_mom && V <= spc::small_row_elems(dtype, vec) &&
+                     b_launch * g1 <= 2 * (int64_t)cus;
   // rows a TV job reads again are loaded through the caches
   const bool nt_loads = !(may_sample && (rules & kTv));
   const int64_t nt = stat_tiles(dtype, vec, V);
@@ -375,9 +381,16 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
     P.argres = reinterpret_cast<int32_t*>(ws + L.argres);
     P.etacnt = reinterpret_cast<int32_t*>(ws + L.etacnt);
     const bool first = b0 == 0;
-    e = spc::launch_step(P, dtype, vec, nt_loads, draw_pass, job_passes, job_groups,
-                         first && ex ? ex->ev_tiles_begin : nullptr,
-                         first && ex ? ex->ev_tiles_end : nullptr, stream);
+    hipEvent_t ev0 = first && ex ? ex->ev_tiles_begin : nullptr;
+    hipEvent_t ev1 = first && ex ? ex->ev_tiles_end : nullptr;
+    if (small) {
+      // one launch: a workgroup per row holding the row in registers
+      P.nsub = spc::kSmallSub;
+      e = spc::launch_small(P, dtype, vec, ev0, ev1, stream);
+    } else {
+      e = spc::launch_step(P, dtype, vec, nt_loads, draw_pass, job_passes, job_groups, ev0, ev1,
+                           stream);
+    }
     if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
   }
   return SPC_OK;

@@ -145,6 +145,13 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec);
 hipError_t launch_draft(const Params& P, int dtype, bool vec, bool argmax, bool long_tiles,
                         hipStream_t stream);
 
+// The small-problem path (k_small): a workgroup per row holding the row in
+// registers; rows of at most small_row_elems entries, kSmallSub sub-chunks.
+constexpr int kSmallSub = 64;
+int small_row_elems(int dtype, bool vec);
+hipError_t launch_small(const Params& P, int dtype, bool vec, hipEvent_t ev_begin,
+                        hipEvent_t ev_end, hipStream_t stream);
+
 // Enqueue one verify launch: the statistics tiles (k_tiles), the draw pass
 // (k_res) when `draw_pass`, then `job_passes` job passes (k_jobs) of
 // `job_groups` workgroups each.

@@ -668,6 +668,11 @@ __device__ __forceinline__ float weight_of(float zq, float zp, const ProbScale& 
   }
 }
 
+template <int DT, int KIND>
+__device__ __forceinline__ float weight_k(float zq, float zp, const ProbScale& s, int) {
+  return weight_of<DT, KIND>(zq, zp, s);
+}
+
 template <int DT>
 __device__ __forceinline__ float load_logit(const void* base, int64_t row, int V, int x) {
   const int64_t i = row * (int64_t)V + x;
@@ -1006,7 +1011,7 @@ __device__ __forceinline__ double find_part(const Params& P, int64_t row, int b,
 // Rounding that leaves rem unreached takes the last entry with mass.
 template <int DT, bool VEC, class C, int KIND>
 __device__ __forceinline__ void pick_wave(const Params& P, int b, int64_t row, int64_t c0,
-                                          double rem, const ProbScale& ps) {
+                                          double rem, const ProbScale& ps, int kind = -1) {
   constexpr int EB = StatTile<DT, VEC>::EB;
   const int lane = threadIdx.x & 63;
   const int V = P.V;
@@ -1025,7 +1030,7 @@ __device__ __forceinline__ void pick_wave(const Params& P, int b, int64_t row, i
     double m = 0.0;
 #pragma unroll
     for (int e = 0; e < C::VW; ++e) {
-      const float w = weight_of<DT, KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
+      const float w = weight_k<DT, KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps, kind);
       m += (double)w;
       if (w > 0.0f) last_pos = max(last_pos, (int)(base + e));
       if (e & 1) __builtin_amdgcn_sched_barrier(0);
@@ -1056,7 +1061,7 @@ __device__ __forceinline__ void pick_wave(const Params& P, int b, int64_t row, i
   int hit = -1, lastw = -1;
 #pragma unroll
   for (int e = 0; e < C::VW; ++e) {
-    const float w = weight_of<DT, KIND>(elem<DT, VEC>(sq, e), elem<DT, VEC>(sp_, e), ps);
+    const float w = weight_k<DT, KIND>(elem<DT, VEC>(sq, e), elem<DT, VEC>(sp_, e), ps, kind);
     run += (double)w;
     if (w > 0.0f) lastw = (int)(hbase + e);
     if (hit < 0 && run > rem && w > 0.0f) hit = (int)(hbase + e);
@@ -1392,26 +1397,21 @@ __device__ __forceinline__ bool arrive_last_w(uint32_t* cnt, uint32_t n, uint32_
   return last;
 }
 
-// Wave: the masses of the sub-chunks of slice w of the tile at entry t0 of
-// a row under the distribution KIND; lane i < U returns sub-chunk i * 4 + w's
-// (float sums per lane load, fp64 across lanes), other lanes 0.
+// Wave: the slice's sub-chunk masses from its loaded entries (lane i < U
+// returns sub-chunk i * 4 + w's).
 template <int DT, bool VEC, int KIND>
-__device__ __forceinline__ double slice_masses_w(const Params& P, int64_t row, int64_t t0, int w,
-                                                 const ProbScale& ps) {
+__device__ __forceinline__ double slice_masses_of(const uint32_t (&cq)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
+                                                  const uint32_t (&cp)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
+                                                  const ProbScale& ps, int kind) {
   using T = StatTile<DT, VEC>;
-  const int lane = threadIdx.x & 63, V = P.V;
-  uint32_t cq[T::U][T::NW] = {}, cp[T::U][T::NW] = {};
-  if (KIND != kP)
-    load_tile<DT, VEC, T::U, true>((const char*)P.q + row * V * T::EB, t0, V, cq, w * 64 + lane);
-  if (KIND != kQ)
-    load_tile<DT, VEC, T::U, true>((const char*)P.p + row * V * T::EB, t0, V, cp, w * 64 + lane);
+  const int lane = threadIdx.x & 63;
   double mine = 0.0;
 #pragma unroll
   for (int i = 0; i < T::U; ++i) {
     float t = 0.0f;
 #pragma unroll
     for (int e = 0; e < T::VW; ++e) {
-      t += weight_of<DT, KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
+      t += weight_k<DT, KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps, kind);
       if (e & 1) __builtin_amdgcn_sched_barrier(0);
     }
     const double s = wave_sum((double)t);
@@ -1421,15 +1421,36 @@ __device__ __forceinline__ double slice_masses_w(const Params& P, int64_t row, i
   return mine;
 }
 
+// Wave: the masses of the sub-chunks of slice w of the tile at entry t0 of
+// a row under the distribution KIND; lane i < U returns sub-chunk i * 4 + w's
+// (float sums per lane load, fp64 across lanes), other lanes 0.
+template <int DT, bool VEC, int KIND>
+__device__ __forceinline__ double slice_masses_w(const Params& P, int64_t row, int64_t t0, int w,
+                                                 const ProbScale& ps, int kind = -1) {
+  using T = StatTile<DT, VEC>;
+  const int lane = threadIdx.x & 63, V = P.V;
+  uint32_t cq[T::U][T::NW] = {}, cp[T::U][T::NW] = {};
+  if (KIND != kP)
+    load_tile<DT, VEC, T::U, true>((const char*)P.q + row * V * T::EB, t0, V, cq, w * 64 + lane);
+  if (KIND != kQ)
+    load_tile<DT, VEC, T::U, true>((const char*)P.p + row * V * T::EB, t0, V, cp, w * 64 + lane);
+  return slice_masses_of<DT, VEC, KIND>(cq, cp, ps, kind);
+}
+
+
 // Wave: the second-pass partial of slice w of tile k of row r -- the TV
 // weight max(0, p - q), or eta's share (the q mass of the entries the rule
 // marks) -- into tvpart[r][k * 4 + w].
 template <int DT, bool VEC, bool TOK, bool NT = true>
 __device__ __forceinline__ void pass2_slice_w(const Params& P, int r, int k, int w,
-                                              const ProbScale& ps) {
+                                              const SeqParam& sp) {
   using T = StatTile<DT, VEC>;
   const int lane = threadIdx.x & 63, V = P.V;
   const int64_t t0 = (int64_t)k * T::N;
+  // the row's statistics first: a wait for a later load is a wait for every
+  // load before it, so the slice's entries are requested after them
+  const ProbScale ps = prob_scale(sp, ld_rowstat(P.rowstat + r), TOK);
+  __builtin_amdgcn_sched_barrier(0);
   uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
   load_tile<DT, VEC, T::U, NT>((const char*)P.q + (int64_t)r * V * T::EB, t0, V, wq, w * 64 + lane);
   load_tile<DT, VEC, T::U, NT>((const char*)P.p + (int64_t)r * V * T::EB, t0, V, wp, w * 64 + lane);
@@ -1560,6 +1581,32 @@ __device__ __forceinline__ void seq_finish_w(const Params& P, int b, int f, cons
   }
 }
 
+// Lane 0: write the outputs and the record of decided row r (d from
+// decide_row; an invalid sequence's rows record "reject, no deferral"),
+// with `extra` in the record's bits 4 and up.
+__device__ __forceinline__ void row_record(const Params& P, int r, const SeqParam& sp,
+                                           const RowDecision& d, int extra) {
+  P.out_defer[r] = sp.valid ? (uint8_t)d.delta : (uint8_t)0;
+  if (sp.valid && P.out_stats) {
+    const double T = sp.greedy ? 1.0 : kLog2e / sp.c;
+    float* o = P.out_stats + (int64_t)r * 8;
+    o[0] = (float)((double)d.rs.zmax_q / T);
+    o[1] = (float)(d.rs.lz_q * kLn2);
+    o[2] = d.maxq;
+    o[3] = (float)((double)d.rs.zmax_p / T);
+    o[4] = (float)(d.rs.lz_p * kLn2);
+    o[5] = d.maxp;
+    o[6] = d.tv;
+    o[7] = (float)d.rs.slog;
+  }
+  if (sp.valid && P.out_argmax) {
+    P.out_argmax[(int64_t)r * 2 + 0] = d.rs.amax_q;
+    P.out_argmax[(int64_t)r * 2 + 1] = d.rs.amax_p;
+  }
+  if (sp.valid) st_rowstat(P.rowstat + r, d.rs);
+  st_i32(P.rowdec + r, (sp.valid ? d.keep | (d.delta << 1) : 0) | (extra << 4));
+}
+
 // Wave: decide row r = (b, j) from its statistics rs (delta_j by the rule,
 // a_j by the acceptance test), write its outputs and add it to the
 // sequence's decided-row mask.  Returns j* when this decision completes the
@@ -1571,7 +1618,6 @@ __device__ __forceinline__ int row_decide_w(const Params& P, int r, int b, int j
   const int gamma = P.gamma, g1 = gamma + 1, V = P.V;
   const int lane = threadIdx.x & 63;
   RowDecision d{};
-  int keep = 0;
   if (sp.valid) {
     int x = -1;
     float zqx = 0.0f, zpx = 0.0f, u = 0.0f;
@@ -1589,29 +1635,10 @@ __device__ __forceinline__ int row_decide_w(const Params& P, int r, int b, int j
       zpx = load_logit<DT>(P.p, r, V, rs.amax_q);
     }
     d = decide_row(sp, rs, j, gamma, V, x, zqx, zpx, u);
-    keep = d.keep;
   }
   uint64_t old = 0;
   if (lane == 0) {
-    P.out_defer[r] = sp.valid ? (uint8_t)d.delta : (uint8_t)0;
-    if (sp.valid && P.out_stats) {
-      const double T = sp.greedy ? 1.0 : kLog2e / sp.c;
-      float* o = P.out_stats + (int64_t)r * 8;
-      o[0] = (float)((double)d.rs.zmax_q / T);
-      o[1] = (float)(d.rs.lz_q * kLn2);
-      o[2] = d.maxq;
-      o[3] = (float)((double)d.rs.zmax_p / T);
-      o[4] = (float)(d.rs.lz_p * kLn2);
-      o[5] = d.maxp;
-      o[6] = d.tv;
-      o[7] = (float)d.rs.slog;
-    }
-    if (sp.valid && P.out_argmax) {
-      P.out_argmax[(int64_t)r * 2 + 0] = d.rs.amax_q;
-      P.out_argmax[(int64_t)r * 2 + 1] = d.rs.amax_p;
-    }
-    if (sp.valid) st_rowstat(P.rowstat + r, d.rs);
-    st_i32(P.rowdec + r, keep | (d.delta << 1));
+    row_record(P, r, sp, d, 0);
     vmem_drain();  // the row's record is stored before its bit is set
     old = or_u64(seq_mask(P, b), 1ull << j);
   }
@@ -1770,8 +1797,7 @@ __device__ __forceinline__ void tv_steal(const Params& P, int rv, int k, const S
     if (threadIdx.x == 0) publish_single(P, 1, kJobTvTile, (uint32_t)k, (uint32_t)rv);
     return;
   }
-  const RowStat rs = ld_rowstat(P.rowstat + rv);
-  pass2_slice_w<DT, VEC, false>(P, rv, k, threadIdx.x >> 6, prob_scale(spv, rs, false));
+  pass2_slice_w<DT, VEC, false>(P, rv, k, threadIdx.x >> 6, spv);
   vmem_drain();
   __syncthreads();  // all four slices are stored
   if (threadIdx.x < 64 &&
@@ -1836,7 +1862,7 @@ __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
 // sums per lane load, fp64 across lanes), other lanes 0.
 template <int DT, bool VEC, int KIND>
 __device__ __forceinline__ double part_masses_w(const Params& P, int64_t row, int64_t e0,
-                                                const ProbScale& ps, int base = 0) {
+                                                const ProbScale& ps, int base = 0, int kind = -1) {
   using C = PartC<DT, VEC>;
   constexpr int EB = StatTile<DT, VEC>::EB;
   const int lane = threadIdx.x & 63, V = P.V;
@@ -1849,7 +1875,7 @@ __device__ __forceinline__ double part_masses_w(const Params& P, int64_t row, in
     float t = 0.0f;
 #pragma unroll
     for (int e = 0; e < C::VW; ++e) {
-      t += weight_of<DT, KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps);
+      t += weight_k<DT, KIND>(elem<DT, VEC>(cq[i], e), elem<DT, VEC>(cp[i], e), ps, kind);
       if (e & 1) __builtin_amdgcn_sched_barrier(0);
     }
     const double s = wave_sum((double)t);
@@ -1866,7 +1892,7 @@ __device__ __forceinline__ double part_masses_w(const Params& P, int64_t row, in
 template <int DT, bool VEC, int KIND>
 __device__ __forceinline__ void draw_in_subs_w(const Params& P, int b, int64_t row, int64_t e0,
                                                double ml, int nsub, double rem,
-                                               const ProbScale& ps) {
+                                               const ProbScale& ps, int kind = -1) {
   const int lane = threadIdx.x & 63;
   ml = lane < nsub ? ml : 0.0;
   const double incl = wave_incl_scan(ml);
@@ -1881,7 +1907,8 @@ __device__ __forceinline__ void draw_in_subs_w(const Params& P, int b, int64_t r
     c = pos ? 63 - __clzll(pos) : 0;
     r = __builtin_huge_val();
   }
-  pick_wave<DT, VEC, SubC<DT, VEC>, KIND>(P, b, row, e0 + (int64_t)c * SubC<DT, VEC>::N, r, ps);
+  pick_wave<DT, VEC, SubC<DT, VEC>, KIND>(P, b, row, e0 + (int64_t)c * SubC<DT, VEC>::N, r, ps,
+                                          kind);
 }
 
 // Wave: the inverse-CDF draw of sequence b at row `row` (the row of j*) from
@@ -1896,27 +1923,15 @@ __device__ __forceinline__ void draw_kind_w(const Params& P, int b, int64_t row,
     // the residual job's sub-chunk masses were searched: ks is a sub-chunk
     pick_wave<DT, VEC, SubC<DT, VEC>, KIND>(P, b, row, (int64_t)ks * SubC<DT, VEC>::N, rem, ps);
   } else {
-    // a statistics tile: the masses of its sub-chunks, in tile order
+    // a statistics tile: the masses of its sub-chunks (its two
+    // wave-contiguous halves, in order), then the sub-chunk's entry
     const int64_t t0 = (int64_t)ks * StatTile<DT, VEC>::N;
+    constexpr int NS = PartC<DT, VEC>::U;
     double m = 0.0;
-    if constexpr (KIND == kTokPi) {
-      // both tensors: one slice (sub-chunks i * 4 + w) at a time
-      const int lane = threadIdx.x & 63;
 #pragma unroll 1
-      for (int w = 0; w < kSlices; ++w) {
-        const double mw = slice_masses_w<DT, VEC, KIND>(P, row, t0, w, ps);
-        const int i = lane / kSlices;  // lane i * 4 + w takes sub-chunk i of slice w
-        const double v = __shfl(mw, i);
-        if (lane % kSlices == w && i < StatTile<DT, VEC>::U) m = v;
-      }
-    } else {
-      // one tensor: the tile's two wave-contiguous halves
-      constexpr int NS = PartC<DT, VEC>::U;
-#pragma unroll 1
-      for (int half = 0; half < 2; ++half)
-        m += part_masses_w<DT, VEC, KIND>(P, row, t0 + half * PartC<DT, VEC>::N, ps, half * NS);
-    }
-    draw_in_subs_w<DT, VEC, KIND>(P, b, row, t0, m, StatTile<DT, VEC>::U * kSlices, rem, ps);
+    for (int half = 0; half < 2; ++half)
+      m += part_masses_w<DT, VEC, KIND>(P, row, t0 + half * PartC<DT, VEC>::N, ps, half * NS);
+    draw_in_subs_w<DT, VEC, KIND>(P, b, row, t0, m, 2 * NS, rem, ps);
   }
 }
 
@@ -1959,9 +1974,7 @@ __device__ __forceinline__ void pass2_item_w(const Params& P, int r, int c) {
     if (k >= ld_i32(P.etacnt + r)) return;  // wave-uniform
     k = ld_i32(P.etalist + (int64_t)r * P.nt + k);
   }
-  const RowStat rs = ld_rowstat(P.rowstat + r);
-  const SeqParam sp = seq_param(P, r / (P.gamma + 1));
-  pass2_slice_w<DT, VEC, TOK>(P, r, k, w, prob_scale(sp, rs, TOK));
+  pass2_slice_w<DT, VEC, TOK>(P, r, k, w, seq_param(P, r / (P.gamma + 1)));
 }
 
 // Wave: half h of the argmax of greedy row r: the lowest index of the row
@@ -2007,14 +2020,21 @@ __device__ __forceinline__ void arg_half_w(const Params& P, int r, int h) {
 template <int DT, bool VEC, int KIND>
 __device__ __forceinline__ void res_slice_w(const Params& P, int b, int c, int f) {
   constexpr int U = StatTile<DT, VEC>::U;
+  using T = StatTile<DT, VEC>;
   const int k = c / kSlices, w = c % kSlices;
+  const int lane = threadIdx.x & 63, V = P.V;
   const int64_t row = (int64_t)b * (P.gamma + 1) + f;
+  const int64_t t0 = (int64_t)k * T::N;
+  // the row's statistics first: a wait for a later load is a wait for every
+  // load before it, so the slice's entries are requested after them
   const RowStat rs = ld_rowstat(P.rowstat + row);
   const SeqParam sp = seq_param(P, b);
   const ProbScale ps = prob_scale(sp, rs, KIND == kTokRes);
-  const int64_t t0 = (int64_t)k * StatTile<DT, VEC>::N;
-  const double ml = slice_masses_w<DT, VEC, KIND>(P, row, t0, w, ps);
-  const int lane = threadIdx.x & 63;
+  __builtin_amdgcn_sched_barrier(0);
+  uint32_t cq[T::U][T::NW], cp[T::U][T::NW];
+  load_tile<DT, VEC, T::U, true>((const char*)P.q + row * V * T::EB, t0, V, cq, w * 64 + lane);
+  load_tile<DT, VEC, T::U, true>((const char*)P.p + row * V * T::EB, t0, V, cp, w * 64 + lane);
+  const double ml = slice_masses_of<DT, VEC, KIND>(cq, cp, ps, -1);
   if (lane < U)
     st_dev_f64(P.submass + (int64_t)b * P.nsub + (int64_t)k * (U * kSlices) + lane * kSlices + w,
                ml);
@@ -2135,11 +2155,10 @@ __global__ __launch_bounds__(kJobThreads) void k_jobs(Params P) {
       const int id = (int)job_id(e);
       if (kind == kJobTvTile) {
         // a tile whose stealing workgroup gave up waiting: its four slices
-        const RowStat rs = ld_rowstat(P.rowstat + id);
-        const ProbScale ps = prob_scale(seq_param(P, id / g1), rs, false);
+        const SeqParam spt = seq_param(P, id / g1);
 #pragma unroll 1
         for (int w = 0; w < kSlices; ++w)
-          pass2_slice_w<DT, VEC, false>(P, id, (int)job_extra(e), w, ps);
+          pass2_slice_w<DT, VEC, false>(P, id, (int)job_extra(e), w, spt);
         if (arrive_last_w(row_word(P, id, kRowTvArrive), (uint32_t)(kSlices * nt), kSlices))
           tv_row_done<DT>(P, id, phase);
       } else if (kind == kJobArg) {
@@ -2192,6 +2211,484 @@ hipError_t launch_step_t(const Params& P, hipStream_t st, bool nt_loads, bool dr
                        Q);
     err = hipGetLastError();
   }
+  return err;
+}
+
+// ================================================================ small problems
+// k_small: one launch for a batch whose rows fit in one workgroup's registers
+// (V up to kSmallThreads * kSmallU lane loads of VW entries).  grid (R),
+// 1024 threads: workgroup r holds row r of q and p (thread t's lane load i
+// covers entries (i * 1024 + t) * VW ..), reduces it to the row statistics,
+// takes the second pass (TV or eta) from the same registers, decides the row,
+// and computes, also from registers, the sub-chunk masses of the
+// distribution it would be sampled from if it were the sequence's j*.  The
+// last row of a sequence to arrive finds j* and draws: a search over row j*'s
+// stored masses, then one sub-chunk read again.  No tile is read twice.
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallWaves = kSmallThreads / 64;
+constexpr int kSmallU = 4;
+static_assert(kSmallU * kSmallWaves == kSmallSub, "sub-chunks per row of the small path");
+
+template <int DT, bool VEC>
+struct SmallRow {
+  using T = Tile<DT, VEC, kSmallU>;  // element geometry (EB, VW, NW)
+  static constexpr int N = kSmallThreads * kSmallU * T::VW;  // entries a workgroup holds
+};
+
+// The packed words stay live across the passes over a row; each pass unpacks
+// them again (otherwise the compiler keeps every unpacked entry of the
+// previous pass, twice the registers).
+template <int NW>
+__device__ __forceinline__ void small_fence(uint32_t (&wq)[kSmallU][NW], uint32_t (&wp)[kSmallU][NW]) {
+#pragma unroll
+  for (int i = 0; i < kSmallU; ++i)
+#pragma unroll
+    for (int k = 0; k < NW; ++k) asm volatile("" : "+v"(wq[i][k]), "+v"(wp[i][k]));
+}
+
+struct SmallShared {
+  float m[kSmallWaves][2];
+  double d[kSmallWaves][2];
+  double h[kSmallWaves][3];
+  int i[kSmallWaves][2];
+  double a[kSmallWaves];
+  RowStat rs;
+  float zx[2];  // q and p logits at the draft token (or p at the drafter's argmax)
+  int delta, kind;
+};
+
+// Whole block: sum of one double per thread, combined in wave order.
+__device__ __forceinline__ double small_sum(double v, SmallShared& sh) {
+  v = wave_sum(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh.a[threadIdx.x >> 6] = v;
+  __syncthreads();
+  double t = sh.a[0];
+#pragma unroll
+  for (int w = 1; w < kSmallWaves; ++w) t += sh.a[w];
+  return t;
+}
+
+// Whole block: the row statistics from the registers, as the statistics
+// tiles and the row merge compute them: per thread against its own maximum,
+// per wavefront against the wavefront's, then (fp64) against the row's; with
+// ARG the lowest index of each row maximum, with MOM the first moments.
+template <int DT, bool VEC>
+using SmallRegs = uint32_t[kSmallU][Tile<DT, VEC, kSmallU>::NW];
+
+// Thread t's lane load i of a row (entries (i * 1024 + t) * VW ..), raw: a
+// lane load past the row reads the row's first entries instead, and every
+// pass reads it as -inf through small_elem (a lane load is wholly inside or
+// wholly outside the row).  Keeping the raw words, rather than selecting
+// the padding once, spares the registers of a second copy.
+template <int DT, bool VEC>
+__device__ __forceinline__ void small_load(const char* row, int V, SmallRegs<DT, VEC>& w) {
+  using T = Tile<DT, VEC, kSmallU>;
+#pragma unroll
+  for (int i = 0; i < kSmallU; ++i) {
+    const int e = (i * kSmallThreads + (int)threadIdx.x) * T::VW;
+    const char* a = row + (uint32_t)((e < V ? e : 0) * T::EB);
+    if constexpr (VEC) {
+      const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a));
+      w[i][0] = v.x;
+      w[i][1] = v.y;
+      w[i][2] = v.z;
+      w[i][3] = v.w;
+    } else if constexpr (DT == 1) {
+      w[i][0] = *reinterpret_cast<const uint16_t*>(a);
+    } else {
+      w[i][0] = *reinterpret_cast<const uint32_t*>(a);
+    }
+  }
+}
+
+template <int DT, bool VEC>
+__device__ __forceinline__ bool small_ok(int i, int V) {
+  return (i * kSmallThreads + (int)threadIdx.x) * Tile<DT, VEC, kSmallU>::VW < V;
+}
+
+// Whether any lane of this wavefront holds entries of lane load i
+// (wavefront-uniform): lane loads wholly past the row are skipped.
+template <int DT, bool VEC>
+__device__ __forceinline__ bool small_live(int i, int V) {
+  return (i * kSmallThreads + (int)(threadIdx.x & ~63)) * Tile<DT, VEC, kSmallU>::VW < V;
+}
+
+template <int DT, bool VEC>
+__device__ __forceinline__ float small_elem(const uint32_t* w, int e, bool ok) {
+  return ok ? elem<DT, VEC>(w, e) : kNegInf;
+}
+
+template <int DT, bool VEC, int MOM, bool ARG>
+__device__ __forceinline__ RowStat small_stats(SmallRegs<DT, VEC>& wq, SmallRegs<DT, VEC>& wp,
+                                               int V, const SeqParam& sp, int mrule,
+                                               SmallShared& sh) {
+  using T = Tile<DT, VEC, kSmallU>;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  float mq = kNegInf, mp = kNegInf;
+#pragma unroll
+  for (int i = 0; i < kSmallU; ++i) {
+    if (!small_live<DT, VEC>(i, V)) continue;  // wavefront-uniform
+    const bool ok = small_ok<DT, VEC>(i, V);
+#pragma unroll
+    for (int e = 0; e < T::VW; ++e) {
+      mq = fmaxf(mq, small_elem<DT, VEC>(wq[i], e, ok));
+      mp = fmaxf(mp, small_elem<DT, VEC>(wp[i], e, ok));
+    }
+  }
+  small_fence(wq, wp);
+  int iq = 0x7fffffff, ip = 0x7fffffff;
+  if constexpr (ARG) {
+    // the first entry equal to the thread maximum, entries in index order
+#pragma unroll
+    for (int i = kSmallU - 1; i >= 0; --i) {
+      if (!small_live<DT, VEC>(i, V)) continue;  // wavefront-uniform
+      const bool ok = small_ok<DT, VEC>(i, V);
+#pragma unroll
+      for (int e = T::VW - 1; e >= 0; --e) {
+        const int idx = (i * kSmallThreads + (int)threadIdx.x) * T::VW + e;
+        if (small_elem<DT, VEC>(wq[i], e, ok) == mq) iq = idx;
+        if (small_elem<DT, VEC>(wp[i], e, ok) == mp) ip = idx;
+      }
+    }
+    if (mq == kNegInf) iq = 0x7fffffff;
+    if (mp == kNegInf) ip = 0x7fffffff;
+    small_fence(wq, wp);
+  }
+  const float rq = (mq == kNegInf) ? 0.0f : mq * sp.c_hi;
+  const float rp = (mp == kNegInf) ? 0.0f : mp * sp.c_hi;
+  float sq = 0.0f, spp = 0.0f, hq = 0.0f, hp = 0.0f, xq = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kSmallU; ++i) {
+    if (!small_live<DT, VEC>(i, V)) continue;  // wavefront-uniform
+    const bool ok = small_ok<DT, VEC>(i, V);
+#pragma unroll
+    for (int e = 0; e < T::VW; ++e) {
+      const float zq = small_elem<DT, VEC>(wq[i], e, ok), zp = small_elem<DT, VEC>(wp[i], e, ok);
+      const float aq = fmaf(zq, sp.c_lo, fmaf(zq, sp.c_hi, -rq));
+      const float ap = fmaf(zp, sp.c_lo, fmaf(zp, sp.c_hi, -rp));
+      const float tq = exp2_hw(aq), tp = exp2_hw(ap);
+      sq += tq;
+      spp += tp;
+      if constexpr (MOM) {
+        hq = fmaf(tq, tq > 0.0f ? aq : 0.0f, hq);
+        xq = fmaf(tq, tq > 0.0f ? ap : 0.0f, xq);
+        hp = fmaf(tp, tp > 0.0f ? ap : 0.0f, hp);
+      }
+      if (e & 1) __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  small_fence(wq, wp);
+  // waves against the wave max, then the block against the row max (fp64)
+  const float Wq = wave_max(mq), Wp = wave_max(mp);
+  const double eq = (double)rq - (double)(Wq * sp.c_hi), ep = (double)rp - (double)(Wp * sp.c_hi);
+  const double fq = exp2_acc(eq), fp = exp2_acc(ep);
+  const double dq = wave_sum(mq == kNegInf ? 0.0 : (double)sq * fq);
+  const double dp = wave_sum(mp == kNegInf ? 0.0 : (double)spp * fp);
+  double mhq = 0.0, mhp = 0.0, mx = 0.0;
+  if constexpr (MOM) {
+    mhq = wave_sum(mq == kNegInf ? 0.0 : mom_move(hq, sq, fq, eq));
+    mhp = wave_sum(mp == kNegInf ? 0.0 : mom_move(hp, spp, fp, ep));
+    mx = wave_sum(mq == kNegInf ? 0.0 : mom_move(xq, sq, fq, ep));
+  }
+  if constexpr (ARG) {
+    iq = wave_min(mq == Wq ? iq : 0x7fffffff);
+    ip = wave_min(mp == Wp ? ip : 0x7fffffff);
+  }
+  if (lane == 0) {
+    sh.m[wv][0] = Wq;
+    sh.m[wv][1] = Wp;
+    sh.d[wv][0] = dq;
+    sh.d[wv][1] = dp;
+    sh.h[wv][0] = mhq;
+    sh.h[wv][1] = mhp;
+    sh.h[wv][2] = mx;
+    sh.i[wv][0] = iq;
+    sh.i[wv][1] = ip;
+  }
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    // wave 0 combines the wavefronts, lane w taking wavefront w's partials
+    const bool in = lane < kSmallWaves;
+    const int w = in ? lane : 0;
+    const float wq_ = in ? sh.m[w][0] : kNegInf, wp_ = in ? sh.m[w][1] : kNegInf;
+    const float Mq = wave_max(wq_), Mp = wave_max(wp_);
+    const double Rq = (double)(Mq * sp.c_hi), Rp = (double)(Mp * sp.c_hi);
+    const double gq = wq_ == kNegInf ? 0.0 : (double)(wq_ * sp.c_hi) - Rq;
+    const double gp = wp_ == kNegInf ? 0.0 : (double)(wp_ * sp.c_hi) - Rp;
+    const double fq_ = exp2_acc(gq), fp_ = exp2_acc(gp);
+    const double Sq = wave_sum(wq_ != kNegInf ? sh.d[w][0] * fq_ : 0.0);
+    const double Sp = wave_sum(wp_ != kNegInf ? sh.d[w][1] * fp_ : 0.0);
+    double Hq = 0.0, Hp = 0.0, X = 0.0;
+    if constexpr (MOM) {
+      Hq = wave_sum(wq_ != kNegInf ? mom_move(sh.h[w][0], sh.d[w][0], fq_, gq) : 0.0);
+      Hp = wave_sum(wp_ != kNegInf ? mom_move(sh.h[w][1], sh.d[w][1], fp_, gp) : 0.0);
+      X = wave_sum(wq_ != kNegInf ? mom_move(sh.h[w][2], sh.d[w][0], fq_,
+                                             wp_ == kNegInf ? -__builtin_huge_val() : gp)
+                                  : 0.0);
+    }
+    const int aq = wave_min(in && wq_ == Mq ? sh.i[w][0] : 0x7fffffff);
+    const int ap = wave_min(in && wp_ == Mp ? sh.i[w][1] : 0x7fffffff);
+    RowStat rs;
+    const double lq2 = log2_acc(Sq), lp2 = log2_acc(Sp);
+    rs.lz_q = (Mq == kNegInf ? (double)kNegInf : Rq) + lq2;
+    rs.lz_p = (Mp == kNegInf ? (double)kNegInf : Rp) + lp2;
+    rs.tv = 0.0;
+    rs.slog = (MOM && mrule) ? log_stat(mrule, lq2, lp2, Sq, Sp, Hq, Hp, X) : 0.0;
+    rs.zmax_q = Mq;
+    rs.zmax_p = Mp;
+    rs.amax_q = (ARG && aq != 0x7fffffff) ? aq : -1;
+    rs.amax_p = (ARG && ap != 0x7fffffff) ? ap : -1;
+    if (lane == 0) sh.rs = rs;
+  }
+  __syncthreads();
+  return sh.rs;
+}
+
+// Thread: sum over its entries of the sampled distribution KIND's weights
+// for lane load i (float, entry order).
+template <int DT, bool VEC, int KIND>
+__device__ __forceinline__ float small_weight_row(const uint32_t (&wq)[Tile<DT, VEC, kSmallU>::NW],
+                                                  const uint32_t (&wp)[Tile<DT, VEC, kSmallU>::NW],
+                                                  bool ok, const ProbScale& ps, int kind) {
+  float t = 0.0f;
+#pragma unroll
+  for (int e = 0; e < Tile<DT, VEC, kSmallU>::VW; ++e) {
+    t += weight_k<DT, KIND>(small_elem<DT, VEC>(wq, e, ok), small_elem<DT, VEC>(wp, e, ok), ps, kind);
+    if (e & 1) __builtin_amdgcn_sched_barrier(0);
+  }
+  return t;
+}
+
+// Whole block: the masses of the row's sub-chunks under KIND (sub-chunk
+// i * 16 + w is wave w's lane load i), stored as set `set` of the row for
+// the sequence's draw; returns their total.
+template <int DT, bool VEC, int KIND>
+__device__ __forceinline__ double small_masses(const Params& P, int r, int set, int kind,
+                                               const uint32_t (&wq)[kSmallU][Tile<DT, VEC, kSmallU>::NW],
+                                               const uint32_t (&wp)[kSmallU][Tile<DT, VEC, kSmallU>::NW],
+                                               const ProbScale& ps, SmallShared& sh) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  double tot = 0.0;
+#pragma unroll
+  for (int i = 0; i < kSmallU; ++i) {
+    double m = 0.0;
+    if (small_live<DT, VEC>(i, P.V))  // wavefront-uniform
+      m = wave_sum((double)small_weight_row<DT, VEC, KIND>(wq[i], wp[i], small_ok<DT, VEC>(i, P.V),
+                                                           ps, kind));
+    if (lane == 0)
+      st_dev_f64(P.submass + ((int64_t)r * 2 + set) * kSmallSub + i * kSmallWaves + wv, m);
+    tot += m;
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  return small_sum(lane == 0 ? tot : 0.0, sh);
+}
+
+template <int DT, bool VEC>
+__device__ __forceinline__ double small_masses_kind(const Params& P, int r, int set, int kind,
+                                                    const uint32_t (&wq)[kSmallU][Tile<DT, VEC, kSmallU>::NW],
+                                                    const uint32_t (&wp)[kSmallU][Tile<DT, VEC, kSmallU>::NW],
+                                                    const ProbScale& ps, SmallShared& sh) {
+  if (kind == kResidual) return small_masses<DT, VEC, kResidual>(P, r, set, kind, wq, wp, ps, sh);
+  if (kind == kTokRes) return small_masses<DT, VEC, kTokRes>(P, r, set, kind, wq, wp, ps, sh);
+  if (kind == kQ) return small_masses<DT, VEC, kQ>(P, r, set, kind, wq, wp, ps, sh);
+  if (kind == kP) return small_masses<DT, VEC, kP>(P, r, set, kind, wq, wp, ps, sh);
+  return small_masses<DT, VEC, kTokPi>(P, r, set, kind, wq, wp, ps, sh);
+}
+
+// Wave: the draw of sequence b at row j* = f from that row's stored
+// sub-chunk masses under `kind`: the sub-chunk where u W is crossed, then
+// the entry inside it (read again).
+template <int DT, bool VEC>
+__device__ __forceinline__ void small_draw_w(const Params& P, int b, int f, int kind, int set,
+                                             const SeqParam& sp) {
+  const int64_t row = (int64_t)b * (P.gamma + 1) + f;
+  const RowStat rs = ld_rowstat(P.rowstat + row);
+  const float u = P.uniforms[(int64_t)b * (P.gamma + 1) + P.gamma];
+  int ks;
+  double rem;
+  // set `set` of the row's masses, read as the residual search reads a
+  // sequence's (nsub = kSmallSub)
+  const double W = find_part<kSrcPass, kSmallSub / 64>(P, row, (int)(row * 2 + set), kSmallSub,
+                                                       rs, u, &ks, &rem);
+  if ((threadIdx.x & 63) == 0) {
+    if (P.out_norm) P.out_norm[b] = (float)W;
+    if (ks < 0) P.out_token[b] = -1;
+  }
+  if (ks < 0) return;  // wave-uniform
+  const ProbScale ps = prob_scale(sp, rs, kind == kTokRes || kind == kTokPi);
+  const int64_t c0 = (int64_t)ks * SubC<DT, VEC>::N;
+  if (kind == kResidual) pick_wave<DT, VEC, SubC<DT, VEC>, kResidual>(P, b, row, c0, rem, ps);
+  else if (kind == kTokRes) pick_wave<DT, VEC, SubC<DT, VEC>, kTokRes>(P, b, row, c0, rem, ps);
+  else if (kind == kQ) pick_wave<DT, VEC, SubC<DT, VEC>, kQ>(P, b, row, c0, rem, ps);
+  else if (kind == kP) pick_wave<DT, VEC, SubC<DT, VEC>, kP>(P, b, row, c0, rem, ps);
+  else pick_wave<DT, VEC, SubC<DT, VEC>, kTokPi>(P, b, row, c0, rem, ps);
+}
+
+template <int DT, bool VEC, int MS>
+__global__ __launch_bounds__(kSmallThreads) void k_small(Params P) {
+  using T = Tile<DT, VEC, kSmallU>;
+  __shared__ SmallShared sh;
+  const int r = blockIdx.x, gamma = P.gamma, g1 = gamma + 1, V = P.V;
+  const int b = r / g1, j = r - b * g1;
+  const int lane = threadIdx.x & 63;
+  const SeqParam sp = seq_param(P, b);
+  const int x = (sp.valid && j < gamma) ? P.draft[(int64_t)b * gamma + j] : -1;
+  const float u = (sp.valid && !sp.greedy) ? P.uniforms[r] : 0.0f;
+  uint32_t wq[kSmallU][T::NW], wp[kSmallU][T::NW];
+  small_load<DT, VEC>((const char*)P.q + (int64_t)r * V * T::EB, V, wq);
+  small_load<DT, VEC>((const char*)P.p + (int64_t)r * V * T::EB, V, wp);
+  const int mrule = (MS != 0 && needs_mom(sp)) ? sp.rule : 0;
+  RowStat rs;
+  if (sp.greedy)  // block-uniform
+    rs = (MS != 0 && mrule) ? small_stats<DT, VEC, 1, true>(wq, wp, V, sp, mrule, sh)
+                            : small_stats<DT, VEC, 0, true>(wq, wp, V, sp, 0, sh);
+  else
+    rs = (MS != 0 && mrule) ? small_stats<DT, VEC, 1, false>(wq, wp, V, sp, mrule, sh)
+                            : small_stats<DT, VEC, 0, false>(wq, wp, V, sp, 0, sh);
+  // the logits the decision reads, from the thread holding them: the draft
+  // token's, or (greedy TokenV2/V3, BiLD*) p's at the drafter's argmax
+  int xi = x;
+  if (sp.valid && sp.greedy)
+    xi = ((is_token(sp.rule) && sp.rule != SPC_RULE_TOKEN_V1) || sp.rule == SPC_RULE_BILD)
+             ? rs.amax_q : -1;
+  if (threadIdx.x == 0) {
+    sh.zx[0] = 0.0f;
+    sh.zx[1] = 0.0f;
+  }
+  __syncthreads();
+  if (xi >= 0 && xi < V) {
+    const int slot = xi / T::VW, e = xi - slot * T::VW;
+    if (slot % kSmallThreads == (int)threadIdx.x) {
+      const int i = slot / kSmallThreads;
+      float zq = 0.0f, zp = 0.0f;
+#pragma unroll
+      for (int ii = 0; ii < kSmallU; ++ii)
+        if (ii == i) {
+#pragma unroll
+          for (int ee = 0; ee < T::VW; ++ee)
+            if (ee == e) {
+              zq = elem<DT, VEC>(wq[ii], ee);
+              zp = elem<DT, VEC>(wp[ii], ee);
+            }
+        }
+      sh.zx[0] = sp.greedy ? 0.0f : zq;
+      sh.zx[1] = zp;
+    }
+  }
+  // the second pass from the registers: D_TV (OPT, OPTLOG) or eta (token
+  // rules) at temperature > 0
+  const bool tv = sp.valid && !sp.greedy && has_tv_parts(sp.rule);
+  const bool eta = sp.valid && !sp.greedy && is_token(sp.rule);
+  if (tv || eta) {  // block-uniform
+    const ProbScale ps = prob_scale(sp, rs, eta);
+    double acc = 0.0;
+#pragma unroll
+    for (int i = 0; i < kSmallU; ++i) {
+      if (!small_live<DT, VEC>(i, V)) continue;  // wavefront-uniform
+      const bool ok = small_ok<DT, VEC>(i, V);
+      float t = 0.0f;
+#pragma unroll
+      for (int e = 0; e < T::VW; ++e) {
+        const float zq = small_elem<DT, VEC>(wq[i], e, ok), zp = small_elem<DT, VEC>(wp[i], e, ok);
+        if (eta) {
+          t += token_r(ps.tok, zq, zp) ? prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo) : 0.0f;
+        } else {
+          const float pq = prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo);
+          const float pp = prob(zp, ps.c_hi, ps.c_lo, ps.p_hi, ps.p_lo);
+          t += fmaxf(pp - pq, 0.0f);
+        }
+        if (e & 1) __builtin_amdgcn_sched_barrier(0);
+      }
+      acc += (double)t;
+    }
+    rs.tv = small_sum(acc, sh);
+    small_fence(wq, wp);
+  }
+  // The distributions this row may be drawn from if it is the sequence's
+  // j*: set 0 for a deferring row (delta = 1) or the rule's fixed kind, set 1
+  // for delta = 0 or for an empty residual (replaced by p).  Both come from
+  // the registers before the decision, which then needs none of them.
+  int kind0 = kNone, kind1 = kNone;
+  if (sp.valid && !sp.greedy) {
+    if (is_token(sp.rule)) {
+      kind0 = j < gamma ? kTokRes : kTokPi;
+      kind1 = j < gamma ? kP : kNone;
+    } else if (sp.rule == SPC_RULE_LOSSY) {
+      kind0 = j < gamma ? kResidual : kP;
+      kind1 = j < gamma ? kP : kNone;
+    } else {
+      kind0 = j < gamma ? kResidual : kP;
+      kind1 = j < gamma ? kP : kQ;
+    }
+  }
+  double W0 = 0.0;
+  if (kind0 != kNone)  // block-uniform
+    W0 = small_masses_kind<DT, VEC>(P, r, 0, kind0, wq, wp,
+                                    prob_scale(sp, rs, kind0 == kTokRes || kind0 == kTokPi), sh);
+  small_fence(wq, wp);
+  if (kind1 != kNone)
+    (void)small_masses_kind<DT, VEC>(P, r, 1, kind1, wq, wp, prob_scale(sp, rs, false), sh);
+  __syncthreads();  // the logits at the draft token are in shared memory
+  // the decision (wave 0)
+  if (threadIdx.x < 64) {
+    RowDecision d{};
+    if (sp.valid) d = decide_row(sp, rs, j, gamma, V, x, sh.zx[0], sh.zx[1], u);
+    if (lane == 0) {
+      int set = 0;
+      if (sp.valid && !sp.greedy) {
+        const bool empty = (kind0 == kResidual || kind0 == kTokRes) && !(W0 > 0.0);
+        set = (is_token(sp.rule) || sp.rule == SPC_RULE_LOSSY) ? (empty ? 1 : 0)
+                                                                : (d.delta && !empty ? 0 : 1);
+      }
+      const int kind = set ? kind1 : kind0;
+      row_record(P, r, sp, d, (kind < 0 ? 0 : kind) | (set << 4));
+    }
+  }
+  vmem_drain();
+  __syncthreads();  // every store of this row is complete
+  if (threadIdx.x >= 64) return;
+  if (!arrive_last_w(row_word(P, b, kSeqResArrive), (uint32_t)g1)) return;
+  // the last row of sequence b: j* is its first rejection
+  const int rec = lane < g1 ? ld_i32(P.rowdec + (int64_t)b * g1 + lane) : 0;
+  const unsigned long long rej = __ballot(lane < g1 && !(rec & 1));
+  const int f = rej ? __ffsll(rej) - 1 : gamma;
+  const int recf = lane_i32(rec, f);
+  if (!sp.valid) {
+    if (lane == 0) {
+      P.out_accept[b] = -1;
+      P.out_token[b] = -1;
+      if (P.out_norm) P.out_norm[b] = 0.0f;
+    }
+    return;
+  }
+  if (lane == 0) P.out_accept[b] = f;
+  if (sp.greedy) {
+    if (lane == 0) {
+      const RowStat rf = ld_rowstat(P.rowstat + (int64_t)b * g1 + f);
+      const int dstar = (recf >> 1) & 1;
+      P.out_token[b] = (dstar || sp.rule == SPC_RULE_LOSSY) ? rf.amax_p : rf.amax_q;
+      if (P.out_norm) P.out_norm[b] = 1.0f;
+    }
+    return;
+  }
+  small_draw_w<DT, VEC>(P, b, f, (recf >> 4) & 0xf, (recf >> 8) & 1, sp);
+}
+
+template <int DT, bool VEC>
+hipError_t launch_small_t(const Params& P, hipStream_t st, hipEvent_t ev_begin,
+                          hipEvent_t ev_end) {
+  if (ev_begin) {
+    const hipError_t e = hipEventRecord(ev_begin, st);
+    if (e != hipSuccess) return e;
+  }
+  // batches with first moments take the tile path (their registers would not
+  // fit beside the row)
+  if (P.mom_set != 0) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)(P.B * (P.gamma + 1))), block(kSmallThreads);
+  hipLaunchKernelGGL((k_small<DT, VEC, 0>), grid, block, 0, st, P);
+  hipError_t err = hipGetLastError();
+  if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, st);
   return err;
 }
 
@@ -2395,6 +2892,20 @@ hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t st) {
   const unsigned groups = (unsigned)std::min<size_t>((n + 255) / 256, 1024);
   hipLaunchKernelGGL(k_fill_zero, dim3(groups), dim3(256), 0, st, static_cast<uint32_t*>(ptr), n);
   return hipGetLastError();
+}
+
+int small_row_elems(int dtype, bool vec) {
+  if (dtype == 1) return vec ? SmallRow<1, true>::N : SmallRow<1, false>::N;
+  return vec ? SmallRow<0, true>::N : SmallRow<0, false>::N;
+}
+
+hipError_t launch_small(const Params& P, int dtype, bool vec, hipEvent_t ev_begin,
+                        hipEvent_t ev_end, hipStream_t st) {
+  if (dtype == 1)
+    return vec ? launch_small_t<1, true>(P, st, ev_begin, ev_end)
+               : launch_small_t<1, false>(P, st, ev_begin, ev_end);
+  return vec ? launch_small_t<0, true>(P, st, ev_begin, ev_end)
+             : launch_small_t<0, false>(P, st, ev_begin, ev_end);
 }
 
 hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, bool draw_pass,
