@@ -210,35 +210,62 @@ def bench_draft(args, wl, dev):
     return 0
 
 
-def bench_decode(args, wl, dev):
+def decode_params(wl):
+    """Rule, alpha and temperature of the decoding loop: the workload's
+    scalars, or for the stress mix per-sequence arrays drawn (seeded) from its
+    rule and temperature sets."""
+    import torch
+    from paper_2405_19261_amd import workloads as W
+    if wl.rule >= 0:
+        return wl.rule, wl.alpha, wl.temperature
+    g = torch.Generator().manual_seed(1000 * wl.cfg)
+    pick = torch.randint(0, len(W.CFG5_RULES), (wl.B,), generator=g)
+    rule = torch.tensor([r for r, _ in W.CFG5_RULES], dtype=torch.int32)[pick]
+    alpha = torch.tensor([a for _, a in W.CFG5_RULES], dtype=torch.float32)[pick]
+    temp = torch.tensor(W.CFG5_TEMPS, dtype=torch.float32)[
+        torch.randint(0, len(W.CFG5_TEMPS), (wl.B,), generator=g)]
+    return rule, alpha, temp
+
+
+def bench_decode(args, wl, dev, backend=None):
     """Rounds of the decoding loop (draft gamma tokens, score, verify, roll
     back) on synthetic models of the workload's vocabulary; emitted tokens/s
-    over the whole loop, host bookkeeping included."""
+    over the whole loop, host bookkeeping included.  ``backend`` defaults to
+    the library's."""
     import torch
     from paper_2405_19261_amd import decode
+    dev = torch.device(dev)
+
+    def sync():
+        if dev.type == "cuda":
+            torch.cuda.synchronize()
+
     dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     q_lm, p_lm = decode.synthetic_pair(wl.V, seed=1, dtype=dt, device=dev)
     first = torch.randint(0, wl.V, (wl.B,), generator=torch.Generator().manual_seed(0))
-    kw = dict(gamma=wl.gamma, rule=wl.rule, alpha=wl.alpha, temperature=wl.temperature,
-              graph=args.graph)
+    rule, alpha, temp = decode_params(wl)
+    kw = dict(gamma=wl.gamma, rule=rule, alpha=alpha, temperature=temp, graph=args.graph,
+              backend=backend)
     decode.spec_decode(q_lm, p_lm, first, rounds=2, seed=5, **kw)  # warm-up
-    torch.cuda.synchronize()
+    sync()
     t0 = time.perf_counter()
     res = decode.spec_decode(q_lm, p_lm, first, rounds=args.decode, seed=6, **kw)
-    torch.cuda.synchronize()
+    sync()
     el = time.perf_counter() - t0
     n = sum(len(t) for t in res.tokens)
-    print(json.dumps(dict(
+    params = (f"rule {wl.rule} alpha={wl.alpha:g} T={wl.temperature}" if wl.rule >= 0 else
+              "per-sequence rule {Chow 0.4, Diff 0.05, OPT 0.1} and T {0.5, 0.7, 1.0}")
+    line = dict(
         metric="emitted tokens/s (decoding loop, synthetic models)", value=n / el,
         unit="tokens/s", n_gpus=1, rounds=args.decode, higher_is_better=True, dtype="f32",
         data="synthetic", ms_per_round=el * 1e3 / args.decode,
         tokens_per_round=res.tokens_per_round(),
         config=dict(workload=f"decoding loop: B={wl.B} gamma={wl.gamma} V={wl.V} {wl.dtype}, "
-                             f"rule {wl.rule} alpha={wl.alpha:g} T={wl.temperature}; "
-                             "synthetic Markov drafter/verifier (table lookups)"
+                             f"{params}; synthetic Markov drafter/verifier (table lookups)"
                              + ("; one HIP graph replay per round (capture included)"
-                                if args.graph else "")))), flush=True)
-    return 0
+                                if args.graph else "")))
+    print(json.dumps(line), flush=True)
+    return line
 
 
 def main():
@@ -301,7 +328,8 @@ def main():
     if args.draft:
         return bench_draft(args, wl, dev)
     if args.decode:
-        return bench_decode(args, wl, dev)
+        bench_decode(args, wl, dev)
+        return 0
     sets = [W.generate(wl, 1000 + i, dev) for i in range(args.sets)]
     B, gamma, V = wl.B, wl.gamma, wl.V
     outs = [(torch.empty(B, dtype=torch.int32, device=dev),

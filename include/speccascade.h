@@ -98,8 +98,8 @@ typedef enum {
 typedef enum {
   SPC_OK = 0,
   SPC_E_NULL = -1,      /* a required pointer is NULL                                 */
-  SPC_E_SHAPE = -2,     /* B < 1, gamma < 1, gamma > SPC_MAX_GAMMA, V < 2, or
-                           B*(gamma+1)*V does not fit the index range                 */
+  SPC_E_SHAPE = -2,     /* B < 1, gamma < 1, gamma > SPC_MAX_GAMMA or V < 2 (any B:
+                           large batches run as several launches)                     */
   SPC_E_RULE = -3,      /* a rule id outside spc_rule                                 */
   SPC_E_PARAM = -4,     /* alpha not finite, temperature not > 0 and finite,
                            or an unknown dtype                                        */
@@ -113,7 +113,10 @@ typedef enum {
 
 /*
  * spc_verify -- one verify step at temperature `temperature` > 0 with the same
- * rule, alpha and temperature for all B sequences.
+ * rule, alpha and temperature for all B sequences.  A temperature below
+ * 2^-107 (any float32 down to the smallest subnormal) is computed as 2^-107:
+ * z / T stays finite for logits up to ~10^6 and the softmax is then already
+ * its T -> 0 limit over logits that differ by more than ~10^-30.
  *
  *   q_logits, p_logits  [B][gamma+1][V] drafter / verifier logits, `dtype`
  *   draft_tokens        [B][gamma] int32: x_t .. x_{t+gamma-1}
@@ -250,7 +253,9 @@ size_t spc_noalloc_scratch_bytes(void);
  *                 out_token = -1
  *   uniforms      [B] float32 in [0,1): the token is the smallest k whose
  *                 cumulative mass (vocabulary order) exceeds u times the
- *                 total; may be NULL when every temperature is 0
+ *                 total; may be NULL only for the batch-wide argmax
+                 (temperature 0 and temp_per_seq NULL): with temp_per_seq
+                 it is required even if every entry is 0
  *   out_token     [B] int32
  * Uses the statistics tiles and the tile-mass draw of spc_verify (one pass
  * over the logits) and the internal workspace.  Errors as spc_verify; a

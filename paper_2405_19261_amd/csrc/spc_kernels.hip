@@ -349,6 +349,18 @@ __device__ __forceinline__ double lane_f64(double v, int l) {
   return __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(v), l),
                           __builtin_amdgcn_readlane(__double2loint(v), l));
 }
+__device__ __forceinline__ RowStat lane_rowstat(const RowStat& x, int l) {
+  RowStat y;
+  y.lz_q = lane_f64(x.lz_q, l);
+  y.lz_p = lane_f64(x.lz_p, l);
+  y.tv = lane_f64(x.tv, l);
+  y.slog = lane_f64(x.slog, l);
+  y.zmax_q = lane_f32(x.zmax_q, l);
+  y.zmax_p = lane_f32(x.zmax_p, l);
+  y.amax_q = lane_i32(x.amax_q, l);
+  y.amax_p = lane_i32(x.amax_p, l);
+  return y;
+}
 
 __device__ __forceinline__ float wave_max(float v) {
   v = fmaxf(v, dpp_f32<kDppXor1>(v));
@@ -2018,16 +2030,14 @@ __device__ __forceinline__ void arg_half_w(const Params& P, int r, int h) {
 // tile k, stored at their place in the row's sub-chunk order, which the draw
 // searches directly.
 template <int DT, bool VEC, int KIND>
-__device__ __forceinline__ void res_slice_w(const Params& P, int b, int c, int f) {
+__device__ __forceinline__ void res_slice_w(const Params& P, int b, int c, int f,
+                                            const RowStat& rs) {
   constexpr int U = StatTile<DT, VEC>::U;
   using T = StatTile<DT, VEC>;
   const int k = c / kSlices, w = c % kSlices;
   const int lane = threadIdx.x & 63, V = P.V;
   const int64_t row = (int64_t)b * (P.gamma + 1) + f;
   const int64_t t0 = (int64_t)k * T::N;
-  // the row's statistics first: a wait for a later load is a wait for every
-  // load before it, so the slice's entries are requested after them
-  const RowStat rs = ld_rowstat(P.rowstat + row);
   const SeqParam sp = seq_param(P, b);
   const ProbScale ps = prob_scale(sp, rs, KIND == kTokRes);
   __builtin_amdgcn_sched_barrier(0);
@@ -2041,11 +2051,14 @@ __device__ __forceinline__ void res_slice_w(const Params& P, int b, int c, int f
 }
 
 // (a branch per kind, each with its own stores, so that the compiler does
-// not evaluate both)
+// not evaluate both).  The row's statistics are loaded first: a wait for a
+// later load is a wait for every load before it, so the slice's entries are
+// requested after them.
 template <int DT, bool VEC>
 __device__ __forceinline__ void res_item_w(const Params& P, int b, int c, int f, int kind) {
-  if (kind == kTokRes) res_slice_w<DT, VEC, kTokRes>(P, b, c, f);
-  else res_slice_w<DT, VEC, kResidual>(P, b, c, f);
+  const RowStat rs = ld_rowstat(P.rowstat + (int64_t)b * (P.gamma + 1) + f);
+  if (kind == kTokRes) res_slice_w<DT, VEC, kTokRes>(P, b, c, f, rs);
+  else res_slice_w<DT, VEC, kResidual>(P, b, c, f, rs);
 }
 
 // ---------------------------------------------------------------- draw pass
@@ -2056,19 +2069,29 @@ __device__ __forceinline__ void res_item_w(const Params& P, int b, int c, int f,
 // statistics partials is made by workgroup (0, b).  The last arrival clears
 // the sequence's outcome word for the next call.  Sequences finished
 // elsewhere (later passes) have no outcome here and are skipped.
+// bfloat16: held to four resident workgroups per SIMD (a Gemma-vocabulary
+// batch of 32 sequences is 1024 workgroups: one round on 256 CUs); the draw
+// code would otherwise take one VGPR too many for it.
 template <int DT, bool VEC>
-__global__ __launch_bounds__(kThreads) void k_res(Params P) {
+__global__ __launch_bounds__(kThreads)
+__attribute__((amdgpu_waves_per_eu(DT == SPC_BF16 ? 4 : 1))) void k_res(Params P) {
   const int k = blockIdx.x, b = blockIdx.y;
+  const int g1 = P.gamma + 1, lane = threadIdx.x & 63;
+  // the statistics of every row of the sequence (lane j: row j), requested
+  // together with the outcome word that names the row the draw needs
+  RowStat mine{};
+  if (lane < g1) mine = ld_rowstat(P.rowstat + (int64_t)b * g1 + lane);
   const uint32_t info = ld_u32(row_word(P, b, kSeqInfo));
   if (!(info & kSeqInfoSet)) return;  // block-uniform
   const int f = (int)(info & 0xffu), kind = (int)((info >> 8) & 0xffu);
-  const int64_t row = (int64_t)b * (P.gamma + 1) + f;
+  const int64_t row = (int64_t)b * g1 + f;
+  const RowStat rs = lane_rowstat(mine, f);
   const SeqParam sp = seq_param(P, b);
   const bool residual = kind == kResidual || kind == kTokRes;
   if (residual) {
     const int w = threadIdx.x >> 6;
-    if (kind == kTokRes) res_slice_w<DT, VEC, kTokRes>(P, b, k * kSlices + w, f);
-    else res_slice_w<DT, VEC, kResidual>(P, b, k * kSlices + w, f);
+    if (kind == kTokRes) res_slice_w<DT, VEC, kTokRes>(P, b, k * kSlices + w, f, rs);
+    else res_slice_w<DT, VEC, kResidual>(P, b, k * kSlices + w, f, rs);
     vmem_drain();
   }
   __syncthreads();  // every wavefront's masses are stored

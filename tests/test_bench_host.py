@@ -51,3 +51,45 @@ def test_more_than_one_gpu_is_refused(n):
                        capture_output=True, text=True, timeout=120)
     assert r.returncode != 0
     assert "one GPU" in r.stderr or "1 GPU" in r.stderr or "single" in r.stderr, r.stderr
+
+
+class _OracleBackend:
+    """The decoding loop's two backend calls answered by the oracle, checking
+    the parameters as the library does (a rule id, a finite alpha and a
+    temperature >= 0 per sequence)."""
+
+    def __init__(self):
+        self.verifies = 0
+
+    def draft_sample(self, logits, temperature, uniforms):
+        import torch
+        t = temperature.numpy()
+        tok, _ = oracle.draft_sample(parity.host_logits(logits), t, uniforms.numpy())
+        return torch.from_numpy(tok.astype("int32"))
+
+    def verify(self, q, p, drafts, uniforms, rule, alpha, temperature):
+        import numpy as np
+        import torch
+        r, a, t = rule.numpy(), alpha.numpy(), temperature.numpy()
+        assert ((r >= 0) & (r <= W.OPTLOG)).all(), r
+        assert np.isfinite(a).all() and (t >= 0).all()
+        o = oracle.verify(parity.host_logits(q), parity.host_logits(p), drafts.numpy(),
+                          uniforms.numpy(), r, a, t)
+        self.verifies += 1
+        return torch.from_numpy(o["accept_len"]), torch.from_numpy(o["next_token"])
+
+
+@pytest.mark.parametrize("cfg", [3, 5])
+def test_decode_bench_runs_every_workload(cfg):
+    """bench.py --decode: the stress mix passes per-sequence arrays (its
+    scalar rule is a placeholder), and the loop completes on the oracle."""
+    import argparse
+    wl = W.WORKLOADS[cfg].with_(B=6, V=700, gamma=3)
+    rule, alpha, temp = bench.decode_params(wl)
+    if cfg == 5:
+        assert rule.shape == (wl.B,) and {int(x) for x in rule} <= {r for r, _ in W.CFG5_RULES}
+        assert {round(float(x), 6) for x in temp} <= set(W.CFG5_TEMPS)
+    be = _OracleBackend()
+    line = bench.bench_decode(argparse.Namespace(decode=3, graph=False), wl, "cpu", backend=be)
+    assert be.verifies == 2 + 3
+    assert line["value"] > 0 and 1.0 <= line["tokens_per_round"] <= wl.gamma + 1

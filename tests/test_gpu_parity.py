@@ -46,8 +46,7 @@ def test_workload_parity(cfg, steps):
     _flush(f"[parity] cfg{cfg} {wl.name} steps={_steps(cfg, steps)}")
     rep = parity.parity_workload(wl, _steps(cfg, steps))
     _flush(f"[parity] cfg{cfg} {dict(rep)}")
-    assert rep["exact"] + rep["excused_defer"] + rep["excused_accept"] + \
-        rep["excused_token"] + rep["excused_eta"] == rep["sequences"]
+    parity.check_accounting(rep)
 
 
 @pytest.mark.parametrize("part", range(4))
@@ -59,6 +58,7 @@ def test_workload2_parity(part):
     rep = parity.parity_workload(wl, n, step0=part * n, stats=(part == 0),
                                  report_name=f"cfg2.{part}")
     _flush(f"[parity] cfg2.{part} {dict(rep)}")
+    parity.check_accounting(rep)
 
 
 @pytest.mark.parametrize("part", range(2))
@@ -69,6 +69,7 @@ def test_workload5_parity(part):
     _flush(f"[parity] cfg5 part {part} steps={n}")
     rep = parity.parity_workload(wl, n, step0=part * n, report_name=f"cfg5.{part}")
     _flush(f"[parity] cfg5.{part} {dict(rep)}")
+    parity.check_accounting(rep)
 
 
 def test_workload3_bench_entry_point():
