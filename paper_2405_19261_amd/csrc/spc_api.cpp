@@ -112,6 +112,18 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
 
 namespace {
 
+// Bound of a statistics workgroup's wait for a TV row's merge, in ticks of
+// the 100 MHz real-time clock: 4000 (40 us).  SPC_TV_WAIT_TICKS overrides it
+// (read at every call); a test sets 0 so that every wait gives up at once
+// and the job pass takes the tiles.
+uint32_t tv_wait_ticks() {
+  const char* e = getenv("SPC_TV_WAIT_TICKS");
+  if (!e || !*e) return 4000u;
+  char* end = nullptr;
+  const unsigned long v = strtoul(e, &end, 10);
+  return (end && *end == '\0' && v <= 1000000ul) ? (uint32_t)v : 4000u;
+}
+
 spc_status check_shape(int32_t B, int32_t gamma, int32_t V) {
   if (B < 1 || gamma < 1 || gamma > SPC_MAX_GAMMA || V < 2)
     return fail(SPC_E_SHAPE, "bad shape B=%d gamma=%d V=%d (need B>=1, 1<=gamma<=%d, V>=2)", B,
@@ -355,14 +367,23 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
     // TV rows far enough from the end get their TV pass from statistics
     // workgroups issued about 640 tiles later (a few microseconds of the
     // stream: the row is merged by then and still in the caches)
-    P.lag = (may_sample && (rules & kTv)) ? (int32_t)std::max<int64_t>(1, (640 + nt - 1) / nt) : 0;
-    // singles: argmax halves, draws, and TV tiles whose stealer gave up
-    P.single_slots = 2 * R + bl + (P.lag > 0 ? R * nt : 0);
+    // stealing workgroups would come too late in a grid that is resident
+    // at once (at most two workgroups per compute unit): there each TV row
+    // takes its TV pass from its own tiles' registers instead
+    const bool tv_rows = may_sample && (rules & kTv);
+    P.tv_self = (tv_rows && R * nt <= 2 * (int64_t)cus) ? 1 : 0;
+    P.lag = (tv_rows && !P.tv_self) ? (int32_t)std::max<int64_t>(1, (640 + nt - 1) / nt) : 0;
+    P.wait_ticks = tv_wait_ticks();
+    // singles: argmax halves, draws, and TV tiles whose wait timed out
+    P.single_slots = 2 * R + bl + (tv_rows ? R * nt : 0);
     P.nsub = (int32_t)(nt * spc::tile_subchunks(dtype, vec));
     // workgroups of a job pass: a wavefront per item of its largest possible
     // list, at most two workgroups per compute unit
     const int64_t np = nt * spc::kSlices;
-    const int64_t items1 = np * (pass2_rows ? R : 0) + (may_greedy ? 2 * R : 0);
+    // (TV passes taken by the rows' own tiles leave pass 1 only the eta
+    // passes of token rules)
+    const bool row_jobs1 = pass2_rows && (!P.tv_self || (rules & kTok));
+    const int64_t items1 = np * (row_jobs1 ? R : 0) + (may_greedy ? 2 * R : 0);
     const int64_t items2 = pass2_rows ? np * bl + bl : 0;
     constexpr int64_t kW = spc::kJobThreads / 64;
     const int job_groups = (int)std::max<int64_t>(

@@ -74,6 +74,8 @@ struct Params {
   int64_t single_slots;    // single jobs a job pass may hold: 2 R + B
   int32_t nsub;            // sub-chunks of a row: nt * tile_subchunks
   int32_t lag;             // TV rows r < R - lag get their TV pass from the tiles of row r + lag
+  int32_t tv_self;         // TV rows get their TV pass from their own tiles (lag 0)
+  uint32_t wait_ticks;     // bound of a wait for a TV row's merge (100 MHz clock ticks)
   // workspace: zero region (counters; every launch leaves it as it found it)
   uint32_t* hdr;           // [kHdrLines][kLineWords] job counters
   uint32_t* rowline;       // [kMaxRows][kLineWords] per-row and per-sequence counters

@@ -1471,6 +1471,19 @@ __device__ __forceinline__ void pass2_slice_w(const Params& P, int r, int k, int
   if (lane == 0) st_dev_f64(P.tvpart + ((int64_t)r * P.nt + k) * kSlices + w, acc);
 }
 
+// Wave: the TV partial of slice w of tile k of row r from the slice's entries
+// already in registers (the statistics tile's own loads), into
+// tvpart[r][k * 4 + w].
+template <int DT, bool VEC>
+__device__ __forceinline__ void tv_slice_regs_w(
+    const Params& P, int r, int k, int w, const SeqParam& sp,
+    const uint32_t (&wq)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
+    const uint32_t (&wp)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW]) {
+  const ProbScale ps = prob_scale(sp, ld_rowstat(P.rowstat + r), false);
+  const double acc = wave_sum(pass2_sum<DT, VEC, false>(wq, wp, ps));
+  if ((threadIdx.x & 63) == 0) st_dev_f64(P.tvpart + ((int64_t)r * P.nt + k) * kSlices + w, acc);
+}
+
 // ================================================================ the step
 // Jobs a row or a sequence publishes for the job pass that follows: a TV or
 // eta second pass over a row and the residual masses of row j* of a sequence
@@ -1771,10 +1784,9 @@ __device__ __forceinline__ void row_job_decide(const Params& P, int kind, int r,
   if (f >= 0) seq_finish_w<DT>(P, b, f, sp, phase + 1);
 }
 
-// The wait of a stealing workgroup for its row's merge is bounded: 40 us of
-// the 100 MHz real-time clock, far beyond the usual lag; past it the tile
-// goes to the job pass.
-constexpr uint64_t kStealWait = 4000;
+// The wait of a workgroup for a TV row's merge is bounded by P.wait_ticks of
+// the 100 MHz real-time clock (by default 4000: 40 us, far beyond the usual
+// wait); past it the tile goes to the job pass.
 
 // Wave: the last of the 4 nt slices of TV row rv arrived: its decision (and
 // the sequence's finish, publishing to job pass 1), then the row's ready
@@ -1783,6 +1795,24 @@ template <int DT>
 __device__ __forceinline__ void tv_row_done(const Params& P, int rv, int phase) {
   row_job_decide<DT>(P, kJobTv, rv, phase);
   if ((threadIdx.x & 63) == 0) st_u32(row_word(P, rv, kRowReady), 0u);
+}
+
+// Wait (bounded, thread 0) for the ready flag of TV row rv; block-uniform
+// result.  On time-out the job pass takes tile k of the row's TV pass.
+__device__ __forceinline__ bool tv_wait_ready(const Params& P, int rv, int k, Shared& sh) {
+  if (threadIdx.x == 0) {
+    const uint32_t* flag = row_word(P, rv, kRowReady);
+    uint32_t f = ld_u32(flag);
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    while (f == 0u && __builtin_amdgcn_s_memrealtime() - t0 < (uint64_t)P.wait_ticks) {
+      __builtin_amdgcn_s_sleep(4);
+      f = ld_u32(flag);
+    }
+    sh.flag = f != 0u;
+    if (f == 0u) publish_single(P, 1, kJobTvTile, (uint32_t)k, (uint32_t)rv);
+  }
+  __syncthreads();
+  return sh.flag != 0;
 }
 
 // Whole block: the TV pass over tile k of row rv, whose statistics tiles
@@ -1794,21 +1824,7 @@ __device__ __forceinline__ void tv_row_done(const Params& P, int rv, int phase) 
 template <int DT, bool VEC>
 __device__ __forceinline__ void tv_steal(const Params& P, int rv, int k, const SeqParam& spv,
                                          Shared& sh) {
-  if (threadIdx.x == 0) {
-    const uint32_t* flag = row_word(P, rv, kRowReady);
-    uint32_t f = ld_u32(flag);
-    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-    while (f == 0u && __builtin_amdgcn_s_memrealtime() - t0 < kStealWait) {
-      __builtin_amdgcn_s_sleep(4);
-      f = ld_u32(flag);
-    }
-    sh.flag = f != 0u;
-  }
-  __syncthreads();
-  if (!sh.flag) {  // block-uniform: the merge is late, the job pass takes the tile
-    if (threadIdx.x == 0) publish_single(P, 1, kJobTvTile, (uint32_t)k, (uint32_t)rv);
-    return;
-  }
+  if (!tv_wait_ready(P, rv, k, sh)) return;  // block-uniform: the job pass takes the tile
   pass2_slice_w<DT, VEC, false>(P, rv, k, threadIdx.x >> 6, spv);
   vmem_drain();
   __syncthreads();  // all four slices are stored
@@ -1817,14 +1833,39 @@ __device__ __forceinline__ void tv_steal(const Params& P, int rv, int k, const S
     tv_row_done<DT>(P, rv, 0);
 }
 
-// The statistics tiles.  grid (nt, R): tile k of row r; NT: read the logits
-// non-temporally (no TV pass reads the rows again), else through the caches.
-// After the tile partial wave 0 arrives on the row's counter, and the last
-// tile of the row merges and decides it.  Without NT, a workgroup of row r
-// then takes tile k of the TV pass of row r - lag when that is a TV row
-// (tv_steal); otherwise waves 1-3 leave after the partial.
-template <int DT, bool VEC, int MS, bool NT>
+// Whole block: the TV pass over tile k of the block's own row r from the
+// registers that hold the tile (small batches: every tile of the grid is
+// resident at once, so the row's last tile arrives while the others wait).
+// Once the row's merge has set its ready flag each wavefront sums its slice;
+// the last of the row's slices decides the row.
+template <int DT, bool VEC>
+__device__ __forceinline__ void tv_self(
+    const Params& P, int r, int k, const SeqParam& sp, Shared& sh,
+    const uint32_t (&wq)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
+    const uint32_t (&wp)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW]) {
+  if (!tv_wait_ready(P, r, k, sh)) return;  // block-uniform
+  tv_slice_regs_w<DT, VEC>(P, r, k, threadIdx.x >> 6, sp, wq, wp);
+  vmem_drain();
+  __syncthreads();  // all four slices are stored
+  if (threadIdx.x < 64 &&
+      arrive_last_w(row_word(P, r, kRowTvArrive), (uint32_t)(kSlices * P.nt), kSlices))
+    tv_row_done<DT>(P, r, 0);
+}
+
+// How the statistics tiles serve the TV pass (OPT / OPTLOG rows at T > 0):
+// not at all (no TV row: the logits are read non-temporally), by taking
+// tile k of row r - lag after their own (tv_steal, reading through the
+// caches), or on their own row from registers (tv_self).
+enum TvMode : int { kTvNone = 0, kTvLag = 1, kTvSelf = 2 };
+
+// The statistics tiles.  grid (nt, R): tile k of row r.  After the tile
+// partial wave 0 arrives on the row's counter, and the last tile of the row
+// merges and decides it (a TV row: publishes it as merged).  Then, by TVM,
+// the block takes its share of a TV pass; otherwise waves 1-3 leave after
+// the partial.
+template <int DT, bool VEC, int MS, int TVM>
 __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
+  constexpr bool NT = TVM != kTvLag;  // no later block reads the row again
   using T = StatTile<DT, VEC>;
   __shared__ Shared sh;
   const int k = blockIdx.x, r = blockIdx.y;
@@ -1836,7 +1877,7 @@ __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
   const int rv = r - P.lag;
   SeqParam spv = sp;
   bool steal = false;
-  if (!NT && P.lag > 0 && rv >= 0) {  // batches that may hold TV rows read through the caches
+  if (TVM == kTvLag && P.lag > 0 && rv >= 0) {
     spv = seq_param(P, rv / g1);
     steal = spv.valid && !spv.greedy && has_tv_parts(spv.rule);
   }
@@ -1863,8 +1904,11 @@ __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
       row_merged_w<DT, MS>(P, r, b, j, sp);
     }
   }
-  if constexpr (!NT) {
+  if constexpr (TVM == kTvLag) {
     if (steal) tv_steal<DT, VEC>(P, rv, k, spv, sh);
+  }
+  if constexpr (TVM == kTvSelf) {
+    if (sp.valid && !sp.greedy && has_tv_parts(sp.rule)) tv_self<DT, VEC>(P, r, k, sp, sh, wq, wp);
   }
 }
 
@@ -2206,20 +2250,26 @@ hipError_t launch_step_t(const Params& P, hipStream_t st, bool nt_loads, bool dr
     const hipError_t e = hipEventRecord(ev_begin, st);
     if (e != hipSuccess) return e;
   }
+  constexpr int kAll = kMomX | kMomHQ | kMomHP;
   if (nt_loads) {
     if (P.mom_set == 0)
-      hipLaunchKernelGGL((k_tiles<DT, VEC, 0, true>), grid, block, 0, st, P);
+      hipLaunchKernelGGL((k_tiles<DT, VEC, 0, kTvNone>), grid, block, 0, st, P);
     else if (P.mom_set == kMomX)
-      hipLaunchKernelGGL((k_tiles<DT, VEC, kMomX, true>), grid, block, 0, st, P);
+      hipLaunchKernelGGL((k_tiles<DT, VEC, kMomX, kTvNone>), grid, block, 0, st, P);
     else if (P.mom_set == kMomHQ)
-      hipLaunchKernelGGL((k_tiles<DT, VEC, kMomHQ, true>), grid, block, 0, st, P);
+      hipLaunchKernelGGL((k_tiles<DT, VEC, kMomHQ, kTvNone>), grid, block, 0, st, P);
     else
-      hipLaunchKernelGGL((k_tiles<DT, VEC, kMomX | kMomHQ | kMomHP, true>), grid, block, 0, st, P);
+      hipLaunchKernelGGL((k_tiles<DT, VEC, kAll, kTvNone>), grid, block, 0, st, P);
+  } else if (P.tv_self) {
+    if (P.mom_set == 0)
+      hipLaunchKernelGGL((k_tiles<DT, VEC, 0, kTvSelf>), grid, block, 0, st, P);
+    else
+      hipLaunchKernelGGL((k_tiles<DT, VEC, kAll, kTvSelf>), grid, block, 0, st, P);
   } else {
     if (P.mom_set == 0)
-      hipLaunchKernelGGL((k_tiles<DT, VEC, 0, false>), grid, block, 0, st, P);
+      hipLaunchKernelGGL((k_tiles<DT, VEC, 0, kTvLag>), grid, block, 0, st, P);
     else
-      hipLaunchKernelGGL((k_tiles<DT, VEC, kMomX | kMomHQ | kMomHP, false>), grid, block, 0, st, P);
+      hipLaunchKernelGGL((k_tiles<DT, VEC, kAll, kTvLag>), grid, block, 0, st, P);
   }
   hipError_t err = hipGetLastError();
   if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, st);

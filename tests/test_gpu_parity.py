@@ -72,6 +72,21 @@ def test_workload5_parity(part):
     parity.check_accounting(rep)
 
 
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_tv_wait_timeout_takes_the_job_pass(cfg, monkeypatch):
+    """A statistics workgroup's wait for a TV row's merge is bounded; with the
+    bound at 0 ticks every wait that does not find the row merged gives up at
+    once and the job pass takes the tile.  The T5 shape takes its TV passes
+    from the rows' own tiles, the Gemma shape from tiles of later rows; both
+    must still match the oracle."""
+    monkeypatch.setenv("SPC_TV_WAIT_TICKS", "0")
+    wl = W.WORKLOADS[cfg].with_(B=8, rule=W.OPT, alpha=0.1, temperature=1.0)
+    _flush(f"[parity] tv wait 0: cfg{cfg} OPT B=8")
+    rep = parity.parity_workload(wl, 3, step0=810, report_name=f"tvwait0.cfg{cfg}")
+    parity.check_accounting(rep)
+    assert rep["sequences"] == 3 * 8
+
+
 def test_workload3_bench_entry_point():
     """The batch-wide entry point the benchmark times (no optional outputs)."""
     wl = W.WORKLOADS[3]
