@@ -4,8 +4,8 @@
                     [--copy-calib-mb N] [--rule NAME --alpha A]
     python bench.py --traffic-from FETCH.csv WRITE.csv --copy-calib-mb N
 
-A step is one spc_verify call (statistics pass + residual sampling pass) on
-the Gemma-vocabulary workload: B=32 sequences, gamma=7 drafted positions,
+A step is one spc_verify call (the statistics tiles, which also merge and
+decide each row, then the draw pass) on the Gemma-vocabulary workload: B=32 sequences, gamma=7 drafted positions,
 V=256000, bfloat16 logits, Diff rule alpha=0.05, temperature 1 (seeded
 synthetic Zipf(1.2) logits).  --rule / --alpha time the same shape under
 another rule (opt, or a token-specific rule token-v1/v2/v3, which add the
@@ -21,7 +21,7 @@ microseconds of step time, so not every step carries one) and the fp64
 oracle's throughput on the host cores (reported baseline).  Step-time
 percentiles come from the spacing of those events (EVERY-step windows).
 
-HBM traffic of the statistics kernel comes from two rocprofv3 counter runs of
+HBM traffic of the statistics kernel (k_tiles) comes from two rocprofv3 counter runs of
 this script (FETCH_SIZE, then WRITE_SIZE) with --copy-calib-mb, which first
 runs an elementwise float32 negation of N MiB (reads N MiB, writes N MiB):
 each counter is scaled by the ratio of the copy's known bytes to what the same
@@ -43,7 +43,9 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, published
 KERNEL_SRC = os.path.join(ROOT, "paper_2405_19261_amd", "csrc", "spc_kernels.hip")
-TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_stats_gemma-vocab_b32_g7_traffic.txt")
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_tiles_gemma-vocab_b32_g7_traffic.txt")
+ROOF_KERNEL = "k_tiles"  # the kernel the roofline object describes
+STEP_KERNELS = ("k_tiles", "k_res", "k_jobs", "k_small")
 MALL_BYTES = 256 << 20  # MI355X Infinity Cache
 COPY_KERNEL_TAG = "neg_kernel"  # the calibration copy is torch.neg
 
@@ -81,12 +83,17 @@ def kernel_sha256():
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def per_dispatch_kib(path, counter, tag):
-    """Mean counter value (KiB) per dispatch of kernels whose name holds tag."""
+def per_dispatch_kib(path, counter, tag, required=True):
+    """Mean counter value (KiB) per dispatch of kernels whose name holds tag
+    (the kernel name up to its template arguments)."""
+    def match(name):  # a library kernel by its own name, else any name holding tag
+        return f"::{tag}<" in name if tag.startswith("k_") else tag in name
     vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(path))
-            if r["Counter_Name"] == counter and tag in r["Kernel_Name"]]
+            if r["Counter_Name"] == counter and match(r["Kernel_Name"])]
     if not vals:
-        raise SystemExit(f"no {counter} rows for kernels matching {tag!r} in {path}")
+        if required:
+            raise SystemExit(f"no {counter} rows for kernels matching {tag!r} in {path}")
+        return None, 0
     return sum(vals) / len(vals), len(vals)
 
 
@@ -95,17 +102,28 @@ def traffic_record(fetch_csv, write_csv, copy_mb):
     copy_bytes = copy_mb * 2 ** 20
     f_copy, n_fc = per_dispatch_kib(fetch_csv, "FETCH_SIZE", COPY_KERNEL_TAG)
     w_copy, n_wc = per_dispatch_kib(write_csv, "WRITE_SIZE", COPY_KERNEL_TAG)
-    f_k, n_fk = per_dispatch_kib(fetch_csv, "FETCH_SIZE", "k_stats")
-    w_k, n_wk = per_dispatch_kib(write_csv, "WRITE_SIZE", "k_stats")
+    f_k, n_fk = per_dispatch_kib(fetch_csv, "FETCH_SIZE", ROOF_KERNEL)
+    w_k, n_wk = per_dispatch_kib(write_csv, "WRITE_SIZE", ROOF_KERNEL)
     fetch_scale = copy_bytes / (f_copy * 1024.0)
     write_scale = copy_bytes / (w_copy * 1024.0)
     fetch_b = f_k * 1024.0 * fetch_scale
     write_b = w_k * 1024.0 * write_scale
-    return dict(kernel="k_stats", kernel_src_sha256=kernel_sha256(), copy_mib=copy_mb,
+    # the step's other kernels, scaled alike
+    others = {}
+    for name in STEP_KERNELS:
+        if name == ROOF_KERNEL:
+            continue
+        f, nf = per_dispatch_kib(fetch_csv, "FETCH_SIZE", name, required=False)
+        w, nw = per_dispatch_kib(write_csv, "WRITE_SIZE", name, required=False)
+        if f is not None and w is not None:
+            others[name] = dict(fetch_bytes=f * 1024.0 * fetch_scale,
+                                write_bytes=w * 1024.0 * write_scale, dispatches=[nf, nw])
+    return dict(kernel=ROOF_KERNEL, kernel_src_sha256=kernel_sha256(), copy_mib=copy_mb,
                 copy_fetch_kib=f_copy, copy_write_kib=w_copy, fetch_scale=fetch_scale,
                 write_scale=write_scale, k_fetch_kib=f_k, k_write_kib=w_k,
                 dispatches=dict(copy_fetch=n_fc, copy_write=n_wc, k_fetch=n_fk, k_write=n_wk),
-                fetch_bytes=fetch_b, write_bytes=write_b, traffic_bytes=fetch_b + write_b)
+                fetch_bytes=fetch_b, write_bytes=write_b, traffic_bytes=fetch_b + write_b,
+                other_kernels=others)
 
 
 def stored_traffic():

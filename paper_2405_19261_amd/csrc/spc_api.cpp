@@ -90,7 +90,8 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
   L.zero_end = o;
   // two job passes, each with at most R + B row jobs and 2 R + B + R nt
   // single jobs (argmax halves, draws, TV tiles handed back by the tiles)
-  L.jobs = o; o = align_up(o + 8 * (size_t)(2 * ((R + B) + (2 * R + B + R * nt))), 256);
+  L.jobs = o;
+  o = align_up(o + 8 * (size_t)(2 * ((R + B) + (2 * R + B + R * nt * kSlices))), 256);
   L.jobline = o; o = align_up(o + 4 * (size_t)kLineWords * 2 * (R + B), 256);
   L.tiles = o; o = align_up(o + sizeof(TilePart) * R * nt, 256);
   L.tvpart = o; o = align_up(o + sizeof(double) * R * nt * kSlices, 256);
@@ -374,16 +375,17 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
     P.tv_self = (tv_rows && R * nt <= 2 * (int64_t)cus) ? 1 : 0;
     P.lag = (tv_rows && !P.tv_self) ? (int32_t)std::max<int64_t>(1, (640 + nt - 1) / nt) : 0;
     P.wait_ticks = tv_wait_ticks();
-    // singles: argmax halves, draws, and TV tiles whose wait timed out
-    P.single_slots = 2 * R + bl + (tv_rows ? R * nt : 0);
+    // singles: argmax halves, draws, TV tiles whose wait timed out, the
+    // slices of the tiles a token row lists for eta
+    P.single_slots = 2 * R + bl + R * nt * spc::kSlices;
     P.nsub = (int32_t)(nt * spc::tile_subchunks(dtype, vec));
     // workgroups of a job pass: a wavefront per item of its largest possible
     // list, at most two workgroups per compute unit
     const int64_t np = nt * spc::kSlices;
     // (TV passes taken by the rows' own tiles leave pass 1 only the eta
     // passes of token rules)
-    const bool row_jobs1 = pass2_rows && (!P.tv_self || (rules & kTok));
-    const int64_t items1 = np * (row_jobs1 ? R : 0) + (may_greedy ? 2 * R : 0);
+    const bool row_jobs1 = pass2_rows && !P.tv_self;
+    const int64_t items1 = np * ((row_jobs1 || (rules & kTok)) ? R : 0) + (may_greedy ? 2 * R : 0);
     const int64_t items2 = pass2_rows ? np * bl + bl : 0;
     constexpr int64_t kW = spc::kJobThreads / 64;
     const int job_groups = (int)std::max<int64_t>(

@@ -1550,6 +1550,19 @@ __device__ __forceinline__ void publish_single(const Params& P, int phase, int k
   if ((int64_t)s >= P.single_slots) return;
   st_u64(job_list(P, phase, true) + s, job_entry(kind, extra, id));
 }
+// Wave: n single jobs (kind, extra = 0 .. n-1, id), one reservation.
+__device__ __forceinline__ void publish_singles_w(const Params& P, int phase, int kind,
+                                                  uint32_t id, uint32_t n) {
+  if (phase > 2 || n == 0u) return;
+  const int lane = threadIdx.x & 63;
+  uint32_t s0 = 0;
+  if (lane == 0) s0 = add_u32(hdr_word(P, hdr_line(phase, true)), n);
+  s0 = (uint32_t)lane_i32((int)s0, 0);
+  for (uint32_t x = (uint32_t)lane; x < n; x += 64u) {
+    if ((int64_t)s0 + x >= P.single_slots) break;
+    st_u64(job_list(P, phase, true) + s0 + x, job_entry(kind, x, id));
+  }
+}
 
 // Shared state of a job workgroup.
 struct StepShared {
@@ -1752,8 +1765,9 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
       if (lane == 0) {
         st_rowstat(P.rowstat + r, rs);
         st_i32(P.etacnt + r, (int32_t)count);
-        publish_row_job(P, 1, kJobEta, (uint32_t)r);
       }
+      // a single job per slice of every listed tile (job pass 1)
+      publish_singles_w(P, 1, kJobEta, (uint32_t)r, count * (uint32_t)kSlices);
       return;
     }
     rs.tv = wave_sum(eta);
@@ -2204,7 +2218,6 @@ __global__ __launch_bounds__(kJobThreads) void k_jobs(Params P) {
       const int kind = job_kind(e);
       const int id = (int)job_id(e);
       if (kind == kJobTv) pass2_item_w<DT, VEC, false>(P, id, c);
-      else if (kind == kJobEta) pass2_item_w<DT, VEC, true>(P, id, c);
       else res_item_w<DT, VEC>(P, id, c, (int)(job_extra(e) & 0xff), (int)(job_extra(e) >> 8));
       if (arrive_last_w(job_done(P, phase, s), (uint32_t)np)) {
         if (kind == kJobRes) {
@@ -2228,6 +2241,11 @@ __global__ __launch_bounds__(kJobThreads) void k_jobs(Params P) {
           pass2_slice_w<DT, VEC, false>(P, id, (int)job_extra(e), w, spt);
         if (arrive_last_w(row_word(P, id, kRowTvArrive), (uint32_t)(kSlices * nt), kSlices))
           tv_row_done<DT>(P, id, phase);
+      } else if (kind == kJobEta) {
+        // slice c % 4 of the (c / 4)-th listed tile of token row id
+        const uint32_t n = (uint32_t)ld_i32(P.etacnt + id) * (uint32_t)kSlices;
+        pass2_item_w<DT, VEC, true>(P, id, (int)job_extra(e));
+        if (arrive_last_w(row_word(P, id, kRowTvArrive), n)) row_job_decide<DT>(P, kind, id, phase);
       } else if (kind == kJobArg) {
         arg_half_w<DT, VEC>(P, id, (int)job_extra(e));
         if (arrive_last_w(row_word(P, id, kRowJobDone), 2u)) row_job_decide<DT>(P, kind, id, phase);

@@ -93,3 +93,31 @@ def test_decode_bench_runs_every_workload(cfg):
     line = bench.bench_decode(argparse.Namespace(decode=3, graph=False), wl, "cpu", backend=be)
     assert be.verifies == 2 + 3
     assert line["value"] > 0 and 1.0 <= line["tokens_per_round"] <= wl.gamma + 1
+
+
+def test_traffic_record_scales_each_kernel_by_the_copy(tmp_path):
+    """--traffic-from: each counter is scaled by what it reads for the copy
+    of known size; the record names the roofline kernel and the step's
+    other kernels, matched by their own names (not by substrings of others)."""
+    import csv
+    rows = [("void at::native::vectorized_elementwise_kernel<4, "
+             "at::native::neg_kernel_cuda(at::TensorIteratorBase&)>", 131072.0, 262144.0),
+            ("void spc::(anonymous namespace)::k_tiles<1, true, 0, 0>(spc::Params)",
+             128000.0, 512.0),
+            ("void spc::(anonymous namespace)::k_res<1, true>(spc::Params)", 16000.0, 8.0)]
+    paths = {}
+    for counter, col in (("FETCH_SIZE", 1), ("WRITE_SIZE", 2)):
+        p = tmp_path / f"{counter}.csv"
+        with open(p, "w", newline="") as fh:
+            w = csv.writer(fh)
+            w.writerow(["Kernel_Name", "Counter_Name", "Counter_Value"])
+            for r in rows:
+                w.writerow([r[0], counter, r[col]])
+        paths[counter] = str(p)
+    rec = bench.traffic_record(paths["FETCH_SIZE"], paths["WRITE_SIZE"], 256)
+    assert rec["kernel"] == "k_tiles"
+    assert rec["fetch_scale"] == pytest.approx(2.0) and rec["write_scale"] == pytest.approx(1.0)
+    assert rec["fetch_bytes"] == pytest.approx(128000.0 * 1024 * 2)
+    assert rec["write_bytes"] == pytest.approx(512.0 * 1024)
+    assert set(rec["other_kernels"]) == {"k_res"}
+    assert rec["other_kernels"]["k_res"]["fetch_bytes"] == pytest.approx(16000.0 * 1024 * 2)
