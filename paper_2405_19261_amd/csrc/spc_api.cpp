@@ -315,19 +315,22 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
                                       ((rules & ((1u << SPC_RULE_DIFFLOG) | (1u << SPC_RULE_OPTLOG)))
                                            ? spc::kMomHQ | spc::kMomHP
                                            : 0);
-  // What the job passes may hold.  Rows of OPT / OPTLOG or a token rule at
-  // T > 0 are decided in the first job pass (after their TV or eta pass), so
-  // their draws fall to a second; every other row is decided by its last
-  // statistics tile, or (T = 0) after its argmax in the first pass.
+  // What the job pass may hold.  Rows of OPT / OPTLOG or a token rule at
+  // T > 0 may be decided in the job pass (after their TV or eta pass), so
+  // their draws fall to a second draw pass after it; every other row is
+  // decided by its last statistics tile, or (T = 0) after its argmax in the
+  // job pass.
   constexpr uint32_t kTok = (1u << SPC_RULE_TOKEN_V1) | (1u << SPC_RULE_TOKEN_V2) |
                             (1u << SPC_RULE_TOKEN_V3);
   const bool pass2_rows = may_sample && (rules & (kTv | kTok));
   const bool may_greedy = force_greedy || per_temp;
   // Sequences the statistics kernel finishes are drawn by the draw pass;
-  // job pass 1 takes TV and eta passes and argmax halves, pass 2 the draws of
-  // sequences decided in pass 1 (greedy ones write their token directly).
+  // the job pass takes TV and eta passes and argmax halves; the sequences it
+  // finishes are drawn by a second draw pass (greedy ones write their token
+  // directly).
   const bool draw_pass = may_sample;
-  const int job_passes = pass2_rows ? 2 : (may_greedy ? 1 : 0);
+  const bool job_pass = pass2_rows || may_greedy;
+  const bool draw_after = pass2_rows;
   // Small problems (rows that fit one workgroup's registers, at most two
   // rows per compute unit, no first moments) take the single-launch path.
   const bool small = !need_mom && V <= spc::small_row_elems(dtype, vec) &&
@@ -386,10 +389,9 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
     // passes of token rules)
     const bool row_jobs1 = pass2_rows && !P.tv_self;
     const int64_t items1 = np * ((row_jobs1 || (rules & kTok)) ? R : 0) + (may_greedy ? 2 * R : 0);
-    const int64_t items2 = pass2_rows ? np * bl + bl : 0;
     constexpr int64_t kW = spc::kJobThreads / 64;
     const int job_groups = (int)std::max<int64_t>(
-        1, std::min<int64_t>((std::max(items1, items2) + kW - 1) / kW, 2 * (int64_t)cus));
+        1, std::min<int64_t>((items1 + kW - 1) / kW, 2 * (int64_t)cus));
     P.hdr = reinterpret_cast<uint32_t*>(ws + L.hdr);
     P.rowline = reinterpret_cast<uint32_t*>(ws + L.rowline);
     P.jobs = reinterpret_cast<uint64_t*>(ws + L.jobs);
@@ -411,8 +413,8 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
       P.nsub = spc::kSmallSub;
       e = spc::launch_small(P, dtype, vec, ev0, ev1, stream);
     } else {
-      e = spc::launch_step(P, dtype, vec, nt_loads, draw_pass, job_passes, job_groups, ev0, ev1,
-                           stream);
+      e = spc::launch_step(P, dtype, vec, nt_loads, draw_pass, job_pass, draw_after, job_groups,
+                           ev0, ev1, stream);
     }
     if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
   }

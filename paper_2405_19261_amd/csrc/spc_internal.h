@@ -69,7 +69,7 @@ struct Params {
   int32_t* out_argmax;
   float* out_norm;
   // launch layout
-  int32_t phase;           // job pass of a k_jobs launch (1 or 2)
+  int32_t phase;           // job pass of a k_jobs launch (1)
   int64_t job_slots;       // row jobs a job pass may hold: R + B
   int64_t single_slots;    // single jobs a job pass may hold: 2 R + B
   int32_t nsub;            // sub-chunks of a row: nt * tile_subchunks
@@ -155,14 +155,15 @@ hipError_t launch_small(const Params& P, int dtype, bool vec, hipEvent_t ev_begi
                         hipEvent_t ev_end, hipStream_t stream);
 
 // Enqueue one verify launch: the statistics tiles (k_tiles), the draw pass
-// (k_res) when `draw_pass`, then `job_passes` job passes (k_jobs) of
-// `job_groups` workgroups each.
+// (k_res) when `draw_pass`, then with `job_pass` the job pass (k_jobs, of
+// `job_groups` workgroups) and, with `draw_after`, a second draw pass for the
+// sequences the job pass finished.
 // nt_loads: the tiles read the logits non-temporally (no job reads a whole
 // row again).
 // ev_begin / ev_end (may be null): recorded right before and after k_tiles.
 hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, bool draw_pass,
-                       int job_passes, int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end,
-                       hipStream_t stream);
+                       bool job_pass, bool draw_after, int job_groups, hipEvent_t ev_begin,
+                       hipEvent_t ev_end, hipStream_t stream);
 
 // Enqueue a kernel writing `bytes` zero bytes at `ptr` (a multiple of 4, ptr
 // 4-byte aligned): a fill a graph capture may record.

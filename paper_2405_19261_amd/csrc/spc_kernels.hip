@@ -1574,12 +1574,11 @@ struct StepShared {
 
 // Wave: sequence b's first rejection is j* = f.  Writes its accept length,
 // then the greedy token; or, for a draw (from the statistics partials, or
-// from the residual of row f), records it for the draw pass when the
-// statistics kernel finished the sequence (phase 1), else publishes it to
-// the job pass `phase`.
+// from the residual of row f), records it in the sequence's outcome word for
+// the draw pass (k_res) that follows the launch finishing the sequence: the
+// statistics kernel's, or the job pass's.
 template <int DT>
-__device__ __forceinline__ void seq_finish_w(const Params& P, int b, int f, const SeqParam& sp,
-                                             int phase) {
+__device__ __forceinline__ void seq_finish_w(const Params& P, int b, int f, const SeqParam& sp) {
   const int gamma = P.gamma, g1 = gamma + 1;
   const int64_t row = (int64_t)b * g1 + f;
   if ((threadIdx.x & 63) != 0) return;
@@ -1608,15 +1607,7 @@ __device__ __forceinline__ void seq_finish_w(const Params& P, int b, int f, cons
     // residual max(0, q - q) is empty, so p is sampled instead
     kind = (f < gamma) ? (dstar ? kResidual : kP) : (dstar ? kP : kQ);
   }
-  if (phase == 1) {
-    // finished by the statistics kernel: the draw pass (k_res) reads the
-    // sequence's outcome from its line
-    st_u32(row_word(P, b, kSeqInfo), kSeqInfoSet | ((uint32_t)kind << 8) | (uint32_t)f);
-  } else if (kind == kResidual || kind == kTokRes) {
-    publish_row_job(P, phase, kJobRes, (uint32_t)b, ((uint32_t)kind << 8) | (uint32_t)f);
-  } else {
-    publish_single(P, phase, kJobDraw, ((uint32_t)kind << 8) | (uint32_t)f, (uint32_t)b);
-  }
+  st_u32(row_word(P, b, kSeqInfo), kSeqInfoSet | ((uint32_t)kind << 8) | (uint32_t)f);
 }
 
 // Lane 0: write the outputs and the record of decided row r (d from
@@ -1773,7 +1764,7 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
     rs.tv = wave_sum(eta);
   }
   const int f = row_decide_w<DT>(P, r, b, j, sp, rs);
-  if (f >= 0) seq_finish_w<DT>(P, b, f, sp, 1);
+  if (f >= 0) seq_finish_w<DT>(P, b, f, sp);
 }
 
 // Wave: the row's decision once its TV, eta or argmax is known; when it
@@ -1795,7 +1786,7 @@ __device__ __forceinline__ void row_job_decide(const Params& P, int kind, int r,
   }
   const SeqParam sp = seq_param(P, b);
   const int f = row_decide_w<DT>(P, r, b, j, sp, rs);
-  if (f >= 0) seq_finish_w<DT>(P, b, f, sp, phase + 1);
+  if (f >= 0) seq_finish_w<DT>(P, b, f, sp);
 }
 
 // The wait of a workgroup for a TV row's merge is bounded by P.wait_ticks of
@@ -2108,16 +2099,6 @@ __device__ __forceinline__ void res_slice_w(const Params& P, int b, int c, int f
                ml);
 }
 
-// (a branch per kind, each with its own stores, so that the compiler does
-// not evaluate both).  The row's statistics are loaded first: a wait for a
-// later load is a wait for every load before it, so the slice's entries are
-// requested after them.
-template <int DT, bool VEC>
-__device__ __forceinline__ void res_item_w(const Params& P, int b, int c, int f, int kind) {
-  const RowStat rs = ld_rowstat(P.rowstat + (int64_t)b * (P.gamma + 1) + f);
-  if (kind == kTokRes) res_slice_w<DT, VEC, kTokRes>(P, b, c, f, rs);
-  else res_slice_w<DT, VEC, kResidual>(P, b, c, f, rs);
-}
 
 // ---------------------------------------------------------------- draw pass
 // k_res: grid (nt, B), after the statistics kernel.  For a sequence that
@@ -2184,14 +2165,17 @@ __device__ __forceinline__ void exit_tree(const Params& P, int phase) {
   st_u32(hdr_word(P, hdr_line(phase, true)), 0u);
 }
 
-// The job pass `phase` (1 or 2): a static walk over the jobs the earlier
-// launches of this call published for it -- every part of every row job
-// (newest job first: its rows are the likeliest still in the caches), then
-// every single job.  Wavefront w of the grid takes items w, w + W, ...  The
-// item that completes a job continues it: a row decision (jobs of the next
-// pass may follow) or the draw.
+// The job pass: a static walk over the jobs the statistics kernel of this
+// call published -- every part of every row job (a TV pass over a row;
+// newest job first: its rows are the likeliest still in the caches), then
+// every single job (a slice of a tile a token row listed for eta, a TV tile
+// whose wait timed out, an argmax half).  Wavefront w of the grid takes
+// items w, w + W, ...  The item that completes a job decides its row; a
+// sequence that decision finishes is drawn by the draw pass that follows.
+// Held to 128 VGPRs: two workgroups per compute unit.
 template <int DT, bool VEC>
-__global__ __launch_bounds__(kJobThreads) void k_jobs(Params P) {
+__global__ __launch_bounds__(kJobThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_jobs(
+    Params P) {
   __shared__ uint32_t counts[2];
   const int phase = P.phase, nt = P.nt, g1 = P.gamma + 1;
   if (threadIdx.x == 0) {
@@ -2217,18 +2201,8 @@ __global__ __launch_bounds__(kJobThreads) void k_jobs(Params P) {
       const uint64_t e = ld_u64(rows + s);
       const int kind = job_kind(e);
       const int id = (int)job_id(e);
-      if (kind == kJobTv) pass2_item_w<DT, VEC, false>(P, id, c);
-      else res_item_w<DT, VEC>(P, id, c, (int)(job_extra(e) & 0xff), (int)(job_extra(e) >> 8));
-      if (arrive_last_w(job_done(P, phase, s), (uint32_t)np)) {
-        if (kind == kJobRes) {
-          const int f = (int)(job_extra(e) & 0xff), skind = (int)(job_extra(e) >> 8);
-          const int64_t row = (int64_t)id * g1 + f;
-          draw_w<DT, VEC>(P, id, row, skind, kSrcPass, seq_param(P, id),
-                          ld_rowstat(P.rowstat + row));
-        } else {
-          row_job_decide<DT>(P, kind, id, phase);
-        }
-      }
+      pass2_item_w<DT, VEC, false>(P, id, c);  // the only row job: a TV pass
+      if (arrive_last_w(job_done(P, phase, s), (uint32_t)np)) row_job_decide<DT>(P, kind, id, phase);
     } else {
       const uint64_t e = ld_u64(singles + (g - n_row_items));
       const int kind = job_kind(e);
@@ -2246,14 +2220,9 @@ __global__ __launch_bounds__(kJobThreads) void k_jobs(Params P) {
         const uint32_t n = (uint32_t)ld_i32(P.etacnt + id) * (uint32_t)kSlices;
         pass2_item_w<DT, VEC, true>(P, id, (int)job_extra(e));
         if (arrive_last_w(row_word(P, id, kRowTvArrive), n)) row_job_decide<DT>(P, kind, id, phase);
-      } else if (kind == kJobArg) {
+      } else {  // kJobArg
         arg_half_w<DT, VEC>(P, id, (int)job_extra(e));
         if (arrive_last_w(row_word(P, id, kRowJobDone), 2u)) row_job_decide<DT>(P, kind, id, phase);
-      } else {  // a draw from the statistics partials
-        const int skind = (int)(job_extra(e) >> 8), f = (int)(job_extra(e) & 0xff);
-        const int64_t row = (int64_t)id * g1 + f;
-        const int src = skind == kQ ? kSrcStatsQ : skind == kP ? kSrcStatsP : kSrcTokPi;
-        draw_w<DT, VEC>(P, id, row, skind, src, seq_param(P, id), ld_rowstat(P.rowstat + row));
       }
     }
   }
@@ -2261,8 +2230,8 @@ __global__ __launch_bounds__(kJobThreads) void k_jobs(Params P) {
 
 template <int DT, bool VEC>
 hipError_t launch_step_t(const Params& P, hipStream_t st, bool nt_loads, bool draw_pass,
-                         int job_passes, int job_groups, hipEvent_t ev_begin,
-                         hipEvent_t ev_end) {
+                         bool job_pass, bool draw_after, int job_groups,
+                         hipEvent_t ev_begin, hipEvent_t ev_end) {
   const dim3 grid((unsigned)P.nt, (unsigned)(P.B * (P.gamma + 1))), block(kThreads);
   if (ev_begin) {
     const hipError_t e = hipEventRecord(ev_begin, st);
@@ -2295,12 +2264,16 @@ hipError_t launch_step_t(const Params& P, hipStream_t st, bool nt_loads, bool dr
     hipLaunchKernelGGL((k_res<DT, VEC>), dim3((unsigned)P.nt, (unsigned)P.B), block, 0, st, P);
     err = hipGetLastError();
   }
-  for (int phase = 1; phase <= job_passes && err == hipSuccess; ++phase) {
+  if (err == hipSuccess && job_pass) {
     Params Q = P;
-    Q.phase = phase;
+    Q.phase = 1;
     hipLaunchKernelGGL((k_jobs<DT, VEC>), dim3((unsigned)job_groups), dim3(kJobThreads), 0, st,
                        Q);
     err = hipGetLastError();
+    if (err == hipSuccess && draw_after) {  // the draws of sequences the job pass finished
+      hipLaunchKernelGGL((k_res<DT, VEC>), dim3((unsigned)P.nt, (unsigned)P.B), block, 0, st, P);
+      err = hipGetLastError();
+    }
   }
   return err;
 }
@@ -3000,16 +2973,16 @@ hipError_t launch_small(const Params& P, int dtype, bool vec, hipEvent_t ev_begi
 }
 
 hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, bool draw_pass,
-                       int job_passes, int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end,
-                       hipStream_t st) {
+                       bool job_pass, bool draw_after, int job_groups, hipEvent_t ev_begin,
+                       hipEvent_t ev_end, hipStream_t st) {
   if (dtype == 1)
-    return vec ? launch_step_t<1, true>(P, st, nt_loads, draw_pass, job_passes, job_groups,
+    return vec ? launch_step_t<1, true>(P, st, nt_loads, draw_pass, job_pass, draw_after, job_groups,
                                         ev_begin, ev_end)
-               : launch_step_t<1, false>(P, st, nt_loads, draw_pass, job_passes, job_groups,
+               : launch_step_t<1, false>(P, st, nt_loads, draw_pass, job_pass, draw_after, job_groups,
                                          ev_begin, ev_end);
-  return vec ? launch_step_t<0, true>(P, st, nt_loads, draw_pass, job_passes, job_groups,
+  return vec ? launch_step_t<0, true>(P, st, nt_loads, draw_pass, job_pass, draw_after, job_groups,
                                       ev_begin, ev_end)
-             : launch_step_t<0, false>(P, st, nt_loads, draw_pass, job_passes, job_groups,
+             : launch_step_t<0, false>(P, st, nt_loads, draw_pass, job_pass, draw_after, job_groups,
                                        ev_begin, ev_end);
 }
 
