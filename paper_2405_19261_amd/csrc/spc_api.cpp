@@ -125,6 +125,10 @@ uint32_t tv_wait_ticks() {
   return (end && *end == '\0' && v <= 1000000ul) ? (uint32_t)v : 4000u;
 }
 
+// TV passes of large batches taken by later statistics workgroups (true) or
+// by a kernel of their own after the statistics kernel (false).
+constexpr bool kTvLag = false;
+
 spc_status check_shape(int32_t B, int32_t gamma, int32_t V) {
   if (B < 1 || gamma < 1 || gamma > SPC_MAX_GAMMA || V < 2)
     return fail(SPC_E_SHAPE, "bad shape B=%d gamma=%d V=%d (need B>=1, 1<=gamma<=%d, V>=2)", B,
@@ -329,14 +333,12 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
   // finishes are drawn by a second draw pass (greedy ones write their token
   // directly).
   const bool draw_pass = may_sample;
-  const bool job_pass = pass2_rows || may_greedy;
   const bool draw_after = pass2_rows;
+  const bool tv_rows = may_sample && (rules & kTv);
   // Small problems (rows that fit one workgroup's registers, at most two
   // rows per compute unit, no first moments) take the single-launch path.
   const bool small = !need_mom && V <= spc::small_row_elems(dtype, vec) &&
                      b_launch * g1 <= 2 * (int64_t)cus;
-  // rows a TV job reads again are loaded through the caches
-  const bool nt_loads = !(may_sample && (rules & kTv));
   const int64_t nt = stat_tiles(dtype, vec, V);
   const int64_t eb = dtype == SPC_BF16 ? 2 : 4;
 
@@ -368,15 +370,21 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
     P.out_argmax = ex ? offset(ex->out_argmax, b0 * g1 * 2) : nullptr;
     P.out_norm = ex ? offset(ex->out_sample_norm, b0) : nullptr;
     P.job_slots = R + bl;
-    // TV rows far enough from the end get their TV pass from statistics
-    // workgroups issued about 640 tiles later (a few microseconds of the
-    // stream: the row is merged by then and still in the caches)
-    // stealing workgroups would come too late in a grid that is resident
-    // at once (at most two workgroups per compute unit): there each TV row
-    // takes its TV pass from its own tiles' registers instead
-    const bool tv_rows = may_sample && (rules & kTv);
+    // Where TV rows get their TV pass.  In a grid that is resident at once
+    // (at most two workgroups per compute unit) each TV row takes it from
+    // its own tiles' registers once the row is merged (tv_self).  Otherwise
+    // a kernel of its own re-reads the TV rows after the statistics kernel
+    // (k_tvpass; the statistics tiles then read non-temporally), or, with
+    // kTvLag, statistics workgroups issued about 640 tiles later take it
+    // (lag rows; the last rows' passes go to the job pass).
     P.tv_self = (tv_rows && R * nt <= 2 * (int64_t)cus) ? 1 : 0;
-    P.lag = (tv_rows && !P.tv_self) ? (int32_t)std::max<int64_t>(1, (640 + nt - 1) / nt) : 0;
+    const bool tv_pass = tv_rows && !P.tv_self && !kTvLag;
+    P.lag = (tv_rows && !P.tv_self && kTvLag) ? (int32_t)std::max<int64_t>(1, (640 + nt - 1) / nt)
+                                              : 0;
+    const bool nt_loads = !tv_rows || tv_pass;
+    // the job pass: argmax halves, eta slices, and the TV tiles whose wait
+    // for their row's merge timed out (tv_self, kTvLag)
+    const bool job_pass = may_greedy || (may_sample && (rules & kTok)) || (tv_rows && !tv_pass);
     P.wait_ticks = tv_wait_ticks();
     // singles: argmax halves, draws, TV tiles whose wait timed out, the
     // slices of the tiles a token row lists for eta
@@ -387,7 +395,7 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
     const int64_t np = nt * spc::kSlices;
     // (TV passes taken by the rows' own tiles leave pass 1 only the eta
     // passes of token rules)
-    const bool row_jobs1 = pass2_rows && !P.tv_self;
+    const bool row_jobs1 = tv_rows && P.lag > 0;
     const int64_t items1 = np * ((row_jobs1 || (rules & kTok)) ? R : 0) + (may_greedy ? 2 * R : 0);
     constexpr int64_t kW = spc::kJobThreads / 64;
     const int job_groups = (int)std::max<int64_t>(
@@ -413,8 +421,8 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
       P.nsub = spc::kSmallSub;
       e = spc::launch_small(P, dtype, vec, ev0, ev1, stream);
     } else {
-      e = spc::launch_step(P, dtype, vec, nt_loads, draw_pass, job_pass, draw_after, job_groups,
-                           ev0, ev1, stream);
+      e = spc::launch_step(P, dtype, vec, nt_loads, draw_pass, tv_pass, job_pass, draw_after,
+                           job_groups, ev0, ev1, stream);
     }
     if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
   }

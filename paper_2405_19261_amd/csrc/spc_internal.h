@@ -155,15 +155,15 @@ hipError_t launch_small(const Params& P, int dtype, bool vec, hipEvent_t ev_begi
                         hipEvent_t ev_end, hipStream_t stream);
 
 // Enqueue one verify launch: the statistics tiles (k_tiles), the draw pass
-// (k_res) when `draw_pass`, then with `job_pass` the job pass (k_jobs, of
-// `job_groups` workgroups) and, with `draw_after`, a second draw pass for the
-// sequences the job pass finished.
-// nt_loads: the tiles read the logits non-temporally (no job reads a whole
-// row again).
+// (k_res) when `draw_pass`, the TV passes (k_tvpass) when `tv_pass`, the job
+// pass (k_jobs, of `job_groups` workgroups) when `job_pass`, and with
+// `draw_after` a second draw pass for the sequences finished after the first.
+// nt_loads: the tiles read the logits non-temporally (no later workgroup of
+// k_tiles reads a row again).
 // ev_begin / ev_end (may be null): recorded right before and after k_tiles.
 hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, bool draw_pass,
-                       bool job_pass, bool draw_after, int job_groups, hipEvent_t ev_begin,
-                       hipEvent_t ev_end, hipStream_t stream);
+                       bool tv_pass, bool job_pass, bool draw_after, int job_groups,
+                       hipEvent_t ev_begin, hipEvent_t ev_end, hipStream_t stream);
 
 // Enqueue a kernel writing `bytes` zero bytes at `ptr` (a multiple of 4, ptr
 // 4-byte aligned): a fill a graph capture may record.

@@ -1917,6 +1917,26 @@ __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
   }
 }
 
+// The TV passes of a batch too large for its statistics workgroups to take
+// them: grid (nt, R), after the statistics kernel (every TV row is merged).
+// Workgroup (k, r) of a TV row (OPT / OPTLOG at T > 0) sums the TV partials
+// of tile k (wavefront w its slice w, the logits read non-temporally: this
+// is their last read); the last of the row's slices decides the row, and a
+// sequence that decision finishes is drawn by the draw pass that follows.
+// Other rows' workgroups leave at once.
+template <int DT, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_tvpass(Params P) {
+  const int k = blockIdx.x, r = blockIdx.y;
+  const SeqParam sp = seq_param(P, r / (P.gamma + 1));
+  if (!(sp.valid && !sp.greedy && has_tv_parts(sp.rule))) return;  // block-uniform
+  pass2_slice_w<DT, VEC, false>(P, r, k, threadIdx.x >> 6, sp);
+  vmem_drain();
+  __syncthreads();  // all four slices are stored
+  if (threadIdx.x < 64 &&
+      arrive_last_w(row_word(P, r, kRowTvArrive), (uint32_t)(kSlices * P.nt), kSlices))
+    tv_row_done<DT>(P, r, 1);
+}
+
 // ---------------------------------------------------------------- job pass
 // Wave: the masses of the NS sub-chunks of the part at entry e0 of a row
 // under the distribution KIND; lane base + i returns sub-chunk i's (float
@@ -2230,7 +2250,7 @@ __global__ __launch_bounds__(kJobThreads) __attribute__((amdgpu_waves_per_eu(4))
 
 template <int DT, bool VEC>
 hipError_t launch_step_t(const Params& P, hipStream_t st, bool nt_loads, bool draw_pass,
-                         bool job_pass, bool draw_after, int job_groups,
+                         bool tv_pass, bool job_pass, bool draw_after, int job_groups,
                          hipEvent_t ev_begin, hipEvent_t ev_end) {
   const dim3 grid((unsigned)P.nt, (unsigned)(P.B * (P.gamma + 1))), block(kThreads);
   if (ev_begin) {
@@ -2264,16 +2284,20 @@ hipError_t launch_step_t(const Params& P, hipStream_t st, bool nt_loads, bool dr
     hipLaunchKernelGGL((k_res<DT, VEC>), dim3((unsigned)P.nt, (unsigned)P.B), block, 0, st, P);
     err = hipGetLastError();
   }
+  if (err == hipSuccess && tv_pass) {
+    hipLaunchKernelGGL((k_tvpass<DT, VEC>), grid, block, 0, st, P);
+    err = hipGetLastError();
+  }
   if (err == hipSuccess && job_pass) {
     Params Q = P;
     Q.phase = 1;
     hipLaunchKernelGGL((k_jobs<DT, VEC>), dim3((unsigned)job_groups), dim3(kJobThreads), 0, st,
                        Q);
     err = hipGetLastError();
-    if (err == hipSuccess && draw_after) {  // the draws of sequences the job pass finished
-      hipLaunchKernelGGL((k_res<DT, VEC>), dim3((unsigned)P.nt, (unsigned)P.B), block, 0, st, P);
-      err = hipGetLastError();
-    }
+  }
+  if (err == hipSuccess && draw_after) {  // the draws of sequences finished after k_res
+    hipLaunchKernelGGL((k_res<DT, VEC>), dim3((unsigned)P.nt, (unsigned)P.B), block, 0, st, P);
+    err = hipGetLastError();
   }
   return err;
 }
@@ -2973,17 +2997,17 @@ hipError_t launch_small(const Params& P, int dtype, bool vec, hipEvent_t ev_begi
 }
 
 hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, bool draw_pass,
-                       bool job_pass, bool draw_after, int job_groups, hipEvent_t ev_begin,
-                       hipEvent_t ev_end, hipStream_t st) {
+                       bool tv_pass, bool job_pass, bool draw_after, int job_groups,
+                       hipEvent_t ev_begin, hipEvent_t ev_end, hipStream_t st) {
   if (dtype == 1)
-    return vec ? launch_step_t<1, true>(P, st, nt_loads, draw_pass, job_pass, draw_after, job_groups,
-                                        ev_begin, ev_end)
-               : launch_step_t<1, false>(P, st, nt_loads, draw_pass, job_pass, draw_after, job_groups,
-                                         ev_begin, ev_end);
-  return vec ? launch_step_t<0, true>(P, st, nt_loads, draw_pass, job_pass, draw_after, job_groups,
-                                      ev_begin, ev_end)
-             : launch_step_t<0, false>(P, st, nt_loads, draw_pass, job_pass, draw_after, job_groups,
-                                       ev_begin, ev_end);
+    return vec ? launch_step_t<1, true>(P, st, nt_loads, draw_pass, tv_pass, job_pass, draw_after,
+                                        job_groups, ev_begin, ev_end)
+               : launch_step_t<1, false>(P, st, nt_loads, draw_pass, tv_pass, job_pass,
+                                         draw_after, job_groups, ev_begin, ev_end);
+  return vec ? launch_step_t<0, true>(P, st, nt_loads, draw_pass, tv_pass, job_pass, draw_after,
+                                      job_groups, ev_begin, ev_end)
+             : launch_step_t<0, false>(P, st, nt_loads, draw_pass, tv_pass, job_pass, draw_after,
+                                       job_groups, ev_begin, ev_end);
 }
 
 }  // namespace spc
