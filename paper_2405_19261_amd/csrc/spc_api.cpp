@@ -90,9 +90,7 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
   L.zero_end = o;
   // two job passes, each with at most R + B row jobs and 2 R + B + R nt
   // single jobs (argmax halves, draws, TV tiles handed back by the tiles)
-  L.jobs = o;
-  o = align_up(o + 8 * (size_t)(2 * ((R + B) + (2 * R + B + R * nt * kSlices))), 256);
-  L.jobline = o; o = align_up(o + 4 * (size_t)kLineWords * 2 * (R + B), 256);
+  L.jobs = o; o = align_up(o + 8 * (size_t)(2 * R + B + R * nt * kSlices), 256);
   L.tiles = o; o = align_up(o + sizeof(TilePart) * R * nt, 256);
   L.tvpart = o; o = align_up(o + sizeof(double) * R * nt * kSlices, 256);
   // residual sub-chunk masses per sequence, or (small path) two sets per row
@@ -124,10 +122,6 @@ uint32_t tv_wait_ticks() {
   const unsigned long v = strtoul(e, &end, 10);
   return (end && *end == '\0' && v <= 1000000ul) ? (uint32_t)v : 4000u;
 }
-
-// TV passes of large batches taken by later statistics workgroups (true) or
-// by a kernel of their own after the statistics kernel (false).
-constexpr bool kTvLag = false;
 
 spc_status check_shape(int32_t B, int32_t gamma, int32_t V) {
   if (B < 1 || gamma < 1 || gamma > SPC_MAX_GAMMA || V < 2)
@@ -369,41 +363,32 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
     P.out_stats = ex ? offset(ex->out_row_stats, b0 * g1 * 8) : nullptr;
     P.out_argmax = ex ? offset(ex->out_argmax, b0 * g1 * 2) : nullptr;
     P.out_norm = ex ? offset(ex->out_sample_norm, b0) : nullptr;
-    P.job_slots = R + bl;
     // Where TV rows get their TV pass.  In a grid that is resident at once
     // (at most two workgroups per compute unit) each TV row takes it from
     // its own tiles' registers once the row is merged (tv_self).  Otherwise
-    // a kernel of its own re-reads the TV rows after the statistics kernel
-    // (k_tvpass; the statistics tiles then read non-temporally), or, with
-    // kTvLag, statistics workgroups issued about 640 tiles later take it
-    // (lag rows; the last rows' passes go to the job pass).
+    // a kernel of its own reads the TV rows again after the statistics
+    // kernel (k_tvpass).
     P.tv_self = (tv_rows && R * nt <= 2 * (int64_t)cus) ? 1 : 0;
-    const bool tv_pass = tv_rows && !P.tv_self && !kTvLag;
-    P.lag = (tv_rows && !P.tv_self && kTvLag) ? (int32_t)std::max<int64_t>(1, (640 + nt - 1) / nt)
-                                              : 0;
-    const bool nt_loads = !tv_rows || tv_pass;
+    const bool tv_pass = tv_rows && !P.tv_self;
     // the job pass: argmax halves, eta slices, and the TV tiles whose wait
-    // for their row's merge timed out (tv_self, kTvLag)
-    const bool job_pass = may_greedy || (may_sample && (rules & kTok)) || (tv_rows && !tv_pass);
+    // for their row's merge timed out (tv_self)
+    const bool job_pass = may_greedy || (may_sample && (rules & kTok)) || P.tv_self;
     P.wait_ticks = tv_wait_ticks();
     // singles: argmax halves, draws, TV tiles whose wait timed out, the
     // slices of the tiles a token row lists for eta
     P.single_slots = 2 * R + bl + R * nt * spc::kSlices;
     P.nsub = (int32_t)(nt * spc::tile_subchunks(dtype, vec));
-    // workgroups of a job pass: a wavefront per item of its largest possible
-    // list, at most two workgroups per compute unit
+    // workgroups of the job pass: a wavefront per item of its largest
+    // expected list (eta slices of every tile, argmax halves), at most two
+    // workgroups per compute unit
     const int64_t np = nt * spc::kSlices;
-    // (TV passes taken by the rows' own tiles leave pass 1 only the eta
-    // passes of token rules)
-    const bool row_jobs1 = tv_rows && P.lag > 0;
-    const int64_t items1 = np * ((row_jobs1 || (rules & kTok)) ? R : 0) + (may_greedy ? 2 * R : 0);
+    const int64_t items1 = np * ((rules & kTok) ? R : 0) + (may_greedy ? 2 * R : 0);
     constexpr int64_t kW = spc::kJobThreads / 64;
     const int job_groups = (int)std::max<int64_t>(
         1, std::min<int64_t>((items1 + kW - 1) / kW, 2 * (int64_t)cus));
     P.hdr = reinterpret_cast<uint32_t*>(ws + L.hdr);
     P.rowline = reinterpret_cast<uint32_t*>(ws + L.rowline);
     P.jobs = reinterpret_cast<uint64_t*>(ws + L.jobs);
-    P.jobline = reinterpret_cast<uint32_t*>(ws + L.jobline);
     P.tiles = reinterpret_cast<spc::TilePart*>(ws + L.tiles);
     P.tvpart = reinterpret_cast<double*>(ws + L.tvpart);
     P.submass = reinterpret_cast<double*>(ws + L.submass);
@@ -421,8 +406,8 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
       P.nsub = spc::kSmallSub;
       e = spc::launch_small(P, dtype, vec, ev0, ev1, stream);
     } else {
-      e = spc::launch_step(P, dtype, vec, nt_loads, draw_pass, tv_pass, job_pass, draw_after,
-                           job_groups, ev0, ev1, stream);
+      e = spc::launch_step(P, dtype, vec, draw_pass, tv_pass, job_pass, draw_after, job_groups,
+                           ev0, ev1, stream);
     }
     if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
   }

@@ -69,20 +69,16 @@ struct Params {
   int32_t* out_argmax;
   float* out_norm;
   // launch layout
-  int32_t phase;           // job pass of a k_jobs launch (1)
-  int64_t job_slots;       // row jobs a job pass may hold: R + B
-  int64_t single_slots;    // single jobs a job pass may hold: 2 R + B
+  int64_t single_slots;    // jobs the job pass may hold: 2 R + B + R nt kSlices
   int32_t nsub;            // sub-chunks of a row: nt * tile_subchunks
-  int32_t lag;             // TV rows r < R - lag get their TV pass from the tiles of row r + lag
-  int32_t tv_self;         // TV rows get their TV pass from their own tiles (lag 0)
+  int32_t tv_self;         // TV rows get their TV pass from their own tiles' registers
   uint32_t wait_ticks;     // bound of a wait for a TV row's merge (100 MHz clock ticks)
   // workspace: zero region (counters; every launch leaves it as it found it)
   uint32_t* hdr;           // [kHdrLines][kLineWords] job counters
   uint32_t* rowline;       // [kMaxRows][kLineWords] per-row and per-sequence counters
   uint32_t* samp_cnt;      // drafter kernel: per-row completion counters (kDraftCntStride)
   // workspace: data (written before it is read in every launch)
-  uint64_t* jobs;          // [2 passes][job_slots + single_slots] job entries
-  uint32_t* jobline;       // [2 passes][job_slots][kLineWords] row-job completion counters
+  uint64_t* jobs;          // [single_slots] job entries of the job pass
   TilePart* tiles;         // [R][nt] statistics partials
   double* tvpart;          // [R][nt][kSlices] TV partials (OPT) or eta partials (token rules)
   double* submass;         // [B][nsub] residual masses per sub-chunk of row j*
@@ -110,9 +106,10 @@ constexpr int kJobThreads = 512;
 // A statistics tile splits into kSlices slices, one per wavefront of its
 // workgroup (the unit of second-pass partials and residual jobs).
 constexpr int kSlices = kThreads / 64;
-// Header lines: row and single jobs published for pass 1 and pass 2, then per
-// pass kExitLeaves + 1 lines counting the workgroups that have read its counts
-// (a two-level tree; the last arrival clears the pass's counts).
+// Header lines: the count of jobs published for the job pass (line 1; lines
+// 0, 2 and 3 stay zero), then kExitLeaves + 1 lines counting the workgroups
+// of the pass that have read it (a two-level tree; the last arrival clears
+// the count).
 constexpr int kExitLeaves = 16;
 constexpr int kHdrExit = 4;
 constexpr int kHdrLines = kHdrExit + 2 * (kExitLeaves + 1);
@@ -134,7 +131,7 @@ constexpr int kDraftCntStride = kLineWords;
 // region (header lines, row lines) has the same size for every shape.
 struct WsLayout {
   size_t hdr, rowline, zero_end;
-  size_t jobs, jobline, tiles, tvpart, submass, moms, rowstat, rowdec, etalist, argres, etacnt,
+  size_t jobs, tiles, tvpart, submass, moms, rowstat, rowdec, etalist, argres, etacnt,
       total;
 };
 WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec);
@@ -154,16 +151,15 @@ int small_row_elems(int dtype, bool vec);
 hipError_t launch_small(const Params& P, int dtype, bool vec, hipEvent_t ev_begin,
                         hipEvent_t ev_end, hipStream_t stream);
 
-// Enqueue one verify launch: the statistics tiles (k_tiles), the draw pass
-// (k_res) when `draw_pass`, the TV passes (k_tvpass) when `tv_pass`, the job
-// pass (k_jobs, of `job_groups` workgroups) when `job_pass`, and with
+// Enqueue one verify launch: the statistics tiles (k_tiles; with P.tv_self
+// they also take their rows' TV passes), the draw pass (k_res) when
+// `draw_pass`, the TV pass kernel (k_tvpass) when `tv_pass`, the job pass
+// (k_jobs, of `job_groups` workgroups) when `job_pass`, and with
 // `draw_after` a second draw pass for the sequences finished after the first.
-// nt_loads: the tiles read the logits non-temporally (no later workgroup of
-// k_tiles reads a row again).
 // ev_begin / ev_end (may be null): recorded right before and after k_tiles.
-hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, bool draw_pass,
-                       bool tv_pass, bool job_pass, bool draw_after, int job_groups,
-                       hipEvent_t ev_begin, hipEvent_t ev_end, hipStream_t stream);
+hipError_t launch_step(const Params& P, int dtype, bool vec, bool draw_pass, bool tv_pass,
+                       bool job_pass, bool draw_after, int job_groups, hipEvent_t ev_begin,
+                       hipEvent_t ev_end, hipStream_t stream);
 
 // Enqueue a kernel writing `bytes` zero bytes at `ptr` (a multiple of 4, ptr
 // 4-byte aligned): a fill a graph capture may record.

@@ -1489,8 +1489,7 @@ __device__ __forceinline__ void tv_slice_regs_w(
 // eta second pass over a row and the residual masses of row j* of a sequence
 // are "row jobs" of nt chunks (one per tile); the two halves of a greedy
 // row's argmax and the draws from statistics partials are single chunks.
-enum JobKind : int { kJobTv = 1, kJobEta = 2, kJobRes = 3, kJobArg = 4, kJobDraw = 5,
-                     kJobTvTile = 6 };
+enum JobKind : int { kJobTv = 1, kJobEta = 2, kJobArg = 4, kJobTvTile = 6 };
 
 // A job entry: kind (bits 60..63), an extra field (bits 32..59: the argmax
 // tensor, or a draw's sample kind and j*) and the row or sequence it belongs
@@ -1510,57 +1509,39 @@ __device__ __forceinline__ uint32_t* hdr_word(const Params& P, int line) {
   return P.hdr + (int64_t)line * kLineWords;
 }
 __device__ __forceinline__ int hdr_line(int phase, bool single) { return 2 * (phase - 1) + single; }
-// The job entries of a pass: its row jobs, then its single jobs.
-__device__ __forceinline__ uint64_t* job_list(const Params& P, int phase, bool single) {
-  return P.jobs + (int64_t)(phase - 1) * (P.job_slots + P.single_slots) +
-         (single ? P.job_slots : 0);
-}
+// The job entries of the job pass.
+__device__ __forceinline__ uint64_t* job_list(const Params& P) { return P.jobs; }
 __device__ __forceinline__ uint32_t* row_word(const Params& P, int64_t r, int w) {
   return P.rowline + r * kLineWords + w;
 }
 __device__ __forceinline__ uint64_t* seq_mask(const Params& P, int64_t b) {
   return reinterpret_cast<uint64_t*>(row_word(P, b, kSeqMask));
 }
-// The completion counter of row job `s` of a phase.
-__device__ __forceinline__ uint32_t* job_done(const Params& P, int phase, int64_t s) {
-  return P.jobline + ((int64_t)(phase - 1) * P.job_slots + s) * kLineWords;
-}
 __device__ __forceinline__ uint64_t lane_u64(uint64_t v, int l) {
   return ((uint64_t)(uint32_t)lane_i32((int)(v >> 32), l) << 32) |
          (uint64_t)(uint32_t)lane_i32((int)(uint32_t)v, l);
 }
 
-// One lane: publish a row job (whose inputs are stored) and initialise its
-// completion counter; the job pass that reads them is a later launch.  A
-// pass never holds more jobs than its lists have slots (at most one TV or
-// eta job per row and one draw per sequence); the bounds only keep a broken
-// count from writing past them.
-__device__ __forceinline__ void publish_row_job(const Params& P, int phase, int kind,
-                                                uint32_t id, uint32_t extra = 0u) {
-  if (phase > 2) return;
-  const uint32_t s = add_u32(hdr_word(P, hdr_line(phase, false)), 1u);
-  if ((int64_t)s >= P.job_slots) return;
-  st_u32(job_done(P, phase, s), 0u);
-  st_u64(job_list(P, phase, false) + s, job_entry(kind, extra, id));
-}
-__device__ __forceinline__ void publish_single(const Params& P, int phase, int kind,
-                                               uint32_t extra, uint32_t id) {
-  if (phase > 2) return;
-  const uint32_t s = add_u32(hdr_word(P, hdr_line(phase, true)), 1u);
+// Publish a job (whose inputs are stored) for the job pass, a later launch.
+// The pass never holds more jobs than its list has slots; the bound only
+// keeps a broken count from writing past it.
+__device__ __forceinline__ void publish_single(const Params& P, int kind, uint32_t extra,
+                                               uint32_t id) {
+  const uint32_t s = add_u32(hdr_word(P, hdr_line(1, true)), 1u);
   if ((int64_t)s >= P.single_slots) return;
-  st_u64(job_list(P, phase, true) + s, job_entry(kind, extra, id));
+  st_u64(job_list(P) + s, job_entry(kind, extra, id));
 }
-// Wave: n single jobs (kind, extra = 0 .. n-1, id), one reservation.
-__device__ __forceinline__ void publish_singles_w(const Params& P, int phase, int kind,
-                                                  uint32_t id, uint32_t n) {
-  if (phase > 2 || n == 0u) return;
+// Wave: n jobs (kind, extra = 0 .. n-1, id), one reservation.
+__device__ __forceinline__ void publish_singles_w(const Params& P, int kind, uint32_t id,
+                                                  uint32_t n) {
+  if (n == 0u) return;
   const int lane = threadIdx.x & 63;
   uint32_t s0 = 0;
-  if (lane == 0) s0 = add_u32(hdr_word(P, hdr_line(phase, true)), n);
+  if (lane == 0) s0 = add_u32(hdr_word(P, hdr_line(1, true)), n);
   s0 = (uint32_t)lane_i32((int)s0, 0);
   for (uint32_t x = (uint32_t)lane; x < n; x += 64u) {
     if ((int64_t)s0 + x >= P.single_slots) break;
-    st_u64(job_list(P, phase, true) + s0 + x, job_entry(kind, x, id));
+    st_u64(job_list(P) + s0 + x, job_entry(kind, x, id));
   }
 }
 
@@ -1705,22 +1686,18 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
       st_rowstat(P.rowstat + r, rs);
       st_i32(P.argres + (int64_t)r * 4 + 0, kq);
       st_i32(P.argres + (int64_t)r * 4 + 1, kp);
-      publish_single(P, 1, kJobArg, 0u, (uint32_t)r);
-      publish_single(P, 1, kJobArg, 1u, (uint32_t)r);
+      publish_single(P, kJobArg, 0u, (uint32_t)r);
+      publish_single(P, kJobArg, 1u, (uint32_t)r);
     }
     return;
   }
   if (sp.valid && has_tv_parts(sp.rule)) {
     if (lane == 0) {
+      // the row is merged: its TV pass may start (the row's own statistics
+      // workgroups in a resident grid, else the TV pass kernel)
       st_rowstat(P.rowstat + r, rs);
-      if (r < P.B * (P.gamma + 1) - P.lag) {
-        // the statistics workgroups of row r + lag take its TV pass, one
-        // tile each, once they see the row merged
-        vmem_drain();
-        st_u32(row_word(P, r, kRowReady), 1u);
-      } else {
-        publish_row_job(P, 1, kJobTv, (uint32_t)r);
-      }
+      vmem_drain();
+      st_u32(row_word(P, r, kRowReady), 1u);
     }
     return;
   }
@@ -1758,7 +1735,7 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
         st_i32(P.etacnt + r, (int32_t)count);
       }
       // a single job per slice of every listed tile (job pass 1)
-      publish_singles_w(P, 1, kJobEta, (uint32_t)r, count * (uint32_t)kSlices);
+      publish_singles_w(P, kJobEta, (uint32_t)r, count * (uint32_t)kSlices);
       return;
     }
     rs.tv = wave_sum(eta);
@@ -1770,7 +1747,7 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
 // Wave: the row's decision once its TV, eta or argmax is known; when it
 // settles j*, the sequence's finish publishes to the next job pass.
 template <int DT>
-__device__ __forceinline__ void row_job_decide(const Params& P, int kind, int r, int phase) {
+__device__ __forceinline__ void row_job_decide(const Params& P, int kind, int r) {
   const int g1 = P.gamma + 1, np = P.nt * kSlices;
   const int b = r / g1, j = r - b * g1;
   RowStat rs = ld_rowstat(P.rowstat + r);
@@ -1797,8 +1774,8 @@ __device__ __forceinline__ void row_job_decide(const Params& P, int kind, int r,
 // the sequence's finish, publishing to job pass 1), then the row's ready
 // flag is cleared for the next call.
 template <int DT>
-__device__ __forceinline__ void tv_row_done(const Params& P, int rv, int phase) {
-  row_job_decide<DT>(P, kJobTv, rv, phase);
+__device__ __forceinline__ void tv_row_done(const Params& P, int rv) {
+  row_job_decide<DT>(P, kJobTv, rv);
   if ((threadIdx.x & 63) == 0) st_u32(row_word(P, rv, kRowReady), 0u);
 }
 
@@ -1814,29 +1791,12 @@ __device__ __forceinline__ bool tv_wait_ready(const Params& P, int rv, int k, Sh
       f = ld_u32(flag);
     }
     sh.flag = f != 0u;
-    if (f == 0u) publish_single(P, 1, kJobTvTile, (uint32_t)k, (uint32_t)rv);
+    if (f == 0u) publish_single(P, kJobTvTile, (uint32_t)k, (uint32_t)rv);
   }
   __syncthreads();
   return sh.flag != 0;
 }
 
-// Whole block: the TV pass over tile k of row rv, whose statistics tiles
-// were issued lag rows before this workgroup's.  Once the row's merge has set
-// its ready flag, wavefront w computes slice w; the workgroup then arrives
-// with all four, and the last arrival decides the row.  The workgroups of row
-// rv were all dispatched before this one, so the wait depends only on
-// workgroups that are running or done.
-template <int DT, bool VEC>
-__device__ __forceinline__ void tv_steal(const Params& P, int rv, int k, const SeqParam& spv,
-                                         Shared& sh) {
-  if (!tv_wait_ready(P, rv, k, sh)) return;  // block-uniform: the job pass takes the tile
-  pass2_slice_w<DT, VEC, false>(P, rv, k, threadIdx.x >> 6, spv);
-  vmem_drain();
-  __syncthreads();  // all four slices are stored
-  if (threadIdx.x < 64 &&
-      arrive_last_w(row_word(P, rv, kRowTvArrive), (uint32_t)(kSlices * P.nt), kSlices))
-    tv_row_done<DT>(P, rv, 0);
-}
 
 // Whole block: the TV pass over tile k of the block's own row r from the
 // registers that hold the tile (small batches: every tile of the grid is
@@ -1854,38 +1814,28 @@ __device__ __forceinline__ void tv_self(
   __syncthreads();  // all four slices are stored
   if (threadIdx.x < 64 &&
       arrive_last_w(row_word(P, r, kRowTvArrive), (uint32_t)(kSlices * P.nt), kSlices))
-    tv_row_done<DT>(P, r, 0);
+    tv_row_done<DT>(P, r);
 }
 
 // How the statistics tiles serve the TV pass (OPT / OPTLOG rows at T > 0):
-// not at all (no TV row: the logits are read non-temporally), by taking
-// tile k of row r - lag after their own (tv_steal, reading through the
-// caches), or on their own row from registers (tv_self).
-enum TvMode : int { kTvNone = 0, kTvLag = 1, kTvSelf = 2 };
+// not at all (the TV pass kernel takes it, or there is no TV row), or, in a
+// grid resident at once, on their own row from registers (tv_self).
+enum TvMode : int { kTvNone = 0, kTvSelf = 2 };
 
-// The statistics tiles.  grid (nt, R): tile k of row r.  After the tile
-// partial wave 0 arrives on the row's counter, and the last tile of the row
-// merges and decides it (a TV row: publishes it as merged).  Then, by TVM,
-// the block takes its share of a TV pass; otherwise waves 1-3 leave after
-// the partial.
+// The statistics tiles.  grid (nt, R): tile k of row r, its logits read
+// non-temporally.  After the tile partial wave 0 arrives on the row's
+// counter, and the last tile of the row merges and decides it (a TV row:
+// marks it merged).  With kTvSelf the block then takes its share of its own
+// row's TV pass; otherwise waves 1-3 leave after the partial.
 template <int DT, bool VEC, int MS, int TVM>
 __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
-  constexpr bool NT = TVM != kTvLag;  // no later block reads the row again
+  constexpr bool NT = true;
   using T = StatTile<DT, VEC>;
   __shared__ Shared sh;
   const int k = blockIdx.x, r = blockIdx.y;
   const int nt = P.nt, g1 = P.gamma + 1, V = P.V;
   const int b = r / g1, j = r - b * g1;
   const SeqParam sp = seq_param(P, b);
-  // the TV pass over tile k of row r - lag (OPT / OPTLOG at T > 0) is this
-  // workgroup's second job
-  const int rv = r - P.lag;
-  SeqParam spv = sp;
-  bool steal = false;
-  if (TVM == kTvLag && P.lag > 0 && rv >= 0) {
-    spv = seq_param(P, rv / g1);
-    steal = spv.valid && !spv.greedy && has_tv_parts(spv.rule);
-  }
   const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
   const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
   const int64_t t0 = (int64_t)k * T::N;
@@ -1909,9 +1859,6 @@ __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
       row_merged_w<DT, MS>(P, r, b, j, sp);
     }
   }
-  if constexpr (TVM == kTvLag) {
-    if (steal) tv_steal<DT, VEC>(P, rv, k, spv, sh);
-  }
   if constexpr (TVM == kTvSelf) {
     if (sp.valid && !sp.greedy && has_tv_parts(sp.rule)) tv_self<DT, VEC>(P, r, k, sp, sh, wq, wp);
   }
@@ -1934,7 +1881,7 @@ __global__ __launch_bounds__(kThreads) void k_tvpass(Params P) {
   __syncthreads();  // all four slices are stored
   if (threadIdx.x < 64 &&
       arrive_last_w(row_word(P, r, kRowTvArrive), (uint32_t)(kSlices * P.nt), kSlices))
-    tv_row_done<DT>(P, r, 1);
+    tv_row_done<DT>(P, r);
 }
 
 // ---------------------------------------------------------------- job pass
@@ -2196,69 +2143,53 @@ __device__ __forceinline__ void exit_tree(const Params& P, int phase) {
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kJobThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_jobs(
     Params P) {
-  __shared__ uint32_t counts[2];
-  const int phase = P.phase, nt = P.nt, g1 = P.gamma + 1;
+  __shared__ uint32_t count;
+  const int phase = 1, nt = P.nt, g1 = P.gamma + 1;
   if (threadIdx.x == 0) {
-    counts[0] = ld_u32(hdr_word(P, hdr_line(phase, false)));
-    counts[1] = ld_u32(hdr_word(P, hdr_line(phase, true)));
-    vmem_drain();  // both counts have arrived before this workgroup counts itself
+    count = ld_u32(hdr_word(P, hdr_line(phase, true)));
+    vmem_drain();  // the count has arrived before this workgroup counts itself
     exit_tree(P, phase);
   }
   __syncthreads();
-  const int64_t n_row = min((int64_t)counts[0], P.job_slots);
-  const int64_t n_single = min((int64_t)counts[1], P.single_slots);
-  const int np = nt * kSlices;
-  const int64_t n_row_items = n_row * np;
-  const int64_t n_items = n_row_items + n_single;
-  const uint64_t* rows = job_list(P, phase, false);
-  const uint64_t* singles = job_list(P, phase, true);
+  const int64_t n_items = min((int64_t)count, P.single_slots);
+  const uint64_t* singles = job_list(P);
   constexpr int kW = kJobThreads / 64;
   const int64_t W = (int64_t)gridDim.x * kW;
   for (int64_t g = (int64_t)blockIdx.x * kW + (threadIdx.x >> 6); g < n_items; g += W) {
-    if (g < n_row_items) {  // wave-uniform
-      const int64_t s = n_row - 1 - g / np;
-      const int c = (int)(g - (g / np) * np);
-      const uint64_t e = ld_u64(rows + s);
-      const int kind = job_kind(e);
-      const int id = (int)job_id(e);
-      pass2_item_w<DT, VEC, false>(P, id, c);  // the only row job: a TV pass
-      if (arrive_last_w(job_done(P, phase, s), (uint32_t)np)) row_job_decide<DT>(P, kind, id, phase);
-    } else {
-      const uint64_t e = ld_u64(singles + (g - n_row_items));
-      const int kind = job_kind(e);
-      const int id = (int)job_id(e);
-      if (kind == kJobTvTile) {
-        // a tile whose stealing workgroup gave up waiting: its four slices
-        const SeqParam spt = seq_param(P, id / g1);
+    const uint64_t e = ld_u64(singles + g);
+    const int kind = job_kind(e);
+    const int id = (int)job_id(e);
+    if (kind == kJobTvTile) {
+      // a tile whose wait for its row's merge timed out: its four slices
+      const SeqParam spt = seq_param(P, id / g1);
 #pragma unroll 1
-        for (int w = 0; w < kSlices; ++w)
-          pass2_slice_w<DT, VEC, false>(P, id, (int)job_extra(e), w, spt);
-        if (arrive_last_w(row_word(P, id, kRowTvArrive), (uint32_t)(kSlices * nt), kSlices))
-          tv_row_done<DT>(P, id, phase);
-      } else if (kind == kJobEta) {
-        // slice c % 4 of the (c / 4)-th listed tile of token row id
-        const uint32_t n = (uint32_t)ld_i32(P.etacnt + id) * (uint32_t)kSlices;
-        pass2_item_w<DT, VEC, true>(P, id, (int)job_extra(e));
-        if (arrive_last_w(row_word(P, id, kRowTvArrive), n)) row_job_decide<DT>(P, kind, id, phase);
-      } else {  // kJobArg
-        arg_half_w<DT, VEC>(P, id, (int)job_extra(e));
-        if (arrive_last_w(row_word(P, id, kRowJobDone), 2u)) row_job_decide<DT>(P, kind, id, phase);
-      }
+      for (int w = 0; w < kSlices; ++w)
+        pass2_slice_w<DT, VEC, false>(P, id, (int)job_extra(e), w, spt);
+      if (arrive_last_w(row_word(P, id, kRowTvArrive), (uint32_t)(kSlices * nt), kSlices))
+        tv_row_done<DT>(P, id);
+    } else if (kind == kJobEta) {
+      // slice c % 4 of the (c / 4)-th listed tile of token row id
+      const uint32_t n = (uint32_t)ld_i32(P.etacnt + id) * (uint32_t)kSlices;
+      pass2_item_w<DT, VEC, true>(P, id, (int)job_extra(e));
+      if (arrive_last_w(row_word(P, id, kRowTvArrive), n)) row_job_decide<DT>(P, kind, id);
+    } else {  // kJobArg
+      arg_half_w<DT, VEC>(P, id, (int)job_extra(e));
+      if (arrive_last_w(row_word(P, id, kRowJobDone), 2u)) row_job_decide<DT>(P, kind, id);
     }
   }
 }
 
 template <int DT, bool VEC>
-hipError_t launch_step_t(const Params& P, hipStream_t st, bool nt_loads, bool draw_pass,
-                         bool tv_pass, bool job_pass, bool draw_after, int job_groups,
-                         hipEvent_t ev_begin, hipEvent_t ev_end) {
+hipError_t launch_step_t(const Params& P, hipStream_t st, bool draw_pass, bool tv_pass,
+                         bool job_pass, bool draw_after, int job_groups, hipEvent_t ev_begin,
+                         hipEvent_t ev_end) {
   const dim3 grid((unsigned)P.nt, (unsigned)(P.B * (P.gamma + 1))), block(kThreads);
   if (ev_begin) {
     const hipError_t e = hipEventRecord(ev_begin, st);
     if (e != hipSuccess) return e;
   }
   constexpr int kAll = kMomX | kMomHQ | kMomHP;
-  if (nt_loads) {
+  if (!P.tv_self) {
     if (P.mom_set == 0)
       hipLaunchKernelGGL((k_tiles<DT, VEC, 0, kTvNone>), grid, block, 0, st, P);
     else if (P.mom_set == kMomX)
@@ -2267,16 +2198,11 @@ hipError_t launch_step_t(const Params& P, hipStream_t st, bool nt_loads, bool dr
       hipLaunchKernelGGL((k_tiles<DT, VEC, kMomHQ, kTvNone>), grid, block, 0, st, P);
     else
       hipLaunchKernelGGL((k_tiles<DT, VEC, kAll, kTvNone>), grid, block, 0, st, P);
-  } else if (P.tv_self) {
+  } else {
     if (P.mom_set == 0)
       hipLaunchKernelGGL((k_tiles<DT, VEC, 0, kTvSelf>), grid, block, 0, st, P);
     else
       hipLaunchKernelGGL((k_tiles<DT, VEC, kAll, kTvSelf>), grid, block, 0, st, P);
-  } else {
-    if (P.mom_set == 0)
-      hipLaunchKernelGGL((k_tiles<DT, VEC, 0, kTvLag>), grid, block, 0, st, P);
-    else
-      hipLaunchKernelGGL((k_tiles<DT, VEC, kAll, kTvLag>), grid, block, 0, st, P);
   }
   hipError_t err = hipGetLastError();
   if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, st);
@@ -2289,10 +2215,8 @@ hipError_t launch_step_t(const Params& P, hipStream_t st, bool nt_loads, bool dr
     err = hipGetLastError();
   }
   if (err == hipSuccess && job_pass) {
-    Params Q = P;
-    Q.phase = 1;
     hipLaunchKernelGGL((k_jobs<DT, VEC>), dim3((unsigned)job_groups), dim3(kJobThreads), 0, st,
-                       Q);
+                       P);
     err = hipGetLastError();
   }
   if (err == hipSuccess && draw_after) {  // the draws of sequences finished after k_res
@@ -2996,18 +2920,18 @@ hipError_t launch_small(const Params& P, int dtype, bool vec, hipEvent_t ev_begi
              : launch_small_t<0, false>(P, st, ev_begin, ev_end);
 }
 
-hipError_t launch_step(const Params& P, int dtype, bool vec, bool nt_loads, bool draw_pass,
-                       bool tv_pass, bool job_pass, bool draw_after, int job_groups,
-                       hipEvent_t ev_begin, hipEvent_t ev_end, hipStream_t st) {
+hipError_t launch_step(const Params& P, int dtype, bool vec, bool draw_pass, bool tv_pass,
+                       bool job_pass, bool draw_after, int job_groups, hipEvent_t ev_begin,
+                       hipEvent_t ev_end, hipStream_t st) {
   if (dtype == 1)
-    return vec ? launch_step_t<1, true>(P, st, nt_loads, draw_pass, tv_pass, job_pass, draw_after,
+    return vec ? launch_step_t<1, true>(P, st, draw_pass, tv_pass, job_pass, draw_after,
                                         job_groups, ev_begin, ev_end)
-               : launch_step_t<1, false>(P, st, nt_loads, draw_pass, tv_pass, job_pass,
-                                         draw_after, job_groups, ev_begin, ev_end);
-  return vec ? launch_step_t<0, true>(P, st, nt_loads, draw_pass, tv_pass, job_pass, draw_after,
-                                      job_groups, ev_begin, ev_end)
-             : launch_step_t<0, false>(P, st, nt_loads, draw_pass, tv_pass, job_pass, draw_after,
-                                       job_groups, ev_begin, ev_end);
+               : launch_step_t<1, false>(P, st, draw_pass, tv_pass, job_pass, draw_after,
+                                         job_groups, ev_begin, ev_end);
+  return vec ? launch_step_t<0, true>(P, st, draw_pass, tv_pass, job_pass, draw_after, job_groups,
+                                      ev_begin, ev_end)
+             : launch_step_t<0, false>(P, st, draw_pass, tv_pass, job_pass, draw_after, job_groups,
+                                       ev_begin, ev_end);
 }
 
 }  // namespace spc

@@ -76,9 +76,10 @@ def test_workload5_parity(part):
 def test_tv_wait_timeout_takes_the_job_pass(cfg, monkeypatch):
     """A statistics workgroup's wait for a TV row's merge is bounded; with the
     bound at 0 ticks every wait that does not find the row merged gives up at
-    once and the job pass takes the tile.  The T5 shape takes its TV passes
-    from the rows' own tiles, the Gemma shape from tiles of later rows; both
-    must still match the oracle."""
+    once and the job pass takes the tile.  The T5 shape (a resident grid)
+    takes its TV passes from the rows' own tiles and so waits; the Gemma
+    shape takes them in the TV pass kernel and never waits.  Both must match
+    the oracle."""
     monkeypatch.setenv("SPC_TV_WAIT_TICKS", "0")
     wl = W.WORKLOADS[cfg].with_(B=8, rule=W.OPT, alpha=0.1, temperature=1.0)
     _flush(f"[parity] tv wait 0: cfg{cfg} OPT B=8")
