@@ -1559,7 +1559,8 @@ struct StepShared {
 // the draw pass (k_res) that follows the launch finishing the sequence: the
 // statistics kernel's, or the job pass's.
 template <int DT>
-__device__ __forceinline__ void seq_finish_w(const Params& P, int b, int f, const SeqParam& sp) {
+__device__ __forceinline__ void seq_finish_w(const Params& P, int b, int f, const SeqParam& sp,
+                                             int rec) {
   const int gamma = P.gamma, g1 = gamma + 1;
   const int64_t row = (int64_t)b * g1 + f;
   if ((threadIdx.x & 63) != 0) return;
@@ -1570,7 +1571,7 @@ __device__ __forceinline__ void seq_finish_w(const Params& P, int b, int f, cons
     return;
   }
   P.out_accept[b] = f;
-  const int dstar = (ld_i32(P.rowdec + row) >> 1) & 1;
+  const int dstar = (rec >> 1) & 1;
   if (sp.greedy) {
     const RowStat rs = ld_rowstat(P.rowstat + row);
     P.out_token[b] = (dstar || sp.rule == SPC_RULE_LOSSY) ? rs.amax_p : rs.amax_q;
@@ -1622,25 +1623,48 @@ __device__ __forceinline__ void row_record(const Params& P, int r, const SeqPara
 // sequence's decided-row mask.  Returns j* when this decision completes the
 // prefix of decided rows 0 .. j* (j* the first rejection; row gamma always
 // rejects), else -1; every lane returns the same value.
+// The inputs of a sampled row's decision besides its statistics: the draft
+// token, its logits and the row's uniform.
+struct DraftIn {
+  int x;
+  float zqx, zpx, u;
+};
+
+// The draft token of row r = (b, j); -1 at the bonus position.
+__device__ __forceinline__ int draft_token(const Params& P, int b, int j) {
+  return j < P.gamma ? P.draft[(int64_t)b * P.gamma + j] : -1;
+}
+
+// Wave: the draft inputs of row r with draft token x (logits only for an
+// in-range draft of a sampled row).
+template <int DT>
+__device__ __forceinline__ DraftIn draft_in(const Params& P, int r, int x, const SeqParam& sp) {
+  DraftIn in{x, 0.0f, 0.0f, 0.0f};
+  if (sp.valid && !sp.greedy) {
+    in.u = P.uniforms[r];
+    if (in.x >= 0 && in.x < P.V) {
+      in.zqx = load_logit<DT>(P.q, r, P.V, in.x);
+      in.zpx = load_logit<DT>(P.p, r, P.V, in.x);
+    }
+  }
+  return in;
+}
+
 template <int DT>
 __device__ __forceinline__ int row_decide_w(const Params& P, int r, int b, int j,
-                                            const SeqParam& sp, const RowStat& rs) {
+                                            const SeqParam& sp, const RowStat& rs,
+                                            const DraftIn* pre, int* rec_f) {
   const int gamma = P.gamma, g1 = gamma + 1, V = P.V;
   const int lane = threadIdx.x & 63;
   RowDecision d{};
   if (sp.valid) {
-    int x = -1;
-    float zqx = 0.0f, zpx = 0.0f, u = 0.0f;
-    if (j < gamma) x = P.draft[(int64_t)b * gamma + j];
-    if (!sp.greedy) {
-      u = P.uniforms[r];
-      if (x >= 0 && x < V) {
-        zqx = load_logit<DT>(P.q, r, V, x);
-        zpx = load_logit<DT>(P.p, r, V, x);
-      }
-    } else if (((is_token(sp.rule) && sp.rule != SPC_RULE_TOKEN_V1) ||
-                sp.rule == SPC_RULE_BILD) &&
-               rs.amax_q >= 0 && rs.amax_q < V) {
+    const DraftIn in = pre ? *pre : draft_in<DT>(P, r, draft_token(P, b, j), sp);
+    const int x = in.x;
+    float zqx = in.zqx, zpx = in.zpx;
+    const float u = in.u;
+    if (sp.greedy &&
+        ((is_token(sp.rule) && sp.rule != SPC_RULE_TOKEN_V1) || sp.rule == SPC_RULE_BILD) &&
+        rs.amax_q >= 0 && rs.amax_q < V) {
       // greedy TokenV2/V3 and BiLD* read p at the drafter's argmax
       zpx = load_logit<DT>(P.p, r, V, rs.amax_q);
     }
@@ -1662,10 +1686,11 @@ __device__ __forceinline__ int row_decide_w(const Params& P, int r, int b, int j
   // rows 0 .. p_now - 1 are decided (their records were stored before their
   // bits were set); the first rejection among them, if it lies in the rows
   // this decision added to the prefix, is j*
-  const int kp = lane < p_now ? (ld_i32(P.rowdec + (int64_t)b * g1 + lane) & 1) : 1;
-  const unsigned long long rej = __ballot(!kp);
+  const int rec = lane < p_now ? ld_i32(P.rowdec + (int64_t)b * g1 + lane) : 1;
+  const unsigned long long rej = __ballot(!(rec & 1));
   if (!rej) return -1;
   const int f = __ffsll(rej) - 1;
+  *rec_f = lane_i32(rec, f);
   return f >= p_old ? f : -1;
 }
 
@@ -1675,9 +1700,11 @@ __device__ __forceinline__ int row_decide_w(const Params& P, int r, int b, int j
 // j*, finish the sequence.
 template <int DT, int MS>
 __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int j,
-                                             const SeqParam& sp) {
+                                             const SeqParam& sp, int x) {
   const int lane = threadIdx.x & 63;
   const int nt = P.nt;
+  // the decision's draft inputs, requested together with the tile partials
+  const DraftIn in = draft_in<DT>(P, r, x, sp);
   int kq, kp;
   RowStat rs = merge_row(P, r, (MS != 0 && needs_mom(sp)) ? sp.rule : 0, &kq, &kp);
   if (sp.valid && sp.greedy) {
@@ -1740,8 +1767,9 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
     }
     rs.tv = wave_sum(eta);
   }
-  const int f = row_decide_w<DT>(P, r, b, j, sp, rs);
-  if (f >= 0) seq_finish_w<DT>(P, b, f, sp);
+  int rec = 0;
+  const int f = row_decide_w<DT>(P, r, b, j, sp, rs, &in, &rec);
+  if (f >= 0) seq_finish_w<DT>(P, b, f, sp, rec);
 }
 
 // Wave: the row's decision once its TV, eta or argmax is known; when it
@@ -1762,8 +1790,9 @@ __device__ __forceinline__ void row_job_decide(const Params& P, int kind, int r)
     rs.tv = wave_sum(s);
   }
   const SeqParam sp = seq_param(P, b);
-  const int f = row_decide_w<DT>(P, r, b, j, sp, rs);
-  if (f >= 0) seq_finish_w<DT>(P, b, f, sp);
+  int rec = 0;
+  const int f = row_decide_w<DT>(P, r, b, j, sp, rs, nullptr, &rec);
+  if (f >= 0) seq_finish_w<DT>(P, b, f, sp, rec);
 }
 
 // The wait of a workgroup for a TV row's merge is bounded by P.wait_ticks of
@@ -1836,6 +1865,8 @@ __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
   const int nt = P.nt, g1 = P.gamma + 1, V = P.V;
   const int b = r / g1, j = r - b * g1;
   const SeqParam sp = seq_param(P, b);
+  // the row's draft token, for the decision should this be its last tile
+  const int x = draft_token(P, b, j);
   const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
   const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
   const int64_t t0 = (int64_t)k * T::N;
@@ -1856,7 +1887,7 @@ __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
     }
     if ((uint32_t)lane_i32((int)prev, 0) == (uint32_t)nt - 1u) {
       vmem_drain();
-      row_merged_w<DT, MS>(P, r, b, j, sp);
+      row_merged_w<DT, MS>(P, r, b, j, sp, x);
     }
   }
   if constexpr (TVM == kTvSelf) {
