@@ -313,21 +313,16 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
                                       ((rules & ((1u << SPC_RULE_DIFFLOG) | (1u << SPC_RULE_OPTLOG)))
                                            ? spc::kMomHQ | spc::kMomHP
                                            : 0);
-  // What the job pass may hold.  Rows of OPT / OPTLOG or a token rule at
-  // T > 0 may be decided in the job pass (after their TV or eta pass), so
-  // their draws fall to a second draw pass after it; every other row is
-  // decided by its last statistics tile, or (T = 0) after its argmax in the
-  // job pass.
+  // Rows of OPT / OPTLOG at T > 0 are decided after their TV pass, rows of
+  // a token rule after their eta pass (the job pass, for the tiles their
+  // statistics leave open), greedy rows after their argmax (the job pass);
+  // every other row by its last statistics tile.
   constexpr uint32_t kTok = (1u << SPC_RULE_TOKEN_V1) | (1u << SPC_RULE_TOKEN_V2) |
                             (1u << SPC_RULE_TOKEN_V3);
-  const bool pass2_rows = may_sample && (rules & (kTv | kTok));
   const bool may_greedy = force_greedy || per_temp;
-  // Sequences the statistics kernel finishes are drawn by the draw pass;
-  // the job pass takes TV and eta passes and argmax halves; the sequences it
-  // finishes are drawn by a second draw pass (greedy ones write their token
-  // directly).
+  // Every sequence with a draw is drawn by the draw pass, the last kernel of
+  // a launch (greedy ones write their token directly).
   const bool draw_pass = may_sample;
-  const bool draw_after = pass2_rows;
   const bool tv_rows = may_sample && (rules & kTv);
   // Small problems (rows that fit one workgroup's registers, at most two
   // rows per compute unit, no first moments) take the single-launch path.
@@ -406,8 +401,8 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
       P.nsub = spc::kSmallSub;
       e = spc::launch_small(P, dtype, vec, ev0, ev1, stream);
     } else {
-      e = spc::launch_step(P, dtype, vec, draw_pass, tv_pass, job_pass, draw_after, job_groups,
-                           ev0, ev1, stream);
+      e = spc::launch_step(P, dtype, vec, draw_pass, tv_pass, job_pass, job_groups, ev0, ev1,
+                           stream);
     }
     if (e != hipSuccess) return fail(SPC_E_HIP, "kernel launch: %s", hipGetErrorString(e));
   }

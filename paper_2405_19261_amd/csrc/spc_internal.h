@@ -152,14 +152,13 @@ hipError_t launch_small(const Params& P, int dtype, bool vec, hipEvent_t ev_begi
                         hipEvent_t ev_end, hipStream_t stream);
 
 // Enqueue one verify launch: the statistics tiles (k_tiles; with P.tv_self
-// they also take their rows' TV passes), the draw pass (k_res) when
-// `draw_pass`, the TV pass kernel (k_tvpass) when `tv_pass`, the job pass
-// (k_jobs, of `job_groups` workgroups) when `job_pass`, and with
-// `draw_after` a second draw pass for the sequences finished after the first.
+// they also take their rows' TV passes), the TV pass kernel (k_tvpass) when
+// `tv_pass`, the job pass (k_jobs, of `job_groups` workgroups) when
+// `job_pass`, and last the draw pass (k_res) when `draw_pass`.
 // ev_begin / ev_end (may be null): recorded right before and after k_tiles.
 hipError_t launch_step(const Params& P, int dtype, bool vec, bool draw_pass, bool tv_pass,
-                       bool job_pass, bool draw_after, int job_groups, hipEvent_t ev_begin,
-                       hipEvent_t ev_end, hipStream_t stream);
+                       bool job_pass, int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end,
+                       hipStream_t stream);
 
 // Enqueue a kernel writing `bytes` zero bytes at `ptr` (a multiple of 4, ptr
 // 4-byte aligned): a fill a graph capture may record.

@@ -2099,13 +2099,13 @@ __device__ __forceinline__ void res_slice_w(const Params& P, int b, int c, int f
 
 
 // ---------------------------------------------------------------- draw pass
-// k_res: grid (nt, B), after the statistics kernel.  For a sequence that
-// kernel finished with a residual draw, workgroup (k, b) sums the residual
-// masses of the sub-chunks of tile k of row j* (wavefront w its slice w);
-// the last of the sequence's workgroups to arrive draws.  A draw from the
-// statistics partials is made by workgroup (0, b).  The last arrival clears
-// the sequence's outcome word for the next call.  Sequences finished
-// elsewhere (later passes) have no outcome here and are skipped.
+// k_res: grid (nt, B), the step's last kernel.  For a sequence finished with
+// a residual draw, workgroup (k, b) sums the residual masses of the
+// sub-chunks of tile k of row j* (wavefront w its slice w); the last of the
+// sequence's workgroups to arrive draws.  A draw from the statistics
+// partials is made by workgroup (0, b).  The last arrival clears the
+// sequence's outcome word for the next call.  Sequences without a draw
+// (greedy or invalid) have no outcome word and are skipped.
 // bfloat16: held to four resident workgroups per SIMD (a Gemma-vocabulary
 // batch of 32 sequences is 1024 workgroups: one round on 256 CUs); the draw
 // code would otherwise take one VGPR too many for it.
@@ -2212,8 +2212,7 @@ __global__ __launch_bounds__(kJobThreads) __attribute__((amdgpu_waves_per_eu(4))
 
 template <int DT, bool VEC>
 hipError_t launch_step_t(const Params& P, hipStream_t st, bool draw_pass, bool tv_pass,
-                         bool job_pass, bool draw_after, int job_groups, hipEvent_t ev_begin,
-                         hipEvent_t ev_end) {
+                         bool job_pass, int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end) {
   const dim3 grid((unsigned)P.nt, (unsigned)(P.B * (P.gamma + 1))), block(kThreads);
   if (ev_begin) {
     const hipError_t e = hipEventRecord(ev_begin, st);
@@ -2237,10 +2236,6 @@ hipError_t launch_step_t(const Params& P, hipStream_t st, bool draw_pass, bool t
   }
   hipError_t err = hipGetLastError();
   if (err == hipSuccess && ev_end) err = hipEventRecord(ev_end, st);
-  if (err == hipSuccess && draw_pass) {
-    hipLaunchKernelGGL((k_res<DT, VEC>), dim3((unsigned)P.nt, (unsigned)P.B), block, 0, st, P);
-    err = hipGetLastError();
-  }
   if (err == hipSuccess && tv_pass) {
     hipLaunchKernelGGL((k_tvpass<DT, VEC>), grid, block, 0, st, P);
     err = hipGetLastError();
@@ -2250,7 +2245,7 @@ hipError_t launch_step_t(const Params& P, hipStream_t st, bool draw_pass, bool t
                        P);
     err = hipGetLastError();
   }
-  if (err == hipSuccess && draw_after) {  // the draws of sequences finished after k_res
+  if (err == hipSuccess && draw_pass) {  // every sequence is finished by now
     hipLaunchKernelGGL((k_res<DT, VEC>), dim3((unsigned)P.nt, (unsigned)P.B), block, 0, st, P);
     err = hipGetLastError();
   }
@@ -2952,17 +2947,17 @@ hipError_t launch_small(const Params& P, int dtype, bool vec, hipEvent_t ev_begi
 }
 
 hipError_t launch_step(const Params& P, int dtype, bool vec, bool draw_pass, bool tv_pass,
-                       bool job_pass, bool draw_after, int job_groups, hipEvent_t ev_begin,
-                       hipEvent_t ev_end, hipStream_t st) {
+                       bool job_pass, int job_groups, hipEvent_t ev_begin, hipEvent_t ev_end,
+                       hipStream_t st) {
   if (dtype == 1)
-    return vec ? launch_step_t<1, true>(P, st, draw_pass, tv_pass, job_pass, draw_after,
-                                        job_groups, ev_begin, ev_end)
-               : launch_step_t<1, false>(P, st, draw_pass, tv_pass, job_pass, draw_after,
-                                         job_groups, ev_begin, ev_end);
-  return vec ? launch_step_t<0, true>(P, st, draw_pass, tv_pass, job_pass, draw_after, job_groups,
-                                      ev_begin, ev_end)
-             : launch_step_t<0, false>(P, st, draw_pass, tv_pass, job_pass, draw_after, job_groups,
-                                       ev_begin, ev_end);
+    return vec ? launch_step_t<1, true>(P, st, draw_pass, tv_pass, job_pass, job_groups, ev_begin,
+                                        ev_end)
+               : launch_step_t<1, false>(P, st, draw_pass, tv_pass, job_pass, job_groups,
+                                         ev_begin, ev_end);
+  return vec ? launch_step_t<0, true>(P, st, draw_pass, tv_pass, job_pass, job_groups, ev_begin,
+                                      ev_end)
+             : launch_step_t<0, false>(P, st, draw_pass, tv_pass, job_pass, job_groups, ev_begin,
+                                       ev_end);
 }
 
 }  // namespace spc
