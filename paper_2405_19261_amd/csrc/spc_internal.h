@@ -24,7 +24,8 @@ struct TilePart {
   double s_q, s_p;
   float r_q, r_p;
   float zmax_q, zmax_p;   // largest raw logit of the tile
-  int32_t amax_q, amax_p; // lowest row index attaining it (greedy batches), else -1
+  int32_t amax_q, amax_p; // statistics tiles: bit w set when slice w attains zmax;
+                          // drafter tiles: lowest row index attaining it, or -1
 };
 
 // First moments of one (row, stats tile) for the log-loss rules and BiLD*,
@@ -86,7 +87,8 @@ struct Params {
   RowStat* rowstat;        // [R] merged row statistics
   int32_t* rowdec;         // [R] bit 0 a_j, bit 1 delta_j
   int32_t* etalist;        // [R][nt] tiles whose eta share needs a second look
-  int32_t* argres;         // [R][4] first tile of the q / p maximum, then its lowest index
+  int32_t* argres;         // [R][4] first tile of the q / p maximum (k * 16 + its slice
+                           // mask), then the lowest index of the maximum
   int32_t* etacnt;         // [R] tiles listed in etalist
 };
 

@@ -727,7 +727,8 @@ __device__ __forceinline__ double log_stat(int rule, double lq2, double lp2, dou
 //   H(q) = ln 2 (log2 S_q - H_q / S_q),  H(p) = ln 2 (log2 S_p - H_p / S_p),
 //   D(q, p) = -sum q log p = ln 2 (log2 S_p - X / S_q),
 // each a sum of two non-negative terms.  kq / kp: the first tile whose
-// largest logit is the row's (it holds the lowest index of the row maximum).
+// largest logit is the row's (it holds the lowest index of the row maximum),
+// as k * 16 + the mask of the tile's slices that attain it.
 // Every lane returns the same RowStat.
 __device__ __forceinline__ RowStat merge_row(const Params& P, int r, int mrule, int* kq_out,
                                              int* kp_out) {
@@ -774,8 +775,17 @@ __device__ __forceinline__ RowStat merge_row(const Params& P, int r, int mrule, 
     add(ld_tile(tp + k), mrule ? ld_mom(mp + k) : TileMom{0.0, 0.0, 0.0}, k);
   sq = wave_sum(sq);
   sp = wave_sum(sp);
-  *kq_out = wave_min(kq);
-  *kp_out = wave_min(kp);
+  kq = wave_min(kq);
+  kp = wave_min(kp);
+  // with the slice masks of those tiles (statistics tiles record them)
+  const auto mask_of = [&](int k, bool pq) {
+    if (k >= nt) return 15;
+    if (k < 64) return lane_i32(pq ? t0.amax_p : t0.amax_q, k) & 15;
+    const TilePart tk = ld_tile(tp + k);
+    return (pq ? tk.amax_p : tk.amax_q) & 15;
+  };
+  *kq_out = kq < nt ? kq * 16 + mask_of(kq, false) : kq;
+  *kp_out = kp < nt ? kp * 16 + mask_of(kp, true) : kp;
   RowStat rs;
   const double lq2 = log2_acc(sq), lp2 = log2_acc(sp);
   rs.lz_q = (double)rq + lq2;
@@ -1300,8 +1310,15 @@ __device__ __forceinline__ void tile_partial(const Params& P, int r, int k, cons
     t.r_p = (Mp == kNegInf) ? kNegInf : Rp;
     t.zmax_q = Mq;
     t.zmax_p = Mp;
-    t.amax_q = -1;
-    t.amax_p = -1;
+    // the slices (waves) whose entries attain the tile maximum
+    int mq = 0, mp = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      mq |= (sh.m[w][0] == Mq) ? 1 << w : 0;
+      mp |= (sh.m[w][1] == Mp) ? 1 << w : 0;
+    }
+    t.amax_q = mq;
+    t.amax_p = mp;
     st_tile(P.tiles + (int64_t)r * P.nt + k, t);
     if constexpr (mom) {
       // the waves' moments against the tile references, in wave order
@@ -2037,39 +2054,42 @@ __device__ __forceinline__ void pass2_item_w(const Params& P, int r, int c) {
 }
 
 // Wave: half h of the argmax of greedy row r: the lowest index of the row
-// maximum of q (h = 0) or p (h = 1), in the first tile holding it.
+// maximum of q (h = 0) or p (h = 1), in the first tile holding it, read only
+// in the slices of that tile that attain it (usually one; a slice's lane
+// loads interleave with the other slices', so the minimum is taken over
+// every slice read).
 template <int DT, bool VEC>
 __device__ __forceinline__ void arg_half_w(const Params& P, int r, int h) {
-  using C = PartC<DT, VEC>;
-  constexpr int EB = StatTile<DT, VEC>::EB;
+  using T = StatTile<DT, VEC>;
   const int V = P.V;
-  int k = ld_i32(P.argres + (int64_t)r * 4 + h);
-  k = (k >= 0 && k < P.nt) ? k : 0;
+  const int lane = threadIdx.x & 63;
+  const int packed = ld_i32(P.argres + (int64_t)r * 4 + h);
+  int k = packed >> 4, mask = packed & 15;
+  if (packed < 0 || k >= P.nt) {  // a broken record: search the whole first tile
+    k = 0;
+    mask = 15;
+  }
+  if (mask == 0) mask = 15;
   const RowStat rs = ld_rowstat(P.rowstat + r);
   const float z = h ? rs.zmax_p : rs.zmax_q;
-  const char* row = (const char*)(h ? P.p : P.q) + (int64_t)r * V * EB;
+  const char* row = (const char*)(h ? P.p : P.q) + (int64_t)r * V * T::EB;
+  const int64_t t0 = (int64_t)k * T::N;
   int idx = 0x7fffffff;
 #pragma unroll 1
-  for (int part = 0; part < 2 && idx == 0x7fffffff; ++part) {  // wave-uniform
-    const int64_t e0 = (int64_t)k * StatTile<DT, VEC>::N + (int64_t)part * C::N;
-    ChunkRegs<C> w;
-    load_chunk<DT, VEC, C>(row, e0, V, w);
-    float g[C::U];
-    float m = kNegInf;
+  for (int w = 0; w < kSlices; ++w) {
+    if (!((mask >> w) & 1)) continue;  // wave-uniform
+    uint32_t c[T::U][T::NW];
+    load_tile<DT, VEC, T::U, true>(row, t0, V, c, w * 64 + lane);
 #pragma unroll
-    for (int i = 0; i < C::U; ++i) {
-      float a = kNegInf;
+    for (int i = T::U - 1; i >= 0; --i) {
+      const int base = (int)t0 + ((i * kSlices + w) * 64 + lane) * T::VW;
 #pragma unroll
-      for (int e = 0; e < C::VW; ++e) a = fmaxf(a, elem<DT, VEC>(w[i], e));
-      g[i] = a;
-      m = fmaxf(m, a);
+      for (int e = T::VW - 1; e >= 0; --e)
+        if (elem<DT, VEC>(c[i], e) == z && base + e < V) idx = min(idx, base + e);
     }
-    const int lane = threadIdx.x & 63;
-    int mine = (m == z) ? first_max_index<DT, VEC, C::U, 64>(w, g, z, (int)e0 + lane * C::VW)
-                        : 0x7fffffff;
-    idx = wave_min(mine);
   }
-  if ((threadIdx.x & 63) == 0) st_i32(P.argres + (int64_t)r * 4 + 2 + h, idx);
+  idx = wave_min(idx);
+  if (lane == 0) st_i32(P.argres + (int64_t)r * 4 + 2 + h, idx);
 }
 
 // Wave: item c = k * 4 + w of sequence b's residual job over row f (= j*),
