@@ -1635,11 +1635,6 @@ __device__ __forceinline__ void row_record(const Params& P, int r, const SeqPara
   st_i32(P.rowdec + r, (sp.valid ? d.keep | (d.delta << 1) : 0) | (extra << 4));
 }
 
-// Wave: decide row r = (b, j) from its statistics rs (delta_j by the rule,
-// a_j by the acceptance test), write its outputs and add it to the
-// sequence's decided-row mask.  Returns j* when this decision completes the
-// prefix of decided rows 0 .. j* (j* the first rejection; row gamma always
-// rejects), else -1; every lane returns the same value.
 // The inputs of a sampled row's decision besides its statistics: the draft
 // token, its logits and the row's uniform.
 struct DraftIn {
@@ -1667,6 +1662,16 @@ __device__ __forceinline__ DraftIn draft_in(const Params& P, int r, int x, const
   return in;
 }
 
+// Blocks of at most kPackRows rows of a sampled sequence carry their
+// decisions in the sequence's 64-bit mask word (three bits a row).
+constexpr int kPackRows = 21;
+
+// Wave: decide row r = (b, j) from its statistics rs (delta_j by the rule,
+// a_j by the acceptance test), write its outputs and add it to the
+// sequence's decided-row mask.  Returns j* when this decision completes the
+// prefix of decided rows 0 .. j* (j* the first rejection; row gamma always
+// rejects), else -1; every lane returns the same value.
+// rec_f: j*'s record (bit 0 a_j*, bit 1 delta_j*).
 template <int DT>
 __device__ __forceinline__ int row_decide_w(const Params& P, int r, int b, int j,
                                             const SeqParam& sp, const RowStat& rs,
@@ -1686,6 +1691,31 @@ __device__ __forceinline__ int row_decide_w(const Params& P, int r, int b, int j
       zpx = load_logit<DT>(P.p, r, V, rs.amax_q);
     }
     d = decide_row(sp, rs, j, gamma, V, x, zqx, zpx, u);
+  }
+  if (g1 <= kPackRows && !sp.greedy) {
+    // the decision travels in the mask word itself: bit j (row decided),
+    // bit kPackRows + j (a_j = 0), bit 2 kPackRows + j (delta_j); no row
+    // reads another's record, so none waits for its stores
+    // (an invalid sequence's rows reject, as their records say)
+    const uint64_t mine = (1ull << j) | ((uint64_t)!(sp.valid && d.keep) << (kPackRows + j)) |
+                          ((uint64_t)(sp.valid && d.delta) << (2 * kPackRows + j));
+    uint64_t old = 0;
+    if (lane == 0) {
+      row_record(P, r, sp, d, 0);
+      old = or_u64(seq_mask(P, b), mine);
+    }
+    old = lane_u64(old, 0);
+    const uint64_t rows = (1ull << g1) - 1ull;
+    const uint64_t now = old | mine;
+    if (lane == 0 && (now & rows) == rows) st_u64(seq_mask(P, b), 0ull);  // the last row resets it
+    const int p_old = __builtin_ctzll(~(old & rows));
+    const int p_now = __builtin_ctzll(~(now & rows));
+    if (p_now <= p_old) return -1;
+    const uint64_t rej = (now >> kPackRows) & ((1ull << p_now) - 1ull);
+    if (!rej) return -1;
+    const int f = __builtin_ctzll(rej);
+    *rec_f = (int)((now >> (2 * kPackRows + f)) & 1ull) << 1;  // a_f = 0, delta_f
+    return f >= p_old ? f : -1;
   }
   uint64_t old = 0;
   if (lane == 0) {

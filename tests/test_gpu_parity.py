@@ -215,8 +215,12 @@ def test_mixed_greedy_and_sampled_sequences():
         parity.compare(gs, o, hs, wl.dtype, greedy=gr)
 
 
-def test_invalid_per_sequence_values():
-    wl = W.WORKLOADS[3].with_(B=6, V=4000)
+@pytest.mark.parametrize("V", [4000, 40000])
+def test_invalid_per_sequence_values(V):
+    """Invalid per-sequence values (an unknown rule, a NaN alpha, a negative
+    temperature) report -1 for that sequence only, on the single-launch path
+    (V = 4000) and on the statistics-tile path (V = 40000)."""
+    wl = W.WORKLOADS[3].with_(B=6, V=V)
     inp = W.generate(wl, 0, DEV)
     inp["rule"][1] = 13
     inp["alpha"][2] = float("nan")
