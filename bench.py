@@ -16,8 +16,10 @@ Infinity Cache cannot serve a repeat.
 Prints one JSON line: verified positions/s (B*gamma per step) for the whole
 path, plus the statistics kernel's roofline (algorithmic logit bytes / its
 mean duration, from HIP events recorded around it on the launch stream on
-every EVERY-th step of the timed region -- an event pair costs a few
-microseconds of step time, so not every step carries one) and the fp64
+every EVERY-th step of the timed region, by default every 32nd -- the four
+event records of a sampled step cost about 10 us of GPU time, which at every
+4th step added 2.4 us to the mean step and at every 32nd adds about 0.3 us)
+and the fp64
 oracle's throughput on the host cores (reported baseline).  Step-time
 percentiles come from the spacing of those events (EVERY-step windows).
 
@@ -294,7 +296,7 @@ def main():
     ap.add_argument("--sets", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib-mb", type=int, default=0)
-    ap.add_argument("--event-every", type=int, default=4)
+    ap.add_argument("--event-every", type=int, default=32)
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--rule", default=None,
                     choices=["chow", "diff", "opt", "always", "never",
