@@ -364,6 +364,10 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
     // a kernel of its own reads the TV rows again after the statistics
     // kernel (k_tvpass).
     P.tv_self = (tv_rows && R * nt <= 2 * (int64_t)cus) ? 1 : 0;
+    // batches of at least 64 statistics tiles per compute unit stream two
+    // tiles per workgroup (without first moments): B = 32 at the Gemma
+    // vocabulary (32 per CU) is faster with one, B = 128 and 256 with two
+    P.pair = (!P.tv_self && mom_set == 0 && R * nt >= 64 * (int64_t)cus) ? 1 : 0;
     const bool tv_pass = tv_rows && !P.tv_self;
     // the job pass: argmax halves, eta slices, and the TV tiles whose wait
     // for their row's merge timed out (tv_self)

@@ -73,6 +73,7 @@ struct Params {
   int64_t single_slots;    // jobs the job pass may hold: 2 R + B + R nt kSlices
   int32_t nsub;            // sub-chunks of a row: nt * tile_subchunks
   int32_t tv_self;         // TV rows get their TV pass from their own tiles' registers
+  int32_t pair;            // statistics workgroups take two tiles each (large batches)
   uint32_t wait_ticks;     // bound of a wait for a TV row's merge (100 MHz clock ticks)
   // workspace: zero region (counters; every launch leaves it as it found it)
   uint32_t* hdr;           // [kHdrLines][kLineWords] job counters

@@ -1899,16 +1899,20 @@ __device__ __forceinline__ void tv_self(
 enum TvMode : int { kTvNone = 0, kTvSelf = 2 };
 
 // The statistics tiles.  grid (nt, R): tile k of row r, its logits read
-// non-temporally.  After the tile partial wave 0 arrives on the row's
-// counter, and the last tile of the row merges and decides it (a TV row:
-// marks it merged).  With kTvSelf the block then takes its share of its own
-// row's TV pass; otherwise waves 1-3 leave after the partial.
-template <int DT, bool VEC, int MS, int TVM>
+// non-temporally; with PAIR, grid (ceil(nt / 2), R) and tiles 2x and 2x + 1,
+// both loaded at once (large batches: half the arrivals, twice the bytes in
+// flight per workgroup).  After the tile partials wave 0 arrives on the
+// row's counter, and the last tile of the row merges and decides it (a TV
+// row: marks it merged).  With kTvSelf the block then takes its share of its
+// own row's TV pass; otherwise waves 1-3 leave after the partials.
+template <int DT, bool VEC, int MS, int TVM, bool PAIR = false>
 __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
+  static_assert(!PAIR || TVM == kTvNone, "a pair of tiles takes no TV pass");
   constexpr bool NT = true;
   using T = StatTile<DT, VEC>;
-  __shared__ Shared sh;
-  const int k = blockIdx.x, r = blockIdx.y;
+  __shared__ Shared shs[PAIR ? 2 : 1];
+  Shared& sh = shs[0];
+  const int k = PAIR ? 2 * (int)blockIdx.x : (int)blockIdx.x, r = blockIdx.y;
   const int nt = P.nt, g1 = P.gamma + 1, V = P.V;
   const int b = r / g1, j = r - b * g1;
   const SeqParam sp = seq_param(P, b);
@@ -1917,22 +1921,36 @@ __global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
   const char* qrow = (const char*)P.q + (int64_t)r * V * T::EB;
   const char* prow = (const char*)P.p + (int64_t)r * V * T::EB;
   const int64_t t0 = (int64_t)k * T::N;
-  uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
+  const bool two = PAIR && k + 1 < nt;  // block-uniform
+  uint32_t wq[T::U][T::NW], wp[T::U][T::NW], vq[T::U][T::NW], vp[T::U][T::NW];
   load_tile<DT, VEC, T::U, NT>(qrow, t0, V, wq, threadIdx.x);
   load_tile<DT, VEC, T::U, NT>(prow, t0, V, wp, threadIdx.x);
+  if (two) {
+    load_tile<DT, VEC, T::U, NT>(qrow, t0 + T::N, V, vq, threadIdx.x);
+    load_tile<DT, VEC, T::U, NT>(prow, t0 + T::N, V, vp, threadIdx.x);
+  }
   if (MS != 0 && needs_mom(sp))
     tile_partial<DT, VEC, MS>(P, r, k, sp, wq, wp, sh);
   else
     tile_partial<DT, VEC, 0>(P, r, k, sp, wq, wp, sh);
+  if constexpr (PAIR) {
+    if (two) {
+      if (MS != 0 && needs_mom(sp))
+        tile_partial<DT, VEC, MS>(P, r, k + 1, sp, vq, vp, shs[PAIR ? 1 : 0]);
+      else
+        tile_partial<DT, VEC, 0>(P, r, k + 1, sp, vq, vp, shs[PAIR ? 1 : 0]);
+    }
+  }
+  const uint32_t n = two ? 2u : 1u;  // tiles this block adds to its row
   if (threadIdx.x < 64) {
-    // wave 0: thread 0 stored the partial; arrive on the row's counter
+    // wave 0: thread 0 stored the partials; arrive on the row's counter
     uint32_t prev = 0;
     if (threadIdx.x == 0) {
       vmem_drain();
-      prev = add_u32(row_word(P, r, kRowArrive), 1u);
-      if (prev == (uint32_t)nt - 1u) st_u32(row_word(P, r, kRowArrive), 0u);
+      prev = add_u32(row_word(P, r, kRowArrive), n);
+      if (prev + n == (uint32_t)nt) st_u32(row_word(P, r, kRowArrive), 0u);
     }
-    if ((uint32_t)lane_i32((int)prev, 0) == (uint32_t)nt - 1u) {
+    if ((uint32_t)lane_i32((int)prev, 0) + n == (uint32_t)nt) {
       vmem_drain();
       row_merged_w<DT, MS>(P, r, b, j, sp, x);
     }
@@ -2269,7 +2287,10 @@ hipError_t launch_step_t(const Params& P, hipStream_t st, bool draw_pass, bool t
     if (e != hipSuccess) return e;
   }
   constexpr int kAll = kMomX | kMomHQ | kMomHP;
-  if (!P.tv_self) {
+  if (!P.tv_self && P.pair && P.mom_set == 0) {
+    const dim3 grid2((unsigned)((P.nt + 1) / 2), (unsigned)(P.B * (P.gamma + 1)));
+    hipLaunchKernelGGL((k_tiles<DT, VEC, 0, kTvNone, true>), grid2, block, 0, st, P);
+  } else if (!P.tv_self) {
     if (P.mom_set == 0)
       hipLaunchKernelGGL((k_tiles<DT, VEC, 0, kTvNone>), grid, block, 0, st, P);
     else if (P.mom_set == kMomX)
