@@ -88,8 +88,9 @@ WsLayout ws_layout(int64_t B, int64_t gamma, int64_t V, int dtype, bool vec) {
   L.rowline = o;
   o = align_up(o + 4 * (size_t)(kMaxRows * kLineWords), 256);
   L.zero_end = o;
-  // two job passes, each with at most R + B row jobs and 2 R + B + R nt
-  // single jobs (argmax halves, draws, TV tiles handed back by the tiles)
+  // the job pass's list: at most 2 R argmax halves, R nt TV tiles handed
+  // back by their workgroups or R nt 4 eta slices (a row is one or the
+  // other), and B spare
   L.jobs = o; o = align_up(o + 8 * (size_t)(2 * R + B + R * nt * kSlices), 256);
   L.tiles = o; o = align_up(o + sizeof(TilePart) * R * nt, 256);
   L.tvpart = o; o = align_up(o + sizeof(double) * R * nt * kSlices, 256);

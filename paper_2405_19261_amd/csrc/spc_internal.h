@@ -110,12 +110,12 @@ constexpr int kJobThreads = 512;
 // workgroup (the unit of second-pass partials and residual jobs).
 constexpr int kSlices = kThreads / 64;
 // Header lines: the count of jobs published for the job pass (line 1; lines
-// 0, 2 and 3 stay zero), then kExitLeaves + 1 lines counting the workgroups
+// 0, 2 and 3 are spare), then kExitLeaves + 1 lines counting the workgroups
 // of the pass that have read it (a two-level tree; the last arrival clears
 // the count).
 constexpr int kExitLeaves = 16;
 constexpr int kHdrExit = 4;
-constexpr int kHdrLines = kHdrExit + 2 * (kExitLeaves + 1);
+constexpr int kHdrLines = kHdrExit + kExitLeaves + 1;
 
 // Words of a row line (counters and flags, zero between calls): the row's
 // tile arrivals, the decided-row mask of the sequence with the same index (64

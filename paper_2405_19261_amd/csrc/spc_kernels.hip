@@ -1525,7 +1525,8 @@ __device__ __forceinline__ uint32_t job_id(uint64_t e) { return (uint32_t)e; }
 __device__ __forceinline__ uint32_t* hdr_word(const Params& P, int line) {
   return P.hdr + (int64_t)line * kLineWords;
 }
-__device__ __forceinline__ int hdr_line(int phase, bool single) { return 2 * (phase - 1) + single; }
+// The header line holding the count of jobs published for the job pass.
+constexpr int kHdrJobs = 1;
 // The job entries of the job pass.
 __device__ __forceinline__ uint64_t* job_list(const Params& P) { return P.jobs; }
 __device__ __forceinline__ uint32_t* row_word(const Params& P, int64_t r, int w) {
@@ -1544,7 +1545,7 @@ __device__ __forceinline__ uint64_t lane_u64(uint64_t v, int l) {
 // keeps a broken count from writing past it.
 __device__ __forceinline__ void publish_single(const Params& P, int kind, uint32_t extra,
                                                uint32_t id) {
-  const uint32_t s = add_u32(hdr_word(P, hdr_line(1, true)), 1u);
+  const uint32_t s = add_u32(hdr_word(P, kHdrJobs), 1u);
   if ((int64_t)s >= P.single_slots) return;
   st_u64(job_list(P) + s, job_entry(kind, extra, id));
 }
@@ -1554,7 +1555,7 @@ __device__ __forceinline__ void publish_singles_w(const Params& P, int kind, uin
   if (n == 0u) return;
   const int lane = threadIdx.x & 63;
   uint32_t s0 = 0;
-  if (lane == 0) s0 = add_u32(hdr_word(P, hdr_line(1, true)), n);
+  if (lane == 0) s0 = add_u32(hdr_word(P, kHdrJobs), n);
   s0 = (uint32_t)lane_i32((int)s0, 0);
   for (uint32_t x = (uint32_t)lane; x < n; x += 64u) {
     if ((int64_t)s0 + x >= P.single_slots) break;
@@ -1743,7 +1744,7 @@ __device__ __forceinline__ int row_decide_w(const Params& P, int r, int b, int j
 
 // Wave, after the last tile of row r = (b, j) arrived: merge the row, then
 // publish its second pass (TV, or eta for the tiles its statistics leave
-// open) or its argmax to job pass 1, or decide it and, when that settles
+// open) or its argmax to the job pass, or decide it and, when that settles
 // j*, finish the sequence.
 template <int DT, int MS>
 __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int j,
@@ -1808,7 +1809,7 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
         st_rowstat(P.rowstat + r, rs);
         st_i32(P.etacnt + r, (int32_t)count);
       }
-      // a single job per slice of every listed tile (job pass 1)
+      // a job per slice of every listed tile (the job pass)
       publish_singles_w(P, kJobEta, (uint32_t)r, count * (uint32_t)kSlices);
       return;
     }
@@ -1847,7 +1848,7 @@ __device__ __forceinline__ void row_job_decide(const Params& P, int kind, int r)
 // wait); past it the tile goes to the job pass.
 
 // Wave: the last of the 4 nt slices of TV row rv arrived: its decision (and
-// the sequence's finish, publishing to job pass 1), then the row's ready
+// the sequence's finish), then the row's ready
 // flag is cleared for the next call.
 template <int DT>
 __device__ __forceinline__ void tv_row_done(const Params& P, int rv) {
@@ -2216,19 +2217,18 @@ __attribute__((amdgpu_waves_per_eu(DT == SPC_BF16 ? 4 : 1))) void k_res(Params P
 // on one of kExitLeaves leaf counters; the last of a leaf arrives on the
 // top counter, and the last there clears the pass's counts (every workgroup
 // has read them by then).  Two levels keep the arrivals on one line few.
-__device__ __forceinline__ void exit_tree(const Params& P, int phase) {
+__device__ __forceinline__ void exit_tree(const Params& P) {
   const uint32_t G = gridDim.x, g = blockIdx.x;
   const uint32_t leaf = g % kExitLeaves;
   const uint32_t n_leaf = (G - leaf + kExitLeaves - 1) / kExitLeaves;
   const uint32_t n_top = G < (uint32_t)kExitLeaves ? G : (uint32_t)kExitLeaves;
-  uint32_t* lc = hdr_word(P, kHdrExit + (phase - 1) * (kExitLeaves + 1) + (int)leaf);
-  uint32_t* tc = hdr_word(P, kHdrExit + (phase - 1) * (kExitLeaves + 1) + kExitLeaves);
+  uint32_t* lc = hdr_word(P, kHdrExit + (int)leaf);
+  uint32_t* tc = hdr_word(P, kHdrExit + kExitLeaves);
   if (add_u32(lc, 1u) != n_leaf - 1u) return;
   st_u32(lc, 0u);
   if (add_u32(tc, 1u) != n_top - 1u) return;
   st_u32(tc, 0u);
-  st_u32(hdr_word(P, hdr_line(phase, false)), 0u);
-  st_u32(hdr_word(P, hdr_line(phase, true)), 0u);
+  st_u32(hdr_word(P, kHdrJobs), 0u);
 }
 
 // The job pass: a static walk over the jobs the statistics kernel of this
@@ -2243,11 +2243,11 @@ template <int DT, bool VEC>
 __global__ __launch_bounds__(kJobThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_jobs(
     Params P) {
   __shared__ uint32_t count;
-  const int phase = 1, nt = P.nt, g1 = P.gamma + 1;
+  const int nt = P.nt, g1 = P.gamma + 1;
   if (threadIdx.x == 0) {
-    count = ld_u32(hdr_word(P, hdr_line(phase, true)));
+    count = ld_u32(hdr_word(P, kHdrJobs));
     vmem_drain();  // the count has arrived before this workgroup counts itself
-    exit_tree(P, phase);
+    exit_tree(P);
   }
   __syncthreads();
   const int64_t n_items = min((int64_t)count, P.single_slots);
@@ -2802,7 +2802,7 @@ hipError_t launch_small_t(const Params& P, hipStream_t st, hipEvent_t ev_begin,
 }
 
 // Drafter sampling step (Alg. 4: x_{t+j} ~ q_{t+j}), one launch.  grid
-// (nt, B): statistics tile k of row b of the drafter's logits, as in k_stats
+// (nt, B): statistics tile k of row b of the drafter's logits, as in k_tiles
 // for one tensor.  The last tile of a row to finish (a per-row counter on a
 // line of its own) merges the row's partials and draws the token: the tile
 // masses give the tile where u W falls, then the tile's sub-chunks and
