@@ -306,6 +306,9 @@ __device__ __forceinline__ void st_i32(int32_t* p, int32_t v) {
 __device__ __forceinline__ uint32_t add_u32(uint32_t* p, uint32_t v) {
   return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ uint32_t xchg_u32(uint32_t* p, uint32_t v) {
+  return __hip_atomic_exchange(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 __device__ __forceinline__ void max_u32(uint32_t* p, uint32_t v) {
   (void)__hip_atomic_fetch_max(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -2245,9 +2248,13 @@ __global__ __launch_bounds__(kJobThreads) __attribute__((amdgpu_waves_per_eu(4))
   __shared__ uint32_t count;
   const int nt = P.nt, g1 = P.gamma + 1;
   if (threadIdx.x == 0) {
-    count = ld_u32(hdr_word(P, kHdrJobs));
-    vmem_drain();  // the count has arrived before this workgroup counts itself
-    exit_tree(P);
+    if (gridDim.x == 1) {
+      count = xchg_u32(hdr_word(P, kHdrJobs), 0u);  // the only reader takes and clears it
+    } else {
+      count = ld_u32(hdr_word(P, kHdrJobs));
+      vmem_drain();  // the count has arrived before this workgroup counts itself
+      exit_tree(P);
+    }
   }
   __syncthreads();
   const int64_t n_items = min((int64_t)count, P.single_slots);
