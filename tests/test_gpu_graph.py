@@ -29,11 +29,19 @@ def _host(t):
     return [x.cpu().numpy() for x in t]
 
 
+# (B, V): the single-launch path (rows held in registers); the statistics
+# tiles with TV passes from their own registers; the statistics tiles with
+# the TV pass kernel and the job pass
+_GRAPH_SHAPES = [(8, 20000), (8, 40000), (32, 40000)]
+
+
+@pytest.mark.parametrize("B,V", _GRAPH_SHAPES)
 @pytest.mark.parametrize("rule,alpha,T", [(W.DIFF, 0.05, 1.0), (W.OPT, 0.1, 0.7),
                                           (W.TOKEN_V3, 0.3, 1.0), (W.BILD, 9.6, 1.0),
                                           (W.CHOW, 0.4, 0.0)])
-def test_verify_graph_replays_match_eager(rule, alpha, T):
-    wl = W.WORKLOADS[3].with_(B=8, gamma=5, V=20000, rule=rule, alpha=alpha, temperature=T)
+def test_verify_graph_replays_match_eager(rule, alpha, T, B, V):
+    wl = W.WORKLOADS[3].with_(B=B, gamma=5 if B == 8 else 7, V=V, rule=rule, alpha=alpha,
+                              temperature=T)
     inputs = [W.generate(wl, s, DEV) for s in range(4)]
     keys = ("q", "p", "draft", "uniforms")
     greedy = T == 0.0
@@ -112,3 +120,57 @@ def test_draft_sample_graph_replays_match_eager():
             e = spc.spc_draft_sample(rows[(i + 1) % 3], 0.0, uniforms=u, temp_per_seq=temps)
             torch.cuda.synchronize()
             np.testing.assert_array_equal(e.cpu().numpy(), ref[(i + 1) % 3])
+
+
+def test_graph_replays_after_the_workspace_grows():
+    """A call captured with the internal workspace at one size still replays
+    correctly after an eager call of a larger shape has grown the workspace:
+    the replaced buffer stays allocated (until spc_release), and the captured
+    launches keep using it."""
+    small = W.WORKLOADS[3].with_(B=4, gamma=3, V=40000, rule=W.OPT, alpha=0.1)
+    large = W.WORKLOADS[3].with_(B=64, gamma=7, V=256000)
+    spc.spc_release()  # start from an empty internal workspace
+    inputs = [W.generate(small, s, DEV) for s in range(2)]
+    keys = ("q", "p", "draft", "uniforms")
+
+    def call(inp, wl, out=None):
+        return spc.spc_verify(inp["q"], inp["p"], inp["draft"], inp["uniforms"], wl.rule,
+                              wl.alpha, wl.temperature, out=out)
+
+    ref = [_host(call(inp, small)) for inp in inputs]
+    torch.cuda.synchronize()
+    static = {k: inputs[0][k].clone() for k in keys}
+    out = (torch.full((small.B,), -9, dtype=torch.int32, device=DEV),
+           torch.full((small.B,), -9, dtype=torch.int32, device=DEV),
+           torch.full((small.B, small.gamma + 1), 9, dtype=torch.uint8, device=DEV))
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        call(static, small, out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call(static, small, out)
+    torch.cuda.synchronize()
+    # an eager call of a shape whose workspace is larger: the buffer grows
+    big = W.generate(large, 0, DEV)
+    before = spc.spc_workspace_bytes(small.B, small.gamma, small.V, 1)
+    assert spc.spc_workspace_bytes(large.B, large.gamma, large.V, 1) > before
+    eager_big = _host(call(big, large))
+    torch.cuda.synchronize()
+    del big
+    # fresh device memory, filled, where a freed buffer could have gone
+    junk = torch.full((16 << 20,), -1, dtype=torch.int32, device=DEV)
+    for rnd in range(2):
+        for i, inp in enumerate(inputs):
+            for k in keys:
+                static[k].copy_(inp[k])
+            g.replay()
+            torch.cuda.synchronize()
+            for a, b in zip(_host(out), ref[i]):
+                np.testing.assert_array_equal(a, b, err_msg=f"replay {rnd}.{i}")
+    assert all(np.isfinite(x).all() for x in eager_big)
+    assert bool((junk == -1).all())
+    del g
+    torch.cuda.synchronize()
