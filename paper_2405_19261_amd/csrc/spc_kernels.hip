@@ -711,6 +711,27 @@ __device__ __forceinline__ int defer_rule(int rule, double alpha, double maxq, d
   }
 }
 
+// The deferral decision of an OPT or OPTLOG row at T > 0 when D_TV cannot
+// change it, else -1.  D_TV lies in [0, 1], so the threshold of eq. (11)
+// (max p - alpha D_TV) or of OPTLog (alpha D_TV) ranges between its values at
+// D_TV = 0 and D_TV = 1; rounding is monotone, so the comparison decide_row
+// makes with any D_TV in [0, 1] agrees with the one made at both ends.
+__device__ __forceinline__ int tv_free_decision(const SeqParam& sp, const RowStat& rs) {
+  const double a = sp.alpha;
+  if (sp.rule == SPC_RULE_OPT) {
+    const double maxq = exp2_acc((double)rs.zmax_q * sp.c - rs.lz_q);
+    const double maxp = exp2_acc((double)rs.zmax_p * sp.c - rs.lz_p);
+    const double t0 = maxp - a * 0.0, t1 = maxp - a * 1.0;
+    if (maxq < fmin(t0, t1)) return 1;
+    if (!(maxq < fmax(t0, t1))) return 0;
+    return -1;
+  }
+  const double t0 = a * 0.0, t1 = a * 1.0;  // OPTLOG: slog > alpha D_TV
+  if (rs.slog > fmax(t0, t1)) return 1;
+  if (!(rs.slog > fmin(t0, t1))) return 0;
+  return -1;
+}
+
 // ------------------------------------------------------------- row merge
 // A log-loss rule's statistic (nats) from row sums S and moments against the
 // row references (contraction off, as in mom_move).
@@ -1770,14 +1791,19 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
     return;
   }
   if (sp.valid && has_tv_parts(sp.rule)) {
-    if (lane == 0) {
-      // the row is merged: its TV pass may start (the row's own statistics
-      // workgroups in a resident grid, else the TV pass kernel)
+    // Without row statistics to report, a row whose decision D_TV cannot
+    // change is decided now and takes no TV pass: its ready flag says 2 to
+    // its own waiting workgroups (tv_self) and stays 0 for the TV pass
+    // kernel.  Every other row is published as merged (flag 1).
+    const bool free = !P.out_stats && tv_free_decision(sp, rs) >= 0;
+    if (lane == 0 && !free) {
       st_rowstat(P.rowstat + r, rs);
       vmem_drain();
       st_u32(row_word(P, r, kRowReady), 1u);
     }
-    return;
+    if (lane == 0 && free && P.tv_self) st_u32(row_word(P, r, kRowReady), 2u);
+    if (!free) return;
+    rs.tv = 0.0;  // any D_TV in [0, 1] decides it alike
   }
   if (sp.valid && is_token(sp.rule)) {
     // eta's share of every tile wholly below the rule's threshold comes from
@@ -1860,8 +1886,9 @@ __device__ __forceinline__ void tv_row_done(const Params& P, int rv) {
 }
 
 // Wait (bounded, thread 0) for the ready flag of TV row rv; block-uniform
-// result.  On time-out the job pass takes tile k of the row's TV pass.
-__device__ __forceinline__ bool tv_wait_ready(const Params& P, int rv, int k, Shared& sh) {
+// result: 1 (merged, take the TV pass), 2 (decided without one) or 0 (timed
+// out: the job pass takes tile k of the row's TV pass).
+__device__ __forceinline__ uint32_t tv_wait_ready(const Params& P, int rv, int k, Shared& sh) {
   if (threadIdx.x == 0) {
     const uint32_t* flag = row_word(P, rv, kRowReady);
     uint32_t f = ld_u32(flag);
@@ -1870,11 +1897,20 @@ __device__ __forceinline__ bool tv_wait_ready(const Params& P, int rv, int k, Sh
       __builtin_amdgcn_s_sleep(4);
       f = ld_u32(flag);
     }
-    sh.flag = f != 0u;
+    sh.flag = (int)f;
     if (f == 0u) publish_single(P, kJobTvTile, (uint32_t)k, (uint32_t)rv);
   }
   __syncthreads();
-  return sh.flag != 0;
+  return (uint32_t)sh.flag;
+}
+
+// Wave 0: a tile of TV row rv arrives (weight kSlices) without a TV pass,
+// the row having been decided without one (flag 2); the last arrival
+// clears the flag for the next call.
+__device__ __forceinline__ void tv_skip_arrive_w(const Params& P, int rv) {
+  if (arrive_last_w(row_word(P, rv, kRowTvArrive), (uint32_t)(kSlices * P.nt), kSlices) &&
+      (threadIdx.x & 63) == 0)
+    st_u32(row_word(P, rv, kRowReady), 0u);
 }
 
 
@@ -1888,7 +1924,12 @@ __device__ __forceinline__ void tv_self(
     const Params& P, int r, int k, const SeqParam& sp, Shared& sh,
     const uint32_t (&wq)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW],
     const uint32_t (&wp)[StatTile<DT, VEC>::U][StatTile<DT, VEC>::NW]) {
-  if (!tv_wait_ready(P, r, k, sh)) return;  // block-uniform
+  const uint32_t f = tv_wait_ready(P, r, k, sh);  // block-uniform
+  if (f == 0u) return;
+  if (f == 2u) {
+    if (threadIdx.x < 64) tv_skip_arrive_w(P, r);
+    return;
+  }
   tv_slice_regs_w<DT, VEC>(P, r, k, threadIdx.x >> 6, sp, wq, wp);
   vmem_drain();
   __syncthreads();  // all four slices are stored
@@ -1976,6 +2017,8 @@ __global__ __launch_bounds__(kThreads) void k_tvpass(Params P) {
   const int k = blockIdx.x, r = blockIdx.y;
   const SeqParam sp = seq_param(P, r / (P.gamma + 1));
   if (!(sp.valid && !sp.greedy && has_tv_parts(sp.rule))) return;  // block-uniform
+  // rows decided without a TV pass have no ready flag
+  if (ld_u32(row_word(P, r, kRowReady)) != 1u) return;  // block-uniform
   pass2_slice_w<DT, VEC, false>(P, r, k, threadIdx.x >> 6, sp);
   vmem_drain();
   __syncthreads();  // all four slices are stored
@@ -2266,7 +2309,12 @@ __global__ __launch_bounds__(kJobThreads) __attribute__((amdgpu_waves_per_eu(4))
     const int kind = job_kind(e);
     const int id = (int)job_id(e);
     if (kind == kJobTvTile) {
-      // a tile whose wait for its row's merge timed out: its four slices
+      // a tile whose wait for its row's merge timed out: its four slices,
+      // unless the row was decided without a TV pass
+      if (ld_u32(row_word(P, id, kRowReady)) == 2u) {  // wave-uniform
+        tv_skip_arrive_w(P, id);
+        continue;
+      }
       const SeqParam spt = seq_param(P, id / g1);
 #pragma unroll 1
       for (int w = 0; w < kSlices; ++w)

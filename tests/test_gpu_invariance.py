@@ -1,8 +1,9 @@
 """Decomposition invariance and the draw's edge uniforms (needs an MI355X).
 
 The launch layout depends on the batch: how many sequences a launch holds,
-how many workgroups the job passes get, which rows take another row's TV
-pass.  None of it may change a result: the same sequences verified inside
+how many workgroups the job pass gets, whether the statistics tiles take
+their rows' TV passes or a kernel of its own does, one or two tiles per
+workgroup.  None of it may change a result: the same sequences verified inside
 batches of B = 1, 8, 32 and 256 at the Gemma vocabulary must give bitwise
 identical outputs, row statistics and sampled masses.  The draws at
 u = 0 and u = 1 - 2^-24 reach the ends of the inverse-CDF search (the first
@@ -49,8 +50,10 @@ _MODES = {
     # Diff at T = 1 (the Gemma-vocabulary step), through the scalar entry point
     "diff-plain": (3, dict(), False, False),
     "diff": (3, dict(), True, False),
-    # OPT: TV passes taken by later rows' tiles at a lag that depends on B
+    # OPT: TV passes from the rows' own tiles (B = 1) or the TV pass kernel
     "opt": (3, dict(rule=W.OPT, alpha=0.1), True, False),
+    # OPT without row statistics: rows D_TV cannot change skip their TV pass
+    "opt-plain": (3, dict(rule=W.OPT, alpha=0.1), False, False),
     # the stress mix: per-sequence rules and temperatures, identical and
     # independent drafters
     "mix": (5, dict(), True, False),

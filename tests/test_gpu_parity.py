@@ -72,6 +72,22 @@ def test_workload5_parity(part):
     parity.check_accounting(rep)
 
 
+@pytest.mark.parametrize("rule,alpha", [(W.OPT, 0.1), (W.OPT, -0.05), (W.OPTLOG, 0.5)])
+@pytest.mark.parametrize("cfg,B", [(2, 8), (3, 16)])
+def test_tv_rules_without_row_statistics(rule, alpha, cfg, B):
+    """Without row statistics to report, an OPT / OPTLog row whose decision
+    D_TV in [0, 1] cannot change is decided at its merge and takes no TV pass
+    (at the T5 shape its own waiting tiles skip theirs; at the Gemma shape
+    the TV pass kernel skips it).  Decisions, accept lengths and tokens must
+    still match the oracle, for alpha of either sign."""
+    wl = W.WORKLOADS[cfg].with_(B=B, rule=rule, alpha=alpha, temperature=1.0)
+    name = f"tvfree.cfg{cfg}.{W.RULE_NAMES[rule]}.{alpha:g}"
+    _flush(f"[parity] {name}")
+    rep = parity.parity_workload(wl, 3, stats=False, step0=840, report_name=name)
+    parity.check_accounting(rep)
+    assert rep["sequences"] == 3 * B
+
+
 @pytest.mark.parametrize("cfg", [2, 3])
 def test_tv_wait_timeout_takes_the_job_pass(cfg, monkeypatch):
     """A statistics workgroup's wait for a TV row's merge is bounded; with the
