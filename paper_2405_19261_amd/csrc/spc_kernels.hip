@@ -712,21 +712,23 @@ __device__ __forceinline__ int defer_rule(int rule, double alpha, double maxq, d
 }
 
 // The deferral decision of an OPT or OPTLOG row at T > 0 when D_TV cannot
-// change it, else -1.  D_TV lies in [0, 1], so the threshold of eq. (11)
-// (max p - alpha D_TV) or of OPTLog (alpha D_TV) ranges between its values at
-// D_TV = 0 and D_TV = 1; rounding is monotone, so the comparison decide_row
-// makes with any D_TV in [0, 1] agrees with the one made at both ends.
-__device__ __forceinline__ int tv_free_decision(const SeqParam& sp, const RowStat& rs) {
+// change it, else -1.  D_TV lies in [lo, 1] (lo a lower bound that the
+// computed D_TV cannot undercut), so the threshold of eq. (11) (max p -
+// alpha D_TV) or of OPTLog (alpha D_TV) ranges between its values at the two
+// ends; rounding is monotone, so the comparison decide_row makes with any
+// D_TV in [lo, 1] agrees with the one made at both ends.
+__device__ __forceinline__ int tv_free_decision(const SeqParam& sp, const RowStat& rs,
+                                                double lo) {
   const double a = sp.alpha;
   if (sp.rule == SPC_RULE_OPT) {
     const double maxq = exp2_acc((double)rs.zmax_q * sp.c - rs.lz_q);
     const double maxp = exp2_acc((double)rs.zmax_p * sp.c - rs.lz_p);
-    const double t0 = maxp - a * 0.0, t1 = maxp - a * 1.0;
+    const double t0 = maxp - a * lo, t1 = maxp - a * 1.0;
     if (maxq < fmin(t0, t1)) return 1;
     if (!(maxq < fmax(t0, t1))) return 0;
     return -1;
   }
-  const double t0 = a * 0.0, t1 = a * 1.0;  // OPTLOG: slog > alpha D_TV
+  const double t0 = a * lo, t1 = a * 1.0;  // OPTLOG: slog > alpha D_TV
   if (rs.slog > fmax(t0, t1)) return 1;
   if (!(rs.slog > fmin(t0, t1))) return 0;
   return -1;
@@ -753,9 +755,12 @@ __device__ __forceinline__ double log_stat(int rule, double lq2, double lp2, dou
 // each a sum of two non-negative terms.  kq / kp: the first tile whose
 // largest logit is the row's (it holds the lowest index of the row maximum),
 // as k * 16 + the mask of the tile's slices that attain it.
+// tv_low (rows of at most 64 tiles, else 0): half the L1 distance between
+// the tile masses of p and q, a lower bound on D_TV (merging entries into
+// tiles can only shrink the distance).
 // Every lane returns the same RowStat.
 __device__ __forceinline__ RowStat merge_row(const Params& P, int r, int mrule, int* kq_out,
-                                             int* kp_out) {
+                                             int* kp_out, bool want_low, double& tv_low) {
   const int lane = threadIdx.x & 63;
   const int nt = P.nt;
   const TilePart* tp = P.tiles + (int64_t)r * nt;
@@ -799,6 +804,15 @@ __device__ __forceinline__ RowStat merge_row(const Params& P, int r, int mrule, 
     add(ld_tile(tp + k), mrule ? ld_mom(mp + k) : TileMom{0.0, 0.0, 0.0}, k);
   sq = wave_sum(sq);
   sp = wave_sum(sp);
+  tv_low = 0.0;
+  if (want_low && nt <= 64) {  // wave-uniform
+    // lane l's tile masses under q and p (tile l)
+    double d = 0.0;
+    if (lane < nt)
+      d = fabs(t0.s_p * exp2_acc((double)t0.r_p - (double)rp) / sp -
+               t0.s_q * exp2_acc((double)t0.r_q - (double)rq) / sq);
+    tv_low = 0.5 * wave_sum(d);
+  }
   kq = wave_min(kq);
   kp = wave_min(kp);
   // with the slice masks of those tiles (statistics tiles record them)
@@ -1778,7 +1792,9 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
   // the decision's draft inputs, requested together with the tile partials
   const DraftIn in = draft_in<DT>(P, r, x, sp);
   int kq, kp;
-  RowStat rs = merge_row(P, r, (MS != 0 && needs_mom(sp)) ? sp.rule : 0, &kq, &kp);
+  double tv_low;
+  RowStat rs = merge_row(P, r, (MS != 0 && needs_mom(sp)) ? sp.rule : 0, &kq, &kp,
+                         sp.valid && !sp.greedy && has_tv_parts(sp.rule) && !P.out_stats, tv_low);
   if (sp.valid && sp.greedy) {
     // the lowest index of each row maximum, from the first tile holding it
     if (lane == 0) {
@@ -1795,7 +1811,10 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
     // change is decided now and takes no TV pass: its ready flag says 2 to
     // its own waiting workgroups (tv_self) and stays 0 for the TV pass
     // kernel.  Every other row is published as merged (flag 1).
-    const bool free = !P.out_stats && tv_free_decision(sp, rs) >= 0;
+    // (the tile-mass bound, lowered by 1e-5 relative and 1e-6 absolute: the
+    // computed D_TV, whose error is ~1e-7 of the mass summed, stays above it)
+    const double lo = fmax(0.0, tv_low * (1.0 - 1e-5) - 1e-6);
+    const bool free = !P.out_stats && tv_free_decision(sp, rs, lo) >= 0;
     if (lane == 0 && !free) {
       st_rowstat(P.rowstat + r, rs);
       vmem_drain();
@@ -1803,7 +1822,7 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
     }
     if (lane == 0 && free && P.tv_self) st_u32(row_word(P, r, kRowReady), 2u);
     if (!free) return;
-    rs.tv = 0.0;  // any D_TV in [0, 1] decides it alike
+    rs.tv = 1.0;  // any D_TV in [lo, 1] decides it alike
   }
   if (sp.valid && is_token(sp.rule)) {
     // eta's share of every tile wholly below the rule's threshold comes from
