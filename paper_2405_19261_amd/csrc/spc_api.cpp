@@ -363,26 +363,31 @@ spc_status verify_impl(const void* q, const void* p, int32_t dtype, const int32_
     // (at most two workgroups per compute unit) each TV row takes it from
     // its own tiles' registers once the row is merged (tv_self).  Otherwise
     // a kernel of its own reads the TV rows again after the statistics
-    // kernel (k_tvpass).
+    // kernel (k_tvpass) when the rule is batch-wide, so that most rows may
+    // need it; with per-sequence rules (a few TV rows among others) their
+    // slices are job-pass items (tv_jobs).
     P.tv_self = (tv_rows && R * nt <= 2 * (int64_t)cus) ? 1 : 0;
     // batches of at least 64 statistics tiles per compute unit stream two
     // tiles per workgroup (without first moments): B = 32 at the Gemma
     // vocabulary (32 per CU) is faster with one, B = 128 and 256 with two
     P.pair = (!P.tv_self && mom_set == 0 && R * nt >= 64 * (int64_t)cus) ? 1 : 0;
-    const bool tv_pass = tv_rows && !P.tv_self;
-    // the job pass: argmax halves, eta slices, and the TV tiles whose wait
-    // for their row's merge timed out (tv_self)
-    const bool job_pass = may_greedy || (may_sample && (rules & kTok)) || P.tv_self;
+    P.tv_jobs = (tv_rows && !P.tv_self && per_rule) ? 1 : 0;
+    const bool tv_pass = tv_rows && !P.tv_self && !P.tv_jobs;
+    // the job pass: argmax halves, eta slices, TV slices (tv_jobs), and the
+    // TV tiles whose wait for their row's merge timed out (tv_self)
+    const bool job_pass =
+        may_greedy || (may_sample && (rules & kTok)) || P.tv_self || P.tv_jobs;
     P.wait_ticks = tv_wait_ticks();
-    // singles: argmax halves, draws, TV tiles whose wait timed out, the
-    // slices of the tiles a token row lists for eta
+    // jobs: argmax halves, TV tiles whose wait timed out or TV slices, the
+    // slices of the tiles a token row lists for eta (a row has one kind)
     P.single_slots = 2 * R + bl + R * nt * spc::kSlices;
     P.nsub = (int32_t)(nt * spc::tile_subchunks(dtype, vec));
     // workgroups of the job pass: a wavefront per item of its largest
     // expected list (eta slices of every tile, argmax halves), at most two
     // workgroups per compute unit
     const int64_t np = nt * spc::kSlices;
-    const int64_t items1 = np * ((rules & kTok) ? R : 0) + (may_greedy ? 2 * R : 0);
+    const int64_t items1 =
+        np * (((rules & kTok) || P.tv_jobs) ? R : 0) + (may_greedy ? 2 * R : 0);
     constexpr int64_t kW = spc::kJobThreads / 64;
     const int job_groups = (int)std::max<int64_t>(
         1, std::min<int64_t>((items1 + kW - 1) / kW, 2 * (int64_t)cus));

@@ -74,6 +74,7 @@ struct Params {
   int32_t nsub;            // sub-chunks of a row: nt * tile_subchunks
   int32_t tv_self;         // TV rows get their TV pass from their own tiles' registers
   int32_t pair;            // statistics workgroups take two tiles each (large batches)
+  int32_t tv_jobs;         // TV rows' slices are job-pass items (else the TV pass kernel)
   uint32_t wait_ticks;     // bound of a wait for a TV row's merge (100 MHz clock ticks)
   // workspace: zero region (counters; every launch leaves it as it found it)
   uint32_t* hdr;           // [kHdrLines][kLineWords] job counters

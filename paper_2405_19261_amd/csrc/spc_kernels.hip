@@ -1544,7 +1544,7 @@ __device__ __forceinline__ void tv_slice_regs_w(
 // eta second pass over a row and the residual masses of row j* of a sequence
 // are "row jobs" of nt chunks (one per tile); the two halves of a greedy
 // row's argmax and the draws from statistics partials are single chunks.
-enum JobKind : int { kJobTv = 1, kJobEta = 2, kJobArg = 4, kJobTvTile = 6 };
+enum JobKind : int { kJobTv = 1, kJobEta = 2, kJobArg = 4, kJobTvTile = 6, kJobTvSlice = 7 };
 
 // A job entry: kind (bits 60..63), an extra field (bits 32..59: the argmax
 // tensor, or a draw's sample kind and j*) and the row or sequence it belongs
@@ -1817,9 +1817,14 @@ __device__ __forceinline__ void row_merged_w(const Params& P, int r, int b, int 
     const bool free = !P.out_stats && tv_free_decision(sp, rs, lo) >= 0;
     if (lane == 0 && !free) {
       st_rowstat(P.rowstat + r, rs);
-      vmem_drain();
-      st_u32(row_word(P, r, kRowReady), 1u);
+      if (!P.tv_jobs) {
+        vmem_drain();
+        st_u32(row_word(P, r, kRowReady), 1u);
+      }
     }
+    // (with tv_jobs the row's TV slices are jobs of the job pass)
+    if (!free && P.tv_jobs)
+      publish_singles_w(P, kJobTvSlice, (uint32_t)r, (uint32_t)(nt * kSlices));
     if (lane == 0 && free && P.tv_self) st_u32(row_word(P, r, kRowReady), 2u);
     if (!free) return;
     rs.tv = 1.0;  // any D_TV in [lo, 1] decides it alike
@@ -2297,10 +2302,9 @@ __device__ __forceinline__ void exit_tree(const Params& P) {
 }
 
 // The job pass: a static walk over the jobs the statistics kernel of this
-// call published -- every part of every row job (a TV pass over a row;
-// newest job first: its rows are the likeliest still in the caches), then
-// every single job (a slice of a tile a token row listed for eta, a TV tile
-// whose wait timed out, an argmax half).  Wavefront w of the grid takes
+// call published: a slice of a TV row (batches of mixed rules), a slice of
+// a tile a token row listed for eta, a TV tile whose wait timed out, an
+// argmax half.  Wavefront w of the grid takes
 // items w, w + W, ...  The item that completes a job decides its row; a
 // sequence that decision finishes is drawn by the draw pass that follows.
 // Held to 128 VGPRs: two workgroups per compute unit.
@@ -2339,6 +2343,12 @@ __global__ __launch_bounds__(kJobThreads) __attribute__((amdgpu_waves_per_eu(4))
       for (int w = 0; w < kSlices; ++w)
         pass2_slice_w<DT, VEC, false>(P, id, (int)job_extra(e), w, spt);
       if (arrive_last_w(row_word(P, id, kRowTvArrive), (uint32_t)(kSlices * nt), kSlices))
+        tv_row_done<DT>(P, id);
+    } else if (kind == kJobTvSlice) {
+      // slice x % 4 of tile x / 4 of TV row id
+      const int x = (int)job_extra(e);
+      pass2_slice_w<DT, VEC, false>(P, id, x / kSlices, x % kSlices, seq_param(P, id / g1));
+      if (arrive_last_w(row_word(P, id, kRowTvArrive), (uint32_t)(kSlices * nt)))
         tv_row_done<DT>(P, id);
     } else if (kind == kJobEta) {
       // slice c % 4 of the (c / 4)-th listed tile of token row id

@@ -83,11 +83,12 @@ def rules_mask(rule):
 
 
 def run_gpu(inp, greedy=False, stats=True, stream=None):
-    """One call through the C interface; returns numpy outputs.  Without
-    statistics, batch-wide parameters go through spc_verify /
-    spc_greedy_verify (the entry points the benchmark times).  With them,
-    spc_verify_ex declares the rules the batch holds (rules_present), as the
-    benchmark's mixed workload does."""
+    """One call through the C interface; returns numpy outputs.  Batch-wide
+    parameters go through spc_verify / spc_greedy_verify (the entry points
+    the benchmark times), or with statistics the scalar form of
+    spc_verify_ex.  Per-sequence parameters go through spc_verify_ex with the
+    arrays and the rules the batch holds (rules_present), as the benchmark's
+    mixed workload does."""
     q, p = inp["q"], inp["p"]
     B, g1, V = q.shape
     dev = q.device
@@ -99,6 +100,13 @@ def run_gpu(inp, greedy=False, stats=True, stream=None):
         acc, tok, dm = spc.spc_greedy_verify(q, p, inp["draft"], uni[0], uni[1], stream=stream)
     elif not greedy and not stats and uni is not None:
         acc, tok, dm = spc.spc_verify(q, p, inp["draft"], inp["uniforms"], *uni, stream=stream)
+    elif uni is not None:
+        # batch-wide parameters with the optional outputs: the scalar form of
+        # spc_verify_ex (temperature 0: the batch-wide greedy step)
+        acc, tok, dm = spc.spc_verify_ex(
+            q, p, inp["draft"], None if greedy else inp["uniforms"], uni[0], uni[1],
+            0.0 if greedy else uni[2], out_row_stats=row_stats, out_argmax=argmax,
+            out_sample_norm=norm, stream=stream)
     else:
         temp = inp["temperature"]
         acc, tok, dm = spc.spc_verify_ex(
