@@ -656,9 +656,19 @@ __device__ __forceinline__ float residual_from_pp(float zq, float zp, float pp,
   return d > 0.0f ? w : 0.0f;
 }
 
+// Residual weight max(0, p_v - q_v) of a replacement draw, as the plain
+// difference of the two probabilities.  Where p_v ~ q_v the difference loses
+// relative precision, but its absolute error stays at a float32 ulp of p_v:
+// over a draw's cumulative masses that is far below the errors the shared
+// log-normalisers already carry (about 2e-8 of the mass), and it spares the
+// log-ratio, the polynomial and the two selects per entry of the pass that
+// sums every entry of row j*.  A masked logit (-inf) gives probability 0 on
+// its side (c_lo > 0), so the weight is p_v or 0 as it should be.
 template <int DT>
 __device__ __forceinline__ float residual_weight(float zq, float zp, const ProbScale& s) {
-  return residual_from_pp<DT>(zq, zp, prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo), s);
+  const float pq = prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
+  const float pp = prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
+  return fmaxf(pp - pq, 0.0f);
 }
 
 // Weight of one entry under a sampled distribution.  With a token rule the p
@@ -1397,9 +1407,9 @@ __device__ __forceinline__ double pass2_sum(const uint32_t (&wq)[StatTile<DT, VE
       if constexpr (TOK) {
         t += token_r(ps.tok, zq, zp) ? prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo) : 0.0f;
       } else {
-        // D_TV for the deferral decision only, where an absolute error of
-        // about 1e-7 is far inside the decision margin; the replacement draw
-        // of a rejected row sums its own cancellation-free residual
+        // D_TV for the deferral decision, where an absolute error of about
+        // 1e-7 is far inside the decision margin (the replacement draw sums
+        // the same difference: residual_weight)
         const float pq = prob(zq, ps.c_hi, ps.c_lo, ps.q_hi, ps.q_lo);
         const float pp = prob(zp, ps.c_hi, ps.c_lo, ps.p_hi, ps.p_lo);
         t += fmaxf(pp - pq, 0.0f);
