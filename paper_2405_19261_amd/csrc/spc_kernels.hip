@@ -1524,13 +1524,28 @@ __device__ __forceinline__ void pass2_slice_w(const Params& P, int r, int k, int
   using T = StatTile<DT, VEC>;
   const int lane = threadIdx.x & 63, V = P.V;
   const int64_t t0 = (int64_t)k * T::N;
-  // the row's statistics first: a wait for a later load is a wait for every
-  // load before it, so the slice's entries are requested after them
-  const ProbScale ps = prob_scale(sp, ld_rowstat(P.rowstat + r), TOK);
+  // the row's statistics and the slice's entries are requested together,
+  // the statistics first: waiting for them (a wait for a load is a wait for
+  // every load issued before it) leaves the entries in flight while the
+  // probability scales are formed -- one round trip, not two.  Only the
+  // words prob_scale reads are loaded (a load whose value is never used
+  // would still hold its register, and reusing that register would wait for
+  // every load before it).
+  const uint64_t* rw = reinterpret_cast<const uint64_t*>(P.rowstat + r);
+  RowStat rs{};
+  rs.lz_q = __longlong_as_double((long long)ld_u64(rw));
+  rs.lz_p = __longlong_as_double((long long)ld_u64(rw + 1));
+  if constexpr (TOK) {  // eta's rule: the row's TV word and maxima too
+    rs.tv = __longlong_as_double((long long)ld_u64(rw + 2));
+    const uint64_t m = ld_u64(rw + 4);
+    __builtin_memcpy(&rs.zmax_q, &m, sizeof m);
+  }
   __builtin_amdgcn_sched_barrier(0);
   uint32_t wq[T::U][T::NW], wp[T::U][T::NW];
   load_tile<DT, VEC, T::U, NT>((const char*)P.q + (int64_t)r * V * T::EB, t0, V, wq, w * 64 + lane);
   load_tile<DT, VEC, T::U, NT>((const char*)P.p + (int64_t)r * V * T::EB, t0, V, wp, w * 64 + lane);
+  __builtin_amdgcn_sched_barrier(0);
+  const ProbScale ps = prob_scale(sp, rs, TOK);
   double acc = pass2_sum<DT, VEC, TOK>(wq, wp, ps);
   acc = wave_sum(acc);
   if (lane == 0) st_dev_f64(P.tvpart + ((int64_t)r * P.nt + k) * kSlices + w, acc);
@@ -2337,37 +2352,48 @@ __global__ __launch_bounds__(kJobThreads) __attribute__((amdgpu_waves_per_eu(4))
   const uint64_t* singles = job_list(P);
   constexpr int kW = kJobThreads / 64;
   const int64_t W = (int64_t)gridDim.x * kW;
-  for (int64_t g = (int64_t)blockIdx.x * kW + (threadIdx.x >> 6); g < n_items; g += W) {
-    const uint64_t e = ld_u64(singles + g);
-    const int kind = job_kind(e);
-    const int id = (int)job_id(e);
-    if (kind == kJobTvTile) {
-      // a tile whose wait for its row's merge timed out: its four slices,
-      // unless the row was decided without a TV pass
-      if (ld_u32(row_word(P, id, kRowReady)) == 2u) {  // wave-uniform
-        tv_skip_arrive_w(P, id);
-        continue;
-      }
-      const SeqParam spt = seq_param(P, id / g1);
+  const int lane = threadIdx.x & 63;
+  // this wavefront's items are g0, g0 + W, ...; the entries of up to 64 of
+  // them are requested at once (lane l: item base + l W), so that an item's
+  // work starts without a round trip for its entry
+  for (int64_t base = (int64_t)blockIdx.x * kW + (threadIdx.x >> 6); base < n_items;
+       base += 64 * W) {
+    const int64_t gl = base + (int64_t)lane * W;
+    const uint64_t mine = gl < n_items ? ld_u64(singles + gl) : 0ull;
+    const int cnt = (int)min<int64_t>(64, (n_items - base + W - 1) / W);
 #pragma unroll 1
-      for (int w = 0; w < kSlices; ++w)
-        pass2_slice_w<DT, VEC, false>(P, id, (int)job_extra(e), w, spt);
-      if (arrive_last_w(row_word(P, id, kRowTvArrive), (uint32_t)(kSlices * nt), kSlices))
-        tv_row_done<DT>(P, id);
-    } else if (kind == kJobTvSlice) {
-      // slice x % 4 of tile x / 4 of TV row id
-      const int x = (int)job_extra(e);
-      pass2_slice_w<DT, VEC, false>(P, id, x / kSlices, x % kSlices, seq_param(P, id / g1));
-      if (arrive_last_w(row_word(P, id, kRowTvArrive), (uint32_t)(kSlices * nt)))
-        tv_row_done<DT>(P, id);
-    } else if (kind == kJobEta) {
-      // slice c % 4 of the (c / 4)-th listed tile of token row id
-      const uint32_t n = (uint32_t)ld_i32(P.etacnt + id) * (uint32_t)kSlices;
-      pass2_item_w<DT, VEC, true>(P, id, (int)job_extra(e));
-      if (arrive_last_w(row_word(P, id, kRowTvArrive), n)) row_job_decide<DT>(P, kind, id);
-    } else {  // kJobArg
-      arg_half_w<DT, VEC>(P, id, (int)job_extra(e));
-      if (arrive_last_w(row_word(P, id, kRowJobDone), 2u)) row_job_decide<DT>(P, kind, id);
+    for (int i = 0; i < cnt; ++i) {
+      const uint64_t e = lane_u64(mine, i);
+      const int kind = job_kind(e);
+      const int id = (int)job_id(e);
+      if (kind == kJobTvTile) {
+        // a tile whose wait for its row's merge timed out: its four slices,
+        // unless the row was decided without a TV pass
+        if (ld_u32(row_word(P, id, kRowReady)) == 2u) {  // wave-uniform
+          tv_skip_arrive_w(P, id);
+          continue;
+        }
+        const SeqParam spt = seq_param(P, id / g1);
+#pragma unroll 1
+        for (int w = 0; w < kSlices; ++w)
+          pass2_slice_w<DT, VEC, false>(P, id, (int)job_extra(e), w, spt);
+        if (arrive_last_w(row_word(P, id, kRowTvArrive), (uint32_t)(kSlices * nt), kSlices))
+          tv_row_done<DT>(P, id);
+      } else if (kind == kJobTvSlice) {
+        // slice x % 4 of tile x / 4 of TV row id
+        const int x = (int)job_extra(e);
+        pass2_slice_w<DT, VEC, false>(P, id, x / kSlices, x % kSlices, seq_param(P, id / g1));
+        if (arrive_last_w(row_word(P, id, kRowTvArrive), (uint32_t)(kSlices * nt)))
+          tv_row_done<DT>(P, id);
+      } else if (kind == kJobEta) {
+        // slice c % 4 of the (c / 4)-th listed tile of token row id
+        const uint32_t n = (uint32_t)ld_i32(P.etacnt + id) * (uint32_t)kSlices;
+        pass2_item_w<DT, VEC, true>(P, id, (int)job_extra(e));
+        if (arrive_last_w(row_word(P, id, kRowTvArrive), n)) row_job_decide<DT>(P, kind, id);
+      } else {  // kJobArg
+        arg_half_w<DT, VEC>(P, id, (int)job_extra(e));
+        if (arrive_last_w(row_word(P, id, kRowJobDone), 2u)) row_job_decide<DT>(P, kind, id);
+      }
     }
   }
 }
