@@ -82,20 +82,20 @@ def rules_mask(rule):
     return sum(1 << r for r in set(int(x) for x in rule.tolist()) if 0 <= r <= W.OPTLOG)
 
 
-def run_gpu(inp, greedy=False, stats=True, stream=None):
+def run_gpu(inp, greedy=False, stats=True, stream=None, per_seq=False):
     """One call through the C interface; returns numpy outputs.  Batch-wide
     parameters go through spc_verify / spc_greedy_verify (the entry points
     the benchmark times), or with statistics the scalar form of
     spc_verify_ex.  Per-sequence parameters go through spc_verify_ex with the
     arrays and the rules the batch holds (rules_present), as the benchmark's
-    mixed workload does."""
+    mixed workload does; per_seq sends batch-wide parameters that way too."""
     q, p = inp["q"], inp["p"]
     B, g1, V = q.shape
     dev = q.device
     row_stats = torch.full((B, g1, 8), float("nan"), device=dev) if stats else None
     argmax = torch.full((B, g1, 2), -7, dtype=torch.int32, device=dev) if stats else None
     norm = torch.full((B,), float("nan"), device=dev) if stats else None
-    uni = _uniform_params(inp)
+    uni = None if per_seq else _uniform_params(inp)
     if greedy and not stats and uni is not None:
         acc, tok, dm = spc.spc_greedy_verify(q, p, inp["draft"], uni[0], uni[1], stream=stream)
     elif not greedy and not stats and uni is not None:

@@ -117,3 +117,33 @@ def test_draw_at_edge_uniforms(shape, u_last):
     assert kinds["residual"] >= 6 and kinds["extra"] == 12
     # the ends of the search are exact draws, not near-ties
     assert rep["exact"] >= rep["sequences"] - 2
+
+
+def test_tv_slice_jobs_match_the_tv_pass_kernel():
+    """Where the rules come per sequence, a large batch's TV rows go to the job
+    pass as single slices; where one rule holds for the batch, to the TV pass
+    kernel.  With every sequence OPT and the row statistics requested (so no
+    row is settled without its TV pass) B = 256, gamma = 8 at the Gemma
+    vocabulary publishes 2304 rows x 32 tiles x 4 slices = 294 912 slice
+    jobs: more than 64 per wavefront of the job pass's 4096, so each
+    wavefront requests its job entries in more than one round.  Both routes
+    must give bitwise identical outputs, row statistics (D_TV in column 6)
+    and sampled masses; eight sequences are also checked against the
+    oracle."""
+    wl = W.WORKLOADS[3].with_(B=256, gamma=8, V=256000, rule=W.OPT, alpha=0.1)
+    _flush(f"[tv-jobs] B=256 gamma=8 V=256000 {wl.dtype} OPT: TV pass kernel")
+    inp = W.generate(wl, 64, DEV)
+    batch_wide = parity.run_gpu(inp, stats=True)
+    _flush("[tv-jobs] the same batch with per-sequence rules: TV slices as jobs")
+    per_seq = parity.run_gpu(inp, stats=True, per_seq=True)
+    for k, v in per_seq.items():
+        assert np.array_equal(_bits(v), _bits(batch_wide[k])), f"{k} differs between the routes"
+    sub = _sub(inp, slice(0, 8))
+    h = parity.host_inputs(sub)
+    del inp
+    torch.cuda.empty_cache()
+    o = parity.run_oracle(h)
+    g = {k: v[:8] for k, v in per_seq.items()}
+    rep = parity.compare(g, o, h, wl.dtype)
+    _flush(f"[tv-jobs] first 8 sequences against the oracle: {dict(rep)}")
+    assert rep["exact"] >= rep["sequences"] - 1
