@@ -583,8 +583,6 @@ __device__ __forceinline__ bool token_r(const TokenRule& t, float zq, float zp) 
 struct ProbScale {
   float c_hi, c_lo, q_hi, q_lo, p_hi, p_lo;
   double c;   // log2(e) / T
-  double dl;  // lz_p - lz_q
-  float dl_hi, dl_lo;  // dl = dl_hi + dl_lo (dl_lo = 0 when dl is not finite)
   TokenRule tok;  // token rules only
 };
 
@@ -607,9 +605,6 @@ __device__ __forceinline__ ProbScale prob_scale(const SeqParam& s, const RowStat
   }
   ps.p_hi = (float)lzp;
   ps.p_lo = isfinite(lzp) ? (float)(lzp - (double)ps.p_hi) : 0.0f;
-  ps.dl = lzp - rs.lz_q;
-  ps.dl_hi = (float)ps.dl;
-  ps.dl_lo = isfinite(ps.dl) ? (float)(ps.dl - (double)ps.dl_hi) : 0.0f;
   return ps;
 }
 
@@ -617,53 +612,15 @@ __device__ __forceinline__ float prob(float z, float c_hi, float c_lo, float l_h
   return exp2_hw(fmaf(z, c_hi, -l_hi) + fmaf(z, c_lo, -l_lo));
 }
 
-// (2^d - 1) / d for d in [0, 1/4]: a degree-4 polynomial fitted here for
-// relative error (4e-10 in exact arithmetic, about one float32 ulp as
-// evaluated), so 2^d - 1 keeps full relative precision as d -> 0.
-__device__ __forceinline__ float exp2m1_over_d(float d) {
-  float r = 0.0014333005528897047f;
-  r = fmaf(r, d, 0.009596072137355804f);
-  r = fmaf(r, d, 0.05550608038902283f);
-  r = fmaf(r, d, 0.24022644758224487f);
-  return fmaf(r, d, 0.6931471824645996f);
-}
-
-// Residual weight max(0, p_v - q_v), without branches, from p_v and
-// d = log2(p_v / q_v): p_v (1 - 2^-d) for d >= 1/4, where 2^-d <= 0.85 bounds
-// the cancellation, and below it q_v d (2^d - 1) / d with q_v = p_v 2^-d, so
-// the weight keeps full relative precision as d -> 0.  d comes from the exact
-// difference zp - zq: bf16 logits differ exactly in float32, and d is then
-// formed with the split constants (c_hi + c_lo, dl_hi + dl_lo) to about an
-// ulp; float32 logits take the difference in fp64.  zq = -inf gives d = +inf
-// and weight p_v; zp = -inf gives d = -inf, and both -inf a NaN d: weight 0.
-// pp is p_v (the caller's, shared with the token-rule target).
-template <int DT>
-__device__ __forceinline__ float residual_from_pp(float zq, float zp, float pp,
-                                                  const ProbScale& s) {
-  float d;
-  if constexpr (DT == 1) {
-    const float dz = zp - zq;
-    d = fmaf(dz, s.c_hi, -s.dl_hi) + fmaf(dz, s.c_lo, -s.dl_lo);
-  } else {
-    d = (float)fma((double)zp - (double)zq, s.c, -s.dl);
-  }
-  const float e = exp2_hw(-d);  // q_v / p_v
-  float small = (pp * e) * (d * exp2m1_over_d(d)), big = fmaf(-pp, e, pp);
-  // both arms stay computed: left alone, the compiler sinks each into a
-  // divergent branch, which costs more than evaluating both
-  asm volatile("" : "+v"(small), "+v"(big));
-  const float w = d < 0.25f ? small : big;
-  return d > 0.0f ? w : 0.0f;
-}
-
 // Residual weight max(0, p_v - q_v) of a replacement draw, as the plain
 // difference of the two probabilities.  Where p_v ~ q_v the difference loses
 // relative precision, but its absolute error stays at a float32 ulp of p_v:
 // over a draw's cumulative masses that is far below the errors the shared
-// log-normalisers already carry (about 2e-8 of the mass), and it spares the
-// log-ratio, the polynomial and the two selects per entry of the pass that
-// sums every entry of row j*.  A masked logit (-inf) gives probability 0 on
-// its side (c_lo > 0), so the weight is p_v or 0 as it should be.
+// log-normalisers already carry (about 2e-8 of the mass).  A form through
+// the log-ratio keeps full relative precision per entry but costs a
+// polynomial and two selects more per entry, in the pass that sums every
+// entry of row j*.  A masked logit (-inf) gives probability 0 on its side
+// (c_lo > 0), so the weight is p_v or 0 as it should be.
 template <int DT>
 __device__ __forceinline__ float residual_weight(float zq, float zp, const ProbScale& s) {
   const float pq = prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
@@ -673,8 +630,9 @@ __device__ __forceinline__ float residual_weight(float zq, float zp, const ProbS
 
 // Weight of one entry under a sampled distribution.  With a token rule the p
 // scale carries eta (prob_scale): the residual max(0, pi - q) of Alg. 6's
-// target is p eta where r = 0 and max(0, p eta - q) where r = 1, and the
-// target itself is p eta where r = 1 and q + p eta where r = 0.
+// target is p eta where r = 0 and max(0, p eta - q) where r = 1 (the plain
+// difference, as in residual_weight), and the target itself is p eta where
+// r = 1 and q + p eta where r = 0.
 template <int DT, int KIND>
 __device__ __forceinline__ float weight_of(float zq, float zp, const ProbScale& s) {
   if constexpr (KIND == kQ) {
@@ -685,7 +643,8 @@ __device__ __forceinline__ float weight_of(float zq, float zp, const ProbScale& 
     return residual_weight<DT>(zq, zp, s);
   } else if constexpr (KIND == kTokRes) {
     const float pe = prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
-    return token_r(s.tok, zq, zp) ? residual_from_pp<DT>(zq, zp, pe, s) : pe;
+    return token_r(s.tok, zq, zp) ? fmaxf(pe - prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo), 0.0f)
+                                  : pe;
   } else {
     const float pe = prob(zp, s.c_hi, s.c_lo, s.p_hi, s.p_lo);
     const float qe = prob(zq, s.c_hi, s.c_lo, s.q_hi, s.q_lo);
