@@ -2229,12 +2229,13 @@ __device__ __forceinline__ void res_slice_w(const Params& P, int b, int c, int f
 // partials is made by workgroup (0, b).  The last arrival clears the
 // sequence's outcome word for the next call.  Sequences without a draw
 // (greedy or invalid) have no outcome word and are skipped.
-// bfloat16: held to four resident workgroups per SIMD (a Gemma-vocabulary
-// batch of 32 sequences is 1024 workgroups: one round on 256 CUs); the draw
-// code would otherwise take one VGPR too many for it.
+// bfloat16: held to 80 VGPRs, six resident workgroups per SIMD, so that in
+// large batches (256 sequences: 8192 workgroups) one workgroup's loads
+// overlap another's residual weights.  What spills is the draw's own code,
+// which only the last arrival of a sequence runs.
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kThreads)
-__attribute__((amdgpu_waves_per_eu(DT == SPC_BF16 ? 4 : 1))) void k_res(Params P) {
+__attribute__((amdgpu_waves_per_eu(DT == SPC_BF16 ? 6 : 1))) void k_res(Params P) {
   const int k = blockIdx.x, b = blockIdx.y;
   const int g1 = P.gamma + 1, lane = threadIdx.x & 63;
   // the statistics of every row of the sequence (lane j: row j), requested
