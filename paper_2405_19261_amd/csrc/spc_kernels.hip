@@ -1958,8 +1958,12 @@ enum TvMode : int { kTvNone = 0, kTvSelf = 2 };
 // row's counter, and the last tile of the row merges and decides it (a TV
 // row: marks it merged).  With kTvSelf the block then takes its share of its
 // own row's TV pass; otherwise waves 1-3 leave after the partials.
+// With first moments the block is held to 96 VGPRs (five workgroups per
+// SIMD); the two-tile form keeps its registers (capped, it spills in the
+// streaming loop).
 template <int DT, bool VEC, int MS, int TVM, bool PAIR = false>
-__global__ __launch_bounds__(kThreads) void k_tiles(Params P) {
+__global__ __launch_bounds__(kThreads)
+__attribute__((amdgpu_waves_per_eu(MS != 0 ? 5 : 1))) void k_tiles(Params P) {
   static_assert(!PAIR || TVM == kTvNone, "a pair of tiles takes no TV pass");
   constexpr bool NT = true;
   using T = StatTile<DT, VEC>;
